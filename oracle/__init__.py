@@ -1,0 +1,262 @@
+"""CPU oracle for low-precision evaluation of bilinear fast-matmul schemes.
+
+TEST INFRASTRUCTURE ONLY.  Only tests/, __graft_entry__.smoke() and the
+CPU-baseline leg of bench.py may import, call or link anything under oracle/.
+The product path (paper_2609_39816_amd and its HIP library) never uses it,
+and the two share no code: no kernels, headers, helpers, coefficient tables
+or constant generators.  Only the seeded input generators of `synthetic`
+feed both.
+
+The oracle follows the paper step by step (plain loops, float64 where the
+paper leaves the precision free):
+  * eq. (1), Sec. 2.1: block sums, R block products, reconstruction;
+  * the FP8 schedule of App. B.1: block sums rounded to e4m3 before
+    multiplying, products and their combination in fp32;
+  * App. F: FP8 simulated by rounding to the format and decoding, against a
+    float64 reference; error = relative Frobenius norm (App. B.1);
+  * orbit statistics with the conventions of App. B.2 (upper median,
+    spread = largest / smallest, count above 2).
+Readings where the paper is silent (one scale per block-sum tensor, fmaf
+combination order, exact block products rounded once) are stated at each
+function in fm_oracle.c.
+
+Every function is parity-pinned by tests/test_oracle_*.py.
+"""
+from __future__ import annotations
+
+import ctypes as ct
+import os
+
+import numpy as np
+
+from . import build as _build
+from . import scheme_ops, schemes  # noqa: F401  (re-exported)
+from .schemes import Scheme
+
+E4M3, E5M2 = 0, 1
+FMT = {"e4m3": E4M3, "e5m2": E5M2}
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if _build.needs_build():
+            _build.build()
+        L = ct.CDLL(_build.LIB)
+        f, d, i, i64, p = ct.c_float, ct.c_double, ct.c_int, ct.c_int64, ct.c_void_p
+        sig = {
+            "orc_fp8_encode": (ct.c_uint8, [f, i]),
+            "orc_fp8_decode": (d, [ct.c_uint8, i]),
+            "orc_fp8_max": (d, [i]),
+            "orc_fp8_encode_array": (None, [p, i64, i, p]),
+            "orc_fp8_decode_array": (None, [p, i64, i, p]),
+            "orc_block_sum": (None, [p, i, i, i, i, p, p]),
+            "orc_tensor_scale": (f, [p, i64, i, p]),
+            "orc_quantize_tensor": (f, [p, i64, i, p]),
+            "orc_block_product": (None, [p, p, f, f, i, i, i, i, p]),
+            "orc_block_product_at": (None, [p, p, f, f, i, i, i, i, p, p, i, p]),
+            "orc_reconstruct": (None, [p, p, i, i, i, i, i, p]),
+            "orc_reference_f64": (None, [p, p, i, i, i, p]),
+            "orc_reference_f64_at": (d, [p, p, i, i, i, i]),
+            "orc_error_sums": (None, [p, p, i64, p, p]),
+            "orc_lowp_matmul": (i, [p, p, i, i, i, i, i, i, i, p, p, p, i, p, p, p, p, p, p]),
+            "orc_form_operands": (None, [p, i, i, i, i, i, p, i, p, p]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ct.c_void_p)
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+# --------------------------------------------------------------------------
+# FP8 codec
+# --------------------------------------------------------------------------
+def fp8_encode(x, fmt: int = E4M3) -> np.ndarray:
+    x = _f32(np.atleast_1d(x))
+    out = np.empty(x.shape, np.uint8)
+    lib().orc_fp8_encode_array(_ptr(x), x.size, fmt, _ptr(out))
+    return out
+
+
+def fp8_decode(c, fmt: int = E4M3) -> np.ndarray:
+    c = np.ascontiguousarray(np.atleast_1d(c), dtype=np.uint8)
+    out = np.empty(c.shape, np.float64)
+    lib().orc_fp8_decode_array(_ptr(c), c.size, fmt, _ptr(out))
+    return out
+
+
+def fp8_max(fmt: int = E4M3) -> float:
+    return lib().orc_fp8_max(fmt)
+
+
+# --------------------------------------------------------------------------
+# Steps of the schedule
+# --------------------------------------------------------------------------
+def block_sum(X, gr: int, gc: int, coef) -> np.ndarray:
+    X = _f32(X)
+    rows, cols = X.shape
+    c = _f32(coef).reshape(-1)
+    assert c.size == gr * gc and rows % gr == 0 and cols % gc == 0
+    T = np.empty((rows // gr, cols // gc), np.float32)
+    lib().orc_block_sum(_ptr(X), rows, cols, gr, gc, _ptr(c), _ptr(T))
+    return T
+
+
+def quantize_tensor(T, fmt: int = E4M3):
+    """(codes, d, r): one scale for the whole tensor."""
+    T = _f32(T)
+    codes = np.empty(T.shape, np.uint8)
+    d = lib().orc_quantize_tensor(_ptr(T), T.size, fmt, _ptr(codes))
+    r = ct.c_float()
+    lib().orc_tensor_scale(_ptr(T), T.size, fmt, ct.byref(r))
+    return codes, np.float32(d), np.float32(r.value)
+
+
+def form_operands(X, gr: int, gc: int, coef, fmt: int = E4M3):
+    """Block sums of one operand for every product r, quantized.
+    Returns codes (R, rows/gr, cols/gc) in X's orientation and scales d (R,)."""
+    X = _f32(X)
+    coef = _f32(coef)
+    R = coef.shape[0]
+    rows, cols = X.shape
+    codes = np.empty((R, rows // gr, cols // gc), np.uint8)
+    d = np.empty(R, np.float32)
+    lib().orc_form_operands(_ptr(X), rows, cols, gr, gc, R, _ptr(coef), fmt, _ptr(codes), _ptr(d))
+    return codes, d
+
+
+def block_product(Tq, Sq, dT, dS, fmt: int = E4M3) -> np.ndarray:
+    Tq = np.ascontiguousarray(Tq, np.uint8)
+    Sq = np.ascontiguousarray(Sq, np.uint8)
+    br, bk = Tq.shape
+    bk2, bc = Sq.shape
+    assert bk == bk2
+    out = np.empty((br, bc), np.float32)
+    lib().orc_block_product(_ptr(Tq), _ptr(Sq), float(dT), float(dS), br, bc, bk, fmt, _ptr(out))
+    return out
+
+
+def block_product_at(Tq, Sq, dT, dS, xs, zs, fmt: int = E4M3) -> np.ndarray:
+    Tq = np.ascontiguousarray(Tq, np.uint8)
+    Sq = np.ascontiguousarray(Sq, np.uint8)
+    br, bk = Tq.shape
+    bc = Sq.shape[1]
+    xs = np.ascontiguousarray(xs, np.int32)
+    zs = np.ascontiguousarray(zs, np.int32)
+    out = np.empty(xs.size, np.float32)
+    lib().orc_block_product_at(_ptr(Tq), _ptr(Sq), float(dT), float(dS), br, bc, bk, fmt,
+                               _ptr(xs), _ptr(zs), xs.size, _ptr(out))
+    return out
+
+
+def reconstruct(Mr, W, gm: int, gn: int) -> np.ndarray:
+    Mr = _f32(Mr)
+    R, br, bc = Mr.shape
+    W = _f32(W)
+    C = np.empty((gm * br, gn * bc), np.float32)
+    lib().orc_reconstruct(_ptr(Mr), _ptr(W), R, gm, gn, br, bc, _ptr(C))
+    return C
+
+
+def reference_f64(A, B) -> np.ndarray:
+    A, B = _f32(A), _f32(B)
+    M, K = A.shape
+    N = B.shape[1]
+    C = np.empty((M, N), np.float64)
+    lib().orc_reference_f64(_ptr(A), _ptr(B), M, N, K, _ptr(C))
+    return C
+
+
+def reference_f64_at(A, B, i: int, j: int) -> float:
+    A, B = _f32(A), _f32(B)
+    return lib().orc_reference_f64_at(_ptr(A), _ptr(B), B.shape[1], A.shape[1], i, j)
+
+
+def error_sums(C, Cref):
+    C = _f32(C)
+    Cref = np.ascontiguousarray(Cref, np.float64)
+    e, r = ct.c_double(), ct.c_double()
+    lib().orc_error_sums(_ptr(C), _ptr(Cref), C.size, ct.byref(e), ct.byref(r))
+    return e.value, r.value
+
+
+def rel_fro(C, Cref) -> float:
+    e, r = error_sums(C, Cref)
+    return float(np.sqrt(e) / np.sqrt(r))
+
+
+# --------------------------------------------------------------------------
+# Whole schedule for one scheme
+# --------------------------------------------------------------------------
+def lowp_matmul(A, B, scheme_f32, dims, fmt: int = E4M3, keep: bool = False):
+    """FP8 evaluation of one scheme (fp32 coefficient tables U, V, W of the
+    flattened scheme, dims = (m, k, n, R)).  Returns C, or with keep=True a
+    dict with C, Tq (R, Mb, Kb), dT, Sq (R, Kb, Nb), dS and Mr (R, Mb, Nb)."""
+    U, V, W = (_f32(t) for t in scheme_f32)
+    gm, gk, gn, R = dims
+    A, B = _f32(A), _f32(B)
+    M, K = A.shape
+    N = B.shape[1]
+    if M % gm or K % gk or N % gn:
+        raise ValueError("shape not divisible by the block grid")
+    br, bk, bc = M // gm, K // gk, N // gn
+    C = np.empty((M, N), np.float32)
+    if keep:
+        Tq = np.empty((R, br, bk), np.uint8)
+        Sq = np.empty((R, bk, bc), np.uint8)
+        dT = np.empty(R, np.float32)
+        dS = np.empty(R, np.float32)
+        Mr = np.empty((R, br, bc), np.float32)
+        args = [_ptr(Tq), _ptr(dT), _ptr(Sq), _ptr(dS), _ptr(Mr)]
+    else:
+        args = [None] * 5
+    rc = lib().orc_lowp_matmul(_ptr(A), _ptr(B), M, N, K, gm, gk, gn, R, _ptr(U), _ptr(V),
+                               _ptr(W), fmt, _ptr(C), *args)
+    if rc != 0:
+        raise ValueError("orc_lowp_matmul failed")
+    if keep:
+        return dict(C=C, Tq=Tq, dT=dT, Sq=Sq, dS=dS, Mr=Mr)
+    return C
+
+
+def flatten_f32(s: Scheme):
+    """(U, V, W) rounded to fp32 and the dims (m, k, n, R)."""
+    return scheme_ops.to_f32(s), (s.m, s.k, s.n, s.R)
+
+
+def classical_fp8(A, B, fmt: int = E4M3):
+    """Classical FP8 baseline: the plain product (R = 1) with one scale per
+    operand, same rule as the block sums."""
+    s = schemes.classical(1, 1, 1)
+    tabs, dims = flatten_f32(s)
+    return lowp_matmul(A, B, tabs, dims, fmt)
+
+
+def orbit_stats(ratios, identity_value=None) -> dict:
+    """Orbit statistics with the conventions of App. B.2: count, smallest,
+    median (the upper of the two middle values for an even count), largest,
+    spread = largest / smallest, and the number above 2."""
+    x = np.sort(np.asarray(ratios, dtype=np.float64))
+    n = x.size
+    out = dict(count=int(n), min=float(x[0]), median=float(x[n // 2]), max=float(x[-1]),
+               spread=float(x[-1] / x[0]), n_above_2=int((x > 2).sum()))
+    if identity_value is not None:
+        out["identity"] = float(identity_value)
+    return out
+
+
+def default_threads() -> int:
+    return int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))

@@ -1,0 +1,362 @@
+/*
+ * fm_oracle.c -- plain, slow CPU oracle for low-precision evaluation of a
+ * bilinear fast matrix multiplication scheme.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this file's library.  The product
+ * path (the HIP library) never calls, links or executes anything here, and
+ * this file shares no code, header, table or helper with it.
+ *
+ * What it computes follows the paper:
+ *   - the bilinear form, eq. (1) of Sec. 2.1: block sums of A and of B, R
+ *     block products M_r, and the reconstruction C_ij = sum_r w_{r,ij} M_r;
+ *   - the FP8 schedule of App. B (criteria and operands paragraph): block sums
+ *     rounded to FP8 (e4m3) before multiplying, products and their
+ *     combination carried out in fp32;
+ *   - the error measure of App. B / App. F: relative error in the Frobenius
+ *     norm against a float64 reference.
+ * Choices the paper leaves open (combination order, one scale per whole
+ * block-sum tensor, exact block-product accumulation rounded once to fp32)
+ * are the readings listed in the design notes; each function states its own.
+ *
+ * Arithmetic rules, so that every step can be checked by eye:
+ *   - fp32 steps use C float arithmetic (SSE, round-to-nearest-even,
+ *     subnormals kept); fused multiply-adds are explicit fmaf() calls and the
+ *     file is compiled with -ffp-contract=off so no other contraction occurs;
+ *   - block products are accumulated exactly in integers and rounded once.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* FP8 formats (OCP 8-bit floating point: E4M3FN and E5M2).                  */
+/* The paper rounds block sums to e4m3 (App. B); E5M2 is the second operand  */
+/* format of the Laderman workload.                                          */
+/* ------------------------------------------------------------------------ */
+
+#define ORC_E4M3 0
+#define ORC_E5M2 1
+
+typedef struct {
+  int exp_bits, man_bits, bias;
+  double max_finite;  /* largest finite magnitude */
+} fp8_format;
+
+static fp8_format fmt_of(int fmt) {
+  fp8_format f;
+  if (fmt == ORC_E4M3) {
+    f.exp_bits = 4; f.man_bits = 3; f.bias = 7; f.max_finite = 448.0;
+  } else {
+    f.exp_bits = 5; f.man_bits = 2; f.bias = 15; f.max_finite = 57344.0;
+  }
+  return f;
+}
+
+double orc_fp8_max(int fmt) { return fmt_of(fmt).max_finite; }
+
+/* Value of an 8-bit code, by the format's definition.  NaN codes give NaN;
+ * E5M2 infinities give +-inf. */
+double orc_fp8_decode(uint8_t code, int fmt) {
+  fp8_format f = fmt_of(fmt);
+  int sign = code >> 7;
+  int e = (code >> f.man_bits) & ((1 << f.exp_bits) - 1);
+  int m = code & ((1 << f.man_bits) - 1);
+  double v;
+  if (fmt == ORC_E4M3 && e == 15 && m == 7) return NAN;
+  if (fmt == ORC_E5M2 && e == 31) return m ? NAN : (sign ? -INFINITY : INFINITY);
+  if (e == 0) /* subnormal: m * 2^(1 - bias - man_bits) */
+    v = ldexp((double)m, 1 - f.bias - f.man_bits);
+  else
+    v = ldexp(1.0 + (double)m / (double)(1 << f.man_bits), e - f.bias);
+  return sign ? -v : v;
+}
+
+/* Encode an fp32 value: round to the nearest representable value, ties to
+ * the even significand, and saturate finite overflow to the largest finite
+ * value ("satfinite").  NaN maps to the format's NaN code, infinities
+ * saturate.  Works in double, where every step below is exact. */
+uint8_t orc_fp8_encode(float x, int fmt) {
+  fp8_format f = fmt_of(fmt);
+  uint8_t sign = signbit(x) ? 0x80 : 0x00;
+  double a = fabs((double)x);
+  if (isnan(x)) return (uint8_t)(fmt == ORC_E4M3 ? 0x7F : 0x7E) | sign;
+  double min_normal = ldexp(1.0, 1 - f.bias);
+  double quantum; /* spacing of representable values around a */
+  if (a < min_normal) {
+    quantum = ldexp(1.0, 1 - f.bias - f.man_bits);
+  } else {
+    int e2;
+    frexp(a, &e2); /* a = frac * 2^e2, frac in [0.5, 1) => binade 2^(e2-1) */
+    quantum = ldexp(1.0, e2 - 1 - f.man_bits);
+  }
+  double n = a / quantum; /* exact: power-of-two divisor */
+  double fl = floor(n);
+  double rem = n - fl;
+  double k;
+  if (rem > 0.5) k = fl + 1.0;
+  else if (rem < 0.5) k = fl;
+  else k = (fmod(fl, 2.0) == 0.0) ? fl : fl + 1.0; /* tie: even multiple */
+  double v = k * quantum;
+  if (v > f.max_finite || isinf(x)) v = f.max_finite;
+  /* bit pattern of v */
+  if (v == 0.0) return sign;
+  if (v < min_normal) {
+    int m = (int)(v / ldexp(1.0, 1 - f.bias - f.man_bits));
+    return sign | (uint8_t)m;
+  }
+  int e2;
+  double fr = frexp(v, &e2); /* v = fr * 2^e2 */
+  int e = e2 - 1 + f.bias;
+  int m = (int)((fr * 2.0 - 1.0) * (double)(1 << f.man_bits));
+  return sign | (uint8_t)(e << f.man_bits) | (uint8_t)m;
+}
+
+void orc_fp8_encode_array(const float* x, int64_t n, int fmt, uint8_t* out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_fp8_encode(x[i], fmt);
+}
+
+void orc_fp8_decode_array(const uint8_t* c, int64_t n, int fmt, double* out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_fp8_decode(c[i], fmt);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Block sums, eq. (1): T[x][y] = sum over blocks (p,q) with c[p*gc+q] != 0, */
+/* in ascending row-major (p,q) order, of c * X_pq[x][y].                    */
+/* X is rows x cols row-major, split into a gr x gc grid of contiguous       */
+/* blocks of size (rows/gr) x (cols/gc).  The accumulator starts at +0.0f    */
+/* and every step is one fmaf.  For A this is sum_{i,l} u_{r,il} A_il; for B */
+/* it is sum_{l,j} v_{r,lj} B_lj, with T left in B's own orientation.        */
+/* ------------------------------------------------------------------------ */
+void orc_block_sum(const float* X, int rows, int cols, int gr, int gc,
+                   const float* c, float* T) {
+  int br = rows / gr, bc = cols / gc;
+  for (int x = 0; x < br; ++x) {
+    for (int y = 0; y < bc; ++y) {
+      float acc = 0.0f;
+      for (int p = 0; p < gr; ++p)
+        for (int q = 0; q < gc; ++q) {
+          float u = c[p * gc + q];
+          if (u == 0.0f) continue;
+          acc = fmaf(u, X[(int64_t)(p * br + x) * cols + (q * bc + y)], acc);
+        }
+      T[(int64_t)x * bc + y] = acc;
+    }
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* One scale per block-sum tensor.  amax = max |T|; if amax == 0 the scale   */
+/* is 1 (an all-zero tensor, as the paper's quantizer sets d = 1 for an      */
+/* all-zero group, App. D); otherwise r = FMAX/amax and d = amax/FMAX, each  */
+/* one correctly rounded fp32 division.  Codes: encode(x * r), one fp32      */
+/* multiplication then FP8 rounding.  Returns d, writes r to *r_out.         */
+/* ------------------------------------------------------------------------ */
+float orc_tensor_scale(const float* T, int64_t n, int fmt, float* r_out) {
+  float amax = 0.0f;
+  for (int64_t i = 0; i < n; ++i) {
+    float a = fabsf(T[i]);
+    if (a > amax) amax = a;
+  }
+  float fmax = (float)fmt_of(fmt).max_finite;
+  if (amax == 0.0f) { *r_out = 1.0f; return 1.0f; }
+  *r_out = fmax / amax;
+  return amax / fmax;
+}
+
+float orc_quantize_tensor(const float* T, int64_t n, int fmt, uint8_t* codes) {
+  float r;
+  float d = orc_tensor_scale(T, n, fmt, &r);
+  for (int64_t i = 0; i < n; ++i) {
+    float y = T[i] * r;
+    codes[i] = orc_fp8_encode(y, fmt);
+  }
+  return d;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Block product M = (Tq * Sq) scaled: the FP8 values are multiples of the   */
+/* format's smallest subnormal q0 (2^-9 for E4M3, 2^-16 for E5M2), so every  */
+/* value is an integer times q0 and every product an integer times q0^2.    */
+/* The sum over the inner index is formed exactly in a 128-bit integer and   */
+/* rounded once to fp32; then M = (M * dT) * dS, two fp32 multiplications.   */
+/* Tq is br x bk (row-major), Sq is bk x bc (row-major, B's orientation).    */
+/* ------------------------------------------------------------------------ */
+static int64_t code_to_int(uint8_t c, int fmt) {
+  fp8_format f = fmt_of(fmt);
+  double v = orc_fp8_decode(c, fmt);
+  return (int64_t)ldexp(v, f.bias + f.man_bits - 1); /* exact */
+}
+
+static float exact_sum_to_float(__int128 s, int fmt) {
+  fp8_format f = fmt_of(fmt);
+  /* value = s * 2^(-2*(bias+man_bits-1)); (float)s is correctly rounded and
+   * the power-of-two scaling is exact (results stay far from fp32's
+   * subnormal and overflow ranges at every supported inner length). */
+  float fs = (float)s;
+  return ldexpf(fs, -2 * (f.bias + f.man_bits - 1));
+}
+
+void orc_block_product(const uint8_t* Tq, const uint8_t* Sq, float dT, float dS,
+                       int br, int bc, int bk, int fmt, float* Mout) {
+  int64_t* ti = (int64_t*)malloc(sizeof(int64_t) * (size_t)br * bk);
+  int64_t* sti = (int64_t*)malloc(sizeof(int64_t) * (size_t)bc * bk); /* Sq^T */
+  for (int64_t i = 0; i < (int64_t)br * bk; ++i) ti[i] = code_to_int(Tq[i], fmt);
+  for (int y = 0; y < bk; ++y)
+    for (int z = 0; z < bc; ++z)
+      sti[(int64_t)z * bk + y] = code_to_int(Sq[(int64_t)y * bc + z], fmt);
+#pragma omp parallel for schedule(static)
+  for (int x = 0; x < br; ++x) {
+    for (int z = 0; z < bc; ++z) {
+      const int64_t* a = ti + (int64_t)x * bk;
+      const int64_t* b = sti + (int64_t)z * bk;
+      __int128 s = 0;
+      for (int y = 0; y < bk; ++y) s += (__int128)a[y] * b[y];
+      float m = exact_sum_to_float(s, fmt);
+      m = m * dT;
+      m = m * dS;
+      Mout[(int64_t)x * bc + z] = m;
+    }
+  }
+  free(ti);
+  free(sti);
+}
+
+/* The same block product at selected positions (xs[t], zs[t]) only. */
+void orc_block_product_at(const uint8_t* Tq, const uint8_t* Sq, float dT, float dS,
+                          int br, int bc, int bk, int fmt, const int* xs,
+                          const int* zs, int npos, float* out) {
+  (void)br;
+  for (int t = 0; t < npos; ++t) {
+    __int128 s = 0;
+    for (int y = 0; y < bk; ++y)
+      s += (__int128)code_to_int(Tq[(int64_t)xs[t] * bk + y], fmt) *
+           code_to_int(Sq[(int64_t)y * bc + zs[t]], fmt);
+    float m = exact_sum_to_float(s, fmt);
+    m = m * dT;
+    m = m * dS;
+    out[t] = m;
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Reconstruction, eq. (1): C_ij = sum_r w_{r,ij} M_r, over r ascending with */
+/* w != 0, from +0.0f, one fmaf per term.  Mr holds R blocks br x bc; W is   */
+/* R x (gm*gn); C is (gm*br) x (gn*bc) row-major.                            */
+/* ------------------------------------------------------------------------ */
+void orc_reconstruct(const float* Mr, const float* W, int R, int gm, int gn,
+                     int br, int bc, float* C) {
+  int64_t bsz = (int64_t)br * bc;
+  int N = gn * bc;
+#pragma omp parallel for schedule(static)
+  for (int i = 0; i < gm; ++i)
+    for (int j = 0; j < gn; ++j)
+      for (int x = 0; x < br; ++x)
+        for (int z = 0; z < bc; ++z) {
+          float acc = 0.0f;
+          for (int r = 0; r < R; ++r) {
+            float w = W[(int64_t)r * gm * gn + i * gn + j];
+            if (w == 0.0f) continue;
+            acc = fmaf(w, Mr[r * bsz + (int64_t)x * bc + z], acc);
+          }
+          C[(int64_t)(i * br + x) * N + (j * bc + z)] = acc;
+        }
+}
+
+/* ------------------------------------------------------------------------ */
+/* float64 reference C = A B from the fp32 operands (App. F: a float64       */
+/* reference), sum over the inner index in ascending order.                  */
+/* ------------------------------------------------------------------------ */
+void orc_reference_f64(const float* A, const float* B, int M, int N, int K,
+                       double* C) {
+#pragma omp parallel for schedule(static)
+  for (int i = 0; i < M; ++i) {
+    double* row = C + (int64_t)i * N;
+    for (int j = 0; j < N; ++j) row[j] = 0.0;
+    for (int k = 0; k < K; ++k) {
+      double a = (double)A[(int64_t)i * K + k];
+      const float* brow = B + (int64_t)k * N;
+      for (int j = 0; j < N; ++j) row[j] += a * (double)brow[j];
+    }
+  }
+}
+
+/* One entry of the float64 reference. */
+double orc_reference_f64_at(const float* A, const float* B, int N, int K, int i,
+                            int j) {
+  double s = 0.0;
+  for (int k = 0; k < K; ++k)
+    s += (double)A[(int64_t)i * K + k] * (double)B[(int64_t)k * N + j];
+  return s;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Squared Frobenius norms for the relative error (App. B, App. F):          */
+/* err_sq = sum (C - Cref)^2, ref_sq = sum Cref^2, in float64.               */
+/* ------------------------------------------------------------------------ */
+void orc_error_sums(const float* C, const double* Cref, int64_t n,
+                    double* err_sq, double* ref_sq) {
+  double e = 0.0, r = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    double d = (double)C[i] - Cref[i];
+    e += d * d;
+    r += Cref[i] * Cref[i];
+  }
+  *err_sq = e;
+  *ref_sq = r;
+}
+
+/* ------------------------------------------------------------------------ */
+/* The whole schedule for one scheme, eq. (1) with FP8 block sums:           */
+/*   for each product r: block sums of A and B (orc_block_sum), one scale   */
+/*   per tensor and FP8 codes (orc_quantize_tensor), the scaled block       */
+/*   product (orc_block_product); then the reconstruction.                  */
+/* U is R x (gm*gk), V is R x (gk*gn), W is R x (gm*gn), all fp32, grid     */
+/* indices row-major.  Optional outputs (NULL to skip): Tq (R x br x bk),   */
+/* dT (R), Sq (R x bk x bc, B's orientation), dS (R), Mr (R x br x bc).     */
+/* ------------------------------------------------------------------------ */
+int orc_lowp_matmul(const float* A, const float* B, int M, int N, int K,
+                    int gm, int gk, int gn, int R, const float* U,
+                    const float* V, const float* W, int fmt, float* C,
+                    uint8_t* Tq_out, float* dT_out, uint8_t* Sq_out,
+                    float* dS_out, float* Mr_out) {
+  if (M % gm || K % gk || N % gn) return -1;
+  int br = M / gm, bk = K / gk, bc = N / gn;
+  int64_t tsz = (int64_t)br * bk, ssz = (int64_t)bk * bc, msz = (int64_t)br * bc;
+  float* T = (float*)malloc(sizeof(float) * (size_t)(tsz > ssz ? tsz : ssz));
+  uint8_t* tq = (uint8_t*)malloc((size_t)tsz);
+  uint8_t* sq = (uint8_t*)malloc((size_t)ssz);
+  float* Mr = Mr_out ? Mr_out : (float*)malloc(sizeof(float) * (size_t)(msz * R));
+  for (int r = 0; r < R; ++r) {
+    orc_block_sum(A, M, K, gm, gk, U + (int64_t)r * gm * gk, T);
+    float dT = orc_quantize_tensor(T, tsz, fmt, tq);
+    orc_block_sum(B, K, N, gk, gn, V + (int64_t)r * gk * gn, T);
+    float dS = orc_quantize_tensor(T, ssz, fmt, sq);
+    if (Tq_out) memcpy(Tq_out + r * tsz, tq, (size_t)tsz);
+    if (Sq_out) memcpy(Sq_out + r * ssz, sq, (size_t)ssz);
+    if (dT_out) dT_out[r] = dT;
+    if (dS_out) dS_out[r] = dS;
+    orc_block_product(tq, sq, dT, dS, br, bc, bk, fmt, Mr + r * msz);
+  }
+  orc_reconstruct(Mr, W, R, gm, gn, br, bc, C);
+  if (!Mr_out) free(Mr);
+  free(T);
+  free(tq);
+  free(sq);
+  return 0;
+}
+
+/* Quantized operands only (block sums, scales and codes) for one side:     */
+/* X rows x cols, grid gr x gc, R coefficient rows.  codes: R x (rows/gr) x */
+/* (cols/gc) in X's orientation; d: R scales.                               */
+void orc_form_operands(const float* X, int rows, int cols, int gr, int gc, int R,
+                       const float* coef, int fmt, uint8_t* codes, float* d) {
+  int64_t sz = (int64_t)(rows / gr) * (cols / gc);
+  float* T = (float*)malloc(sizeof(float) * (size_t)sz);
+  for (int r = 0; r < R; ++r) {
+    orc_block_sum(X, rows, cols, gr, gc, coef + (int64_t)r * gr * gc, T);
+    d[r] = orc_quantize_tensor(T, sz, fmt, codes + r * sz);
+  }
+  free(T);
+}
