@@ -1,0 +1,220 @@
+#!/usr/bin/env python3
+"""Benchmark of the FP8 gauge-orbit evaluation on one MI355X.
+
+One step = the whole hot path once for the headline workload: two-level
+Strassen (4x4x4, 49 products) on A 2048x4096 (N(0,1), 8 outlier channels
+x100) times B 4096x4096 (N(0, 0.02^2)), for every one of its 512 sign
+variants: scheme preparation (the gauge action on the host), the float64
+reference, the classical FP8 baseline with its error, and for every variant
+the FP8 operands, the 49 block products, the reconstruction and its error on
+the device.  Inputs are resident in HBM before timing starts.
+
+Prints one JSON line on stdout (progress goes to stderr):
+  value  = classical-equivalent FP8 TFLOP/s = G * 2MNK / t,
+  roofline = the kernel class with the most time in the timed region, its
+             achieved rate from HIP events around each of its launches,
+  cpu_baseline = the oracle on one variant of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HEADLINE = "strassen2_2048x4096x4096_sign512"
+PEAK_FP8_TFLOPS = 5000.0     # MI355X dense FP8 matrix peak
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_units(cls, w, geo, chunk, G):
+    """Algorithmic work of one launch of a kernel class (flops or bytes) and
+    its roofline bound.  Per unit of work:
+      block_gemm: 2*Mb*Nb*Kb flops per block product; one launch does chunk*R
+                  products;
+      recon:      per gauge, reads R*Mb*Nb fp32 products and M*N float64
+                  reference values (C itself is not written);
+      form_amax:  reads the operand once (fp32) -- A or B^T alternately;
+      form_quant: reads the operand once and writes chunk*R*(block) codes.
+    """
+    gm, gk, gn, R = geo
+    Mb, Kb, Nb = w.M // gm, w.K // gk, w.N // gn
+    if cls == "block_gemm":
+        return "mfma", chunk * R * 2.0 * Mb * Nb * Kb, "TFLOP/s"
+    if cls == "recon":
+        return "hbm", chunk * (R * Mb * Nb * 4.0 + w.M * w.N * 8.0), "GB/s"
+    if cls == "form_amax":
+        return "hbm", (w.M * w.K + w.N * w.K) * 4.0 / 2, "GB/s"  # average of the two operands
+    if cls == "form_quant":
+        return "hbm", ((w.M * w.K + w.N * w.K) * 4.0 + chunk * R * (Mb * Kb + Nb * Kb)) / 2, "GB/s"
+    if cls == "reference":
+        return "hbm", (w.M * w.K + w.K * w.N) * 4.0 + w.M * w.N * 8.0, "GB/s"
+    raise ValueError(cls)
+
+
+def cpu_baseline(w, A, B, gauge):
+    """The oracle (plain C, OpenMP) on one gauge of the workload."""
+    import oracle
+    from oracle import scheme_ops as so
+    from oracle import schemes as osch
+
+    base = osch.BASE_SCHEMES[w.scheme]()
+    s = so.gauge(so.power(base, w.levels), *gauge) if w.gauge_kind == "sign" else \
+        so.power(so.gauge(base, *gauge), w.levels)
+    tabs, dims = oracle.flatten_f32(s)
+    t0 = time.perf_counter()
+    oracle.lowp_matmul(A, B, tabs, dims)
+    t = time.perf_counter() - t0
+    cores = oracle.default_threads()
+    return dict(value=2.0 * w.M * w.N * w.K / t / 1e12, unit="TFLOP/s (classical-equivalent)",
+                cores=cores, kind="oracle",
+                sample=f"1 of {w.G} gauge variants (the identity) at the full "
+                       f"{w.M}x{w.K}x{w.N} shape: FP8 operands, {dims[3]} block products, "
+                       f"reconstruction; {t:.2f} s; the float64 reference is not included")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default=HEADLINE)
+    ap.add_argument("--chunk", type=int, default=32, help="gauges per launch batch")
+    ap.add_argument("--fmt", default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-timing", action="store_true", help="do not bracket kernels with events")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only; the gauge orbit would "
+                                   "shard over GPUs by gauge (see the design notes)",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synthetic as sy
+    from paper_2609_39816_amd import fm
+
+    w = sy.WORKLOADS[args.workload]
+    fmt_name = args.fmt or w.fmts[0]
+    fmt = fm.FMTS[fmt_name]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"[bench] workload {w.name}: generating inputs")
+    A, B = sy.operands(w)
+    gauges = sy.gauges(w)
+    G = len(gauges)
+    At = torch.from_numpy(A).to(dev)
+    Bt = torch.from_numpy(B).to(dev)
+
+    base = fm.Scheme.base(w.scheme)
+    if w.gauge_kind == "sign":
+        flat = base.kron(w.levels) if w.levels > 1 else base
+        levels = 1
+    else:
+        flat = base
+        levels = w.levels
+    classical = fm.Scheme.base("classical")
+    geo = flat.flat_dims(levels)
+    chunk = min(args.chunk, G) if args.chunk > 0 else G
+    ws = fm.workspace(fm.workspace_size(flat, w.M, w.N, w.K, levels, G, chunk))
+    ws_cl = fm.workspace(fm.workspace_size(classical, w.M, w.N, w.K, 1, 1, 1))
+    ws_err = fm.workspace(fm.lib.fm_error_workspace_size(w.M, w.N))
+    Cref = torch.empty((w.M, w.N), dtype=torch.float64, device=dev)
+    C_cl = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
+    log(f"[bench] workspace {ws.numel() / 1e9:.2f} GB, chunk {chunk}, family "
+        f"{flat.kernel_family(levels)}")
+
+    def step():
+        if w.gauge_kind == "sign":
+            hips = [flat.gauge(P, Q, S) for P, Q, S in gauges]
+        else:
+            hips = [base.gauge(P, Q, S) for P, Q, S in gauges]
+        fm.reference_f64(At, Bt, out=Cref)
+        fm.matmul_lowp(classical, At, Bt, 1, fmt, ws=ws_cl, out=C_cl)
+        st = fm.error_stats(C_cl, Cref, ws=ws_err)
+        errs = fm.orbit_eval(hips, At, Bt, Cref, levels, fmt, ws=ws)
+        return errs / st["rel_fro"], st["rel_fro"]
+
+    for i in range(args.warmup):
+        step()
+        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+    torch.cuda.synchronize()
+    if not args.no_timing:
+        fm.timing_reset()
+        fm.timing_enable(True)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ratios, err_cl = step()
+        log(f"[bench] step {i + 1}/{args.steps} done")
+    torch.cuda.synchronize()
+    t = (time.perf_counter() - t0) / args.steps
+    roof = None
+    per_class = {}
+    if not args.no_timing:
+        fm.timing_enable(False)
+        for cls in fm.TIMED_CLASSES:
+            n, ms = fm.timing_read(cls)
+            per_class[cls] = dict(launches=n, total_ms=ms)
+        fm.timing_reset()
+        dom = max(per_class, key=lambda c: per_class[c]["total_ms"])
+        n, ms = per_class[dom]["launches"], per_class[dom]["total_ms"]
+        bound, work, unit = kernel_units(dom, w, geo, chunk, G)
+        avg_s = ms / 1e3 / max(1, n)
+        if unit == "TFLOP/s":
+            achieved, peak = work / avg_s / 1e12, PEAK_FP8_TFLOPS
+        else:
+            achieved, peak = work / avg_s / 1e9, PEAK_HBM_GBS
+        roof = dict(bound=bound, kernel=dom, achieved=round(achieved, 2), peak=peak, unit=unit,
+                    frac=round(achieved / peak, 4), traffic=None,
+                    avg_launch_ms=round(avg_s * 1e3, 4), launches_per_step=n / args.steps)
+        log("[bench] per-class kernel time per step (ms): " +
+            ", ".join(f"{c} {v['total_ms'] / args.steps:.2f} ({v['launches'] // args.steps} launches)"
+                      for c, v in per_class.items()))
+
+    flops = G * 2.0 * w.M * w.N * w.K
+    value = flops / t / 1e12
+    mfma_flops = G * geo[3] * 2.0 * (w.M // geo[0]) * (w.N // geo[2]) * (w.K // geo[1])
+    st = dict(min=float(ratios.min()), median=float(np.sort(ratios)[len(ratios) // 2]),
+              max=float(ratios.max()), identity=float(ratios[0]))
+    out = {
+        "metric": "classical-equiv FP8 TFLOP/s (2MNK/t) + gauge-scheme evals/sec; % of MFMA peak",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": fmt_name,
+        "data": "synthetic",
+        "config": {"workload": w.name, "M": w.M, "K": w.K, "N": w.N, "scheme": w.scheme,
+                   "levels": w.levels, "gauges": G, "gauge_kind": w.gauge_kind, "fmt": fmt_name,
+                   "chunk": chunk, "parallelism": "none (1 GPU)"},
+        "evals_per_s": round(G / t, 1),
+        "pct_mfma_peak_classical_equiv": round(100 * value / PEAK_FP8_TFLOPS, 2),
+        "pct_mfma_peak_actual": round(100 * mfma_flops / t / 1e12 / PEAK_FP8_TFLOPS, 2),
+        "classical_fp8_rel_fro": err_cl,
+        "ratio_stats": st,
+        "roofline": roof,
+        "kernel_ms_per_step": {c: round(v["total_ms"] / args.steps, 3) for c, v in per_class.items()},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] oracle baseline on the host cores")
+        out["cpu_baseline"] = cpu_baseline(w, A, B, gauges[0])
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

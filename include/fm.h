@@ -1,0 +1,253 @@
+/*
+ * fm.h -- C ABI of libfm: low-precision (FP8) evaluation of bilinear fast
+ * matrix multiplication schemes on AMD Instinct MI355X (gfx950), across
+ * batches of gauge-transformed copies of a scheme.
+ *
+ * The method (Xie et al., "Beyond Accuracy: Prefix-Invariant Realizations of
+ * Low-Precision Fast Matrix Multiplication"):
+ *   eq. (1), Sec. 2.1 -- A is split into an m x k grid of blocks A_il and B
+ *     into a k x n grid B_lj; R products of block sums
+ *       M_r = (sum_il u_{r,il} A_il)(sum_lj v_{r,lj} B_lj)
+ *     are combined as C_ij = sum_r w_{r,ij} M_r;
+ *   Sec. 2.1 -- sign variants: running the scheme on DAE and EBF and flipping
+ *     back gives coefficients d_i e_l u, e_l f_j v, d_i f_j w; the same exact
+ *     product;
+ *   App. B.1 -- the FP8 schedule: block sums rounded to FP8 (e4m3) before
+ *     multiplying, products combined in fp32; relative Frobenius error
+ *     against a float64 reference (App. F).
+ *
+ * Conventions for every call:
+ *   - Return value: FM_OK (0) or a negative FM_E_* code; no call throws or
+ *     aborts across the ABI.  fm_last_error() gives a thread-local message
+ *     describing the most recent failure on the calling thread.
+ *   - Host arrays are row-major doubles and are copied; the library never
+ *     keeps a caller's host pointer.
+ *   - Device arrays are caller-owned, row-major, and must be device memory
+ *     of the current HIP device.  No call allocates device memory: scratch
+ *     space comes from the caller's workspace.
+ *   - `hip_stream` is a hipStream_t passed as void* (NULL = default stream).
+ *     Calls marked "async" only enqueue work on it; calls marked
+ *     "synchronizes" wait for the stream before returning.
+ *   - Grid index flattening: (i,l) -> i*k + l, (l,j) -> l*n + j,
+ *     (i,j) -> i*n + j.  Blocks are contiguous: block (i,l) of A covers rows
+ *     [i*M/m, (i+1)*M/m) and columns [l*K/k, (l+1)*K/k).
+ *   - A scheme flattened to L levels (the scheme applied recursively inside
+ *     its own blocks, Sec. 1: "two-level Strassen") has grid m^L x k^L x n^L
+ *     and R^L products, product index r = r1*R^(L-1) + ... + rL and block
+ *     index i = i1*m^(L-1) + ... + iL (outer level first).
+ */
+#ifndef FM_H
+#define FM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- errors */
+#define FM_OK 0
+#define FM_E_ARG (-1)        /* null pointer, non-positive size, bad enum   */
+#define FM_E_SHAPE (-2)      /* M, N, K not divisible by the block grid, or */
+                             /* a dimension beyond the supported range      */
+#define FM_E_BRENT (-3)      /* coefficients do not compute AB (residual of */
+                             /* the Brent equations above 1e-9)             */
+#define FM_E_SINGULAR (-4)   /* a gauge matrix is not invertible            */
+#define FM_E_NONFINITE (-5)  /* an Inf/NaN reached a block sum              */
+#define FM_E_WORKSPACE (-6)  /* workspace NULL, misaligned or too small     */
+#define FM_E_HIP (-7)        /* the HIP runtime reported an error           */
+#define FM_E_MISMATCH (-8)   /* schemes of one orbit differ in shape        */
+#define FM_E_NOMEM (-9)      /* host allocation failed                      */
+#define FM_E_UNSUPPORTED (-10) /* no kernel for this grid size              */
+
+typedef struct fm_scheme fm_scheme; /* opaque, immutable, library-owned     */
+
+typedef enum { FM_E4M3 = 0, FM_E5M2 = 1 } fm_fmt; /* OCP E4M3FN, OCP E5M2  */
+
+typedef struct {
+  double rel_fro; /* ||C - C_ref||_F / ||C_ref||_F (0 if C_ref = 0)         */
+  double err_sq;  /* sum (C - C_ref)^2, float64                             */
+  double ref_sq;  /* sum C_ref^2, float64                                   */
+  double max_abs; /* max |C - C_ref|                                        */
+} fm_stats;
+
+/* Text for an FM_E_* code (static storage). */
+const char* fm_strerror(int code);
+/* Message for the last failure on this thread ("" if none). */
+const char* fm_last_error(void);
+/* Library version string. */
+const char* fm_version(void);
+
+/* ------------------------------------------------------- scheme (host) */
+
+/* Load a scheme from its coefficients, eq. (1) of Sec. 2.1.
+ * U: R x (m*k), V: R x (k*n), W: R x (m*n), row-major float64, copied.
+ * The scheme is accepted only if it computes AB: the largest residual of the
+ * Brent equations sum_r u_{r,il} v_{r,l'j} w_{r,i'j'} = [i=i'][l=l'][j=j']
+ * must be <= 1e-9 (FM_E_BRENT otherwise).  On success *out owns a new scheme
+ * that the caller releases with fm_scheme_free.  Sizes: 1 <= m,n,k <= 16,
+ * 1 <= R <= 4096. */
+int fm_scheme_load(const double* U, const double* V, const double* W, int m,
+                   int n, int k, int R, fm_scheme** out);
+
+/* Gauge-transformed copy of a scheme (the sign variants of Sec. 2.1,
+ * generalized to invertible P (m x m), Q (k x k), S (n x n), row-major
+ * float64): the scheme run on P A Q and Q^-1 B S and undone with
+ * P^-1 . S^-1, i.e.
+ *   U'_r = (P^T U_r) Q^T,   V'_r = (Q^-T V_r) S^T,   W'_r = (P^-1 W_r) S^-1,
+ * computed in float64 (each matrix product summed over its inner index in
+ * ascending order; inverses of order <= 3 by adjugate / determinant, larger
+ * ones by Gauss-Jordan elimination with partial pivoting).  Diagonal +-1
+ * P, Q, S give exactly the paper's sign variants.  FM_E_SINGULAR if P, Q or
+ * S has zero determinant (or a zero pivot); the result is re-validated with
+ * the Brent check (tolerance 1e-9 relative to the coefficient magnitudes). */
+int fm_gauge_apply(const fm_scheme* s, const double* P, const double* Q,
+                   const double* S, fm_scheme** out);
+
+/* The scheme applied recursively `levels` times and flattened to one level
+ * (Kronecker power, outer level first; coefficients multiplied in float64
+ * from the outer level in).  levels = 1 returns a copy.  Two-level Strassen
+ * is fm_scheme_kron(strassen, 2): grid 4 x 4 x 4, 49 products. */
+int fm_scheme_kron(const fm_scheme* s, int levels, fm_scheme** out);
+
+/* Grid and rank of a scheme (any pointer may be NULL). */
+int fm_scheme_dims(const fm_scheme* s, int* m, int* n, int* k, int* R);
+
+/* Float64 coefficients (U: R x m*k, V: R x k*n, W: R x m*n). */
+int fm_scheme_coeffs(const fm_scheme* s, double* U, double* V, double* W);
+
+/* Coefficients of the scheme flattened to `levels` levels, each rounded once
+ * from float64 to fp32 (round to nearest even): exactly the tables the
+ * kernels use.  Sizes R^L x (mk)^L, R^L x (kn)^L, R^L x (mn)^L. */
+int fm_scheme_coeffs_f32(const fm_scheme* s, int levels, float* U, float* V,
+                         float* W);
+
+void fm_scheme_free(fm_scheme* s);
+
+/* ------------------------------------------------------ workspace sizing */
+
+/* Bytes of device workspace needed to evaluate G gauged copies of `s`
+ * (flattened to `levels`) at M x K times K x N, `chunk` copies at a time
+ * (chunk <= 0 means all G at once).  0 if the arguments are invalid.
+ * fm_matmul_lowp and fm_form_operands need fm_workspace_size(s,M,N,K,L,1,1).
+ * The workspace must be 256-byte aligned. */
+size_t fm_workspace_size(const fm_scheme* s, int M, int N, int K, int levels,
+                         int G, int chunk);
+
+/* Bytes of workspace fm_error_stats needs for an M x N output. */
+size_t fm_error_workspace_size(int M, int N);
+
+/* --------------------------------------------------- the FP8 schedule */
+
+/* Operand formation only (steps: block sums, one scale per block-sum
+ * tensor, FP8 codes), for checking.  Async.
+ * For every product r of the scheme flattened to `levels` (grid gm x gk x gn):
+ *   T_r = sum over nonzero u_{r,il}, ascending row-major (i,l), of
+ *         u * A_il, formed in fp32 as a chain of fused multiply-adds
+ *         starting from +0;   S_r likewise from v_{r,lj} and B_lj, (l,j)
+ *         ascending row-major;
+ *   amax = max |T_r| over the whole tensor; d = amax / FMAX and
+ *         q = FMAX / amax (each a correctly rounded fp32 division;
+ *         d = q = 1 if amax = 0); FMAX = 448 (E4M3) or 57344 (E5M2);
+ *   code = FP8(fl(x * q)), round to nearest even, saturating (no overflow
+ *         can occur since |x * q| <= FMAX (1 + 2^-23)^2).
+ * Outputs (device, caller-owned):
+ *   Tq: R^L x (M/gm) x (K/gk) bytes (row-major per product),
+ *   Sq: R^L x (N/gn) x (K/gk) bytes -- S_r TRANSPOSED (inner dimension
+ *       contiguous), i.e. Sq[r][z][y] is the code of S_r[y][z],
+ *   dT, dS: R^L floats.
+ * A non-finite block sum makes the next synchronizing call on this
+ * workspace (fm_error_stats, fm_orbit_eval, fm_status) return
+ * FM_E_NONFINITE. */
+int fm_form_operands(const fm_scheme* s, int levels, const float* A,
+                     const float* B, int M, int N, int K, fm_fmt fmt,
+                     uint8_t* Tq, uint8_t* Sq, float* dT, float* dS,
+                     void* workspace, size_t ws_bytes, void* hip_stream);
+
+/* Block products (step M_r of eq. (1) on FP8 operands), batched.  Async.
+ * For b in [0, batch): Mout[b] = ((Tq[b] * Sq[b]^T accumulated in fp32 by
+ * the matrix cores) * dT[b]) * dS[b], two fp32 multiplications.
+ * Tq: batch x Mb x Kb, Sq: batch x Nb x Kb (inner dimension contiguous),
+ * dT, dS: batch floats, Mout: batch x Mb x Nb fp32.  Mb, Nb, Kb >= 1; Kb a
+ * multiple of 16. */
+int fm_block_products(const uint8_t* Tq, const uint8_t* Sq, const float* dT,
+                      const float* dS, int batch, int Mb, int Nb, int Kb,
+                      fm_fmt fmt, float* Mout, void* hip_stream);
+
+/* Reconstruction C_ij = sum_r w_{r,ij} M_r (eq. (1)), fp32 fused
+ * multiply-adds over nonzero w in ascending r, starting from +0.  Async.
+ * Mprod: R^L x (M/gm) x (N/gn) fp32; C: M x N fp32. */
+int fm_reconstruct(const fm_scheme* s, int levels, const float* Mprod, int M,
+                   int N, float* C, void* workspace, size_t ws_bytes,
+                   void* hip_stream);
+
+/* The whole FP8 schedule for one scheme: C (M x N fp32, device) from
+ * A (M x K) and B (K x N) fp32 device arrays.  Async.  Workspace:
+ * fm_workspace_size(s, M, N, K, levels, 1, 1) bytes.  The classical FP8
+ * baseline is this call with the 1 x 1 x 1 rank-1 scheme. */
+int fm_matmul_lowp(const fm_scheme* s, const float* A, const float* B,
+                   float* C, int M, int N, int K, int levels, fm_fmt fmt,
+                   void* workspace, size_t ws_bytes, void* hip_stream);
+
+/* Float64 reference C_ref = A B from fp32 A (M x K) and B (K x N), device
+ * arrays (App. F: a float64 reference).  Async. */
+int fm_reference_f64(const float* A, const float* B, double* C_ref, int M,
+                     int N, int K, void* hip_stream);
+
+/* Relative Frobenius error of C against C_ref (App. B.1), float64 sums in a
+ * fixed order (bit-reproducible run to run).  Synchronizes; writes *out. */
+int fm_error_stats(const float* C, const double* C_ref, int M, int N,
+                   fm_stats* out, void* workspace, size_t ws_bytes,
+                   void* hip_stream);
+
+/* Orbit evaluation: for each of G gauged schemes (same grid and rank after
+ * flattening to `levels`), the whole FP8 schedule on A, B and the float64
+ * relative Frobenius error against C_ref (M x N float64, device), reduced on
+ * the device; rel_fro_out (host, G doubles) receives the errors.  C is not
+ * materialized.  Works through the gauges in chunks that fit `ws_bytes`
+ * (fm_workspace_size(.., G, chunk)).  Synchronizes. */
+int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A,
+                  const float* B, const double* C_ref, int M, int N, int K,
+                  int levels, fm_fmt fmt, double* rel_fro_out,
+                  void* workspace, size_t ws_bytes, void* hip_stream);
+
+/* ------------------------------------------------------------ diagnostics */
+
+/* FP8 codes of n fp32 device values x, written to out (device, n bytes):
+ * impl 0 = the encoder the formation kernels use, 1 = the gfx950 conversion
+ * instructions (v_cvt_pk_fp8_f32 / v_cvt_pk_bf8_f32), 2 = the integer
+ * encoder.  Round to nearest even; values beyond the largest finite value
+ * saturate (impl 2) -- the schedule never produces such values.  Async. */
+int fm_fp8_encode(const float* x, int64_t n, fm_fmt fmt, int impl, uint8_t* out,
+                  void* hip_stream);
+
+/* Name of the kernel family that evaluates `s` flattened to `levels`
+ * ("Strassen2", "DenseR7G2", ... or "generic"): families have formation and
+ * reconstruction kernels compiled for their nonzero structure.  Static
+ * string; "" on error. */
+const char* fm_scheme_kernel_family(const fm_scheme* s, int levels);
+
+/* Kernel timing for measurement.  While enabled (on != 0), every launch of
+ * the kernel classes below made by this library is bracketed by two HIP
+ * events recorded on the launch's own stream:
+ *   "form_amax", "form_quant" (operand formation, both operands),
+ *   "block_gemm" (FP8 block products), "recon" (reconstruction + error),
+ *   "reference" (float64 reference).
+ * fm_timing_read synchronizes on the recorded events and returns the number
+ * of launches and their summed duration in milliseconds for one class;
+ * fm_timing_reset drops all records.  Process-wide, not thread-safe; costs
+ * two event records per launch while enabled. */
+int fm_timing_enable(int on);
+int fm_timing_reset(void);
+int fm_timing_read(const char* kernel_class, int* launches, double* total_ms);
+
+/* Waits for `hip_stream` and reports a deferred device-side error recorded
+ * in `workspace` by earlier async calls (FM_E_NONFINITE), then clears it. */
+int fm_status(void* workspace, size_t ws_bytes, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FM_H */

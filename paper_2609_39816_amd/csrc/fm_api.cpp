@@ -1,0 +1,834 @@
+// C ABI of libfm (include/fm.h): argument checks, workspace layout, table
+// upload and the launch sequence of the FP8 schedule.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "fm_internal.h"
+
+namespace fm {
+
+namespace {
+thread_local std::string g_err;
+
+constexpr size_t kAlign = 256;
+size_t up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+// Pinned host staging buffer for table uploads and small downloads.  An
+// event recorded after each upload guards reuse of the buffer.
+struct Staging {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+thread_local Staging g_stage;
+
+int stage_reserve(size_t n) {
+  if (g_stage.pending) {
+    if (int rc = hip_check(hipEventSynchronize(g_stage.ev), "hipEventSynchronize")) return rc;
+    g_stage.pending = false;
+  }
+  if (n <= g_stage.cap) return FM_OK;
+  if (g_stage.host) (void)hipHostFree(g_stage.host);
+  g_stage.host = nullptr;
+  g_stage.cap = 0;
+  size_t cap = std::max<size_t>(n, 1 << 20);
+  if (int rc = hip_check(hipHostMalloc(&g_stage.host, cap, hipHostMallocDefault), "hipHostMalloc"))
+    return rc;
+  g_stage.cap = cap;
+  return FM_OK;
+}
+
+// Copies the host pieces into the staging buffer and uploads them with one
+// asynchronous copy to `dst`.
+int upload(void* dst, const std::vector<std::pair<const void*, size_t>>& pieces,
+           const std::vector<size_t>& offsets, size_t total, hipStream_t st) {
+  if (int rc = stage_reserve(total)) return rc;
+  for (size_t i = 0; i < pieces.size(); ++i)
+    std::memcpy((char*)g_stage.host + offsets[i], pieces[i].first, pieces[i].second);
+  if (int rc = hip_check(hipMemcpyAsync(dst, g_stage.host, total, hipMemcpyHostToDevice, st),
+                         "hipMemcpyAsync(H2D)"))
+    return rc;
+  if (!g_stage.ev)
+    if (int rc = hip_check(hipEventCreateWithFlags(&g_stage.ev, hipEventDisableTiming),
+                           "hipEventCreate"))
+      return rc;
+  if (int rc = hip_check(hipEventRecord(g_stage.ev, st), "hipEventRecord")) return rc;
+  g_stage.pending = true;
+  return FM_OK;
+}
+
+int download(void* host, const void* dev, size_t n, hipStream_t st) {
+  if (int rc = stage_reserve(n)) return rc;
+  if (int rc = hip_check(hipMemcpyAsync(g_stage.host, dev, n, hipMemcpyDeviceToHost, st),
+                         "hipMemcpyAsync(D2H)"))
+    return rc;
+  if (int rc = hip_check(hipStreamSynchronize(st), "hipStreamSynchronize")) return rc;
+  std::memcpy(host, g_stage.host, n);
+  return FM_OK;
+}
+
+// Concatenated coefficient lists of G flattened schemes: offsets are
+// absolute indices into the concatenated idx/coef arrays.  pat[side][g] is
+// the pattern family of gauge g's list on that side (-1: none).
+struct Tables {
+  int G = 0, R = 0;
+  Side s[3];
+  std::vector<int> pat[3];
+};
+
+void append(Tables& T, const Lists& L, int R, const int nb[3]) {
+  const Side* src[3] = {&L.a, &L.b, &L.w};
+  for (int k = 0; k < 3; ++k) {
+    Side& d = T.s[k];
+    const int32_t base = (int32_t)d.idx.size();
+    for (int r = 0; r <= R; ++r) d.off.push_back(base + src[k]->off[r]);
+    d.idx.insert(d.idx.end(), src[k]->idx.begin(), src[k]->idx.end());
+    d.coef.insert(d.coef.end(), src[k]->coef.begin(), src[k]->coef.end());
+    T.pat[k].push_back(match_pattern(k, *src[k], R, nb[k]));
+  }
+  T.G += 1;
+}
+
+// Pattern shared by gauges [g0, g0 + n) on one side, or -1.
+int chunk_pattern(const Tables& T, int side, int g0, int n) {
+  const int p = T.pat[side][g0];
+  for (int g = g0 + 1; g < g0 + n; ++g)
+    if (T.pat[side][g] != p) return -1;
+  return p;
+}
+
+// Workspace layout for G gauges processed `chunk` at a time.
+struct Layout {
+  size_t flags, bt, off[3], idx[3], coef[3], amax, q, d, tq, sq, mprod, partial, errsq, out3,
+      total;
+  int recon_nblk;
+};
+
+Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true) {
+  Layout L{};
+  const size_t R = (size_t)g.R;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o += up(bytes);
+    return at;
+  };
+  L.flags = take(kAlign);
+  L.bt = take(need_bt ? (size_t)g.N * g.K * 4 : 0);
+  const size_t nbk[3] = {(size_t)g.NBa(), (size_t)g.NBb(), (size_t)g.NC()};
+  for (int k = 0; k < 3; ++k) {
+    L.off[k] = take((size_t)G * (R + 1) * 4);
+    L.idx[k] = take((size_t)G * R * nbk[k] * 4);
+    L.coef[k] = take((size_t)G * R * nbk[k] * 4);
+  }
+  L.amax = take((size_t)2 * chunk * R * 4);
+  L.q = take((size_t)2 * chunk * R * 4);
+  L.d = take((size_t)2 * chunk * R * 4);
+  L.tq = take((size_t)chunk * R * g.Mb * g.Kb);
+  L.sq = take((size_t)chunk * R * g.Nb * g.Kb);
+  L.mprod = take((size_t)chunk * R * g.Mb * g.Nb * 4);
+  ReconArgs ra{};
+  ra.G = chunk;
+  ra.gm = g.gm;
+  ra.gn = g.gn;
+  ra.Mb = g.Mb;
+  ra.Nb = g.Nb;
+  ra.N = g.N;
+  L.recon_nblk = recon_blocks(ra);
+  L.partial = take((size_t)chunk * L.recon_nblk * 8);
+  L.errsq = take((size_t)G * 8);
+  L.out3 = take(3 * 8);
+  L.total = o;
+  return L;
+}
+
+int check_geometry(const fm_scheme* s, int levels, int M, int N, int K, Geometry& g) {
+  if (!s) return fail(FM_E_ARG, "null scheme");
+  if (levels < 1 || levels > 8) return fail(FM_E_ARG, "levels must be in [1, 8]");
+  if (M < 1 || N < 1 || K < 1) return fail(FM_E_ARG, "M, N, K must be positive");
+  long long gm = 1, gk = 1, gn = 1, R = 1;
+  for (int l = 0; l < levels; ++l) {
+    gm *= s->m;
+    gk *= s->k;
+    gn *= s->n;
+    R *= s->R;
+    if (gm > 64 || gk > 64 || gn > 64 || R > (1 << 20))
+      return fail(FM_E_UNSUPPORTED, "flattened scheme too large");
+  }
+  g.gm = (int)gm;
+  g.gk = (int)gk;
+  g.gn = (int)gn;
+  g.R = (int)R;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  if (M % gm || N % gn || K % gk)
+    return fail(FM_E_SHAPE, "M, N, K must be multiples of the flattened grid (" +
+                                std::to_string(gm) + ", " + std::to_string(gn) + ", " +
+                                std::to_string(gk) + ")");
+  g.Mb = M / (int)gm;
+  g.Nb = N / (int)gn;
+  g.Kb = K / (int)gk;
+  if (g.Kb % 16) return fail(FM_E_SHAPE, "inner block length K/k^L must be a multiple of 16");
+  if ((long long)M * K >= (1LL << 40) || (long long)K * N >= (1LL << 40) ||
+      (long long)M * N >= (1LL << 40))
+    return fail(FM_E_SHAPE, "operand too large");
+  if (g.NBa() > 64 || g.NBb() > 64 || g.NC() > 64)
+    return fail(FM_E_UNSUPPORTED, "more than 64 blocks per operand");
+  return FM_OK;
+}
+
+int check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (!ws) return fail(FM_E_WORKSPACE, "null workspace");
+  if ((uintptr_t)ws % kAlign) return fail(FM_E_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < need)
+    return fail(FM_E_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes, got " +
+                                    std::to_string(ws_bytes));
+  return FM_OK;
+}
+
+Tables make_tables(const fm_scheme* const* schemes, int G, int levels, const Geometry& geo,
+                   int& rc) {
+  Tables T;
+  T.R = geo.R;
+  rc = FM_OK;
+  for (int g = 0; g < G; ++g) {
+    const fm_scheme* s = schemes[g];
+    if (!s) {
+      rc = fail(FM_E_ARG, "null scheme in orbit");
+      return T;
+    }
+    fm_scheme flat = power(*s, levels);
+    if (flat.m != geo.gm || flat.k != geo.gk || flat.n != geo.gn || flat.R != geo.R) {
+      rc = fail(FM_E_MISMATCH, "schemes of one orbit must share grid and rank");
+      return T;
+    }
+    Lists L;
+    build_lists(flat, L);
+    const int nb[3] = {geo.NBa(), geo.NBb(), geo.NC()};
+    append(T, L, geo.R, nb);
+  }
+  return T;
+}
+
+int upload_tables(const Tables& T, char* ws, const Layout& L, hipStream_t st) {
+  // one contiguous region from the first table to the end of the last
+  const size_t base = L.off[0];
+  const size_t total = L.coef[2] + T.s[2].coef.size() * 4 - base;
+  std::vector<std::pair<const void*, size_t>> pieces;
+  std::vector<size_t> offs;
+  for (int k = 0; k < 3; ++k) {
+    pieces.push_back({T.s[k].off.data(), T.s[k].off.size() * 4});
+    offs.push_back(L.off[k] - base);
+    pieces.push_back({T.s[k].idx.data(), T.s[k].idx.size() * 4});
+    offs.push_back(L.idx[k] - base);
+    pieces.push_back({T.s[k].coef.data(), T.s[k].coef.size() * 4});
+    offs.push_back(L.coef[k] - base);
+  }
+  return upload(ws + base, pieces, offs, total, st);
+}
+
+// Operand formation for gauges [g0, g0 + n) of the uploaded tables.
+int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, const Layout& L,
+               const Tables& T, int g0, int n, int fmt, uint8_t* Tq, uint8_t* Sq, float* dT,
+               float* dS, hipStream_t st) {
+  const int R = geo.R;
+  uint32_t* amax = (uint32_t*)(ws + L.amax);
+  float* q = (float*)(ws + L.q);
+  float* dd = (float*)(ws + L.d);
+  auto off = [&](int k) { return (const int32_t*)(ws + L.off[k]) + (size_t)g0 * (R + 1); };
+  auto idx = [&](int k) { return (const int32_t*)(ws + L.idx[k]); };
+  auto coef = [&](int k) { return (const float*)(ws + L.coef[k]); };
+  const int pa = chunk_pattern(T, 0, g0, n), pb = chunk_pattern(T, 1, g0, n);
+  if (int rc = launch_fill_u32(amax, (size_t)2 * n * R, 0u, st)) return rc;
+  FormArgs fa{A,      geo.M, geo.K, geo.gm, geo.gk, geo.Mb, geo.Kb, off(0), idx(0), coef(0), R, n,
+              amax,   q,     Tq,    fmt};
+  FormArgs fb{Bt, geo.N, geo.K, geo.gn, geo.gk, geo.Nb, geo.Kb, off(1), idx(1), coef(1), R, n,
+              amax + (size_t)n * R, q + (size_t)n * R, Sq, fmt};
+  for (int side = 0; side < 2; ++side) {
+    timing_begin(T_FORM_AMAX, st);
+    if (int rc = launch_form(side ? fb : fa, 0, side ? pb : pa, side, st)) return rc;
+    timing_end(T_FORM_AMAX, st);
+  }
+  if (int rc = launch_scales(amax, q, dd, 2 * n * R, fmt, (uint32_t*)(ws + L.flags), st)) return rc;
+  for (int side = 0; side < 2; ++side) {
+    timing_begin(T_FORM_QUANT, st);
+    if (int rc = launch_form(side ? fb : fa, 1, side ? pb : pa, side, st)) return rc;
+    timing_end(T_FORM_QUANT, st);
+  }
+  if (dT)
+    if (int rc = hip_check(hipMemcpyAsync(dT, dd, (size_t)n * R * 4, hipMemcpyDeviceToDevice, st),
+                           "hipMemcpyAsync(dT)"))
+      return rc;
+  if (dS)
+    if (int rc = hip_check(hipMemcpyAsync(dS, dd + (size_t)n * R, (size_t)n * R * 4,
+                                          hipMemcpyDeviceToDevice, st),
+                           "hipMemcpyAsync(dS)"))
+      return rc;
+  return FM_OK;
+}
+
+ReconArgs recon_args(const Geometry& geo, const char* ws, const Layout& L, int g0, int n,
+                     const float* Mp, float* C, const double* Cref) {
+  ReconArgs ra{Mp,
+               (const int32_t*)(ws + L.off[2]) + (size_t)g0 * (geo.R + 1),
+               (const int32_t*)(ws + L.idx[2]),
+               (const float*)(ws + L.coef[2]),
+               geo.R,
+               n,
+               geo.gm,
+               geo.gn,
+               geo.Mb,
+               geo.Nb,
+               geo.N,
+               C,
+               Cref,
+               (double*)(ws + L.partial)};
+  return ra;
+}
+
+int fmt_ok(int fmt) { return fmt == FM_E4M3 || fmt == FM_E5M2; }
+
+fm_scheme* clone(const fm_scheme& s) {
+  try {
+    return new fm_scheme(s);
+  } catch (...) {
+    return nullptr;
+  }
+}
+
+}  // namespace
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+// ----------------------------------------------------------- kernel timing
+namespace {
+const char* const kTimedNames[T_COUNT] = {"form_amax", "form_quant", "block_gemm", "recon",
+                                          "reference"};
+struct TimingRec {
+  int cls;
+  hipEvent_t start, stop;
+};
+struct Timing {
+  bool on = false;
+  std::vector<TimingRec> recs;
+  std::vector<hipEvent_t> pool;
+  int open_cls = -1;
+  hipEvent_t open_start = nullptr;
+} g_timing;
+
+hipEvent_t timing_event() {
+  if (!g_timing.pool.empty()) {
+    hipEvent_t e = g_timing.pool.back();
+    g_timing.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+}  // namespace
+
+void timing_begin(int cls, hipStream_t st) {
+  if (!g_timing.on) return;
+  g_timing.open_cls = cls;
+  g_timing.open_start = timing_event();
+  if (g_timing.open_start) (void)hipEventRecord(g_timing.open_start, st);
+}
+
+void timing_end(int cls, hipStream_t st) {
+  if (!g_timing.on || g_timing.open_cls != cls || !g_timing.open_start) return;
+  hipEvent_t stop = timing_event();
+  if (!stop) return;
+  (void)hipEventRecord(stop, st);
+  g_timing.recs.push_back({cls, g_timing.open_start, stop});
+  g_timing.open_cls = -1;
+  g_timing.open_start = nullptr;
+}
+
+void clear_error() { g_err.clear(); }
+
+int hip_check(hipError_t e, const char* what) {
+  if (e == hipSuccess) return FM_OK;
+  return fail(FM_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+}  // namespace fm
+
+using namespace fm;
+
+extern "C" {
+
+const char* fm_strerror(int code) {
+  switch (code) {
+    case FM_OK: return "ok";
+    case FM_E_ARG: return "invalid argument";
+    case FM_E_SHAPE: return "shape not supported by the block grid";
+    case FM_E_BRENT: return "coefficients do not compute the matrix product";
+    case FM_E_SINGULAR: return "singular gauge matrix";
+    case FM_E_NONFINITE: return "non-finite value in a block sum";
+    case FM_E_WORKSPACE: return "workspace missing, misaligned or too small";
+    case FM_E_HIP: return "HIP runtime error";
+    case FM_E_MISMATCH: return "schemes of one orbit differ in shape";
+    case FM_E_NOMEM: return "host allocation failed";
+    case FM_E_UNSUPPORTED: return "unsupported scheme size";
+    default: return "unknown error";
+  }
+}
+
+const char* fm_last_error(void) { return g_err.c_str(); }
+
+const char* fm_version(void) { return "libfm 0.1 (gfx950)"; }
+
+int fm_scheme_load(const double* U, const double* V, const double* W, int m, int n, int k, int R,
+                   fm_scheme** out) {
+  clear_error();
+  if (!U || !V || !W || !out) return fail(FM_E_ARG, "null pointer");
+  *out = nullptr;
+  if (m < 1 || n < 1 || k < 1 || m > 16 || n > 16 || k > 16 || R < 1 || R > 4096)
+    return fail(FM_E_ARG, "sizes out of range");
+  fm_scheme s;
+  s.m = m;
+  s.n = n;
+  s.k = k;
+  s.R = R;
+  s.U.assign(U, U + (size_t)R * m * k);
+  s.V.assign(V, V + (size_t)R * k * n);
+  s.W.assign(W, W + (size_t)R * m * n);
+  for (double x : s.U)
+    if (!std::isfinite(x)) return fail(FM_E_ARG, "non-finite coefficient");
+  for (double x : s.V)
+    if (!std::isfinite(x)) return fail(FM_E_ARG, "non-finite coefficient");
+  for (double x : s.W)
+    if (!std::isfinite(x)) return fail(FM_E_ARG, "non-finite coefficient");
+  const double res = brent_residual(s);
+  if (!(res <= 1e-9))
+    return fail(FM_E_BRENT, "Brent residual " + std::to_string(res) + " exceeds 1e-9");
+  *out = clone(s);
+  return *out ? FM_OK : fail(FM_E_NOMEM, "out of host memory");
+}
+
+int fm_gauge_apply(const fm_scheme* s, const double* P, const double* Q, const double* S,
+                   fm_scheme** out) {
+  clear_error();
+  if (!s || !P || !Q || !S || !out) return fail(FM_E_ARG, "null pointer");
+  *out = nullptr;
+  const int m = s->m, k = s->k, n = s->n;
+  std::vector<double> Pm(P, P + (size_t)m * m), Qm(Q, Q + (size_t)k * k), Sm(S, S + (size_t)n * n);
+  for (double x : Pm)
+    if (!std::isfinite(x)) return fail(FM_E_ARG, "non-finite gauge entry");
+  for (double x : Qm)
+    if (!std::isfinite(x)) return fail(FM_E_ARG, "non-finite gauge entry");
+  for (double x : Sm)
+    if (!std::isfinite(x)) return fail(FM_E_ARG, "non-finite gauge entry");
+  std::vector<double> Pi, Qi, Si;
+  if (!invert(Pm, m, Pi) || !invert(Qm, k, Qi) || !invert(Sm, n, Si))
+    return fail(FM_E_SINGULAR, "gauge matrix is singular");
+  fm_scheme g;
+  g.m = m;
+  g.n = n;
+  g.k = k;
+  g.R = s->R;
+  g.U.assign(s->U.size(), 0.0);
+  g.V.assign(s->V.size(), 0.0);
+  g.W.assign(s->W.size(), 0.0);
+  std::vector<double> t1, t2;
+  for (int r = 0; r < s->R; ++r) {
+    // U'_r = (P^T U_r) Q^T
+    const double* u = &s->U[(size_t)r * m * k];
+    t1.assign((size_t)m * k, 0.0);
+    for (int a = 0; a < m; ++a)
+      for (int b = 0; b < k; ++b) {
+        double acc = 0.0;
+        for (int c = 0; c < m; ++c) acc = acc + Pm[(size_t)c * m + a] * u[(size_t)c * k + b];
+        t1[(size_t)a * k + b] = acc;
+      }
+    for (int a = 0; a < m; ++a)
+      for (int b = 0; b < k; ++b) {
+        double acc = 0.0;
+        for (int c = 0; c < k; ++c) acc = acc + t1[(size_t)a * k + c] * Qm[(size_t)b * k + c];
+        g.U[(size_t)r * m * k + (size_t)a * k + b] = acc;
+      }
+    // V'_r = (Q^-T V_r) S^T
+    const double* v = &s->V[(size_t)r * k * n];
+    t2.assign((size_t)k * n, 0.0);
+    for (int a = 0; a < k; ++a)
+      for (int b = 0; b < n; ++b) {
+        double acc = 0.0;
+        for (int c = 0; c < k; ++c) acc = acc + Qi[(size_t)c * k + a] * v[(size_t)c * n + b];
+        t2[(size_t)a * n + b] = acc;
+      }
+    for (int a = 0; a < k; ++a)
+      for (int b = 0; b < n; ++b) {
+        double acc = 0.0;
+        for (int c = 0; c < n; ++c) acc = acc + t2[(size_t)a * n + c] * Sm[(size_t)b * n + c];
+        g.V[(size_t)r * k * n + (size_t)a * n + b] = acc;
+      }
+    // W'_r = (P^-1 W_r) S^-1
+    const double* w = &s->W[(size_t)r * m * n];
+    t1.assign((size_t)m * n, 0.0);
+    for (int a = 0; a < m; ++a)
+      for (int b = 0; b < n; ++b) {
+        double acc = 0.0;
+        for (int c = 0; c < m; ++c) acc = acc + Pi[(size_t)a * m + c] * w[(size_t)c * n + b];
+        t1[(size_t)a * n + b] = acc;
+      }
+    for (int a = 0; a < m; ++a)
+      for (int b = 0; b < n; ++b) {
+        double acc = 0.0;
+        for (int c = 0; c < n; ++c) acc = acc + t1[(size_t)a * n + c] * Si[(size_t)c * n + b];
+        g.W[(size_t)r * m * n + (size_t)a * n + b] = acc;
+      }
+  }
+  double cu = 0, cv = 0, cw = 0;
+  for (double x : g.U) cu = std::max(cu, std::fabs(x));
+  for (double x : g.V) cv = std::max(cv, std::fabs(x));
+  for (double x : g.W) cw = std::max(cw, std::fabs(x));
+  const double res = brent_residual(g);
+  if (!(res <= 1e-9 * std::max(1.0, cu * cv * cw)))
+    return fail(FM_E_BRENT, "gauged scheme fails the Brent check (residual " +
+                                std::to_string(res) + ")");
+  *out = clone(g);
+  return *out ? FM_OK : fail(FM_E_NOMEM, "out of host memory");
+}
+
+int fm_scheme_kron(const fm_scheme* s, int levels, fm_scheme** out) {
+  clear_error();
+  if (!s || !out) return fail(FM_E_ARG, "null pointer");
+  *out = nullptr;
+  if (levels < 1 || levels > 8) return fail(FM_E_ARG, "levels must be in [1, 8]");
+  long long R = 1, m = 1, n = 1, k = 1;
+  for (int l = 0; l < levels; ++l) {
+    R *= s->R;
+    m *= s->m;
+    n *= s->n;
+    k *= s->k;
+  }
+  if (R > (1 << 20) || m * k * R > (1LL << 28) || k * n * R > (1LL << 28) || m * n * R > (1LL << 28))
+    return fail(FM_E_UNSUPPORTED, "Kronecker power too large");
+  *out = clone(power(*s, levels));
+  return *out ? FM_OK : fail(FM_E_NOMEM, "out of host memory");
+}
+
+int fm_scheme_dims(const fm_scheme* s, int* m, int* n, int* k, int* R) {
+  clear_error();
+  if (!s) return fail(FM_E_ARG, "null scheme");
+  if (m) *m = s->m;
+  if (n) *n = s->n;
+  if (k) *k = s->k;
+  if (R) *R = s->R;
+  return FM_OK;
+}
+
+int fm_scheme_coeffs(const fm_scheme* s, double* U, double* V, double* W) {
+  clear_error();
+  if (!s || !U || !V || !W) return fail(FM_E_ARG, "null pointer");
+  std::copy(s->U.begin(), s->U.end(), U);
+  std::copy(s->V.begin(), s->V.end(), V);
+  std::copy(s->W.begin(), s->W.end(), W);
+  return FM_OK;
+}
+
+int fm_scheme_coeffs_f32(const fm_scheme* s, int levels, float* U, float* V, float* W) {
+  clear_error();
+  if (!s || !U || !V || !W) return fail(FM_E_ARG, "null pointer");
+  if (levels < 1 || levels > 8) return fail(FM_E_ARG, "levels must be in [1, 8]");
+  const fm_scheme f = power(*s, levels);
+  for (size_t i = 0; i < f.U.size(); ++i) U[i] = (float)f.U[i];
+  for (size_t i = 0; i < f.V.size(); ++i) V[i] = (float)f.V[i];
+  for (size_t i = 0; i < f.W.size(); ++i) W[i] = (float)f.W[i];
+  return FM_OK;
+}
+
+void fm_scheme_free(fm_scheme* s) { delete s; }
+
+size_t fm_workspace_size(const fm_scheme* s, int M, int N, int K, int levels, int G, int chunk) {
+  Geometry g;
+  if (G < 1 || check_geometry(s, levels, M, N, K, g) != FM_OK) return 0;
+  if (chunk <= 0 || chunk > G) chunk = G;
+  return make_layout(g, G, chunk).total;
+}
+
+size_t fm_error_workspace_size(int M, int N) {
+  if (M < 1 || N < 1) return 0;
+  const size_t n = (size_t)M * N;
+  return up((size_t)error_stats_blocks(n) * 3 * 8) + up(3 * 8);
+}
+
+int fm_form_operands(const fm_scheme* s, int levels, const float* A, const float* B, int M, int N,
+                     int K, fm_fmt fmt, uint8_t* Tq, uint8_t* Sq, float* dT, float* dS,
+                     void* workspace, size_t ws_bytes, void* hip_stream) {
+  clear_error();
+  if (!A || !B || !Tq || !Sq || !dT || !dS) return fail(FM_E_ARG, "null pointer");
+  if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
+  Geometry geo;
+  if (int rc = check_geometry(s, levels, M, N, K, geo)) return rc;
+  const Layout L = make_layout(geo, 1, 1);
+  if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
+  hipStream_t st = (hipStream_t)hip_stream;
+  char* ws = (char*)workspace;
+  int rc = FM_OK;
+  const fm_scheme* one[1] = {s};
+  Tables T = make_tables(one, 1, levels, geo, rc);
+  if (rc) return rc;
+  if ((rc = upload_tables(T, ws, L, st))) return rc;
+  float* Bt = (float*)(ws + L.bt);
+  if ((rc = launch_transpose(B, Bt, K, N, st))) return rc;
+  return form_chunk(geo, A, Bt, ws, L, T, 0, 1, fmt, Tq, Sq, dT, dS, st);
+}
+
+int fm_block_products(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
+                      int batch, int Mb, int Nb, int Kb, fm_fmt fmt, float* Mout,
+                      void* hip_stream) {
+  clear_error();
+  if (!Tq || !Sq || !dT || !dS || !Mout) return fail(FM_E_ARG, "null pointer");
+  if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
+  if (batch < 1 || Mb < 1 || Nb < 1 || Kb < 1) return fail(FM_E_ARG, "sizes must be positive");
+  if (Kb % 16) return fail(FM_E_SHAPE, "Kb must be a multiple of 16");
+  return launch_block_gemm(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, (hipStream_t)hip_stream);
+}
+
+int fm_reconstruct(const fm_scheme* s, int levels, const float* Mprod, int M, int N, float* C,
+                   void* workspace, size_t ws_bytes, void* hip_stream) {
+  clear_error();
+  if (!Mprod || !C) return fail(FM_E_ARG, "null pointer");
+  Geometry geo;
+  // K does not matter for the reconstruction; use the grid's k^L (Kb = 16).
+  long long gk = 1;
+  if (s)
+    for (int l = 0; l < levels && gk <= 64; ++l) gk *= s->k;
+  if (int rc = check_geometry(s, levels, M, N, (int)std::min<long long>(gk, 64) * 16, geo)) return rc;
+  const Layout L = make_layout(geo, 1, 1, false);
+  if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
+  hipStream_t st = (hipStream_t)hip_stream;
+  char* ws = (char*)workspace;
+  int rc = FM_OK;
+  const fm_scheme* one[1] = {s};
+  Tables T = make_tables(one, 1, levels, geo, rc);
+  if (rc) return rc;
+  if ((rc = upload_tables(T, ws, L, st))) return rc;
+  const ReconArgs ra = recon_args(geo, ws, L, 0, 1, Mprod, C, nullptr);
+  return launch_recon(ra, chunk_pattern(T, 2, 0, 1), st);
+}
+
+int fm_matmul_lowp(const fm_scheme* s, const float* A, const float* B, float* C, int M, int N,
+                   int K, int levels, fm_fmt fmt, void* workspace, size_t ws_bytes,
+                   void* hip_stream) {
+  clear_error();
+  if (!A || !B || !C) return fail(FM_E_ARG, "null pointer");
+  if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
+  Geometry geo;
+  if (int rc = check_geometry(s, levels, M, N, K, geo)) return rc;
+  const Layout L = make_layout(geo, 1, 1);
+  if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
+  hipStream_t st = (hipStream_t)hip_stream;
+  char* ws = (char*)workspace;
+  int rc = FM_OK;
+  const fm_scheme* one[1] = {s};
+  Tables T = make_tables(one, 1, levels, geo, rc);
+  if (rc) return rc;
+  if ((rc = upload_tables(T, ws, L, st))) return rc;
+  float* Bt = (float*)(ws + L.bt);
+  if ((rc = launch_transpose(B, Bt, K, N, st))) return rc;
+  uint8_t* Tq = (uint8_t*)(ws + L.tq);
+  uint8_t* Sq = (uint8_t*)(ws + L.sq);
+  if ((rc = form_chunk(geo, A, Bt, ws, L, T, 0, 1, fmt, Tq, Sq, nullptr, nullptr, st))) return rc;
+  const float* dd = (const float*)(ws + L.d);
+  float* Mp = (float*)(ws + L.mprod);
+  timing_begin(T_BLOCK_GEMM, st);
+  if ((rc = launch_block_gemm(Tq, Sq, dd, dd + geo.R, Mp, geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, st)))
+    return rc;
+  timing_end(T_BLOCK_GEMM, st);
+  const ReconArgs ra = recon_args(geo, ws, L, 0, 1, Mp, C, nullptr);
+  return launch_recon(ra, chunk_pattern(T, 2, 0, 1), st);
+}
+
+int fm_reference_f64(const float* A, const float* B, double* C_ref, int M, int N, int K,
+                     void* hip_stream) {
+  clear_error();
+  if (!A || !B || !C_ref) return fail(FM_E_ARG, "null pointer");
+  if (M < 1 || N < 1 || K < 1) return fail(FM_E_ARG, "sizes must be positive");
+  timing_begin(T_REFERENCE, (hipStream_t)hip_stream);
+  const int rc = launch_reference_f64(A, B, C_ref, M, N, K, (hipStream_t)hip_stream);
+  timing_end(T_REFERENCE, (hipStream_t)hip_stream);
+  return rc;
+}
+
+int fm_error_stats(const float* C, const double* C_ref, int M, int N, fm_stats* out,
+                   void* workspace, size_t ws_bytes, void* hip_stream) {
+  clear_error();
+  if (!C || !C_ref || !out) return fail(FM_E_ARG, "null pointer");
+  if (M < 1 || N < 1) return fail(FM_E_ARG, "sizes must be positive");
+  const size_t n = (size_t)M * N;
+  if (int rc = check_ws(workspace, ws_bytes, fm_error_workspace_size(M, N))) return rc;
+  hipStream_t st = (hipStream_t)hip_stream;
+  char* ws = (char*)workspace;
+  const int nblk = error_stats_blocks(n);
+  double* partial = (double*)ws;
+  double* out3 = (double*)(ws + up((size_t)nblk * 3 * 8));
+  if (int rc = launch_error_stats(C, C_ref, n, partial, st)) return rc;
+  if (int rc = launch_error_finalize(partial, nblk, out3, st)) return rc;
+  double h[3];
+  if (int rc = download(h, out3, sizeof(h), st)) return rc;
+  out->err_sq = h[0];
+  out->ref_sq = h[1];
+  out->max_abs = h[2];
+  out->rel_fro = h[1] > 0 ? std::sqrt(h[0]) / std::sqrt(h[1]) : 0.0;
+  if (!std::isfinite(h[0])) return fail(FM_E_NONFINITE, "non-finite error sum");
+  return FM_OK;
+}
+
+int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A, const float* B,
+                  const double* C_ref, int M, int N, int K, int levels, fm_fmt fmt,
+                  double* rel_fro_out, void* workspace, size_t ws_bytes, void* hip_stream) {
+  clear_error();
+  if (!gauged || !A || !B || !C_ref || !rel_fro_out) return fail(FM_E_ARG, "null pointer");
+  if (G < 1) return fail(FM_E_ARG, "G must be positive");
+  if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
+  Geometry geo;
+  if (int rc = check_geometry(gauged[0], levels, M, N, K, geo)) return rc;
+  int chunk = G;
+  Layout L = make_layout(geo, G, chunk);
+  while (chunk > 1 && L.total > ws_bytes) {
+    chunk = std::max(1, chunk / 2);
+    L = make_layout(geo, G, chunk);
+  }
+  if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
+  hipStream_t st = (hipStream_t)hip_stream;
+  char* ws = (char*)workspace;
+  int rc = FM_OK;
+  Tables T = make_tables(gauged, G, levels, geo, rc);
+  if (rc) return rc;
+  if ((rc = upload_tables(T, ws, L, st))) return rc;
+  if ((rc = launch_fill_u32((uint32_t*)(ws + L.flags), 1, 0u, st))) return rc;
+  float* Bt = (float*)(ws + L.bt);
+  if ((rc = launch_transpose(B, Bt, K, N, st))) return rc;
+  uint8_t* Tq = (uint8_t*)(ws + L.tq);
+  uint8_t* Sq = (uint8_t*)(ws + L.sq);
+  float* Mp = (float*)(ws + L.mprod);
+  const float* dd = (const float*)(ws + L.d);
+  double* errsq = (double*)(ws + L.errsq);
+  for (int g0 = 0; g0 < G; g0 += chunk) {
+    const int n = std::min(chunk, G - g0);
+    if ((rc = form_chunk(geo, A, Bt, ws, L, T, g0, n, fmt, Tq, Sq, nullptr, nullptr, st))) return rc;
+    timing_begin(T_BLOCK_GEMM, st);
+    if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)n * geo.R, Mp, n * geo.R, geo.Mb, geo.Nb,
+                                geo.Kb, fmt, st)))
+      return rc;
+    timing_end(T_BLOCK_GEMM, st);
+    const ReconArgs ra = recon_args(geo, ws, L, g0, n, Mp, nullptr, C_ref);
+    const int nblk = recon_blocks(ra);
+    timing_begin(T_RECON, st);
+    if ((rc = launch_recon(ra, chunk_pattern(T, 2, g0, n), st))) return rc;
+    timing_end(T_RECON, st);
+    if ((rc = launch_reduce_rows((double*)(ws + L.partial), nblk, n, errsq + g0, st))) return rc;
+  }
+  // sum of squares of the reference (err_sq of a zero output)
+  {
+    const size_t nel = (size_t)M * N;
+    const int nblk = error_stats_blocks(nel);
+    // reuse the product buffer as scratch for the partial sums
+    double* partial = (double*)Mp;
+    if ((size_t)nblk * 3 * 8 > (size_t)chunk * geo.R * geo.Mb * geo.Nb * 4)
+      return fail(FM_E_WORKSPACE, "workspace too small for the reference norm");
+    if ((rc = launch_error_stats(nullptr, C_ref, nel, partial, st))) return rc;
+    if ((rc = launch_error_finalize(partial, nblk, (double*)(ws + L.out3), st))) return rc;
+  }
+  std::vector<double> h((size_t)G + 3 + 1);
+  if ((rc = download(h.data(), errsq, (size_t)G * 8, st))) return rc;
+  double o3[3];
+  if ((rc = download(o3, ws + L.out3, sizeof(o3), st))) return rc;
+  uint32_t flag = 0;
+  if ((rc = download(&flag, ws + L.flags, 4, st))) return rc;
+  if (flag) return fail(FM_E_NONFINITE, "a block sum was not finite");
+  const double ref = std::sqrt(o3[1]);
+  for (int g = 0; g < G; ++g) rel_fro_out[g] = ref > 0 ? std::sqrt(h[g]) / ref : 0.0;
+  return FM_OK;
+}
+
+int fm_fp8_encode(const float* x, int64_t n, fm_fmt fmt, int impl, uint8_t* out,
+                  void* hip_stream) {
+  clear_error();
+  if (!x || !out) return fail(FM_E_ARG, "null pointer");
+  if (n < 0 || impl < 0 || impl > 2 || !fmt_ok(fmt)) return fail(FM_E_ARG, "bad argument");
+  return launch_fp8_encode(x, out, (size_t)n, fmt, impl, (hipStream_t)hip_stream);
+}
+
+const char* fm_scheme_kernel_family(const fm_scheme* s, int levels) {
+  clear_error();
+  if (!s || levels < 1 || levels > 8) {
+    fail(FM_E_ARG, "bad argument");
+    return "";
+  }
+  const fm_scheme f = power(*s, levels);
+  Lists L;
+  build_lists(f, L);
+  const int pa = match_pattern(0, L.a, f.R, f.m * f.k);
+  const int pb = match_pattern(1, L.b, f.R, f.n * f.k);
+  const int pw = match_pattern(2, L.w, f.R, f.m * f.n);
+  if (pa >= 0 && pa == pb && pb == pw) return pattern_name(pa);
+  return "generic";
+}
+
+int fm_timing_enable(int on) {
+  clear_error();
+  g_timing.on = on != 0;
+  return FM_OK;
+}
+
+int fm_timing_reset(void) {
+  clear_error();
+  for (auto& r : g_timing.recs) {
+    (void)hipEventSynchronize(r.stop);
+    g_timing.pool.push_back(r.start);
+    g_timing.pool.push_back(r.stop);
+  }
+  g_timing.recs.clear();
+  return FM_OK;
+}
+
+int fm_timing_read(const char* kernel_class, int* launches, double* total_ms) {
+  clear_error();
+  if (!kernel_class || !launches || !total_ms) return fail(FM_E_ARG, "null pointer");
+  int cls = -1;
+  for (int c = 0; c < T_COUNT; ++c)
+    if (std::strcmp(kernel_class, kTimedNames[c]) == 0) cls = c;
+  if (cls < 0) return fail(FM_E_ARG, std::string("unknown kernel class ") + kernel_class);
+  int n = 0;
+  double ms = 0.0;
+  for (auto& r : g_timing.recs) {
+    if (r.cls != cls) continue;
+    if (int rc = hip_check(hipEventSynchronize(r.stop), "hipEventSynchronize")) return rc;
+    float t = 0.f;
+    if (int rc = hip_check(hipEventElapsedTime(&t, r.start, r.stop), "hipEventElapsedTime"))
+      return rc;
+    ms += t;
+    ++n;
+  }
+  *launches = n;
+  *total_ms = ms;
+  return FM_OK;
+}
+
+int fm_status(void* workspace, size_t ws_bytes, void* hip_stream) {
+  clear_error();
+  if (!workspace || ws_bytes < kAlign) return fail(FM_E_WORKSPACE, "workspace too small");
+  hipStream_t st = (hipStream_t)hip_stream;
+  uint32_t flag = 0;
+  if (int rc = download(&flag, workspace, 4, st)) return rc;
+  if (int rc = launch_fill_u32((uint32_t*)workspace, 1, 0u, st)) return rc;
+  if (flag) return fail(FM_E_NONFINITE, "a block sum was not finite");
+  return FM_OK;
+}
+
+}  // extern "C"

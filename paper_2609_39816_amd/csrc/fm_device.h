@@ -1,0 +1,538 @@
+// Device-side building blocks of libfm shared by the kernel translation
+// units: wave reductions, FP8 encoders, compile-time loops, and the
+// operand-formation and reconstruction kernels (specialized for a nonzero
+// structure, or generic) with their launch helpers.  Each specialized
+// family is instantiated in its own translation unit (fm_fam_*.hip) so the
+// large unrolled kernels compile in parallel.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <utility>
+
+#include "fm_internal.h"
+#include "fm_patterns.inc"
+
+#ifndef FM_FP8_HW
+#define FM_FP8_HW 0  // 1: v_cvt_pk_{fp8,bf8}_f32 for FP8 rounding; 0: integer encoder
+#endif
+
+namespace fm {
+namespace dev {
+
+inline constexpr int kThreads = 256;
+
+// ------------------------------------------------------------ wave helpers
+// Maximum over the 64 lanes of a wave of non-negative values; every lane
+// returns the result.  DPP row shifts build each row's maximum in its lane
+// 15, two row broadcasts carry it to lane 63.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false));
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// ------------------------------------------------------------ FP8 encoding
+// Integer encoders (round to nearest even, saturating to the largest finite
+// value).  Normal range: round the fp32 significand at the FP8 mantissa
+// width with the usual add-bias-and-truncate; the exponent follows through
+// any carry.  Below the smallest normal the FP8 values are multiples of the
+// subnormal quantum, so scaling by its inverse (a power of two, exact) and
+// rounding to the nearest integer (ties to even) gives the code directly.
+__device__ __forceinline__ uint32_t enc_e4m3_sw(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const uint32_t s = (u >> 24) & 0x80u;
+  const uint32_t a = u & 0x7fffffffu;
+  uint32_t code;
+  if (a >= 0x3C800000u) {  // |x| >= 2^-6
+    const uint32_t r = a + 0x7FFFFu + ((a >> 20) & 1u);
+    code = min((r >> 20) - (120u << 3), 0x7Eu);
+  } else {
+    code = (uint32_t)__builtin_rintf(__uint_as_float(a) * 512.0f);
+  }
+  return s | code;
+}
+
+__device__ __forceinline__ uint32_t enc_e5m2_sw(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const uint32_t s = (u >> 24) & 0x80u;
+  const uint32_t a = u & 0x7fffffffu;
+  uint32_t code;
+  if (a >= 0x38800000u) {  // |x| >= 2^-14
+    const uint32_t r = a + 0xFFFFFu + ((a >> 21) & 1u);
+    code = min((r >> 21) - (112u << 2), 0x7Bu);
+  } else {
+    code = (uint32_t)__builtin_rintf(__uint_as_float(a) * 65536.0f);
+  }
+  return s | code;
+}
+
+// Two values -> two code bytes (low half of the result).
+template <int IMPL>
+__device__ __forceinline__ uint32_t enc2(float x0, float x1, int fmt) {
+  if (IMPL == 1) {
+    if (fmt == FM_E4M3) return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x0, x1, 0, false) & 0xffffu;
+    return (uint32_t)__builtin_amdgcn_cvt_pk_bf8_f32(x0, x1, 0, false) & 0xffffu;
+  }
+  if (fmt == FM_E4M3) return enc_e4m3_sw(x0) | (enc_e4m3_sw(x1) << 8);
+  return enc_e5m2_sw(x0) | (enc_e5m2_sw(x1) << 8);
+}
+
+__device__ __forceinline__ uint32_t enc2d(float x0, float x1, int fmt) {
+  return enc2<FM_FP8_HW>(x0, x1, fmt);
+}
+
+// ----------------------------------------------------- compile-time loops
+// sfor<B, E>(f) calls f(std::integral_constant<int, i>) for i in [B, E), so
+// the body sees i as a constant expression.
+template <int B, class F, int... I>
+__device__ __forceinline__ void sfor_impl(F& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, B + I>{}), ...);
+}
+template <int B, int E, class F>
+__device__ __forceinline__ void sfor(F&& f) {
+  if constexpr (E > B) sfor_impl<B>(f, std::make_integer_sequence<int, E - B>{});
+}
+
+// ------------------------------------------------------- operand formation
+// A thread owns VW consecutive positions (x, y0..y0+VW-1) of the block-sum
+// tensors and reads the matching entries of every grid block once per
+// position group; for each gauge of its slice and each product r it forms
+// the block sum as a chain of fmaf over the product's list (ascending grid
+// order) from +0, then either folds |T| into the per-tensor maximum
+// (MODE 0) or writes the FP8 codes of T * (FMAX / amax) (MODE 1).
+
+template <int NB, int VW>
+__device__ __forceinline__ void form_load(const FormArgs& a, float (&xv)[NB][VW], bool active,
+                                          int x, int y0) {
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    if (active) {
+      const int bi = b / a.gc, bj = b - (b / a.gc) * a.gc;
+      const float* src = a.X + (size_t)(bi * a.br + x) * a.cols + (size_t)bj * a.bc + y0;
+      if constexpr (VW % 4 == 0) {
+#pragma unroll
+        for (int v = 0; v < VW; v += 4) {
+          const float4 t = *reinterpret_cast<const float4*>(src + v);
+          xv[b][v] = t.x;
+          xv[b][v + 1] = t.y;
+          xv[b][v + 2] = t.z;
+          xv[b][v + 3] = t.w;
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < VW; ++v) xv[b][v] = src[v];
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < VW; ++v) xv[b][v] = 0.0f;
+    }
+  }
+}
+
+template <int VW, int MODE>
+__device__ __forceinline__ void form_finish(const FormArgs& a, const float (&acc)[VW], int g,
+                                            int g0, int r, bool active, int x, int y0,
+                                            uint32_t* smax, int lane) {
+  if constexpr (MODE == 0) {
+    uint32_t mx = 0u;
+#pragma unroll
+    for (int v = 0; v < VW; ++v) mx = max(mx, __float_as_uint(acc[v]) & 0x7fffffffu);
+    if (!active) mx = 0u;
+    mx = wave_max_u32(mx);
+    if (lane == 0 && mx) atomicMax(&smax[(g - g0) * a.R + r], mx);
+  } else {
+    if (!active) return;
+    const float q = a.q[(size_t)g * a.R + r];
+    uint8_t* dst =
+        a.codes + ((size_t)g * a.R + r) * ((size_t)a.br * a.bc) + (size_t)x * a.bc + y0;
+    if constexpr (VW >= 4) {
+      uint32_t w[VW / 4];
+#pragma unroll
+      for (int t = 0; t < VW / 4; ++t)
+        w[t] = enc2d(acc[4 * t] * q, acc[4 * t + 1] * q, a.fmt) |
+               (enc2d(acc[4 * t + 2] * q, acc[4 * t + 3] * q, a.fmt) << 16);
+      if constexpr (VW == 4) {
+        *reinterpret_cast<uint32_t*>(dst) = w[0];
+      } else if constexpr (VW == 8) {
+        *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
+      } else {
+#pragma unroll
+        for (int t = 0; t < VW / 4; t += 4)
+          *reinterpret_cast<uint4*>(dst + 4 * t) = make_uint4(w[t], w[t + 1], w[t + 2], w[t + 3]);
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < VW; ++v) dst[v] = (uint8_t)(enc2d(acc[v] * q, 0.0f, a.fmt) & 0xffu);
+    }
+  }
+}
+
+template <int MODE>
+__device__ __forceinline__ void form_flush(const FormArgs& a, const uint32_t* smax, int g0,
+                                           int g1) {
+  if constexpr (MODE == 0) {
+    __syncthreads();
+    const int n = (g1 - g0) * a.R;
+    for (int i = threadIdx.x; i < n; i += kThreads)
+      if (smax[i]) atomicMax(&a.amax[(size_t)g0 * a.R + i], smax[i]);
+  }
+}
+
+// Specialized for one nonzero structure P (fm_patterns.inc): block indices
+// are compile-time constants, so the operand blocks stay in registers.
+template <class P, int VW, int MODE>
+__global__ __launch_bounds__(kThreads) void form_static_kernel(FormArgs a, int gpb) {
+  extern __shared__ uint32_t smax[];
+  const int bcv = a.bc / VW;
+  const int Ptot = a.br * bcv;
+  const int g0 = blockIdx.y * gpb;
+  const int g1 = min(a.G, g0 + gpb);
+  const int lane = threadIdx.x & 63;
+  if constexpr (MODE == 0) {
+    for (int i = threadIdx.x; i < gpb * P::R; i += kThreads) smax[i] = 0u;
+    __syncthreads();
+  }
+  for (int base = blockIdx.x * kThreads; base < Ptot; base += gridDim.x * kThreads) {
+    const int p = base + threadIdx.x;
+    const bool active = p < Ptot;
+    const int x = active ? p / bcv : 0;
+    const int y0 = active ? (p - x * bcv) * VW : 0;
+    float xv[P::NB][VW];
+    form_load<P::NB, VW>(a, xv, active, x, y0);
+    for (int g = g0; g < g1; ++g) {
+      const float* coef = a.coef + a.off[(size_t)g * (P::R + 1)];
+      sfor<0, P::R>([&](auto rc) {
+        constexpr int r = decltype(rc)::value;
+        float acc[VW];
+#pragma unroll
+        for (int v = 0; v < VW; ++v) acc[v] = 0.0f;
+        sfor<P::rowptr[r], P::rowptr[r + 1]>([&](auto ec) {
+          constexpr int e = decltype(ec)::value;
+          constexpr int b = P::idx[e];
+          const float c = coef[e];
+#pragma unroll
+          for (int v = 0; v < VW; ++v) acc[v] = __builtin_fmaf(c, xv[b][v], acc[v]);
+        });
+        form_finish<VW, MODE>(a, acc, g, g0, r, active, x, y0, smax, lane);
+      });
+    }
+  }
+  form_flush<MODE>(a, smax, g0, g1);
+}
+
+// Any nonzero structure: each thread parks its operand values in its own
+// slots of LDS ([block][thread][VW]) and gathers them by the run-time block
+// index of each list entry.
+template <int VW, int MODE>
+__global__ __launch_bounds__(kThreads) void form_generic_kernel(FormArgs a, int gpb) {
+  extern __shared__ float dyn[];
+  const int nb = a.gr * a.gc;
+  float* lx = dyn;
+  uint32_t* smax = reinterpret_cast<uint32_t*>(dyn + (size_t)nb * kThreads * VW);
+  const int R = a.R;
+  const int bcv = a.bc / VW;
+  const int Ptot = a.br * bcv;
+  const int g0 = blockIdx.y * gpb;
+  const int g1 = min(a.G, g0 + gpb);
+  const int lane = threadIdx.x & 63;
+  if constexpr (MODE == 0) {
+    for (int i = threadIdx.x; i < gpb * R; i += kThreads) smax[i] = 0u;
+    __syncthreads();
+  }
+  for (int base = blockIdx.x * kThreads; base < Ptot; base += gridDim.x * kThreads) {
+    const int p = base + threadIdx.x;
+    const bool active = p < Ptot;
+    const int x = active ? p / bcv : 0;
+    const int y0 = active ? (p - x * bcv) * VW : 0;
+    for (int b = 0; b < nb; ++b) {
+      float* slot = lx + ((size_t)b * kThreads + threadIdx.x) * VW;
+      const int bi = b / a.gc, bj = b - (b / a.gc) * a.gc;
+      const float* src = a.X + (size_t)(bi * a.br + x) * a.cols + (size_t)bj * a.bc + y0;
+#pragma unroll
+      for (int v = 0; v < VW; ++v) slot[v] = active ? src[v] : 0.0f;
+    }
+    for (int g = g0; g < g1; ++g) {
+      const int32_t* off = a.off + (size_t)g * (R + 1);
+      for (int r = 0; r < R; ++r) {
+        const int e0 = off[r], e1 = off[r + 1];
+        float acc[VW];
+#pragma unroll
+        for (int v = 0; v < VW; ++v) acc[v] = 0.0f;
+        for (int e = e0; e < e1; ++e) {
+          const float c = a.coef[e];
+          const float* slot = lx + ((size_t)a.idx[e] * kThreads + threadIdx.x) * VW;
+#pragma unroll
+          for (int v = 0; v < VW; ++v) acc[v] = __builtin_fmaf(c, slot[v], acc[v]);
+        }
+        form_finish<VW, MODE>(a, acc, g, g0, r, active, x, y0, smax, lane);
+      }
+    }
+  }
+  form_flush<MODE>(a, smax, g0, g1);
+}
+// ------------------------------------------------- reconstruction + error
+// A thread owns VW consecutive positions (x, z0..) of every output block;
+// it reads each product's values there once, adds w * M_r into the output
+// blocks the product feeds (ascending r for every block, fmaf from +0), and
+// then writes C and/or accumulates (C - Cref)^2 in float64.
+template <int VW>
+__device__ __forceinline__ void recon_load(const float* src, float (&m)[VW]) {
+  if constexpr (VW % 4 == 0) {
+#pragma unroll
+    for (int v = 0; v < VW; v += 4) {
+      const float4 t = *reinterpret_cast<const float4*>(src + v);
+      m[v] = t.x;
+      m[v + 1] = t.y;
+      m[v + 2] = t.z;
+      m[v + 3] = t.w;
+    }
+  } else {
+#pragma unroll
+    for (int v = 0; v < VW; ++v) m[v] = src[v];
+  }
+}
+
+template <int VW>
+__device__ __forceinline__ void recon_emit(const ReconArgs& a, int c, int x, int z0,
+                                           const float (&acc)[VW], double& esq) {
+  const int i = c / a.gn, j = c - (c / a.gn) * a.gn;
+  const size_t o = (size_t)(i * a.Mb + x) * a.N + (size_t)j * a.Nb + z0;
+  if (a.C) {
+#pragma unroll
+    for (int v = 0; v < VW; ++v) a.C[o + v] = acc[v];
+  }
+  if (a.Cref) {
+#pragma unroll
+    for (int v = 0; v < VW; ++v) {
+      const double dlt = (double)acc[v] - a.Cref[o + v];
+      esq = __fma_rn(dlt, dlt, esq);
+    }
+  }
+}
+
+__device__ __forceinline__ void recon_reduce(const ReconArgs& a, double esq, double* red) {
+  if (!a.Cref) return;
+  red[threadIdx.x] = esq;
+  __syncthreads();
+  for (int s = kThreads / 2; s > 0; s >>= 1) {
+    if (threadIdx.x < s) red[threadIdx.x] = red[threadIdx.x] + red[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) a.partial[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = red[0];
+}
+
+template <class P, int VW>
+__global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a) {
+  __shared__ double red[kThreads];
+  const int g = blockIdx.y;
+  const int bcv = a.Nb / VW;
+  const int Ptot = a.Mb * bcv;
+  const size_t bsz = (size_t)a.Mb * a.Nb;
+  const float* coef = a.coef + a.off[(size_t)g * (P::R + 1)];
+  double esq = 0.0;
+  for (int base = blockIdx.x * kThreads; base < Ptot; base += gridDim.x * kThreads) {
+    const int p = base + threadIdx.x;
+    if (p >= Ptot) break;
+    const int x = p / bcv, z0 = (p - x * bcv) * VW;
+    float acc[P::NB][VW];
+#pragma unroll
+    for (int c = 0; c < P::NB; ++c)
+#pragma unroll
+      for (int v = 0; v < VW; ++v) acc[c][v] = 0.0f;
+    const float* mb = a.Mprod + (size_t)g * P::R * bsz + (size_t)x * a.Nb + z0;
+    sfor<0, P::R>([&](auto rc) {
+      constexpr int r = decltype(rc)::value;
+      // keep the scheduler from hoisting every product's load to the top
+      // (343 products would not fit in registers): one group of 8 at a time
+      if constexpr (r % 8 == 0 && r > 0) __builtin_amdgcn_sched_barrier(0);
+      if constexpr (P::rowptr[r + 1] > P::rowptr[r]) {
+        float m[VW];
+        recon_load<VW>(mb + (size_t)r * bsz, m);
+        sfor<P::rowptr[r], P::rowptr[r + 1]>([&](auto ec) {
+          constexpr int e = decltype(ec)::value;
+          constexpr int c = P::idx[e];
+          const float w = coef[e];
+#pragma unroll
+          for (int v = 0; v < VW; ++v) acc[c][v] = __builtin_fmaf(w, m[v], acc[c][v]);
+        });
+      }
+    });
+#pragma unroll
+    for (int c = 0; c < P::NB; ++c) recon_emit<VW>(a, c, x, z0, acc[c], esq);
+  }
+  recon_reduce(a, esq, red);
+}
+
+template <int VW>
+__global__ __launch_bounds__(kThreads) void recon_generic_kernel(ReconArgs a) {
+  __shared__ double red[kThreads];
+  extern __shared__ float lacc[];  // [NC][thread][VW]
+  const int g = blockIdx.y;
+  const int R = a.R, NC = a.gm * a.gn;
+  const int bcv = a.Nb / VW;
+  const int Ptot = a.Mb * bcv;
+  const size_t bsz = (size_t)a.Mb * a.Nb;
+  const int32_t* off = a.off + (size_t)g * (R + 1);
+  double esq = 0.0;
+  for (int base = blockIdx.x * kThreads; base < Ptot; base += gridDim.x * kThreads) {
+    const int p = base + threadIdx.x;
+    if (p >= Ptot) break;
+    const int x = p / bcv, z0 = (p - x * bcv) * VW;
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int v = 0; v < VW; ++v) lacc[((size_t)c * kThreads + threadIdx.x) * VW + v] = 0.0f;
+    const float* mb = a.Mprod + (size_t)g * R * bsz + (size_t)x * a.Nb + z0;
+    for (int r = 0; r < R; ++r) {
+      const int e0 = off[r], e1 = off[r + 1];
+      if (e0 == e1) continue;
+      float m[VW];
+      recon_load<VW>(mb + (size_t)r * bsz, m);
+      for (int e = e0; e < e1; ++e) {
+        const float w = a.coef[e];
+        float* s = lacc + ((size_t)a.idx[e] * kThreads + threadIdx.x) * VW;
+#pragma unroll
+        for (int v = 0; v < VW; ++v) s[v] = __builtin_fmaf(w, m[v], s[v]);
+      }
+    }
+    for (int c = 0; c < NC; ++c) {
+      float acc[VW];
+#pragma unroll
+      for (int v = 0; v < VW; ++v) acc[v] = lacc[((size_t)c * kThreads + threadIdx.x) * VW + v];
+      recon_emit<VW>(a, c, x, z0, acc, esq);
+    }
+  }
+  recon_reduce(a, esq, red);
+}
+
+inline int launched(const char* what) { return hip_check(hipGetLastError(), what); }
+
+// Workgroups for operand formation: enough to cover the GPU several times,
+// each looping over position groups; gauges split over grid.y.
+inline dim3 form_grid(const FormArgs& a, int vw, int mode, int& gpb) {
+  const int P = a.br * (a.bc / vw);
+  gpb = (mode == 0) ? std::max(1, std::min(a.G, 4096 / std::max(1, a.R)))
+                    : std::max(1, std::min(a.G, 8));
+  const int gy = (a.G + gpb - 1) / gpb;
+  int gx = (P + kThreads - 1) / kThreads;
+  const int target = 8192;
+  if ((long long)gx * gy > target) gx = std::max(1, target / gy);
+  return dim3(gx, gy);
+}
+
+template <class P>
+constexpr int static_vw() {
+  return P::NB <= 4 ? 16 : (P::NB <= 16 ? 8 : 2);
+}
+
+template <class P, int MODE>
+int launch_form_static(const FormArgs& a, hipStream_t st) {
+  constexpr int VW = static_vw<P>();
+  int gpb;
+  const dim3 grid = form_grid(a, VW, MODE, gpb);
+  const size_t shm = (MODE == 0) ? (size_t)gpb * a.R * 4 : 0;
+  form_static_kernel<P, VW, MODE><<<grid, kThreads, shm, st>>>(a, gpb);
+  return launched("form_static_kernel");
+}
+
+template <class P>
+bool static_ok(const FormArgs& a) {
+  constexpr int VW = static_vw<P>();
+  return a.gr * a.gc == P::NB && a.R == P::R && a.bc % VW == 0 && (VW < 4 || a.cols % 4 == 0);
+}
+
+template <int VW>
+int launch_form_generic_t(const FormArgs& a, int mode, hipStream_t st) {
+  int gpb;
+  const dim3 grid = form_grid(a, VW, mode, gpb);
+  const size_t shm = (size_t)a.gr * a.gc * kThreads * VW * 4 + (mode == 0 ? (size_t)gpb * a.R * 4 : 0);
+  if (shm > 160 * 1024) return fail(FM_E_UNSUPPORTED, "formation needs too much LDS");
+  const void* fn = mode == 0 ? reinterpret_cast<const void*>(&form_generic_kernel<VW, 0>)
+                             : reinterpret_cast<const void*>(&form_generic_kernel<VW, 1>);
+  if (int rc = hip_check(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)shm),
+                         "hipFuncSetAttribute"))
+    return rc;
+  if (mode == 0)
+    form_generic_kernel<VW, 0><<<grid, kThreads, shm, st>>>(a, gpb);
+  else
+    form_generic_kernel<VW, 1><<<grid, kThreads, shm, st>>>(a, gpb);
+  return launched("form_generic_kernel");
+}
+
+inline int launch_form_generic(const FormArgs& a, int mode, hipStream_t st) {
+  const int nb = a.gr * a.gc;
+  if (nb <= 16 && a.bc % 4 == 0) return launch_form_generic_t<4>(a, mode, st);
+  return launch_form_generic_t<1>(a, mode, st);
+}
+
+template <class P>
+constexpr int recon_vw() {
+  return P::NB <= 16 ? 4 : 1;
+}
+
+template <class P>
+int launch_recon_static(const ReconArgs& a, hipStream_t st) {
+  constexpr int VW = recon_vw<P>();
+  dim3 grid(recon_blocks(a), a.G);
+  recon_static_kernel<P, VW><<<grid, kThreads, 0, st>>>(a);
+  return launched("recon_static_kernel");
+}
+
+inline int launch_recon_generic(const ReconArgs& a, hipStream_t st) {
+  const int nc = a.gm * a.gn;
+  dim3 grid(recon_blocks(a), a.G);
+  const bool wide = nc <= 16 && a.Nb % 4 == 0 && a.N % 4 == 0;
+  const size_t shm = (size_t)nc * kThreads * 4 * (wide ? 4 : 1);
+  const void* fn = wide ? reinterpret_cast<const void*>(&recon_generic_kernel<4>)
+                        : reinterpret_cast<const void*>(&recon_generic_kernel<1>);
+  if (int rc = hip_check(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)shm),
+                         "hipFuncSetAttribute"))
+    return rc;
+  if (wide) {
+    recon_generic_kernel<4><<<grid, kThreads, shm, st>>>(a);
+  } else {
+    recon_generic_kernel<1><<<grid, kThreads, shm, st>>>(a);
+  }
+  return launched("recon_generic_kernel");
+}
+
+
+}  // namespace dev
+
+// Entry points of one specialized family (defined in fm_fam_<P>.hip).
+// Return 1 when the arguments do not fit the family's kernels (the caller
+// then uses the generic kernels), else FM_OK or an error code.
+#define FM_DECLARE_FAMILY(P)                                                  \
+  int form_family_##P(const FormArgs& a, int mode, int side, hipStream_t st); \
+  int recon_family_##P(const ReconArgs& a, hipStream_t st);
+FM_PATTERN_FAMILIES(FM_DECLARE_FAMILY)
+#undef FM_DECLARE_FAMILY
+
+#define FM_DEFINE_FAMILY(P)                                                          \
+  int form_family_##P(const FormArgs& a, int mode, int side, hipStream_t st) {       \
+    using namespace dev;                                                             \
+    if (side == 0) {                                                                 \
+      if (!static_ok<pat::P::A>(a)) return 1;                                        \
+      return mode ? launch_form_static<pat::P::A, 1>(a, st)                          \
+                  : launch_form_static<pat::P::A, 0>(a, st);                         \
+    }                                                                                \
+    if (!static_ok<pat::P::B>(a)) return 1;                                          \
+    return mode ? launch_form_static<pat::P::B, 1>(a, st)                            \
+                : launch_form_static<pat::P::B, 0>(a, st);                           \
+  }                                                                                  \
+  int recon_family_##P(const ReconArgs& a, hipStream_t st) {                         \
+    using namespace dev;                                                             \
+    using W = pat::P::W;                                                             \
+    if (a.gm * a.gn != W::NB || a.R != W::R || a.Nb % recon_vw<W>() != 0 || a.N % 4) \
+      return 1;                                                                      \
+    return launch_recon_static<W>(a, st);                                            \
+  }
+
+}  // namespace fm

@@ -1,0 +1,146 @@
+// Internal declarations shared by the host code and the HIP kernels of
+// libfm.  Not part of the public ABI (include/fm.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "fm.h"
+
+struct fm_scheme {
+  int m = 0, n = 0, k = 0, R = 0;
+  std::vector<double> U, V, W;  // R x (m*k), R x (k*n), R x (m*n)
+};
+
+namespace fm {
+
+// ---------------------------------------------------------------- errors
+int fail(int code, const std::string& msg);  // records msg, returns code
+void clear_error();
+int hip_check(hipError_t e, const char* what);
+
+// ------------------------------------------------------- scheme (host)
+double brent_residual(const fm_scheme& s);
+fm_scheme kron(const fm_scheme& a, const fm_scheme& b);
+fm_scheme power(const fm_scheme& s, int levels);
+// Inverse of an n x n row-major matrix (false if singular).
+bool invert(const std::vector<double>& P, int n, std::vector<double>& out);
+
+// Coefficient lists of one flattened scheme, in the orders the kernels use
+// (struct of arrays: offsets, block indices, fp32 coefficients):
+//   a: per product r, nonzero u in ascending row-major (i,l); idx = i*gk + l
+//      (block index in A's gm x gk grid);
+//   b: per product r, nonzero v in ascending row-major (l,j); idx = j*gk + l
+//      (block index in B^T's gn x gk grid, where the kernels read B);
+//   w: per product r, nonzero w with idx = i*gn + j, r-major (so every
+//      output block receives its terms in ascending r).
+struct Side {
+  std::vector<int32_t> off;  // R + 1
+  std::vector<int32_t> idx;
+  std::vector<float> coef;
+};
+struct Lists {
+  Side a, b, w;
+};
+void build_lists(const fm_scheme& flat, Lists& out);
+
+// Pattern family of one side of a list (compiled specializations), or -1.
+int match_pattern(int side, const Side& s, int R, int NB);
+// Number of pattern families; side: 0 = A, 1 = B, 2 = W.
+int pattern_count();
+const char* pattern_name(int id);
+
+// Geometry of one evaluation.
+struct Geometry {
+  int gm, gk, gn, R;       // flattened grid and rank
+  int M, N, K;             // full sizes
+  int Mb, Nb, Kb;          // block sizes
+  int NBa() const { return gm * gk; }
+  int NBb() const { return gn * gk; }
+  int NC() const { return gm * gn; }
+};
+
+// ------------------------------------------------------ kernel timing
+// Kernel classes timed by fm_timing_*; timing_begin/timing_end bracket one
+// launch with events on its stream when timing is enabled.
+enum TimedClass { T_FORM_AMAX = 0, T_FORM_QUANT, T_BLOCK_GEMM, T_RECON, T_REFERENCE, T_COUNT };
+void timing_begin(int cls, hipStream_t st);
+void timing_end(int cls, hipStream_t st);
+
+// ----------------------------------------------------- kernel launchers
+// All launchers enqueue on `st` and return FM_OK or FM_E_HIP /
+// FM_E_UNSUPPORTED.
+
+// Fill n 32-bit words with `value`.
+int launch_fill_u32(uint32_t* p, size_t n, uint32_t value, hipStream_t st);
+
+// Bt (cols x rows) = X^T for X rows x cols, fp32.
+int launch_transpose(const float* X, float* Xt, int rows, int cols, hipStream_t st);
+
+// Operand formation over a chunk of gauges (G gauges, lists already on the
+// device).  X: rows x cols fp32, grid gr x gc; off: G*(R+1) offsets into ent.
+// mode 0: amax[g*R + r] = max(amax, bits(|T|)) (atomic max on uint bits);
+// mode 1: codes[(g*R + r)*br*bc + ...] = FP8(T * q[g*R + r]).
+struct FormArgs {
+  const float* X;
+  int rows, cols, gr, gc, br, bc;
+  const int32_t* off;  // G*(R+1), absolute indices into idx/coef
+  const int32_t* idx;
+  const float* coef;
+  int R, G;
+  uint32_t* amax;   // mode 0
+  const float* q;   // mode 1
+  uint8_t* codes;   // mode 1
+  int fmt;
+};
+// pattern: family id from match_pattern (side A or B), or -1 for the
+// generic kernel.
+int launch_form(const FormArgs& a, int mode, int pattern, int side, hipStream_t st);
+
+// Scales from amax: for i < n: q[i] = FMAX/amax, d[i] = amax/FMAX (1, 1 for
+// amax = 0); a non-finite amax sets *flag |= 1.
+int launch_scales(const uint32_t* amax, float* q, float* d, int n, int fmt, uint32_t* flag,
+                  hipStream_t st);
+
+// Batched FP8 block products: Mout[b] = ((Tq[b] Sq[b]^T) * dT[b]) * dS[b].
+int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
+                      float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, hipStream_t st);
+
+// Reconstruction + error: for gauge g < G, C_g = sum_r w M_{g,r}; if C is not
+// null it is written (G must be 1); if Cref is not null, partial sums of
+// (C - Cref)^2 go to partial[g*nblk + blk].  Returns nblk through *nblk_out.
+struct ReconArgs {
+  const float* Mprod;  // G x R x Mb x Nb
+  const int32_t* off;  // G*(R+1)
+  const int32_t* idx;
+  const float* coef;
+  int R, G, gm, gn, Mb, Nb, N;
+  float* C;            // optional
+  const double* Cref;  // optional
+  double* partial;     // G x nblk (if Cref)
+};
+int recon_blocks(const ReconArgs& a);  // number of blocks per gauge the launcher uses
+int launch_recon(const ReconArgs& a, int pattern, hipStream_t st);
+
+// out[g] = sum_{b < nblk} partial[g*nblk + b] (fixed order), g < G.
+int launch_reduce_rows(const double* partial, int nblk, int G, double* out, hipStream_t st);
+
+// Float64 reference C = A B.
+int launch_reference_f64(const float* A, const float* B, double* C, int M, int N, int K,
+                         hipStream_t st);
+
+// Error statistics partials over n elements: per block (err_sq, ref_sq,
+// max_abs) into partial[3*blk...]; nblk blocks.
+int error_stats_blocks(size_t n);
+int launch_error_stats(const float* C, const double* Cref, size_t n, double* partial,
+                       hipStream_t st);
+int launch_error_finalize(const double* partial, int nblk, double* out3, hipStream_t st);
+
+// Diagnostic encoder: codes for n fp32 values with the kernels' encoder.
+int launch_fp8_encode(const float* x, uint8_t* out, size_t n, int fmt, int impl, hipStream_t st);
+
+}  // namespace fm

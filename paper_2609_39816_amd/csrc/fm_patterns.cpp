@@ -1,0 +1,51 @@
+// Run-time matching of a scheme's coefficient lists against the nonzero
+// structures that have specialized kernels (fm_patterns.inc).
+#include <cstring>
+
+#include "fm_internal.h"
+#include "fm_patterns.inc"
+
+namespace fm {
+namespace {
+
+struct PatternRef {
+  const char* name;
+  int R;
+  int nb[3];
+  int nnz[3];
+  const int16_t* rowptr[3];
+  const int16_t* idx[3];
+};
+
+#define FM_PATTERN_REF(P)                                                    \
+  PatternRef{#P,                                                             \
+             pat::P::R,                                                      \
+             {pat::P::A::NB, pat::P::B::NB, pat::P::W::NB},                  \
+             {pat::P::A::NNZ, pat::P::B::NNZ, pat::P::W::NNZ},               \
+             {pat::P::A::rowptr, pat::P::B::rowptr, pat::P::W::rowptr},      \
+             {pat::P::A::idx, pat::P::B::idx, pat::P::W::idx}},
+
+const PatternRef kPatterns[] = {FM_PATTERN_FAMILIES(FM_PATTERN_REF)};
+constexpr int kNumPatterns = sizeof(kPatterns) / sizeof(kPatterns[0]);
+
+}  // namespace
+
+int pattern_count() { return kNumPatterns; }
+
+const char* pattern_name(int id) {
+  return (id >= 0 && id < kNumPatterns) ? kPatterns[id].name : "generic";
+}
+
+int match_pattern(int side, const Side& s, int R, int NB) {
+  for (int p = 0; p < kNumPatterns; ++p) {
+    const PatternRef& P = kPatterns[p];
+    if (P.R != R || P.nb[side] != NB || P.nnz[side] != (int)s.idx.size()) continue;
+    bool ok = true;
+    for (int r = 0; r <= R && ok; ++r) ok = (P.rowptr[side][r] == s.off[r] - s.off[0]);
+    for (size_t e = 0; e < s.idx.size() && ok; ++e) ok = (P.idx[side][e] == s.idx[e]);
+    if (ok) return p;
+  }
+  return -1;
+}
+
+}  // namespace fm

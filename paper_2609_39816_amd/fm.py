@@ -1,0 +1,327 @@
+"""Python binding of libfm (include/fm.h): argument marshalling only.
+
+Every step of the FP8 schedule runs in the library's HIP kernels; PyTorch
+only provides device memory and the current stream.  Importing this module
+fails loudly if the compiled library is missing: there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes as ct
+import os
+import re
+
+import numpy as np
+
+try:  # torch first: libfm then binds to the HIP runtime torch has loaded
+    import torch
+except ImportError:  # pragma: no cover - torch is part of the environment
+    torch = None
+
+from . import schemes as _schemes
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libfm.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "fm.h")
+
+E4M3, E5M2 = 0, 1
+FMTS = {"e4m3": E4M3, "e5m2": E5M2}
+ERRORS = {0: "FM_OK", -1: "FM_E_ARG", -2: "FM_E_SHAPE", -3: "FM_E_BRENT", -4: "FM_E_SINGULAR",
+          -5: "FM_E_NONFINITE", -6: "FM_E_WORKSPACE", -7: "FM_E_HIP", -8: "FM_E_MISMATCH",
+          -9: "FM_E_NOMEM", -10: "FM_E_UNSUPPORTED"}
+
+
+class FmError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+        self.name = ERRORS.get(code, str(code))
+
+
+class _Stats(ct.Structure):
+    _fields_ = [("rel_fro", ct.c_double), ("err_sq", ct.c_double), ("ref_sq", ct.c_double),
+                ("max_abs", ct.c_double)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"libfm is not built ({LIB_PATH} missing); run __graft_entry__.build() "
+                          "or python paper_2609_39816_amd/build.py")
+    L = ct.CDLL(LIB_PATH)
+    p, i, d, sz, i64 = ct.c_void_p, ct.c_int, ct.c_double, ct.c_size_t, ct.c_int64
+    pp = ct.POINTER(ct.c_void_p)
+    sig = {
+        "fm_strerror": (ct.c_char_p, [i]),
+        "fm_last_error": (ct.c_char_p, []),
+        "fm_version": (ct.c_char_p, []),
+        "fm_scheme_load": (i, [p, p, p, i, i, i, i, pp]),
+        "fm_gauge_apply": (i, [p, p, p, p, pp]),
+        "fm_scheme_kron": (i, [p, i, pp]),
+        "fm_scheme_dims": (i, [p, p, p, p, p]),
+        "fm_scheme_coeffs": (i, [p, p, p, p]),
+        "fm_scheme_coeffs_f32": (i, [p, i, p, p, p]),
+        "fm_scheme_free": (None, [p]),
+        "fm_workspace_size": (sz, [p, i, i, i, i, i, i]),
+        "fm_error_workspace_size": (sz, [i, i]),
+        "fm_form_operands": (i, [p, i, p, p, i, i, i, i, p, p, p, p, p, sz, p]),
+        "fm_block_products": (i, [p, p, p, p, i, i, i, i, i, p, p]),
+        "fm_reconstruct": (i, [p, i, p, i, i, p, p, sz, p]),
+        "fm_matmul_lowp": (i, [p, p, p, p, i, i, i, i, i, p, sz, p]),
+        "fm_reference_f64": (i, [p, p, p, i, i, i, p]),
+        "fm_error_stats": (i, [p, p, i, i, ct.POINTER(_Stats), p, sz, p]),
+        "fm_orbit_eval": (i, [p, i, p, p, p, i, i, i, i, i, p, p, sz, p]),
+        "fm_fp8_encode": (i, [p, i64, i, i, p, p]),
+        "fm_scheme_kernel_family": (ct.c_char_p, [p, i]),
+        "fm_status": (i, [p, sz, p]),
+        "fm_timing_enable": (i, [i]),
+        "fm_timing_reset": (i, []),
+        "fm_timing_read": (i, [ct.c_char_p, ct.POINTER(ct.c_int), ct.POINTER(ct.c_double)]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    return L
+
+
+lib = _load()
+
+
+def header_functions():
+    """Names of the functions include/fm.h declares."""
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]+?\b(fm_\w+)\s*\(", text, re.M)))
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise FmError(rc, lib.fm_last_error().decode())
+
+
+def _dptr(t):
+    return ct.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ct.c_void_p(stream.cuda_stream)
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _np_ptr(a):
+    return a.ctypes.data_as(ct.c_void_p)
+
+
+def _cuda(t, dtype):
+    if not (t.is_cuda and t.dtype == dtype and t.is_contiguous()):
+        raise ValueError(f"expected a contiguous {dtype} tensor on the GPU")
+    return t
+
+
+class Scheme:
+    """A bilinear scheme held by the library (fm_scheme*)."""
+
+    def __init__(self, handle: int):
+        self._h = ct.c_void_p(handle)
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        free = getattr(lib, "fm_scheme_free", None) if lib is not None else None
+        if h is not None and h.value and free is not None:
+            free(h)
+            self._h = None
+
+    @property
+    def handle(self):
+        return self._h
+
+    @classmethod
+    def load(cls, U, V, W, m: int, k: int, n: int) -> "Scheme":
+        U, V, W = _f64(U), _f64(V), _f64(W)
+        R = U.shape[0]
+        out = ct.c_void_p()
+        _check(lib.fm_scheme_load(_np_ptr(U), _np_ptr(V), _np_ptr(W), m, n, k, R, ct.byref(out)))
+        return cls(out.value)
+
+    @classmethod
+    def base(cls, name: str) -> "Scheme":
+        U, V, W, m, k, n = _schemes.BASE[name]()
+        return cls.load(U, V, W, m, k, n)
+
+    def gauge(self, P, Q, S) -> "Scheme":
+        P, Q, S = _f64(P), _f64(Q), _f64(S)
+        out = ct.c_void_p()
+        _check(lib.fm_gauge_apply(self._h, _np_ptr(P), _np_ptr(Q), _np_ptr(S), ct.byref(out)))
+        return Scheme(out.value)
+
+    def kron(self, levels: int) -> "Scheme":
+        out = ct.c_void_p()
+        _check(lib.fm_scheme_kron(self._h, levels, ct.byref(out)))
+        return Scheme(out.value)
+
+    @property
+    def dims(self):
+        m, n, k, R = ct.c_int(), ct.c_int(), ct.c_int(), ct.c_int()
+        _check(lib.fm_scheme_dims(self._h, ct.byref(m), ct.byref(n), ct.byref(k), ct.byref(R)))
+        return m.value, k.value, n.value, R.value  # (m, k, n, R)
+
+    def coeffs(self):
+        m, k, n, R = self.dims
+        U, V, W = np.empty((R, m * k)), np.empty((R, k * n)), np.empty((R, m * n))
+        _check(lib.fm_scheme_coeffs(self._h, _np_ptr(U), _np_ptr(V), _np_ptr(W)))
+        return U, V, W
+
+    def coeffs_f32(self, levels: int = 1):
+        m, k, n, R = self.dims
+        m, k, n, R = m ** levels, k ** levels, n ** levels, R ** levels
+        U = np.empty((R, m * k), np.float32)
+        V = np.empty((R, k * n), np.float32)
+        W = np.empty((R, m * n), np.float32)
+        _check(lib.fm_scheme_coeffs_f32(self._h, levels, _np_ptr(U), _np_ptr(V), _np_ptr(W)))
+        return U, V, W
+
+    def kernel_family(self, levels: int = 1) -> str:
+        return lib.fm_scheme_kernel_family(self._h, levels).decode()
+
+    def flat_dims(self, levels: int = 1):
+        m, k, n, R = self.dims
+        return m ** levels, k ** levels, n ** levels, R ** levels
+
+
+def workspace_size(s: Scheme, M: int, N: int, K: int, levels: int = 1, G: int = 1,
+                   chunk: int = 0) -> int:
+    return int(lib.fm_workspace_size(s.handle, M, N, K, levels, G, chunk))
+
+
+def workspace(nbytes: int, device=None):
+    """Zero-filled device workspace (torch allocations are 256-byte aligned)."""
+    return torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device=device or "cuda")
+
+
+def form_operands(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, stream=None):
+    """Quantized block sums: Tq (R, Mb, Kb) u8, Sq (R, Nb, Kb) u8 (transposed),
+    dT (R,), dS (R,) fp32."""
+    _cuda(A, torch.float32), _cuda(B, torch.float32)
+    M, K = A.shape
+    N = B.shape[1]
+    gm, gk, gn, R = s.flat_dims(levels)
+    Tq = torch.empty((R, M // gm, K // gk), dtype=torch.uint8, device=A.device)
+    Sq = torch.empty((R, N // gn, K // gk), dtype=torch.uint8, device=A.device)
+    dT = torch.empty(R, dtype=torch.float32, device=A.device)
+    dS = torch.empty(R, dtype=torch.float32, device=A.device)
+    if ws is None:
+        ws = workspace(workspace_size(s, M, N, K, levels, 1, 1), A.device)
+    _check(lib.fm_form_operands(s.handle, levels, _dptr(A), _dptr(B), M, N, K, fmt, _dptr(Tq),
+                                _dptr(Sq), _dptr(dT), _dptr(dS), _dptr(ws), ws.numel(),
+                                _stream(stream)))
+    return Tq, Sq, dT, dS
+
+
+def block_products(Tq, Sq, dT, dS, fmt: int = E4M3, out=None, stream=None):
+    _cuda(Tq, torch.uint8), _cuda(Sq, torch.uint8)
+    batch, Mb, Kb = Tq.shape
+    Nb = Sq.shape[1]
+    if out is None:
+        out = torch.empty((batch, Mb, Nb), dtype=torch.float32, device=Tq.device)
+    _check(lib.fm_block_products(_dptr(Tq), _dptr(Sq), _dptr(dT), _dptr(dS), batch, Mb, Nb, Kb,
+                                 fmt, _dptr(out), _stream(stream)))
+    return out
+
+
+def reconstruct(s: Scheme, Mprod, M: int, N: int, levels: int = 1, ws=None, stream=None):
+    _cuda(Mprod, torch.float32)
+    C = torch.empty((M, N), dtype=torch.float32, device=Mprod.device)
+    gm, gk, gn, R = s.flat_dims(levels)
+    if ws is None:
+        ws = workspace(workspace_size(s, M, N, gk * 16, levels, 1, 1), Mprod.device)
+    _check(lib.fm_reconstruct(s.handle, levels, _dptr(Mprod), M, N, _dptr(C), _dptr(ws),
+                              ws.numel(), _stream(stream)))
+    return C
+
+
+def matmul_lowp(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, out=None,
+                stream=None):
+    _cuda(A, torch.float32), _cuda(B, torch.float32)
+    M, K = A.shape
+    N = B.shape[1]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    if ws is None:
+        ws = workspace(workspace_size(s, M, N, K, levels, 1, 1), A.device)
+    _check(lib.fm_matmul_lowp(s.handle, _dptr(A), _dptr(B), _dptr(out), M, N, K, levels, fmt,
+                              _dptr(ws), ws.numel(), _stream(stream)))
+    return out
+
+
+def reference_f64(A, B, out=None, stream=None):
+    _cuda(A, torch.float32), _cuda(B, torch.float32)
+    M, K = A.shape
+    N = B.shape[1]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float64, device=A.device)
+    _check(lib.fm_reference_f64(_dptr(A), _dptr(B), _dptr(out), M, N, K, _stream(stream)))
+    return out
+
+
+def error_stats(C, Cref, ws=None, stream=None) -> dict:
+    _cuda(C, torch.float32), _cuda(Cref, torch.float64)
+    M, N = C.shape
+    if ws is None:
+        ws = workspace(lib.fm_error_workspace_size(M, N), C.device)
+    st = _Stats()
+    _check(lib.fm_error_stats(_dptr(C), _dptr(Cref), M, N, ct.byref(st), _dptr(ws), ws.numel(),
+                              _stream(stream)))
+    return dict(rel_fro=st.rel_fro, err_sq=st.err_sq, ref_sq=st.ref_sq, max_abs=st.max_abs)
+
+
+def orbit_eval(gauged, A, B, Cref, levels: int = 1, fmt: int = E4M3, ws=None, chunk: int = 0,
+               stream=None) -> np.ndarray:
+    """Relative Frobenius errors of the FP8 schedule for every gauged scheme."""
+    _cuda(A, torch.float32), _cuda(B, torch.float32), _cuda(Cref, torch.float64)
+    M, K = A.shape
+    N = B.shape[1]
+    G = len(gauged)
+    handles = (ct.c_void_p * G)(*[g.handle.value for g in gauged])
+    if ws is None:
+        ws = workspace(workspace_size(gauged[0], M, N, K, levels, G, chunk), A.device)
+    out = np.empty(G, np.float64)
+    _check(lib.fm_orbit_eval(ct.cast(handles, ct.c_void_p), G, _dptr(A), _dptr(B), _dptr(Cref), M,
+                             N, K, levels, fmt, _np_ptr(out), _dptr(ws), ws.numel(),
+                             _stream(stream)))
+    return out
+
+
+def fp8_encode(x, fmt: int = E4M3, impl: int = 0, stream=None):
+    _cuda(x, torch.float32)
+    out = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    _check(lib.fm_fp8_encode(_dptr(x), x.numel(), fmt, impl, _dptr(out), _stream(stream)))
+    return out
+
+
+def status(ws, stream=None):
+    _check(lib.fm_status(_dptr(ws), ws.numel(), _stream(stream)))
+
+
+def timing_enable(on: bool = True):
+    _check(lib.fm_timing_enable(1 if on else 0))
+
+
+def timing_reset():
+    _check(lib.fm_timing_reset())
+
+
+def timing_read(kernel_class: str):
+    """(launches, total milliseconds) of one kernel class since the last reset."""
+    n, ms = ct.c_int(), ct.c_double()
+    _check(lib.fm_timing_read(kernel_class.encode(), ct.byref(n), ct.byref(ms)))
+    return n.value, ms.value
+
+
+TIMED_CLASSES = ("form_amax", "form_quant", "block_gemm", "recon", "reference")
+
+
+def version() -> str:
+    return lib.fm_version().decode()

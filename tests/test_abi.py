@@ -1,0 +1,184 @@
+"""The C-ABI library on the CPU: it loads, exports every function include/fm.h
+declares, and its host-side scheme code agrees with the oracle bit for bit
+(no GPU call is made here).  Host-side error paths are exercised too."""
+import ctypes as ct
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import scheme_ops as so
+from oracle import schemes as osch
+import synthetic as sy
+
+torch = pytest.importorskip("torch")
+fm = pytest.importorskip("paper_2609_39816_amd.fm")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_header_function():
+    names = fm.header_functions()
+    assert len(names) >= 20
+    out = subprocess.run(["nm", "-D", "--defined-only", fm.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (fm_\w+)", out))
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    for n in names:
+        assert hasattr(fm.lib, n)
+
+
+def test_header_documents_every_entry_point():
+    text = open(os.path.join(ROOT, "include", "fm.h")).read()
+    for n in fm.header_functions():
+        # a comment block precedes each declaration
+        m = re.search(r"^(?:const\s+)?[\w ]+\*?\s*" + n + r"\(", text, re.M)
+        assert m, n
+        i = m.start()
+        assert "*/" in text[max(0, i - 900):i], n
+
+
+def _hip_scheme(name, levels=1, gauge=None, gauge_after_kron=True):
+    s = fm.Scheme.base(name)
+    if gauge is not None and not gauge_after_kron:
+        s = s.gauge(*gauge)
+    if levels > 1:
+        s = s.kron(levels)
+    if gauge is not None and gauge_after_kron:
+        s = s.gauge(*gauge)
+    return s
+
+
+def _orc_scheme(name, levels=1, gauge=None, gauge_after_kron=True):
+    s = osch.BASE_SCHEMES[name]()
+    if gauge is not None and not gauge_after_kron:
+        s = so.gauge(s, *gauge)
+    if levels > 1:
+        s = so.power(s, levels)
+    if gauge is not None and gauge_after_kron:
+        s = so.gauge(s, *gauge)
+    return s
+
+
+@pytest.mark.parametrize("name,levels", [("strassen", 1), ("strassen", 2), ("strassen", 3),
+                                         ("laderman", 1)])
+def test_flattened_tables_match_oracle(name, levels):
+    h = _hip_scheme(name, levels)
+    o = _orc_scheme(name, levels)
+    for a, b in zip(h.coeffs(), (o.U, o.V, o.W)):
+        assert np.array_equal(a, b)
+    # coefficient tables at levels=L on the base equal levels=1 on the power
+    base = fm.Scheme.base(name)
+    for a, b in zip(base.coeffs_f32(levels), oracle.flatten_f32(o)[0]):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+@pytest.mark.parametrize("name", ["strassen", "laderman"])
+def test_gl_gauge_tables_bit_identical_to_oracle(name):
+    m = {"strassen": 2, "laderman": 3}[name]
+    for P, Q, S in sy.gl_gauges(m, m, m, 64, seed=123):
+        h = _hip_scheme(name, 1, (P, Q, S))
+        o = _orc_scheme(name, 1, (P, Q, S))
+        for a, b in zip(h.coeffs(), (o.U, o.V, o.W)):
+            assert np.array_equal(a.view(np.uint64), b.view(np.uint64))
+        for a, b in zip(h.coeffs_f32(1), oracle.flatten_f32(o)[0]):
+            assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_sign_orbit_tables_bit_identical_to_oracle():
+    orbit = sy.sign_orbit(4, 4, 4)
+    for d, e, f in orbit[::29]:
+        g = (np.diag(d), np.diag(e), np.diag(f))
+        h = _hip_scheme("strassen", 2, g)
+        o = _orc_scheme("strassen", 2, g)
+        for a, b in zip(h.coeffs(), (o.U, o.V, o.W)):
+            assert np.array_equal(a, b)
+        assert h.kernel_family(1) == "Strassen2"
+
+
+def test_gauge_then_levels_matches_oracle_power_of_gauged():
+    P, Q, S = sy.gl_gauges(2, 2, 2, 1, seed=9)[0]
+    h = _hip_scheme("strassen", 1, (P, Q, S))
+    o = so.power(so.gauge(osch.strassen(), P, Q, S), 2)
+    for a, b in zip(h.coeffs_f32(2), oracle.flatten_f32(o)[0]):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_kernel_families():
+    assert fm.Scheme.base("strassen").kernel_family(1) == "Strassen1"
+    assert fm.Scheme.base("strassen").kernel_family(2) == "Strassen2"
+    assert fm.Scheme.base("strassen").kernel_family(3) == "Strassen3"
+    assert fm.Scheme.base("laderman").kernel_family(1) == "Laderman1"
+    assert fm.Scheme.base("classical").kernel_family(1) == "Classical1"
+    P, Q, S = sy.gl_gauges(2, 2, 2, 1, seed=1)[0]
+    assert fm.Scheme.base("strassen").gauge(P, Q, S).kernel_family(1) == "DenseR7G2"
+    P, Q, S = sy.gl_gauges(3, 3, 3, 1, seed=1)[0]
+    assert fm.Scheme.base("laderman").gauge(P, Q, S).kernel_family(1) == "DenseR23G3"
+    U, V, W, m, k, n = fm._schemes.classical(2, 2, 2)
+    assert fm.Scheme.load(U, V, W, m, k, n).kernel_family(1) == "generic"
+
+
+def test_brent_rejection_and_singular_gauge():
+    U, V, W, m, k, n = fm._schemes.strassen()
+    W = W.copy()
+    W[0, 0] = -W[0, 0]
+    with pytest.raises(fm.FmError) as e:
+        fm.Scheme.load(U, V, W, m, k, n)
+    assert e.value.name == "FM_E_BRENT"
+    s = fm.Scheme.base("strassen")
+    with pytest.raises(fm.FmError) as e:
+        s.gauge(np.array([[1.0, 2.0], [2.0, 4.0]]), np.eye(2), np.eye(2))
+    assert e.value.name == "FM_E_SINGULAR"
+    with pytest.raises(fm.FmError) as e:
+        s.kron(0)
+    assert e.value.name == "FM_E_ARG"
+
+
+def test_workspace_size_and_shape_checks():
+    s2 = fm.Scheme.base("strassen").kron(2)
+    assert fm.workspace_size(s2, 2048, 4096, 4096, 1, 512, 16) > 0
+    assert fm.workspace_size(s2, 2048, 4096, 4094, 1, 1, 1) == 0   # K not divisible by 4
+    assert fm.workspace_size(s2, 2048, 4096, 4 * 24, 1, 1, 1) == 0  # Kb = 24, not a multiple of 16
+    one = fm.workspace_size(s2, 2048, 4096, 4096, 1, 512, 1)
+    many = fm.workspace_size(s2, 2048, 4096, 4096, 1, 512, 16)
+    assert many > one
+
+
+# The next two tests pass placeholder device pointers that the argument checks
+# must reject before any device work; they run only where no GPU is visible,
+# so a placeholder can never reach a kernel.
+no_gpu = pytest.mark.skipif(torch.cuda.is_available(), reason="host-only check, run without a GPU")
+
+
+@no_gpu
+def test_host_side_errors_before_any_device_work():
+    """Argument errors are reported from the host, before a kernel launch."""
+    s = fm.Scheme.base("strassen")
+    p = ct.c_void_p(256)  # never dereferenced: the checks fail first
+    rc = fm.lib.fm_matmul_lowp(s.handle, p, p, p, 131, 128, 128, 1, 0, p, 1 << 30, None)
+    assert rc == -2 and "multiples" in fm.lib.fm_last_error().decode()
+    rc = fm.lib.fm_matmul_lowp(s.handle, p, p, p, 128, 128, 128, 1, 7, p, 1 << 30, None)
+    assert rc == -1
+    rc = fm.lib.fm_matmul_lowp(s.handle, p, p, p, 128, 128, 128, 1, 0, None, 1 << 30, None)
+    assert rc == -6
+    rc = fm.lib.fm_matmul_lowp(s.handle, p, p, p, 128, 128, 128, 1, 0, ct.c_void_p(512), 16, None)
+    assert rc == -6 and "too small" in fm.lib.fm_last_error().decode()
+    rc = fm.lib.fm_matmul_lowp(s.handle, p, p, p, 128, 128, 128, 1, 0, ct.c_void_p(100), 1 << 30, None)
+    assert rc == -6 and "aligned" in fm.lib.fm_last_error().decode()
+    assert fm.lib.fm_strerror(-5).decode().startswith("non-finite")
+
+
+@no_gpu
+def test_mismatched_orbit_is_rejected():
+    s1 = fm.Scheme.base("strassen")
+    s2 = fm.Scheme.base("strassen").kron(2)
+    handles = (ct.c_void_p * 2)(s1.handle.value, s2.handle.value)
+    p = ct.c_void_p(256)
+    out = np.empty(2)
+    rc = fm.lib.fm_orbit_eval(ct.cast(handles, ct.c_void_p), 2, p, p, p, 256, 256, 256, 1, 0,
+                              out.ctypes.data_as(ct.c_void_p), p, 1 << 40, None)
+    assert rc == -8

@@ -1,0 +1,298 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on
+the same seeded inputs.
+
+Bars (written into each check):
+  * FP8 operand codes and scales: bit-exact.
+  * Block products: relative Frobenius <= 1e-5 per product (the oracle's are
+    the exact sums rounded once; the matrix cores accumulate in fp32).
+  * Output C: relative Frobenius <= 1e-5 against the oracle's C.
+  * Orbit errors: within 1% relative of the oracle's.
+  * float64 reference: relative <= 1e-12.
+Shapes cover several tiles and ragged tails (block sizes not multiples of
+the 128 x 128 x 128 GEMM tile), every kernel family and the generic kernels.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import scheme_ops as so
+from oracle import schemes as osch
+import synthetic as sy
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU-only machines, never run
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2609_39816_amd import fm  # noqa: E402
+
+DEV = torch.device("cuda:0")
+FMT = {"e4m3": fm.E4M3, "e5m2": fm.E5M2}
+OFMT = {"e4m3": oracle.E4M3, "e5m2": oracle.E5M2}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    nb = np.linalg.norm(b)
+    return np.linalg.norm(a - b) / (nb if nb > 0 else 1.0)
+
+
+def gpu(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+class OracleSchemes:
+    """Oracle-side gauged schemes, built on first use (pure-Python float64)."""
+
+    def __init__(self, w, gauges):
+        self.w, self.gauges, self.cache = w, gauges, {}
+        self.base = osch.BASE_SCHEMES[w.scheme]()
+        self.flat = so.power(self.base, w.levels) if w.gauge_kind == "sign" else None
+
+    def __getitem__(self, i):
+        if i not in self.cache:
+            P, Q, S = self.gauges[i]
+            if self.w.gauge_kind == "sign":
+                self.cache[i] = so.gauge(self.flat, P, Q, S)
+            else:
+                self.cache[i] = so.power(so.gauge(self.base, P, Q, S), self.w.levels)
+        return self.cache[i]
+
+
+def schemes_for(w, gauges):
+    """(hip schemes, oracle schemes, levels passed to the library)."""
+    base_h = fm.Scheme.base(w.scheme)
+    if w.gauge_kind == "sign":
+        flat_h = base_h.kron(w.levels) if w.levels > 1 else base_h
+        hips = [flat_h.gauge(P, Q, S) for P, Q, S in gauges]
+        return hips, OracleSchemes(w, gauges), 1
+    hips = [base_h.gauge(P, Q, S) for P, Q, S in gauges]
+    return hips, OracleSchemes(w, gauges), w.levels
+
+
+def check_operands(h, o, levels, A, B, At, Bt, fmt):
+    Tq, Sq, dT, dS = fm.form_operands(h, At, Bt, levels, FMT[fmt])
+    tabs, dims = oracle.flatten_f32(o)
+    U, V, W = tabs
+    gm, gk, gn, R = dims
+    tq, dt = oracle.form_operands(A, gm, gk, U, OFMT[fmt])
+    sq, ds = oracle.form_operands(B, gk, gn, V, OFMT[fmt])
+    assert np.array_equal(Tq.cpu().numpy(), tq), "Tq not bit-exact"
+    assert np.array_equal(Sq.cpu().numpy(), sq.transpose(0, 2, 1)), "Sq not bit-exact"
+    assert np.array_equal(dT.cpu().numpy().view(np.uint32), dt.view(np.uint32)), "dT not bit-exact"
+    assert np.array_equal(dS.cpu().numpy().view(np.uint32), ds.view(np.uint32)), "dS not bit-exact"
+    return Tq, Sq, dT, dS, tq, sq, dt, ds
+
+
+def run_workload(w, n_oracle, fmt="e4m3", check_products=2):
+    say(f"[parity] {w.name} fmt={fmt} G={w.G}")
+    A, B = sy.operands(w)
+    At, Bt = gpu(A), gpu(B)
+    gauges = [sy.identity_gauge(w)] + sy.gauges(w)
+    hips, orcs, levels = schemes_for(w, gauges)
+    Cref_o = oracle.reference_f64(A, B)
+    Cref = fm.reference_f64(At, Bt)
+    assert rel(Cref.cpu().numpy(), Cref_o) <= 1e-12
+    # classical baseline
+    cl_h = fm.Scheme.base("classical")
+    C_cl = fm.matmul_lowp(cl_h, At, Bt, 1, FMT[fmt])
+    C_cl_o = oracle.lowp_matmul(A, B, *oracle.flatten_f32(osch.classical()), OFMT[fmt])
+    assert rel(C_cl.cpu().numpy(), C_cl_o) <= 1e-5
+    st = fm.error_stats(C_cl, Cref)
+    e_o, r_o = oracle.error_sums(C_cl_o, Cref_o)
+    err_cl_o = np.sqrt(e_o) / np.sqrt(r_o)
+    assert abs(st["rel_fro"] / err_cl_o - 1) <= 1e-2
+    assert abs(st["ref_sq"] / r_o - 1) <= 1e-12
+    # orbit on the GPU, all gauges
+    errs = fm.orbit_eval(hips, At, Bt, Cref, levels, FMT[fmt])
+    assert np.all(np.isfinite(errs))
+    picks = sorted(set([0, 1, len(hips) - 1] + list(range(0, len(hips), max(1, len(hips) // n_oracle)))))[:n_oracle]
+    for gi in picks:
+        h, o = hips[gi], orcs[gi]
+        Tq, Sq, dT, dS, tq, sq, dt, ds = check_operands(h, o, levels, A, B, At, Bt, fmt)
+        Mg = fm.block_products(Tq, Sq, dT, dS, FMT[fmt])
+        for r in range(min(check_products, tq.shape[0])):
+            Mo = oracle.block_product(tq[r], sq[r], dt[r], ds[r], OFMT[fmt])
+            assert rel(Mg[r].cpu().numpy(), Mo) <= 1e-5, f"block product {r}"
+        tabs, dims = oracle.flatten_f32(o)
+        Co = oracle.lowp_matmul(A, B, tabs, dims, OFMT[fmt])
+        Cg = fm.matmul_lowp(h, At, Bt, levels, FMT[fmt]).cpu().numpy()
+        assert rel(Cg, Co) <= 1e-5, f"gauge {gi}: C rel {rel(Cg, Co):.3e}"
+        Cr = fm.reconstruct(h, Mg, w.M, w.N, levels).cpu().numpy()
+        assert rel(Cr, Co) <= 1e-5
+        e_want = oracle.rel_fro(Co, Cref_o)
+        assert abs(errs[gi] / e_want - 1) <= 1e-2, f"gauge {gi}: {errs[gi]} vs {e_want}"
+    return errs / st["rel_fro"]
+
+
+# ----------------------------------------------------------------- codec
+def structured_values(limit):
+    hi = np.arange(1 << 16, dtype=np.uint32) << 16
+    lows = np.array([0, 1, 0x7FFF, 0x8000, 0x8001, 0xFFFF], dtype=np.uint32)
+    x = (hi[:, None] | lows[None, :]).reshape(-1).view(np.float32)
+    return x[np.isfinite(x) & (np.abs(x) <= limit)]
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+def test_fp8_encoder_bit_exact(fmt):
+    """The kernels' encoder equals the oracle's on every fp32 high half with
+    low halves on, above and below each rounding tie, up to the largest value
+    the schedule can produce, FMAX (1 + 2^-23)^2."""
+    fmax = 448.0 if fmt == "e4m3" else 57344.0
+    x = structured_values(fmax * (1 + 2.0 ** -21))
+    want = oracle.fp8_encode(x, OFMT[fmt])
+    xg = gpu(x)
+    for impl in (0, 2):
+        got = fm.fp8_encode(xg, FMT[fmt], impl).cpu().numpy()
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, (impl, x[bad[:8]], got[bad[:8]], want[bad[:8]])
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+def test_fp8_hardware_conversion_report(fmt):
+    """Reports whether the gfx950 conversion instructions round like the
+    oracle over the reachable range (they are used only if they do)."""
+    fmax = 448.0 if fmt == "e4m3" else 57344.0
+    x = structured_values(fmax * (1 + 2.0 ** -21))
+    want = oracle.fp8_encode(x, OFMT[fmt])
+    got = fm.fp8_encode(gpu(x), FMT[fmt], 1).cpu().numpy()
+    bad = np.nonzero(got != want)[0]
+    say(f"[codec] hardware {fmt}: {bad.size} of {x.size} differ; first: "
+        f"{[(float(x[i]), int(got[i]), int(want[i])) for i in bad[:6]]}")
+
+
+# ------------------------------------------------------------ workloads
+def test_strassen1_gl64_full_workload():
+    w = sy.WORKLOADS["strassen1_256_gl64"]
+    ratios = run_workload(w, n_oracle=65)
+    st = oracle.orbit_stats(ratios[1:], identity_value=ratios[0])
+    say(f"[parity] {w.name} ratio stats {st}")
+    assert st["max"] > st["min"] > 0
+
+
+def test_strassen2_sign_orbit_scaled():
+    w = sy.scaled(sy.WORKLOADS["strassen2_2048x4096x4096_sign512"], 256, 512, 512, G=512)
+    ratios = run_workload(w, n_oracle=6)
+    assert ratios.shape == (513,)
+
+
+def test_laderman_gl_scaled_ragged_both_formats():
+    # block sizes 48 x 64 x 80: every GEMM tile is ragged, K is shorter than one step
+    w = sy.scaled(sy.WORKLOADS["laderman1_3072x4608x12288_gl512"], 144, 192, 240, G=8)
+    for fmt in ("e4m3", "e5m2"):
+        run_workload(w, n_oracle=3, fmt=fmt)
+
+
+def test_strassen2_student_t_scaled():
+    w = sy.scaled(sy.WORKLOADS["strassen2_4096x4096x14336_sign512"], 512, 256, 896, G=16)
+    run_workload(w, n_oracle=3)
+
+
+def test_strassen3_sampled_signs_scaled():
+    w = sy.scaled(sy.WORKLOADS["strassen3_8192x27648x5120_sign512"], 256, 512, 384, G=8)
+    run_workload(w, n_oracle=3, check_products=3)
+
+
+def test_generic_kernels_dense_gauge_on_flat_grid():
+    """A GL(4) gauge on two-level Strassen's 4 x 4 grid matches no compiled
+    structure: the generic formation and reconstruction kernels run."""
+    say("[parity] generic kernels")
+    w = sy.scaled(sy.WORKLOADS["strassen2_2048x4096x4096_sign512"], 128, 256, 192, G=1)
+    A, B = sy.operands(w)
+    At, Bt = gpu(A), gpu(B)
+    P, Q, S = sy.gl_gauges(4, 4, 4, 1, seed=77)[0]
+    h = fm.Scheme.base("strassen").kron(2).gauge(P, Q, S)
+    assert h.kernel_family(1) == "generic"
+    o = so.gauge(so.power(osch.strassen(), 2), P, Q, S)
+    check_operands(h, o, 1, A, B, At, Bt, "e4m3")
+    Co = oracle.lowp_matmul(A, B, *oracle.flatten_f32(o))
+    Cg = fm.matmul_lowp(h, At, Bt).cpu().numpy()
+    assert rel(Cg, Co) <= 1e-5
+    U, V, W, m, k, n = fm._schemes.classical(2, 2, 2)
+    hc = fm.Scheme.load(U, V, W, m, k, n)
+    assert hc.kernel_family(1) == "generic"
+    oc = osch.classical(2, 2, 2)
+    check_operands(hc, oc, 1, A, B, At, Bt, "e5m2")
+    Co = oracle.lowp_matmul(A, B, *oracle.flatten_f32(oc))
+    assert rel(fm.matmul_lowp(hc, At, Bt).cpu().numpy(), Co) <= 1e-5
+
+
+# ---------------------------------------------------------- edge cases
+def test_zero_operand_and_single_tile():
+    say("[parity] zero operand")
+    A = np.zeros((64, 64), np.float32)
+    B = np.random.default_rng(1).standard_normal((64, 64)).astype(np.float32)
+    h = fm.Scheme.base("strassen")
+    Tq, Sq, dT, dS = fm.form_operands(h, gpu(A), gpu(B))
+    assert not Tq.cpu().numpy().any() and np.all(dT.cpu().numpy() == 1.0)
+    C = fm.matmul_lowp(h, gpu(A), gpu(B)).cpu().numpy()
+    assert not C.any()
+    Cref = fm.reference_f64(gpu(A), gpu(B))
+    errs = fm.orbit_eval([h], gpu(A), gpu(B), Cref)
+    assert errs[0] == 0.0
+
+
+def test_nonfinite_input_is_reported():
+    say("[parity] non-finite input")
+    rng = np.random.default_rng(2)
+    A = rng.standard_normal((64, 64)).astype(np.float32)
+    B = rng.standard_normal((64, 64)).astype(np.float32)
+    A[5, 7] = np.inf
+    h = fm.Scheme.base("strassen")
+    Cref = fm.reference_f64(gpu(A), gpu(B))
+    with pytest.raises(fm.FmError) as e:
+        fm.orbit_eval([h], gpu(A), gpu(B), Cref)
+    assert e.value.name == "FM_E_NONFINITE"
+    ws = fm.workspace(fm.workspace_size(h, 64, 64, 64))
+    fm.matmul_lowp(h, gpu(A), gpu(B), ws=ws)
+    with pytest.raises(fm.FmError):
+        fm.status(ws)
+    fm.status(ws)  # cleared
+
+
+def test_chunked_orbit_equals_single_launch_and_is_deterministic():
+    say("[parity] chunking and determinism")
+    w = sy.scaled(sy.WORKLOADS["strassen2_2048x4096x4096_sign512"], 256, 256, 256, G=24)
+    A, B = sy.operands(w)
+    At, Bt = gpu(A), gpu(B)
+    hips, _, levels = schemes_for(w, sy.gauges(w))
+    Cref = fm.reference_f64(At, Bt)
+    e1 = fm.orbit_eval(hips, At, Bt, Cref, levels)
+    e2 = fm.orbit_eval(hips, At, Bt, Cref, levels)
+    ws = fm.workspace(fm.workspace_size(hips[0], w.M, w.N, w.K, levels, len(hips), 5))
+    e3 = fm.orbit_eval(hips, At, Bt, Cref, levels, ws=ws)
+    assert np.array_equal(e1.view(np.uint64), e2.view(np.uint64))
+    assert np.array_equal(e1.view(np.uint64), e3.view(np.uint64))
+    c1 = fm.matmul_lowp(hips[3], At, Bt, levels).cpu().numpy()
+    c2 = fm.matmul_lowp(hips[3], At, Bt, levels).cpu().numpy()
+    assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
+
+
+def test_full_size_headline_workload_sampled():
+    """Two-level Strassen at 2048 x 4096 x 4096, all 512 sign variants in the
+    launch configuration the benchmark times; the oracle checks the identity
+    variant's operands bit for bit and three variants' errors in full."""
+    w = sy.WORKLOADS["strassen2_2048x4096x4096_sign512"]
+    say(f"[parity] {w.name} full size")
+    A, B = sy.operands(w)
+    At, Bt = gpu(A), gpu(B)
+    gauges = sy.gauges(w)
+    hips, orcs, levels = schemes_for(w, gauges)
+    Cref = fm.reference_f64(At, Bt)
+    errs = fm.orbit_eval(hips, At, Bt, Cref, levels)
+    check_operands(hips[0], orcs[0], levels, A, B, At, Bt, "e4m3")
+    Cref_o = oracle.reference_f64(A, B)
+    for gi in (0, 137, 511):
+        Co = oracle.lowp_matmul(A, B, *oracle.flatten_f32(orcs[gi]))
+        e_want = oracle.rel_fro(Co, Cref_o)
+        say(f"[parity] gauge {gi}: gpu {errs[gi]:.6e} oracle {e_want:.6e}")
+        assert abs(errs[gi] / e_want - 1) <= 1e-2
