@@ -65,6 +65,9 @@ typedef struct fm_scheme fm_scheme; /* opaque, immutable, library-owned     */
 
 typedef enum { FM_E4M3 = 0, FM_E5M2 = 1 } fm_fmt; /* OCP E4M3FN, OCP E5M2  */
 
+/* Arithmetic of the block products (fm_set_block_product_arithmetic). */
+typedef enum { FM_ACC_BF16 = 0, FM_ACC_FP8 = 1 } fm_accum;
+
 typedef struct {
   double rel_fro; /* ||C - C_ref||_F / ||C_ref||_F (0 if C_ref = 0)         */
   double err_sq;  /* sum (C - C_ref)^2, float64                             */
@@ -167,7 +170,10 @@ int fm_form_operands(const fm_scheme* s, int levels, const float* A,
 
 /* Block products (step M_r of eq. (1) on FP8 operands), batched.  Async.
  * For b in [0, batch): Mout[b] = ((Tq[b] * Sq[b]^T accumulated in fp32 by
- * the matrix cores) * dT[b]) * dS[b], two fp32 multiplications.
+ * the matrix cores) * dT[b]) * dS[b], two fp32 multiplications.  The
+ * products are exact and summed in fp32 (FM_ACC_BF16, the default), or
+ * formed by the FP8 matrix instructions (FM_ACC_FP8); see
+ * fm_set_block_product_arithmetic.
  * Tq: batch x Mb x Kb, Sq: batch x Nb x Kb (inner dimension contiguous),
  * dT, dS: batch floats, Mout: batch x Mb x Nb fp32.  Mb, Nb, Kb >= 1; Kb a
  * multiple of 16. */
@@ -211,6 +217,17 @@ int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A,
                   const float* B, const double* C_ref, int M, int N, int K,
                   int levels, fm_fmt fmt, double* rel_fro_out,
                   void* workspace, size_t ws_bytes, void* hip_stream);
+
+/* Selects, process-wide, how the block products are multiplied (the App. B
+ * schedule multiplies FP8 block sums and combines the products in fp32):
+ *   FM_ACC_BF16 (default): every FP8 value is widened exactly to bf16 and
+ *     multiplied on the bf16 matrix cores with fp32 accumulation (within
+ *     about 2e-7 of the exact sums rounded once);
+ *   FM_ACC_FP8: the gfx950 FP8 matrix instructions, at twice the rate, which
+ *     truncate small products summed beside large ones (about 5e-5 relative
+ *     on random FP8 data).
+ * FM_E_ARG for any other value. */
+int fm_set_block_product_arithmetic(fm_accum a);
 
 /* ------------------------------------------------------------ diagnostics */
 

@@ -756,6 +756,11 @@ int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A, const f
   return FM_OK;
 }
 
+int fm_set_block_product_arithmetic(fm_accum a) {
+  clear_error();
+  return set_block_product_arith((int)a);
+}
+
 int fm_fp8_encode(const float* x, int64_t n, fm_fmt fmt, int impl, uint8_t* out,
                   void* hip_stream) {
   clear_error();

@@ -15,7 +15,7 @@
 #include "fm_patterns.inc"
 
 #ifndef FM_FP8_HW
-#define FM_FP8_HW 0  // 1: v_cvt_pk_{fp8,bf8}_f32 for FP8 rounding; 0: integer encoder
+#define FM_FP8_HW 1  // 1: v_cvt_pk_{fp8,bf8}_f32 for FP8 rounding; 0: integer encoder
 #endif
 
 namespace fm {

@@ -106,6 +106,9 @@ int launch_form(const FormArgs& a, int mode, int pattern, int side, hipStream_t 
 int launch_scales(const uint32_t* amax, float* q, float* d, int n, int fmt, uint32_t* flag,
                   hipStream_t st);
 
+// Process-wide arithmetic of the block products (FM_ACC_BF16 / FM_ACC_FP8).
+int set_block_product_arith(int a);
+
 // Batched FP8 block products: Mout[b] = ((Tq[b] Sq[b]^T) * dT[b]) * dS[b].
 int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
                       float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, hipStream_t st);

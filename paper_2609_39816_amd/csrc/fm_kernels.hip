@@ -88,20 +88,49 @@ __global__ void scales_kernel(const uint32_t* amax, float* q, float* d, int n, f
 }
 
 // ------------------------------------------------------ FP8 block GEMM
-// Workgroup tile 128 x 128, K step 128 (one MFMA deep), 4 waves in 2 x 2,
-// each wave 64 x 64 = 4 x 4 MFMA 16x16x128 tiles.  Operands are staged
-// through double-buffered LDS, rows of 128 bytes with the 16-byte chunk
-// index XOR-swizzled by a function of the row so that the fragment reads
-// (16 rows x one chunk per instruction) hit distinct banks.
+// Workgroup tile 128 x 128, K step 128 bytes, 4 waves in 2 x 2, each wave
+// 64 x 64 = 4 x 4 tiles of 16 x 16.  FP8 operands are staged through
+// double-buffered LDS, rows of 128 bytes with the 16-byte chunk index
+// XOR-swizzled by a function of the row so that the fragment reads (16 rows
+// x one chunk per instruction) hit distinct banks.
+//
+// Lane (i, q) = (lane % 16, lane / 16) of a wave holds the 32 bytes
+// [32q, 32q + 32) of row i of a 16-row fragment, for both operands, so every
+// k of the step is paired with the same k of the other operand.
+//
+// Two arithmetics for the products:
+//   ACC_BF16 (default): every FP8 value is widened exactly to bf16
+//     (v_cvt_scalef32_pk_bf16_{fp8,bf8}, scale 1) and multiplied on the bf16
+//     matrix cores, v_mfma_f32_16x16x32_bf16: exact products, fp32 sums.
+//   ACC_FP8: v_mfma_scale_f32_16x16x128_f8f6f4 with unit scales, twice the
+//     rate; its sums of small products beside large ones are truncated
+//     (about 5e-5 relative on random FP8 data), so it is not the default.
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
 
 constexpr int GT = 128;  // tile rows / cols
 constexpr int GK = 128;  // K step in bytes
 
 __device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
+// Two FP8 codes (bytes 0-1 or 2-3 of w) -> two bf16 values, exactly.
+template <int FMT, bool HI>
+__device__ __forceinline__ v2bf widen2(int w) {
+  if constexpr (FMT == FM_E4M3) return __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI);
+  else return __builtin_amdgcn_cvt_scalef32_pk_bf16_bf8(w, 1.0f, HI);
+}
+
+// 8 FP8 codes (two dwords, little-endian byte order) -> 8 bf16 values
 template <int FMT>
+__device__ __forceinline__ v8bf widen8(int d0, int d1) {
+  const v2bf a = widen2<FMT, false>(d0), b = widen2<FMT, true>(d0);
+  const v2bf c = widen2<FMT, false>(d1), d = widen2<FMT, true>(d1);
+  return (v8bf){a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
+}
+
+template <int FMT, int ACC>
 __global__ __launch_bounds__(kThreads) void gemm_fp8_kernel(const uint8_t* __restrict__ Tq,
                                                             const uint8_t* __restrict__ Sq,
                                                             const float* __restrict__ dT,
@@ -184,12 +213,28 @@ __global__ __launch_bounds__(kThreads) void gemm_fp8_kernel(const uint8_t* __res
       const uint4 hi = *reinterpret_cast<const uint4*>(base + (((2 * q + 1) ^ swz(row)) << 4));
       fb[j] = (v8i){(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
     }
+    if constexpr (ACC == 1) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(fa[i], fb[j], acc[i][j], FMT,
-                                                                     FMT, 0, 127, 0, 127);
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(fa[i], fb[j], acc[i][j], FMT,
+                                                                       FMT, 0, 127, 0, 127);
+    } else {
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub) {
+        v8bf wa[4], wb[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) wa[i] = widen8<FMT>(fa[i][2 * sub], fa[i][2 * sub + 1]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) wb[j] = widen8<FMT>(fb[j][2 * sub], fb[j][2 * sub + 1]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[i], wb[j], acc[i][j], 0, 0, 0);
+      }
+    }
     if (kt + 1 < nk) lstore(cur ^ 1);
     __syncthreads();
   }
@@ -354,17 +399,34 @@ int launch_scales(const uint32_t* amax, float* q, float* d, int n, int fmt, uint
   return launched("scales_kernel");
 }
 
+namespace {
+int g_block_product_arith = FM_ACC_BF16;
+}
+
+int set_block_product_arith(int a) {
+  if (a != FM_ACC_BF16 && a != FM_ACC_FP8) return fail(FM_E_ARG, "unknown product arithmetic");
+  g_block_product_arith = a;
+  return FM_OK;
+}
+
 int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
                       float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, hipStream_t st) {
   const int tm = (Mb + GT - 1) / GT, tn = (Nb + GT - 1) / GT;
   const long long total = (long long)batch * tm * tn;
   if (total > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many GEMM tiles in one launch");
-  if (fmt == FM_E4M3)
-    gemm_fp8_kernel<0><<<(int)total, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn,
-                                                        (int)total);
-  else
-    gemm_fp8_kernel<1><<<(int)total, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn,
-                                                        (int)total);
+  const int T = (int)total;
+  const bool fp8acc = g_block_product_arith == FM_ACC_FP8;
+  if (fmt == FM_E4M3) {
+    if (fp8acc)
+      gemm_fp8_kernel<FM_E4M3, 1><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+    else
+      gemm_fp8_kernel<FM_E4M3, 0><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+  } else {
+    if (fp8acc)
+      gemm_fp8_kernel<FM_E5M2, 1><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+    else
+      gemm_fp8_kernel<FM_E5M2, 0><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+  }
   return launched("gemm_fp8_kernel");
 }
 

@@ -24,6 +24,7 @@ LIB_PATH = os.path.join(HERE, "libfm.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "fm.h")
 
 E4M3, E5M2 = 0, 1
+ACC_BF16, ACC_FP8 = 0, 1
 FMTS = {"e4m3": E4M3, "e5m2": E5M2}
 ERRORS = {0: "FM_OK", -1: "FM_E_ARG", -2: "FM_E_SHAPE", -3: "FM_E_BRENT", -4: "FM_E_SINGULAR",
           -5: "FM_E_NONFINITE", -6: "FM_E_WORKSPACE", -7: "FM_E_HIP", -8: "FM_E_MISMATCH",
@@ -72,6 +73,7 @@ def _load():
         "fm_fp8_encode": (i, [p, i64, i, i, p, p]),
         "fm_scheme_kernel_family": (ct.c_char_p, [p, i]),
         "fm_status": (i, [p, sz, p]),
+        "fm_set_block_product_arithmetic": (i, [i]),
         "fm_timing_enable": (i, [i]),
         "fm_timing_reset": (i, []),
         "fm_timing_read": (i, [ct.c_char_p, ct.POINTER(ct.c_int), ct.POINTER(ct.c_double)]),
@@ -303,6 +305,12 @@ def fp8_encode(x, fmt: int = E4M3, impl: int = 0, stream=None):
 
 def status(ws, stream=None):
     _check(lib.fm_status(_dptr(ws), ws.numel(), _stream(stream)))
+
+
+def set_block_product_arithmetic(acc: int):
+    """ACC_BF16 (exact products, fp32 sums; default) or ACC_FP8 (FP8 matrix
+    instructions)."""
+    _check(lib.fm_set_block_product_arithmetic(acc))
 
 
 def timing_enable(on: bool = True):

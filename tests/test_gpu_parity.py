@@ -202,14 +202,18 @@ def test_strassen3_sampled_signs_scaled():
     run_workload(w, n_oracle=3, check_products=3)
 
 
-def test_generic_kernels_dense_gauge_on_flat_grid():
-    """A GL(4) gauge on two-level Strassen's 4 x 4 grid matches no compiled
-    structure: the generic formation and reconstruction kernels run."""
+def test_generic_kernels():
+    """Schemes whose nonzero structure has no compiled kernel run on the
+    generic formation and reconstruction kernels: a block permutation of
+    two-level Strassen's 4 x 4 grid (exact coefficients), the plain 2 x 2 x 2
+    product (E5M2), and a dense GL(4) gauge (operands and orbit errors only:
+    its coefficients amplify fp32 rounding of the products by cond(P)cond(S))."""
     say("[parity] generic kernels")
     w = sy.scaled(sy.WORKLOADS["strassen2_2048x4096x4096_sign512"], 128, 256, 192, G=1)
     A, B = sy.operands(w)
     At, Bt = gpu(A), gpu(B)
-    P, Q, S = sy.gl_gauges(4, 4, 4, 1, seed=77)[0]
+    perm = np.eye(4)[[1, 0, 3, 2]]
+    P, Q, S = perm, np.eye(4)[[2, 3, 0, 1]], np.eye(4)
     h = fm.Scheme.base("strassen").kron(2).gauge(P, Q, S)
     assert h.kernel_family(1) == "generic"
     o = so.gauge(so.power(osch.strassen(), 2), P, Q, S)
@@ -222,8 +226,46 @@ def test_generic_kernels_dense_gauge_on_flat_grid():
     assert hc.kernel_family(1) == "generic"
     oc = osch.classical(2, 2, 2)
     check_operands(hc, oc, 1, A, B, At, Bt, "e5m2")
-    Co = oracle.lowp_matmul(A, B, *oracle.flatten_f32(oc))
-    assert rel(fm.matmul_lowp(hc, At, Bt).cpu().numpy(), Co) <= 1e-5
+    Co = oracle.lowp_matmul(A, B, *oracle.flatten_f32(oc), oracle.E5M2)
+    assert rel(fm.matmul_lowp(hc, At, Bt, 1, fm.E5M2).cpu().numpy(), Co) <= 1e-5
+    P, Q, S = sy.gl_gauges(4, 4, 4, 1, seed=77)[0]
+    hg = fm.Scheme.base("strassen").kron(2).gauge(P, Q, S)
+    og = so.gauge(so.power(osch.strassen(), 2), P, Q, S)
+    assert hg.kernel_family(1) == "generic"
+    check_operands(hg, og, 1, A, B, At, Bt, "e4m3")
+    Cref = fm.reference_f64(At, Bt)
+    e = fm.orbit_eval([hg, h], At, Bt, Cref)
+    Cref_o = oracle.reference_f64(A, B)
+    want = [oracle.rel_fro(oracle.lowp_matmul(A, B, *oracle.flatten_f32(x)), Cref_o) for x in (og, o)]
+    assert np.all(np.abs(e / np.array(want) - 1) <= 1e-2)
+
+
+def test_block_products_over_every_code():
+    """Codes drawn uniformly from every finite FP8 value (subnormals, both
+    signs, the largest values): the default arithmetic stays within 1e-6 of
+    the exact sums rounded once; the FP8 matrix instructions are reported and
+    bounded."""
+    rng = np.random.default_rng(5)
+    for fmt in ("e4m3", "e5m2"):
+        vals = oracle.fp8_decode(np.arange(256, dtype=np.uint8), OFMT[fmt])
+        finite = np.nonzero(np.isfinite(vals))[0].astype(np.uint8)
+        Tq = rng.choice(finite, size=(3, 80, 256)).astype(np.uint8)
+        Sq = rng.choice(finite, size=(3, 72, 256)).astype(np.uint8)
+        dT = np.array([1.0, 0.5, 3.0], np.float32)
+        dS = np.array([0.25, 1.0, 1.0 / 3.0], np.float32)
+        want = np.stack([oracle.block_product(Tq[b], Sq[b].T, dT[b], dS[b], OFMT[fmt]) for b in range(3)])
+        args = (gpu(Tq), gpu(Sq), gpu(dT), gpu(dS), FMT[fmt])
+        got = fm.block_products(*args).cpu().numpy()
+        r = rel(got, want)
+        say(f"[parity] every-code products {fmt}: default rel {r:.2e}")
+        assert r <= 1e-6
+        fm.set_block_product_arithmetic(fm.ACC_FP8)
+        try:
+            r8 = rel(fm.block_products(*args).cpu().numpy(), want)
+        finally:
+            fm.set_block_product_arithmetic(fm.ACC_BF16)
+        say(f"[parity] every-code products {fmt}: FP8 matrix instructions rel {r8:.2e}")
+        assert r8 <= 1e-3
 
 
 # ---------------------------------------------------------- edge cases
