@@ -91,6 +91,8 @@ def main():
     ap.add_argument("--fmt", default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="do not bracket kernels with events")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; the gauge orbit would "
@@ -145,6 +147,13 @@ def main():
         errs = fm.orbit_eval(hips, At, Bt, Cref, levels, fmt, ws=ws)
         return errs / st["rel_fro"], st["rel_fro"]
 
+    if args.copy_calibration:
+        x = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        y = torch.empty_like(x)
+        y.copy_(x)
+        torch.cuda.synchronize()
+        log("[bench] copy calibration: 1 GiB read + 1 GiB written by one copy kernel")
+        del x, y
     for i in range(args.warmup):
         step()
         log(f"[bench] warmup {i + 1}/{args.warmup} done")
