@@ -35,28 +35,34 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_units(cls, w, geo, chunk, G):
-    """Algorithmic work of one launch of a kernel class (flops or bytes) and
-    its roofline bound.  Per unit of work:
-      block_gemm: 2*Mb*Nb*Kb flops per block product; one launch does chunk*R
-                  products;
-      recon:      per gauge, reads R*Mb*Nb fp32 products and M*N float64
-                  reference values (C itself is not written);
-      form_amax:  reads the operand once (fp32) -- A or B^T alternately;
-      form_quant: reads the operand once and writes chunk*R*(block) codes.
+def kernel_work(cls, w, geo, chunk, G):
+    """Algorithmic work per step of one kernel class, summed over its launches
+    (the orbit's chunks and the classical baseline's single launch), and the
+    class's roofline bound.  Units of work:
+      block_gemm: 2*Mb*Nb*Kb flops per block product; G*R products for the
+                  orbit plus the classical product 2*M*N*K;
+      recon:      per gauge, R*Mb*Nb fp32 products read and M*N float64
+                  reference values read (C is not written); the classical
+                  baseline reads M*N products and writes C;
+      form_amax:  each launch reads one operand once in fp32 (A, or B^T);
+      form_quant: each launch reads one operand and writes its FP8 codes;
+      reference:  reads A and B in fp32, writes C_ref in float64.
     """
     gm, gk, gn, R = geo
-    Mb, Kb, Nb = w.M // gm, w.K // gk, w.N // gn
+    M, N, K = w.M, w.N, w.K
+    Mb, Kb, Nb = M // gm, K // gk, N // gn
+    chunks = -(-G // chunk)
+    ops = (M * K + N * K) * 4.0
     if cls == "block_gemm":
-        return "mfma", chunk * R * 2.0 * Mb * Nb * Kb, "TFLOP/s"
+        return "mfma", G * R * 2.0 * Mb * Nb * Kb + 2.0 * M * N * K, "TFLOP/s"
     if cls == "recon":
-        return "hbm", chunk * (R * Mb * Nb * 4.0 + w.M * w.N * 8.0), "GB/s"
+        return "hbm", G * (R * Mb * Nb * 4.0 + M * N * 8.0) + M * N * 8.0, "GB/s"
     if cls == "form_amax":
-        return "hbm", (w.M * w.K + w.N * w.K) * 4.0 / 2, "GB/s"  # average of the two operands
+        return "hbm", (chunks + 1) * ops, "GB/s"
     if cls == "form_quant":
-        return "hbm", ((w.M * w.K + w.N * w.K) * 4.0 + chunk * R * (Mb * Kb + Nb * Kb)) / 2, "GB/s"
+        return "hbm", (chunks + 1) * ops + G * R * (Mb * Kb + Nb * Kb) + (M * K + N * K), "GB/s"
     if cls == "reference":
-        return "hbm", (w.M * w.K + w.K * w.N) * 4.0 + w.M * w.N * 8.0, "GB/s"
+        return "hbm", ops + M * N * 8.0, "GB/s"
     raise ValueError(cls)
 
 
@@ -177,12 +183,14 @@ def main():
         fm.timing_reset()
         dom = max(per_class, key=lambda c: per_class[c]["total_ms"])
         n, ms = per_class[dom]["launches"], per_class[dom]["total_ms"]
-        bound, work, unit = kernel_units(dom, w, geo, chunk, G)
+        bound, work, unit = kernel_work(dom, w, geo, chunk, G)
+        # achieved = work per launch / average launch duration = work / time
         avg_s = ms / 1e3 / max(1, n)
+        tot_s = ms / 1e3 / args.steps
         if unit == "TFLOP/s":
-            achieved, peak = work / avg_s / 1e12, PEAK_FP8_TFLOPS
+            achieved, peak = work / tot_s / 1e12, PEAK_FP8_TFLOPS
         else:
-            achieved, peak = work / avg_s / 1e9, PEAK_HBM_GBS
+            achieved, peak = work / tot_s / 1e9, PEAK_HBM_GBS
         roof = dict(bound=bound, kernel=dom, achieved=round(achieved, 2), peak=peak, unit=unit,
                     frac=round(achieved / peak, 4), traffic=None,
                     avg_launch_ms=round(avg_s * 1e3, 4), launches_per_step=n / args.steps)
