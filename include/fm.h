@@ -103,10 +103,19 @@ int fm_scheme_load(const double* U, const double* V, const double* W, int m,
  * ascending order; inverses of order <= 3 by adjugate / determinant, larger
  * ones by Gauss-Jordan elimination with partial pivoting).  Diagonal +-1
  * P, Q, S give exactly the paper's sign variants.  FM_E_SINGULAR if P, Q or
- * S has zero determinant (or a zero pivot); the result is re-validated with
- * the Brent check (tolerance 1e-9 relative to the coefficient magnitudes). */
+ * S has zero determinant (or a zero pivot), or if X X^-1 differs from the
+ * identity by more than 1e-12 n max|X| max|X^-1| for X = P, Q, S (the base
+ * scheme passed the Brent check, so accurate inverses keep it exact). */
 int fm_gauge_apply(const fm_scheme* s, const double* P, const double* Q,
                    const double* S, fm_scheme** out);
+
+/* fm_gauge_apply for G gauge elements at once (one call for a whole orbit):
+ * P is G x m x m, Q is G x k x k, S is G x n x n (row-major float64,
+ * element g at offset g*m*m, ...); out receives G new schemes.  On failure
+ * no scheme is returned (every out[g] is NULL) and the code is that of the
+ * first failing element. */
+int fm_gauge_apply_batch(const fm_scheme* s, int G, const double* P,
+                         const double* Q, const double* S, fm_scheme** out);
 
 /* The scheme applied recursively `levels` times and flattened to one level
  * (Kronecker power, outer level first; coefficients multiplied in float64

@@ -418,10 +418,8 @@ int fm_scheme_load(const double* U, const double* V, const double* W, int m, int
   return *out ? FM_OK : fail(FM_E_NOMEM, "out of host memory");
 }
 
-int fm_gauge_apply(const fm_scheme* s, const double* P, const double* Q, const double* S,
-                   fm_scheme** out) {
-  clear_error();
-  if (!s || !P || !Q || !S || !out) return fail(FM_E_ARG, "null pointer");
+static int gauge_one(const fm_scheme* s, const double* P, const double* Q, const double* S,
+                     fm_scheme** out) {
   *out = nullptr;
   const int m = s->m, k = s->k, n = s->n;
   std::vector<double> Pm(P, P + (size_t)m * m), Qm(Q, Q + (size_t)k * k), Sm(S, S + (size_t)n * n);
@@ -442,6 +440,40 @@ int fm_gauge_apply(const fm_scheme* s, const double* P, const double* Q, const d
   g.U.assign(s->U.size(), 0.0);
   g.V.assign(s->V.size(), 0.0);
   g.W.assign(s->W.size(), 0.0);
+  auto diagonal = [](const std::vector<double>& X, int n) {
+    for (int a = 0; a < n; ++a)
+      for (int b = 0; b < n; ++b)
+        if (a != b && X[(size_t)a * n + b] != 0.0) return false;
+    return true;
+  };
+  if (diagonal(Pm, m) && diagonal(Qm, k) && diagonal(Sm, n)) {
+    // Each sum of the general formula below has one nonzero term, and the
+    // accumulator starts at +0, so the result is exactly
+    // (P_aa u_ab) Q_bb, (Qi_aa v_ab) S_bb, (Pi_aa w_ab) Si_bb.
+    for (int r = 0; r < s->R; ++r) {
+      for (int a = 0; a < m; ++a)
+        for (int b = 0; b < k; ++b) {
+          const size_t o = (size_t)r * m * k + (size_t)a * k + b;
+          g.U[o] = (Pm[(size_t)a * m + a] * s->U[o]) * Qm[(size_t)b * k + b];
+        }
+      for (int a = 0; a < k; ++a)
+        for (int b = 0; b < n; ++b) {
+          const size_t o = (size_t)r * k * n + (size_t)a * n + b;
+          g.V[o] = (Qi[(size_t)a * k + a] * s->V[o]) * Sm[(size_t)b * n + b];
+        }
+      for (int a = 0; a < m; ++a)
+        for (int b = 0; b < n; ++b) {
+          const size_t o = (size_t)r * m * n + (size_t)a * n + b;
+          g.W[o] = (Pi[(size_t)a * m + a] * s->W[o]) * Si[(size_t)b * n + b];
+        }
+    }
+    *out = clone(g);
+    return *out ? FM_OK : fail(FM_E_NOMEM, "out of host memory");
+  }
+  // Terms with an exactly zero factor are skipped: the accumulator starts at
+  // +0 and can never become -0, so adding a zero term would leave it
+  // unchanged anyway (inputs are finite); the results are bit-identical to
+  // the plain sums and diagonal gauges cost a quarter of the work.
   std::vector<double> t1, t2;
   for (int r = 0; r < s->R; ++r) {
     // U'_r = (P^T U_r) Q^T
@@ -450,13 +482,13 @@ int fm_gauge_apply(const fm_scheme* s, const double* P, const double* Q, const d
     for (int a = 0; a < m; ++a)
       for (int b = 0; b < k; ++b) {
         double acc = 0.0;
-        for (int c = 0; c < m; ++c) acc = acc + Pm[(size_t)c * m + a] * u[(size_t)c * k + b];
+        for (int c = 0; c < m; ++c) if (Pm[(size_t)c * m + a] != 0.0 && u[(size_t)c * k + b] != 0.0) acc = acc + Pm[(size_t)c * m + a] * u[(size_t)c * k + b];
         t1[(size_t)a * k + b] = acc;
       }
     for (int a = 0; a < m; ++a)
       for (int b = 0; b < k; ++b) {
         double acc = 0.0;
-        for (int c = 0; c < k; ++c) acc = acc + t1[(size_t)a * k + c] * Qm[(size_t)b * k + c];
+        for (int c = 0; c < k; ++c) if (t1[(size_t)a * k + c] != 0.0 && Qm[(size_t)b * k + c] != 0.0) acc = acc + t1[(size_t)a * k + c] * Qm[(size_t)b * k + c];
         g.U[(size_t)r * m * k + (size_t)a * k + b] = acc;
       }
     // V'_r = (Q^-T V_r) S^T
@@ -465,13 +497,13 @@ int fm_gauge_apply(const fm_scheme* s, const double* P, const double* Q, const d
     for (int a = 0; a < k; ++a)
       for (int b = 0; b < n; ++b) {
         double acc = 0.0;
-        for (int c = 0; c < k; ++c) acc = acc + Qi[(size_t)c * k + a] * v[(size_t)c * n + b];
+        for (int c = 0; c < k; ++c) if (Qi[(size_t)c * k + a] != 0.0 && v[(size_t)c * n + b] != 0.0) acc = acc + Qi[(size_t)c * k + a] * v[(size_t)c * n + b];
         t2[(size_t)a * n + b] = acc;
       }
     for (int a = 0; a < k; ++a)
       for (int b = 0; b < n; ++b) {
         double acc = 0.0;
-        for (int c = 0; c < n; ++c) acc = acc + t2[(size_t)a * n + c] * Sm[(size_t)b * n + c];
+        for (int c = 0; c < n; ++c) if (t2[(size_t)a * n + c] != 0.0 && Sm[(size_t)b * n + c] != 0.0) acc = acc + t2[(size_t)a * n + c] * Sm[(size_t)b * n + c];
         g.V[(size_t)r * k * n + (size_t)a * n + b] = acc;
       }
     // W'_r = (P^-1 W_r) S^-1
@@ -480,26 +512,63 @@ int fm_gauge_apply(const fm_scheme* s, const double* P, const double* Q, const d
     for (int a = 0; a < m; ++a)
       for (int b = 0; b < n; ++b) {
         double acc = 0.0;
-        for (int c = 0; c < m; ++c) acc = acc + Pi[(size_t)a * m + c] * w[(size_t)c * n + b];
+        for (int c = 0; c < m; ++c) if (Pi[(size_t)a * m + c] != 0.0 && w[(size_t)c * n + b] != 0.0) acc = acc + Pi[(size_t)a * m + c] * w[(size_t)c * n + b];
         t1[(size_t)a * n + b] = acc;
       }
     for (int a = 0; a < m; ++a)
       for (int b = 0; b < n; ++b) {
         double acc = 0.0;
-        for (int c = 0; c < n; ++c) acc = acc + t1[(size_t)a * n + c] * Si[(size_t)c * n + b];
+        for (int c = 0; c < n; ++c) if (t1[(size_t)a * n + c] != 0.0 && Si[(size_t)c * n + b] != 0.0) acc = acc + t1[(size_t)a * n + c] * Si[(size_t)c * n + b];
         g.W[(size_t)r * m * n + (size_t)a * n + b] = acc;
       }
   }
-  double cu = 0, cv = 0, cw = 0;
-  for (double x : g.U) cu = std::max(cu, std::fabs(x));
-  for (double x : g.V) cv = std::max(cv, std::fabs(x));
-  for (double x : g.W) cw = std::max(cw, std::fabs(x));
-  const double res = brent_residual(g);
-  if (!(res <= 1e-9 * std::max(1.0, cu * cv * cw)))
-    return fail(FM_E_BRENT, "gauged scheme fails the Brent check (residual " +
-                                std::to_string(res) + ")");
+  // The base scheme passed the Brent check at load; the gauged scheme then
+  // computes AB exactly whenever the inverses are inverses.  Check that
+  // (relative to the matrices' magnitudes) instead of the O(R (mkn)^2) Brent
+  // tensor, which dominated the cost of gauging an orbit.
+  auto inverse_ok = [](const std::vector<double>& X, const std::vector<double>& Xi, int n) {
+    double mx = 0, mi = 0;
+    for (double v : X) mx = std::max(mx, std::fabs(v));
+    for (double v : Xi) mi = std::max(mi, std::fabs(v));
+    for (int a = 0; a < n; ++a)
+      for (int b = 0; b < n; ++b) {
+        double acc = 0.0;
+        for (int c = 0; c < n; ++c) acc = acc + X[(size_t)a * n + c] * Xi[(size_t)c * n + b];
+        if (!(std::fabs(acc - (a == b ? 1.0 : 0.0)) <= 1e-12 * std::max(1.0, n * mx * mi)))
+          return false;
+      }
+    return true;
+  };
+  if (!inverse_ok(Pm, Pi, m) || !inverse_ok(Qm, Qi, k) || !inverse_ok(Sm, Si, n))
+    return fail(FM_E_SINGULAR, "gauge matrix is too ill-conditioned to invert accurately");
   *out = clone(g);
   return *out ? FM_OK : fail(FM_E_NOMEM, "out of host memory");
+}
+
+int fm_gauge_apply(const fm_scheme* s, const double* P, const double* Q, const double* S,
+                   fm_scheme** out) {
+  clear_error();
+  if (!s || !P || !Q || !S || !out) return fail(FM_E_ARG, "null pointer");
+  return gauge_one(s, P, Q, S, out);
+}
+
+int fm_gauge_apply_batch(const fm_scheme* s, int G, const double* P, const double* Q,
+                         const double* S, fm_scheme** out) {
+  clear_error();
+  if (!s || !P || !Q || !S || !out) return fail(FM_E_ARG, "null pointer");
+  if (G < 0) return fail(FM_E_ARG, "G must be non-negative");
+  const size_t mm = (size_t)s->m * s->m, kk = (size_t)s->k * s->k, nn = (size_t)s->n * s->n;
+  for (int g = 0; g < G; ++g) out[g] = nullptr;
+  for (int g = 0; g < G; ++g) {
+    if (int rc = gauge_one(s, P + g * mm, Q + g * kk, S + g * nn, &out[g])) {
+      for (int h = 0; h < g; ++h) {
+        fm_scheme_free(out[h]);
+        out[h] = nullptr;
+      }
+      return rc;
+    }
+  }
+  return FM_OK;
 }
 
 int fm_scheme_kron(const fm_scheme* s, int levels, fm_scheme** out) {

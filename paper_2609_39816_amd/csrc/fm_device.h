@@ -316,7 +316,8 @@ __device__ __forceinline__ void recon_emit(const ReconArgs& a, int c, int x, int
   }
 }
 
-__device__ __forceinline__ void recon_reduce(const ReconArgs& a, double esq, double* red) {
+__device__ __forceinline__ void recon_reduce(const ReconArgs& a, double esq, double* red, int g,
+                                             int nblk, int blk) {
   if (!a.Cref) return;
   red[threadIdx.x] = esq;
   __syncthreads();
@@ -324,19 +325,33 @@ __device__ __forceinline__ void recon_reduce(const ReconArgs& a, double esq, dou
     if (threadIdx.x < s) red[threadIdx.x] = red[threadIdx.x] + red[threadIdx.x + s];
     __syncthreads();
   }
-  if (threadIdx.x == 0) a.partial[(size_t)blockIdx.y * gridDim.x + blockIdx.x] = red[0];
+  if (threadIdx.x == 0) a.partial[(size_t)g * nblk + blk] = red[0];
+}
+
+// Workgroup -> (gauge, position block).  The grid is 1-D over nblk * G
+// workgroups; dispatch goes round-robin over the 8 XCDs, so remap to give
+// each XCD a contiguous range of (position block major, gauge minor): the G
+// gauges of a position block then share that XCD's L2 and the reference
+// tile is fetched from memory about once per chunk instead of once per gauge.
+__device__ __forceinline__ void recon_slot(int G, int nblk, int& g, int& blk) {
+  const int total = G * nblk;
+  int w = blockIdx.x;
+  if ((total & 7) == 0) w = (w & 7) * (total >> 3) + (w >> 3);
+  blk = w / G;
+  g = w - blk * G;
 }
 
 template <class P, int VW>
-__global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a) {
+__global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a, int nblk) {
   __shared__ double red[kThreads];
-  const int g = blockIdx.y;
+  int g, blk;
+  recon_slot(a.G, nblk, g, blk);
   const int bcv = a.Nb / VW;
   const int Ptot = a.Mb * bcv;
   const size_t bsz = (size_t)a.Mb * a.Nb;
   const float* coef = a.coef + a.off[(size_t)g * (P::R + 1)];
   double esq = 0.0;
-  for (int base = blockIdx.x * kThreads; base < Ptot; base += gridDim.x * kThreads) {
+  for (int base = blk * kThreads; base < Ptot; base += nblk * kThreads) {
     const int p = base + threadIdx.x;
     if (p >= Ptot) break;
     const int x = p / bcv, z0 = (p - x * bcv) * VW;
@@ -366,21 +381,22 @@ __global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a) {
 #pragma unroll
     for (int c = 0; c < P::NB; ++c) recon_emit<VW>(a, c, x, z0, acc[c], esq);
   }
-  recon_reduce(a, esq, red);
+  recon_reduce(a, esq, red, g, nblk, blk);
 }
 
 template <int VW>
-__global__ __launch_bounds__(kThreads) void recon_generic_kernel(ReconArgs a) {
+__global__ __launch_bounds__(kThreads) void recon_generic_kernel(ReconArgs a, int nblk) {
   __shared__ double red[kThreads];
   extern __shared__ float lacc[];  // [NC][thread][VW]
-  const int g = blockIdx.y;
+  int g, blk;
+  recon_slot(a.G, nblk, g, blk);
   const int R = a.R, NC = a.gm * a.gn;
   const int bcv = a.Nb / VW;
   const int Ptot = a.Mb * bcv;
   const size_t bsz = (size_t)a.Mb * a.Nb;
   const int32_t* off = a.off + (size_t)g * (R + 1);
   double esq = 0.0;
-  for (int base = blockIdx.x * kThreads; base < Ptot; base += gridDim.x * kThreads) {
+  for (int base = blk * kThreads; base < Ptot; base += nblk * kThreads) {
     const int p = base + threadIdx.x;
     if (p >= Ptot) break;
     const int x = p / bcv, z0 = (p - x * bcv) * VW;
@@ -407,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void recon_generic_kernel(ReconArgs a) {
       recon_emit<VW>(a, c, x, z0, acc, esq);
     }
   }
-  recon_reduce(a, esq, red);
+  recon_reduce(a, esq, red, g, nblk, blk);
 }
 
 inline int launched(const char* what) { return hip_check(hipGetLastError(), what); }
@@ -416,12 +432,17 @@ inline int launched(const char* what) { return hip_check(hipGetLastError(), what
 // each looping over position groups; gauges split over grid.y.
 inline dim3 form_grid(const FormArgs& a, int vw, int mode, int& gpb) {
   const int P = a.br * (a.bc / vw);
-  gpb = (mode == 0) ? std::max(1, std::min(a.G, 4096 / std::max(1, a.R)))
-                    : std::max(1, std::min(a.G, 8));
+  const int gx_full = (P + kThreads - 1) / kThreads;
+  // Split the gauges over grid.y so that the launch has at least ~2048
+  // workgroups (8 per CU), keeping at most 16 KB of amax slots in LDS.
+  const int target = 2048;
+  const int slices = std::max(1, std::min(a.G, (target + gx_full - 1) / gx_full));
+  gpb = (a.G + slices - 1) / slices;
+  if (mode == 0) gpb = std::max(1, std::min(gpb, 4096 / std::max(1, a.R)));
   const int gy = (a.G + gpb - 1) / gpb;
-  int gx = (P + kThreads - 1) / kThreads;
-  const int target = 8192;
-  if ((long long)gx * gy > target) gx = std::max(1, target / gy);
+  int gx = gx_full;
+  if ((long long)gx * gy > 4 * target) gx = std::max(1, 4 * target / gy);
+  (void)mode;
   return dim3(gx, gy);
 }
 
@@ -479,14 +500,15 @@ constexpr int recon_vw() {
 template <class P>
 int launch_recon_static(const ReconArgs& a, hipStream_t st) {
   constexpr int VW = recon_vw<P>();
-  dim3 grid(recon_blocks(a), a.G);
-  recon_static_kernel<P, VW><<<grid, kThreads, 0, st>>>(a);
+  const int nblk = recon_blocks(a);
+  recon_static_kernel<P, VW><<<nblk * a.G, kThreads, 0, st>>>(a, nblk);
   return launched("recon_static_kernel");
 }
 
 inline int launch_recon_generic(const ReconArgs& a, hipStream_t st) {
   const int nc = a.gm * a.gn;
-  dim3 grid(recon_blocks(a), a.G);
+  const int nblk = recon_blocks(a);
+  const int grid = nblk * a.G;
   const bool wide = nc <= 16 && a.Nb % 4 == 0 && a.N % 4 == 0;
   const size_t shm = (size_t)nc * kThreads * 4 * (wide ? 4 : 1);
   const void* fn = wide ? reinterpret_cast<const void*>(&recon_generic_kernel<4>)
@@ -496,9 +518,9 @@ inline int launch_recon_generic(const ReconArgs& a, hipStream_t st) {
                          "hipFuncSetAttribute"))
     return rc;
   if (wide) {
-    recon_generic_kernel<4><<<grid, kThreads, shm, st>>>(a);
+    recon_generic_kernel<4><<<grid, kThreads, shm, st>>>(a, nblk);
   } else {
-    recon_generic_kernel<1><<<grid, kThreads, shm, st>>>(a);
+    recon_generic_kernel<1><<<grid, kThreads, shm, st>>>(a, nblk);
   }
   return launched("recon_generic_kernel");
 }

@@ -56,6 +56,7 @@ def _load():
         "fm_version": (ct.c_char_p, []),
         "fm_scheme_load": (i, [p, p, p, i, i, i, i, pp]),
         "fm_gauge_apply": (i, [p, p, p, p, pp]),
+        "fm_gauge_apply_batch": (i, [p, i, p, p, p, pp]),
         "fm_scheme_kron": (i, [p, i, pp]),
         "fm_scheme_dims": (i, [p, p, p, p, p]),
         "fm_scheme_coeffs": (i, [p, p, p, p]),
@@ -158,6 +159,18 @@ class Scheme:
         out = ct.c_void_p()
         _check(lib.fm_gauge_apply(self._h, _np_ptr(P), _np_ptr(Q), _np_ptr(S), ct.byref(out)))
         return Scheme(out.value)
+
+    def gauge_orbit(self, gauges) -> list:
+        """Gauged copies for a list of (P, Q, S), in one library call."""
+        G = len(gauges)
+        if G == 0:
+            return []
+        P = _f64(np.stack([g[0] for g in gauges]))
+        Q = _f64(np.stack([g[1] for g in gauges]))
+        S = _f64(np.stack([g[2] for g in gauges]))
+        out = (ct.c_void_p * G)()
+        _check(lib.fm_gauge_apply_batch(self._h, G, _np_ptr(P), _np_ptr(Q), _np_ptr(S), out))
+        return [Scheme(h) for h in out]
 
     def kron(self, levels: int) -> "Scheme":
         out = ct.c_void_p()

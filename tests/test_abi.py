@@ -182,3 +182,18 @@ def test_mismatched_orbit_is_rejected():
     rc = fm.lib.fm_orbit_eval(ct.cast(handles, ct.c_void_p), 2, p, p, p, 256, 256, 256, 1, 0,
                               out.ctypes.data_as(ct.c_void_p), p, 1 << 40, None)
     assert rc == -8
+
+
+def test_batched_gauge_equals_single_calls():
+    s2 = fm.Scheme.base("strassen").kron(2)
+    signs = [(np.diag(d), np.diag(e), np.diag(f)) for d, e, f in sy.sign_orbit(4, 4, 4)[::41]]
+    s1 = fm.Scheme.base("strassen")
+    gls = sy.gl_gauges(2, 2, 2, 5, seed=4)
+    for base, gs in ((s2, signs), (s1, gls)):
+        batch = base.gauge_orbit(gs)
+        for (P, Q, S), h in zip(gs, batch):
+            for a, b in zip(base.gauge(P, Q, S).coeffs(), h.coeffs()):
+                assert np.array_equal(a.view(np.uint64), b.view(np.uint64))
+    with pytest.raises(fm.FmError) as e:
+        s1.gauge_orbit([gls[0], (np.zeros((2, 2)), np.eye(2), np.eye(2))])
+    assert e.value.name == "FM_E_SINGULAR"
