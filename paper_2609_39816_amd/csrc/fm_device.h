@@ -341,45 +341,111 @@ __device__ __forceinline__ void recon_slot(int G, int nblk, int& g, int& blk) {
   g = w - blk * G;
 }
 
+// Products are read through a buffer resource over the gauge's slab of R
+// products (base in the descriptor, r * block bytes as the scalar offset, the
+// position as the vector offset), which keeps the 64-bit address arithmetic
+// of the R product streams off the registers; the launcher checks that the
+// slab fits the 32-bit offsets.  The gauge's coefficients are staged in LDS.
+// Product loads go in groups of 8, double-buffered: the loads of group k+1
+// are in flight while group k is accumulated (scheduling barriers keep the
+// compiler from hoisting further).  The error epilogue goes 4 blocks at a
+// time.  The grid gives every thread one position group (no loop), so no
+// loop-invariant value is held across positions.
+// Keeps the compiler from moving memory operations (or merging loads) across
+// a group boundary, at the IR and the machine level; emits no instruction.
+__device__ __forceinline__ void group_fence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Makes the accumulators appear read and written here, so every
+// accumulation issued before this point in source order is done before it.
+template <int NB, int VW>
+__device__ __forceinline__ void pin_acc(float (&acc)[NB][VW]) {
+#pragma unroll
+  for (int c = 0; c < NB; ++c)
+#pragma unroll
+    for (int v = 0; v < VW; ++v) asm volatile("" : "+v"(acc[c][v]));
+}
+
+template <int VW>
+__device__ __forceinline__ void recon_load_buf(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff,
+                                               uint32_t soff, float (&m)[VW]) {
+  if constexpr (VW == 4) {
+    const auto t = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)voff, (int)soff, 0);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) m[v] = __uint_as_float(t[v]);
+  } else {
+#pragma unroll
+    for (int v = 0; v < VW; ++v)
+      m[v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, (int)(voff + 4 * v), (int)soff, 0));
+  }
+}
+
 template <class P, int VW>
 __global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a, int nblk) {
+  constexpr int NNZ = P::rowptr[P::R];
+  constexpr int GR = 8, NG = (P::R + GR - 1) / GR;
   __shared__ double red[kThreads];
+  __shared__ float cl[NNZ];
   int g, blk;
   recon_slot(a.G, nblk, g, blk);
+  const float* coef = a.coef + a.off[(size_t)g * (P::R + 1)];
+  for (int e = threadIdx.x; e < NNZ; e += kThreads) cl[e] = coef[e];
+  __syncthreads();
   const int bcv = a.Nb / VW;
   const int Ptot = a.Mb * bcv;
   const size_t bsz = (size_t)a.Mb * a.Nb;
-  const float* coef = a.coef + a.off[(size_t)g * (P::R + 1)];
+  const uint32_t bbytes = (uint32_t)(bsz * 4);
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.Mprod + (size_t)g * P::R * bsz), (short)0, (int)(P::R * bbytes),
+      0x00020000);
   double esq = 0.0;
-  for (int base = blk * kThreads; base < Ptot; base += nblk * kThreads) {
-    const int p = base + threadIdx.x;
-    if (p >= Ptot) break;
+  const int p = blk * kThreads + threadIdx.x;
+  if (p < Ptot) {
     const int x = p / bcv, z0 = (p - x * bcv) * VW;
+    const uint32_t voff = (uint32_t)(x * a.Nb + z0) * 4u;
     float acc[P::NB][VW];
 #pragma unroll
     for (int c = 0; c < P::NB; ++c)
 #pragma unroll
       for (int v = 0; v < VW; ++v) acc[c][v] = 0.0f;
-    const float* mb = a.Mprod + (size_t)g * P::R * bsz + (size_t)x * a.Nb + z0;
-    sfor<0, P::R>([&](auto rc) {
-      constexpr int r = decltype(rc)::value;
-      // keep the scheduler from hoisting every product's load to the top
-      // (343 products would not fit in registers): one group of 8 at a time
-      if constexpr (r % 8 == 0 && r > 0) __builtin_amdgcn_sched_barrier(0);
-      if constexpr (P::rowptr[r + 1] > P::rowptr[r]) {
-        float m[VW];
-        recon_load<VW>(mb + (size_t)r * bsz, m);
-        sfor<P::rowptr[r], P::rowptr[r + 1]>([&](auto ec) {
-          constexpr int e = decltype(ec)::value;
-          constexpr int c = P::idx[e];
-          const float w = coef[e];
+    float mb[2][GR][VW];
+    auto load_group = [&](auto gc) {
+      constexpr int gi = decltype(gc)::value;
+      sfor<0, GR>([&](auto jc) {
+        constexpr int j = decltype(jc)::value, r = gi * GR + j;
+        if constexpr (r < P::R) {
+          if constexpr (P::rowptr[r + 1] > P::rowptr[r])
+            recon_load_buf<VW>(rsrc, voff, (uint32_t)r * bbytes, mb[gi & 1][j]);
+        }
+      });
+    };
+    load_group(std::integral_constant<int, 0>{});
+    sfor<0, NG>([&](auto gc) {
+      constexpr int gi = decltype(gc)::value;
+      if constexpr (gi + 1 < NG) load_group(std::integral_constant<int, gi + 1>{});
+      group_fence();
+      sfor<0, GR>([&](auto jc) {
+        constexpr int j = decltype(jc)::value, r = gi * GR + j;
+        if constexpr (r < P::R) {
+          sfor<P::rowptr[r], P::rowptr[r + 1]>([&](auto ec) {
+            constexpr int e = decltype(ec)::value;
+            constexpr int c = P::idx[e];
+            const float w = cl[e];
 #pragma unroll
-          for (int v = 0; v < VW; ++v) acc[c][v] = __builtin_fmaf(w, m[v], acc[c][v]);
-        });
-      }
+            for (int v = 0; v < VW; ++v) acc[c][v] = __builtin_fmaf(w, mb[gi & 1][j][v], acc[c][v]);
+          });
+        }
+      });
+      pin_acc(acc);
+      group_fence();
     });
-#pragma unroll
-    for (int c = 0; c < P::NB; ++c) recon_emit<VW>(a, c, x, z0, acc[c], esq);
+    sfor<0, P::NB>([&](auto cc) {
+      constexpr int c = decltype(cc)::value;
+      if constexpr (c % 4 == 0) group_fence();
+      recon_emit<VW>(a, c, x, z0, acc[c], esq);
+    });
   }
   recon_reduce(a, esq, red, g, nblk, blk);
 }
@@ -501,6 +567,9 @@ template <class P>
 int launch_recon_static(const ReconArgs& a, hipStream_t st) {
   constexpr int VW = recon_vw<P>();
   const int nblk = recon_blocks(a);
+  // the kernel gives each thread exactly one position group
+  if (recon_width(a) != VW || (long long)nblk * kThreads < (long long)a.Mb * (a.Nb / VW))
+    return fail(FM_E_UNSUPPORTED, "reconstruction grid does not cover the block");
   recon_static_kernel<P, VW><<<nblk * a.G, kThreads, 0, st>>>(a, nblk);
   return launched("recon_static_kernel");
 }
@@ -509,7 +578,7 @@ inline int launch_recon_generic(const ReconArgs& a, hipStream_t st) {
   const int nc = a.gm * a.gn;
   const int nblk = recon_blocks(a);
   const int grid = nblk * a.G;
-  const bool wide = nc <= 16 && a.Nb % 4 == 0 && a.N % 4 == 0;
+  const bool wide = recon_width(a) == 4;
   const size_t shm = (size_t)nc * kThreads * 4 * (wide ? 4 : 1);
   const void* fn = wide ? reinterpret_cast<const void*>(&recon_generic_kernel<4>)
                         : reinterpret_cast<const void*>(&recon_generic_kernel<1>);
@@ -552,7 +621,8 @@ FM_PATTERN_FAMILIES(FM_DECLARE_FAMILY)
   int recon_family_##P(const ReconArgs& a, hipStream_t st) {                         \
     using namespace dev;                                                             \
     using W = pat::P::W;                                                             \
-    if (a.gm * a.gn != W::NB || a.R != W::R || a.Nb % recon_vw<W>() != 0 || a.N % 4) \
+    if (a.gm * a.gn != W::NB || a.R != W::R || a.Nb % recon_vw<W>() != 0 || a.N % 4 || \
+        (size_t)a.R * a.Mb * a.Nb * 4 >= ((size_t)1 << 32))                          \
       return 1;                                                                      \
     return launch_recon_static<W>(a, st);                                            \
   }

@@ -126,7 +126,12 @@ struct ReconArgs {
   const double* Cref;  // optional
   double* partial;     // G x nblk (if Cref)
 };
-int recon_blocks(const ReconArgs& a);  // number of blocks per gauge the launcher uses
+// Positions per thread in the reconstruction kernels (4 or 1) and the
+// number of workgroups per gauge (one position group per thread).
+inline int recon_width(const ReconArgs& a) {
+  return (a.gm * a.gn <= 16 && a.Nb % 4 == 0 && a.N % 4 == 0) ? 4 : 1;
+}
+int recon_blocks(const ReconArgs& a);
 int launch_recon(const ReconArgs& a, int pattern, hipStream_t st);
 
 // out[g] = sum_{b < nblk} partial[g*nblk + b] (fixed order), g < G.

@@ -268,6 +268,31 @@ def test_block_products_over_every_code():
         assert r8 <= 1e-3
 
 
+@pytest.mark.parametrize("batch,Mb,Nb,Kb", [
+    (96, 300, 260, 384),   # ragged in both directions, several tiles per workgroup
+    (70, 256, 128, 128),   # exactly one tile and one K step per product
+    (9, 512, 256, 1024),   # interior tiles only, eight K steps
+    (12, 200, 130, 256),   # a row length not a multiple of 4 (element stores)
+    (5, 72, 80, 96),       # inner length not a multiple of 128
+])
+def test_block_products_tilings(batch, Mb, Nb, Kb):
+    """Batched block products over tilings that exercise the persistent
+    pipelined kernel (ring wrap-around, tile changes inside the ring, ragged
+    edges) against the exact sums rounded once."""
+    say(f"[parity] block products batch {batch} {Mb}x{Nb}x{Kb}")
+    rng = np.random.default_rng(batch * 7 + Kb)
+    vals = oracle.fp8_decode(np.arange(256, dtype=np.uint8), oracle.E4M3)
+    finite = np.nonzero(np.isfinite(vals) & (np.abs(vals) <= 64))[0].astype(np.uint8)
+    Tq = rng.choice(finite, size=(batch, Mb, Kb)).astype(np.uint8)
+    Sq = rng.choice(finite, size=(batch, Nb, Kb)).astype(np.uint8)
+    dT = (rng.random(batch) + 0.5).astype(np.float32)
+    dS = (rng.random(batch) + 0.5).astype(np.float32)
+    got = fm.block_products(gpu(Tq), gpu(Sq), gpu(dT), gpu(dS), fm.E4M3).cpu().numpy()
+    for b in sorted({0, 1, batch // 2, batch - 1}):
+        want = oracle.block_product(Tq[b], Sq[b].T, dT[b], dS[b], oracle.E4M3)
+        assert rel(got[b], want) <= 1e-6, f"product {b}: rel {rel(got[b], want):.2e}"
+
+
 # ---------------------------------------------------------- edge cases
 def test_zero_operand_and_single_tile():
     say("[parity] zero operand")
