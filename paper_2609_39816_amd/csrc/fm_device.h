@@ -23,6 +23,15 @@ namespace dev {
 
 inline constexpr int kThreads = 256;
 
+// Read-only tables (coefficient lists, per-product scales) are read through
+// the constant address space: the kernels never write them, and this lets
+// wave-uniform reads go through the scalar cache into SGPRs even in kernels
+// that store to other global memory.
+template <class T>
+__device__ __forceinline__ const __attribute__((address_space(4))) T* ro(const T* p) {
+  return (const __attribute__((address_space(4))) T*)p;
+}
+
 // ------------------------------------------------------------ wave helpers
 // Maximum over the 64 lanes of a wave of non-negative values; every lane
 // returns the result.  DPP row shifts build each row's maximum in its lane
@@ -186,44 +195,147 @@ __device__ __forceinline__ void form_flush(const FormArgs& a, const uint32_t* sm
 
 // Specialized for one nonzero structure P (fm_patterns.inc): block indices
 // are compile-time constants, so the operand blocks stay in registers.
-template <class P, int VW, int MODE>
-__global__ __launch_bounds__(kThreads) void form_static_kernel(FormArgs a, int gpb) {
-  extern __shared__ uint32_t smax[];
+// Products are handled in groups of 8.  Mode 0 folds each product's values
+// into a per-lane maximum, reduces the group's 8 maxima within 16-lane rows
+// with interleaved DPP steps (no hazard stalls between dependent steps), and
+// the last lane of each row keeps the result in its own LDS slot (plain
+// stores, no atomics); the workgroup combines the 16 slots of each product
+// once at the end.  Mode 1
+// writes the codes through a buffer descriptor over the gauge's R tensors
+// (product offset in the scalar offset, position in the vector offset); an
+// inactive lane gets an offset past the end, so its store is dropped by the
+// range check instead of branched around.  The launcher checks that the R
+// tensors of one gauge fit the 31-bit offsets.
+template <int FMT, int VW>
+__device__ __forceinline__ void form_encode_store(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff,
+                                                  uint32_t soff, const float (&acc)[VW], float q) {
+  static_assert(VW == 2 || VW % 4 == 0, "code store width");
+  uint32_t w[(VW + 3) / 4];
+#pragma unroll
+  for (int t = 0; t < (VW + 3) / 4; ++t) {
+    const float x0 = acc[4 * t] * q, x1 = acc[4 * t + 1] * q;
+    if constexpr (FMT == FM_E4M3) w[t] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x0, x1, 0, false);
+    else w[t] = (uint32_t)__builtin_amdgcn_cvt_pk_bf8_f32(x0, x1, 0, false);
+    if constexpr (VW >= 4) {
+      const float x2 = acc[4 * t + 2] * q, x3 = acc[4 * t + 3] * q;
+      if constexpr (FMT == FM_E4M3) w[t] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x2, x3, (int)w[t], true);
+      else w[t] = (uint32_t)__builtin_amdgcn_cvt_pk_bf8_f32(x2, x3, (int)w[t], true);
+    }
+  }
+  if constexpr (VW == 2) {
+    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)(w[0] & 0xffffu), rsrc, (int)voff, (int)soff, 0);
+  } else if constexpr (VW == 4) {
+    __builtin_amdgcn_raw_buffer_store_b32(w[0], rsrc, (int)voff, (int)soff, 0);
+  } else if constexpr (VW == 8) {
+    __builtin_amdgcn_raw_buffer_store_b64((__attribute__((ext_vector_type(2))) unsigned){w[0], w[1]},
+                                          rsrc, (int)voff, (int)soff, 0);
+  } else {
+#pragma unroll
+    for (int t = 0; t < VW / 4; t += 4)
+      __builtin_amdgcn_raw_buffer_store_b128(
+          (__attribute__((ext_vector_type(4))) unsigned){w[t], w[t + 1], w[t + 2], w[t + 3]}, rsrc,
+          (int)(voff + 4 * t), (int)soff, 0);
+  }
+}
+
+template <class P, int VW, int MODE, int FMT>
+__device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uint32_t* smax) {
+  constexpr int GR = 8, NG = (P::R + GR - 1) / GR;
   const int bcv = a.bc / VW;
   const int Ptot = a.br * bcv;
   const int g0 = blockIdx.y * gpb;
   const int g1 = min(a.G, g0 + gpb);
   const int lane = threadIdx.x & 63;
-  if constexpr (MODE == 0) {
-    for (int i = threadIdx.x; i < gpb * P::R; i += kThreads) smax[i] = 0u;
-    __syncthreads();
-  }
+  const uint32_t bsz = (uint32_t)a.br * (uint32_t)a.bc;
   for (int base = blockIdx.x * kThreads; base < Ptot; base += gridDim.x * kThreads) {
     const int p = base + threadIdx.x;
     const bool active = p < Ptot;
     const int x = active ? p / bcv : 0;
     const int y0 = active ? (p - x * bcv) * VW : 0;
+    const uint32_t voff = active ? (uint32_t)(x * a.bc + y0) : 0x80000000u;
     float xv[P::NB][VW];
     form_load<P::NB, VW>(a, xv, active, x, y0);
     for (int g = g0; g < g1; ++g) {
-      const float* coef = a.coef + a.off[(size_t)g * (P::R + 1)];
-      sfor<0, P::R>([&](auto rc) {
-        constexpr int r = decltype(rc)::value;
-        float acc[VW];
+      const auto coef = ro(a.coef) + ro(a.off)[(size_t)g * (P::R + 1)];
+      __amdgpu_buffer_rsrc_t rsrc;
+      if constexpr (MODE == 1)
+        rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + (size_t)g * P::R * bsz, (short)0,
+                                                 (int)(P::R * bsz), 0x00020000);
+      sfor<0, NG>([&](auto gc) {
+        constexpr int gi = decltype(gc)::value;
+        uint32_t lm[GR];
+        sfor<0, GR>([&](auto jc) {
+          constexpr int j = decltype(jc)::value, r = gi * GR + j;
+          if constexpr (r < P::R) {
+            float acc[VW];
 #pragma unroll
-        for (int v = 0; v < VW; ++v) acc[v] = 0.0f;
-        sfor<P::rowptr[r], P::rowptr[r + 1]>([&](auto ec) {
-          constexpr int e = decltype(ec)::value;
-          constexpr int b = P::idx[e];
-          const float c = coef[e];
+            for (int v = 0; v < VW; ++v) acc[v] = 0.0f;
+            sfor<P::rowptr[r], P::rowptr[r + 1]>([&](auto ec) {
+              constexpr int e = decltype(ec)::value;
+              constexpr int b = P::idx[e];
+              const float c = coef[e];
 #pragma unroll
-          for (int v = 0; v < VW; ++v) acc[v] = __builtin_fmaf(c, xv[b][v], acc[v]);
+              for (int v = 0; v < VW; ++v) acc[v] = __builtin_fmaf(c, xv[b][v], acc[v]);
+            });
+            if constexpr (MODE == 0) {
+              uint32_t mx = 0u;
+#pragma unroll
+              for (int v = 0; v < VW; ++v) mx = max(mx, __float_as_uint(acc[v]) & 0x7fffffffu);
+              lm[j] = active ? mx : 0u;
+            } else {
+              form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, acc,
+                                         ro(a.q)[(size_t)g * P::R + r]);
+            }
+          }
         });
-        form_finish<VW, MODE>(a, acc, g, g0, r, active, x, y0, smax, lane);
+        if constexpr (MODE == 0) {
+          constexpr int NJ = (gi * GR + GR <= P::R) ? GR : P::R - gi * GR;
+          // row maxima: after shifts 1, 2, 4, 8 lane 15 of each row holds
+          // the maximum of its row (lanes shifted in from outside the row
+          // read 0, the bound-control value)
+          sfor<0, 4>([&](auto sc) {
+            constexpr int ctl = 0x111 + (1 << decltype(sc)::value) - 1;  // row_shr:1,2,4,8
+            uint32_t sh[NJ];
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+              sh[j] = (uint32_t)__builtin_amdgcn_mov_dpp((int)lm[j], ctl, 0xf, 0xf, true);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) lm[j] = max(lm[j], sh[j]);
+          });
+          // the last lane of each row keeps its row's maximum in the
+          // (wave, row) slot of the product; slots are combined per workgroup
+          if ((lane & 15) == 15) {
+            uint32_t* slot = smax + ((g - g0) * P::R + gi * GR) * 16 + (threadIdx.x >> 4);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) slot[j * 16] = max(slot[j * 16], lm[j]);
+          }
+        }
       });
     }
   }
-  form_flush<MODE>(a, smax, g0, g1);
+}
+
+template <class P, int VW, int MODE>
+__global__ __launch_bounds__(kThreads) void form_static_kernel(FormArgs a, int gpb) {
+  extern __shared__ uint32_t smax[];  // mode 0: [gauge][product][wave * 4 + row]
+  const int g0 = blockIdx.y * gpb;
+  const int g1 = min(a.G, g0 + gpb);
+  if constexpr (MODE == 0) {
+    for (int i = threadIdx.x; i < gpb * P::R * 16; i += kThreads) smax[i] = 0u;
+    __syncthreads();
+    form_static_body<P, VW, 0, FM_E4M3>(a, gpb, smax);
+    __syncthreads();
+    const int n = (g1 - g0) * P::R;
+    for (int k = threadIdx.x; k < n; k += kThreads) {
+      uint32_t m = 0u;
+#pragma unroll
+      for (int t = 0; t < 16; ++t) m = max(m, smax[k * 16 + t]);
+      if (m) atomicMax(&a.amax[(size_t)g0 * P::R + k], m);
+    }
+  } else {
+    if (a.fmt == FM_E4M3) form_static_body<P, VW, 1, FM_E4M3>(a, gpb, smax);
+    else form_static_body<P, VW, 1, FM_E5M2>(a, gpb, smax);
+  }
 }
 
 // Any nonzero structure: each thread parks its operand values in its own
@@ -390,7 +502,7 @@ __global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a, int
   __shared__ float cl[NNZ];
   int g, blk;
   recon_slot(a.G, nblk, g, blk);
-  const float* coef = a.coef + a.off[(size_t)g * (P::R + 1)];
+  const auto coef = ro(a.coef) + ro(a.off)[(size_t)g * (P::R + 1)];
   for (int e = threadIdx.x; e < NNZ; e += kThreads) cl[e] = coef[e];
   __syncthreads();
   const int bcv = a.Nb / VW;
@@ -496,7 +608,7 @@ inline int launched(const char* what) { return hip_check(hipGetLastError(), what
 
 // Workgroups for operand formation: enough to cover the GPU several times,
 // each looping over position groups; gauges split over grid.y.
-inline dim3 form_grid(const FormArgs& a, int vw, int mode, int& gpb) {
+inline dim3 form_grid(const FormArgs& a, int vw, int max_gpb, int& gpb) {
   const int P = a.br * (a.bc / vw);
   const int gx_full = (P + kThreads - 1) / kThreads;
   // Split the gauges over grid.y so that the launch has at least ~2048
@@ -504,11 +616,10 @@ inline dim3 form_grid(const FormArgs& a, int vw, int mode, int& gpb) {
   const int target = 2048;
   const int slices = std::max(1, std::min(a.G, (target + gx_full - 1) / gx_full));
   gpb = (a.G + slices - 1) / slices;
-  if (mode == 0) gpb = std::max(1, std::min(gpb, 4096 / std::max(1, a.R)));
+  gpb = std::max(1, std::min(gpb, max_gpb));
   const int gy = (a.G + gpb - 1) / gpb;
   int gx = gx_full;
   if ((long long)gx * gy > 4 * target) gx = std::max(1, 4 * target / gy);
-  (void)mode;
   return dim3(gx, gy);
 }
 
@@ -520,9 +631,11 @@ constexpr int static_vw() {
 template <class P, int MODE>
 int launch_form_static(const FormArgs& a, hipStream_t st) {
   constexpr int VW = static_vw<P>();
+  // mode 0 LDS: 16 row slots per (gauge, product), at most 48 KB
+  const int max_gpb = MODE == 0 ? std::max(1, 12288 / (P::R * 16)) : a.G;
   int gpb;
-  const dim3 grid = form_grid(a, VW, MODE, gpb);
-  const size_t shm = (MODE == 0) ? (size_t)gpb * a.R * 4 : 0;
+  const dim3 grid = form_grid(a, VW, max_gpb, gpb);
+  const size_t shm = (MODE == 0) ? (size_t)gpb * P::R * 16 * 4 : 0;
   form_static_kernel<P, VW, MODE><<<grid, kThreads, shm, st>>>(a, gpb);
   return launched("form_static_kernel");
 }
@@ -530,13 +643,14 @@ int launch_form_static(const FormArgs& a, hipStream_t st) {
 template <class P>
 bool static_ok(const FormArgs& a) {
   constexpr int VW = static_vw<P>();
-  return a.gr * a.gc == P::NB && a.R == P::R && a.bc % VW == 0 && (VW < 4 || a.cols % 4 == 0);
+  return a.gr * a.gc == P::NB && a.R == P::R && a.bc % VW == 0 && (VW < 4 || a.cols % 4 == 0) &&
+         (size_t)P::R * a.br * a.bc < ((size_t)1 << 31);
 }
 
 template <int VW>
 int launch_form_generic_t(const FormArgs& a, int mode, hipStream_t st) {
   int gpb;
-  const dim3 grid = form_grid(a, VW, mode, gpb);
+  const dim3 grid = form_grid(a, VW, mode == 0 ? std::max(1, 4096 / std::max(1, a.R)) : a.G, gpb);
   const size_t shm = (size_t)a.gr * a.gc * kThreads * VW * 4 + (mode == 0 ? (size_t)gpb * a.R * 4 : 0);
   if (shm > 160 * 1024) return fail(FM_E_UNSUPPORTED, "formation needs too much LDS");
   const void* fn = mode == 0 ? reinterpret_cast<const void*>(&form_generic_kernel<VW, 0>)
