@@ -4,13 +4,7 @@
 //                   gauged schemes (eq. (1), Sec. 2.1), in two modes: per-
 //                   tensor amax (atomic max on the uint bits of |x|), then
 //                   FP8 codes of x * (FMAX / amax) (App. B.1 schedule).
-//  gemm_dma_kernel  batched block products M_r on FP8 operands: persistent,
-//                   256 x 128 tiles, a 3-stage LDS ring filled by direct
-//                   global-to-LDS loads; the codes are widened exactly to
-//                   bf16 and multiplied on the matrix cores
-//                   (v_mfma_f32_16x16x32_bf16) with fp32 accumulation, scale
-//                   epilogue.  gemm_tile_kernel covers inner lengths that are
-//                   not multiples of 128.
+//  (block products: fm_gemm.hip)
 //  recon_kernel     C_ij = sum_r w_{r,ij} M_r (eq. (1)) with the squared
 //                   error against the float64 reference reduced on chip.
 //  ref_f64_kernel   float64 reference product (App. F).
@@ -91,454 +85,22 @@ __global__ void scales_kernel(const uint32_t* amax, float* q, float* d, int n, f
   }
 }
 
-// ------------------------------------------------------ FP8 block GEMM
-// Workgroup tile 128 x 128, K step 128 bytes, 4 waves in 2 x 2, each wave
-// 64 x 64 = 4 x 4 tiles of 16 x 16.  FP8 operands are staged through
-// double-buffered LDS, rows of 128 bytes with the 16-byte chunk index
-// XOR-swizzled by a function of the row so that the fragment reads (16 rows
-// x one chunk per instruction) hit distinct banks.
-//
-// Lane (i, q) = (lane % 16, lane / 16) of a wave holds the 32 bytes
-// [32q, 32q + 32) of row i of a 16-row fragment, for both operands, so every
-// k of the step is paired with the same k of the other operand.
-//
-// Two arithmetics for the products:
-//   ACC_BF16 (default): every FP8 value is widened exactly to bf16
-//     (v_cvt_scalef32_pk_bf16_{fp8,bf8}, scale 1) and multiplied on the bf16
-//     matrix cores, v_mfma_f32_16x16x32_bf16: exact products, fp32 sums.
-//   ACC_FP8: v_mfma_scale_f32_16x16x128_f8f6f4 with unit scales, twice the
-//     rate; its sums of small products beside large ones are truncated
-//     (about 5e-5 relative on random FP8 data), so it is not the default.
-typedef int v8i __attribute__((ext_vector_type(8)));
-typedef float v4f __attribute__((ext_vector_type(4)));
-typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
-typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
-
-constexpr int GT = 128;  // tile rows / cols
-constexpr int GK = 128;  // K step in bytes
-
-__device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
-
-// Two FP8 codes (bytes 0-1 or 2-3 of w) -> two bf16 values, exactly.
-template <int FMT, bool HI>
-__device__ __forceinline__ v2bf widen2(int w) {
-  if constexpr (FMT == FM_E4M3) return __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI);
-  else return __builtin_amdgcn_cvt_scalef32_pk_bf16_bf8(w, 1.0f, HI);
+// One wave per row: lane l sums entries l, l+64, ... in order, then a fixed
+// butterfly over the lanes; the result does not depend on scheduling.
+__device__ __forceinline__ double wave_sum_f64(double s) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s = s + __shfl_xor(s, off, 64);
+  return s;
 }
 
-// 8 FP8 codes (two dwords, little-endian byte order) -> 8 bf16 values
-template <int FMT>
-__device__ __forceinline__ v8bf widen8(int d0, int d1) {
-  const v2bf a = widen2<FMT, false>(d0), b = widen2<FMT, true>(d0);
-  const v2bf c = widen2<FMT, false>(d1), d = widen2<FMT, true>(d1);
-  return (v8bf){a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
-}
-
-// Non-persistent variant: one 128 x 128 tile per workgroup, 4 waves.
-template <int FMT, int ACC>
-__global__ __launch_bounds__(kThreads) void gemm_tile_kernel(const uint8_t* __restrict__ Tq,
-                                                            const uint8_t* __restrict__ Sq,
-                                                            const float* __restrict__ dT,
-                                                            const float* __restrict__ dS,
-                                                            float* __restrict__ Mout, int Mb,
-                                                            int Nb, int Kb, int tiles_m,
-                                                            int tiles_n, int total) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2][2][GT * GK];
-  // Workgroups are dispatched round-robin over the 8 XCDs; remap so that
-  // each XCD works through a contiguous range of tiles (whole products),
-  // keeping a product's operand panels in one L2.
-  int w = blockIdx.x;
-  if ((total & 7) == 0) w = (w & 7) * (total >> 3) + (w >> 3);
-  const int tiles = tiles_m * tiles_n;
-  const int b = w / tiles;
-  const int t = w - b * tiles;
-  const int tm = t / tiles_n, tn = t - (t / tiles_n) * tiles_n;
-  const int m0 = tm * GT, n0 = tn * GT;
-  const uint8_t* Ab = Tq + (size_t)b * Mb * Kb;
-  const uint8_t* Bb = Sq + (size_t)b * Nb * Kb;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-
-  uint4 ra[4], rb[4];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + kThreads * i;
-      const int row = c >> 3, ch = c & 7;
-      const int kk = k0 + ch * 16;
-      ra[i] = make_uint4(0, 0, 0, 0);
-      rb[i] = make_uint4(0, 0, 0, 0);
-      if (kk < Kb) {
-        if (m0 + row < Mb) ra[i] = *reinterpret_cast<const uint4*>(Ab + (size_t)(m0 + row) * Kb + kk);
-        if (n0 + row < Nb) rb[i] = *reinterpret_cast<const uint4*>(Bb + (size_t)(n0 + row) * Kb + kk);
-      }
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + kThreads * i;
-      const int row = c >> 3, ch = c & 7;
-      const int o = row * GK + ((ch ^ swz(row)) << 4);
-      *reinterpret_cast<uint4*>(&lds[buf][0][o]) = ra[i];
-      *reinterpret_cast<uint4*>(&lds[buf][1][o]) = rb[i];
-    }
-  };
-
-  v4f acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
-
-  const int nk = (Kb + GK - 1) / GK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  const int q = lane >> 4, l16 = lane & 15;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * GK);
-    v8i fa[4], fb[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = wm * 64 + i * 16 + l16;
-      const uint8_t* base = &lds[cur][0][row * GK];
-      const uint4 lo = *reinterpret_cast<const uint4*>(base + (((2 * q) ^ swz(row)) << 4));
-      const uint4 hi = *reinterpret_cast<const uint4*>(base + (((2 * q + 1) ^ swz(row)) << 4));
-      fa[i] = (v8i){(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int row = wn * 64 + j * 16 + l16;
-      const uint8_t* base = &lds[cur][1][row * GK];
-      const uint4 lo = *reinterpret_cast<const uint4*>(base + (((2 * q) ^ swz(row)) << 4));
-      const uint4 hi = *reinterpret_cast<const uint4*>(base + (((2 * q + 1) ^ swz(row)) << 4));
-      fb[j] = (v8i){(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
-    }
-    if constexpr (ACC == 1) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(fa[i], fb[j], acc[i][j], FMT,
-                                                                       FMT, 0, 127, 0, 127);
-    } else {
-#pragma unroll
-      for (int sub = 0; sub < 4; ++sub) {
-        v8bf wa[4], wb[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) wa[i] = widen8<FMT>(fa[i][2 * sub], fa[i][2 * sub + 1]);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) wb[j] = widen8<FMT>(fb[j][2 * sub], fb[j][2 * sub + 1]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[i], wb[j], acc[i][j], 0, 0, 0);
-      }
-    }
-    if (kt + 1 < nk) lstore(cur ^ 1);
-    __syncthreads();
-  }
-
-  const float sT = dT[b], sS = dS[b];
-  float* Mo = Mout + (size_t)b * Mb * Nb;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = n0 + wn * 64 + j * 16 + l16;
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int row = m0 + wm * 64 + i * 16 + 4 * q + v;
-        if (row < Mb && col < Nb) {
-          float m = acc[i][j][v] * sT;
-          m = m * sS;
-          Mo[(size_t)row * Nb + col] = m;
-        }
-      }
-    }
-}
-
-// Pipelined persistent kernel (inner block length a multiple of 128):
-// workgroup tile 256 x 128, 8 waves of 64 x 64 (4 x 2), K step 128 bytes, a
-// ring of 3 LDS stages of 48 KB filled by direct global-to-LDS loads
-// (global_load_lds_dwordx4: lane L of a wave writes the 16 bytes it fetched
-// at M0 + 16 L, so the XOR swizzle is applied by choosing each lane's source
-// chunk).  Each workgroup walks a flattened sequence of (tile, K-step) pairs
-// with two pairs in flight while it computes a third, so the next tile's
-// loads run under the current tile's epilogue.  Rows beyond the operand
-// (ragged M or N) read row 0 instead: they only feed outputs never stored.
-//
-// The loads are issued from inline assembly and awaited with explicit vmcnt
-// counts: the compiler's own tracking of LDS DMA cannot tell the ring stages
-// apart and would drain every load in flight before each LDS read.  Vector
-// memory operations complete in issue order on this architecture, so "the
-// group for stage s is complete" is "at most n operations outstanding", n =
-// the number issued after that group (the next group's loads and any
-// epilogue stores); a lower bound on n is always safe.  The products are
-// accumulated transposed (operands swapped in the MFMA) so that each lane
-// holds 4 consecutive output columns and the epilogue writes 16-byte stores.
-constexpr int DBM = 256, DBN = 128, DROWS = DBM + DBN, DSTAGE = DROWS * GK, DNS = 3;
-constexpr int DNT = 512;                       // 8 waves
-constexpr int DLOADS = DROWS * GK / 1024 / 8;  // 1 KB wave-loads per wave per stage (= 6)
-constexpr int DSTORES = 16;                    // 16-byte stores per lane, interior tile
-
-__device__ __forceinline__ void dma16(const void* src, uint32_t lds_addr) {
-  // M0 written by SALU then read by an LDS-DMA load needs one wait state
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(src), "s"(lds_addr)
-               : "memory", "m0");
-}
-
-// s_waitcnt constraining only the vector-memory counter (gfx9 encoding:
-// vmcnt low bits [3:0], expcnt [6:4], lgkmcnt [11:8], vmcnt high bits [15:14])
-template <int N>
-__device__ __forceinline__ void wait_vm_n() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
-}
-__device__ __forceinline__ void wait_vm(int n) {
-  // n is uniform and one of few values; anything else waits for everything
-  if (n >= DLOADS + DSTORES) wait_vm_n<DLOADS + DSTORES>();
-  else if (n >= DSTORES) wait_vm_n<DSTORES>();
-  else if (n >= DLOADS) wait_vm_n<DLOADS>();
-  else wait_vm_n<0>();
-}
-#define FM_COMPILER_FENCE() asm volatile("" ::: "memory")
-
-template <int FMT, int ACC>
-__global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict__ Tq,
-                                                       const uint8_t* __restrict__ Sq,
-                                                       const float* __restrict__ dT,
-                                                       const float* __restrict__ dS,
-                                                       float* __restrict__ Mout, int Mb, int Nb,
-                                                       int Kb, int tiles_m, int tiles_n, int total) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[DNS * DSTAGE];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  const int q = lane >> 4, l16 = lane & 15;
-  const int tiles = tiles_m * tiles_n;
-  const int nk = Kb / GK;
-  const bool vec_store = (Nb & 3) == 0;
-
-  const int G = gridDim.x;
-  const bool xcd_split = (G & 7) == 0 && (total & 7) == 0;
-  const int t = xcd_split ? (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3) : blockIdx.x;
-  const int tstep = xcd_split ? (G >> 3) : G;
-  const int t_end = xcd_split ? ((blockIdx.x & 7) + 1) * (total >> 3) : total;
-  if (t >= t_end) return;
-  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)lds;
-
-  auto issue = [&](int tile, int kt, int buf) {
-    const int b = tile / tiles, tt = tile - b * tiles;
-    const int tmi = tt / tiles_n;
-    const int m0 = tmi * DBM, n0 = (tt - tmi * tiles_n) * DBN;
-    const uint8_t* Ab = Tq + (size_t)b * Mb * Kb + (size_t)kt * GK;
-    const uint8_t* Bb = Sq + (size_t)b * Nb * Kb + (size_t)kt * GK;
-#pragma unroll
-    for (int j = 0; j < DLOADS; ++j) {
-      const int r0 = (wave * DLOADS + j) * 8;  // first of the 8 rows this wave-load fills
-      const int r = r0 + (lane >> 3);
-      const int ch = (lane & 7) ^ swz(r);
-      const uint8_t* src;
-      if (r0 < DBM) {  // uniform: a wave-load never straddles the A/B boundary
-        int row = m0 + r;
-        row = row < Mb ? row : 0;
-        src = Ab + (size_t)row * Kb + ch * 16;
-      } else {
-        int row = n0 + r - DBM;
-        row = row < Nb ? row : 0;
-        src = Bb + (size_t)row * Kb + ch * 16;
-      }
-      dma16(src, lds_base + (uint32_t)(buf * DSTAGE + r0 * GK));
-    }
-  };
-  // Half h of a K step: lane (l16, q) of fragment i holds bytes
-  // [32q + 16h, 32q + 16h + 16) of its row, i.e. the k values of two 16x16x32
-  // sub-steps (2h and 2h + 1).
-  uint4 fa[2][4], fb[2][4];
-  auto read_half = [&](int h, int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = wm * 64 + i * 16 + l16;
-      fa[h][i] = *reinterpret_cast<const uint4*>(lds + buf * DSTAGE + row * GK +
-                                                 (((2 * q + h) ^ swz(row)) << 4));
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int row = DBM + wn * 64 + j * 16 + l16;
-      fb[h][j] = *reinterpret_cast<const uint4*>(lds + buf * DSTAGE + row * GK +
-                                                 (((2 * q + h) ^ swz(row)) << 4));
-    }
-  };
-
-  v4f acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
-
-  // acc[i][j] holds the transposed 16 x 16 product: element (4q+v, l16) is
-  // output row i*16 + l16, column j*16 + 4q + v of the wave's 64 x 64 block
-  auto compute_half = [&](int h) {
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      if constexpr (ACC == 1) {
-        long xa[4], xb[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          xa[i] = sub ? (long)(((unsigned long)(uint32_t)fa[h][i].w << 32) | (uint32_t)fa[h][i].z)
-                      : (long)(((unsigned long)(uint32_t)fa[h][i].y << 32) | (uint32_t)fa[h][i].x);
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          xb[j] = sub ? (long)(((unsigned long)(uint32_t)fb[h][j].w << 32) | (uint32_t)fb[h][j].z)
-                      : (long)(((unsigned long)(uint32_t)fb[h][j].y << 32) | (uint32_t)fb[h][j].x);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            if constexpr (FMT == FM_E4M3)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_fp8_fp8(xb[j], xa[i], acc[i][j], 0, 0, 0);
-            else
-              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf8_bf8(xb[j], xa[i], acc[i][j], 0, 0, 0);
-          }
-      } else {
-        v8bf wa[4], wb[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          wa[i] = sub ? widen8<FMT>((int)fa[h][i].z, (int)fa[h][i].w) : widen8<FMT>((int)fa[h][i].x, (int)fa[h][i].y);
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          wb[j] = sub ? widen8<FMT>((int)fb[h][j].z, (int)fb[h][j].w) : widen8<FMT>((int)fb[h][j].x, (int)fb[h][j].y);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb[j], wa[i], acc[i][j], 0, 0, 0);
-      }
-    }
-  };
-  auto epilogue = [&](int tile) -> int {  // returns the number of stores counted
-    const int b = tile / tiles, tt = tile - b * tiles;
-    const int tmi = tt / tiles_n;
-    const int m0 = tmi * DBM, n0 = (tt - tmi * tiles_n) * DBN;
-    const float sT = dT[b], sS = dS[b];
-    float* Mo = Mout + (size_t)b * Mb * Nb;
-    const int r_base = m0 + wm * 64 + l16, c_base = n0 + wn * 64 + 4 * q;
-    int counted = 0;
-    if (vec_store && m0 + DBM <= Mb && n0 + DBN <= Nb) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float* prow = Mo + (size_t)(r_base + i * 16) * Nb + c_base;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float4 o;
-          o.x = (acc[i][j][0] * sT) * sS;
-          o.y = (acc[i][j][1] * sT) * sS;
-          o.z = (acc[i][j][2] * sT) * sS;
-          o.w = (acc[i][j][3] * sT) * sS;
-          *reinterpret_cast<float4*>(prow + j * 16) = o;
-        }
-      }
-      counted = DSTORES;
-    } else {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = r_base + i * 16;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int col = c_base + j * 16 + v;
-            if (row < Mb && col < Nb) Mo[(size_t)row * Nb + col] = (acc[i][j][v] * sT) * sS;
-          }
-      }
-      // a data-dependent number of stores: counted as none (a lower bound)
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
-    return counted;
-  };
-
-  // Sequence of (tile, K-step) pairs p_0, p_1, ...; p_s lives in LDS buffer
-  // s mod 3.  Iteration s: read the high half of p_s while the matrix cores
-  // work on its low half; wait until p_{s+1} has landed and every wave is done
-  // reading p_s; start the loads of p_{s+3} into the buffer of p_s; read the
-  // low half of p_{s+1} while the matrix cores work on the high half of p_s.
-  auto advance = [&](int& tt, int& kk) {
-    if (++kk == nk) {
-      kk = 0;
-      tt += tstep;
-    }
-  };
-  int t1 = t, k1 = 0;  // p_{s+1}
-  advance(t1, k1);
-  int t2 = t1, k2 = k1;  // p_{s+2}
-  advance(t2, k2);
-  int t3 = t2, k3 = k2;  // p_{s+3}
-  advance(t3, k3);
-  int ct = t, ck = 0;  // p_s
-  issue(ct, ck, 0);
-  int after1 = 0;  // vector-memory operations issued after the group of p_{s+1}
-  if (t1 < t_end) issue(t1, k1, 1);
-  if (t2 < t_end) {
-    issue(t2, k2, 2);
-    after1 = DLOADS;
-  }
-  wait_vm(t1 < t_end ? after1 + DLOADS : 0);  // p_0 has landed
-  FM_COMPILER_FENCE();
-  __builtin_amdgcn_s_barrier();
-  FM_COMPILER_FENCE();
-  read_half(0, 0);
-  int cb = 0;  // buffer of p_s
-  while (true) {
-    read_half(1, cb);
-    compute_half(0);
-    wait_vm(after1);                     // p_{s+1} has landed (this wave's share)
-    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of p_s are done
-    FM_COMPILER_FENCE();
-    __builtin_amdgcn_s_barrier();
-    FM_COMPILER_FENCE();
-    const int nb = cb == 2 ? 0 : cb + 1;
-    int after2 = 0;  // operations issued after the group of p_{s+2}
-    if (t3 < t_end) {
-      issue(t3, k3, cb);
-      after2 = DLOADS;
-    }
-    FM_COMPILER_FENCE();
-    const bool more = t1 < t_end;
-    if (more) read_half(0, nb);
-    compute_half(1);
-    if (ck == nk - 1) after2 += epilogue(ct);
-    FM_COMPILER_FENCE();
-    if (!more) break;
-    ct = t1;
-    ck = k1;
-    t1 = t2;
-    k1 = k2;
-    t2 = t3;
-    k2 = k3;
-    advance(t3, k3);
-    after1 = after2;
-    cb = nb;
-  }
-}
-
-__global__ void reduce_rows_kernel(const double* partial, int nblk, int G, double* out) {
-  const int g = blockIdx.x * blockDim.x + threadIdx.x;
+__global__ __launch_bounds__(64) void reduce_rows_kernel(const double* partial, int nblk, int G,
+                                                          double* out) {
+  const int g = blockIdx.x, lane = threadIdx.x;
   if (g >= G) return;
   double s = 0.0;
-  for (int b = 0; b < nblk; ++b) s = s + partial[(size_t)g * nblk + b];
-  out[g] = s;
+  for (int b = lane; b < nblk; b += 64) s = s + partial[(size_t)g * nblk + b];
+  s = wave_sum_f64(s);
+  if (lane == 0) out[g] = s;
 }
 
 // ----------------------------------------------------- float64 reference
@@ -624,17 +186,25 @@ __global__ __launch_bounds__(kThreads) void error_stats_kernel(const float* __re
   }
 }
 
-__global__ void error_finalize_kernel(const double* partial, int nblk, double* out3) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+__global__ __launch_bounds__(64) void error_finalize_kernel(const double* partial, int nblk,
+                                                             double* out3) {
+  if (blockIdx.x != 0) return;
+  const int lane = threadIdx.x;
   double e = 0.0, r = 0.0, m = 0.0;
-  for (int b = 0; b < nblk; ++b) {
+  for (int b = lane; b < nblk; b += 64) {
     e = e + partial[3 * b];
     r = r + partial[3 * b + 1];
     m = fmax(m, partial[3 * b + 2]);
   }
-  out3[0] = e;
-  out3[1] = r;
-  out3[2] = m;
+  e = wave_sum_f64(e);
+  r = wave_sum_f64(r);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off, 64));
+  if (lane == 0) {
+    out3[0] = e;
+    out3[1] = r;
+    out3[2] = m;
+  }
 }
 
 
@@ -674,50 +244,6 @@ int launch_scales(const uint32_t* amax, float* q, float* d, int n, int fmt, uint
   return launched("scales_kernel");
 }
 
-namespace {
-int g_block_product_arith = FM_ACC_BF16;
-}
-
-int set_block_product_arith(int a) {
-  if (a != FM_ACC_BF16 && a != FM_ACC_FP8) return fail(FM_E_ARG, "unknown product arithmetic");
-  g_block_product_arith = a;
-  return FM_OK;
-}
-
-int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
-                      float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, hipStream_t st) {
-  const bool fp8acc = g_block_product_arith == FM_ACC_FP8;
-  if (Kb % GK == 0) {
-    // pipelined persistent kernel: one 144 KB-LDS workgroup per CU
-    const int tm = (Mb + DBM - 1) / DBM, tn = (Nb + DBN - 1) / DBN;
-    const long long total = (long long)batch * tm * tn;
-    if (total > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many GEMM tiles in one launch");
-    const int T = (int)total;
-    const int grid = (int)std::min<long long>(total, 256);
-    if (fmt == FM_E4M3) {
-      if (fp8acc) gemm_dma_kernel<FM_E4M3, 1><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-      else gemm_dma_kernel<FM_E4M3, 0><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-    } else {
-      if (fp8acc) gemm_dma_kernel<FM_E5M2, 1><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-      else gemm_dma_kernel<FM_E5M2, 0><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-    }
-    return launched("gemm_dma_kernel");
-  }
-  // inner length a multiple of 16 only: one 128 x 128 tile per workgroup
-  const int tm = (Mb + GT - 1) / GT, tn = (Nb + GT - 1) / GT;
-  const long long total = (long long)batch * tm * tn;
-  if (total > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many GEMM tiles in one launch");
-  const int T = (int)total;
-  if (fmt == FM_E4M3) {
-    if (fp8acc) gemm_tile_kernel<FM_E4M3, 1><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-    else gemm_tile_kernel<FM_E4M3, 0><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-  } else {
-    if (fp8acc) gemm_tile_kernel<FM_E5M2, 1><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-    else gemm_tile_kernel<FM_E5M2, 0><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-  }
-  return launched("gemm_tile_kernel");
-}
-
 int recon_blocks(const ReconArgs& a) {
   // one position group per thread (the static kernels assume it); positions
   // counted at the width both kernel kinds use: 4 for grids of at most 16
@@ -742,7 +268,8 @@ int launch_recon(const ReconArgs& a, int pattern, hipStream_t st) {
 }
 
 int launch_reduce_rows(const double* partial, int nblk, int G, double* out, hipStream_t st) {
-  reduce_rows_kernel<<<(G + 63) / 64, 64, 0, st>>>(partial, nblk, G, out);
+  if (G <= 0) return FM_OK;
+  reduce_rows_kernel<<<G, 64, 0, st>>>(partial, nblk, G, out);
   return launched("reduce_rows_kernel");
 }
 

@@ -320,10 +320,20 @@ def status(ws, stream=None):
     _check(lib.fm_status(_dptr(ws), ws.numel(), _stream(stream)))
 
 
+_arith = ACC_BF16
+
+
 def set_block_product_arithmetic(acc: int):
     """ACC_BF16 (exact products, fp32 sums; default) or ACC_FP8 (FP8 matrix
     instructions)."""
+    global _arith
     _check(lib.fm_set_block_product_arithmetic(acc))
+    _arith = acc
+
+
+def get_block_product_arithmetic() -> int:
+    """The arithmetic last selected through set_block_product_arithmetic."""
+    return _arith
 
 
 def timing_enable(on: bool = True):
