@@ -16,9 +16,11 @@ paper leaves the precision free):
     float64 reference; error = relative Frobenius norm (App. B.1);
   * orbit statistics with the conventions of App. B.2 (upper median,
     spread = largest / smallest, count above 2).
-Readings where the paper is silent (one scale per block-sum tensor, fmaf
-combination order, exact block products rounded once) are stated at each
-function in fm_oracle.c.
+Readings where the paper is silent (one scale per block-sum tensor by
+default, fmaf combination order, exact block products rounded once) are
+stated at each function in fm_oracle.c; the finer granularity of App. B.1's
+synthetic matrices (one scale per row of A's block sums and per column of
+B's) is the SCALE_ROWCOL mode.
 
 Every function is parity-pinned by tests/test_oracle_*.py.
 """
@@ -35,6 +37,10 @@ from .schemes import Scheme
 
 E4M3, E5M2 = 0, 1
 FMT = {"e4m3": E4M3, "e5m2": E5M2}
+# scale granularity: one scale per block-sum tensor, or (App. B.1's
+# synthetic form) one per row of each A-side and per column of each B-side
+# block sum
+SCALE_TENSOR, SCALE_ROWCOL = 0, 1
 
 _lib = None
 
@@ -63,6 +69,11 @@ def lib():
             "orc_error_sums": (None, [p, p, i64, p, p]),
             "orc_lowp_matmul": (i, [p, p, i, i, i, i, i, i, i, p, p, p, i, p, p, p, p, p, p]),
             "orc_form_operands": (None, [p, i, i, i, i, i, p, i, p, p]),
+            "orc_quantize_rows": (None, [p, i, i, i, p, p]),
+            "orc_quantize_cols": (None, [p, i, i, i, p, p]),
+            "orc_block_product_rc": (None, [p, p, p, p, i, i, i, i, p]),
+            "orc_lowp_matmul_sm": (i, [p, p, i, i, i, i, i, i, i, p, p, p, i, i, p, p, p, p, p, p]),
+            "orc_form_operands_sm": (None, [p, i, i, i, i, i, p, i, i, i, p, p]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -125,16 +136,43 @@ def quantize_tensor(T, fmt: int = E4M3):
     return codes, np.float32(d), np.float32(r.value)
 
 
-def form_operands(X, gr: int, gc: int, coef, fmt: int = E4M3):
+def quantize_rows(T, fmt: int = E4M3):
+    """(codes, d): one scale per row of T (App. B.1, block sums of A)."""
+    T = _f32(T)
+    rows, cols = T.shape
+    codes = np.empty(T.shape, np.uint8)
+    d = np.empty(rows, np.float32)
+    lib().orc_quantize_rows(_ptr(T), rows, cols, fmt, _ptr(codes), _ptr(d))
+    return codes, d
+
+
+def quantize_cols(T, fmt: int = E4M3):
+    """(codes, d): one scale per column of T (App. B.1, block sums of B)."""
+    T = _f32(T)
+    rows, cols = T.shape
+    codes = np.empty(T.shape, np.uint8)
+    d = np.empty(cols, np.float32)
+    lib().orc_quantize_cols(_ptr(T), rows, cols, fmt, _ptr(codes), _ptr(d))
+    return codes, d
+
+
+def form_operands(X, gr: int, gc: int, coef, fmt: int = E4M3, scale_mode: int = SCALE_TENSOR,
+                  side: int = 0):
     """Block sums of one operand for every product r, quantized.
-    Returns codes (R, rows/gr, cols/gc) in X's orientation and scales d (R,)."""
+    Returns codes (R, rows/gr, cols/gc) in X's orientation and scales d: (R,)
+    per tensor, or with SCALE_ROWCOL (R, rows/gr) for side 0 (A, per row)
+    and (R, cols/gc) for side 1 (B, per column)."""
     X = _f32(X)
     coef = _f32(coef)
     R = coef.shape[0]
     rows, cols = X.shape
     codes = np.empty((R, rows // gr, cols // gc), np.uint8)
-    d = np.empty(R, np.float32)
-    lib().orc_form_operands(_ptr(X), rows, cols, gr, gc, R, _ptr(coef), fmt, _ptr(codes), _ptr(d))
+    if scale_mode == SCALE_TENSOR:
+        d = np.empty(R, np.float32)
+    else:
+        d = np.empty((R, rows // gr if side == 0 else cols // gc), np.float32)
+    lib().orc_form_operands_sm(_ptr(X), rows, cols, gr, gc, R, _ptr(coef), fmt, scale_mode, side,
+                               _ptr(codes), _ptr(d))
     return codes, d
 
 
@@ -146,6 +184,21 @@ def block_product(Tq, Sq, dT, dS, fmt: int = E4M3) -> np.ndarray:
     assert bk == bk2
     out = np.empty((br, bc), np.float32)
     lib().orc_block_product(_ptr(Tq), _ptr(Sq), float(dT), float(dS), br, bc, bk, fmt, _ptr(out))
+    return out
+
+
+def block_product_rc(Tq, Sq, dT, dS, fmt: int = E4M3) -> np.ndarray:
+    """Block product with a scale per row of Tq (dT, br values) and per
+    column of Sq (dS, bc values)."""
+    Tq = np.ascontiguousarray(Tq, np.uint8)
+    Sq = np.ascontiguousarray(Sq, np.uint8)
+    br, bk = Tq.shape
+    bk2, bc = Sq.shape
+    assert bk == bk2
+    dT, dS = _f32(dT), _f32(dS)
+    assert dT.size == br and dS.size == bc
+    out = np.empty((br, bc), np.float32)
+    lib().orc_block_product_rc(_ptr(Tq), _ptr(Sq), _ptr(dT), _ptr(dS), br, bc, bk, fmt, _ptr(out))
     return out
 
 
@@ -201,10 +254,12 @@ def rel_fro(C, Cref) -> float:
 # --------------------------------------------------------------------------
 # Whole schedule for one scheme
 # --------------------------------------------------------------------------
-def lowp_matmul(A, B, scheme_f32, dims, fmt: int = E4M3, keep: bool = False):
+def lowp_matmul(A, B, scheme_f32, dims, fmt: int = E4M3, keep: bool = False,
+                scale_mode: int = SCALE_TENSOR):
     """FP8 evaluation of one scheme (fp32 coefficient tables U, V, W of the
     flattened scheme, dims = (m, k, n, R)).  Returns C, or with keep=True a
-    dict with C, Tq (R, Mb, Kb), dT, Sq (R, Kb, Nb), dS and Mr (R, Mb, Nb)."""
+    dict with C, Tq (R, Mb, Kb), dT, Sq (R, Kb, Nb), dS and Mr (R, Mb, Nb);
+    dT and dS are (R,) per tensor or (R, Mb) and (R, Nb) with SCALE_ROWCOL."""
     U, V, W = (_f32(t) for t in scheme_f32)
     gm, gk, gn, R = dims
     A, B = _f32(A), _f32(B)
@@ -217,14 +272,15 @@ def lowp_matmul(A, B, scheme_f32, dims, fmt: int = E4M3, keep: bool = False):
     if keep:
         Tq = np.empty((R, br, bk), np.uint8)
         Sq = np.empty((R, bk, bc), np.uint8)
-        dT = np.empty(R, np.float32)
-        dS = np.empty(R, np.float32)
+        rc_mode = scale_mode == SCALE_ROWCOL
+        dT = np.empty((R, br) if rc_mode else R, np.float32)
+        dS = np.empty((R, bc) if rc_mode else R, np.float32)
         Mr = np.empty((R, br, bc), np.float32)
         args = [_ptr(Tq), _ptr(dT), _ptr(Sq), _ptr(dS), _ptr(Mr)]
     else:
         args = [None] * 5
-    rc = lib().orc_lowp_matmul(_ptr(A), _ptr(B), M, N, K, gm, gk, gn, R, _ptr(U), _ptr(V),
-                               _ptr(W), fmt, _ptr(C), *args)
+    rc = lib().orc_lowp_matmul_sm(_ptr(A), _ptr(B), M, N, K, gm, gk, gn, R, _ptr(U), _ptr(V),
+                                  _ptr(W), fmt, scale_mode, _ptr(C), *args)
     if rc != 0:
         raise ValueError("orc_lowp_matmul failed")
     if keep:
@@ -237,12 +293,12 @@ def flatten_f32(s: Scheme):
     return scheme_ops.to_f32(s), (s.m, s.k, s.n, s.R)
 
 
-def classical_fp8(A, B, fmt: int = E4M3):
+def classical_fp8(A, B, fmt: int = E4M3, scale_mode: int = SCALE_TENSOR):
     """Classical FP8 baseline: the plain product (R = 1) with one scale per
-    operand, same rule as the block sums."""
+    operand (or per row of A and column of B), same rule as the block sums."""
     s = schemes.classical(1, 1, 1)
     tabs, dims = flatten_f32(s)
-    return lowp_matmul(A, B, tabs, dims, fmt)
+    return lowp_matmul(A, B, tabs, dims, fmt, scale_mode=scale_mode)
 
 
 def orbit_stats(ratios, identity_value=None) -> dict:

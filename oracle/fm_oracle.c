@@ -15,9 +15,12 @@
  *     combination carried out in fp32;
  *   - the error measure of App. B / App. F: relative error in the Frobenius
  *     norm against a float64 reference.
+ *   - the finer scale granularity of App. B.1's synthetic matrices: one scale
+ *     per row of each block sum of A and per column of each block sum of B.
  * Choices the paper leaves open (combination order, one scale per whole
- * block-sum tensor, exact block-product accumulation rounded once to fp32)
- * are the readings listed in the design notes; each function states its own.
+ * block-sum tensor by default, exact block-product accumulation rounded once
+ * to fp32) are the readings listed in the design notes; each function states
+ * its own.
  *
  * Arithmetic rules, so that every step can be checked by eye:
  *   - fp32 steps use C float arithmetic (SSE, round-to-nearest-even,
@@ -153,16 +156,21 @@ void orc_block_sum(const float* X, int rows, int cols, int gr, int gc,
 /* one correctly rounded fp32 division.  Codes: encode(x * r), one fp32      */
 /* multiplication then FP8 rounding.  Returns d, writes r to *r_out.         */
 /* ------------------------------------------------------------------------ */
+/* The scale rule for one group of values with largest magnitude amax. */
+static float scale_from_amax(float amax, int fmt, float* r_out) {
+  float fmax = (float)fmt_of(fmt).max_finite;
+  if (amax == 0.0f) { *r_out = 1.0f; return 1.0f; }
+  *r_out = fmax / amax;
+  return amax / fmax;
+}
+
 float orc_tensor_scale(const float* T, int64_t n, int fmt, float* r_out) {
   float amax = 0.0f;
   for (int64_t i = 0; i < n; ++i) {
     float a = fabsf(T[i]);
     if (a > amax) amax = a;
   }
-  float fmax = (float)fmt_of(fmt).max_finite;
-  if (amax == 0.0f) { *r_out = 1.0f; return 1.0f; }
-  *r_out = fmax / amax;
-  return amax / fmax;
+  return scale_from_amax(amax, fmt, r_out);
 }
 
 float orc_quantize_tensor(const float* T, int64_t n, int fmt, uint8_t* codes) {
@@ -173,6 +181,35 @@ float orc_quantize_tensor(const float* T, int64_t n, int fmt, uint8_t* codes) {
     codes[i] = orc_fp8_encode(y, fmt);
   }
   return d;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Finer scale granularity (App. B.1, the synthetic-matrix form): one scale  */
+/* for every row of a block sum of A and for every column of a block sum of  */
+/* B, each with the same rule as a whole tensor.  T is rows x cols           */
+/* row-major (B's block sums in B's orientation, bk x bc).                   */
+/* ------------------------------------------------------------------------ */
+void orc_quantize_rows(const float* T, int rows, int cols, int fmt, uint8_t* codes, float* d) {
+  for (int x = 0; x < rows; ++x) {
+    const float* t = T + (int64_t)x * cols;
+    float r;
+    d[x] = orc_tensor_scale(t, cols, fmt, &r);
+    for (int y = 0; y < cols; ++y) codes[(int64_t)x * cols + y] = orc_fp8_encode(t[y] * r, fmt);
+  }
+}
+
+void orc_quantize_cols(const float* T, int rows, int cols, int fmt, uint8_t* codes, float* d) {
+  for (int z = 0; z < cols; ++z) {
+    float amax = 0.0f;
+    for (int y = 0; y < rows; ++y) {
+      float a = fabsf(T[(int64_t)y * cols + z]);
+      if (a > amax) amax = a;
+    }
+    float r;
+    d[z] = scale_from_amax(amax, fmt, &r);
+    for (int y = 0; y < rows; ++y)
+      codes[(int64_t)y * cols + z] = orc_fp8_encode(T[(int64_t)y * cols + z] * r, fmt);
+  }
 }
 
 /* ------------------------------------------------------------------------ */
@@ -221,6 +258,20 @@ void orc_block_product(const uint8_t* Tq, const uint8_t* Sq, float dT, float dS,
   }
   free(ti);
   free(sti);
+}
+
+/* The block product with a scale per row of Tq (dT[x]) and per column of   */
+/* Sq (dS[z]): M[x][z] = (exact sum rounded once * dT[x]) * dS[z].           */
+void orc_block_product_rc(const uint8_t* Tq, const uint8_t* Sq, const float* dT,
+                          const float* dS, int br, int bc, int bk, int fmt, float* Mout) {
+  orc_block_product(Tq, Sq, 1.0f, 1.0f, br, bc, bk, fmt, Mout); /* exact sums, x1 x1 */
+  for (int x = 0; x < br; ++x)
+    for (int z = 0; z < bc; ++z) {
+      float m = Mout[(int64_t)x * bc + z];
+      m = m * dT[x];
+      m = m * dS[z];
+      Mout[(int64_t)x * bc + z] = m;
+    }
 }
 
 /* The same block product at selected positions (xs[t], zs[t]) only. */
@@ -347,6 +398,49 @@ int orc_lowp_matmul(const float* A, const float* B, int M, int N, int K,
   return 0;
 }
 
+/* The whole schedule with a choice of scale granularity: scale_mode 0 is   */
+/* one scale per block-sum tensor (orc_lowp_matmul), 1 is one per row of     */
+/* each A-side block sum and one per column of each B-side block sum.        */
+/* Scale outputs hold R values (mode 0) or R x br and R x bc (mode 1).       */
+int orc_lowp_matmul_sm(const float* A, const float* B, int M, int N, int K,
+                       int gm, int gk, int gn, int R, const float* U,
+                       const float* V, const float* W, int fmt, int scale_mode,
+                       float* C, uint8_t* Tq_out, float* dT_out, uint8_t* Sq_out,
+                       float* dS_out, float* Mr_out) {
+  if (scale_mode == 0)
+    return orc_lowp_matmul(A, B, M, N, K, gm, gk, gn, R, U, V, W, fmt, C, Tq_out, dT_out,
+                           Sq_out, dS_out, Mr_out);
+  if (scale_mode != 1) return -2;
+  if (M % gm || K % gk || N % gn) return -1;
+  int br = M / gm, bk = K / gk, bc = N / gn;
+  int64_t tsz = (int64_t)br * bk, ssz = (int64_t)bk * bc, msz = (int64_t)br * bc;
+  float* T = (float*)malloc(sizeof(float) * (size_t)(tsz > ssz ? tsz : ssz));
+  uint8_t* tq = (uint8_t*)malloc((size_t)tsz);
+  uint8_t* sq = (uint8_t*)malloc((size_t)ssz);
+  float* dT = (float*)malloc(sizeof(float) * (size_t)br);
+  float* dS = (float*)malloc(sizeof(float) * (size_t)bc);
+  float* Mr = Mr_out ? Mr_out : (float*)malloc(sizeof(float) * (size_t)(msz * R));
+  for (int r = 0; r < R; ++r) {
+    orc_block_sum(A, M, K, gm, gk, U + (int64_t)r * gm * gk, T);
+    orc_quantize_rows(T, br, bk, fmt, tq, dT);
+    orc_block_sum(B, K, N, gk, gn, V + (int64_t)r * gk * gn, T);
+    orc_quantize_cols(T, bk, bc, fmt, sq, dS);
+    if (Tq_out) memcpy(Tq_out + r * tsz, tq, (size_t)tsz);
+    if (Sq_out) memcpy(Sq_out + r * ssz, sq, (size_t)ssz);
+    if (dT_out) memcpy(dT_out + (int64_t)r * br, dT, sizeof(float) * (size_t)br);
+    if (dS_out) memcpy(dS_out + (int64_t)r * bc, dS, sizeof(float) * (size_t)bc);
+    orc_block_product_rc(tq, sq, dT, dS, br, bc, bk, fmt, Mr + r * msz);
+  }
+  orc_reconstruct(Mr, W, R, gm, gn, br, bc, C);
+  if (!Mr_out) free(Mr);
+  free(T);
+  free(tq);
+  free(sq);
+  free(dT);
+  free(dS);
+  return 0;
+}
+
 /* Quantized operands only (block sums, scales and codes) for one side:     */
 /* X rows x cols, grid gr x gc, R coefficient rows.  codes: R x (rows/gr) x */
 /* (cols/gc) in X's orientation; d: R scales.                               */
@@ -357,6 +451,29 @@ void orc_form_operands(const float* X, int rows, int cols, int gr, int gc, int R
   for (int r = 0; r < R; ++r) {
     orc_block_sum(X, rows, cols, gr, gc, coef + (int64_t)r * gr * gc, T);
     d[r] = orc_quantize_tensor(T, sz, fmt, codes + r * sz);
+  }
+  free(T);
+}
+
+/* The same with a choice of scale granularity: scale_mode 1 gives one scale */
+/* per row of each block sum (side 0, A) or per column (side 1, B); d holds  */
+/* R x (rows/gr) or R x (cols/gc) values.                                    */
+void orc_form_operands_sm(const float* X, int rows, int cols, int gr, int gc, int R,
+                          const float* coef, int fmt, int scale_mode, int side,
+                          uint8_t* codes, float* d) {
+  if (scale_mode == 0) {
+    orc_form_operands(X, rows, cols, gr, gc, R, coef, fmt, codes, d);
+    return;
+  }
+  int br = rows / gr, bc = cols / gc;
+  int64_t sz = (int64_t)br * bc;
+  float* T = (float*)malloc(sizeof(float) * (size_t)sz);
+  for (int r = 0; r < R; ++r) {
+    orc_block_sum(X, rows, cols, gr, gc, coef + (int64_t)r * gr * gc, T);
+    if (side == 0)
+      orc_quantize_rows(T, br, bc, fmt, codes + r * sz, d + (int64_t)r * br);
+    else
+      orc_quantize_cols(T, br, bc, fmt, codes + r * sz, d + (int64_t)r * bc);
   }
   free(T);
 }

@@ -227,11 +227,13 @@ def test_block_product_equals_library_matmul_of_decoded_codes():
     assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
 
 
-def brute_force_schedule(A, B, U, V, W, dims, fmt):
+def brute_force_schedule(A, B, U, V, W, dims, fmt, rowcol=False):
     """The whole FP8 schedule in exact rationals, written independently:
-    ascending row-major fmaf block sums from +0, tensor amax, correctly
-    rounded scales, nearest-code rounding, exact block products rounded
-    once and scaled by two fp32 multiplications, fmaf reconstruction."""
+    ascending row-major fmaf block sums from +0, tensor amax (or, with
+    rowcol, the amax of each row of A's block sums and of each column of
+    B's, App. B.1), correctly rounded scales, nearest-code rounding, exact
+    block products rounded once and scaled by two fp32 multiplications,
+    fmaf reconstruction."""
     gm, gk, gn, R = dims
     M, K = A.shape
     N = B.shape[1]
@@ -239,7 +241,14 @@ def brute_force_schedule(A, B, U, V, W, dims, fmt):
     fmax = Fraction(448 if fmt == E4M3 else 57344)
     codes_val = {c: Fraction(float(v)) for c, v in enumerate(oracle.fp8_decode(np.arange(256, dtype=np.uint8), fmt)) if np.isfinite(v)}
 
-    def form(X, gr, gc, coef, rows, cols):
+    def scale(values):
+        amax = max(abs(Fraction(float(t))) for t in values)
+        if amax == 0:
+            return np.float32(1), np.float32(1)
+        return round_to_f32(fmax / amax), round_to_f32(amax / fmax)
+
+    def form(X, gr, gc, coef, rows, cols, per=None):
+        # per: None (one scale), "row" or "col"
         T = np.zeros((rows, cols), np.float32)
         for x in range(rows):
             for y in range(cols):
@@ -251,29 +260,36 @@ def brute_force_schedule(A, B, U, V, W, dims, fmt):
                             continue
                         acc = fmaf_exact(u, X[p * rows + x, q * cols + y], acc)
                 T[x, y] = acc
-        amax = max(abs(Fraction(float(t))) for t in T.reshape(-1))
-        if amax == 0:
-            r, d = np.float32(1), np.float32(1)
+        if per is None:
+            r, d = scale(T.reshape(-1))
+            R_ = np.full((rows, cols), r, np.float32)
+        elif per == "row":
+            rd = [scale(T[x]) for x in range(rows)]
+            R_ = np.array([[rd[x][0]] * cols for x in range(rows)], np.float32)
+            d = np.array([rd[x][1] for x in range(rows)], np.float32)
         else:
-            r = round_to_f32(fmax / amax)
-            d = round_to_f32(amax / fmax)
+            rd = [scale(T[:, y]) for y in range(cols)]
+            R_ = np.array([[rd[y][0] for y in range(cols)] for _ in range(rows)], np.float32)
+            d = np.array([rd[y][1] for y in range(cols)], np.float32)
         Q = np.zeros((rows, cols), np.uint8)
         for x in range(rows):
             for y in range(cols):
-                Q[x, y] = nearest_code(np.float32(T[x, y] * r), fmt)
+                Q[x, y] = nearest_code(np.float32(T[x, y] * R_[x, y]), fmt)
         return Q, d
 
     Mr = []
     Tqs, Sqs, dTs, dSs = [], [], [], []
     for r in range(R):
-        Tq, dT = form(A, gm, gk, U[r], br, bk)
-        Sq, dS = form(B, gk, gn, V[r], bk, bc)
+        Tq, dT = form(A, gm, gk, U[r], br, bk, "row" if rowcol else None)
+        Sq, dS = form(B, gk, gn, V[r], bk, bc, "col" if rowcol else None)
         P = np.zeros((br, bc), np.float32)
         for x in range(br):
             for z in range(bc):
                 q = sum(codes_val[int(Tq[x, y])] * codes_val[int(Sq[y, z])] for y in range(bk))
                 m = round_to_f32(q)
-                P[x, z] = np.float32(np.float32(m * dT) * dS)
+                st = dT[x] if rowcol else dT
+                ss = dS[z] if rowcol else dS
+                P[x, z] = np.float32(np.float32(m * st) * ss)
         Mr.append(P)
         Tqs.append(Tq), Sqs.append(Sq), dTs.append(dT), dSs.append(dS)
     C = np.zeros((M, N), np.float32)
@@ -305,6 +321,30 @@ def test_whole_schedule_matches_exact_brute_force(fmt, which):
     tabs, dims = oracle.flatten_f32(s)
     got = oracle.lowp_matmul(A, B, tabs, dims, fmt, keep=True)
     want = brute_force_schedule(A, B, *tabs, dims, fmt)
+    for key in ("Tq", "Sq"):
+        assert np.array_equal(got[key], want[key]), key
+    for key in ("dT", "dS", "Mr", "C"):
+        assert np.array_equal(np.asarray(got[key]).view(np.uint32),
+                              np.asarray(want[key], np.float32).view(np.uint32)), key
+
+
+@pytest.mark.parametrize("fmt", [E4M3, E5M2])
+@pytest.mark.parametrize("which", ["identity", "gl"])
+def test_row_column_scales_match_exact_brute_force(fmt, which):
+    """App. B.1's finer granularity (a scale per row of A's block sums and
+    per column of B's) against the exact-rational schedule."""
+    rng = np.random.default_rng(12)
+    A = rng.standard_normal((4, 6)).astype(np.float32)
+    B = rng.standard_normal((6, 8)).astype(np.float32)
+    A[1] *= 300.0  # rows of very different magnitude
+    s = schemes.strassen()
+    if which == "gl":
+        P, Q, S = sy.gl_gauges(2, 2, 2, 1, seed=6)[0]
+        s = so.gauge(s, P, Q, S)
+    tabs, dims = oracle.flatten_f32(s)
+    got = oracle.lowp_matmul(A, B, tabs, dims, fmt, keep=True, scale_mode=oracle.SCALE_ROWCOL)
+    want = brute_force_schedule(A, B, *tabs, dims, fmt, rowcol=True)
+    assert got["dT"].shape == (7, 2) and got["dS"].shape == (7, 4)
     for key in ("Tq", "Sq"):
         assert np.array_equal(got[key], want[key]), key
     for key in ("dT", "dS", "Mr", "C"):

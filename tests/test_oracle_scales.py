@@ -1,0 +1,187 @@
+"""Pins of the finer scale granularity on the CPU oracle: one scale per row
+of each block sum of A and per column of each block sum of B, the form the
+paper uses on synthetic matrices (App. B.1) and, on the input side, the form
+its models' schedule reduces to when a block-sum row is one 128-entry group.
+
+What pins it (besides the exact-rational brute force in
+test_oracle_numerics.py):
+  * App. C.3's row map: replacing row 40 of a 48-row input under two-level
+    Strassen changes output rows 4, 16, 28 and 40 and no other; under the
+    classical product only row 40;
+  * Sec. 4.2's count: among 32 token rows in four blocks, 48 of the 496
+    (earlier, later) pairs move, exactly those sharing an offset in their
+    blocks;
+  * App. B.1's ensemble, on a subset: sign variants differ reproducibly on
+    operands uniform on [0, 1] and not on operands uniform on [-1, 1];
+  * exact invariants: blocks of one row and one column reduce to tensor
+    scales, and a power-of-two factor on the rows at one block offset scales
+    exactly those output rows and nothing else.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import scheme_ops as so
+from oracle import schemes
+import synthetic as sy
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_values.json")))
+RC = oracle.SCALE_ROWCOL
+
+
+def strassen2_tabs():
+    return oracle.flatten_f32(so.power(schemes.strassen(), 2))
+
+
+def classical_tabs():
+    return oracle.flatten_f32(schemes.classical(1, 1, 1))
+
+
+def changed_rows(C0, C1):
+    return [int(r) for r in np.nonzero(np.any(C0 != C1, axis=1))[0]]
+
+
+def test_row_map_of_a_later_row():
+    """App. C.3: 40 Gaussian rows padded with zeros to 48 (four blocks of 12
+    under two-level Strassen), a Gaussian 512 x 512 weight; replacing row 40
+    changes output rows 4, 16, 28 and 40 (1-based) and no other.  With K =
+    512 each block-sum row of the input is one 128-entry group, so the
+    models' input schedule is one scale per block-sum row; the weight is the
+    same in both runs, so its scales cannot decide which rows move."""
+    rng = np.random.default_rng(40)
+    A = np.zeros((48, 512), np.float32)
+    A[:40] = rng.standard_normal((40, 512))
+    B = rng.standard_normal((512, 512)).astype(np.float32)
+    A1 = A.copy()
+    A1[39] = rng.standard_normal(512)
+    tabs, dims = strassen2_tabs()
+    rows = changed_rows(oracle.lowp_matmul(A, B, tabs, dims, scale_mode=RC),
+                        oracle.lowp_matmul(A1, B, tabs, dims, scale_mode=RC))
+    assert [r + 1 for r in rows] == GOLD["rowmap_changed_rows_1based"]["value"]
+    # the classical product, rounded to FP8 the same way, and unrounded
+    ct, cd = classical_tabs()
+    rows_cl = changed_rows(oracle.lowp_matmul(A, B, ct, cd, scale_mode=RC),
+                           oracle.lowp_matmul(A1, B, ct, cd, scale_mode=RC))
+    assert [r + 1 for r in rows_cl] == GOLD["rowmap_classical_changed_rows_1based"]["value"]
+    rows_fp32 = changed_rows(A.astype(np.float64) @ B, A1.astype(np.float64) @ B)
+    assert [r + 1 for r in rows_fp32] == GOLD["rowmap_classical_changed_rows_1based"]["value"]
+
+
+def moved_pairs(tabs, dims, A, B, rng):
+    C0 = oracle.lowp_matmul(A, B, tabs, dims, scale_mode=RC)
+    moved = set()
+    for j in range(1, A.shape[0]):
+        A1 = A.copy()
+        A1[j] = rng.standard_normal(A.shape[1])
+        C1 = oracle.lowp_matmul(A1, B, tabs, dims, scale_mode=RC)
+        moved |= {(i, j) for i in range(j) if np.any(C0[i] != C1[i])}
+    return moved
+
+
+def test_prefix_pairs_moved_by_fp8_block_sums():
+    """Sec. 4.2: 32 token rows in four blocks of 8, inner length 128 (four
+    block columns of 32 spanning one 128-group, so one scale per block-sum
+    row); changing one later row at a time moves 48 of the 496 pairs,
+    exactly those whose rows share an offset in their blocks."""
+    rng = np.random.default_rng(32)
+    A = rng.standard_normal((32, 128)).astype(np.float32)
+    B = rng.standard_normal((128, 128)).astype(np.float32)
+    tabs, dims = strassen2_tabs()
+    moved = moved_pairs(tabs, dims, A, B, np.random.default_rng(33))
+    same_offset = {(i, j) for j in range(32) for i in range(j) if i % 8 == j % 8}
+    assert 32 * 31 // 2 == GOLD["prefix_pairs_total"]["value"]
+    assert len(moved) == GOLD["prefix_pairs_moved_fp8"]["value"]
+    assert moved == same_offset
+    ct, cd = classical_tabs()
+    assert moved_pairs(ct, cd, A, B, np.random.default_rng(33)) == set()
+
+
+def ensemble(lo, variants, pairs, seed):
+    """Average relative errors of the given sign variants over pairs of
+    128 x 128 operands with entries uniform on [lo, 1]; every pair is
+    evaluated under every variant.  Returns (all, even-pair, odd-pair)
+    averages per variant."""
+    s2 = so.power(schemes.strassen(), 2)
+    orbit = sy.sign_orbit(4, 4, 4)
+    tabs = [oracle.flatten_f32(so.gauge(s2, np.diag(orbit[v][0]), np.diag(orbit[v][1]),
+                                        np.diag(orbit[v][2]))) for v in variants]
+    rng = np.random.default_rng(seed)
+    err = np.zeros((len(variants), pairs))
+    for p in range(pairs):
+        A = rng.uniform(lo, 1.0, (128, 128)).astype(np.float32)
+        B = rng.uniform(lo, 1.0, (128, 128)).astype(np.float32)
+        Cref = oracle.reference_f64(A, B)
+        for vi, (t, d) in enumerate(tabs):
+            err[vi, p] = oracle.rel_fro(oracle.lowp_matmul(A, B, t, d, scale_mode=RC), Cref)
+    return err.mean(1), err[:, 0::2].mean(1), err[:, 1::2].mean(1)
+
+
+def test_sign_variants_differ_reproducibly_on_nonnegative_operands():
+    """App. B.1 on a subset (64 of the 512 variants, identity first, 4 pairs):
+    on U[0, 1] the variants' average errors spread by a large factor (the
+    paper: 2.59 over all 512 with 200 pairs) and the two halves agree
+    (0.9997); on U[-1, 1] the spread is near 1 (1.005) and the halves hardly
+    correlate (0.121).  Thresholds leave room for the smaller sample: fewer
+    variants lower the largest spread, fewer pairs add noise."""
+    variants = list(range(0, 512, 8))
+    avg, ev, od = ensemble(0.0, variants, 4, seed=2)
+    spread01 = avg.max() / avg.min()
+    corr01 = np.corrcoef(ev, od)[0, 1]
+    assert spread01 > 0.7 * GOLD["ensemble_spread_uniform_01"]["value"]
+    assert corr01 > 0.9
+    avg, ev, od = ensemble(-1.0, variants, 4, seed=3)
+    spread_pm = avg.max() / avg.min()
+    corr_pm = np.corrcoef(ev, od)[0, 1]
+    assert spread_pm < 1.08 and spread_pm > 1.0
+    assert abs(corr_pm) < 0.5
+
+
+def test_single_row_and_column_blocks_reduce_to_tensor_scales():
+    """A block sum with one row (A side) or one column (B side) has one
+    scale either way, so the two granularities agree bit for bit."""
+    rng = np.random.default_rng(5)
+    A = rng.standard_normal((4, 12)).astype(np.float32)   # 4x4 grid: block rows of 1
+    B = rng.standard_normal((12, 4)).astype(np.float32)   # block columns of 1
+    tabs, dims = strassen2_tabs()
+    t = oracle.lowp_matmul(A, B, tabs, dims, keep=True)
+    r = oracle.lowp_matmul(A, B, tabs, dims, keep=True, scale_mode=RC)
+    for key in ("Tq", "Sq", "C", "Mr"):
+        assert np.array_equal(t[key], r[key]), key
+    assert np.array_equal(t["dT"], r["dT"][:, 0]) and np.array_equal(t["dS"], r["dS"][:, 0])
+
+
+def test_power_of_two_on_one_block_offset_scales_only_those_rows():
+    """Multiplying the rows at offset x of every block row of A by 2^5
+    multiplies row x of every block sum by 2^5: its codes are unchanged,
+    its scale is multiplied by 2^5, and so exactly the output rows at
+    offset x are multiplied by 2^5 (all steps are exact under power-of-two
+    scaling away from the subnormal and overflow ranges); every other
+    output bit is unchanged.  The same holds for columns of B."""
+    rng = np.random.default_rng(6)
+    br, bc = 6, 5
+    A = rng.standard_normal((4 * br, 4 * 7)).astype(np.float32)
+    B = rng.standard_normal((4 * 7, 4 * bc)).astype(np.float32)
+    tabs, dims = strassen2_tabs()
+    base = oracle.lowp_matmul(A, B, tabs, dims, keep=True, scale_mode=RC)
+    x = 2
+    A2 = A.copy()
+    A2[x::br] *= np.float32(32.0)
+    got = oracle.lowp_matmul(A2, B, tabs, dims, keep=True, scale_mode=RC)
+    assert np.array_equal(got["Tq"], base["Tq"])
+    want_dT = base["dT"].copy()
+    want_dT[:, x] *= np.float32(32.0)
+    assert np.array_equal(got["dT"], want_dT)
+    want_C = base["C"].copy()
+    want_C[x::br] *= np.float32(32.0)
+    assert np.array_equal(got["C"], want_C)
+    z = 4
+    B2 = B.copy()
+    B2[:, z::bc] *= np.float32(0.125)
+    got = oracle.lowp_matmul(A, B2, tabs, dims, keep=True, scale_mode=RC)
+    assert np.array_equal(got["Sq"], base["Sq"])
+    want_C = base["C"].copy()
+    want_C[:, z::bc] *= np.float32(0.125)
+    assert np.array_equal(got["C"], want_C)
