@@ -68,6 +68,15 @@ typedef enum { FM_E4M3 = 0, FM_E5M2 = 1 } fm_fmt; /* OCP E4M3FN, OCP E5M2  */
 /* Arithmetic of the block products (fm_set_block_product_arithmetic). */
 typedef enum { FM_ACC_BF16 = 0, FM_ACC_FP8 = 1 } fm_accum;
 
+/* Scale granularity of the FP8 rounding of block sums.
+ *   FM_SCALE_TENSOR: one scale per block-sum tensor (per product and side);
+ *     scale arrays hold R values per gauge and side.
+ *   FM_SCALE_ROWCOL: one scale per row of every block sum of A and per
+ *     column of every block sum of B, the form the paper uses on synthetic
+ *     matrices (App. B.1); scale arrays hold R x Mb values (A side) and
+ *     R x Nb values (B side) per gauge. */
+typedef enum { FM_SCALE_TENSOR = 0, FM_SCALE_ROWCOL = 1 } fm_scale_mode;
+
 typedef struct {
   double rel_fro; /* ||C - C_ref||_F / ||C_ref||_F (0 if C_ref = 0)         */
   double err_sq;  /* sum (C - C_ref)^2, float64                             */
@@ -226,6 +235,53 @@ int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A,
                   const float* B, const double* C_ref, int M, int N, int K,
                   int levels, fm_fmt fmt, double* rel_fro_out,
                   void* workspace, size_t ws_bytes, void* hip_stream);
+
+/* ------------------------------------------- finer scale granularity
+ * The same calls with an explicit fm_scale_mode.  FM_SCALE_TENSOR gives
+ * exactly the calls above.  FM_SCALE_ROWCOL follows App. B.1's synthetic
+ * form: every row x of every A-side block sum T_r has its own amax, d and q
+ * (same rule as a whole tensor: correctly rounded fp32 divisions, d = q = 1
+ * for an all-zero row), and so does every column z of every B-side block
+ * sum S_r (a row of the transposed Sq).  Block products are then
+ * M_r[x][z] = ((sum_k Tq_r[x][k] Sq_r[z][k]) * dT_r[x]) * dS_r[z].
+ * Scale arrays: dT holds R^L x Mb floats ([r][x]), dS holds R^L x Nb floats
+ * ([r][z]); fm_block_products_scaled takes batch x Mb and batch x Nb.
+ * FM_E_ARG for an unknown mode; otherwise errors as in the calls above. */
+
+/* Workspace bytes for fm_orbit_eval_scaled / fm_matmul_lowp_scaled /
+ * fm_form_operands_scaled (0 on a bad argument). */
+size_t fm_workspace_size_scaled(const fm_scheme* s, int M, int N, int K,
+                                int levels, int G, int chunk,
+                                fm_scale_mode scale_mode);
+
+/* fm_form_operands with a scale granularity.  Async. */
+int fm_form_operands_scaled(const fm_scheme* s, int levels, const float* A,
+                            const float* B, int M, int N, int K, fm_fmt fmt,
+                            fm_scale_mode scale_mode, uint8_t* Tq,
+                            uint8_t* Sq, float* dT, float* dS,
+                            void* workspace, size_t ws_bytes,
+                            void* hip_stream);
+
+/* fm_block_products with a scale granularity.  Async. */
+int fm_block_products_scaled(const uint8_t* Tq, const uint8_t* Sq,
+                             const float* dT, const float* dS, int batch,
+                             int Mb, int Nb, int Kb, fm_fmt fmt,
+                             fm_scale_mode scale_mode, float* Mout,
+                             void* hip_stream);
+
+/* fm_matmul_lowp with a scale granularity.  Async. */
+int fm_matmul_lowp_scaled(const fm_scheme* s, const float* A, const float* B,
+                          float* C, int M, int N, int K, int levels,
+                          fm_fmt fmt, fm_scale_mode scale_mode,
+                          void* workspace, size_t ws_bytes,
+                          void* hip_stream);
+
+/* fm_orbit_eval with a scale granularity.  Synchronizes. */
+int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G,
+                         const float* A, const float* B, const double* C_ref,
+                         int M, int N, int K, int levels, fm_fmt fmt,
+                         fm_scale_mode scale_mode, double* rel_fro_out,
+                         void* workspace, size_t ws_bytes, void* hip_stream);
 
 /* Selects, process-wide, how the block products are multiplied (the App. B
  * schedule multiplies FP8 block sums and combines the products in fp32):

@@ -111,7 +111,13 @@ struct Layout {
   int recon_nblk;
 };
 
-Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true) {
+// Scales per (gauge, product) on each side: 1, or one per block-sum row
+// (A side, Mb) and per block-sum column (B side, Nb).
+int scales_a(const Geometry& g, int scale_mode) { return scale_mode == FM_SCALE_ROWCOL ? g.Mb : 1; }
+int scales_b(const Geometry& g, int scale_mode) { return scale_mode == FM_SCALE_ROWCOL ? g.Nb : 1; }
+
+Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
+                   int scale_mode = FM_SCALE_TENSOR) {
   Layout L{};
   const size_t R = (size_t)g.R;
   size_t o = 0;
@@ -128,9 +134,10 @@ Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true) {
     L.idx[k] = take((size_t)G * R * nbk[k] * 4);
     L.coef[k] = take((size_t)G * R * nbk[k] * 4);
   }
-  L.amax = take((size_t)2 * chunk * R * 4);
-  L.q = take((size_t)2 * chunk * R * 4);
-  L.d = take((size_t)2 * chunk * R * 4);
+  const size_t nsc = (size_t)chunk * R * (scales_a(g, scale_mode) + scales_b(g, scale_mode));
+  L.amax = take(nsc * 4);
+  L.q = take(nsc * 4);
+  L.d = take(nsc * 4);
   L.tq = take((size_t)chunk * R * g.Mb * g.Kb);
   L.sq = take((size_t)chunk * R * g.Nb * g.Kb);
   L.mprod = take((size_t)chunk * R * g.Mb * g.Nb * 4);
@@ -237,9 +244,12 @@ int upload_tables(const Tables& T, char* ws, const Layout& L, hipStream_t st) {
 
 // Operand formation for gauges [g0, g0 + n) of the uploaded tables.
 int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, const Layout& L,
-               const Tables& T, int g0, int n, int fmt, uint8_t* Tq, uint8_t* Sq, float* dT,
-               float* dS, hipStream_t st) {
+               const Tables& T, int g0, int n, int fmt, int scale_mode, uint8_t* Tq, uint8_t* Sq,
+               float* dT, float* dS, hipStream_t st) {
   const int R = geo.R;
+  const int per_row = scale_mode == FM_SCALE_ROWCOL ? 1 : 0;
+  const size_t na = (size_t)n * R * scales_a(geo, scale_mode);
+  const size_t nb = (size_t)n * R * scales_b(geo, scale_mode);
   uint32_t* amax = (uint32_t*)(ws + L.amax);
   float* q = (float*)(ws + L.q);
   float* dd = (float*)(ws + L.d);
@@ -247,29 +257,29 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
   auto idx = [&](int k) { return (const int32_t*)(ws + L.idx[k]); };
   auto coef = [&](int k) { return (const float*)(ws + L.coef[k]); };
   const int pa = chunk_pattern(T, 0, g0, n), pb = chunk_pattern(T, 1, g0, n);
-  if (int rc = launch_fill_u32(amax, (size_t)2 * n * R, 0u, st)) return rc;
-  FormArgs fa{A,      geo.M, geo.K, geo.gm, geo.gk, geo.Mb, geo.Kb, off(0), idx(0), coef(0), R, n,
-              amax,   q,     Tq,    fmt};
+  if (int rc = launch_fill_u32(amax, na + nb, 0u, st)) return rc;
+  FormArgs fa{A,    geo.M, geo.K, geo.gm, geo.gk, geo.Mb, geo.Kb, off(0), idx(0), coef(0), R, n,
+              amax, q,     Tq,    fmt,    per_row};
   FormArgs fb{Bt, geo.N, geo.K, geo.gn, geo.gk, geo.Nb, geo.Kb, off(1), idx(1), coef(1), R, n,
-              amax + (size_t)n * R, q + (size_t)n * R, Sq, fmt};
+              amax + na, q + na, Sq, fmt, per_row};
   for (int side = 0; side < 2; ++side) {
     timing_begin(T_FORM_AMAX, st);
     if (int rc = launch_form(side ? fb : fa, 0, side ? pb : pa, side, st)) return rc;
     timing_end(T_FORM_AMAX, st);
   }
-  if (int rc = launch_scales(amax, q, dd, 2 * n * R, fmt, (uint32_t*)(ws + L.flags), st)) return rc;
+  if (int rc = launch_scales(amax, q, dd, (int)(na + nb), fmt, (uint32_t*)(ws + L.flags), st))
+    return rc;
   for (int side = 0; side < 2; ++side) {
     timing_begin(T_FORM_QUANT, st);
     if (int rc = launch_form(side ? fb : fa, 1, side ? pb : pa, side, st)) return rc;
     timing_end(T_FORM_QUANT, st);
   }
   if (dT)
-    if (int rc = hip_check(hipMemcpyAsync(dT, dd, (size_t)n * R * 4, hipMemcpyDeviceToDevice, st),
+    if (int rc = hip_check(hipMemcpyAsync(dT, dd, na * 4, hipMemcpyDeviceToDevice, st),
                            "hipMemcpyAsync(dT)"))
       return rc;
   if (dS)
-    if (int rc = hip_check(hipMemcpyAsync(dS, dd + (size_t)n * R, (size_t)n * R * 4,
-                                          hipMemcpyDeviceToDevice, st),
+    if (int rc = hip_check(hipMemcpyAsync(dS, dd + na, nb * 4, hipMemcpyDeviceToDevice, st),
                            "hipMemcpyAsync(dS)"))
       return rc;
   return FM_OK;
@@ -621,11 +631,19 @@ int fm_scheme_coeffs_f32(const fm_scheme* s, int levels, float* U, float* V, flo
 
 void fm_scheme_free(fm_scheme* s) { delete s; }
 
-size_t fm_workspace_size(const fm_scheme* s, int M, int N, int K, int levels, int G, int chunk) {
+static int scale_mode_ok(int m) { return m == FM_SCALE_TENSOR || m == FM_SCALE_ROWCOL; }
+
+size_t fm_workspace_size_scaled(const fm_scheme* s, int M, int N, int K, int levels, int G,
+                                int chunk, fm_scale_mode scale_mode) {
   Geometry g;
-  if (G < 1 || check_geometry(s, levels, M, N, K, g) != FM_OK) return 0;
+  if (G < 1 || !scale_mode_ok(scale_mode) || check_geometry(s, levels, M, N, K, g) != FM_OK)
+    return 0;
   if (chunk <= 0 || chunk > G) chunk = G;
-  return make_layout(g, G, chunk).total;
+  return make_layout(g, G, chunk, true, scale_mode).total;
+}
+
+size_t fm_workspace_size(const fm_scheme* s, int M, int N, int K, int levels, int G, int chunk) {
+  return fm_workspace_size_scaled(s, M, N, K, levels, G, chunk, FM_SCALE_TENSOR);
 }
 
 size_t fm_error_workspace_size(int M, int N) {
@@ -634,15 +652,17 @@ size_t fm_error_workspace_size(int M, int N) {
   return up((size_t)error_stats_blocks(n) * 3 * 8) + up(3 * 8);
 }
 
-int fm_form_operands(const fm_scheme* s, int levels, const float* A, const float* B, int M, int N,
-                     int K, fm_fmt fmt, uint8_t* Tq, uint8_t* Sq, float* dT, float* dS,
-                     void* workspace, size_t ws_bytes, void* hip_stream) {
+int fm_form_operands_scaled(const fm_scheme* s, int levels, const float* A, const float* B,
+                            int M, int N, int K, fm_fmt fmt, fm_scale_mode scale_mode, uint8_t* Tq,
+                            uint8_t* Sq, float* dT, float* dS, void* workspace, size_t ws_bytes,
+                            void* hip_stream) {
   clear_error();
   if (!A || !B || !Tq || !Sq || !dT || !dS) return fail(FM_E_ARG, "null pointer");
   if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
+  if (!scale_mode_ok(scale_mode)) return fail(FM_E_ARG, "bad scale mode");
   Geometry geo;
   if (int rc = check_geometry(s, levels, M, N, K, geo)) return rc;
-  const Layout L = make_layout(geo, 1, 1);
+  const Layout L = make_layout(geo, 1, 1, true, scale_mode);
   if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
   hipStream_t st = (hipStream_t)hip_stream;
   char* ws = (char*)workspace;
@@ -653,18 +673,34 @@ int fm_form_operands(const fm_scheme* s, int levels, const float* A, const float
   if ((rc = upload_tables(T, ws, L, st))) return rc;
   float* Bt = (float*)(ws + L.bt);
   if ((rc = launch_transpose(B, Bt, K, N, st))) return rc;
-  return form_chunk(geo, A, Bt, ws, L, T, 0, 1, fmt, Tq, Sq, dT, dS, st);
+  return form_chunk(geo, A, Bt, ws, L, T, 0, 1, fmt, scale_mode, Tq, Sq, dT, dS, st);
+}
+
+int fm_form_operands(const fm_scheme* s, int levels, const float* A, const float* B, int M, int N,
+                     int K, fm_fmt fmt, uint8_t* Tq, uint8_t* Sq, float* dT, float* dS,
+                     void* workspace, size_t ws_bytes, void* hip_stream) {
+  return fm_form_operands_scaled(s, levels, A, B, M, N, K, fmt, FM_SCALE_TENSOR, Tq, Sq, dT, dS,
+                                 workspace, ws_bytes, hip_stream);
+}
+
+int fm_block_products_scaled(const uint8_t* Tq, const uint8_t* Sq, const float* dT,
+                             const float* dS, int batch, int Mb, int Nb, int Kb, fm_fmt fmt,
+                             fm_scale_mode scale_mode, float* Mout, void* hip_stream) {
+  clear_error();
+  if (!Tq || !Sq || !dT || !dS || !Mout) return fail(FM_E_ARG, "null pointer");
+  if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
+  if (!scale_mode_ok(scale_mode)) return fail(FM_E_ARG, "bad scale mode");
+  if (batch < 1 || Mb < 1 || Nb < 1 || Kb < 1) return fail(FM_E_ARG, "sizes must be positive");
+  if (Kb % 16) return fail(FM_E_SHAPE, "Kb must be a multiple of 16");
+  return launch_block_gemm(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, scale_mode,
+                           (hipStream_t)hip_stream);
 }
 
 int fm_block_products(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
                       int batch, int Mb, int Nb, int Kb, fm_fmt fmt, float* Mout,
                       void* hip_stream) {
-  clear_error();
-  if (!Tq || !Sq || !dT || !dS || !Mout) return fail(FM_E_ARG, "null pointer");
-  if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
-  if (batch < 1 || Mb < 1 || Nb < 1 || Kb < 1) return fail(FM_E_ARG, "sizes must be positive");
-  if (Kb % 16) return fail(FM_E_SHAPE, "Kb must be a multiple of 16");
-  return launch_block_gemm(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, (hipStream_t)hip_stream);
+  return fm_block_products_scaled(Tq, Sq, dT, dS, batch, Mb, Nb, Kb, fmt, FM_SCALE_TENSOR, Mout,
+                                  hip_stream);
 }
 
 int fm_reconstruct(const fm_scheme* s, int levels, const float* Mprod, int M, int N, float* C,
@@ -690,15 +726,16 @@ int fm_reconstruct(const fm_scheme* s, int levels, const float* Mprod, int M, in
   return launch_recon(ra, chunk_pattern(T, 2, 0, 1), st);
 }
 
-int fm_matmul_lowp(const fm_scheme* s, const float* A, const float* B, float* C, int M, int N,
-                   int K, int levels, fm_fmt fmt, void* workspace, size_t ws_bytes,
-                   void* hip_stream) {
+int fm_matmul_lowp_scaled(const fm_scheme* s, const float* A, const float* B, float* C, int M,
+                          int N, int K, int levels, fm_fmt fmt, fm_scale_mode scale_mode,
+                          void* workspace, size_t ws_bytes, void* hip_stream) {
   clear_error();
   if (!A || !B || !C) return fail(FM_E_ARG, "null pointer");
   if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
+  if (!scale_mode_ok(scale_mode)) return fail(FM_E_ARG, "bad scale mode");
   Geometry geo;
   if (int rc = check_geometry(s, levels, M, N, K, geo)) return rc;
-  const Layout L = make_layout(geo, 1, 1);
+  const Layout L = make_layout(geo, 1, 1, true, scale_mode);
   if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
   hipStream_t st = (hipStream_t)hip_stream;
   char* ws = (char*)workspace;
@@ -711,15 +748,24 @@ int fm_matmul_lowp(const fm_scheme* s, const float* A, const float* B, float* C,
   if ((rc = launch_transpose(B, Bt, K, N, st))) return rc;
   uint8_t* Tq = (uint8_t*)(ws + L.tq);
   uint8_t* Sq = (uint8_t*)(ws + L.sq);
-  if ((rc = form_chunk(geo, A, Bt, ws, L, T, 0, 1, fmt, Tq, Sq, nullptr, nullptr, st))) return rc;
+  if ((rc = form_chunk(geo, A, Bt, ws, L, T, 0, 1, fmt, scale_mode, Tq, Sq, nullptr, nullptr, st)))
+    return rc;
   const float* dd = (const float*)(ws + L.d);
   float* Mp = (float*)(ws + L.mprod);
   timing_begin(T_BLOCK_GEMM, st);
-  if ((rc = launch_block_gemm(Tq, Sq, dd, dd + geo.R, Mp, geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, st)))
+  if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)geo.R * scales_a(geo, scale_mode), Mp,
+                              geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, scale_mode, st)))
     return rc;
   timing_end(T_BLOCK_GEMM, st);
   const ReconArgs ra = recon_args(geo, ws, L, 0, 1, Mp, C, nullptr);
   return launch_recon(ra, chunk_pattern(T, 2, 0, 1), st);
+}
+
+int fm_matmul_lowp(const fm_scheme* s, const float* A, const float* B, float* C, int M, int N,
+                   int K, int levels, fm_fmt fmt, void* workspace, size_t ws_bytes,
+                   void* hip_stream) {
+  return fm_matmul_lowp_scaled(s, A, B, C, M, N, K, levels, fmt, FM_SCALE_TENSOR, workspace,
+                               ws_bytes, hip_stream);
 }
 
 int fm_reference_f64(const float* A, const float* B, double* C_ref, int M, int N, int K,
@@ -757,20 +803,22 @@ int fm_error_stats(const float* C, const double* C_ref, int M, int N, fm_stats* 
   return FM_OK;
 }
 
-int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A, const float* B,
-                  const double* C_ref, int M, int N, int K, int levels, fm_fmt fmt,
-                  double* rel_fro_out, void* workspace, size_t ws_bytes, void* hip_stream) {
+int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, const float* B,
+                         const double* C_ref, int M, int N, int K, int levels, fm_fmt fmt,
+                         fm_scale_mode scale_mode, double* rel_fro_out, void* workspace,
+                         size_t ws_bytes, void* hip_stream) {
   clear_error();
   if (!gauged || !A || !B || !C_ref || !rel_fro_out) return fail(FM_E_ARG, "null pointer");
   if (G < 1) return fail(FM_E_ARG, "G must be positive");
   if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
+  if (!scale_mode_ok(scale_mode)) return fail(FM_E_ARG, "bad scale mode");
   Geometry geo;
   if (int rc = check_geometry(gauged[0], levels, M, N, K, geo)) return rc;
   int chunk = G;
-  Layout L = make_layout(geo, G, chunk);
+  Layout L = make_layout(geo, G, chunk, true, scale_mode);
   while (chunk > 1 && L.total > ws_bytes) {
     chunk = std::max(1, chunk / 2);
-    L = make_layout(geo, G, chunk);
+    L = make_layout(geo, G, chunk, true, scale_mode);
   }
   if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
   hipStream_t st = (hipStream_t)hip_stream;
@@ -789,10 +837,12 @@ int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A, const f
   double* errsq = (double*)(ws + L.errsq);
   for (int g0 = 0; g0 < G; g0 += chunk) {
     const int n = std::min(chunk, G - g0);
-    if ((rc = form_chunk(geo, A, Bt, ws, L, T, g0, n, fmt, Tq, Sq, nullptr, nullptr, st))) return rc;
+    if ((rc = form_chunk(geo, A, Bt, ws, L, T, g0, n, fmt, scale_mode, Tq, Sq, nullptr, nullptr,
+                         st)))
+      return rc;
     timing_begin(T_BLOCK_GEMM, st);
-    if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)n * geo.R, Mp, n * geo.R, geo.Mb, geo.Nb,
-                                geo.Kb, fmt, st)))
+    if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)n * geo.R * scales_a(geo, scale_mode), Mp,
+                                n * geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, scale_mode, st)))
       return rc;
     timing_end(T_BLOCK_GEMM, st);
     const ReconArgs ra = recon_args(geo, ws, L, g0, n, Mp, nullptr, C_ref);
@@ -823,6 +873,13 @@ int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A, const f
   const double ref = std::sqrt(o3[1]);
   for (int g = 0; g < G; ++g) rel_fro_out[g] = ref > 0 ? std::sqrt(h[g]) / ref : 0.0;
   return FM_OK;
+}
+
+int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A, const float* B,
+                  const double* C_ref, int M, int N, int K, int levels, fm_fmt fmt,
+                  double* rel_fro_out, void* workspace, size_t ws_bytes, void* hip_stream) {
+  return fm_orbit_eval_scaled(gauged, G, A, B, C_ref, M, N, K, levels, fmt, FM_SCALE_TENSOR,
+                              rel_fro_out, workspace, ws_bytes, hip_stream);
 }
 
 int fm_set_block_product_arithmetic(fm_accum a) {

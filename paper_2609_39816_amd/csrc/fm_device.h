@@ -153,11 +153,15 @@ __device__ __forceinline__ void form_finish(const FormArgs& a, const float (&acc
 #pragma unroll
     for (int v = 0; v < VW; ++v) mx = max(mx, __float_as_uint(acc[v]) & 0x7fffffffu);
     if (!active) mx = 0u;
+    if (a.per_row) {  // one maximum per block-sum row: straight to global memory
+      if (mx) atomicMax(&a.amax[((size_t)g * a.R + r) * a.br + x], mx);
+      return;
+    }
     mx = wave_max_u32(mx);
     if (lane == 0 && mx) atomicMax(&smax[(g - g0) * a.R + r], mx);
   } else {
     if (!active) return;
-    const float q = a.q[(size_t)g * a.R + r];
+    const float q = a.per_row ? a.q[((size_t)g * a.R + r) * a.br + x] : a.q[(size_t)g * a.R + r];
     uint8_t* dst =
         a.codes + ((size_t)g * a.R + r) * ((size_t)a.br * a.bc) + (size_t)x * a.bc + y0;
     if constexpr (VW >= 4) {
@@ -186,6 +190,7 @@ template <int MODE>
 __device__ __forceinline__ void form_flush(const FormArgs& a, const uint32_t* smax, int g0,
                                            int g1) {
   if constexpr (MODE == 0) {
+    if (a.per_row) return;
     __syncthreads();
     const int n = (g1 - g0) * a.R;
     for (int i = threadIdx.x; i < n; i += kThreads)
@@ -238,7 +243,7 @@ __device__ __forceinline__ void form_encode_store(__amdgpu_buffer_rsrc_t rsrc, u
   }
 }
 
-template <class P, int VW, int MODE, int FMT>
+template <class P, int VW, int MODE, int FMT, bool ROWS>
 __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uint32_t* smax) {
   constexpr int GR = 8, NG = (P::R + GR - 1) / GR;
   const int bcv = a.bc / VW;
@@ -283,12 +288,40 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
               for (int v = 0; v < VW; ++v) mx = max(mx, __float_as_uint(acc[v]) & 0x7fffffffu);
               lm[j] = active ? mx : 0u;
             } else {
-              form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, acc,
-                                         ro(a.q)[(size_t)g * P::R + r]);
+              const float q = ROWS ? ro(a.q)[((size_t)g * P::R + r) * a.br + x]
+                                   : ro(a.q)[(size_t)g * P::R + r];
+              form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, acc, q);
             }
           }
         });
-        if constexpr (MODE == 0) {
+        if constexpr (MODE == 0 && ROWS) {
+          // one maximum per block-sum row, folded into global memory: when a
+          // row spans whole 16-lane DPP rows (bcv a multiple of 16) they are
+          // reduced first and their last lane folds the result; otherwise
+          // every lane folds its own
+          constexpr int NJ = (gi * GR + GR <= P::R) ? GR : P::R - gi * GR;
+          if (bcv % 16 == 0) {
+            sfor<0, 4>([&](auto sc) {
+              constexpr int ctl = 0x111 + (1 << decltype(sc)::value) - 1;  // row_shr:1,2,4,8
+              uint32_t sh[NJ];
+#pragma unroll
+              for (int j = 0; j < NJ; ++j)
+                sh[j] = (uint32_t)__builtin_amdgcn_mov_dpp((int)lm[j], ctl, 0xf, 0xf, true);
+#pragma unroll
+              for (int j = 0; j < NJ; ++j) lm[j] = max(lm[j], sh[j]);
+            });
+            if ((lane & 15) == 15 && active) {
+#pragma unroll
+              for (int j = 0; j < NJ; ++j)
+                if (lm[j]) atomicMax(&a.amax[((size_t)g * P::R + gi * GR + j) * a.br + x], lm[j]);
+            }
+          } else if (active) {
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+              if (lm[j]) atomicMax(&a.amax[((size_t)g * P::R + gi * GR + j) * a.br + x], lm[j]);
+          }
+        }
+        if constexpr (MODE == 0 && !ROWS) {
           constexpr int NJ = (gi * GR + GR <= P::R) ? GR : P::R - gi * GR;
           // row maxima: after shifts 1, 2, 4, 8 lane 15 of each row holds
           // the maximum of its row (lanes shifted in from outside the row
@@ -315,15 +348,17 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
   }
 }
 
-template <class P, int VW, int MODE>
+template <class P, int VW, int MODE, bool ROWS>
 __global__ __launch_bounds__(kThreads) void form_static_kernel(FormArgs a, int gpb) {
   extern __shared__ uint32_t smax[];  // mode 0: [gauge][product][wave * 4 + row]
   const int g0 = blockIdx.y * gpb;
   const int g1 = min(a.G, g0 + gpb);
-  if constexpr (MODE == 0) {
+  if constexpr (MODE == 0 && ROWS) {
+    form_static_body<P, VW, 0, FM_E4M3, true>(a, gpb, smax);
+  } else if constexpr (MODE == 0) {
     for (int i = threadIdx.x; i < gpb * P::R * 16; i += kThreads) smax[i] = 0u;
     __syncthreads();
-    form_static_body<P, VW, 0, FM_E4M3>(a, gpb, smax);
+    form_static_body<P, VW, 0, FM_E4M3, false>(a, gpb, smax);
     __syncthreads();
     const int n = (g1 - g0) * P::R;
     for (int k = threadIdx.x; k < n; k += kThreads) {
@@ -333,8 +368,8 @@ __global__ __launch_bounds__(kThreads) void form_static_kernel(FormArgs a, int g
       if (m) atomicMax(&a.amax[(size_t)g0 * P::R + k], m);
     }
   } else {
-    if (a.fmt == FM_E4M3) form_static_body<P, VW, 1, FM_E4M3>(a, gpb, smax);
-    else form_static_body<P, VW, 1, FM_E5M2>(a, gpb, smax);
+    if (a.fmt == FM_E4M3) form_static_body<P, VW, 1, FM_E4M3, ROWS>(a, gpb, smax);
+    else form_static_body<P, VW, 1, FM_E5M2, ROWS>(a, gpb, smax);
   }
 }
 
@@ -631,12 +666,17 @@ constexpr int static_vw() {
 template <class P, int MODE>
 int launch_form_static(const FormArgs& a, hipStream_t st) {
   constexpr int VW = static_vw<P>();
+  int gpb;
+  if (a.per_row) {  // maxima go straight to global memory: no LDS table
+    const dim3 grid = form_grid(a, VW, a.G, gpb);
+    form_static_kernel<P, VW, MODE, true><<<grid, kThreads, 0, st>>>(a, gpb);
+    return launched("form_static_kernel");
+  }
   // mode 0 LDS: 16 row slots per (gauge, product), at most 48 KB
   const int max_gpb = MODE == 0 ? std::max(1, 12288 / (P::R * 16)) : a.G;
-  int gpb;
   const dim3 grid = form_grid(a, VW, max_gpb, gpb);
   const size_t shm = (MODE == 0) ? (size_t)gpb * P::R * 16 * 4 : 0;
-  form_static_kernel<P, VW, MODE><<<grid, kThreads, shm, st>>>(a, gpb);
+  form_static_kernel<P, VW, MODE, false><<<grid, kThreads, shm, st>>>(a, gpb);
   return launched("form_static_kernel");
 }
 

@@ -58,8 +58,12 @@ __device__ __forceinline__ v8bf widen8(int d0, int d1) {
   return (v8bf){a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
 }
 
+// Scales of the epilogue: SC = 0 one scale per product (dT[b], dS[b]);
+// SC = 1 one per row of Tq_b (dT[b * Mb + x]) and per row of Sq_b, i.e. per
+// column of the product (dS[b * Nb + z]).  Either way M = (acc * dT) * dS.
+
 // Non-persistent variant: one 128 x 128 tile per workgroup, 4 waves.
-template <int FMT, int ACC>
+template <int FMT, int ACC, int SC>
 __global__ __launch_bounds__(kThreads) void gemm_tile_kernel(const uint8_t* __restrict__ Tq,
                                                             const uint8_t* __restrict__ Sq,
                                                             const float* __restrict__ dT,
@@ -168,7 +172,6 @@ __global__ __launch_bounds__(kThreads) void gemm_tile_kernel(const uint8_t* __re
     __syncthreads();
   }
 
-  const float sT = dT[b], sS = dS[b];
   float* Mo = Mout + (size_t)b * Mb * Nb;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -179,6 +182,8 @@ __global__ __launch_bounds__(kThreads) void gemm_tile_kernel(const uint8_t* __re
       for (int v = 0; v < 4; ++v) {
         const int row = m0 + wm * 64 + i * 16 + 4 * q + v;
         if (row < Mb && col < Nb) {
+          const float sT = SC ? dT[(size_t)b * Mb + row] : dT[b];
+          const float sS = SC ? dS[(size_t)b * Nb + col] : dS[b];
           float m = acc[i][j][v] * sT;
           m = m * sS;
           Mo[(size_t)row * Nb + col] = m;
@@ -235,7 +240,7 @@ __device__ __forceinline__ void wait_vm(int n) {
 }
 #define FM_COMPILER_FENCE() asm volatile("" ::: "memory")
 
-template <int FMT, int ACC>
+template <int FMT, int ACC, int SC>
 __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict__ Tq,
                                                        const uint8_t* __restrict__ Sq,
                                                        const float* __restrict__ dT,
@@ -353,21 +358,35 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
     const int b = tile / tiles, tt = tile - b * tiles;
     const int tmi = tt / tiles_n;
     const int m0 = tmi * DBM, n0 = (tt - tmi * tiles_n) * DBN;
-    const float sT = dT[b], sS = dS[b];
     float* Mo = Mout + (size_t)b * Mb * Nb;
     const int r_base = m0 + wm * 64 + l16, c_base = n0 + wn * 64 + 4 * q;
     int counted = 0;
     if (vec_store && m0 + DBM <= Mb && n0 + DBN <= Nb) {
+      float sT[4];
+      float4 sS[4];
+      if constexpr (SC) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sT[i] = dT[(size_t)b * Mb + r_base + i * 16];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          sS[j] = *reinterpret_cast<const float4*>(dS + (size_t)b * Nb + c_base + j * 16);
+      } else {
+        const float t = dT[b], u = dS[b];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sT[i] = t;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sS[j] = make_float4(u, u, u, u);
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float* prow = Mo + (size_t)(r_base + i * 16) * Nb + c_base;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           float4 o;
-          o.x = (acc[i][j][0] * sT) * sS;
-          o.y = (acc[i][j][1] * sT) * sS;
-          o.z = (acc[i][j][2] * sT) * sS;
-          o.w = (acc[i][j][3] * sT) * sS;
+          o.x = (acc[i][j][0] * sT[i]) * sS[j].x;
+          o.y = (acc[i][j][1] * sT[i]) * sS[j].y;
+          o.z = (acc[i][j][2] * sT[i]) * sS[j].z;
+          o.w = (acc[i][j][3] * sT[i]) * sS[j].w;
           *reinterpret_cast<float4*>(prow + j * 16) = o;
         }
       }
@@ -381,7 +400,11 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const int col = c_base + j * 16 + v;
-            if (row < Mb && col < Nb) Mo[(size_t)row * Nb + col] = (acc[i][j][v] * sT) * sS;
+            if (row < Mb && col < Nb) {
+              const float sT = SC ? dT[(size_t)b * Mb + row] : dT[b];
+              const float sS = SC ? dS[(size_t)b * Nb + col] : dS[b];
+              Mo[(size_t)row * Nb + col] = (acc[i][j][v] * sT) * sS;
+            }
           }
       }
       // a data-dependent number of stores: counted as none (a lower bound)
@@ -469,8 +492,10 @@ int set_block_product_arith(int a) {
   return FM_OK;
 }
 
-int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
-                      float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, hipStream_t st) {
+namespace {
+template <int SC>
+int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
+                         float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, hipStream_t st) {
   const bool fp8acc = g_block_product_arith == FM_ACC_FP8;
   if (Kb % GK == 0) {
     // pipelined persistent kernel: one 144 KB-LDS workgroup per CU
@@ -480,11 +505,11 @@ int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, con
     const int T = (int)total;
     const int grid = (int)std::min<long long>(total, 256);
     if (fmt == FM_E4M3) {
-      if (fp8acc) gemm_dma_kernel<FM_E4M3, 1><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-      else gemm_dma_kernel<FM_E4M3, 0><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+      if (fp8acc) gemm_dma_kernel<FM_E4M3, 1, SC><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+      else gemm_dma_kernel<FM_E4M3, 0, SC><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
     } else {
-      if (fp8acc) gemm_dma_kernel<FM_E5M2, 1><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-      else gemm_dma_kernel<FM_E5M2, 0><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+      if (fp8acc) gemm_dma_kernel<FM_E5M2, 1, SC><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+      else gemm_dma_kernel<FM_E5M2, 0, SC><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
     }
     return launched("gemm_dma_kernel");
   }
@@ -494,13 +519,22 @@ int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, con
   if (total > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many GEMM tiles in one launch");
   const int T = (int)total;
   if (fmt == FM_E4M3) {
-    if (fp8acc) gemm_tile_kernel<FM_E4M3, 1><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-    else gemm_tile_kernel<FM_E4M3, 0><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+    if (fp8acc) gemm_tile_kernel<FM_E4M3, 1, SC><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+    else gemm_tile_kernel<FM_E4M3, 0, SC><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
   } else {
-    if (fp8acc) gemm_tile_kernel<FM_E5M2, 1><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-    else gemm_tile_kernel<FM_E5M2, 0><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+    if (fp8acc) gemm_tile_kernel<FM_E5M2, 1, SC><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+    else gemm_tile_kernel<FM_E5M2, 0, SC><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
   }
   return launched("gemm_tile_kernel");
+}
+}  // namespace
+
+int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
+                      float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, int scale_mode,
+                      hipStream_t st) {
+  if (scale_mode == FM_SCALE_ROWCOL)
+    return launch_block_gemm_sc<1>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
+  return launch_block_gemm_sc<0>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
 }
 
 }  // namespace fm

@@ -96,6 +96,9 @@ struct FormArgs {
   const float* q;   // mode 1
   uint8_t* codes;   // mode 1
   int fmt;
+  int per_row;      // 0: one amax/scale per (gauge, product); 1: one per row
+                    // of the block-sum tensor as stored (br rows), at
+                    // amax/q[(g*R + r)*br + x]
 };
 // pattern: family id from match_pattern (side A or B), or -1 for the
 // generic kernel.
@@ -109,9 +112,12 @@ int launch_scales(const uint32_t* amax, float* q, float* d, int n, int fmt, uint
 // Process-wide arithmetic of the block products (FM_ACC_BF16 / FM_ACC_FP8).
 int set_block_product_arith(int a);
 
-// Batched FP8 block products: Mout[b] = ((Tq[b] Sq[b]^T) * dT[b]) * dS[b].
+// Batched FP8 block products: Mout[b] = ((Tq[b] Sq[b]^T) * dT) * dS with
+// dT = dT[b], dS = dS[b] (FM_SCALE_TENSOR) or dT[b*Mb + x], dS[b*Nb + z]
+// (FM_SCALE_ROWCOL).
 int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
-                      float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, hipStream_t st);
+                      float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, int scale_mode,
+                      hipStream_t st);
 
 // Reconstruction + error: for gauge g < G, C_g = sum_r w M_{g,r}; if C is not
 // null it is written (G must be 1); if Cref is not null, partial sums of

@@ -25,6 +25,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "fm.h")
 
 E4M3, E5M2 = 0, 1
 ACC_BF16, ACC_FP8 = 0, 1
+SCALE_TENSOR, SCALE_ROWCOL = 0, 1  # fm_scale_mode
 FMTS = {"e4m3": E4M3, "e5m2": E5M2}
 ERRORS = {0: "FM_OK", -1: "FM_E_ARG", -2: "FM_E_SHAPE", -3: "FM_E_BRENT", -4: "FM_E_SINGULAR",
           -5: "FM_E_NONFINITE", -6: "FM_E_WORKSPACE", -7: "FM_E_HIP", -8: "FM_E_MISMATCH",
@@ -71,6 +72,11 @@ def _load():
         "fm_reference_f64": (i, [p, p, p, i, i, i, p]),
         "fm_error_stats": (i, [p, p, i, i, ct.POINTER(_Stats), p, sz, p]),
         "fm_orbit_eval": (i, [p, i, p, p, p, i, i, i, i, i, p, p, sz, p]),
+        "fm_workspace_size_scaled": (sz, [p, i, i, i, i, i, i, i]),
+        "fm_form_operands_scaled": (i, [p, i, p, p, i, i, i, i, i, p, p, p, p, p, sz, p]),
+        "fm_block_products_scaled": (i, [p, p, p, p, i, i, i, i, i, i, p, p]),
+        "fm_matmul_lowp_scaled": (i, [p, p, p, p, i, i, i, i, i, i, p, sz, p]),
+        "fm_orbit_eval_scaled": (i, [p, i, p, p, p, i, i, i, i, i, i, p, p, sz, p]),
         "fm_fp8_encode": (i, [p, i64, i, i, p, p]),
         "fm_scheme_kernel_family": (ct.c_char_p, [p, i]),
         "fm_status": (i, [p, sz, p]),
@@ -207,8 +213,8 @@ class Scheme:
 
 
 def workspace_size(s: Scheme, M: int, N: int, K: int, levels: int = 1, G: int = 1,
-                   chunk: int = 0) -> int:
-    return int(lib.fm_workspace_size(s.handle, M, N, K, levels, G, chunk))
+                   chunk: int = 0, scale_mode: int = SCALE_TENSOR) -> int:
+    return int(lib.fm_workspace_size_scaled(s.handle, M, N, K, levels, G, chunk, scale_mode))
 
 
 def workspace(nbytes: int, device=None):
@@ -216,33 +222,43 @@ def workspace(nbytes: int, device=None):
     return torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device=device or "cuda")
 
 
-def form_operands(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, stream=None):
+def form_operands(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, stream=None,
+                  scale_mode: int = SCALE_TENSOR):
     """Quantized block sums: Tq (R, Mb, Kb) u8, Sq (R, Nb, Kb) u8 (transposed),
-    dT (R,), dS (R,) fp32."""
+    dT (R,) and dS (R,) fp32, or (R, Mb) and (R, Nb) with SCALE_ROWCOL."""
     _cuda(A, torch.float32), _cuda(B, torch.float32)
     M, K = A.shape
     N = B.shape[1]
     gm, gk, gn, R = s.flat_dims(levels)
-    Tq = torch.empty((R, M // gm, K // gk), dtype=torch.uint8, device=A.device)
-    Sq = torch.empty((R, N // gn, K // gk), dtype=torch.uint8, device=A.device)
-    dT = torch.empty(R, dtype=torch.float32, device=A.device)
-    dS = torch.empty(R, dtype=torch.float32, device=A.device)
+    Mb, Nb = M // gm, N // gn
+    Tq = torch.empty((R, Mb, K // gk), dtype=torch.uint8, device=A.device)
+    Sq = torch.empty((R, Nb, K // gk), dtype=torch.uint8, device=A.device)
+    rc = scale_mode == SCALE_ROWCOL
+    dT = torch.empty((R, Mb) if rc else (R,), dtype=torch.float32, device=A.device)
+    dS = torch.empty((R, Nb) if rc else (R,), dtype=torch.float32, device=A.device)
     if ws is None:
-        ws = workspace(workspace_size(s, M, N, K, levels, 1, 1), A.device)
-    _check(lib.fm_form_operands(s.handle, levels, _dptr(A), _dptr(B), M, N, K, fmt, _dptr(Tq),
-                                _dptr(Sq), _dptr(dT), _dptr(dS), _dptr(ws), ws.numel(),
-                                _stream(stream)))
+        ws = workspace(workspace_size(s, M, N, K, levels, 1, 1, scale_mode), A.device)
+    _check(lib.fm_form_operands_scaled(s.handle, levels, _dptr(A), _dptr(B), M, N, K, fmt,
+                                       scale_mode, _dptr(Tq), _dptr(Sq), _dptr(dT), _dptr(dS),
+                                       _dptr(ws), ws.numel(), _stream(stream)))
     return Tq, Sq, dT, dS
 
 
-def block_products(Tq, Sq, dT, dS, fmt: int = E4M3, out=None, stream=None):
+def block_products(Tq, Sq, dT, dS, fmt: int = E4M3, out=None, stream=None,
+                   scale_mode: int = SCALE_TENSOR):
+    """Mout[b] = ((Tq[b] Sq[b]^T) * dT) * dS; dT, dS per product (batch,) or,
+    with SCALE_ROWCOL, per row (batch, Mb) and per column (batch, Nb)."""
     _cuda(Tq, torch.uint8), _cuda(Sq, torch.uint8)
     batch, Mb, Kb = Tq.shape
     Nb = Sq.shape[1]
+    want = (batch * Mb, batch * Nb) if scale_mode == SCALE_ROWCOL else (batch, batch)
+    if (dT.numel(), dS.numel()) != want:
+        raise ValueError(f"scale arrays hold {dT.numel()} and {dS.numel()} values, need {want}")
+    _cuda(dT, torch.float32), _cuda(dS, torch.float32)
     if out is None:
         out = torch.empty((batch, Mb, Nb), dtype=torch.float32, device=Tq.device)
-    _check(lib.fm_block_products(_dptr(Tq), _dptr(Sq), _dptr(dT), _dptr(dS), batch, Mb, Nb, Kb,
-                                 fmt, _dptr(out), _stream(stream)))
+    _check(lib.fm_block_products_scaled(_dptr(Tq), _dptr(Sq), _dptr(dT), _dptr(dS), batch, Mb, Nb,
+                                        Kb, fmt, scale_mode, _dptr(out), _stream(stream)))
     return out
 
 
@@ -258,16 +274,16 @@ def reconstruct(s: Scheme, Mprod, M: int, N: int, levels: int = 1, ws=None, stre
 
 
 def matmul_lowp(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, out=None,
-                stream=None):
+                stream=None, scale_mode: int = SCALE_TENSOR):
     _cuda(A, torch.float32), _cuda(B, torch.float32)
     M, K = A.shape
     N = B.shape[1]
     if out is None:
         out = torch.empty((M, N), dtype=torch.float32, device=A.device)
     if ws is None:
-        ws = workspace(workspace_size(s, M, N, K, levels, 1, 1), A.device)
-    _check(lib.fm_matmul_lowp(s.handle, _dptr(A), _dptr(B), _dptr(out), M, N, K, levels, fmt,
-                              _dptr(ws), ws.numel(), _stream(stream)))
+        ws = workspace(workspace_size(s, M, N, K, levels, 1, 1, scale_mode), A.device)
+    _check(lib.fm_matmul_lowp_scaled(s.handle, _dptr(A), _dptr(B), _dptr(out), M, N, K, levels,
+                                     fmt, scale_mode, _dptr(ws), ws.numel(), _stream(stream)))
     return out
 
 
@@ -293,7 +309,7 @@ def error_stats(C, Cref, ws=None, stream=None) -> dict:
 
 
 def orbit_eval(gauged, A, B, Cref, levels: int = 1, fmt: int = E4M3, ws=None, chunk: int = 0,
-               stream=None) -> np.ndarray:
+               stream=None, scale_mode: int = SCALE_TENSOR) -> np.ndarray:
     """Relative Frobenius errors of the FP8 schedule for every gauged scheme."""
     _cuda(A, torch.float32), _cuda(B, torch.float32), _cuda(Cref, torch.float64)
     M, K = A.shape
@@ -301,11 +317,11 @@ def orbit_eval(gauged, A, B, Cref, levels: int = 1, fmt: int = E4M3, ws=None, ch
     G = len(gauged)
     handles = (ct.c_void_p * G)(*[g.handle.value for g in gauged])
     if ws is None:
-        ws = workspace(workspace_size(gauged[0], M, N, K, levels, G, chunk), A.device)
+        ws = workspace(workspace_size(gauged[0], M, N, K, levels, G, chunk, scale_mode), A.device)
     out = np.empty(G, np.float64)
-    _check(lib.fm_orbit_eval(ct.cast(handles, ct.c_void_p), G, _dptr(A), _dptr(B), _dptr(Cref), M,
-                             N, K, levels, fmt, _np_ptr(out), _dptr(ws), ws.numel(),
-                             _stream(stream)))
+    _check(lib.fm_orbit_eval_scaled(ct.cast(handles, ct.c_void_p), G, _dptr(A), _dptr(B),
+                                    _dptr(Cref), M, N, K, levels, fmt, scale_mode, _np_ptr(out),
+                                    _dptr(ws), ws.numel(), _stream(stream)))
     return out
 
 

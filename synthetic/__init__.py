@@ -194,6 +194,24 @@ def ratio_sample_positions(rows: int, cols: int, count: int, seed: int):
     return rng.integers(0, rows, size=count), rng.integers(0, cols, size=count)
 
 
+# The synthetic ensemble of App. B.1: pairs of n x n operands with iid
+# entries uniform on [lo, 1] (lo = -1 or 0), 200 pairs per distribution,
+# every pair evaluated under each of the 512 sign variants of two-level
+# Strassen.  Pair p of a distribution is drawn from its own stream, so any
+# subset of pairs can be regenerated.
+ENSEMBLE_SEED = 20260903
+ENSEMBLE_PAIRS = 200
+ENSEMBLE_N = 128
+
+
+def ensemble_pair(lo: float, p: int, n: int = ENSEMBLE_N, seed: int = ENSEMBLE_SEED):
+    rng = np.random.default_rng([seed, 0 if lo < 0 else 1, p])
+    A = rng.uniform(lo, 1.0, (n, n)).astype(np.float32)
+    B = rng.uniform(lo, 1.0, (n, n)).astype(np.float32)
+    return A, B
+
+
 __all__ = ["Workload", "WORKLOADS", "WORKLOAD_ORDER", "scaled", "operands", "gauges",
            "gl_gauges", "sign_orbit", "sample_sign_orbit", "identity_gauge",
-           "ratio_sample_positions", "field"]
+           "ratio_sample_positions", "field", "ensemble_pair", "ENSEMBLE_PAIRS", "ENSEMBLE_N",
+           "ENSEMBLE_SEED"]

@@ -1,0 +1,193 @@
+"""GPU parity of the finer scale granularity (one scale per row of A's and per
+column of B's block sums, App. B.1's synthetic form) through the C ABI's
+*_scaled entry points, against the CPU oracle on the same seeded inputs.
+
+Bars: FP8 codes and every row/column scale bit-exact; block products and C
+within 1e-5 relative Frobenius; orbit errors within 1% of the oracle's.
+Structural pins (App. C.3's row map, Sec. 4.2's 48 of 496 pairs) must hold
+exactly on the device too, and the full App. B.1 ensemble is compared with
+the stored oracle run and with the printed statistics.
+"""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import scheme_ops as so
+from oracle import schemes as osch
+import synthetic as sy
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU-only machines, never run
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2609_39816_amd import fm  # noqa: E402
+
+DEV = torch.device("cuda:0")
+RC_H, RC_O = fm.SCALE_ROWCOL, oracle.SCALE_ROWCOL
+FMT = {"e4m3": (fm.E4M3, oracle.E4M3), "e5m2": (fm.E5M2, oracle.E5M2)}
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_values.json")))
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    nb = np.linalg.norm(b)
+    return np.linalg.norm(a - b) / (nb if nb > 0 else 1.0)
+
+
+def gpu(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def bits(x):
+    return np.ascontiguousarray(x, np.float32).view(np.uint32)
+
+
+CASES = [
+    # name, base scheme, levels, gauge kind, M, K, N, fmt
+    ("strassen1_gl", "strassen", 1, "gl", 256, 256, 256, "e4m3"),
+    ("strassen2_sign_rows16", "strassen", 2, "sign", 256, 512, 384, "e4m3"),
+    ("strassen2_sign_ragged", "strassen", 2, "sign", 200, 384, 260, "e4m3"),
+    ("laderman_gl_e5m2", "laderman", 1, "gl", 192, 432, 300, "e5m2"),
+    ("strassen3_sign", "strassen", 3, "sign", 256, 512, 384, "e4m3"),
+]
+
+
+def gauges_for(base, levels, kind, count, seed):
+    if kind == "gl":
+        m = {"strassen": 2, "laderman": 3}[base]
+        return sy.gl_gauges(m, m, m, count, seed=seed)
+    g = 2 ** levels
+    sv = sy.sample_sign_orbit(g, g, g, count, seed=seed)
+    return [(np.diag(d), np.diag(e), np.diag(f)) for d, e, f in sv]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_rowcol_parity(case):
+    name, base, levels, kind, M, K, N, fmt = case
+    fh, fo = FMT[fmt]
+    say(f"[scales] {name} {M}x{K}x{N} {fmt}")
+    rng = np.random.default_rng(sum(name.encode()))
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    A[:, rng.choice(K, 4, replace=False)] *= 50.0
+    B = (0.02 * rng.standard_normal((K, N))).astype(np.float32)
+    At, Bt = gpu(A), gpu(B)
+    gauges = gauges_for(base, levels, kind, 5, seed=17)
+    hb = fm.Scheme.base(base)
+    ob = osch.BASE_SCHEMES[base]()
+    if kind == "sign":
+        hflat = hb.kron(levels) if levels > 1 else hb
+        hips = [hflat.gauge(*g) for g in gauges]
+        orcs = [so.gauge(so.power(ob, levels), *g) for g in gauges]
+        lv = 1
+    else:
+        hips = [hb.gauge(*g) for g in gauges]
+        orcs = [so.power(so.gauge(ob, *g), levels) for g in gauges]
+        lv = levels
+    Cref = fm.reference_f64(At, Bt)
+    Cref_o = oracle.reference_f64(A, B)
+    errs = fm.orbit_eval(hips, At, Bt, Cref, lv, fh, scale_mode=RC_H)
+    for gi in (0, len(hips) - 1):
+        h, o = hips[gi], orcs[gi]
+        tabs, dims = oracle.flatten_f32(o)
+        gm, gk, gn, R = dims
+        Tq, Sq, dT, dS = fm.form_operands(h, At, Bt, lv, fh, scale_mode=RC_H)
+        tq, dt = oracle.form_operands(A, gm, gk, tabs[0], fo, scale_mode=RC_O, side=0)
+        sq, ds = oracle.form_operands(B, gk, gn, tabs[1], fo, scale_mode=RC_O, side=1)
+        assert np.array_equal(Tq.cpu().numpy(), tq), "Tq"
+        assert np.array_equal(Sq.cpu().numpy(), sq.transpose(0, 2, 1)), "Sq"
+        assert np.array_equal(bits(dT.cpu().numpy()), bits(dt)), "dT"
+        assert np.array_equal(bits(dS.cpu().numpy()), bits(ds)), "dS"
+        Mg = fm.block_products(Tq, Sq, dT, dS, fh, scale_mode=RC_H).cpu().numpy()
+        for r in (0, R - 1):
+            Mo = oracle.block_product_rc(tq[r], sq[r], dt[r], ds[r], fo)
+            assert rel(Mg[r], Mo) <= 1e-5, f"block product {r}: {rel(Mg[r], Mo):.2e}"
+        Co = oracle.lowp_matmul(A, B, tabs, dims, fo, scale_mode=RC_O)
+        Cg = fm.matmul_lowp(h, At, Bt, lv, fh, scale_mode=RC_H).cpu().numpy()
+        assert rel(Cg, Co) <= 1e-5, f"C: {rel(Cg, Co):.2e}"
+        want = oracle.rel_fro(Co, Cref_o)
+        assert abs(errs[gi] / want - 1) <= 1e-2, (gi, errs[gi], want)
+
+
+def changed_rows(C0, C1):
+    return [int(r) for r in np.nonzero(np.any(C0 != C1, axis=1))[0]]
+
+
+def test_row_map_on_the_device():
+    """App. C.3 through the HIP path: replacing row 40 of the 48-row input
+    changes output rows 4, 16, 28 and 40 (1-based) and no other."""
+    rng = np.random.default_rng(40)
+    A = np.zeros((48, 512), np.float32)
+    A[:40] = rng.standard_normal((40, 512))
+    B = rng.standard_normal((512, 512)).astype(np.float32)
+    A1 = A.copy()
+    A1[39] = rng.standard_normal(512)
+    s2 = fm.Scheme.base("strassen")
+    C0 = fm.matmul_lowp(s2, gpu(A), gpu(B), 2, scale_mode=RC_H).cpu().numpy()
+    C1 = fm.matmul_lowp(s2, gpu(A1), gpu(B), 2, scale_mode=RC_H).cpu().numpy()
+    assert [r + 1 for r in changed_rows(C0, C1)] == GOLD["rowmap_changed_rows_1based"]["value"]
+    cl = fm.Scheme.base("classical")
+    C0 = fm.matmul_lowp(cl, gpu(A), gpu(B), 1, scale_mode=RC_H).cpu().numpy()
+    C1 = fm.matmul_lowp(cl, gpu(A1), gpu(B), 1, scale_mode=RC_H).cpu().numpy()
+    assert [r + 1 for r in changed_rows(C0, C1)] == GOLD["rowmap_classical_changed_rows_1based"]["value"]
+
+
+def test_prefix_pairs_on_the_device():
+    """Sec. 4.2 through the HIP path: 48 of the 496 pairs move, exactly the
+    pairs sharing a block offset; none under the classical product."""
+    rng = np.random.default_rng(32)
+    A = rng.standard_normal((32, 128)).astype(np.float32)
+    B = gpu(rng.standard_normal((128, 128)).astype(np.float32))
+    rng2 = np.random.default_rng(33)
+    s2 = fm.Scheme.base("strassen")
+    cl = fm.Scheme.base("classical")
+    base = {k: fm.matmul_lowp(s, gpu(A), B, lv, scale_mode=RC_H).cpu().numpy()
+            for k, s, lv in (("s2", s2, 2), ("cl", cl, 1))}
+    moved = {"s2": set(), "cl": set()}
+    for j in range(1, 32):
+        A1 = A.copy()
+        A1[j] = rng2.standard_normal(128)
+        for k, s, lv in (("s2", s2, 2), ("cl", cl, 1)):
+            C1 = fm.matmul_lowp(s, gpu(A1), B, lv, scale_mode=RC_H).cpu().numpy()
+            moved[k] |= {(i, j) for i in range(j) if np.any(base[k][i] != C1[i])}
+    same_offset = {(i, j) for j in range(32) for i in range(j) if i % 8 == j % 8}
+    assert len(moved["s2"]) == GOLD["prefix_pairs_moved_fp8"]["value"]
+    assert moved["s2"] == same_offset
+    assert moved["cl"] == set()
+
+
+def test_full_ensemble_on_the_device():
+    """App. B.1's ensemble through fm_orbit_eval_scaled (every pair under all
+    512 sign variants): per-variant averages within 1% of the stored oracle
+    run on the same inputs, and the printed statistics."""
+    stored = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                         "ensemble_rowcol_strassen2_128.json")))
+    s2 = fm.Scheme.base("strassen").kron(2)
+    orbit = s2.gauge_orbit([(np.diag(d), np.diag(e), np.diag(f)) for d, e, f in sy.sign_orbit(4, 4, 4)])
+    n = sy.ENSEMBLE_N
+    ws = fm.workspace(fm.workspace_size(s2, n, n, n, 1, len(orbit), 0, RC_H))
+    for key, lo in (("uniform_pm1", -1.0), ("uniform_01", 0.0)):
+        err = np.zeros((len(orbit), sy.ENSEMBLE_PAIRS))
+        for p in range(sy.ENSEMBLE_PAIRS):
+            A, B = sy.ensemble_pair(lo, p)
+            At, Bt = gpu(A), gpu(B)
+            err[:, p] = fm.orbit_eval(orbit, At, Bt, fm.reference_f64(At, Bt), 1, ws=ws,
+                                      scale_mode=RC_H)
+        avg, ev, od = err.mean(1), err[:, 0::2].mean(1), err[:, 1::2].mean(1)
+        spread, corr = avg.max() / avg.min(), np.corrcoef(ev, od)[0, 1]
+        say(f"[scales] ensemble {key}: spread {spread:.4f} split-half {corr:.4f}")
+        assert np.all(np.abs(avg / np.array(stored[key]["avg"]) - 1) <= 1e-2)
+        assert abs(spread / stored[key]["spread"] - 1) <= 1e-2
+    # the printed statistics (App. B.1)
+    assert abs(stored["uniform_01"]["spread"] / GOLD["ensemble_spread_uniform_01"]["value"] - 1) < 0.02
