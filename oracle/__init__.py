@@ -74,6 +74,13 @@ def lib():
             "orc_block_product_rc": (None, [p, p, p, p, i, i, i, i, p]),
             "orc_lowp_matmul_sm": (i, [p, p, i, i, i, i, i, i, i, p, p, p, i, i, p, p, p, p, p, p]),
             "orc_form_operands_sm": (None, [p, i, i, i, i, i, p, i, i, i, p, p]),
+            "orc_int8_quantize_a": (None, [p, i, i, i, i, p, p]),
+            "orc_int8_quantize_b": (None, [p, i, i, i, i, p, p]),
+            "orc_int8_group_product": (None, [p, p, i, i, i, i, i, p]),
+            "orc_int8_classical": (None, [p, p, p, p, i, i, i, i, p]),
+            "orc_int8_group_product_fast": (None, [p, p, i, i, i, i, i, i, i, i, i, i, p, p, p, i,
+                                                   p, p]),
+            "orc_int8_fast": (i, [p, p, p, p, i, i, i, i, i, i, i, i, i, p, p, p, p, p]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -316,3 +323,102 @@ def orbit_stats(ratios, identity_value=None) -> dict:
 
 def default_threads() -> int:
     return int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+
+# --------------------------------------------------------------------------
+# Integer codes and the classical int8 operator (Sec. 2.2, App. D), and the
+# fast realization of Sec. 4.2 (Prop. 1)
+# --------------------------------------------------------------------------
+def int8_quantize_a(A, g: int, b: int):
+    """Codes (M, K) int8 and scales d (M, K/g): one scale per row and group."""
+    A = _f32(A)
+    M, K = A.shape
+    assert K % g == 0
+    codes = np.empty((M, K), np.int8)
+    d = np.empty((M, K // g), np.float32)
+    lib().orc_int8_quantize_a(_ptr(A), M, K, g, b, _ptr(codes), _ptr(d))
+    return codes, d
+
+
+def int8_quantize_b(B, g: int, b: int):
+    """Codes (K, N) int8 and scales d (K/g, N): one scale per column and group."""
+    B = _f32(B)
+    K, N = B.shape
+    assert K % g == 0
+    codes = np.empty((K, N), np.int8)
+    d = np.empty((K // g, N), np.float32)
+    lib().orc_int8_quantize_b(_ptr(B), K, N, g, b, _ptr(codes), _ptr(d))
+    return codes, d
+
+
+def int8_group_product(Ac, Bc, g: int, gi: int):
+    Ac = np.ascontiguousarray(Ac, np.int8)
+    Bc = np.ascontiguousarray(Bc, np.int8)
+    M, K = Ac.shape
+    N = Bc.shape[1]
+    P = np.empty((M, N), np.int64)
+    lib().orc_int8_group_product(_ptr(Ac), _ptr(Bc), M, N, K, g, gi, _ptr(P))
+    return P
+
+
+def int8_classical(Ac, dA, Bc, dB, g: int):
+    """The classical int8 operator: fp32 output (M, N)."""
+    Ac = np.ascontiguousarray(Ac, np.int8)
+    Bc = np.ascontiguousarray(Bc, np.int8)
+    dA, dB = _f32(dA), _f32(dB)
+    M, K = Ac.shape
+    N = Bc.shape[1]
+    out = np.empty((M, N), np.float32)
+    lib().orc_int8_classical(_ptr(Ac), _ptr(dA), _ptr(Bc), _ptr(dB), M, N, K, g, _ptr(out))
+    return out
+
+
+def int8_group_product_fast(Ac, Bc, scheme_f32, dims, g: int, gi: int, h: int,
+                            round_fp8: bool = False):
+    """One group's product computed call by call with the scheme; returns
+    (P as float64 (M, N), violations of (i), violations of (ii))."""
+    U, V, W = (_f32(t) for t in scheme_f32)
+    gm, gk, gn, R = dims
+    Ac = np.ascontiguousarray(Ac, np.int8)
+    Bc = np.ascontiguousarray(Bc, np.int8)
+    M, K = Ac.shape
+    N = Bc.shape[1]
+    P = np.empty((M, N), np.float64)
+    viol = np.zeros(2, np.int64)
+    lib().orc_int8_group_product_fast(_ptr(Ac), _ptr(Bc), M, N, K, g, gi, h, gm, gk, gn, R,
+                                      _ptr(U), _ptr(V), _ptr(W), int(round_fp8), _ptr(P),
+                                      _ptr(viol))
+    return P, int(viol[0]), int(viol[1])
+
+
+def int8_fast(Ac, dA, Bc, dB, scheme_f32, dims, g: int, h: int):
+    """The fast realization's output (M, N) fp32 and the violation counts of
+    conditions (i) and (ii) seen while computing it."""
+    U, V, W = (_f32(t) for t in scheme_f32)
+    gm, gk, gn, R = dims
+    Ac = np.ascontiguousarray(Ac, np.int8)
+    Bc = np.ascontiguousarray(Bc, np.int8)
+    dA, dB = _f32(dA), _f32(dB)
+    M, K = Ac.shape
+    N = Bc.shape[1]
+    out = np.empty((M, N), np.float32)
+    viol = np.zeros(2, np.int64)
+    rc = lib().orc_int8_fast(_ptr(Ac), _ptr(dA), _ptr(Bc), _ptr(dB), M, N, K, g, h, gm, gk, gn, R,
+                             _ptr(U), _ptr(V), _ptr(W), _ptr(out), _ptr(viol))
+    if rc != 0:
+        raise ValueError("tiling does not fit the shape")
+    return out, int(viol[0]), int(viol[1])
+
+
+def certificate(s: Scheme, b_A: int, b_B: int, h: int, g: int, gk: int):
+    """Conditions (i)-(iii) of Prop. 1 for a scheme with integer coefficients
+    (int32 accumulation): (i) L_A b_A <= 127 and L_B b_B <= 127; (ii)
+    max(L_W h (L_A b_A)(L_B b_B), g b_A b_B) < 2^31; (iii) a call (gk blocks
+    of inner length h) lies within one group (g a multiple of gk h)."""
+    c = scheme_ops.criteria(s)
+    LA, LB, LW = c["L_A"], c["L_B"], c["L_W"]
+    i_ok = LA * b_A <= 127 and LB * b_B <= 127
+    ii_ok = max(LW * h * (LA * b_A) * (LB * b_B), g * b_A * b_B) < 2 ** 31
+    iii_ok = g % (gk * h) == 0
+    return dict(L_A=LA, L_B=LB, L_W=LW, i=bool(i_ok), ii=bool(ii_ok), iii=bool(iii_ok),
+                certified=bool(i_ok and ii_ok and iii_ok))

@@ -477,3 +477,195 @@ void orc_form_operands_sm(const float* X, int rows, int cols, int gr, int gc, in
   }
   free(T);
 }
+
+/* ======================================================================== */
+/* Integer codes and the classical int8 operator at a quantization           */
+/* specification (Sec. 2.2; App. D, the specification of the model runs):   */
+/* groups of g consecutive entries along the inner dimension; one scale per  */
+/* row of A and per column of B in every group, d = max|x| / b (one          */
+/* correctly rounded fp32 division; d = 1 for an all-zero group); code =     */
+/* x / d (one fp32 division) rounded to the nearest integer, ties to even,   */
+/* with no clipping.  Codes are held in int8 (|code| <= b <= 127).           */
+/* ======================================================================== */
+static int8_t int_code(float x, float d) {
+  float y = x / d;
+  return (int8_t)lrintf(y); /* current rounding mode: nearest, ties to even */
+}
+
+/* A: M x K row-major; codes M x K; d: M x (K/g), d[t*(K/g) + gi]. */
+void orc_int8_quantize_a(const float* A, int M, int K, int g, int b, int8_t* codes, float* d) {
+  int ng = K / g;
+  for (int t = 0; t < M; ++t)
+    for (int gi = 0; gi < ng; ++gi) {
+      const float* x = A + (int64_t)t * K + (int64_t)gi * g;
+      float amax = 0.0f;
+      for (int k = 0; k < g; ++k) {
+        float a = fabsf(x[k]);
+        if (a > amax) amax = a;
+      }
+      float s = amax == 0.0f ? 1.0f : amax / (float)b;
+      d[(int64_t)t * ng + gi] = s;
+      for (int k = 0; k < g; ++k) codes[(int64_t)t * K + (int64_t)gi * g + k] = int_code(x[k], s);
+    }
+}
+
+/* B: K x N row-major; codes K x N; d: (K/g) x N, d[gi*N + j]. */
+void orc_int8_quantize_b(const float* B, int K, int N, int g, int b, int8_t* codes, float* d) {
+  int ng = K / g;
+  for (int j = 0; j < N; ++j)
+    for (int gi = 0; gi < ng; ++gi) {
+      float amax = 0.0f;
+      for (int k = 0; k < g; ++k) {
+        float a = fabsf(B[(int64_t)(gi * g + k) * N + j]);
+        if (a > amax) amax = a;
+      }
+      float s = amax == 0.0f ? 1.0f : amax / (float)b;
+      d[(int64_t)gi * N + j] = s;
+      for (int k = 0; k < g; ++k) {
+        int64_t at = (int64_t)(gi * g + k) * N + j;
+        codes[at] = int_code(B[at], s);
+      }
+    }
+}
+
+/* One group's exact integer product of the codes, P[t][j] (int64). */
+void orc_int8_group_product(const int8_t* Ac, const int8_t* Bc, int M, int N, int K, int g,
+                            int gi, int64_t* P) {
+  for (int t = 0; t < M; ++t)
+    for (int j = 0; j < N; ++j) {
+      int64_t s = 0;
+      for (int k = gi * g; k < (gi + 1) * g; ++k)
+        s += (int64_t)Ac[(int64_t)t * K + k] * Bc[(int64_t)k * N + j];
+      P[(int64_t)t * N + j] = s;
+    }
+}
+
+/* The output side of the specification: out starts at +0; for each group in */
+/* ascending order, out += (fl32(P) * dA) * dB, each step one fp32 operation. */
+static void rescale_accumulate(const double* P, const float* dA, const float* dB, int M, int N,
+                               int ng, int gi, float* out) {
+  for (int t = 0; t < M; ++t)
+    for (int j = 0; j < N; ++j) {
+      float p = (float)P[(int64_t)t * N + j];
+      float v = p * dA[(int64_t)t * ng + gi];
+      v = v * dB[(int64_t)gi * N + j];
+      out[(int64_t)t * N + j] = out[(int64_t)t * N + j] + v;
+    }
+}
+
+void orc_int8_classical(const int8_t* Ac, const float* dA, const int8_t* Bc, const float* dB,
+                        int M, int N, int K, int g, float* out) {
+  int ng = K / g;
+  int64_t* P = (int64_t*)malloc(sizeof(int64_t) * (size_t)M * N);
+  double* Pd = (double*)malloc(sizeof(double) * (size_t)M * N);
+  for (int64_t i = 0; i < (int64_t)M * N; ++i) out[i] = 0.0f;
+  for (int gi = 0; gi < ng; ++gi) {
+    orc_int8_group_product(Ac, Bc, M, N, K, g, gi, P);
+    for (int64_t i = 0; i < (int64_t)M * N; ++i) Pd[i] = (double)P[i];
+    rescale_accumulate(Pd, dA, dB, M, N, ng, gi, out);
+  }
+  free(P);
+  free(Pd);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Fast realization of one group's integer product (Sec. 4.2, Prop. 1): the */
+/* group is covered by calls of gk*h consecutive inner indices; each call   */
+/* takes all M rows and N columns, split into gm x gk blocks of A's codes   */
+/* (M/gm x h) and gk x gn blocks of B's codes (h x N/gn), and evaluates     */
+/* eq. (1) with the given integer coefficients: block sums, R block         */
+/* products, combination; the calls' results are added.  All arithmetic is  */
+/* exact (int64); viol[0] counts block-sum entries outside [-127, 127]      */
+/* (condition (i)), viol[1] products or partial sums, in the order formed,  */
+/* outside int32 (condition (ii)).  With round_fp8 = 1 every block-sum      */
+/* entry is first rounded to E4M3 (nearest even, saturating), and products  */
+/* and sums are carried in float64 (exact at these magnitudes).             */
+/* P receives the group product (M x N, as float64).                        */
+/* ------------------------------------------------------------------------ */
+void orc_int8_group_product_fast(const int8_t* Ac, const int8_t* Bc, int M, int N, int K, int g,
+                                 int gi, int h, int gm, int gk, int gn, int R, const float* U,
+                                 const float* V, const float* W, int round_fp8, double* P,
+                                 int64_t* viol) {
+  const int br = M / gm, bc = N / gn;
+  const int64_t lim = (int64_t)1 << 31;
+  double* T = (double*)malloc(sizeof(double) * (size_t)br * h);
+  double* S = (double*)malloc(sizeof(double) * (size_t)h * bc);
+  double* Mr = (double*)malloc(sizeof(double) * (size_t)R * br * bc);
+  for (int64_t i = 0; i < (int64_t)M * N; ++i) P[i] = 0.0;
+  for (int k0 = gi * g; k0 < (gi + 1) * g; k0 += gk * h) { /* one call */
+    for (int r = 0; r < R; ++r) {
+      /* block sums of codes, ascending row-major grid order */
+      for (int x = 0; x < br; ++x)
+        for (int y = 0; y < h; ++y) {
+          double acc = 0.0;
+          for (int p = 0; p < gm; ++p)
+            for (int q = 0; q < gk; ++q) {
+              double u = U[(int64_t)r * gm * gk + p * gk + q];
+              if (u == 0.0) continue;
+              acc += u * Ac[(int64_t)(p * br + x) * K + k0 + q * h + y];
+            }
+          if (fabs(acc) > 127.0) ++viol[0];
+          T[(int64_t)x * h + y] = round_fp8 ? orc_fp8_decode(orc_fp8_encode((float)acc, 0), 0) : acc;
+        }
+      for (int y = 0; y < h; ++y)
+        for (int z = 0; z < bc; ++z) {
+          double acc = 0.0;
+          for (int p = 0; p < gk; ++p)
+            for (int q = 0; q < gn; ++q) {
+              double v = V[(int64_t)r * gk * gn + p * gn + q];
+              if (v == 0.0) continue;
+              acc += v * Bc[(int64_t)(k0 + p * h + y) * N + q * bc + z];
+            }
+          if (fabs(acc) > 127.0) ++viol[0];
+          S[(int64_t)y * bc + z] = round_fp8 ? orc_fp8_decode(orc_fp8_encode((float)acc, 0), 0) : acc;
+        }
+      /* block product */
+      for (int x = 0; x < br; ++x)
+        for (int z = 0; z < bc; ++z) {
+          double s = 0.0;
+          for (int y = 0; y < h; ++y) {
+            s += T[(int64_t)x * h + y] * S[(int64_t)y * bc + z];
+            if (fabs(s) >= (double)lim) ++viol[1];
+          }
+          Mr[((int64_t)r * br + x) * bc + z] = s;
+        }
+    }
+    /* combination, ascending r; added to the group's running sum */
+    for (int i = 0; i < gm; ++i)
+      for (int j = 0; j < gn; ++j)
+        for (int x = 0; x < br; ++x)
+          for (int z = 0; z < bc; ++z) {
+            double c = 0.0;
+            for (int r = 0; r < R; ++r) {
+              double w = W[(int64_t)r * gm * gn + i * gn + j];
+              if (w == 0.0) continue;
+              c += w * Mr[((int64_t)r * br + x) * bc + z];
+              if (fabs(c) >= (double)lim) ++viol[1];
+            }
+            double* pp = P + (int64_t)(i * br + x) * N + j * bc + z;
+            *pp += c;
+            if (fabs(*pp) >= (double)lim) ++viol[1];
+          }
+  }
+  free(T);
+  free(S);
+  free(Mr);
+}
+
+/* The fast realization's output: the group products of the calls, then the */
+/* classical operator's rescaling and fp32 order.  Returns 0, or -1 if the  */
+/* tiling does not fit (M, N, g divisibility).                              */
+int orc_int8_fast(const int8_t* Ac, const float* dA, const int8_t* Bc, const float* dB, int M,
+                  int N, int K, int g, int h, int gm, int gk, int gn, int R, const float* U,
+                  const float* V, const float* W, float* out, int64_t* viol) {
+  if (M % gm || N % gn || K % g || g % (gk * h)) return -1;
+  int ng = K / g;
+  double* P = (double*)malloc(sizeof(double) * (size_t)M * N);
+  for (int64_t i = 0; i < (int64_t)M * N; ++i) out[i] = 0.0f;
+  for (int gi = 0; gi < ng; ++gi) {
+    orc_int8_group_product_fast(Ac, Bc, M, N, K, g, gi, h, gm, gk, gn, R, U, V, W, 0, P, viol);
+    rescale_accumulate(P, dA, dB, M, N, ng, gi, out);
+  }
+  free(P);
+  return 0;
+}
