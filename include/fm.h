@@ -60,6 +60,10 @@ extern "C" {
 #define FM_E_MISMATCH (-8)   /* schemes of one orbit differ in shape        */
 #define FM_E_NOMEM (-9)      /* host allocation failed                      */
 #define FM_E_UNSUPPORTED (-10) /* no kernel for this grid size              */
+#define FM_E_RANGE (-11)       /* a block sum of integer codes left int8:
+                                  codes beyond the certified bound          */
+#define FM_E_UNCERTIFIED (-12) /* the scheme, code bounds and tiling do not
+                                  meet Prop. 1's conditions                 */
 
 typedef struct fm_scheme fm_scheme; /* opaque, immutable, library-owned     */
 
@@ -282,6 +286,72 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G,
                          int M, int N, int K, int levels, fm_fmt fmt,
                          fm_scale_mode scale_mode, double* rel_fro_out,
                          void* workspace, size_t ws_bytes, void* hip_stream);
+
+/* ------------------------------------------------------ integer path
+ * The quantization specification of Sec. 2.2 / App. D and the two operators
+ * of Sec. 4.2 on it.  Codes are int8; groups of g consecutive entries along
+ * the inner dimension share a scale per row of A and per column of B.
+ * Scale arrays are group-major: dA[gi * M + t], dB[gi * N + j].
+ * B always enters transposed (N x K codes), so both operands have the
+ * inner dimension contiguous. */
+
+/* Integer codes of X (rows x K fp32, device): for every row t and group gi,
+ * d = max|x| / b over the group's g entries (one correctly rounded fp32
+ * division; d = 1 for an all-zero group) and code = x / d (one fp32
+ * division) rounded to the nearest integer, ties to even, no clipping
+ * (|code| <= b).  codes: rows x K int8; d: (K/g) x rows fp32 (group-major).
+ * A group holding Inf or NaN ORs 1 into *flag (device, may be NULL).
+ * g a multiple of 64 and at most 512, K a multiple of g, 1 <= b <= 127.
+ * Quantize A directly and B through its transpose.  Async. */
+int fm_int8_quantize(const float* X, int rows, int K, int g, int b,
+                     int8_t* codes, float* d, uint32_t* flag,
+                     void* hip_stream);
+
+/* The classical int8 operator at the specification (Sec. 2.2): for every
+ * group gi in ascending order, the exact integer product P of the group's
+ * codes (int32 on the matrix cores, exact since |P| <= g b^2 < 2^24) is
+ * converted to fp32 and added as out += (P * dA) * dB, each step a
+ * separate fp32 operation, to an output starting at +0.  Ac: M x K, BTc:
+ * N x K codes; dA: (K/g) x M, dB: (K/g) x N; out: M x N fp32 (device).
+ * g a multiple of 128; M, N multiples of 4.  Async. */
+int fm_int8_matmul_classical(const int8_t* Ac, const float* dA,
+                             const int8_t* BTc, const float* dB, int M,
+                             int N, int K, int g, float* out,
+                             void* hip_stream);
+
+/* Prop. 1's certificate for the scheme flattened to `levels`, code bounds
+ * b_A, b_B, blocks of inner length h and groups of g (int32 accumulation):
+ *   (i)   L_A b_A <= 127 and L_B b_B <= 127,
+ *   (ii)  max(L_W h (L_A b_A)(L_B b_B), g b_A b_B) < 2^31,
+ *   (iii) a call (k^levels blocks of length h) lies within one group.
+ * conditions (host, 3 ints) receive 1/0 per condition; L (host, 3 doubles)
+ * receives L_A, L_B, L_W (largest coefficient 1-norms of the block sums and
+ * largest total weight of an output block).  FM_E_ARG if the coefficients
+ * are not integers. */
+int fm_int8_certify(const fm_scheme* s, int levels, int b_A, int b_B, int h,
+                    int g, int* conditions, double* L);
+
+/* Workspace bytes for fm_int8_matmul_fast (0 on a bad argument). */
+size_t fm_int8_workspace_size(const fm_scheme* s, int levels, int M, int N,
+                              int K, int g, int h);
+
+/* The certified fast realization (Sec. 4.2): the classical operator's
+ * quantization, rescaling and fp32 order, with every group's integer
+ * product computed call by call by the scheme: for each call (k^levels
+ * consecutive blocks of inner length h within one group) the block sums of
+ * the codes T_r, S_r (exact int8 under the certificate), and every output
+ * block C_ij = sum_r w_{r,ij} T_r S_r on the matrix cores in int32.  Output
+ * bits equal fm_int8_matmul_classical's on every input whose codes are
+ * within b_A, b_B.  FM_E_UNCERTIFIED if (i)-(iii) fail or the combination
+ * weights are not in {-1, 0, 1}; a block sum outside int8 (codes beyond the
+ * bounds) is reported as FM_E_RANGE by the next fm_status on the
+ * workspace.  h a multiple of 16 dividing 128; M, N multiples of 4 m^levels
+ * and 4 n^levels.  Async. */
+int fm_int8_matmul_fast(const fm_scheme* s, int levels, const int8_t* Ac,
+                        const float* dA, const int8_t* BTc, const float* dB,
+                        int M, int N, int K, int g, int h, int b_A, int b_B,
+                        float* out, void* workspace, size_t ws_bytes,
+                        void* hip_stream);
 
 /* Selects, process-wide, how the block products are multiplied (the App. B
  * schedule multiplies FP8 block sums and combines the products in fp32):

@@ -392,6 +392,8 @@ const char* fm_strerror(int code) {
     case FM_E_MISMATCH: return "schemes of one orbit differ in shape";
     case FM_E_NOMEM: return "host allocation failed";
     case FM_E_UNSUPPORTED: return "unsupported scheme size";
+    case FM_E_RANGE: return "a block sum of integer codes left int8";
+    case FM_E_UNCERTIFIED: return "not certified: the conditions of Prop. 1 fail";
     default: return "unknown error";
   }
 }
@@ -958,8 +960,227 @@ int fm_status(void* workspace, size_t ws_bytes, void* hip_stream) {
   uint32_t flag = 0;
   if (int rc = download(&flag, workspace, 4, st)) return rc;
   if (int rc = launch_fill_u32((uint32_t*)workspace, 1, 0u, st)) return rc;
+  if (flag & 2u) return fail(FM_E_RANGE, "a block sum of integer codes left int8");
   if (flag) return fail(FM_E_NONFINITE, "a block sum was not finite");
   return FM_OK;
+}
+
+// ------------------------------------------------------------ integer path
+int fm_int8_quantize(const float* X, int rows, int K, int g, int b, int8_t* codes, float* d,
+                     uint32_t* flag, void* hip_stream) {
+  clear_error();
+  if (!X || !codes || !d) return fail(FM_E_ARG, "null pointer");
+  if (rows < 1 || K < 1) return fail(FM_E_ARG, "sizes must be positive");
+  if (b < 1 || b > 127) return fail(FM_E_ARG, "code bound must be in [1, 127]");
+  if (g < 64 || g > 512 || g % 64) return fail(FM_E_ARG, "group length must be 64..512, a multiple of 64");
+  if (K % g) return fail(FM_E_SHAPE, "K must be a multiple of the group length");
+  return launch_i8_quantize(X, rows, K, g, b, codes, d, flag, (hipStream_t)hip_stream);
+}
+
+int fm_int8_matmul_classical(const int8_t* Ac, const float* dA, const int8_t* BTc, const float* dB,
+                             int M, int N, int K, int g, float* out, void* hip_stream) {
+  clear_error();
+  if (!Ac || !dA || !BTc || !dB || !out) return fail(FM_E_ARG, "null pointer");
+  if (M < 1 || N < 1 || K < 1) return fail(FM_E_ARG, "sizes must be positive");
+  if (g < 128 || g % 128 || K % g) return fail(FM_E_SHAPE, "g must be a multiple of 128 dividing K");
+  if (M % 4 || N % 4) return fail(FM_E_SHAPE, "M and N must be multiples of 4");
+  return launch_i8_gemm(false, Ac, BTc, nullptr, nullptr, dA, dB, out, nullptr, nullptr, 0, M, N,
+                        K, g, 1, 1, 1, 0, 1, (hipStream_t)hip_stream);
+}
+
+namespace {
+// The flattened scheme's integer tables and certificate quantities.
+struct IntScheme {
+  int gm = 0, gk = 0, gn = 0, R = 0;
+  std::vector<int> U, V, W;
+  double LA = 0, LB = 0, LW = 0;
+};
+
+int int_scheme(const fm_scheme* s, int levels, IntScheme& out) {
+  if (!s) return fail(FM_E_ARG, "null scheme");
+  if (levels < 1 || levels > 3) return fail(FM_E_ARG, "levels must be 1..3");
+  const fm_scheme f = levels > 1 ? power(*s, levels) : *s;
+  out.gm = f.m;
+  out.gk = f.k;
+  out.gn = f.n;
+  out.R = f.R;
+  auto conv = [&](const std::vector<double>& x, std::vector<int>& y) {
+    y.resize(x.size());
+    for (size_t i = 0; i < x.size(); ++i) {
+      if (x[i] != std::floor(x[i]) || std::fabs(x[i]) > 127) return false;
+      y[i] = (int)x[i];
+    }
+    return true;
+  };
+  if (!conv(f.U, out.U) || !conv(f.V, out.V) || !conv(f.W, out.W))
+    return fail(FM_E_ARG, "coefficients are not small integers");
+  const int R = f.R, na = f.m * f.k, nb = f.k * f.n, nc = f.m * f.n;
+  out.LA = out.LB = out.LW = 0;
+  for (int r = 0; r < R; ++r) {
+    double a = 0, b = 0;
+    for (int i = 0; i < na; ++i) a += std::abs(out.U[(size_t)r * na + i]);
+    for (int i = 0; i < nb; ++i) b += std::abs(out.V[(size_t)r * nb + i]);
+    out.LA = std::max(out.LA, a);
+    out.LB = std::max(out.LB, b);
+  }
+  for (int c = 0; c < nc; ++c) {
+    double w = 0;
+    for (int r = 0; r < R; ++r) w += std::abs(out.W[(size_t)r * nc + c]);
+    out.LW = std::max(out.LW, w);
+  }
+  return FM_OK;
+}
+
+void certify(const IntScheme& is, int bA, int bB, int h, int g, int cond[3]) {
+  const double alpha = is.LA * bA, beta = is.LB * bB;
+  cond[0] = alpha <= 127 && beta <= 127;
+  cond[1] = std::max(is.LW * h * alpha * beta, (double)g * bA * bB) < 2147483648.0;
+  cond[2] = h > 0 && g % (is.gk * h) == 0;
+}
+
+// Fast-path workspace: flags, a zero segment, coefficient tables, segment
+// tables, then per call the block sums T (R x Mb x h), S and -S (R x Nb x h).
+struct I8Layout {
+  size_t flags, zero, coefa, coefb, segs, segoff, t, s, sn, total;
+  int nsegs;
+};
+
+I8Layout i8_layout(const IntScheme& is, int M, int N, int K, int h) {
+  I8Layout L{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o += up(bytes);
+    return at;
+  };
+  const int per_step = 128 / h;
+  int nsegs = 0;
+  for (int c = 0; c < is.gm * is.gn; ++c) {
+    int n = 0;
+    for (int r = 0; r < is.R; ++r) n += is.W[(size_t)r * is.gm * is.gn + c] != 0;
+    nsegs += (n + per_step - 1) / per_step * per_step;
+  }
+  L.nsegs = nsegs;
+  const size_t ncall = (size_t)K / ((size_t)is.gk * h);
+  L.flags = take(kAlign);
+  L.zero = take(kAlign);
+  L.coefa = take((size_t)is.R * is.gm * is.gk);
+  L.coefb = take((size_t)is.R * is.gn * is.gk);
+  L.segs = take((size_t)nsegs * 4);
+  L.segoff = take((size_t)(is.gm * is.gn + 1) * 4);
+  L.t = take(ncall * is.R * (M / is.gm) * h);
+  L.s = take(ncall * is.R * (N / is.gn) * h);
+  L.sn = take(ncall * is.R * (N / is.gn) * h);
+  L.total = o;
+  return L;
+}
+
+int i8_fast_shape_ok(const IntScheme& is, int M, int N, int K, int g, int h) {
+  if (M < 1 || N < 1 || K < 1) return fail(FM_E_ARG, "sizes must be positive");
+  if (h < 16 || h > 128 || h % 16 || 128 % h) return fail(FM_E_ARG, "h must be 16, 32, 64 or 128");
+  if (g < 128 || g % 128 || K % g) return fail(FM_E_SHAPE, "g must be a multiple of 128 dividing K");
+  if (M % (4 * is.gm) || N % (4 * is.gn))
+    return fail(FM_E_SHAPE, "M and N must be multiples of 4 m^L and 4 n^L");
+  if (is.gm * is.gn > 64) return fail(FM_E_UNSUPPORTED, "output grid larger than 64 blocks");
+  return FM_OK;
+}
+}  // namespace
+
+int fm_int8_certify(const fm_scheme* s, int levels, int b_A, int b_B, int h, int g,
+                    int* conditions, double* L) {
+  clear_error();
+  if (!conditions || !L) return fail(FM_E_ARG, "null pointer");
+  IntScheme is;
+  if (int rc = int_scheme(s, levels, is)) return rc;
+  certify(is, b_A, b_B, h, g, conditions);
+  L[0] = is.LA;
+  L[1] = is.LB;
+  L[2] = is.LW;
+  return FM_OK;
+}
+
+size_t fm_int8_workspace_size(const fm_scheme* s, int levels, int M, int N, int K, int g, int h) {
+  IntScheme is;
+  if (int_scheme(s, levels, is) != FM_OK) return 0;
+  if (i8_fast_shape_ok(is, M, N, K, g, h) != FM_OK) return 0;
+  return i8_layout(is, M, N, K, h).total;
+}
+
+int fm_int8_matmul_fast(const fm_scheme* s, int levels, const int8_t* Ac, const float* dA,
+                        const int8_t* BTc, const float* dB, int M, int N, int K, int g, int h,
+                        int b_A, int b_B, float* out, void* workspace, size_t ws_bytes,
+                        void* hip_stream) {
+  clear_error();
+  if (!Ac || !dA || !BTc || !dB || !out) return fail(FM_E_ARG, "null pointer");
+  IntScheme is;
+  if (int rc = int_scheme(s, levels, is)) return rc;
+  if (int rc = i8_fast_shape_ok(is, M, N, K, g, h)) return rc;
+  if (b_A < 1 || b_A > 127 || b_B < 1 || b_B > 127) return fail(FM_E_ARG, "code bounds must be in [1, 127]");
+  int cond[3];
+  certify(is, b_A, b_B, h, g, cond);
+  if (!cond[0]) return fail(FM_E_UNCERTIFIED, "condition (i): a block sum of codes can leave int8");
+  if (!cond[1]) return fail(FM_E_UNCERTIFIED, "condition (ii): a partial sum can leave int32");
+  if (!cond[2]) return fail(FM_E_UNCERTIFIED, "condition (iii): a call spans two groups");
+  const int calls_per_group = g / (is.gk * h);
+  // the kernel accumulates a whole group (all its calls) in int32
+  if ((double)calls_per_group * is.LW * h * (is.LA * b_A) * (is.LB * b_B) >= 2147483648.0)
+    return fail(FM_E_UNCERTIFIED, "a group's calls together can leave int32");
+  const int nc = is.gm * is.gn;
+  for (int v : is.W)
+    if (v < -1 || v > 1) return fail(FM_E_UNCERTIFIED, "combination weights must be -1, 0 or 1");
+  const I8Layout L = i8_layout(is, M, N, K, h);
+  if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
+  hipStream_t st = (hipStream_t)hip_stream;
+  char* ws = (char*)workspace;
+  // host tables: coefficients per block (A: [r][i*gk + l], B: [r][j*gk + l])
+  // and the segments of every output block (ascending r, padded)
+  std::vector<int8_t> ca((size_t)is.R * is.gm * is.gk), cbt((size_t)is.R * is.gn * is.gk);
+  for (int r = 0; r < is.R; ++r) {
+    for (int i = 0; i < is.gm * is.gk; ++i) ca[(size_t)r * is.gm * is.gk + i] = (int8_t)is.U[(size_t)r * is.gm * is.gk + i];
+    for (int l = 0; l < is.gk; ++l)
+      for (int j = 0; j < is.gn; ++j)
+        cbt[(size_t)r * is.gn * is.gk + j * is.gk + l] = (int8_t)is.V[(size_t)r * is.gk * is.gn + l * is.gn + j];
+  }
+  const int per_step = 128 / h;
+  std::vector<int32_t> segs, off(1, 0);
+  for (int c = 0; c < nc; ++c) {
+    int n = 0;
+    for (int r = 0; r < is.R; ++r) {
+      const int w = is.W[(size_t)r * nc + c];
+      if (!w) continue;
+      segs.push_back(r | (w < 0 ? 1 << 16 : 0));
+      ++n;
+    }
+    if (n == 0) return fail(FM_E_ARG, "an output block combines no products");
+    for (; n % per_step; ++n) segs.push_back(0xffff);
+    off.push_back((int32_t)segs.size());
+  }
+  int rc = FM_OK;
+  if ((rc = launch_fill_u32((uint32_t*)(ws + L.flags), kAlign / 4, 0u, st))) return rc;
+  if ((rc = launch_fill_u32((uint32_t*)(ws + L.zero), kAlign / 4, 0u, st))) return rc;
+  if ((int)segs.size() != L.nsegs) return fail(FM_E_ARG, "segment table size mismatch");
+  // the four tables are adjacent in the workspace: one staged copy
+  if ((rc = upload(ws + L.coefa,
+                   {{ca.data(), ca.size()},
+                    {cbt.data(), cbt.size()},
+                    {segs.data(), segs.size() * 4},
+                    {off.data(), off.size() * 4}},
+                   {0, L.coefb - L.coefa, L.segs - L.coefa, L.segoff - L.coefa},
+                   L.segoff - L.coefa + off.size() * 4, st)))
+    return rc;
+  uint32_t* flag = (uint32_t*)(ws + L.flags);
+  int8_t* T = (int8_t*)(ws + L.t);
+  int8_t* S = (int8_t*)(ws + L.s);
+  int8_t* Sn = (int8_t*)(ws + L.sn);
+  if ((rc = launch_i8_form(Ac, M, K, is.gm, is.gk, h, is.R, (const int8_t*)(ws + L.coefa), T,
+                           nullptr, flag, st)))
+    return rc;
+  if ((rc = launch_i8_form(BTc, N, K, is.gn, is.gk, h, is.R, (const int8_t*)(ws + L.coefb), S, Sn,
+                           flag, st)))
+    return rc;
+  return launch_i8_gemm(true, T, S, Sn, (const int8_t*)(ws + L.zero), dA, dB, out,
+                        (const int32_t*)(ws + L.segs), (const int32_t*)(ws + L.segoff),
+                        (int)segs.size(), M, N, K, g, is.gm, is.gn, is.R, h, calls_per_group, st);
 }
 
 }  // extern "C"

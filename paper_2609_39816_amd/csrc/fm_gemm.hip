@@ -10,10 +10,12 @@
 #include <hip/hip_runtime.h>
 
 #include "fm_device.h"
+#include "fm_lds_ring.h"
 
 namespace fm {
 namespace {
 using namespace dev;
+using namespace ring;
 
 // ------------------------------------------------------ FP8 block GEMM
 // Workgroup tile 128 x 128, K step 128 bytes, 4 waves in 2 x 2, each wave
@@ -39,9 +41,6 @@ typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
 
 constexpr int GT = 128;  // tile rows / cols
-constexpr int GK = 128;  // K step in bytes
-
-__device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
 // Two FP8 codes (bytes 0-1 or 2-3 of w) -> two bf16 values, exactly.
 template <int FMT, bool HI>
@@ -202,44 +201,10 @@ __global__ __launch_bounds__(kThreads) void gemm_tile_kernel(const uint8_t* __re
 // loads run under the current tile's epilogue.  Rows beyond the operand
 // (ragged M or N) read row 0 instead: they only feed outputs never stored.
 //
-// The loads are issued from inline assembly and awaited with explicit vmcnt
-// counts: the compiler's own tracking of LDS DMA cannot tell the ring stages
-// apart and would drain every load in flight before each LDS read.  Vector
-// memory operations complete in issue order on this architecture, so "the
-// group for stage s is complete" is "at most n operations outstanding", n =
-// the number issued after that group (the next group's loads and any
-// epilogue stores); a lower bound on n is always safe.  The products are
-// accumulated transposed (operands swapped in the MFMA) so that each lane
-// holds 4 consecutive output columns and the epilogue writes 16-byte stores.
-constexpr int DBM = 256, DBN = 128, DROWS = DBM + DBN, DSTAGE = DROWS * GK, DNS = 3;
-constexpr int DNT = 512;                       // 8 waves
-constexpr int DLOADS = DROWS * GK / 1024 / 8;  // 1 KB wave-loads per wave per stage (= 6)
-constexpr int DSTORES = 16;                    // 16-byte stores per lane, interior tile
-
-__device__ __forceinline__ void dma16(const void* src, uint32_t lds_addr) {
-  // M0 written by SALU then read by an LDS-DMA load needs one wait state
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(src), "s"(lds_addr)
-               : "memory", "m0");
-}
-
-// s_waitcnt constraining only the vector-memory counter (gfx9 encoding:
-// vmcnt low bits [3:0], expcnt [6:4], lgkmcnt [11:8], vmcnt high bits [15:14])
-template <int N>
-__device__ __forceinline__ void wait_vm_n() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
-}
-__device__ __forceinline__ void wait_vm(int n) {
-  // n is uniform and one of few values; anything else waits for everything
-  if (n >= DLOADS + DSTORES) wait_vm_n<DLOADS + DSTORES>();
-  else if (n >= DSTORES) wait_vm_n<DSTORES>();
-  else if (n >= DLOADS) wait_vm_n<DLOADS>();
-  else wait_vm_n<0>();
-}
-#define FM_COMPILER_FENCE() asm volatile("" ::: "memory")
-
+// The ring, its direct loads and their vmcnt accounting are in
+// fm_lds_ring.h.  The products are accumulated transposed (operands swapped
+// in the MFMA) so that each lane holds 4 consecutive output columns and the
+// epilogue writes 16-byte stores.
 template <int FMT, int ACC, int SC>
 __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict__ Tq,
                                                        const uint8_t* __restrict__ Sq,

@@ -143,6 +143,16 @@ int launch_recon(const ReconArgs& a, int pattern, hipStream_t st);
 // out[g] = sum_{b < nblk} partial[g*nblk + b] (fixed order), g < G.
 int launch_reduce_rows(const double* partial, int nblk, int G, double* out, hipStream_t st);
 
+// Integer path (fm_int8.hip).
+int launch_i8_quantize(const float* X, int rows, int K, int g, int b, int8_t* codes, float* d,
+                       uint32_t* flag, hipStream_t st);
+int launch_i8_form(const int8_t* X, int rows, int K, int gp, int gk, int h, int R,
+                   const int8_t* coef, int8_t* out, int8_t* outn, uint32_t* flag, hipStream_t st);
+int launch_i8_gemm(bool fast, const int8_t* A, const int8_t* B, const int8_t* Bn,
+                   const int8_t* zero, const float* dA, const float* dB, float* out,
+                   const int32_t* segs, const int32_t* seg_off, int nsegs, int M, int N, int K,
+                   int g, int gm, int gn, int R, int h, int calls_per_group, hipStream_t st);
+
 // Float64 reference C = A B.
 int launch_reference_f64(const float* A, const float* B, double* C, int M, int N, int K,
                          hipStream_t st);

@@ -29,7 +29,7 @@ SCALE_TENSOR, SCALE_ROWCOL = 0, 1  # fm_scale_mode
 FMTS = {"e4m3": E4M3, "e5m2": E5M2}
 ERRORS = {0: "FM_OK", -1: "FM_E_ARG", -2: "FM_E_SHAPE", -3: "FM_E_BRENT", -4: "FM_E_SINGULAR",
           -5: "FM_E_NONFINITE", -6: "FM_E_WORKSPACE", -7: "FM_E_HIP", -8: "FM_E_MISMATCH",
-          -9: "FM_E_NOMEM", -10: "FM_E_UNSUPPORTED"}
+          -9: "FM_E_NOMEM", -10: "FM_E_UNSUPPORTED", -11: "FM_E_RANGE", -12: "FM_E_UNCERTIFIED"}
 
 
 class FmError(RuntimeError):
@@ -77,6 +77,11 @@ def _load():
         "fm_block_products_scaled": (i, [p, p, p, p, i, i, i, i, i, i, p, p]),
         "fm_matmul_lowp_scaled": (i, [p, p, p, p, i, i, i, i, i, i, p, sz, p]),
         "fm_orbit_eval_scaled": (i, [p, i, p, p, p, i, i, i, i, i, i, p, p, sz, p]),
+        "fm_int8_quantize": (i, [p, i, i, i, i, p, p, p, p]),
+        "fm_int8_matmul_classical": (i, [p, p, p, p, i, i, i, i, p, p]),
+        "fm_int8_certify": (i, [p, i, i, i, i, i, p, p]),
+        "fm_int8_workspace_size": (sz, [p, i, i, i, i, i, i]),
+        "fm_int8_matmul_fast": (i, [p, i, p, p, p, p, i, i, i, i, i, i, i, p, p, sz, p]),
         "fm_fp8_encode": (i, [p, i64, i, i, p, p]),
         "fm_scheme_kernel_family": (ct.c_char_p, [p, i]),
         "fm_status": (i, [p, sz, p]),
@@ -372,3 +377,65 @@ TIMED_CLASSES = ("form_amax", "form_quant", "block_gemm", "recon", "reference")
 
 def version() -> str:
     return lib.fm_version().decode()
+
+
+# ------------------------------------------------------------ integer path
+def int8_quantize(X, g: int = 128, b: int = 31, flag=None, stream=None):
+    """Codes (rows, K) int8 and group-major scales (K/g, rows) fp32 of X:
+    one scale per row and group of g along K (App. D).  Quantize B through
+    its transpose."""
+    _cuda(X, torch.float32)
+    rows, K = X.shape
+    codes = torch.empty((rows, K), dtype=torch.int8, device=X.device)
+    d = torch.empty((K // g, rows), dtype=torch.float32, device=X.device)
+    _check(lib.fm_int8_quantize(_dptr(X), rows, K, g, b, _dptr(codes), _dptr(d),
+                                _dptr(flag) if flag is not None else None, _stream(stream)))
+    return codes, d
+
+
+def int8_matmul_classical(Ac, dA, BTc, dB, g: int = 128, out=None, stream=None):
+    """The classical int8 operator: Ac (M, K), BTc (N, K) codes; dA (K/g, M),
+    dB (K/g, N); fp32 output (M, N)."""
+    _cuda(Ac, torch.int8), _cuda(BTc, torch.int8), _cuda(dA, torch.float32), _cuda(dB, torch.float32)
+    M, K = Ac.shape
+    N = BTc.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=Ac.device)
+    _check(lib.fm_int8_matmul_classical(_dptr(Ac), _dptr(dA), _dptr(BTc), _dptr(dB), M, N, K, g,
+                                        _dptr(out), _stream(stream)))
+    return out
+
+
+def int8_certify(s: Scheme, levels: int = 1, b_A: int = 31, b_B: int = 31, h: int = 32,
+                 g: int = 128) -> dict:
+    """Prop. 1's conditions (i)-(iii) and L_A, L_B, L_W for the flattened scheme."""
+    cond = (ct.c_int * 3)()
+    L = (ct.c_double * 3)()
+    _check(lib.fm_int8_certify(s.handle, levels, b_A, b_B, h, g, cond, L))
+    return dict(i=bool(cond[0]), ii=bool(cond[1]), iii=bool(cond[2]),
+                certified=bool(cond[0] and cond[1] and cond[2]), L_A=L[0], L_B=L[1], L_W=L[2])
+
+
+def int8_workspace_size(s: Scheme, M: int, N: int, K: int, levels: int = 1, g: int = 128,
+                        h: int = 32) -> int:
+    return int(lib.fm_int8_workspace_size(s.handle, levels, M, N, K, g, h))
+
+
+def int8_matmul_fast(s: Scheme, Ac, dA, BTc, dB, levels: int = 1, g: int = 128, h: int = 32,
+                     b_A: int = 31, b_B: int = 31, ws=None, out=None, stream=None):
+    """The certified fast realization (Sec. 4.2): same output bits as
+    int8_matmul_classical for codes within the bounds."""
+    _cuda(Ac, torch.int8), _cuda(BTc, torch.int8), _cuda(dA, torch.float32), _cuda(dB, torch.float32)
+    M, K = Ac.shape
+    N = BTc.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=Ac.device)
+    if ws is None:
+        n = int8_workspace_size(s, M, N, K, levels, g, h)
+        if n == 0:
+            raise FmError(-1, "fm_int8_workspace_size: arguments not supported")
+        ws = workspace(n, Ac.device)
+    _check(lib.fm_int8_matmul_fast(s.handle, levels, _dptr(Ac), _dptr(dA), _dptr(BTc), _dptr(dB),
+                                   M, N, K, g, h, b_A, b_B, _dptr(out), _dptr(ws), ws.numel(),
+                                   _stream(stream)))
+    return out

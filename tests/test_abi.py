@@ -197,3 +197,25 @@ def test_batched_gauge_equals_single_calls():
     with pytest.raises(fm.FmError) as e:
         s1.gauge_orbit([gls[0], (np.zeros((2, 2)), np.eye(2), np.eye(2))])
     assert e.value.name == "FM_E_SINGULAR"
+
+
+def test_int8_certificate_from_the_library():
+    """Prop. 1's quantities as the library computes them (host side): the
+    printed L_A = L_B = 4, L_W = 16 for two-level Strassen, certified at code
+    bound 31 with blocks of 32 in groups of 128, not at 32 or with a call
+    spanning two groups; agrees with the oracle's certificate."""
+    s = fm.Scheme.base("strassen")
+    c = fm.int8_certify(s, 2, 31, 31, 32, 128)
+    assert (c["L_A"], c["L_B"], c["L_W"]) == (4, 4, 16) and c["certified"]
+    assert not fm.int8_certify(s, 2, 32, 32, 32, 128)["i"]
+    assert not fm.int8_certify(s, 2, 31, 31, 8730, 128)["ii"]
+    assert not fm.int8_certify(s, 2, 31, 31, 32, 96)["iii"]
+    o = oracle.certificate(so.power(osch.strassen(), 2), 31, 31, 32, 128, 4)
+    assert o["certified"] and (o["L_A"], o["L_B"], o["L_W"]) == (4, 4, 16)
+    one = fm.int8_certify(s, 1, 63, 63, 64, 128)
+    assert (one["L_A"], one["L_B"], one["L_W"]) == (2, 2, 4) and one["certified"]
+    # non-integer coefficients (a GL gauge) cannot be certified
+    P, Q, S = sy.gl_gauges(2, 2, 2, 1, seed=3)[0]
+    with pytest.raises(fm.FmError) as e:
+        fm.int8_certify(s.gauge(P, Q, S), 1, 31, 31, 32, 128)
+    assert e.value.name == "FM_E_ARG"

@@ -1,0 +1,141 @@
+"""GPU parity of the integer path through the C ABI: the quantizer and the
+classical int8 operator bit for bit against the CPU oracle, and the
+certified fast realization (Sec. 4.2, Prop. 1) bit for bit against the
+classical operator -- for two-level Strassen at code bound 31 (blocks of 32,
+groups of 128), every one of its 512 sign variants, and one-level Strassen
+at code bound 63.  Uncertified configurations are rejected before any
+kernel runs; codes beyond the certified bound are reported.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import scheme_ops as so
+from oracle import schemes as osch
+import synthetic as sy
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU-only machines, never run
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2609_39816_amd import fm  # noqa: E402
+
+DEV = torch.device("cuda:0")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def gpu(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def bits(x):
+    return np.ascontiguousarray(x, np.float32).view(np.uint32)
+
+
+def quantize_both(A, B, g, b):
+    """Device codes and scales (B through its transpose) and the oracle's."""
+    Ac, dA = fm.int8_quantize(gpu(A), g, b)
+    BTc, dB = fm.int8_quantize(gpu(np.ascontiguousarray(B.T)), g, b)
+    oAc, odA = oracle.int8_quantize_a(A, g, b)
+    oBc, odB = oracle.int8_quantize_b(B, g, b)
+    return (Ac, dA, BTc, dB), (oAc, odA, oBc, odB)
+
+
+@pytest.mark.parametrize("M,K,N,g,b", [(96, 384, 80, 128, 31), (64, 512, 200, 256, 127),
+                                       (300, 256, 132, 128, 63)])
+def test_quantizer_and_classical_operator_bit_exact(M, K, N, g, b):
+    say(f"[int8] classical {M}x{K}x{N} g={g} b={b}")
+    rng = np.random.default_rng(M + K + N)
+    A = (rng.standard_normal((M, K)) * rng.uniform(0.1, 10, (M, 1))).astype(np.float32)
+    B = rng.standard_normal((K, N)).astype(np.float32)
+    (Ac, dA, BTc, dB), (oAc, odA, oBc, odB) = quantize_both(A, B, g, b)
+    assert np.array_equal(Ac.cpu().numpy(), oAc)
+    assert np.array_equal(BTc.cpu().numpy(), oBc.T)
+    assert np.array_equal(bits(dA.cpu().numpy()), bits(odA.T))
+    assert np.array_equal(bits(dB.cpu().numpy()), bits(odB))
+    out = fm.int8_matmul_classical(Ac, dA, BTc, dB, g).cpu().numpy()
+    want = oracle.int8_classical(oAc, odA, oBc, odB, g)
+    assert np.array_equal(bits(out), bits(want))
+
+
+def fast_vs_classical(s, levels, M, K, N, g, h, b, seed, variants=None):
+    rng = np.random.default_rng(seed)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    B = rng.standard_normal((K, N)).astype(np.float32)
+    (Ac, dA, BTc, dB), (oAc, odA, oBc, odB) = quantize_both(A, B, g, b)
+    cl = fm.int8_matmul_classical(Ac, dA, BTc, dB, g).cpu().numpy()
+    assert np.array_equal(bits(cl), bits(oracle.int8_classical(oAc, odA, oBc, odB, g)))
+    schemes = [s] if variants is None else variants
+    ws = fm.workspace(fm.int8_workspace_size(schemes[0], M, N, K, levels, g, h))
+    for sc in schemes:
+        out = fm.int8_matmul_fast(sc, Ac, dA, BTc, dB, levels, g, h, b, b, ws=ws).cpu().numpy()
+        fm.status(ws)  # no block sum left int8
+        assert np.array_equal(bits(out), bits(cl))
+    return cl
+
+
+def test_two_level_strassen_equals_classical():
+    say("[int8] fast two-level Strassen 256x512x384")
+    fast_vs_classical(fm.Scheme.base("strassen"), 2, 256, 512, 384, 128, 32, 31, 1)
+
+
+def test_two_level_strassen_groups_of_256_and_ragged_tiles():
+    say("[int8] fast two-level Strassen 400x768x208, g=256")
+    fast_vs_classical(fm.Scheme.base("strassen"), 2, 400, 768, 208, 256, 32, 31, 2)
+
+
+def test_one_level_strassen_at_code_bound_63():
+    say("[int8] fast one-level Strassen b=63 h=64")
+    fast_vs_classical(fm.Scheme.base("strassen"), 1, 192, 384, 136, 128, 64, 63, 3)
+
+
+def test_every_sign_variant_equals_classical():
+    """All 512 sign variants of two-level Strassen on one problem: every
+    output bit equals classical int8's (Sec. 4.2: one distinct output)."""
+    say("[int8] 512 sign variants 64x256x64")
+    s2 = fm.Scheme.base("strassen").kron(2)
+    orbit = s2.gauge_orbit([(np.diag(d), np.diag(e), np.diag(f)) for d, e, f in sy.sign_orbit(4, 4, 4)])
+    fast_vs_classical(None, 1, 64, 256, 64, 128, 32, 31, 4, variants=orbit)
+
+
+def test_larger_problem_equals_classical():
+    say("[int8] fast two-level Strassen 2048x2048x2048")
+    fast_vs_classical(fm.Scheme.base("strassen"), 2, 2048, 2048, 2048, 128, 32, 31, 5)
+
+
+def test_uncertified_configurations_are_rejected():
+    """Prop. 1 is checked before any kernel: code bound 32 (block sums can
+    reach 128), a call spanning two groups, GL-gauged coefficients."""
+    s = fm.Scheme.base("strassen")
+    z8 = torch.zeros((64, 256), dtype=torch.int8, device=DEV)
+    d = torch.ones((2, 64), dtype=torch.float32, device=DEV)
+    ws = fm.workspace(fm.int8_workspace_size(s, 64, 64, 256, 2, 128, 32))
+    with pytest.raises(fm.FmError) as e:
+        fm.int8_matmul_fast(s, z8, d, z8, d, 2, 128, 32, 32, 32, ws=ws)
+    assert e.value.name == "FM_E_UNCERTIFIED"
+    with pytest.raises(fm.FmError) as e:
+        fm.int8_matmul_fast(s, z8, d, z8, d, 2, 128, 64, 31, 31, ws=ws)  # a call of 256 > 128
+    assert e.value.name in ("FM_E_UNCERTIFIED", "FM_E_WORKSPACE")
+
+
+def test_codes_beyond_the_bound_are_reported():
+    """Codes quantized at 127 but claimed to be within 31: some block sums
+    leave int8; the device flags it and fm_status reports FM_E_RANGE."""
+    rng = np.random.default_rng(6)
+    A = rng.standard_normal((64, 128)).astype(np.float32)
+    B = rng.standard_normal((128, 64)).astype(np.float32)
+    (Ac, dA, BTc, dB), _ = quantize_both(A, B, 128, 127)
+    s = fm.Scheme.base("strassen")
+    ws = fm.workspace(fm.int8_workspace_size(s, 64, 64, 128, 2, 128, 32))
+    fm.int8_matmul_fast(s, Ac, dA, BTc, dB, 2, 128, 32, 31, 31, ws=ws)
+    with pytest.raises(fm.FmError) as e:
+        fm.status(ws)
+    assert e.value.name == "FM_E_RANGE"
