@@ -121,6 +121,77 @@ def cpu_baseline(w, A, B, gauge):
                        f"reconstruction; {t:.2f} s; the float64 reference is not included")
 
 
+# The paper's integer timings (App. E, one H20 at 4096 x 4096 x 4096 from
+# prequantized codes and scales): classical int8 563-774 us over groups of
+# 128/256/512; one Strassen level (code bound 63) 2.04/3.17/2.09x as long as
+# classical int8; two levels (code bound 31, groups of 256) 27.9x.
+PAPER_INT8_RATIO = {("strassen1", 128): 2.04, ("strassen1", 256): 3.17, ("strassen1", 512): 2.09,
+                    ("strassen2", 256): 27.9}
+
+
+def int8_bench(args):
+    """Classical int8 and the certified fast realizations at 4096^3: the
+    upper median of 30 timed calls (HIP events), each after zeroing a 256 MB
+    buffer so no operand stays in the caches, after 8 warmup calls; the fast
+    outputs are checked bit for bit against the classical ones."""
+    import numpy as np
+    import torch
+    from paper_2609_39816_amd import fm
+
+    n = args.int8_size
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    rng = np.random.default_rng(20261202)
+    A = torch.from_numpy(rng.standard_normal((n, n)).astype(np.float32)).to(dev)
+    B = torch.from_numpy(rng.standard_normal((n, n)).astype(np.float32)).to(dev)
+    flush = torch.empty(64 << 20, dtype=torch.float32, device=dev)
+    s = fm.Scheme.base("strassen")
+
+    def timed(fn):
+        for _ in range(8):
+            fn()
+        ts = []
+        for _ in range(30):
+            flush.zero_()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3)
+        return float(np.sort(ts)[len(ts) // 2])
+
+    rows = []
+    configs = [("strassen1", 1, 63, 64, g) for g in (128, 256, 512)] + [("strassen2", 2, 31, 32, 256)]
+    classical_us = {}
+    for name, levels, b, h, g in configs:
+        Ac, dA = fm.int8_quantize(A, g, b)
+        BTc, dB = fm.int8_quantize(B.t().contiguous(), g, b)
+        out_c = torch.empty((n, n), dtype=torch.float32, device=dev)
+        out_f = torch.empty_like(out_c)
+        us_c = timed(lambda: fm.int8_matmul_classical(Ac, dA, BTc, dB, g, out=out_c))
+        ws = fm.workspace(fm.int8_workspace_size(s, n, n, n, levels, g, h))
+        us_f = timed(lambda: fm.int8_matmul_fast(s, Ac, dA, BTc, dB, levels, g, h, b, b, ws=ws,
+                                                 out=out_f))
+        fm.status(ws)
+        same = bool(torch.equal(out_c.view(torch.int32), out_f.view(torch.int32)))
+        classical_us[(b, g)] = us_c
+        rows.append(dict(scheme=name, code_bound=b, group=g, block_inner=h, classical_us=round(us_c, 1),
+                         fast_us=round(us_f, 1), ratio=round(us_f / us_c, 3),
+                         paper_ratio=PAPER_INT8_RATIO.get((name, g)),
+                         classical_tops=round(2.0 * n ** 3 / us_c / 1e6, 1),
+                         bit_identical=same))
+        log(f"[bench] int8 {name} b={b} g={g}: classical {us_c:.1f} us, fast {us_f:.1f} us, "
+            f"ratio {us_f / us_c:.3f}, bits equal {same}")
+    out = {"metric": "certified int8 matmul time relative to classical int8 (4096^3, upper median)",
+           "value": rows[-1]["ratio"], "unit": "x classical int8 (two-level Strassen, b=31, g=256)",
+           "higher_is_better": False, "n_gpus": 1, "data": "synthetic",
+           "config": {"workload": f"int8_{n}x{n}x{n}", "M": n, "K": n, "N": n},
+           "vs_baseline": round(rows[-1]["ratio"] / PAPER_INT8_RATIO[("strassen2", 256)], 4),
+           "rows": rows}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -131,6 +202,9 @@ def main():
     ap.add_argument("--fmt", default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="do not bracket kernels with events")
+    ap.add_argument("--int8", action="store_true",
+                    help="time the integer path (classical int8 and the certified realizations)")
+    ap.add_argument("--int8-size", type=int, default=4096)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -139,6 +213,10 @@ def main():
                                    "shard over GPUs by gauge (see the design notes)",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+
+    if args.int8:
+        int8_bench(args)
+        return
 
     import numpy as np
     import torch
