@@ -353,6 +353,24 @@ int fm_int8_matmul_fast(const fm_scheme* s, int levels, const int8_t* Ac,
                         float* out, void* workspace, size_t ws_bytes,
                         void* hip_stream);
 
+/* A fast call prepared once: fm_int8_plan_create validates and certifies
+ * exactly as fm_int8_matmul_fast does, then writes the scheme's tables and
+ * the tile schedule into the caller's workspace (async on hip_stream, which
+ * orders them before any later work on it).  The plan records the
+ * workspace; keep it alive and unchanged while the plan is used.
+ * fm_int8_plan_run performs the call on new codes and scales of the planned
+ * shapes, with the same result and errors as fm_int8_matmul_fast; runs that
+ * share a plan on different streams race on its workspace.  Library-owned
+ * handle, freed by fm_int8_plan_free (null is ignored). */
+typedef struct fm_int8_plan fm_int8_plan;
+int fm_int8_plan_create(const fm_scheme* s, int levels, int M, int N, int K,
+                        int g, int h, int b_A, int b_B, void* workspace,
+                        size_t ws_bytes, void* hip_stream, fm_int8_plan** out);
+int fm_int8_plan_run(const fm_int8_plan* p, const int8_t* Ac, const float* dA,
+                     const int8_t* BTc, const float* dB, float* out,
+                     void* hip_stream);
+void fm_int8_plan_free(fm_int8_plan* p);
+
 /* Selects, process-wide, how the block products are multiplied (the App. B
  * schedule multiplies FP8 block sums and combines the products in fp32):
  *   FM_ACC_BF16 (default): every FP8 value is widened exactly to bf16 and

@@ -984,8 +984,8 @@ int fm_int8_matmul_classical(const int8_t* Ac, const float* dA, const int8_t* BT
   if (M < 1 || N < 1 || K < 1) return fail(FM_E_ARG, "sizes must be positive");
   if (g < 128 || g % 128 || K % g) return fail(FM_E_SHAPE, "g must be a multiple of 128 dividing K");
   if (M % 4 || N % 4) return fail(FM_E_SHAPE, "M and N must be multiples of 4");
-  return launch_i8_gemm(false, Ac, BTc, nullptr, nullptr, dA, dB, out, nullptr, nullptr, 0, M, N,
-                        K, g, 1, 1, 1, 0, 1, (hipStream_t)hip_stream);
+  return launch_i8_gemm(false, Ac, BTc, nullptr, nullptr, dA, dB, out, nullptr, nullptr, 0,
+                        nullptr, nullptr, 0, M, N, K, g, 1, 1, 1, 0, 1, (hipStream_t)hip_stream);
 }
 
 namespace {
@@ -1038,10 +1038,15 @@ void certify(const IntScheme& is, int bA, int bB, int h, int g, int cond[3]) {
   cond[2] = h > 0 && g % (is.gk * h) == 0;
 }
 
+// Bytes per product in a block-sum coefficient table: the blocks' int8
+// coefficients, zero-padded to whole dwords.
+int coef_stride(int blocks) { return (blocks + 3) / 4 * 4; }
+
 // Fast-path workspace: flags, a zero segment, coefficient tables, segment
-// tables, then per call the block sums T (R x Mb x h), S and -S (R x Nb x h).
+// tables, the tile schedule, then per call the block sums T (R x Mb x h), S
+// and -S (R x Nb x h).
 struct I8Layout {
-  size_t flags, zero, coefa, coefb, segs, segoff, t, s, sn, total;
+  size_t flags, zero, coefa, coefb, segs, segoff, order, order_off, t, s, sn, total;
   int nsegs;
 };
 
@@ -1064,10 +1069,12 @@ I8Layout i8_layout(const IntScheme& is, int M, int N, int K, int h) {
   const size_t ncall = (size_t)K / ((size_t)is.gk * h);
   L.flags = take(kAlign);
   L.zero = take(kAlign);
-  L.coefa = take((size_t)is.R * is.gm * is.gk);
-  L.coefb = take((size_t)is.R * is.gn * is.gk);
+  L.coefa = take((size_t)is.R * coef_stride(is.gm * is.gk));
+  L.coefb = take((size_t)is.R * coef_stride(is.gn * is.gk));
   L.segs = take((size_t)nsegs * 4);
   L.segoff = take((size_t)(is.gm * is.gn + 1) * 4);
+  L.order = take((size_t)i8_fast_tiles(is.gm, is.gn, M / is.gm, N / is.gn) * 4);
+  L.order_off = take(257 * 4);
   L.t = take(ncall * is.R * (M / is.gm) * h);
   L.s = take(ncall * is.R * (N / is.gn) * h);
   L.sn = take(ncall * is.R * (N / is.gn) * h);
@@ -1083,6 +1090,130 @@ int i8_fast_shape_ok(const IntScheme& is, int M, int N, int K, int g, int h) {
     return fail(FM_E_SHAPE, "M and N must be multiples of 4 m^L and 4 n^L");
   if (is.gm * is.gn > 64) return fail(FM_E_UNSUPPORTED, "output grid larger than 64 blocks");
   return FM_OK;
+}
+
+// Validation, certificate, tables and schedule of a fast call (everything
+// that depends on the scheme and the shapes, not on the codes): the tables
+// go to the workspace with one staged copy on st.
+int i8_plan_prepare(const fm_scheme* s, int levels, int M, int N, int K, int g, int h, int b_A,
+                    int b_B, void* workspace, size_t ws_bytes, hipStream_t st, fm_int8_plan& p) {
+  IntScheme is;
+  if (int rc = int_scheme(s, levels, is)) return rc;
+  if (int rc = i8_fast_shape_ok(is, M, N, K, g, h)) return rc;
+  if (b_A < 1 || b_A > 127 || b_B < 1 || b_B > 127) return fail(FM_E_ARG, "code bounds must be in [1, 127]");
+  int cond[3];
+  certify(is, b_A, b_B, h, g, cond);
+  if (!cond[0]) return fail(FM_E_UNCERTIFIED, "condition (i): a block sum of codes can leave int8");
+  if (!cond[1]) return fail(FM_E_UNCERTIFIED, "condition (ii): a partial sum can leave int32");
+  if (!cond[2]) return fail(FM_E_UNCERTIFIED, "condition (iii): a call spans two groups");
+  const int calls_per_group = g / (is.gk * h);
+  // the kernel accumulates a whole group (all its calls) in int32
+  if ((double)calls_per_group * is.LW * h * (is.LA * b_A) * (is.LB * b_B) >= 2147483648.0)
+    return fail(FM_E_UNCERTIFIED, "a group's calls together can leave int32");
+  const int nc = is.gm * is.gn;
+  for (int v : is.W)
+    if (v < -1 || v > 1) return fail(FM_E_UNCERTIFIED, "combination weights must be -1, 0 or 1");
+  const I8Layout L = i8_layout(is, M, N, K, h);
+  if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
+  char* ws = (char*)workspace;
+  // host tables: coefficients per block (A: [r][i*gk + l], B: [r][j*gk + l],
+  // rows zero-padded to coef_stride bytes) and the segments of every output
+  // block (ascending r, padded)
+  const int sa = coef_stride(is.gm * is.gk), sb = coef_stride(is.gn * is.gk);
+  std::vector<int8_t> ca((size_t)is.R * sa, 0), cbt((size_t)is.R * sb, 0);
+  for (int r = 0; r < is.R; ++r) {
+    for (int i = 0; i < is.gm * is.gk; ++i) ca[(size_t)r * sa + i] = (int8_t)is.U[(size_t)r * is.gm * is.gk + i];
+    for (int l = 0; l < is.gk; ++l)
+      for (int j = 0; j < is.gn; ++j)
+        cbt[(size_t)r * sb + j * is.gk + l] = (int8_t)is.V[(size_t)r * is.gk * is.gn + l * is.gn + j];
+  }
+  const int per_step = 128 / h;
+  std::vector<int32_t> segs, off(1, 0);
+  for (int c = 0; c < nc; ++c) {
+    int n = 0;
+    for (int r = 0; r < is.R; ++r) {
+      const int w = is.W[(size_t)r * nc + c];
+      if (!w) continue;
+      segs.push_back(r | (w < 0 ? 1 << 16 : 0));
+      ++n;
+    }
+    if (n == 0) return fail(FM_E_ARG, "an output block combines no products");
+    for (; n % per_step; ++n) segs.push_back(0xffff);
+    off.push_back((int32_t)segs.size());
+  }
+  if ((int)segs.size() != L.nsegs) return fail(FM_E_ARG, "segment table size mismatch");
+  // K steps of every output block's tiles, and their schedule
+  std::vector<int> block_steps(nc);
+  for (int c = 0; c < nc; ++c)
+    block_steps[c] = (K / g) * calls_per_group * (off[c + 1] - off[c]) * h / 128;
+  std::vector<int32_t> order, order_off;
+  const int grid = i8_fast_schedule(is.gm, is.gn, M / is.gm, N / is.gn, block_steps, order, order_off);
+  int rc = FM_OK;
+  if ((rc = launch_fill_u32((uint32_t*)(ws + L.zero), kAlign / 4, 0u, st))) return rc;
+  // the six tables are adjacent in the workspace: one staged copy
+  if ((rc = upload(ws + L.coefa,
+                   {{ca.data(), ca.size()},
+                    {cbt.data(), cbt.size()},
+                    {segs.data(), segs.size() * 4},
+                    {off.data(), off.size() * 4},
+                    {order.data(), order.size() * 4},
+                    {order_off.data(), order_off.size() * 4}},
+                   {0, L.coefb - L.coefa, L.segs - L.coefa, L.segoff - L.coefa,
+                    L.order - L.coefa, L.order_off - L.coefa},
+                   L.order_off - L.coefa + order_off.size() * 4, st)))
+    return rc;
+  p.M = M;
+  p.N = N;
+  p.K = K;
+  p.g = g;
+  p.h = h;
+  p.gm = is.gm;
+  p.gn = is.gn;
+  p.gk = is.gk;
+  p.R = is.R;
+  p.calls_per_group = calls_per_group;
+  p.nsegs = (int)segs.size();
+  p.grid = grid;
+  p.sa = sa;
+  p.sb = sb;
+  p.ws = ws;
+  p.ws_bytes = ws_bytes;
+  p.flags = L.flags;
+  p.zero = L.zero;
+  p.coefa = L.coefa;
+  p.coefb = L.coefb;
+  p.segs = L.segs;
+  p.segoff = L.segoff;
+  p.order = L.order;
+  p.order_off = L.order_off;
+  p.t = L.t;
+  p.s = L.s;
+  p.sn = L.sn;
+  return FM_OK;
+}
+
+// One fast call on a prepared workspace: block sums of A and B, then the
+// grouped products.
+int i8_plan_run(const fm_int8_plan& p, const int8_t* Ac, const float* dA, const int8_t* BTc,
+                const float* dB, float* out, hipStream_t st) {
+  if (!Ac || !dA || !BTc || !dB || !out) return fail(FM_E_ARG, "null pointer");
+  char* ws = p.ws;
+  uint32_t* flag = (uint32_t*)(ws + p.flags);
+  int8_t* T = (int8_t*)(ws + p.t);
+  int8_t* S = (int8_t*)(ws + p.s);
+  int8_t* Sn = (int8_t*)(ws + p.sn);
+  int rc = FM_OK;
+  if ((rc = launch_fill_u32(flag, kAlign / 4, 0u, st))) return rc;
+  if ((rc = launch_i8_form(Ac, p.M, p.K, p.gm, p.gk, p.h, p.R, (const int8_t*)(ws + p.coefa), p.sa,
+                           T, nullptr, flag, st)))
+    return rc;
+  if ((rc = launch_i8_form(BTc, p.N, p.K, p.gn, p.gk, p.h, p.R, (const int8_t*)(ws + p.coefb), p.sb,
+                           S, Sn, flag, st)))
+    return rc;
+  return launch_i8_gemm(true, T, S, Sn, (const int8_t*)(ws + p.zero), dA, dB, out,
+                        (const int32_t*)(ws + p.segs), (const int32_t*)(ws + p.segoff), p.nsegs,
+                        (const int32_t*)(ws + p.order), (const int32_t*)(ws + p.order_off), p.grid,
+                        p.M, p.N, p.K, p.g, p.gm, p.gn, p.R, p.h, p.calls_per_group, st);
 }
 }  // namespace
 
@@ -1106,81 +1237,41 @@ size_t fm_int8_workspace_size(const fm_scheme* s, int levels, int M, int N, int 
   return i8_layout(is, M, N, K, h).total;
 }
 
+int fm_int8_plan_create(const fm_scheme* s, int levels, int M, int N, int K, int g, int h,
+                        int b_A, int b_B, void* workspace, size_t ws_bytes, void* hip_stream,
+                        fm_int8_plan** out) {
+  clear_error();
+  if (!out) return fail(FM_E_ARG, "null pointer");
+  *out = nullptr;
+  std::unique_ptr<fm_int8_plan> p(new (std::nothrow) fm_int8_plan());
+  if (!p) return fail(FM_E_ARG, "out of host memory");
+  if (int rc = i8_plan_prepare(s, levels, M, N, K, g, h, b_A, b_B, workspace, ws_bytes,
+                               (hipStream_t)hip_stream, *p))
+    return rc;
+  *out = p.release();
+  return FM_OK;
+}
+
+int fm_int8_plan_run(const fm_int8_plan* p, const int8_t* Ac, const float* dA, const int8_t* BTc,
+                     const float* dB, float* out, void* hip_stream) {
+  clear_error();
+  if (!p) return fail(FM_E_ARG, "null plan");
+  return i8_plan_run(*p, Ac, dA, BTc, dB, out, (hipStream_t)hip_stream);
+}
+
+void fm_int8_plan_free(fm_int8_plan* p) { delete p; }
+
 int fm_int8_matmul_fast(const fm_scheme* s, int levels, const int8_t* Ac, const float* dA,
                         const int8_t* BTc, const float* dB, int M, int N, int K, int g, int h,
                         int b_A, int b_B, float* out, void* workspace, size_t ws_bytes,
                         void* hip_stream) {
   clear_error();
   if (!Ac || !dA || !BTc || !dB || !out) return fail(FM_E_ARG, "null pointer");
-  IntScheme is;
-  if (int rc = int_scheme(s, levels, is)) return rc;
-  if (int rc = i8_fast_shape_ok(is, M, N, K, g, h)) return rc;
-  if (b_A < 1 || b_A > 127 || b_B < 1 || b_B > 127) return fail(FM_E_ARG, "code bounds must be in [1, 127]");
-  int cond[3];
-  certify(is, b_A, b_B, h, g, cond);
-  if (!cond[0]) return fail(FM_E_UNCERTIFIED, "condition (i): a block sum of codes can leave int8");
-  if (!cond[1]) return fail(FM_E_UNCERTIFIED, "condition (ii): a partial sum can leave int32");
-  if (!cond[2]) return fail(FM_E_UNCERTIFIED, "condition (iii): a call spans two groups");
-  const int calls_per_group = g / (is.gk * h);
-  // the kernel accumulates a whole group (all its calls) in int32
-  if ((double)calls_per_group * is.LW * h * (is.LA * b_A) * (is.LB * b_B) >= 2147483648.0)
-    return fail(FM_E_UNCERTIFIED, "a group's calls together can leave int32");
-  const int nc = is.gm * is.gn;
-  for (int v : is.W)
-    if (v < -1 || v > 1) return fail(FM_E_UNCERTIFIED, "combination weights must be -1, 0 or 1");
-  const I8Layout L = i8_layout(is, M, N, K, h);
-  if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
+  fm_int8_plan p;
   hipStream_t st = (hipStream_t)hip_stream;
-  char* ws = (char*)workspace;
-  // host tables: coefficients per block (A: [r][i*gk + l], B: [r][j*gk + l])
-  // and the segments of every output block (ascending r, padded)
-  std::vector<int8_t> ca((size_t)is.R * is.gm * is.gk), cbt((size_t)is.R * is.gn * is.gk);
-  for (int r = 0; r < is.R; ++r) {
-    for (int i = 0; i < is.gm * is.gk; ++i) ca[(size_t)r * is.gm * is.gk + i] = (int8_t)is.U[(size_t)r * is.gm * is.gk + i];
-    for (int l = 0; l < is.gk; ++l)
-      for (int j = 0; j < is.gn; ++j)
-        cbt[(size_t)r * is.gn * is.gk + j * is.gk + l] = (int8_t)is.V[(size_t)r * is.gk * is.gn + l * is.gn + j];
-  }
-  const int per_step = 128 / h;
-  std::vector<int32_t> segs, off(1, 0);
-  for (int c = 0; c < nc; ++c) {
-    int n = 0;
-    for (int r = 0; r < is.R; ++r) {
-      const int w = is.W[(size_t)r * nc + c];
-      if (!w) continue;
-      segs.push_back(r | (w < 0 ? 1 << 16 : 0));
-      ++n;
-    }
-    if (n == 0) return fail(FM_E_ARG, "an output block combines no products");
-    for (; n % per_step; ++n) segs.push_back(0xffff);
-    off.push_back((int32_t)segs.size());
-  }
-  int rc = FM_OK;
-  if ((rc = launch_fill_u32((uint32_t*)(ws + L.flags), kAlign / 4, 0u, st))) return rc;
-  if ((rc = launch_fill_u32((uint32_t*)(ws + L.zero), kAlign / 4, 0u, st))) return rc;
-  if ((int)segs.size() != L.nsegs) return fail(FM_E_ARG, "segment table size mismatch");
-  // the four tables are adjacent in the workspace: one staged copy
-  if ((rc = upload(ws + L.coefa,
-                   {{ca.data(), ca.size()},
-                    {cbt.data(), cbt.size()},
-                    {segs.data(), segs.size() * 4},
-                    {off.data(), off.size() * 4}},
-                   {0, L.coefb - L.coefa, L.segs - L.coefa, L.segoff - L.coefa},
-                   L.segoff - L.coefa + off.size() * 4, st)))
+  if (int rc = i8_plan_prepare(s, levels, M, N, K, g, h, b_A, b_B, workspace, ws_bytes, st, p))
     return rc;
-  uint32_t* flag = (uint32_t*)(ws + L.flags);
-  int8_t* T = (int8_t*)(ws + L.t);
-  int8_t* S = (int8_t*)(ws + L.s);
-  int8_t* Sn = (int8_t*)(ws + L.sn);
-  if ((rc = launch_i8_form(Ac, M, K, is.gm, is.gk, h, is.R, (const int8_t*)(ws + L.coefa), T,
-                           nullptr, flag, st)))
-    return rc;
-  if ((rc = launch_i8_form(BTc, N, K, is.gn, is.gk, h, is.R, (const int8_t*)(ws + L.coefb), S, Sn,
-                           flag, st)))
-    return rc;
-  return launch_i8_gemm(true, T, S, Sn, (const int8_t*)(ws + L.zero), dA, dB, out,
-                        (const int32_t*)(ws + L.segs), (const int32_t*)(ws + L.segoff),
-                        (int)segs.size(), M, N, K, g, is.gm, is.gn, is.R, h, calls_per_group, st);
+  return i8_plan_run(p, Ac, dA, BTc, dB, out, st);
 }
 
 }  // extern "C"

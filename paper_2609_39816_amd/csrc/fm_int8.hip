@@ -5,9 +5,10 @@
 //  i8_quantize_kernel  codes x / d rounded to nearest even, d = max|x| / b,
 //                      one scale per row and group of g along the inner
 //                      dimension (B is quantized through its transpose).
-//  i8_form_kernel      block sums of codes for every call of the fast
+//  i8_form_dot_kernel  block sums of codes for every call of the fast
 //                      realization (exact integers; a flag records any that
-//                      leaves int8).
+//                      leaves int8), on v_dot4 for up to 16 blocks;
+//                      i8_form_kernel for larger grids.
 //  i8_gemm_kernel      grouped int8 products on the matrix cores
 //                      (v_mfma_i32_16x16x64_i8, exact int32 sums), each
 //                      group's integer product rescaled as (P dA) dB and
@@ -19,6 +20,10 @@
 //                      C_c = sum_r w_rc T_r S_r = [T_r ...] [w_rc S_r ...]^T,
 //                      exact in int32 under the certificate.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <utility>
+#include <vector>
 
 #include "fm_device.h"
 #include "fm_lds_ring.h"
@@ -71,14 +76,110 @@ __global__ __launch_bounds__(kThreads) void i8_quantize_kernel(const float* __re
 // X: rows x K codes (A, or B's transpose); for every call kappa (gk blocks of
 // inner length h, consecutive along K) and product r:
 //   out[kappa][r][x][y] = sum_{p,q} coef[r][p*gk + q] * X[p*br + x][kappa*gk*h + q*h + y]
-// for x < br = rows / gp, y < h; with neg, outn holds the negation.  One
-// thread per (kappa, x, four consecutive y) and all r.  The sums are exact
-// in int32; any outside int8 sets *flag (the certificate rules it out for
-// codes within the bound).
+// for x < br = rows / gp, y < h; with neg, outn holds the negation.  coef is
+// int8 with a row stride of `stride` bytes (zero beyond the gp*gk blocks).
+// The sums are exact in int32; any outside [-127, 127] sets bit 2 of *flag
+// (the certificate rules it out for codes within the bound).
+
+// Bytewise two's-complement negation of four packed int8 (no carries between
+// bytes: the low seven bits of ~x + 1 never carry past bit 7).
+__device__ __forceinline__ uint32_t neg_bytes(uint32_t x) {
+  const uint32_t n = ~x;
+  return ((n & 0x7f7f7f7fu) + 0x01010101u) ^ (n & 0x80808080u);
+}
+
+__device__ __forceinline__ uint32_t byte_of(uint32_t x, int j) { return (x >> (8 * j)) & 0xffu; }
+
+__device__ __forceinline__ uint32_t dword_of(const uint4& v, int w) {
+  return w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
+}
+
+// Up to 4 * NG blocks (NG packed dwords of coefficients per product): one
+// thread per (call, row x, 16 consecutive y) and grid row per group of rg
+// products.  The thread loads
+// each block's 16 bytes once, transposes them so that one dword holds four
+// blocks' codes at one position, and forms every product of its group with
+// v_dot4 (four int8 products summed exactly into int32) against the packed
+// coefficient dwords, which are wave-uniform.
+template <int NG>
+__global__ __launch_bounds__(kThreads) void i8_form_dot_kernel(
+    const int8_t* __restrict__ X, int rows, int K, int gp, int gk, int h, int R, int rg,
+    const int8_t* __restrict__ coef, int stride, int8_t* __restrict__ out,
+    int8_t* __restrict__ outn, uint32_t* flag) {
+  const int br = rows / gp;
+  const int hc = h / 16;
+  const int ncall = K / (gk * h);
+  const int rgi = blockIdx.y;  // product group: wave-uniform, so coefficients load as scalars
+  const long long id = (long long)blockIdx.x * kThreads + threadIdx.x;
+  const long long per_call = (long long)br * hc;
+  if (id >= per_call * ncall) return;
+  const int kap = (int)(id / per_call);
+  const int rem = (int)(id - kap * per_call);
+  const int x = rem / hc, y0 = (rem - (rem / hc) * hc) * 16;
+  const int nb = gp * gk;
+  // t[w][G][j]: byte i is block 4G+i's code at position y0 + 4w + j
+  uint32_t t[4][NG][4];
+#pragma unroll
+  for (int G = 0; G < NG; ++G) {
+    uint4 v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int bi = 4 * G + i;
+      if (bi < nb) {
+        const int p = bi / gk, q = bi - (bi / gk) * gk;
+        v[i] = *reinterpret_cast<const uint4*>(X + (size_t)(p * br + x) * K +
+                                               (size_t)kap * gk * h + q * h + y0);
+      } else {
+        v[i] = make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t d[4] = {dword_of(v[0], w), dword_of(v[1], w), dword_of(v[2], w),
+                             dword_of(v[3], w)};
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        t[w][G][j] = byte_of(d[0], j) | (byte_of(d[1], j) << 8) | (byte_of(d[2], j) << 16) |
+                     (byte_of(d[3], j) << 24);
+    }
+  }
+  const auto cf = ro(reinterpret_cast<const int32_t*>(coef));
+  const int sw = stride / 4;
+  uint32_t worst = 0u;  // max of s + 127 over the sums, unsigned: > 254 leaves int8
+  const int r0 = rgi * rg, r1 = min(R, r0 + rg);
+  for (int r = r0; r < r1; ++r) {
+    int c[NG];
+#pragma unroll
+    for (int G = 0; G < NG; ++G) c[G] = cf[(size_t)r * sw + G];
+    uint32_t o[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      uint32_t packed = 0u;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        int s = 0;
+#pragma unroll
+        for (int G = 0; G < NG; ++G) s = __builtin_amdgcn_sdot4((int)t[w][G][j], c[G], s, false);
+        worst = max(worst, (uint32_t)(s + 127));
+        packed |= ((uint32_t)s & 0xffu) << (8 * j);
+      }
+      o[w] = packed;
+    }
+    const size_t off = (((size_t)kap * R + r) * br + x) * h + y0;
+    *reinterpret_cast<uint4*>(out + off) = make_uint4(o[0], o[1], o[2], o[3]);
+    if (outn)
+      *reinterpret_cast<uint4*>(outn + off) =
+          make_uint4(neg_bytes(o[0]), neg_bytes(o[1]), neg_bytes(o[2]), neg_bytes(o[3]));
+  }
+  if (worst > 254u && flag) atomicOr(flag, 2u);
+}
+
+// Any number of blocks: one thread per (call, x, four consecutive y) and all
+// products, each block's four codes loaded per nonzero coefficient.
 __global__ __launch_bounds__(kThreads) void i8_form_kernel(const int8_t* __restrict__ X, int rows,
                                                            int K, int gp, int gk, int h, int R,
                                                            const int8_t* __restrict__ coef,
-                                                           int8_t* __restrict__ out,
+                                                           int stride, int8_t* __restrict__ out,
                                                            int8_t* __restrict__ outn,
                                                            uint32_t* flag) {
   const int br = rows / gp;
@@ -95,7 +196,7 @@ __global__ __launch_bounds__(kThreads) void i8_form_kernel(const int8_t* __restr
     int s0 = 0, s1 = 0, s2 = 0, s3 = 0;
     for (int p = 0; p < gp; ++p)
       for (int q = 0; q < gk; ++q) {
-        const int c = cf[(size_t)r * gp * gk + p * gk + q];
+        const int c = cf[(size_t)r * stride + p * gk + q];
         if (c == 0) continue;
         const char4 v = *reinterpret_cast<const char4*>(
             X + (size_t)(p * br + x) * K + (size_t)kap * gk * h + q * h + y0);
@@ -125,17 +226,30 @@ struct I8Args {
   float* out;           // M x N
   const int32_t* segs;  // fast: segments per block, r | (w < 0) << 16; r = 0xffff: padding
   const int32_t* seg_off;  // fast: gm * gn + 1 offsets into segs
+  const int32_t* order;    // fast: the tiles of every workgroup, consecutively
+  const int32_t* order_off;  // fast: gridDim.x + 1 offsets into order
   int M, N, K, g;
   int gm, gn, Mb, Nb, tiles_m, tiles_n, total;
-  int R, h, calls_per_group;
+  int R, calls_per_group;
 };
 
 constexpr int SCALE_BYTES = 2048;            // per stage: dA (1 KB) + dB (1 KB slot)
 constexpr int I8STAGE = DSTAGE + SCALE_BYTES;
 constexpr int MAX_SEGS = 1024;
 
-template <bool FAST>
+// Position of a workgroup in its work: the slot of its tile list (fast) or
+// the tile itself (classical), the tile's geometry and K-step count per
+// call, and the step (group gi, call kc within the group, step st within the
+// call).  All wave-uniform; advanced incrementally so that no step divides.
+struct I8Cursor {
+  int slot, ib, jb, m0, n0, spc, sb, gi, kc, st;
+};
+
+// H: the block inner length h of the fast realization (0: classical).
+template <int H>
 __global__ __launch_bounds__(DNT) void i8_gemm_kernel(I8Args a) {
+  constexpr bool FAST = H > 0;
+  static_assert(!FAST || (H >= 16 && H <= GK && GK % H == 0), "block inner length");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[DNS * I8STAGE];
   __shared__ int32_t seg_lds[FAST ? MAX_SEGS : 1];
   __shared__ int32_t off_lds[FAST ? 65 : 1];
@@ -146,6 +260,7 @@ __global__ __launch_bounds__(DNT) void i8_gemm_kernel(I8Args a) {
   const int q = lane >> 4, l16 = lane & 15;
   const int tiles_blk = a.tiles_m * a.tiles_n;
   const int ng = a.K / a.g;
+  const int cpg = FAST ? a.calls_per_group : 1;
   if constexpr (FAST) {
     const int nb = a.gm * a.gn;
     for (int i = tid; i <= nb; i += DNT) off_lds[i] = ro(a.seg_off)[i];
@@ -153,81 +268,102 @@ __global__ __launch_bounds__(DNT) void i8_gemm_kernel(I8Args a) {
     for (int i = tid; i < ns; i += DNT) seg_lds[i] = ro(a.segs)[i];
     __syncthreads();
   }
-  // K steps per group for the block of a tile
-  auto steps_per_group = [&](int c) -> int {
-    if constexpr (FAST) return a.calls_per_group * (off_lds[c + 1] - off_lds[c]) * a.h / GK;
-    else return a.g / GK;
-  };
   const bool vec_store = (a.Nb & 3) == 0 && (a.N & 3) == 0;
 
-  const int G = gridDim.x;
-  const int total = a.total;
-  const bool xcd_split = (G & 7) == 0 && (total & 7) == 0;
-  const int t = xcd_split ? (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3) : blockIdx.x;
-  const int tstep = xcd_split ? (G >> 3) : G;
-  const int t_end = xcd_split ? ((blockIdx.x & 7) + 1) * (total >> 3) : total;
-  if (t >= t_end) return;
+  // the workgroup's tiles: fast, its list; classical, a stride through the
+  // tiles, consecutive ones on one XCD
+  int slot0, slot_end, slot_step;
+  if constexpr (FAST) {
+    slot0 = ro(a.order_off)[blockIdx.x];
+    slot_end = ro(a.order_off)[blockIdx.x + 1];
+    slot_step = 1;
+  } else {
+    const int G = gridDim.x;
+    const bool xcd_split = (G & 7) == 0 && (a.total & 7) == 0;
+    slot0 = xcd_split ? (blockIdx.x & 7) * (a.total >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+    slot_step = xcd_split ? (G >> 3) : G;
+    slot_end = xcd_split ? ((blockIdx.x & 7) + 1) * (a.total >> 3) : a.total;
+  }
+  if (slot0 >= slot_end) return;
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)lds;
 
-  struct TileGeo {
-    int c, ib, jb, m0, n0;
-  };
-  auto geo = [&](int tile) {
-    TileGeo r;
-    r.c = tile / tiles_blk;
-    const int tt = tile - r.c * tiles_blk;
-    r.ib = r.c / a.gn;
-    r.jb = r.c - r.ib * a.gn;
+  // classical tiles have one block (ib = jb = 0), one call per group and
+  // g / GK steps per call: those fields stay constant and fold away
+  const int spc_cl = a.g / GK;
+  auto spc_of = [&](const I8Cursor& u) { return FAST ? u.spc : spc_cl; };
+  auto enter = [&](I8Cursor& u) {  // u.slot valid: load the tile's geometry
+    const int tile = FAST ? ro(a.order)[u.slot] : u.slot;
+    const int c = tile / tiles_blk;
+    const int tt = tile - c * tiles_blk;
     const int tmi = tt / a.tiles_n;
-    r.m0 = tmi * DBM;
-    r.n0 = (tt - tmi * a.tiles_n) * DBN;
-    return r;
+    u.m0 = tmi * DBM;
+    u.n0 = (tt - tmi * a.tiles_n) * DBN;
+    if constexpr (FAST) {
+      u.ib = c / a.gn;
+      u.jb = c - u.ib * a.gn;
+      u.sb = off_lds[c];
+      u.spc = (off_lds[c + 1] - u.sb) * H / GK;
+    } else {
+      u.ib = u.jb = u.sb = u.spc = 0;
+    }
+    u.gi = u.kc = u.st = 0;
+  };
+  auto advance = [&](I8Cursor& u) {
+    if (++u.st < spc_of(u)) return;
+    u.st = 0;
+    if constexpr (FAST) {
+      if (++u.kc < cpg) return;
+      u.kc = 0;
+    }
+    if (++u.gi < ng) return;
+    u.slot += slot_step;
+    if (u.slot < slot_end) enter(u);
   };
 
-  auto issue = [&](int tile, int kt, int buf) {
-    const TileGeo tg = geo(tile);
-    const int spg = steps_per_group(tg.c);
-    const int gi = kt / spg, sg = kt - (kt / spg) * spg;
-    int kap = 0, st = 0, sbase = 0;
+  auto issue = [&](const I8Cursor& u, int buf) {
+    // row r of the stage (wave-load j, lane) takes 16-byte chunk
+    // (lane & 7) ^ swz(r) = (lane & 7) ^ (lane >> 3) ^ (j & 1)
+    const int ch_even = (lane & 7) ^ (lane >> 3);
+    [[maybe_unused]] int e_even = 0, e_odd = 0;
+    [[maybe_unused]] int kap = 0;
     if constexpr (FAST) {
-      const int spc = spg / a.calls_per_group;  // steps per call
-      const int kc = sg / spc;
-      st = sg - kc * spc;
-      kap = gi * a.calls_per_group + kc;
-      sbase = off_lds[tg.c] + st * (GK / a.h);
+      kap = u.gi * cpg + u.kc;
+      const int sbase = u.sb + u.st * (GK / H);
+      e_even = seg_lds[sbase + (ch_even * 16) / H];
+      e_odd = H >= 32 ? e_even : seg_lds[sbase + ((ch_even ^ 1) * 16) / H];
     }
 #pragma unroll
     for (int j = 0; j < DLOADS; ++j) {
       const int r0 = (wave * DLOADS + j) * 8;  // first of the 8 rows this wave-load fills
       const int r = r0 + (lane >> 3);
-      const int ch = (lane & 7) ^ swz(r);
+      const int ch = ch_even ^ (j & 1);
       const uint8_t* src;
       if constexpr (FAST) {
-        const int s = sbase + (ch * 16) / a.h;
-        const int oin = (ch * 16) % a.h;
-        const int e = seg_lds[s];
+        const int e = (j & 1) ? e_odd : e_even;
         const int pr = e & 0xffff;
+        const int oin = (ch * 16) % H;
         if (r0 < DBM) {
-          int row = tg.m0 + r;
+          int row = u.m0 + r;
           row = row < a.Mb ? row : 0;
           src = pr == 0xffff ? (const uint8_t*)a.zero
-                             : (const uint8_t*)a.A + (((size_t)kap * a.R + pr) * a.Mb + row) * a.h + oin;
+                             : (const uint8_t*)a.A + (((size_t)kap * a.R + pr) * a.Mb + row) * H + oin;
         } else {
-          int col = tg.n0 + r - DBM;
+          int col = u.n0 + r - DBM;
           col = col < a.Nb ? col : 0;
           const int8_t* S = (e >> 16) ? a.Bn : a.B;
           src = pr == 0xffff ? (const uint8_t*)a.zero
-                             : (const uint8_t*)S + (((size_t)kap * a.R + pr) * a.Nb + col) * a.h + oin;
+                             : (const uint8_t*)S + (((size_t)kap * a.R + pr) * a.Nb + col) * H + oin;
         }
       } else {
+        const size_t k0 = (size_t)u.gi * a.g + (size_t)u.st * GK + ch * 16;
         if (r0 < DBM) {
-          int row = tg.m0 + r;
+          int row = u.m0 + r;
           row = row < a.M ? row : 0;
-          src = (const uint8_t*)a.A + (size_t)row * a.K + (size_t)kt * GK + ch * 16;
+          src = (const uint8_t*)a.A + (size_t)row * a.K + k0;
         } else {
-          int col = tg.n0 + r - DBM;
+          int col = u.n0 + r - DBM;
           col = col < a.N ? col : 0;
-          src = (const uint8_t*)a.B + (size_t)col * a.K + (size_t)kt * GK + ch * 16;
+          src = (const uint8_t*)a.B + (size_t)col * a.K + k0;
         }
       }
       dma16(src, lds_base + (uint32_t)(buf * I8STAGE + r0 * GK));
@@ -235,14 +371,14 @@ __global__ __launch_bounds__(DNT) void i8_gemm_kernel(I8Args a) {
     // the group's scales ride with its last step: wave 0 loads dA for the
     // tile's 256 rows, wave 1 dB for its 128 columns (lanes 32-63 repeat
     // lanes 0-31); 4 rows or columns per lane, all in or all out of range
-    if (sg == spg - 1 && wave < 2) {
+    if (u.st == spc_of(u) - 1 && (!FAST || u.kc == cpg - 1) && wave < 2) {
       const float* src;
       if (wave == 0) {
-        const int row = tg.m0 + 4 * lane;
-        src = a.dA + (size_t)gi * a.M + (size_t)tg.ib * a.Mb + (row < a.Mb ? row : 0);
+        const int row = u.m0 + 4 * lane;
+        src = a.dA + (size_t)u.gi * a.M + (size_t)u.ib * a.Mb + (row < a.Mb ? row : 0);
       } else {
-        const int col = tg.n0 + 4 * (lane & 31);
-        src = a.dB + (size_t)gi * a.N + (size_t)tg.jb * a.Nb + (col < a.Nb ? col : 0);
+        const int col = u.n0 + 4 * (lane & 31);
+        src = a.dB + (size_t)u.gi * a.N + (size_t)u.jb * a.Nb + (col < a.Nb ? col : 0);
       }
       dma16(src, lds_base + (uint32_t)(buf * I8STAGE + DSTAGE + wave * 1024));
     }
@@ -311,12 +447,11 @@ __global__ __launch_bounds__(DNT) void i8_gemm_kernel(I8Args a) {
         acc[i][j] = (v4i){0, 0, 0, 0};
       }
   };
-  auto epilogue = [&](int tile) -> int {  // returns the number of stores counted
-    const TileGeo tg = geo(tile);
-    const int r_base = tg.m0 + wm * 64 + l16, c_base = tg.n0 + wn * 64 + 4 * q;
-    float* Ob = a.out + (size_t)tg.ib * a.Mb * a.N + (size_t)tg.jb * a.Nb;
+  auto epilogue = [&](const I8Cursor& u) -> int {  // returns the number of stores counted
+    const int r_base = u.m0 + wm * 64 + l16, c_base = u.n0 + wn * 64 + 4 * q;
+    float* Ob = a.out + (size_t)u.ib * a.Mb * a.N + (size_t)u.jb * a.Nb;
     int counted = 0;
-    if (vec_store && tg.m0 + DBM <= a.Mb && tg.n0 + DBN <= a.Nb) {
+    if (vec_store && u.m0 + DBM <= a.Mb && u.n0 + DBN <= a.Nb) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float* prow = Ob + (size_t)(r_base + i * 16) * a.N + c_base;
@@ -346,67 +481,59 @@ __global__ __launch_bounds__(DNT) void i8_gemm_kernel(I8Args a) {
     return counted;
   };
 
-  // (tile, K-step) pairs p_0, p_1, ... in LDS buffer s mod 3, as in the
-  // block-product kernel; a group ends with the last K step of its span
-  auto nsteps = [&](int tile) { return ng * steps_per_group(tile / tiles_blk); };
-  auto advance = [&](int& tt, int& kk) {
-    if (++kk == nsteps(tt)) {
-      kk = 0;
-      tt += tstep;
-    }
-  };
-  int t1 = t, k1 = 0;
-  advance(t1, k1);
-  int t2 = t1, k2 = k1;
-  advance(t2, k2);
-  int t3 = t2, k3 = k2;
-  advance(t3, k3);
-  int ct = t, ck = 0;
-  issue(ct, ck, 0);
+  // K steps s_0, s_1, ... (cursors u0..u3) in LDS buffer s mod 3, as in the
+  // block-product kernel; a group ends with the last step of its last call
+  I8Cursor u0;
+  u0.slot = slot0;
+  enter(u0);
+  I8Cursor u1 = u0;
+  advance(u1);
+  I8Cursor u2 = u1;
+  advance(u2);
+  I8Cursor u3 = u2;
+  advance(u3);
+  issue(u0, 0);
   int after1 = 0;
-  if (t1 < t_end) issue(t1, k1, 1);
-  if (t2 < t_end) {
-    issue(t2, k2, 2);
+  if (u1.slot < slot_end) issue(u1, 1);
+  if (u2.slot < slot_end) {
+    issue(u2, 2);
     after1 = DLOADS;
   }
-  wait_vm(t1 < t_end ? after1 + DLOADS : 0);
+  wait_vm(u1.slot < slot_end ? after1 + DLOADS : 0);
   FM_COMPILER_FENCE();
   __builtin_amdgcn_s_barrier();
   FM_COMPILER_FENCE();
   read_half(0, 0);
   int cb = 0;
   while (true) {
-    const int spg = steps_per_group(ct / tiles_blk);
-    const bool group_end = (ck % spg) == spg - 1;
+    const bool group_end = u0.st == spc_of(u0) - 1 && (!FAST || u0.kc == cpg - 1);
+    const bool tile_end = group_end && u0.gi == ng - 1;
     read_half(1, cb);
     if (group_end) read_scales(cb);
     compute_half(0);
     wait_vm(after1);
-    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of p_s are done
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of stage cb are done
     FM_COMPILER_FENCE();
     __builtin_amdgcn_s_barrier();
     FM_COMPILER_FENCE();
     const int nb = cb == 2 ? 0 : cb + 1;
     int after2 = 0;
-    if (t3 < t_end) {
-      issue(t3, k3, cb);
+    if (u3.slot < slot_end) {
+      issue(u3, cb);
       after2 = DLOADS;
     }
     FM_COMPILER_FENCE();
-    const bool more = t1 < t_end;
+    const bool more = u1.slot < slot_end;
     if (more) read_half(0, nb);
     compute_half(1);
     if (group_end) rescale();
-    if (ck == nsteps(ct) - 1) after2 += epilogue(ct);
+    if (tile_end) after2 += epilogue(u0);
     FM_COMPILER_FENCE();
     if (!more) break;
-    ct = t1;
-    ck = k1;
-    t1 = t2;
-    k1 = k2;
-    t2 = t3;
-    k2 = k3;
-    advance(t3, k3);
+    u0 = u1;
+    u1 = u2;
+    u2 = u3;
+    advance(u3);
     after1 = after2;
     cb = nb;
   }
@@ -424,19 +551,92 @@ int launch_i8_quantize(const float* X, int rows, int K, int g, int b, int8_t* co
 }
 
 int launch_i8_form(const int8_t* X, int rows, int K, int gp, int gk, int h, int R,
-                   const int8_t* coef, int8_t* out, int8_t* outn, uint32_t* flag, hipStream_t st) {
+                   const int8_t* coef, int stride, int8_t* out, int8_t* outn, uint32_t* flag,
+                   hipStream_t st) {
+  const int nb = gp * gk;
+  const int ng = (nb + 3) / 4;
+  if (h % 16 || stride < 4 * ng || stride % 4) return fail(FM_E_ARG, "block-sum layout");
+  if (ng <= 4) {
+    const int nrg = (R + 7) / 8, rg = (R + nrg - 1) / nrg;
+    const long long n = (long long)(K / (gk * h)) * (rows / gp) * (h / 16);
+    const long long blocks = (n + kThreads - 1) / kThreads;
+    if (blocks > 0x7fffffffLL || nrg > 65535) return fail(FM_E_SHAPE, "too many block sums");
+    const dim3 grid((unsigned)blocks, (unsigned)nrg);
+    switch (ng) {
+#define FM_FORM_DOT(NG)                                                                    \
+  case NG:                                                                                \
+    i8_form_dot_kernel<NG><<<grid, kThreads, 0, st>>>(X, rows, K, gp, gk, h, R, rg, coef, \
+                                                      stride, out, outn, flag);           \
+    break;
+      FM_FORM_DOT(1)
+      FM_FORM_DOT(2)
+      FM_FORM_DOT(3)
+      FM_FORM_DOT(4)
+#undef FM_FORM_DOT
+    }
+    return launched("i8_form_dot_kernel");
+  }
   const long long n = (long long)(K / (gk * h)) * (rows / gp) * (h / 4);
   const long long blocks = (n + kThreads - 1) / kThreads;
   if (blocks > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many block sums");
-  i8_form_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(X, rows, K, gp, gk, h, R, coef, out, outn,
-                                                        flag);
+  i8_form_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(X, rows, K, gp, gk, h, R, coef, stride,
+                                                        out, outn, flag);
   return launched("i8_form_kernel");
+}
+
+long long i8_fast_tiles(int gm, int gn, int Mb, int Nb) {
+  return (long long)gm * gn * ((Mb + DBM - 1) / DBM) * ((Nb + DBN - 1) / DBN);
+}
+
+// Longest-first assignment of the fast kernel's tiles to its workgroups: the
+// tiles of block c cost block_steps[c] K steps plus two for the epilogue;
+// in descending cost (ascending tile among equals) each goes to the least
+// loaded of min(tiles, 256) workgroups (lowest first among equals).  The
+// workgroups are numbered so that consecutive ones share an XCD (the
+// hardware deals workgroup w to XCD w mod 8), which keeps a block's tiles,
+// and the block sums they read, in one L2.
+int i8_fast_schedule(int gm, int gn, int Mb, int Nb, const std::vector<int>& block_steps,
+                     std::vector<int32_t>& order, std::vector<int32_t>& off) {
+  const int tiles_m = (Mb + DBM - 1) / DBM, tiles_n = (Nb + DBN - 1) / DBN;
+  const int per_blk = tiles_m * tiles_n;
+  const int total = gm * gn * per_blk;
+  const int grid = std::min(total, 256);
+  std::vector<int> tiles(total);
+  for (int t = 0; t < total; ++t) tiles[t] = t;
+  auto cost = [&](int t) { return (long long)block_steps[t / per_blk] + 2; };
+  std::stable_sort(tiles.begin(), tiles.end(), [&](int x, int y) { return cost(x) > cost(y); });
+  const int per_xcd = grid % 8 == 0 ? grid / 8 : grid;
+  auto physical = [&](int v) { return grid % 8 == 0 ? 8 * (v % per_xcd) + v / per_xcd : v; };
+  std::vector<long long> load(grid, 0);
+  std::vector<std::vector<int32_t>> lists(grid);
+  // (load, virtual index) min-heap
+  std::vector<std::pair<long long, int>> heap;
+  for (int v = 0; v < grid; ++v) heap.emplace_back(0, v);
+  auto later = [](const std::pair<long long, int>& x, const std::pair<long long, int>& y) {
+    return x > y;
+  };
+  std::make_heap(heap.begin(), heap.end(), later);
+  for (int t : tiles) {
+    std::pop_heap(heap.begin(), heap.end(), later);
+    auto& top = heap.back();
+    lists[physical(top.second)].push_back(t);
+    top.first += cost(t);
+    std::push_heap(heap.begin(), heap.end(), later);
+  }
+  order.clear();
+  off.assign(1, 0);
+  for (int w = 0; w < grid; ++w) {
+    order.insert(order.end(), lists[w].begin(), lists[w].end());
+    off.push_back((int32_t)order.size());
+  }
+  return grid;
 }
 
 int launch_i8_gemm(bool fast, const int8_t* A, const int8_t* B, const int8_t* Bn,
                    const int8_t* zero, const float* dA, const float* dB, float* out,
-                   const int32_t* segs, const int32_t* seg_off, int nsegs, int M, int N, int K,
-                   int g, int gm, int gn, int R, int h, int calls_per_group, hipStream_t st) {
+                   const int32_t* segs, const int32_t* seg_off, int nsegs, const int32_t* order,
+                   const int32_t* order_off, int grid, int M, int N, int K, int g, int gm, int gn,
+                   int R, int h, int calls_per_group, hipStream_t st) {
   I8Args a{};
   a.A = A;
   a.B = B;
@@ -447,6 +647,8 @@ int launch_i8_gemm(bool fast, const int8_t* A, const int8_t* B, const int8_t* Bn
   a.out = out;
   a.segs = segs;
   a.seg_off = seg_off;
+  a.order = order;
+  a.order_off = order_off;
   a.M = M;
   a.N = N;
   a.K = K;
@@ -463,11 +665,19 @@ int launch_i8_gemm(bool fast, const int8_t* A, const int8_t* B, const int8_t* Bn
     return fail(FM_E_UNSUPPORTED, "scheme too large for the fast integer kernel");
   a.total = (int)total;
   a.R = R;
-  a.h = h;
   a.calls_per_group = calls_per_group;
-  const int grid = (int)std::min<long long>(total, 256);
-  if (fast) i8_gemm_kernel<true><<<grid, DNT, 0, st>>>(a);
-  else i8_gemm_kernel<false><<<grid, DNT, 0, st>>>(a);
+  if (!fast) {
+    i8_gemm_kernel<0><<<(int)std::min<long long>(total, 256), DNT, 0, st>>>(a);
+    return launched("i8_gemm_kernel");
+  }
+  if (!order || !order_off || grid < 1 || grid > total) return fail(FM_E_ARG, "tile schedule");
+  switch (h) {
+    case 16: i8_gemm_kernel<16><<<grid, DNT, 0, st>>>(a); break;
+    case 32: i8_gemm_kernel<32><<<grid, DNT, 0, st>>>(a); break;
+    case 64: i8_gemm_kernel<64><<<grid, DNT, 0, st>>>(a); break;
+    case 128: i8_gemm_kernel<128><<<grid, DNT, 0, st>>>(a); break;
+    default: return fail(FM_E_ARG, "h must be 16, 32, 64 or 128");
+  }
   return launched("i8_gemm_kernel");
 }
 

@@ -16,6 +16,17 @@ struct fm_scheme {
   std::vector<double> U, V, W;  // R x (m*k), R x (k*n), R x (m*n)
 };
 
+// A prepared fast integer call (fm_int8_plan_create): shapes, the scheme's
+// block grid and the workspace offsets of its tables and block sums.
+struct fm_int8_plan {
+  int M = 0, N = 0, K = 0, g = 0, h = 0, gm = 0, gn = 0, gk = 0, R = 0;
+  int calls_per_group = 0, nsegs = 0, grid = 0, sa = 0, sb = 0;
+  char* ws = nullptr;
+  size_t ws_bytes = 0;
+  size_t flags = 0, zero = 0, coefa = 0, coefb = 0, segs = 0, segoff = 0, order = 0,
+         order_off = 0, t = 0, s = 0, sn = 0;
+};
+
 namespace fm {
 
 // ---------------------------------------------------------------- errors
@@ -147,11 +158,19 @@ int launch_reduce_rows(const double* partial, int nblk, int G, double* out, hipS
 int launch_i8_quantize(const float* X, int rows, int K, int g, int b, int8_t* codes, float* d,
                        uint32_t* flag, hipStream_t st);
 int launch_i8_form(const int8_t* X, int rows, int K, int gp, int gk, int h, int R,
-                   const int8_t* coef, int8_t* out, int8_t* outn, uint32_t* flag, hipStream_t st);
+                   const int8_t* coef, int stride, int8_t* out, int8_t* outn, uint32_t* flag,
+                   hipStream_t st);
+// Tiles of the fast integer kernel, and their longest-first assignment to
+// workgroups (returns the grid; order holds every workgroup's tiles, off its
+// grid + 1 offsets).
+long long i8_fast_tiles(int gm, int gn, int Mb, int Nb);
+int i8_fast_schedule(int gm, int gn, int Mb, int Nb, const std::vector<int>& block_steps,
+                     std::vector<int32_t>& order, std::vector<int32_t>& off);
 int launch_i8_gemm(bool fast, const int8_t* A, const int8_t* B, const int8_t* Bn,
                    const int8_t* zero, const float* dA, const float* dB, float* out,
-                   const int32_t* segs, const int32_t* seg_off, int nsegs, int M, int N, int K,
-                   int g, int gm, int gn, int R, int h, int calls_per_group, hipStream_t st);
+                   const int32_t* segs, const int32_t* seg_off, int nsegs, const int32_t* order,
+                   const int32_t* order_off, int grid, int M, int N, int K, int g, int gm, int gn,
+                   int R, int h, int calls_per_group, hipStream_t st);
 
 // Float64 reference C = A B.
 int launch_reference_f64(const float* A, const float* B, double* C, int M, int N, int K,

@@ -82,6 +82,9 @@ def _load():
         "fm_int8_certify": (i, [p, i, i, i, i, i, p, p]),
         "fm_int8_workspace_size": (sz, [p, i, i, i, i, i, i]),
         "fm_int8_matmul_fast": (i, [p, i, p, p, p, p, i, i, i, i, i, i, i, p, p, sz, p]),
+        "fm_int8_plan_create": (i, [p, i, i, i, i, i, i, i, i, p, sz, p, pp]),
+        "fm_int8_plan_run": (i, [p, p, p, p, p, p, p]),
+        "fm_int8_plan_free": (None, [p]),
         "fm_fp8_encode": (i, [p, i64, i, i, p, p]),
         "fm_scheme_kernel_family": (ct.c_char_p, [p, i]),
         "fm_status": (i, [p, sz, p]),
@@ -393,14 +396,29 @@ def int8_quantize(X, g: int = 128, b: int = 31, flag=None, stream=None):
     return codes, d
 
 
-def int8_matmul_classical(Ac, dA, BTc, dB, g: int = 128, out=None, stream=None):
-    """The classical int8 operator: Ac (M, K), BTc (N, K) codes; dA (K/g, M),
-    dB (K/g, N); fp32 output (M, N)."""
+def _int8_operands(Ac, dA, BTc, dB, g, out):
+    """Shapes of the integer operators' arguments, checked against each other
+    (the library sees only pointers): Ac (M, K), BTc (N, K) int8; dA (K/g, M),
+    dB (K/g, N) fp32; out (M, N) fp32."""
     _cuda(Ac, torch.int8), _cuda(BTc, torch.int8), _cuda(dA, torch.float32), _cuda(dB, torch.float32)
     M, K = Ac.shape
     N = BTc.shape[0]
+    if BTc.shape[1] != K or g <= 0 or K % g:
+        raise ValueError("Ac and BTc must share K, a multiple of g")
+    if tuple(dA.shape) != (K // g, M) or tuple(dB.shape) != (K // g, N):
+        raise ValueError("scales must be (K/g, M) and (K/g, N)")
     if out is None:
         out = torch.empty((M, N), dtype=torch.float32, device=Ac.device)
+    _cuda(out, torch.float32)
+    if tuple(out.shape) != (M, N):
+        raise ValueError("out must be (M, N)")
+    return M, N, K, out
+
+
+def int8_matmul_classical(Ac, dA, BTc, dB, g: int = 128, out=None, stream=None):
+    """The classical int8 operator: Ac (M, K), BTc (N, K) codes; dA (K/g, M),
+    dB (K/g, N); fp32 output (M, N)."""
+    M, N, K, out = _int8_operands(Ac, dA, BTc, dB, g, out)
     _check(lib.fm_int8_matmul_classical(_dptr(Ac), _dptr(dA), _dptr(BTc), _dptr(dB), M, N, K, g,
                                         _dptr(out), _stream(stream)))
     return out
@@ -425,17 +443,45 @@ def int8_matmul_fast(s: Scheme, Ac, dA, BTc, dB, levels: int = 1, g: int = 128, 
                      b_A: int = 31, b_B: int = 31, ws=None, out=None, stream=None):
     """The certified fast realization (Sec. 4.2): same output bits as
     int8_matmul_classical for codes within the bounds."""
-    _cuda(Ac, torch.int8), _cuda(BTc, torch.int8), _cuda(dA, torch.float32), _cuda(dB, torch.float32)
-    M, K = Ac.shape
-    N = BTc.shape[0]
-    if out is None:
-        out = torch.empty((M, N), dtype=torch.float32, device=Ac.device)
+    M, N, K, out = _int8_operands(Ac, dA, BTc, dB, g, out)
     if ws is None:
-        n = int8_workspace_size(s, M, N, K, levels, g, h)
-        if n == 0:
+        need = int8_workspace_size(s, M, N, K, levels, g, h)
+        if need == 0:
             raise FmError(-1, "fm_int8_workspace_size: arguments not supported")
-        ws = workspace(n, Ac.device)
+        ws = workspace(need, Ac.device)
     _check(lib.fm_int8_matmul_fast(s.handle, levels, _dptr(Ac), _dptr(dA), _dptr(BTc), _dptr(dB),
                                    M, N, K, g, h, b_A, b_B, _dptr(out), _dptr(ws), ws.numel(),
                                    _stream(stream)))
     return out
+
+
+class Int8Plan:
+    """A prepared fast call (fm_int8_plan_*): the scheme's tables and tile
+    schedule are written to the workspace once; run() then launches only the
+    block-sum and product kernels.  Holds its workspace."""
+
+    def __init__(self, s: Scheme, M: int, N: int, K: int, levels: int = 1, g: int = 128,
+                 h: int = 32, b_A: int = 31, b_B: int = 31, ws=None, device=None, stream=None):
+        self._h = None
+        need = int8_workspace_size(s, M, N, K, levels, g, h)
+        if need == 0:
+            raise FmError(-1, "fm_int8_workspace_size: arguments not supported")
+        self.ws = ws if ws is not None else workspace(need, device)
+        self.M, self.N, self.K, self.g = M, N, K, g
+        out = ct.c_void_p()
+        _check(lib.fm_int8_plan_create(s.handle, levels, M, N, K, g, h, b_A, b_B, _dptr(self.ws),
+                                       self.ws.numel(), _stream(stream), ct.byref(out)))
+        self._h = out.value
+
+    def __del__(self):
+        if getattr(self, "_h", None) and lib is not None:
+            lib.fm_int8_plan_free(ct.c_void_p(self._h))
+            self._h = None
+
+    def run(self, Ac, dA, BTc, dB, out=None, stream=None):
+        M, N, K, out = _int8_operands(Ac, dA, BTc, dB, self.g, out)
+        if (M, N, K) != (self.M, self.N, self.K):
+            raise ValueError("operands do not have the planned shapes")
+        _check(lib.fm_int8_plan_run(ct.c_void_p(self._h), _dptr(Ac), _dptr(dA), _dptr(BTc),
+                                    _dptr(dB), _dptr(out), _stream(stream)))
+        return out

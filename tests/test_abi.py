@@ -219,3 +219,23 @@ def test_int8_certificate_from_the_library():
     with pytest.raises(fm.FmError) as e:
         fm.int8_certify(s.gauge(P, Q, S), 1, 31, 31, 32, 128)
     assert e.value.name == "FM_E_ARG"
+
+
+ERR = {v: k for k, v in fm.ERRORS.items()}
+
+
+def test_int8_plan_rejects_before_any_device_work():
+    """fm_int8_plan_create certifies before it touches the device: code
+    bound 32 fails condition (i), a call of 4 x 64 > g = 128 condition (iii);
+    a null plan is an argument error."""
+    s = fm.Scheme.base("strassen")
+    out = ct.c_void_p()
+    rc = fm.lib.fm_int8_plan_create(s.handle, 2, 64, 64, 256, 128, 32, 32, 32, None, 0, None,
+                                    ct.byref(out))
+    assert rc == ERR["FM_E_UNCERTIFIED"] and not out.value
+    rc = fm.lib.fm_int8_plan_create(s.handle, 2, 64, 64, 256, 128, 64, 31, 31, None, 0, None,
+                                    ct.byref(out))
+    assert rc == ERR["FM_E_UNCERTIFIED"] and not out.value
+    assert fm.lib.fm_int8_plan_run(None, None, None, None, None, None, None) == \
+        ERR["FM_E_ARG"]
+    fm.lib.fm_int8_plan_free(None)

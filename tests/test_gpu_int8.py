@@ -139,3 +139,23 @@ def test_codes_beyond_the_bound_are_reported():
     with pytest.raises(fm.FmError) as e:
         fm.status(ws)
     assert e.value.name == "FM_E_RANGE"
+
+
+def test_prepared_plan_runs_new_codes():
+    """A plan made once serves later calls: two runs on different codes of the
+    planned shapes give the classical operator's bits; other shapes are
+    rejected by the binding."""
+    say("[int8] plan: two-level Strassen 256x512x384, two runs")
+    s = fm.Scheme.base("strassen")
+    M, K, N, g, h, b = 256, 512, 384, 128, 32, 31
+    plan = fm.Int8Plan(s, M, N, K, 2, g, h, b, b, device=DEV)
+    for seed in (7, 8):
+        rng = np.random.default_rng(seed)
+        A = rng.standard_normal((M, K)).astype(np.float32)
+        B = rng.standard_normal((K, N)).astype(np.float32)
+        (Ac, dA, BTc, dB), (oAc, odA, oBc, odB) = quantize_both(A, B, g, b)
+        out = plan.run(Ac, dA, BTc, dB).cpu().numpy()
+        fm.status(plan.ws)
+        assert np.array_equal(bits(out), bits(oracle.int8_classical(oAc, odA, oBc, odB, g)))
+    with pytest.raises(ValueError):
+        plan.run(Ac[:128].contiguous(), dA[:, :128].contiguous(), BTc, dB)
