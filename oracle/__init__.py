@@ -81,6 +81,11 @@ def lib():
             "orc_int8_group_product_fast": (None, [p, p, i, i, i, i, i, i, i, i, i, i, p, p, p, i,
                                                    p, p]),
             "orc_int8_fast": (i, [p, p, p, p, i, i, i, i, i, i, i, i, i, p, p, p, p, p]),
+            "orc_int8_split": (None, [i64, p, p]),
+            "orc_int8_group_product_corrected": (None, [p, p, i, i, i, i, i, i, i, i, i, i, p, p,
+                                                        p, p, p, p]),
+            "orc_int8_fast_corrected": (i, [p, p, p, p, i, i, i, i, i, i, i, i, i, p, p, p, p,
+                                            p, p]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -408,6 +413,40 @@ def int8_fast(Ac, dA, Bc, dB, scheme_f32, dims, g: int, h: int):
     if rc != 0:
         raise ValueError("tiling does not fit the shape")
     return out, int(viol[0]), int(viol[1])
+
+
+def int8_split(s: int):
+    """Eq. (2)'s split of an exact block sum: (s0, q) with s = s0 + 256 q,
+    q = floor((s + 128) / 256)."""
+    s0, q = ct.c_int64(), ct.c_int64()
+    lib().orc_int8_split(int(s), ct.byref(s0), ct.byref(q))
+    return s0.value, q.value
+
+
+def int8_fast_corrected(Ac, dA, Bc, dB, scheme_f32, dims, g: int, h: int):
+    """The corrected realization (Sec. 4.3, eq. (2)): output (M, N) fp32 and a
+    dict with the largest sum of absolute weighted terms per output entry
+    (term_bound), split-range violations, the number of overflowing block
+    sums, and the multiplication counts: main (A0 B0 products), sparse and
+    gathered correction counts, and classical int8's M N K."""
+    U, V, W = (_f32(t) for t in scheme_f32)
+    gm, gk, gn, R = dims
+    Ac = np.ascontiguousarray(Ac, np.int8)
+    Bc = np.ascontiguousarray(Bc, np.int8)
+    dA, dB = _f32(dA), _f32(dB)
+    M, K = Ac.shape
+    N = Bc.shape[1]
+    out = np.empty((M, N), np.float32)
+    stats = np.zeros(3, np.float64)
+    counts = np.zeros(3, np.float64)
+    rc = lib().orc_int8_fast_corrected(_ptr(Ac), _ptr(dA), _ptr(Bc), _ptr(dB), M, N, K, g, h, gm,
+                                       gk, gn, R, _ptr(U), _ptr(V), _ptr(W), _ptr(out),
+                                       _ptr(stats), _ptr(counts))
+    if rc != 0:
+        raise ValueError("tiling does not fit the shape")
+    return out, dict(term_bound=stats[0], split_violations=int(stats[1]), overflows=int(stats[2]),
+                     main=counts[0], sparse=counts[1], gathered=counts[2],
+                     classical=float(M) * N * K)
 
 
 def certificate(s: Scheme, b_A: int, b_B: int, h: int, g: int, gk: int):

@@ -669,3 +669,166 @@ int orc_int8_fast(const int8_t* Ac, const float* dA, const int8_t* Bc, const flo
   free(P);
   return 0;
 }
+
+/* ------------------------------------------------ the overflow correction */
+/* Sec. 4.3 (eq. (2)) and App. D (the corrected computation's certificate):  */
+/* a block sum of codes s, exact in a wide integer type, splits as           */
+/* s = s0 + 256 q with q = floor((s + 128) / 256) and s0 = s - 256 q, so      */
+/* s0 lies in [-128, 127]; then  s_A s_B = A0 B0 + 256 (R_A B0 + A0 R_B)      */
+/* + 256^2 R_A R_B  with every multiplicand an int8 value.                  */
+void orc_int8_split(int64_t s, int64_t* s0, int64_t* q) {
+  int64_t t = s + 128;
+  int64_t f = t >= 0 ? t / 256 : -((-t + 255) / 256); /* floor division */
+  *q = f;
+  *s0 = s - 256 * f;
+}
+
+/* One group's product with the correction: per call and product r, the     */
+/* exact block sums are split, the block product is formed as the four       */
+/* terms of eq. (2) (each an integer matrix product), and the output blocks  */
+/* combine the products with the weights W.                                  */
+/*   stats[0]: max over output entries and calls of the sum of the absolute  */
+/*             values of every weighted scalar term (bounds every partial    */
+/*             sum, in any order);                                           */
+/*   stats[1]: split parts outside s0 in [-128, 127], |q| <= 2 (count);     */
+/*   stats[2]: block sums whose q is nonzero (the overflows, count);         */
+/*   counts[0]: multiplications of the A0 B0 products;                       */
+/*   counts[1]: the correction's multiplications counting only nonzero       */
+/*              entries of R_A and R_B (R_A B0: each nonzero of R_A times a   */
+/*              row of B0; A0 R_B: a column of A0 times each nonzero of R_B;  */
+/*              R_A R_B: the pairs of nonzeros that meet);                   */
+/*   counts[2]: the correction's multiplications as dense products over the  */
+/*              rows of R_A and the columns of R_B holding a nonzero entry.  */
+void orc_int8_group_product_corrected(const int8_t* Ac, const int8_t* Bc, int M, int N, int K,
+                                      int g, int gi, int h, int gm, int gk, int gn, int R,
+                                      const float* U, const float* V, const float* W, double* P,
+                                      double* stats, double* counts) {
+  const int br = M / gm, bc = N / gn;
+  int64_t* A0 = (int64_t*)malloc(sizeof(int64_t) * (size_t)br * h);
+  int64_t* RA = (int64_t*)malloc(sizeof(int64_t) * (size_t)br * h);
+  int64_t* B0 = (int64_t*)malloc(sizeof(int64_t) * (size_t)h * bc);
+  int64_t* RB = (int64_t*)malloc(sizeof(int64_t) * (size_t)h * bc);
+  int64_t* Mr = (int64_t*)malloc(sizeof(int64_t) * (size_t)R * br * bc);
+  double* Mabs = (double*)malloc(sizeof(double) * (size_t)R * br * bc);
+  for (int64_t i = 0; i < (int64_t)M * N; ++i) P[i] = 0.0;
+  for (int k0 = gi * g; k0 < (gi + 1) * g; k0 += gk * h) { /* one call */
+    for (int r = 0; r < R; ++r) {
+      for (int x = 0; x < br; ++x)
+        for (int y = 0; y < h; ++y) {
+          int64_t acc = 0;
+          for (int p = 0; p < gm; ++p)
+            for (int q = 0; q < gk; ++q) {
+              int64_t u = (int64_t)U[(int64_t)r * gm * gk + p * gk + q];
+              if (u == 0) continue;
+              acc += u * Ac[(int64_t)(p * br + x) * K + k0 + q * h + y];
+            }
+          int64_t s0, qq;
+          orc_int8_split(acc, &s0, &qq);
+          if (s0 < -128 || s0 > 127 || qq < -2 || qq > 2) stats[1] += 1;
+          if (qq != 0) stats[2] += 1;
+          A0[(int64_t)x * h + y] = s0;
+          RA[(int64_t)x * h + y] = qq;
+        }
+      for (int y = 0; y < h; ++y)
+        for (int z = 0; z < bc; ++z) {
+          int64_t acc = 0;
+          for (int p = 0; p < gk; ++p)
+            for (int q = 0; q < gn; ++q) {
+              int64_t v = (int64_t)V[(int64_t)r * gk * gn + p * gn + q];
+              if (v == 0) continue;
+              acc += v * Bc[(int64_t)(k0 + p * h + y) * N + q * bc + z];
+            }
+          int64_t s0, qq;
+          orc_int8_split(acc, &s0, &qq);
+          if (s0 < -128 || s0 > 127 || qq < -2 || qq > 2) stats[1] += 1;
+          if (qq != 0) stats[2] += 1;
+          B0[(int64_t)y * bc + z] = s0;
+          RB[(int64_t)y * bc + z] = qq;
+        }
+      /* the block product as the four terms of eq. (2) */
+      for (int x = 0; x < br; ++x)
+        for (int z = 0; z < bc; ++z) {
+          int64_t t00 = 0, t10 = 0, t01 = 0, t11 = 0;
+          double ab = 0.0;
+          for (int y = 0; y < h; ++y) {
+            int64_t a0 = A0[(int64_t)x * h + y], ra = RA[(int64_t)x * h + y];
+            int64_t b0 = B0[(int64_t)y * bc + z], rb = RB[(int64_t)y * bc + z];
+            t00 += a0 * b0;
+            t10 += ra * b0;
+            t01 += a0 * rb;
+            t11 += ra * rb;
+            ab += (double)llabs(a0 * b0) + 256.0 * (double)llabs(ra * b0) +
+                  256.0 * (double)llabs(a0 * rb) + 65536.0 * (double)llabs(ra * rb);
+          }
+          Mr[((int64_t)r * br + x) * bc + z] = t00 + 256 * (t10 + t01) + 65536 * t11;
+          Mabs[((int64_t)r * br + x) * bc + z] = ab;
+        }
+      /* multiplication counts of this product */
+      counts[0] += (double)br * bc * h;
+      int64_t nnzA = 0, nnzB = 0, rowsA = 0, colsB = 0;
+      double pairs = 0.0;
+      for (int x = 0; x < br; ++x) {
+        int any = 0;
+        for (int y = 0; y < h; ++y)
+          if (RA[(int64_t)x * h + y]) ++nnzA, any = 1;
+        rowsA += any;
+      }
+      for (int z = 0; z < bc; ++z) {
+        int any = 0;
+        for (int y = 0; y < h; ++y)
+          if (RB[(int64_t)y * bc + z]) ++nnzB, any = 1;
+        colsB += any;
+      }
+      for (int y = 0; y < h; ++y) {
+        int64_t ca = 0, cb = 0;
+        for (int x = 0; x < br; ++x) ca += RA[(int64_t)x * h + y] != 0;
+        for (int z = 0; z < bc; ++z) cb += RB[(int64_t)y * bc + z] != 0;
+        pairs += (double)ca * cb;
+      }
+      counts[1] += (double)nnzA * bc + (double)br * nnzB + pairs;
+      counts[2] += (double)rowsA * h * bc + (double)br * h * colsB + (double)rowsA * h * colsB;
+    }
+    /* combination, ascending r; added to the group's running sum */
+    for (int i = 0; i < gm; ++i)
+      for (int j = 0; j < gn; ++j)
+        for (int x = 0; x < br; ++x)
+          for (int z = 0; z < bc; ++z) {
+            int64_t c = 0;
+            double cabs = 0.0;
+            for (int r = 0; r < R; ++r) {
+              int64_t w = (int64_t)W[(int64_t)r * gm * gn + i * gn + j];
+              if (w == 0) continue;
+              c += w * Mr[((int64_t)r * br + x) * bc + z];
+              cabs += (double)llabs(w) * Mabs[((int64_t)r * br + x) * bc + z];
+            }
+            if (cabs > stats[0]) stats[0] = cabs;
+            P[(int64_t)(i * br + x) * N + j * bc + z] += (double)c;
+          }
+  }
+  free(A0);
+  free(RA);
+  free(B0);
+  free(RB);
+  free(Mr);
+  free(Mabs);
+}
+
+/* The corrected realization's output: group products as above, then the    */
+/* classical operator's rescaling and fp32 order.  Returns 0, or -1 if the   */
+/* tiling does not fit.                                                      */
+int orc_int8_fast_corrected(const int8_t* Ac, const float* dA, const int8_t* Bc, const float* dB,
+                            int M, int N, int K, int g, int h, int gm, int gk, int gn, int R,
+                            const float* U, const float* V, const float* W, float* out,
+                            double* stats, double* counts) {
+  if (M % gm || N % gn || K % g || g % (gk * h)) return -1;
+  int ng = K / g;
+  double* P = (double*)malloc(sizeof(double) * (size_t)M * N);
+  for (int64_t i = 0; i < (int64_t)M * N; ++i) out[i] = 0.0f;
+  for (int gi = 0; gi < ng; ++gi) {
+    orc_int8_group_product_corrected(Ac, Bc, M, N, K, g, gi, h, gm, gk, gn, R, U, V, W, P, stats,
+                                     counts);
+    rescale_accumulate(P, dA, dB, M, N, ng, gi, out);
+  }
+  free(P);
+  return 0;
+}

@@ -65,6 +65,23 @@ WORKLOADS = {
         a_dist="t3", a_outliers=32, a_outlier_scale=1000.0, b_sigma=0.015, sign_sampled=True),
 }
 
+# Stand-ins for the layer slices on which App. E counts the overflow
+# correction's multiplications (512 token rows, 1024 output channels, the
+# layer's full inner dimension; groups of 128, blocks of inner length 32):
+# two down projections (heavy-tailed inputs with a few large channels) and a
+# gate projection (Gaussian inputs with outlier channels).
+CORRECTION_SLICES = {
+    "down_512x13824x1024": Workload(
+        "down_512x13824x1024", 512, 13824, 1024, "strassen", 2, "sign", 1,
+        a_dist="t3", a_outliers=8, a_outlier_scale=50.0, b_sigma=0.02, seed=20261203),
+    "gate_512x4096x1024": Workload(
+        "gate_512x4096x1024", 512, 4096, 1024, "strassen", 2, "sign", 1,
+        a_outliers=16, a_outlier_scale=20.0, b_sigma=0.02, seed=20261204),
+    "down_512x11008x1024": Workload(
+        "down_512x11008x1024", 512, 11008, 1024, "strassen", 2, "sign", 1,
+        a_dist="t3", a_outliers=4, a_outlier_scale=100.0, b_sigma=0.02, seed=20261205),
+}
+
 # Order of the workloads as listed for the method's evaluation: the first is
 # the small case the oracle finishes in seconds, the second the headline one.
 WORKLOAD_ORDER = list(WORKLOADS)
