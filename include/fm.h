@@ -353,19 +353,46 @@ int fm_int8_matmul_fast(const fm_scheme* s, int levels, const int8_t* Ac,
                         float* out, void* workspace, size_t ws_bytes,
                         void* hip_stream);
 
+/* The overflow correction (Sec. 4.3, eq. (2); App. D, the corrected
+ * computation's certificate): every exact block sum s of codes is split as
+ * s = s0 + 256 q, q = floor((s + 128) / 256), s0 in [-128, 127], and each
+ * block product as A0 B0 + 256 (R_A B0 + A0 R_B) + 256^2 R_A R_B on the
+ * int8 matrix cores, all in one exact int32 accumulator; the result is
+ * classical int8's at the same specification bit for bit, up to code bound
+ * 127.  fm_int8_certify_corrected: conditions[0] the split parts q fit int8
+ * (|q| <= qmax = floor((L b + 128) / 256)), [1] the sum of the absolute
+ * weighted terms per output entry, L_W h (128 + 256 qmax_A)(128 + 256
+ * qmax_B), and g b_A b_B stay below 2^31, [2] a call lies within one group;
+ * bounds[0] that sum, bounds[1..2] qmax_A, qmax_B (two-level Strassen at 127
+ * with h = 32: 16 * 13,107,200 and 2, 2).  The kernel needs one call per
+ * group (g = k^levels h), else FM_E_UNSUPPORTED; a split part beyond qmax
+ * (codes beyond the bounds) is FM_E_RANGE at the next fm_status.  Async. */
+int fm_int8_certify_corrected(const fm_scheme* s, int levels, int b_A, int b_B,
+                              int h, int g, int* conditions, double* bounds);
+size_t fm_int8_workspace_size_corrected(const fm_scheme* s, int levels, int M,
+                                        int N, int K, int g, int h);
+int fm_int8_matmul_corrected(const fm_scheme* s, int levels, const int8_t* Ac,
+                             const float* dA, const int8_t* BTc,
+                             const float* dB, int M, int N, int K, int g,
+                             int h, int b_A, int b_B, float* out,
+                             void* workspace, size_t ws_bytes,
+                             void* hip_stream);
+
 /* A fast call prepared once: fm_int8_plan_create validates and certifies
- * exactly as fm_int8_matmul_fast does, then writes the scheme's tables and
- * the tile schedule into the caller's workspace (async on hip_stream, which
- * orders them before any later work on it).  The plan records the
- * workspace; keep it alive and unchanged while the plan is used.
- * fm_int8_plan_run performs the call on new codes and scales of the planned
- * shapes, with the same result and errors as fm_int8_matmul_fast; runs that
- * share a plan on different streams race on its workspace.  Library-owned
- * handle, freed by fm_int8_plan_free (null is ignored). */
+ * exactly as fm_int8_matmul_fast (correct = 0) or fm_int8_matmul_corrected
+ * (correct = 1) does, then writes the scheme's tables and the tile schedule
+ * into the caller's workspace (async on hip_stream, which orders them before
+ * any later work on it; sized by the matching workspace-size call).  The
+ * plan records the workspace; keep it alive and unchanged while the plan is
+ * used.  fm_int8_plan_run performs the call on new codes and scales of the
+ * planned shapes, with the same result and errors as the one-shot call;
+ * runs that share a plan on different streams race on its workspace.
+ * Library-owned handle, freed by fm_int8_plan_free (null is ignored). */
 typedef struct fm_int8_plan fm_int8_plan;
 int fm_int8_plan_create(const fm_scheme* s, int levels, int M, int N, int K,
-                        int g, int h, int b_A, int b_B, void* workspace,
-                        size_t ws_bytes, void* hip_stream, fm_int8_plan** out);
+                        int g, int h, int b_A, int b_B, int correct,
+                        void* workspace, size_t ws_bytes, void* hip_stream,
+                        fm_int8_plan** out);
 int fm_int8_plan_run(const fm_int8_plan* p, const int8_t* Ac, const float* dA,
                      const int8_t* BTc, const float* dB, float* out,
                      void* hip_stream);

@@ -985,7 +985,8 @@ int fm_int8_matmul_classical(const int8_t* Ac, const float* dA, const int8_t* BT
   if (g < 128 || g % 128 || K % g) return fail(FM_E_SHAPE, "g must be a multiple of 128 dividing K");
   if (M % 4 || N % 4) return fail(FM_E_SHAPE, "M and N must be multiples of 4");
   return launch_i8_gemm(false, Ac, BTc, nullptr, nullptr, dA, dB, out, nullptr, nullptr, 0,
-                        nullptr, nullptr, 0, M, N, K, g, 1, 1, 1, 0, 1, (hipStream_t)hip_stream);
+                        nullptr, nullptr, 0, M, N, K, g, 1, 1, 1, 0, 1, nullptr, nullptr, nullptr,
+                        nullptr, (hipStream_t)hip_stream);
 }
 
 namespace {
@@ -1038,6 +1039,26 @@ void certify(const IntScheme& is, int bA, int bB, int h, int g, int cond[3]) {
   cond[2] = h > 0 && g % (is.gk * h) == 0;
 }
 
+// The corrected computation's certificate (App. D, generalized from two-level
+// Strassen at code bound 127): block sums reach at most alpha = L_A b_A, so
+// the split parts satisfy |q| <= qmax = floor((alpha + 128) / 256) and
+// remainders lie in [-128, 127]; every weighted scalar term of eq. (2) for an
+// output entry adds up to at most L_W h (128 + 256 qmax_A)(128 + 256 qmax_B),
+// which must stay below 2^31 (condition 1; it bounds every partial sum in
+// any order), with the split parts within int8 (condition 0) and a call
+// inside one group (condition 2).  bound[0] is that sum, bound[1..2] qmax.
+int corr_qmax(double alpha) { return (int)std::floor((alpha + 128.0) / 256.0); }
+void certify_corrected(const IntScheme& is, int bA, int bB, int h, int g, int cond[3],
+                       double bound[3]) {
+  const int qa = corr_qmax(is.LA * bA), qb = corr_qmax(is.LB * bB);
+  bound[0] = is.LW * h * (128.0 + 256.0 * qa) * (128.0 + 256.0 * qb);
+  bound[1] = qa;
+  bound[2] = qb;
+  cond[0] = qa <= 127 && qb <= 127;
+  cond[1] = std::max(bound[0], (double)g * bA * bB) < 2147483648.0;
+  cond[2] = h > 0 && g % (is.gk * h) == 0;
+}
+
 // Bytes per product in a block-sum coefficient table: the blocks' int8
 // coefficients, zero-padded to whole dwords.
 int coef_stride(int blocks) { return (blocks + 3) / 4 * 4; }
@@ -1046,11 +1067,20 @@ int coef_stride(int blocks) { return (blocks + 3) / 4 * 4; }
 // tables, the tile schedule, then per call the block sums T (R x Mb x h), S
 // and -S (R x Nb x h).
 struct I8Layout {
-  size_t flags, zero, coefa, coefb, segs, segoff, order, order_off, t, s, sn, total;
+  size_t flags, zero, coefa, coefb, segs, segoff, order, order_off, phase, t, s, sn, tr, sr, snr,
+      total;
   int nsegs;
 };
 
-I8Layout i8_layout(const IntScheme& is, int M, int N, int K, int h) {
+// Segments of one output block per call: its n nonzero weights once
+// (padded to whole K steps), or with the correction in three phases of n,
+// 2 n and n segments, each padded.
+int block_segments(int n, int per_step, bool corr) {
+  auto pad = [&](int k) { return (k + per_step - 1) / per_step * per_step; };
+  return corr ? 2 * pad(n) + pad(2 * n) : pad(n);
+}
+
+I8Layout i8_layout(const IntScheme& is, int M, int N, int K, int h, bool corr) {
   I8Layout L{};
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -1063,7 +1093,7 @@ I8Layout i8_layout(const IntScheme& is, int M, int N, int K, int h) {
   for (int c = 0; c < is.gm * is.gn; ++c) {
     int n = 0;
     for (int r = 0; r < is.R; ++r) n += is.W[(size_t)r * is.gm * is.gn + c] != 0;
-    nsegs += (n + per_step - 1) / per_step * per_step;
+    nsegs += block_segments(n, per_step, corr);
   }
   L.nsegs = nsegs;
   const size_t ncall = (size_t)K / ((size_t)is.gk * h);
@@ -1075,9 +1105,14 @@ I8Layout i8_layout(const IntScheme& is, int M, int N, int K, int h) {
   L.segoff = take((size_t)(is.gm * is.gn + 1) * 4);
   L.order = take((size_t)i8_fast_tiles(is.gm, is.gn, M / is.gm, N / is.gn) * 4);
   L.order_off = take(257 * 4);
-  L.t = take(ncall * is.R * (M / is.gm) * h);
-  L.s = take(ncall * is.R * (N / is.gn) * h);
-  L.sn = take(ncall * is.R * (N / is.gn) * h);
+  L.phase = take((size_t)is.gm * is.gn * 2 * 4);
+  const size_t tb = ncall * is.R * (M / is.gm) * h, sb = ncall * is.R * (N / is.gn) * h;
+  L.t = take(tb);
+  L.s = take(sb);
+  L.sn = take(sb);
+  L.tr = corr ? take(tb) : 0;
+  L.sr = corr ? take(sb) : 0;
+  L.snr = corr ? take(sb) : 0;
   L.total = o;
   return L;
 }
@@ -1094,26 +1129,42 @@ int i8_fast_shape_ok(const IntScheme& is, int M, int N, int K, int g, int h) {
 
 // Validation, certificate, tables and schedule of a fast call (everything
 // that depends on the scheme and the shapes, not on the codes): the tables
-// go to the workspace with one staged copy on st.
+// go to the workspace with one staged copy on st.  corr selects the overflow
+// correction (eq. (2)).
 int i8_plan_prepare(const fm_scheme* s, int levels, int M, int N, int K, int g, int h, int b_A,
-                    int b_B, void* workspace, size_t ws_bytes, hipStream_t st, fm_int8_plan& p) {
+                    int b_B, bool corr, void* workspace, size_t ws_bytes, hipStream_t st,
+                    fm_int8_plan& p) {
   IntScheme is;
   if (int rc = int_scheme(s, levels, is)) return rc;
   if (int rc = i8_fast_shape_ok(is, M, N, K, g, h)) return rc;
   if (b_A < 1 || b_A > 127 || b_B < 1 || b_B > 127) return fail(FM_E_ARG, "code bounds must be in [1, 127]");
-  int cond[3];
-  certify(is, b_A, b_B, h, g, cond);
-  if (!cond[0]) return fail(FM_E_UNCERTIFIED, "condition (i): a block sum of codes can leave int8");
-  if (!cond[1]) return fail(FM_E_UNCERTIFIED, "condition (ii): a partial sum can leave int32");
-  if (!cond[2]) return fail(FM_E_UNCERTIFIED, "condition (iii): a call spans two groups");
   const int calls_per_group = g / (is.gk * h);
-  // the kernel accumulates a whole group (all its calls) in int32
-  if ((double)calls_per_group * is.LW * h * (is.LA * b_A) * (is.LB * b_B) >= 2147483648.0)
-    return fail(FM_E_UNCERTIFIED, "a group's calls together can leave int32");
+  int qa = 0, qb = 0;
+  if (corr) {
+    int cond[3];
+    double bound[3];
+    certify_corrected(is, b_A, b_B, h, g, cond, bound);
+    if (!cond[0]) return fail(FM_E_UNCERTIFIED, "the split parts of a block sum leave int8");
+    if (!cond[1]) return fail(FM_E_UNCERTIFIED, "a corrected partial sum can leave int32");
+    if (!cond[2]) return fail(FM_E_UNCERTIFIED, "condition (iii): a call spans two groups");
+    if (calls_per_group != 1)
+      return fail(FM_E_UNSUPPORTED, "the corrected kernel needs one call per group (g = k^levels h)");
+    qa = (int)bound[1];
+    qb = (int)bound[2];
+  } else {
+    int cond[3];
+    certify(is, b_A, b_B, h, g, cond);
+    if (!cond[0]) return fail(FM_E_UNCERTIFIED, "condition (i): a block sum of codes can leave int8");
+    if (!cond[1]) return fail(FM_E_UNCERTIFIED, "condition (ii): a partial sum can leave int32");
+    if (!cond[2]) return fail(FM_E_UNCERTIFIED, "condition (iii): a call spans two groups");
+    // the kernel accumulates a whole group (all its calls) in int32
+    if ((double)calls_per_group * is.LW * h * (is.LA * b_A) * (is.LB * b_B) >= 2147483648.0)
+      return fail(FM_E_UNCERTIFIED, "a group's calls together can leave int32");
+  }
   const int nc = is.gm * is.gn;
   for (int v : is.W)
     if (v < -1 || v > 1) return fail(FM_E_UNCERTIFIED, "combination weights must be -1, 0 or 1");
-  const I8Layout L = i8_layout(is, M, N, K, h);
+  const I8Layout L = i8_layout(is, M, N, K, h, corr);
   if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
   char* ws = (char*)workspace;
   // host tables: coefficients per block (A: [r][i*gk + l], B: [r][j*gk + l],
@@ -1127,18 +1178,32 @@ int i8_plan_prepare(const fm_scheme* s, int levels, int M, int N, int K, int g, 
       for (int j = 0; j < is.gn; ++j)
         cbt[(size_t)r * sb + j * is.gk + l] = (int8_t)is.V[(size_t)r * is.gk * is.gn + l * is.gn + j];
   }
+  // segment entry: r | (w < 0) << 16 | (A side from the split parts q) << 17
+  // | (B side from q) << 18; r = 0xffff pads a K step with zeros
   const int per_step = 128 / h;
-  std::vector<int32_t> segs, off(1, 0);
+  constexpr int32_t kNeg = 1 << 16, kQA = 1 << 17, kQB = 1 << 18;
+  std::vector<int32_t> segs, off(1, 0), phase(2 * nc, -1);
+  auto pad = [&]() {
+    while ((segs.size() - off.back()) % per_step) segs.push_back(0xffff);
+  };
   for (int c = 0; c < nc; ++c) {
-    int n = 0;
+    std::vector<int32_t> base;
     for (int r = 0; r < is.R; ++r) {
       const int w = is.W[(size_t)r * nc + c];
-      if (!w) continue;
-      segs.push_back(r | (w < 0 ? 1 << 16 : 0));
-      ++n;
+      if (w) base.push_back(r | (w < 0 ? kNeg : 0));
     }
-    if (n == 0) return fail(FM_E_ARG, "an output block combines no products");
-    for (; n % per_step; ++n) segs.push_back(0xffff);
+    if (base.empty()) return fail(FM_E_ARG, "an output block combines no products");
+    if (corr) {
+      for (int32_t e : base) segs.push_back(e | kQA | kQB);  // R_A R_B
+      pad();
+      phase[2 * c] = (int32_t)(segs.size() - off.back()) / per_step;
+      for (int32_t e : base) segs.push_back(e | kQA);  // R_A B0
+      for (int32_t e : base) segs.push_back(e | kQB);  // A0 R_B
+      pad();
+      phase[2 * c + 1] = (int32_t)(segs.size() - off.back()) / per_step;
+    }
+    for (int32_t e : base) segs.push_back(e);  // A0 B0 (or the plain block sums)
+    pad();
     off.push_back((int32_t)segs.size());
   }
   if ((int)segs.size() != L.nsegs) return fail(FM_E_ARG, "segment table size mismatch");
@@ -1150,17 +1215,18 @@ int i8_plan_prepare(const fm_scheme* s, int levels, int M, int N, int K, int g, 
   const int grid = i8_fast_schedule(is.gm, is.gn, M / is.gm, N / is.gn, block_steps, order, order_off);
   int rc = FM_OK;
   if ((rc = launch_fill_u32((uint32_t*)(ws + L.zero), kAlign / 4, 0u, st))) return rc;
-  // the six tables are adjacent in the workspace: one staged copy
+  // the seven tables are adjacent in the workspace: one staged copy
   if ((rc = upload(ws + L.coefa,
                    {{ca.data(), ca.size()},
                     {cbt.data(), cbt.size()},
                     {segs.data(), segs.size() * 4},
                     {off.data(), off.size() * 4},
                     {order.data(), order.size() * 4},
-                    {order_off.data(), order_off.size() * 4}},
+                    {order_off.data(), order_off.size() * 4},
+                    {phase.data(), phase.size() * 4}},
                    {0, L.coefb - L.coefa, L.segs - L.coefa, L.segoff - L.coefa,
-                    L.order - L.coefa, L.order_off - L.coefa},
-                   L.order_off - L.coefa + order_off.size() * 4, st)))
+                    L.order - L.coefa, L.order_off - L.coefa, L.phase - L.coefa},
+                   L.phase - L.coefa + phase.size() * 4, st)))
     return rc;
   p.M = M;
   p.N = N;
@@ -1176,6 +1242,9 @@ int i8_plan_prepare(const fm_scheme* s, int levels, int M, int N, int K, int g, 
   p.grid = grid;
   p.sa = sa;
   p.sb = sb;
+  p.corr = corr;
+  p.qmax_a = qa;
+  p.qmax_b = qb;
   p.ws = ws;
   p.ws_bytes = ws_bytes;
   p.flags = L.flags;
@@ -1186,14 +1255,18 @@ int i8_plan_prepare(const fm_scheme* s, int levels, int M, int N, int K, int g, 
   p.segoff = L.segoff;
   p.order = L.order;
   p.order_off = L.order_off;
+  p.phase = L.phase;
   p.t = L.t;
   p.s = L.s;
   p.sn = L.sn;
+  p.tr = L.tr;
+  p.sr = L.sr;
+  p.snr = L.snr;
   return FM_OK;
 }
 
-// One fast call on a prepared workspace: block sums of A and B, then the
-// grouped products.
+// One fast call on a prepared workspace: block sums of A and B (split, with
+// the correction), then the grouped products.
 int i8_plan_run(const fm_int8_plan& p, const int8_t* Ac, const float* dA, const int8_t* BTc,
                 const float* dB, float* out, hipStream_t st) {
   if (!Ac || !dA || !BTc || !dB || !out) return fail(FM_E_ARG, "null pointer");
@@ -1202,18 +1275,22 @@ int i8_plan_run(const fm_int8_plan& p, const int8_t* Ac, const float* dA, const 
   int8_t* T = (int8_t*)(ws + p.t);
   int8_t* S = (int8_t*)(ws + p.s);
   int8_t* Sn = (int8_t*)(ws + p.sn);
+  int8_t* TR = p.corr ? (int8_t*)(ws + p.tr) : nullptr;
+  int8_t* SR = p.corr ? (int8_t*)(ws + p.sr) : nullptr;
+  int8_t* SnR = p.corr ? (int8_t*)(ws + p.snr) : nullptr;
   int rc = FM_OK;
   if ((rc = launch_fill_u32(flag, kAlign / 4, 0u, st))) return rc;
   if ((rc = launch_i8_form(Ac, p.M, p.K, p.gm, p.gk, p.h, p.R, (const int8_t*)(ws + p.coefa), p.sa,
-                           T, nullptr, flag, st)))
+                           T, nullptr, TR, nullptr, p.qmax_a, flag, st)))
     return rc;
   if ((rc = launch_i8_form(BTc, p.N, p.K, p.gn, p.gk, p.h, p.R, (const int8_t*)(ws + p.coefb), p.sb,
-                           S, Sn, flag, st)))
+                           S, Sn, SR, SnR, p.qmax_b, flag, st)))
     return rc;
   return launch_i8_gemm(true, T, S, Sn, (const int8_t*)(ws + p.zero), dA, dB, out,
                         (const int32_t*)(ws + p.segs), (const int32_t*)(ws + p.segoff), p.nsegs,
                         (const int32_t*)(ws + p.order), (const int32_t*)(ws + p.order_off), p.grid,
-                        p.M, p.N, p.K, p.g, p.gm, p.gn, p.R, p.h, p.calls_per_group, st);
+                        p.M, p.N, p.K, p.g, p.gm, p.gn, p.R, p.h, p.calls_per_group, TR, SR, SnR,
+                        p.corr ? (const int32_t*)(ws + p.phase) : nullptr, st);
 }
 }  // namespace
 
@@ -1230,23 +1307,42 @@ int fm_int8_certify(const fm_scheme* s, int levels, int b_A, int b_B, int h, int
   return FM_OK;
 }
 
+int fm_int8_certify_corrected(const fm_scheme* s, int levels, int b_A, int b_B, int h, int g,
+                              int* conditions, double* bounds) {
+  clear_error();
+  if (!conditions || !bounds) return fail(FM_E_ARG, "null pointer");
+  IntScheme is;
+  if (int rc = int_scheme(s, levels, is)) return rc;
+  certify_corrected(is, b_A, b_B, h, g, conditions, bounds);
+  return FM_OK;
+}
+
 size_t fm_int8_workspace_size(const fm_scheme* s, int levels, int M, int N, int K, int g, int h) {
   IntScheme is;
   if (int_scheme(s, levels, is) != FM_OK) return 0;
   if (i8_fast_shape_ok(is, M, N, K, g, h) != FM_OK) return 0;
-  return i8_layout(is, M, N, K, h).total;
+  return i8_layout(is, M, N, K, h, false).total;
+}
+
+size_t fm_int8_workspace_size_corrected(const fm_scheme* s, int levels, int M, int N, int K, int g,
+                                        int h) {
+  IntScheme is;
+  if (int_scheme(s, levels, is) != FM_OK) return 0;
+  if (i8_fast_shape_ok(is, M, N, K, g, h) != FM_OK) return 0;
+  return i8_layout(is, M, N, K, h, true).total;
 }
 
 int fm_int8_plan_create(const fm_scheme* s, int levels, int M, int N, int K, int g, int h,
-                        int b_A, int b_B, void* workspace, size_t ws_bytes, void* hip_stream,
-                        fm_int8_plan** out) {
+                        int b_A, int b_B, int correct, void* workspace, size_t ws_bytes,
+                        void* hip_stream, fm_int8_plan** out) {
   clear_error();
   if (!out) return fail(FM_E_ARG, "null pointer");
   *out = nullptr;
+  if (correct != 0 && correct != 1) return fail(FM_E_ARG, "correct must be 0 or 1");
   std::unique_ptr<fm_int8_plan> p(new (std::nothrow) fm_int8_plan());
   if (!p) return fail(FM_E_ARG, "out of host memory");
-  if (int rc = i8_plan_prepare(s, levels, M, N, K, g, h, b_A, b_B, workspace, ws_bytes,
-                               (hipStream_t)hip_stream, *p))
+  if (int rc = i8_plan_prepare(s, levels, M, N, K, g, h, b_A, b_B, correct != 0, workspace,
+                               ws_bytes, (hipStream_t)hip_stream, *p))
     return rc;
   *out = p.release();
   return FM_OK;
@@ -1261,17 +1357,36 @@ int fm_int8_plan_run(const fm_int8_plan* p, const int8_t* Ac, const float* dA, c
 
 void fm_int8_plan_free(fm_int8_plan* p) { delete p; }
 
-int fm_int8_matmul_fast(const fm_scheme* s, int levels, const int8_t* Ac, const float* dA,
-                        const int8_t* BTc, const float* dB, int M, int N, int K, int g, int h,
-                        int b_A, int b_B, float* out, void* workspace, size_t ws_bytes,
-                        void* hip_stream) {
+namespace {
+int int8_fast_once(const fm_scheme* s, int levels, const int8_t* Ac, const float* dA,
+                   const int8_t* BTc, const float* dB, int M, int N, int K, int g, int h, int b_A,
+                   int b_B, bool corr, float* out, void* workspace, size_t ws_bytes,
+                   void* hip_stream) {
   clear_error();
   if (!Ac || !dA || !BTc || !dB || !out) return fail(FM_E_ARG, "null pointer");
   fm_int8_plan p;
   hipStream_t st = (hipStream_t)hip_stream;
-  if (int rc = i8_plan_prepare(s, levels, M, N, K, g, h, b_A, b_B, workspace, ws_bytes, st, p))
+  if (int rc = i8_plan_prepare(s, levels, M, N, K, g, h, b_A, b_B, corr, workspace, ws_bytes, st,
+                               p))
     return rc;
   return i8_plan_run(p, Ac, dA, BTc, dB, out, st);
+}
+}  // namespace
+
+int fm_int8_matmul_fast(const fm_scheme* s, int levels, const int8_t* Ac, const float* dA,
+                        const int8_t* BTc, const float* dB, int M, int N, int K, int g, int h,
+                        int b_A, int b_B, float* out, void* workspace, size_t ws_bytes,
+                        void* hip_stream) {
+  return int8_fast_once(s, levels, Ac, dA, BTc, dB, M, N, K, g, h, b_A, b_B, false, out,
+                        workspace, ws_bytes, hip_stream);
+}
+
+int fm_int8_matmul_corrected(const fm_scheme* s, int levels, const int8_t* Ac, const float* dA,
+                             const int8_t* BTc, const float* dB, int M, int N, int K, int g, int h,
+                             int b_A, int b_B, float* out, void* workspace, size_t ws_bytes,
+                             void* hip_stream) {
+  return int8_fast_once(s, levels, Ac, dA, BTc, dB, M, N, K, g, h, b_A, b_B, true, out,
+                        workspace, ws_bytes, hip_stream);
 }
 
 }  // extern "C"

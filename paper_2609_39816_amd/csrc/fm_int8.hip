@@ -101,11 +101,12 @@ __device__ __forceinline__ uint32_t dword_of(const uint4& v, int w) {
 // blocks' codes at one position, and forms every product of its group with
 // v_dot4 (four int8 products summed exactly into int32) against the packed
 // coefficient dwords, which are wave-uniform.
-template <int NG>
+template <int NG, bool CORR>
 __global__ __launch_bounds__(kThreads) void i8_form_dot_kernel(
     const int8_t* __restrict__ X, int rows, int K, int gp, int gk, int h, int R, int rg,
     const int8_t* __restrict__ coef, int stride, int8_t* __restrict__ out,
-    int8_t* __restrict__ outn, uint32_t* flag) {
+    int8_t* __restrict__ outn, int8_t* __restrict__ outR, int8_t* __restrict__ outnR, int qmax,
+    uint32_t* flag) {
   const int br = rows / gp;
   const int hc = h / 16;
   const int ncall = K / (gk * h);
@@ -145,33 +146,58 @@ __global__ __launch_bounds__(kThreads) void i8_form_dot_kernel(
   }
   const auto cf = ro(reinterpret_cast<const int32_t*>(coef));
   const int sw = stride / 4;
-  uint32_t worst = 0u;  // max of s + 127 over the sums, unsigned: > 254 leaves int8
+  // plain: max of s + 127 over the sums, unsigned (> 254 leaves int8);
+  // corrected: max |q| over the split parts (> qmax leaves the certificate)
+  uint32_t worst = 0u;
   const int r0 = rgi * rg, r1 = min(R, r0 + rg);
   for (int r = r0; r < r1; ++r) {
     int c[NG];
 #pragma unroll
     for (int G = 0; G < NG; ++G) c[G] = cf[(size_t)r * sw + G];
-    uint32_t o[4];
+    uint32_t o[4], oq[4], on[4], onq[4];
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      uint32_t packed = 0u;
+      uint32_t packed = 0u, pq = 0u, pn = 0u, pnq = 0u;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         int s = 0;
 #pragma unroll
         for (int G = 0; G < NG; ++G) s = __builtin_amdgcn_sdot4((int)t[w][G][j], c[G], s, false);
-        worst = max(worst, (uint32_t)(s + 127));
-        packed |= ((uint32_t)s & 0xffu) << (8 * j);
+        if constexpr (CORR) {
+          // eq. (2): s = s0 + 256 q, q = floor((s + 128) / 256), s0 in [-128, 127];
+          // the negation is split on its own (-s0 may be 128)
+          const int q = (s + 128) >> 8, s0 = s - (q << 8);
+          const int qn = (128 - s) >> 8, s0n = -s - (qn << 8);
+          worst = max(worst, (uint32_t)max(abs(q), abs(qn)));
+          packed |= ((uint32_t)s0 & 0xffu) << (8 * j);
+          pq |= ((uint32_t)q & 0xffu) << (8 * j);
+          pn |= ((uint32_t)s0n & 0xffu) << (8 * j);
+          pnq |= ((uint32_t)qn & 0xffu) << (8 * j);
+        } else {
+          worst = max(worst, (uint32_t)(s + 127));
+          packed |= ((uint32_t)s & 0xffu) << (8 * j);
+        }
       }
       o[w] = packed;
+      oq[w] = pq;
+      on[w] = pn;
+      onq[w] = pnq;
     }
     const size_t off = (((size_t)kap * R + r) * br + x) * h + y0;
     *reinterpret_cast<uint4*>(out + off) = make_uint4(o[0], o[1], o[2], o[3]);
-    if (outn)
+    if constexpr (CORR) {
+      *reinterpret_cast<uint4*>(outR + off) = make_uint4(oq[0], oq[1], oq[2], oq[3]);
+      if (outn) {
+        *reinterpret_cast<uint4*>(outn + off) = make_uint4(on[0], on[1], on[2], on[3]);
+        *reinterpret_cast<uint4*>(outnR + off) = make_uint4(onq[0], onq[1], onq[2], onq[3]);
+      }
+    } else if (outn) {
       *reinterpret_cast<uint4*>(outn + off) =
           make_uint4(neg_bytes(o[0]), neg_bytes(o[1]), neg_bytes(o[2]), neg_bytes(o[3]));
+    }
   }
-  if (worst > 254u && flag) atomicOr(flag, 2u);
+  const bool bad = CORR ? worst > (uint32_t)qmax : worst > 254u;
+  if (bad && flag) atomicOr(flag, 2u);
 }
 
 // Any number of blocks: one thread per (call, x, four consecutive y) and all
@@ -228,6 +254,13 @@ struct I8Args {
   const int32_t* seg_off;  // fast: gm * gn + 1 offsets into segs
   const int32_t* order;    // fast: the tiles of every workgroup, consecutively
   const int32_t* order_off;  // fast: gridDim.x + 1 offsets into order
+  // corrected fast path (eq. (2)): the split parts q of the block sums (the
+  // remainders s0 are A, B, Bn above), and per block the K steps of a call
+  // where the cross terms and the remainder products begin
+  const int8_t* AR;
+  const int8_t* BR;
+  const int8_t* BnR;
+  const int32_t* phase;  // [gm * gn][2]
   int M, N, K, g;
   int gm, gn, Mb, Nb, tiles_m, tiles_n, total;
   int R, calls_per_group;
@@ -242,17 +275,24 @@ constexpr int MAX_SEGS = 1024;
 // call, and the step (group gi, call kc within the group, step st within the
 // call).  All wave-uniform; advanced incrementally so that no step divides.
 struct I8Cursor {
-  int slot, ib, jb, m0, n0, spc, sb, gi, kc, st;
+  int slot, ib, jb, m0, n0, spc, sb, gi, kc, st, p1, p0;
 };
 
 // H: the block inner length h of the fast realization (0: classical).
-template <int H>
+// CORR: the overflow correction (eq. (2)).  A call's segments then come in
+// three phases, R_A R_B, then R_A B0 and A0 R_B, then A0 B0, and the int32
+// accumulator is multiplied by 256 as each of the last two begins (Horner's
+// rule: ((R_A R_B) 256 + cross terms) 256 + A0 B0), so one accumulator holds
+// the exact product; a group is one call.
+template <int H, bool CORR>
 __global__ __launch_bounds__(DNT) void i8_gemm_kernel(I8Args a) {
   constexpr bool FAST = H > 0;
   static_assert(!FAST || (H >= 16 && H <= GK && GK % H == 0), "block inner length");
+  static_assert(FAST || !CORR, "the correction belongs to the fast path");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[DNS * I8STAGE];
   __shared__ int32_t seg_lds[FAST ? MAX_SEGS : 1];
   __shared__ int32_t off_lds[FAST ? 65 : 1];
+  __shared__ int32_t ph_lds[CORR ? 128 : 1];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -266,6 +306,8 @@ __global__ __launch_bounds__(DNT) void i8_gemm_kernel(I8Args a) {
     for (int i = tid; i <= nb; i += DNT) off_lds[i] = ro(a.seg_off)[i];
     const int ns = ro(a.seg_off)[nb];
     for (int i = tid; i < ns; i += DNT) seg_lds[i] = ro(a.segs)[i];
+    if constexpr (CORR)
+      for (int i = tid; i < 2 * nb; i += DNT) ph_lds[i] = ro(a.phase)[i];
     __syncthreads();
   }
   const bool vec_store = (a.Nb & 3) == 0 && (a.N & 3) == 0;
@@ -306,6 +348,12 @@ __global__ __launch_bounds__(DNT) void i8_gemm_kernel(I8Args a) {
     } else {
       u.ib = u.jb = u.sb = u.spc = 0;
     }
+    if constexpr (CORR) {
+      u.p1 = ph_lds[2 * c];
+      u.p0 = ph_lds[2 * c + 1];
+    } else {
+      u.p1 = u.p0 = -1;
+    }
     u.gi = u.kc = u.st = 0;
   };
   auto advance = [&](I8Cursor& u) {
@@ -345,12 +393,14 @@ __global__ __launch_bounds__(DNT) void i8_gemm_kernel(I8Args a) {
         if (r0 < DBM) {
           int row = u.m0 + r;
           row = row < a.Mb ? row : 0;
+          const int8_t* T = CORR && ((e >> 17) & 1) ? a.AR : a.A;
           src = pr == 0xffff ? (const uint8_t*)a.zero
-                             : (const uint8_t*)a.A + (((size_t)kap * a.R + pr) * a.Mb + row) * H + oin;
+                             : (const uint8_t*)T + (((size_t)kap * a.R + pr) * a.Mb + row) * H + oin;
         } else {
           int col = u.n0 + r - DBM;
           col = col < a.Nb ? col : 0;
-          const int8_t* S = (e >> 16) ? a.Bn : a.B;
+          const bool neg = (e >> 16) & 1;
+          const int8_t* S = CORR && ((e >> 18) & 1) ? (neg ? a.BnR : a.BR) : (neg ? a.Bn : a.B);
           src = pr == 0xffff ? (const uint8_t*)a.zero
                              : (const uint8_t*)S + (((size_t)kap * a.R + pr) * a.Nb + col) * H + oin;
         }
@@ -510,6 +560,12 @@ __global__ __launch_bounds__(DNT) void i8_gemm_kernel(I8Args a) {
     const bool tile_end = group_end && u0.gi == ng - 1;
     read_half(1, cb);
     if (group_end) read_scales(cb);
+    if (CORR && (u0.st == u0.p1 || u0.st == u0.p0)) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = acc[i][j] << 8;
+    }
     compute_half(0);
     wait_vm(after1);
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of stage cb are done
@@ -551,29 +607,34 @@ int launch_i8_quantize(const float* X, int rows, int K, int g, int b, int8_t* co
 }
 
 int launch_i8_form(const int8_t* X, int rows, int K, int gp, int gk, int h, int R,
-                   const int8_t* coef, int stride, int8_t* out, int8_t* outn, uint32_t* flag,
-                   hipStream_t st) {
+                   const int8_t* coef, int stride, int8_t* out, int8_t* outn, int8_t* outR,
+                   int8_t* outnR, int qmax, uint32_t* flag, hipStream_t st) {
   const int nb = gp * gk;
   const int ng = (nb + 3) / 4;
+  const bool corr = outR != nullptr;
   if (h % 16 || stride < 4 * ng || stride % 4) return fail(FM_E_ARG, "block-sum layout");
+  if (corr && (ng > 4 || (outn && !outnR))) return fail(FM_E_ARG, "corrected block sums");
   if (ng <= 4) {
     const int nrg = (R + 7) / 8, rg = (R + nrg - 1) / nrg;
     const long long n = (long long)(K / (gk * h)) * (rows / gp) * (h / 16);
     const long long blocks = (n + kThreads - 1) / kThreads;
     if (blocks > 0x7fffffffLL || nrg > 65535) return fail(FM_E_SHAPE, "too many block sums");
     const dim3 grid((unsigned)blocks, (unsigned)nrg);
-    switch (ng) {
-#define FM_FORM_DOT(NG)                                                                    \
-  case NG:                                                                                \
-    i8_form_dot_kernel<NG><<<grid, kThreads, 0, st>>>(X, rows, K, gp, gk, h, R, rg, coef, \
-                                                      stride, out, outn, flag);           \
-    break;
-      FM_FORM_DOT(1)
-      FM_FORM_DOT(2)
-      FM_FORM_DOT(3)
-      FM_FORM_DOT(4)
-#undef FM_FORM_DOT
+#define FM_FORM_DOT(NG, C)                                                                    \
+  i8_form_dot_kernel<NG, C><<<grid, kThreads, 0, st>>>(X, rows, K, gp, gk, h, R, rg, coef,   \
+                                                       stride, out, outn, outR, outnR, qmax, \
+                                                       flag)
+    switch (ng * 2 + (corr ? 1 : 0)) {
+      case 2: FM_FORM_DOT(1, false); break;
+      case 3: FM_FORM_DOT(1, true); break;
+      case 4: FM_FORM_DOT(2, false); break;
+      case 5: FM_FORM_DOT(2, true); break;
+      case 6: FM_FORM_DOT(3, false); break;
+      case 7: FM_FORM_DOT(3, true); break;
+      case 8: FM_FORM_DOT(4, false); break;
+      default: FM_FORM_DOT(4, true); break;
     }
+#undef FM_FORM_DOT
     return launched("i8_form_dot_kernel");
   }
   const long long n = (long long)(K / (gk * h)) * (rows / gp) * (h / 4);
@@ -636,7 +697,8 @@ int launch_i8_gemm(bool fast, const int8_t* A, const int8_t* B, const int8_t* Bn
                    const int8_t* zero, const float* dA, const float* dB, float* out,
                    const int32_t* segs, const int32_t* seg_off, int nsegs, const int32_t* order,
                    const int32_t* order_off, int grid, int M, int N, int K, int g, int gm, int gn,
-                   int R, int h, int calls_per_group, hipStream_t st) {
+                   int R, int h, int calls_per_group, const int8_t* AR, const int8_t* BR,
+                   const int8_t* BnR, const int32_t* phase, hipStream_t st) {
   I8Args a{};
   a.A = A;
   a.B = B;
@@ -649,6 +711,10 @@ int launch_i8_gemm(bool fast, const int8_t* A, const int8_t* B, const int8_t* Bn
   a.seg_off = seg_off;
   a.order = order;
   a.order_off = order_off;
+  a.AR = AR;
+  a.BR = BR;
+  a.BnR = BnR;
+  a.phase = phase;
   a.M = M;
   a.N = N;
   a.K = K;
@@ -667,15 +733,22 @@ int launch_i8_gemm(bool fast, const int8_t* A, const int8_t* B, const int8_t* Bn
   a.R = R;
   a.calls_per_group = calls_per_group;
   if (!fast) {
-    i8_gemm_kernel<0><<<(int)std::min<long long>(total, 256), DNT, 0, st>>>(a);
+    i8_gemm_kernel<0, false><<<(int)std::min<long long>(total, 256), DNT, 0, st>>>(a);
     return launched("i8_gemm_kernel");
   }
   if (!order || !order_off || grid < 1 || grid > total) return fail(FM_E_ARG, "tile schedule");
-  switch (h) {
-    case 16: i8_gemm_kernel<16><<<grid, DNT, 0, st>>>(a); break;
-    case 32: i8_gemm_kernel<32><<<grid, DNT, 0, st>>>(a); break;
-    case 64: i8_gemm_kernel<64><<<grid, DNT, 0, st>>>(a); break;
-    case 128: i8_gemm_kernel<128><<<grid, DNT, 0, st>>>(a); break;
+  const bool corr = phase != nullptr;
+  if (corr && (!AR || !BR || !BnR || calls_per_group != 1))
+    return fail(FM_E_ARG, "corrected products need the split parts and one call per group");
+  switch (h * 2 + (corr ? 1 : 0)) {
+    case 32: i8_gemm_kernel<16, false><<<grid, DNT, 0, st>>>(a); break;
+    case 33: i8_gemm_kernel<16, true><<<grid, DNT, 0, st>>>(a); break;
+    case 64: i8_gemm_kernel<32, false><<<grid, DNT, 0, st>>>(a); break;
+    case 65: i8_gemm_kernel<32, true><<<grid, DNT, 0, st>>>(a); break;
+    case 128: i8_gemm_kernel<64, false><<<grid, DNT, 0, st>>>(a); break;
+    case 129: i8_gemm_kernel<64, true><<<grid, DNT, 0, st>>>(a); break;
+    case 256: i8_gemm_kernel<128, false><<<grid, DNT, 0, st>>>(a); break;
+    case 257: i8_gemm_kernel<128, true><<<grid, DNT, 0, st>>>(a); break;
     default: return fail(FM_E_ARG, "h must be 16, 32, 64 or 128");
   }
   return launched("i8_gemm_kernel");

@@ -21,10 +21,12 @@ struct fm_scheme {
 struct fm_int8_plan {
   int M = 0, N = 0, K = 0, g = 0, h = 0, gm = 0, gn = 0, gk = 0, R = 0;
   int calls_per_group = 0, nsegs = 0, grid = 0, sa = 0, sb = 0;
+  bool corr = false;          // the overflow correction (eq. (2))
+  int qmax_a = 0, qmax_b = 0;  // bounds on the split parts q of the block sums
   char* ws = nullptr;
   size_t ws_bytes = 0;
   size_t flags = 0, zero = 0, coefa = 0, coefb = 0, segs = 0, segoff = 0, order = 0,
-         order_off = 0, t = 0, s = 0, sn = 0;
+         order_off = 0, phase = 0, t = 0, s = 0, sn = 0, tr = 0, sr = 0, snr = 0;
 };
 
 namespace fm {
@@ -158,8 +160,8 @@ int launch_reduce_rows(const double* partial, int nblk, int G, double* out, hipS
 int launch_i8_quantize(const float* X, int rows, int K, int g, int b, int8_t* codes, float* d,
                        uint32_t* flag, hipStream_t st);
 int launch_i8_form(const int8_t* X, int rows, int K, int gp, int gk, int h, int R,
-                   const int8_t* coef, int stride, int8_t* out, int8_t* outn, uint32_t* flag,
-                   hipStream_t st);
+                   const int8_t* coef, int stride, int8_t* out, int8_t* outn, int8_t* outR,
+                   int8_t* outnR, int qmax, uint32_t* flag, hipStream_t st);
 // Tiles of the fast integer kernel, and their longest-first assignment to
 // workgroups (returns the grid; order holds every workgroup's tiles, off its
 // grid + 1 offsets).
@@ -170,7 +172,8 @@ int launch_i8_gemm(bool fast, const int8_t* A, const int8_t* B, const int8_t* Bn
                    const int8_t* zero, const float* dA, const float* dB, float* out,
                    const int32_t* segs, const int32_t* seg_off, int nsegs, const int32_t* order,
                    const int32_t* order_off, int grid, int M, int N, int K, int g, int gm, int gn,
-                   int R, int h, int calls_per_group, hipStream_t st);
+                   int R, int h, int calls_per_group, const int8_t* AR, const int8_t* BR,
+                   const int8_t* BnR, const int32_t* phase, hipStream_t st);
 
 // Float64 reference C = A B.
 int launch_reference_f64(const float* A, const float* B, double* C, int M, int N, int K,

@@ -82,7 +82,10 @@ def _load():
         "fm_int8_certify": (i, [p, i, i, i, i, i, p, p]),
         "fm_int8_workspace_size": (sz, [p, i, i, i, i, i, i]),
         "fm_int8_matmul_fast": (i, [p, i, p, p, p, p, i, i, i, i, i, i, i, p, p, sz, p]),
-        "fm_int8_plan_create": (i, [p, i, i, i, i, i, i, i, i, p, sz, p, pp]),
+        "fm_int8_certify_corrected": (i, [p, i, i, i, i, i, p, p]),
+        "fm_int8_workspace_size_corrected": (sz, [p, i, i, i, i, i, i]),
+        "fm_int8_matmul_corrected": (i, [p, i, p, p, p, p, i, i, i, i, i, i, i, p, p, sz, p]),
+        "fm_int8_plan_create": (i, [p, i, i, i, i, i, i, i, i, i, p, sz, p, pp]),
         "fm_int8_plan_run": (i, [p, p, p, p, p, p, p]),
         "fm_int8_plan_free": (None, [p]),
         "fm_fp8_encode": (i, [p, i64, i, i, p, p]),
@@ -435,8 +438,20 @@ def int8_certify(s: Scheme, levels: int = 1, b_A: int = 31, b_B: int = 31, h: in
 
 
 def int8_workspace_size(s: Scheme, M: int, N: int, K: int, levels: int = 1, g: int = 128,
-                        h: int = 32) -> int:
-    return int(lib.fm_int8_workspace_size(s.handle, levels, M, N, K, g, h))
+                        h: int = 32, correct: bool = False) -> int:
+    fn = lib.fm_int8_workspace_size_corrected if correct else lib.fm_int8_workspace_size
+    return int(fn(s.handle, levels, M, N, K, g, h))
+
+
+def int8_certify_corrected(s: Scheme, levels: int = 1, b_A: int = 127, b_B: int = 127,
+                           h: int = 32, g: int = 128) -> dict:
+    """The corrected computation's certificate (App. D): conditions and bounds."""
+    cond = (ct.c_int * 3)()
+    bnd = (ct.c_double * 3)()
+    _check(lib.fm_int8_certify_corrected(s.handle, levels, b_A, b_B, h, g, cond, bnd))
+    return dict(split=bool(cond[0]), int32=bool(cond[1]), one_group=bool(cond[2]),
+                certified=bool(cond[0] and cond[1] and cond[2]), term_bound=bnd[0],
+                qmax_A=int(bnd[1]), qmax_B=int(bnd[2]))
 
 
 def int8_matmul_fast(s: Scheme, Ac, dA, BTc, dB, levels: int = 1, g: int = 128, h: int = 32,
@@ -455,22 +470,41 @@ def int8_matmul_fast(s: Scheme, Ac, dA, BTc, dB, levels: int = 1, g: int = 128, 
     return out
 
 
+def int8_matmul_corrected(s: Scheme, Ac, dA, BTc, dB, levels: int = 1, g: int = 128,
+                          h: int = 32, b_A: int = 127, b_B: int = 127, ws=None, out=None,
+                          stream=None):
+    """The fast realization with the overflow correction (Sec. 4.3, eq. (2)):
+    same output bits as int8_matmul_classical up to code bound 127."""
+    M, N, K, out = _int8_operands(Ac, dA, BTc, dB, g, out)
+    if ws is None:
+        need = int8_workspace_size(s, M, N, K, levels, g, h, correct=True)
+        if need == 0:
+            raise FmError(-1, "fm_int8_workspace_size_corrected: arguments not supported")
+        ws = workspace(need, Ac.device)
+    _check(lib.fm_int8_matmul_corrected(s.handle, levels, _dptr(Ac), _dptr(dA), _dptr(BTc),
+                                        _dptr(dB), M, N, K, g, h, b_A, b_B, _dptr(out),
+                                        _dptr(ws), ws.numel(), _stream(stream)))
+    return out
+
+
 class Int8Plan:
     """A prepared fast call (fm_int8_plan_*): the scheme's tables and tile
     schedule are written to the workspace once; run() then launches only the
     block-sum and product kernels.  Holds its workspace."""
 
     def __init__(self, s: Scheme, M: int, N: int, K: int, levels: int = 1, g: int = 128,
-                 h: int = 32, b_A: int = 31, b_B: int = 31, ws=None, device=None, stream=None):
+                 h: int = 32, b_A: int = 31, b_B: int = 31, correct: bool = False, ws=None,
+                 device=None, stream=None):
         self._h = None
-        need = int8_workspace_size(s, M, N, K, levels, g, h)
+        need = int8_workspace_size(s, M, N, K, levels, g, h, correct)
         if need == 0:
             raise FmError(-1, "fm_int8_workspace_size: arguments not supported")
         self.ws = ws if ws is not None else workspace(need, device)
         self.M, self.N, self.K, self.g = M, N, K, g
         out = ct.c_void_p()
-        _check(lib.fm_int8_plan_create(s.handle, levels, M, N, K, g, h, b_A, b_B, _dptr(self.ws),
-                                       self.ws.numel(), _stream(stream), ct.byref(out)))
+        _check(lib.fm_int8_plan_create(s.handle, levels, M, N, K, g, h, b_A, b_B, int(correct),
+                                       _dptr(self.ws), self.ws.numel(), _stream(stream),
+                                       ct.byref(out)))
         self._h = out.value
 
     def __del__(self):

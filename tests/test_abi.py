@@ -230,12 +230,30 @@ def test_int8_plan_rejects_before_any_device_work():
     a null plan is an argument error."""
     s = fm.Scheme.base("strassen")
     out = ct.c_void_p()
-    rc = fm.lib.fm_int8_plan_create(s.handle, 2, 64, 64, 256, 128, 32, 32, 32, None, 0, None,
+    rc = fm.lib.fm_int8_plan_create(s.handle, 2, 64, 64, 256, 128, 32, 32, 32, 0, None, 0, None,
                                     ct.byref(out))
     assert rc == ERR["FM_E_UNCERTIFIED"] and not out.value
-    rc = fm.lib.fm_int8_plan_create(s.handle, 2, 64, 64, 256, 128, 64, 31, 31, None, 0, None,
+    rc = fm.lib.fm_int8_plan_create(s.handle, 2, 64, 64, 256, 128, 64, 31, 31, 0, None, 0, None,
                                     ct.byref(out))
     assert rc == ERR["FM_E_UNCERTIFIED"] and not out.value
     assert fm.lib.fm_int8_plan_run(None, None, None, None, None, None, None) == \
         ERR["FM_E_ARG"]
     fm.lib.fm_int8_plan_free(None)
+
+
+def test_corrected_certificate_from_the_library():
+    """App. D: at code bound 127 with blocks of 32 in groups of 128 the split
+    parts of two-level Strassen's block sums stay within +-2 and the weighted
+    terms of an output entry add up to at most 16 x 13,107,200 < 2^31; the
+    oracle's split agrees on the bound.  The corrected kernel needs one call
+    per group: groups of 256 are refused before any device work."""
+    s = fm.Scheme.base("strassen")
+    c = fm.int8_certify_corrected(s, 2, 127, 127, 32, 128)
+    assert c["certified"] and (c["qmax_A"], c["qmax_B"]) == (2, 2)
+    assert c["term_bound"] == 16 * 13107200
+    assert max(abs(oracle.int8_split(v)[1]) for v in (-508, 508)) == 2
+    assert not fm.int8_certify_corrected(s, 2, 127, 127, 64, 128)["one_group"]
+    out = ct.c_void_p()
+    rc = fm.lib.fm_int8_plan_create(s.handle, 2, 64, 64, 256, 256, 32, 127, 127, 1, None, 0, None,
+                                    ct.byref(out))
+    assert rc == ERR["FM_E_UNSUPPORTED"] and not out.value

@@ -159,3 +159,79 @@ def test_prepared_plan_runs_new_codes():
         assert np.array_equal(bits(out), bits(oracle.int8_classical(oAc, odA, oBc, odB, g)))
     with pytest.raises(ValueError):
         plan.run(Ac[:128].contiguous(), dA[:, :128].contiguous(), BTc, dB)
+
+
+def corrected_vs_classical(s, levels, M, K, N, seed, variants=None, dist="normal", b=127):
+    rng = np.random.default_rng(seed)
+    A = (rng.standard_normal((M, K)) if dist == "normal"
+         else rng.standard_t(3, (M, K))).astype(np.float32)
+    B = rng.standard_normal((K, N)).astype(np.float32)
+    (Ac, dA, BTc, dB), (oAc, odA, oBc, odB) = quantize_both(A, B, 128, b)
+    cl = fm.int8_matmul_classical(Ac, dA, BTc, dB, 128).cpu().numpy()
+    assert np.array_equal(bits(cl), bits(oracle.int8_classical(oAc, odA, oBc, odB, 128)))
+    schemes = [s] if variants is None else variants
+    ws = fm.workspace(fm.int8_workspace_size(schemes[0], M, N, K, levels, 128, 32, correct=True))
+    for sc in schemes:
+        out = fm.int8_matmul_corrected(sc, Ac, dA, BTc, dB, levels, 128, 32, b, b, ws=ws)
+        fm.status(ws)
+        assert np.array_equal(bits(out.cpu().numpy()), bits(cl))
+    return (oAc, odA, oBc, odB), cl
+
+
+def test_corrected_two_level_at_code_bound_127():
+    """Sec. 4.3: with the overflow correction two-level Strassen computes
+    classical int8 at code bound 127 bit for bit (blocks of 32, groups of
+    128), as the oracle's corrected realization does."""
+    say("[int8] corrected two-level Strassen 256x512x384, b=127")
+    (oAc, odA, oBc, odB), cl = corrected_vs_classical(fm.Scheme.base("strassen"), 2, 256, 512,
+                                                      384, 21)
+    (U, V, W), dims = oracle.flatten_f32(so.power(osch.strassen(), 2))
+    want, st = oracle.int8_fast_corrected(oAc, odA, oBc, odB, (U, V, W), dims, 128, 32)
+    assert st["overflows"] > 0
+    assert np.array_equal(bits(cl), bits(want))
+
+
+def test_corrected_ragged_tiles_and_heavy_tails():
+    say("[int8] corrected two-level Strassen 400x768x208, t(3), b=127")
+    corrected_vs_classical(fm.Scheme.base("strassen"), 2, 400, 768, 208, 22, dist="t3")
+
+
+def test_corrected_every_sign_variant():
+    say("[int8] corrected: 512 sign variants 64x256x64, b=127")
+    s2 = fm.Scheme.base("strassen").kron(2)
+    orbit = s2.gauge_orbit([(np.diag(d), np.diag(e), np.diag(f)) for d, e, f in sy.sign_orbit(4, 4, 4)])
+    corrected_vs_classical(None, 1, 64, 256, 64, 23, variants=orbit)
+
+
+def test_corrected_layer_slice_at_full_size():
+    """App. E's slice shape (512 token rows, 1024 output channels, inner
+    dimension 13824, groups of 128, blocks of 32) on the heavy-tailed
+    stand-in: corrected output equals classical int8 on every bit."""
+    say("[int8] corrected slice down_512x13824x1024, b=127")
+    w = sy.CORRECTION_SLICES["down_512x13824x1024"]
+    A, B = sy.operands(w)
+    s = fm.Scheme.base("strassen")
+    Ac, dA = fm.int8_quantize(gpu(A), 128, 127)
+    BTc, dB = fm.int8_quantize(gpu(np.ascontiguousarray(B.T)), 128, 127)
+    cl = fm.int8_matmul_classical(Ac, dA, BTc, dB, 128)
+    plan = fm.Int8Plan(s, w.M, w.N, w.K, 2, 128, 32, 127, 127, correct=True, device=DEV)
+    out = plan.run(Ac, dA, BTc, dB)
+    fm.status(plan.ws)
+    assert torch.equal(out.view(torch.int32), cl.view(torch.int32))
+
+
+def test_corrected_split_beyond_its_bound_is_reported():
+    """Codes quantized at 127 but declared within 63: the certificate allows
+    split parts |q| <= 1, block sums reach 2; the device reports FM_E_RANGE."""
+    rng = np.random.default_rng(24)
+    A = rng.standard_normal((64, 128)).astype(np.float32)
+    B = rng.standard_normal((128, 64)).astype(np.float32)
+    (Ac, dA, BTc, dB), _ = quantize_both(A, B, 128, 127)
+    s = fm.Scheme.base("strassen")
+    c = fm.int8_certify_corrected(s, 2, 63, 63, 32, 128)
+    assert c["certified"] and c["qmax_A"] == 1
+    ws = fm.workspace(fm.int8_workspace_size(s, 64, 64, 128, 2, 128, 32, correct=True))
+    fm.int8_matmul_corrected(s, Ac, dA, BTc, dB, 2, 128, 32, 63, 63, ws=ws)
+    with pytest.raises(fm.FmError) as e:
+        fm.status(ws)
+    assert e.value.name == "FM_E_RANGE"
