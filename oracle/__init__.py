@@ -20,7 +20,9 @@ Readings where the paper is silent (one scale per block-sum tensor by
 default, fmaf combination order, exact block products rounded once) are
 stated at each function in fm_oracle.c; the finer granularity of App. B.1's
 synthetic matrices (one scale per row of A's block sums and per column of
-B's) is the SCALE_ROWCOL mode.
+B's) is the SCALE_ROWCOL mode; the models' group scales (1 x 128 groups on
+A's block sums, 128 x 128 blocks on B's bf16-rounded block sums, products
+returned in bf16) are SCALE_GROUP.
 
 Every function is parity-pinned by tests/test_oracle_*.py.
 """
@@ -40,7 +42,8 @@ FMT = {"e4m3": E4M3, "e5m2": E5M2}
 # scale granularity: one scale per block-sum tensor, or (App. B.1's
 # synthetic form) one per row of each A-side and per column of each B-side
 # block sum
-SCALE_TENSOR, SCALE_ROWCOL = 0, 1
+SCALE_TENSOR, SCALE_ROWCOL, SCALE_GROUP = 0, 1, 2
+GROUP = 128  # inner-dimension group (and B-side block width) of SCALE_GROUP
 
 _lib = None
 
@@ -82,6 +85,9 @@ def lib():
                                                    p, p]),
             "orc_int8_fast": (i, [p, p, p, p, i, i, i, i, i, i, i, i, i, p, p, p, p, p]),
             "orc_int8_split": (None, [i64, p, p]),
+            "orc_block_product_groups": (None, [p, p, p, p, i, i, i, i, p]),
+            "orc_block_product_groups_acc": (None, [p, p, p, p, i, i, i, i, i, p]),
+            "orc_bf16_round": (f, [f]),
             "orc_int8_group_product_corrected": (None, [p, p, i, i, i, i, i, i, i, i, i, i, p, p,
                                                         p, p, p, p]),
             "orc_int8_fast_corrected": (i, [p, p, p, p, i, i, i, i, i, i, i, i, i, p, p, p, p,
@@ -173,16 +179,22 @@ def form_operands(X, gr: int, gc: int, coef, fmt: int = E4M3, scale_mode: int = 
     """Block sums of one operand for every product r, quantized.
     Returns codes (R, rows/gr, cols/gc) in X's orientation and scales d: (R,)
     per tensor, or with SCALE_ROWCOL (R, rows/gr) for side 0 (A, per row)
-    and (R, cols/gc) for side 1 (B, per column)."""
+    and (R, cols/gc) for side 1 (B, per column), or with SCALE_GROUP
+    (R, Kb/128, Mb) for side 0 and (R, Kb/128, Nb/128) for side 1."""
     X = _f32(X)
     coef = _f32(coef)
     R = coef.shape[0]
     rows, cols = X.shape
     codes = np.empty((R, rows // gr, cols // gc), np.uint8)
+    br, bc = rows // gr, cols // gc
     if scale_mode == SCALE_TENSOR:
         d = np.empty(R, np.float32)
+    elif scale_mode == SCALE_ROWCOL:
+        d = np.empty((R, br if side == 0 else bc), np.float32)
     else:
-        d = np.empty((R, rows // gr if side == 0 else cols // gc), np.float32)
+        assert bc % GROUP == 0 and (side == 0 or br % GROUP == 0)
+        d = np.empty((R, bc // GROUP, br) if side == 0 else (R, br // GROUP, bc // GROUP),
+                     np.float32)
     lib().orc_form_operands_sm(_ptr(X), rows, cols, gr, gc, R, _ptr(coef), fmt, scale_mode, side,
                                _ptr(codes), _ptr(d))
     return codes, d
@@ -212,6 +224,31 @@ def block_product_rc(Tq, Sq, dT, dS, fmt: int = E4M3) -> np.ndarray:
     out = np.empty((br, bc), np.float32)
     lib().orc_block_product_rc(_ptr(Tq), _ptr(Sq), _ptr(dT), _ptr(dS), br, bc, bk, fmt, _ptr(out))
     return out
+
+
+def block_product_groups(Tq, Sq, dT, dS, fmt: int = E4M3, bf16: bool = True) -> np.ndarray:
+    """Block product with group scales: dT (Kb/128, br), dS (Kb/128, bc/128);
+    per group the exact sum rounded once is added by fmaf with dT * dS, and
+    the product is returned rounded to bf16 (bf16=False: the fp32
+    accumulator itself)."""
+    Tq = np.ascontiguousarray(Tq, np.uint8)
+    Sq = np.ascontiguousarray(Sq, np.uint8)
+    br, bk = Tq.shape
+    bk2, bc = Sq.shape
+    assert bk == bk2 and bk % GROUP == 0 and bc % GROUP == 0
+    dT, dS = _f32(dT), _f32(dS)
+    assert dT.shape == (bk // GROUP, br) and dS.shape == (bk // GROUP, bc // GROUP)
+    out = np.empty((br, bc), np.float32)
+    lib().orc_block_product_groups_acc(_ptr(Tq), _ptr(Sq), _ptr(dT), _ptr(dS), br, bc, bk, fmt,
+                                       int(bf16), _ptr(out))
+    return out
+
+
+def bf16_round(x) -> np.ndarray:
+    """fp32 values rounded to the nearest bf16 (ties to even), as fp32."""
+    x = _f32(x)
+    f = lib().orc_bf16_round
+    return np.array([f(float(v)) for v in x.reshape(-1)], np.float32).reshape(x.shape)
 
 
 def block_product_at(Tq, Sq, dT, dS, xs, zs, fmt: int = E4M3) -> np.ndarray:
@@ -271,7 +308,8 @@ def lowp_matmul(A, B, scheme_f32, dims, fmt: int = E4M3, keep: bool = False,
     """FP8 evaluation of one scheme (fp32 coefficient tables U, V, W of the
     flattened scheme, dims = (m, k, n, R)).  Returns C, or with keep=True a
     dict with C, Tq (R, Mb, Kb), dT, Sq (R, Kb, Nb), dS and Mr (R, Mb, Nb);
-    dT and dS are (R,) per tensor or (R, Mb) and (R, Nb) with SCALE_ROWCOL."""
+    dT and dS are (R,) per tensor, (R, Mb) and (R, Nb) with SCALE_ROWCOL, or
+    (R, Kb/128, Mb) and (R, Kb/128, Nb/128) with SCALE_GROUP."""
     U, V, W = (_f32(t) for t in scheme_f32)
     gm, gk, gn, R = dims
     A, B = _f32(A), _f32(B)
@@ -284,9 +322,13 @@ def lowp_matmul(A, B, scheme_f32, dims, fmt: int = E4M3, keep: bool = False,
     if keep:
         Tq = np.empty((R, br, bk), np.uint8)
         Sq = np.empty((R, bk, bc), np.uint8)
-        rc_mode = scale_mode == SCALE_ROWCOL
-        dT = np.empty((R, br) if rc_mode else R, np.float32)
-        dS = np.empty((R, bc) if rc_mode else R, np.float32)
+        if scale_mode == SCALE_ROWCOL:
+            dT, dS = np.empty((R, br), np.float32), np.empty((R, bc), np.float32)
+        elif scale_mode == SCALE_GROUP:
+            dT = np.empty((R, bk // GROUP, br), np.float32)
+            dS = np.empty((R, bk // GROUP, bc // GROUP), np.float32)
+        else:
+            dT, dS = np.empty(R, np.float32), np.empty(R, np.float32)
         Mr = np.empty((R, br, bc), np.float32)
         args = [_ptr(Tq), _ptr(dT), _ptr(Sq), _ptr(dS), _ptr(Mr)]
     else:

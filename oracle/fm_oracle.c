@@ -213,6 +213,67 @@ void orc_quantize_cols(const float* T, int rows, int cols, int fmt, uint8_t* cod
 }
 
 /* ------------------------------------------------------------------------ */
+/* Group scales (App. B.1, the models' schedule): the block sums of A get a  */
+/* scale for every 128 consecutive entries of a row; those of B are first    */
+/* rounded to bf16 and get a scale for every 128 x 128 block.  Each scale    */
+/* follows the tensor rule on its group.  T is rows x cols row-major (B's    */
+/* block sums in B's orientation, bk x bc).  d is group-major:               */
+/* A: d[kg * rows + x]; B: d[kg * (cols / 128) + zb].                        */
+/* ------------------------------------------------------------------------ */
+#define ORC_GROUP 128
+
+/* fp32 -> nearest bf16 (ties to even), returned as the fp32 it equals. */
+float orc_bf16_round(float x) {
+  uint32_t u;
+  memcpy(&u, &x, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u) { /* Inf, NaN: truncate, keep NaN */
+    uint32_t t = u & 0xffff0000u;
+    if ((u & 0x007fffffu) && !(t & 0x007fffffu)) t |= 0x00400000u;
+    memcpy(&x, &t, 4);
+    return x;
+  }
+  uint32_t lsb = (u >> 16) & 1u;
+  u = (u + 0x7fffu + lsb) & 0xffff0000u;
+  memcpy(&x, &u, 4);
+  return x;
+}
+
+void orc_quantize_row_groups(const float* T, int rows, int cols, int fmt, uint8_t* codes,
+                             float* d) {
+  int ng = cols / ORC_GROUP;
+  for (int x = 0; x < rows; ++x)
+    for (int kg = 0; kg < ng; ++kg) {
+      const float* t = T + (int64_t)x * cols + (int64_t)kg * ORC_GROUP;
+      float r;
+      d[(int64_t)kg * rows + x] = orc_tensor_scale(t, ORC_GROUP, fmt, &r);
+      for (int y = 0; y < ORC_GROUP; ++y)
+        codes[(int64_t)x * cols + (int64_t)kg * ORC_GROUP + y] = orc_fp8_encode(t[y] * r, fmt);
+    }
+}
+
+void orc_quantize_bf16_blocks(const float* T, int rows, int cols, int fmt, uint8_t* codes,
+                              float* d) {
+  int nkg = rows / ORC_GROUP, nzb = cols / ORC_GROUP;
+  float* t = (float*)malloc(sizeof(float) * (size_t)rows * cols);
+  for (int64_t i = 0; i < (int64_t)rows * cols; ++i) t[i] = orc_bf16_round(T[i]);
+  for (int kg = 0; kg < nkg; ++kg)
+    for (int zb = 0; zb < nzb; ++zb) {
+      float amax = 0.0f;
+      for (int y = kg * ORC_GROUP; y < (kg + 1) * ORC_GROUP; ++y)
+        for (int z = zb * ORC_GROUP; z < (zb + 1) * ORC_GROUP; ++z) {
+          float a = fabsf(t[(int64_t)y * cols + z]);
+          if (a > amax) amax = a;
+        }
+      float r;
+      d[(int64_t)kg * nzb + zb] = scale_from_amax(amax, fmt, &r);
+      for (int y = kg * ORC_GROUP; y < (kg + 1) * ORC_GROUP; ++y)
+        for (int z = zb * ORC_GROUP; z < (zb + 1) * ORC_GROUP; ++z)
+          codes[(int64_t)y * cols + z] = orc_fp8_encode(t[(int64_t)y * cols + z] * r, fmt);
+    }
+  free(t);
+}
+
+/* ------------------------------------------------------------------------ */
 /* Block product M = (Tq * Sq) scaled: the FP8 values are multiples of the   */
 /* format's smallest subnormal q0 (2^-9 for E4M3, 2^-16 for E5M2), so every  */
 /* value is an integer times q0 and every product an integer times q0^2.    */
@@ -272,6 +333,49 @@ void orc_block_product_rc(const uint8_t* Tq, const uint8_t* Sq, const float* dT,
       m = m * dS[z];
       Mout[(int64_t)x * bc + z] = m;
     }
+}
+
+/* The block product with group scales: for every group kg of 128 inner     */
+/* indices, the exact sum P rounded once to fp32 is added as                  */
+/* acc = fmaf(P, fl(dT[kg][x] * dS[kg][z / 128]), acc) from +0 in ascending   */
+/* kg; the product is returned rounded to bf16 (held as fp32).               */
+void orc_block_product_groups_acc(const uint8_t* Tq, const uint8_t* Sq, const float* dT,
+                                  const float* dS, int br, int bc, int bk, int fmt, int bf16_out,
+                                  float* Mout);
+void orc_block_product_groups(const uint8_t* Tq, const uint8_t* Sq, const float* dT,
+                              const float* dS, int br, int bc, int bk, int fmt, float* Mout) {
+  orc_block_product_groups_acc(Tq, Sq, dT, dS, br, bc, bk, fmt, 1, Mout);
+}
+
+/* The same with the fp32 accumulator itself returned when bf16_out is 0. */
+void orc_block_product_groups_acc(const uint8_t* Tq, const uint8_t* Sq, const float* dT,
+                                  const float* dS, int br, int bc, int bk, int fmt, int bf16_out,
+                                  float* Mout) {
+  int ng = bk / ORC_GROUP, nzb = bc / ORC_GROUP;
+  int64_t* ti = (int64_t*)malloc(sizeof(int64_t) * (size_t)br * bk);
+  int64_t* sti = (int64_t*)malloc(sizeof(int64_t) * (size_t)bc * bk); /* Sq^T */
+  for (int64_t i = 0; i < (int64_t)br * bk; ++i) ti[i] = code_to_int(Tq[i], fmt);
+  for (int y = 0; y < bk; ++y)
+    for (int z = 0; z < bc; ++z)
+      sti[(int64_t)z * bk + y] = code_to_int(Sq[(int64_t)y * bc + z], fmt);
+#pragma omp parallel for schedule(static)
+  for (int x = 0; x < br; ++x) {
+    for (int z = 0; z < bc; ++z) {
+      const int64_t* a = ti + (int64_t)x * bk;
+      const int64_t* b = sti + (int64_t)z * bk;
+      float acc = 0.0f;
+      for (int kg = 0; kg < ng; ++kg) {
+        __int128 sum = 0;
+        for (int y = kg * ORC_GROUP; y < (kg + 1) * ORC_GROUP; ++y) sum += (__int128)a[y] * b[y];
+        float P = exact_sum_to_float(sum, fmt);
+        float sc = dT[(int64_t)kg * br + x] * dS[(int64_t)kg * nzb + z / ORC_GROUP];
+        acc = fmaf(P, sc, acc);
+      }
+      Mout[(int64_t)x * bc + z] = bf16_out ? orc_bf16_round(acc) : acc;
+    }
+  }
+  free(ti);
+  free(sti);
 }
 
 /* The same block product at selected positions (xs[t], zs[t]) only. */
@@ -400,8 +504,11 @@ int orc_lowp_matmul(const float* A, const float* B, int M, int N, int K,
 
 /* The whole schedule with a choice of scale granularity: scale_mode 0 is   */
 /* one scale per block-sum tensor (orc_lowp_matmul), 1 is one per row of     */
-/* each A-side block sum and one per column of each B-side block sum.        */
-/* Scale outputs hold R values (mode 0) or R x br and R x bc (mode 1).       */
+/* each A-side block sum and one per column of each B-side block sum, 2 the  */
+/* group scales (1 x 128 on A's block sums, 128 x 128 on B's bf16-rounded    */
+/* ones, products returned in bf16).  Scale outputs hold R values (mode 0),  */
+/* R x br and R x bc (mode 1), or R x (bk/128) x br and                      */
+/* R x (bk/128) x (bc/128) (mode 2).                                          */
 int orc_lowp_matmul_sm(const float* A, const float* B, int M, int N, int K,
                        int gm, int gk, int gn, int R, const float* U,
                        const float* V, const float* W, int fmt, int scale_mode,
@@ -410,26 +517,33 @@ int orc_lowp_matmul_sm(const float* A, const float* B, int M, int N, int K,
   if (scale_mode == 0)
     return orc_lowp_matmul(A, B, M, N, K, gm, gk, gn, R, U, V, W, fmt, C, Tq_out, dT_out,
                            Sq_out, dS_out, Mr_out);
-  if (scale_mode != 1) return -2;
+  if (scale_mode != 1 && scale_mode != 2) return -2;
   if (M % gm || K % gk || N % gn) return -1;
   int br = M / gm, bk = K / gk, bc = N / gn;
+  if (scale_mode == 2 && (bk % ORC_GROUP || bc % ORC_GROUP)) return -1;
+  /* scales per product: mode 1 br and bc; mode 2 (bk/128) br and (bk/128) (bc/128) */
+  int64_t nta = scale_mode == 1 ? br : (int64_t)(bk / ORC_GROUP) * br;
+  int64_t nsb = scale_mode == 1 ? bc : (int64_t)(bk / ORC_GROUP) * (bc / ORC_GROUP);
   int64_t tsz = (int64_t)br * bk, ssz = (int64_t)bk * bc, msz = (int64_t)br * bc;
   float* T = (float*)malloc(sizeof(float) * (size_t)(tsz > ssz ? tsz : ssz));
   uint8_t* tq = (uint8_t*)malloc((size_t)tsz);
   uint8_t* sq = (uint8_t*)malloc((size_t)ssz);
-  float* dT = (float*)malloc(sizeof(float) * (size_t)br);
-  float* dS = (float*)malloc(sizeof(float) * (size_t)bc);
+  float* dT = (float*)malloc(sizeof(float) * (size_t)nta);
+  float* dS = (float*)malloc(sizeof(float) * (size_t)nsb);
   float* Mr = Mr_out ? Mr_out : (float*)malloc(sizeof(float) * (size_t)(msz * R));
   for (int r = 0; r < R; ++r) {
     orc_block_sum(A, M, K, gm, gk, U + (int64_t)r * gm * gk, T);
-    orc_quantize_rows(T, br, bk, fmt, tq, dT);
+    if (scale_mode == 1) orc_quantize_rows(T, br, bk, fmt, tq, dT);
+    else orc_quantize_row_groups(T, br, bk, fmt, tq, dT);
     orc_block_sum(B, K, N, gk, gn, V + (int64_t)r * gk * gn, T);
-    orc_quantize_cols(T, bk, bc, fmt, sq, dS);
+    if (scale_mode == 1) orc_quantize_cols(T, bk, bc, fmt, sq, dS);
+    else orc_quantize_bf16_blocks(T, bk, bc, fmt, sq, dS);
     if (Tq_out) memcpy(Tq_out + r * tsz, tq, (size_t)tsz);
     if (Sq_out) memcpy(Sq_out + r * ssz, sq, (size_t)ssz);
-    if (dT_out) memcpy(dT_out + (int64_t)r * br, dT, sizeof(float) * (size_t)br);
-    if (dS_out) memcpy(dS_out + (int64_t)r * bc, dS, sizeof(float) * (size_t)bc);
-    orc_block_product_rc(tq, sq, dT, dS, br, bc, bk, fmt, Mr + r * msz);
+    if (dT_out) memcpy(dT_out + (int64_t)r * nta, dT, sizeof(float) * (size_t)nta);
+    if (dS_out) memcpy(dS_out + (int64_t)r * nsb, dS, sizeof(float) * (size_t)nsb);
+    if (scale_mode == 1) orc_block_product_rc(tq, sq, dT, dS, br, bc, bk, fmt, Mr + r * msz);
+    else orc_block_product_groups(tq, sq, dT, dS, br, bc, bk, fmt, Mr + r * msz);
   }
   orc_reconstruct(Mr, W, R, gm, gn, br, bc, C);
   if (!Mr_out) free(Mr);
@@ -457,7 +571,9 @@ void orc_form_operands(const float* X, int rows, int cols, int gr, int gc, int R
 
 /* The same with a choice of scale granularity: scale_mode 1 gives one scale */
 /* per row of each block sum (side 0, A) or per column (side 1, B); d holds  */
-/* R x (rows/gr) or R x (cols/gc) values.                                    */
+/* R x (rows/gr) or R x (cols/gc) values.  scale_mode 2: the group scales   */
+/* (side 0: 1 x 128 groups, d R x (bc/128) x br; side 1: bf16 rounding then */
+/* 128 x 128 blocks, d R x (br/128) x (bc/128)).                             */
 void orc_form_operands_sm(const float* X, int rows, int cols, int gr, int gc, int R,
                           const float* coef, int fmt, int scale_mode, int side,
                           uint8_t* codes, float* d) {
@@ -468,12 +584,20 @@ void orc_form_operands_sm(const float* X, int rows, int cols, int gr, int gc, in
   int br = rows / gr, bc = cols / gc;
   int64_t sz = (int64_t)br * bc;
   float* T = (float*)malloc(sizeof(float) * (size_t)sz);
+  /* mode 2 scales per product: A (bc/128) br, B (br/128) (bc/128) */
+  int64_t nd = scale_mode == 1 ? (side == 0 ? br : bc)
+                               : (side == 0 ? (int64_t)(bc / ORC_GROUP) * br
+                                            : (int64_t)(br / ORC_GROUP) * (bc / ORC_GROUP));
   for (int r = 0; r < R; ++r) {
     orc_block_sum(X, rows, cols, gr, gc, coef + (int64_t)r * gr * gc, T);
-    if (side == 0)
-      orc_quantize_rows(T, br, bc, fmt, codes + r * sz, d + (int64_t)r * br);
+    if (scale_mode == 1 && side == 0)
+      orc_quantize_rows(T, br, bc, fmt, codes + r * sz, d + r * nd);
+    else if (scale_mode == 1)
+      orc_quantize_cols(T, br, bc, fmt, codes + r * sz, d + r * nd);
+    else if (side == 0)
+      orc_quantize_row_groups(T, br, bc, fmt, codes + r * sz, d + r * nd);
     else
-      orc_quantize_cols(T, br, bc, fmt, codes + r * sz, d + (int64_t)r * bc);
+      orc_quantize_bf16_blocks(T, br, bc, fmt, codes + r * sz, d + r * nd);
   }
   free(T);
 }
