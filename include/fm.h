@@ -78,8 +78,13 @@ typedef enum { FM_ACC_BF16 = 0, FM_ACC_FP8 = 1 } fm_accum;
  *   FM_SCALE_ROWCOL: one scale per row of every block sum of A and per
  *     column of every block sum of B, the form the paper uses on synthetic
  *     matrices (App. B.1); scale arrays hold R x Mb values (A side) and
- *     R x Nb values (B side) per gauge. */
-typedef enum { FM_SCALE_TENSOR = 0, FM_SCALE_ROWCOL = 1 } fm_scale_mode;
+ *     R x Nb values (B side) per gauge.
+ *   FM_SCALE_GROUP: the models' schedule (App. B.1): one scale per row of
+ *     A's block sums and 128 consecutive inner entries; B's block sums are
+ *     first rounded to bf16, then get one scale per 128 x 128 block; block
+ *     products are returned in bf16 (as fp32 values).  Scale arrays hold
+ *     R x (Kb/128) x Mb (A) and R x (Kb/128) x (Nb/128) (B) per gauge. */
+typedef enum { FM_SCALE_TENSOR = 0, FM_SCALE_ROWCOL = 1, FM_SCALE_GROUP = 2 } fm_scale_mode;
 
 typedef struct {
   double rel_fro; /* ||C - C_ref||_F / ||C_ref||_F (0 if C_ref = 0)         */
@@ -250,6 +255,16 @@ int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A,
  * M_r[x][z] = ((sum_k Tq_r[x][k] Sq_r[z][k]) * dT_r[x]) * dS_r[z].
  * Scale arrays: dT holds R^L x Mb floats ([r][x]), dS holds R^L x Nb floats
  * ([r][z]); fm_block_products_scaled takes batch x Mb and batch x Nb.
+ * FM_SCALE_GROUP (App. B.1, the models' schedule): every group of 128
+ * consecutive inner entries of a row of T_r has its own scale, and S_r,
+ * rounded to bf16 (nearest even) first, one per 128 x 128 block (128
+ * columns z by 128 inner entries); then for every group kg in ascending
+ * order acc = fmaf(P_kg, dT_r[kg][x] * dS_r[kg][z / 128], acc) from +0,
+ * where P_kg is the group's sum of code products, and M_r = bf16(acc).
+ * Needs Kb and Nb multiples of 128 and Mb of 4 (FM_E_SHAPE otherwise).
+ * Scale arrays: dT [r][kg][x] (R^L x Kb/128 x Mb), dS [r][kg][zb]
+ * (R^L x Kb/128 x Nb/128); fm_block_products_scaled takes them per batch
+ * entry in that layout.
  * FM_E_ARG for an unknown mode; otherwise errors as in the calls above. */
 
 /* Workspace bytes for fm_orbit_eval_scaled / fm_matmul_lowp_scaled /

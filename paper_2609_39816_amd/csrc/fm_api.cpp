@@ -112,9 +112,22 @@ struct Layout {
 };
 
 // Scales per (gauge, product) on each side: 1, or one per block-sum row
-// (A side, Mb) and per block-sum column (B side, Nb).
-int scales_a(const Geometry& g, int scale_mode) { return scale_mode == FM_SCALE_ROWCOL ? g.Mb : 1; }
-int scales_b(const Geometry& g, int scale_mode) { return scale_mode == FM_SCALE_ROWCOL ? g.Nb : 1; }
+// (A side, Mb) and per block-sum column (B side, Nb), or per group: (Kb/128)
+// Mb on A's side and (Kb/128) (Nb/128) on B's.
+int scales_a(const Geometry& g, int scale_mode) {
+  return scale_mode == FM_SCALE_ROWCOL ? g.Mb : scale_mode == FM_SCALE_GROUP ? g.Kb / 128 * g.Mb : 1;
+}
+int scales_b(const Geometry& g, int scale_mode) {
+  return scale_mode == FM_SCALE_ROWCOL ? g.Nb
+                                       : scale_mode == FM_SCALE_GROUP ? g.Kb / 128 * (g.Nb / 128) : 1;
+}
+// Block shapes a scale mode needs (group scales: Kb, Nb multiples of 128,
+// Mb of 4).
+int scale_shape_ok(int Mb, int Nb, int Kb, int scale_mode) {
+  if (scale_mode == FM_SCALE_GROUP && (Kb % 128 || Nb % 128 || Mb % 4))
+    return fail(FM_E_SHAPE, "group scales need Kb, Nb multiples of 128 and Mb of 4");
+  return FM_OK;
+}
 
 Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
                    int scale_mode = FM_SCALE_TENSOR) {
@@ -137,7 +150,7 @@ Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
   const size_t nsc = (size_t)chunk * R * (scales_a(g, scale_mode) + scales_b(g, scale_mode));
   L.amax = take(nsc * 4);
   L.q = take(nsc * 4);
-  L.d = take(nsc * 4);
+  L.d = take(nsc * 4 + 16);  // whole 16-byte chunks for the kernels' scale loads
   L.tq = take((size_t)chunk * R * g.Mb * g.Kb);
   L.sq = take((size_t)chunk * R * g.Nb * g.Kb);
   L.mprod = take((size_t)chunk * R * g.Mb * g.Nb * 4);
@@ -257,11 +270,21 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
   auto idx = [&](int k) { return (const int32_t*)(ws + L.idx[k]); };
   auto coef = [&](int k) { return (const float*)(ws + L.coef[k]); };
   const int pa = chunk_pattern(T, 0, g0, n), pb = chunk_pattern(T, 1, g0, n);
-  if (int rc = launch_fill_u32(amax, na + nb, 0u, st)) return rc;
   FormArgs fa{A,    geo.M, geo.K, geo.gm, geo.gk, geo.Mb, geo.Kb, off(0), idx(0), coef(0), R, n,
               amax, q,     Tq,    fmt,    per_row};
   FormArgs fb{Bt, geo.N, geo.K, geo.gn, geo.gk, geo.Nb, geo.Kb, off(1), idx(1), coef(1), R, n,
               amax + na, q + na, Sq, fmt, per_row};
+  if (scale_mode == FM_SCALE_GROUP) {
+    // one pass per side: every group's maximum is local to its wave or workgroup
+    for (int side = 0; side < 2; ++side) {
+      timing_begin(T_FORM_QUANT, st);
+      if (int rc = launch_form_group(side ? fb : fa, side, side ? dd + na : dd,
+                                     (uint32_t*)(ws + L.flags), st))
+        return rc;
+      timing_end(T_FORM_QUANT, st);
+    }
+  } else {
+  if (int rc = launch_fill_u32(amax, na + nb, 0u, st)) return rc;
   for (int side = 0; side < 2; ++side) {
     timing_begin(T_FORM_AMAX, st);
     if (int rc = launch_form(side ? fb : fa, 0, side ? pb : pa, side, st)) return rc;
@@ -273,6 +296,7 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
     timing_begin(T_FORM_QUANT, st);
     if (int rc = launch_form(side ? fb : fa, 1, side ? pb : pa, side, st)) return rc;
     timing_end(T_FORM_QUANT, st);
+  }
   }
   if (dT)
     if (int rc = hip_check(hipMemcpyAsync(dT, dd, na * 4, hipMemcpyDeviceToDevice, st),
@@ -633,12 +657,15 @@ int fm_scheme_coeffs_f32(const fm_scheme* s, int levels, float* U, float* V, flo
 
 void fm_scheme_free(fm_scheme* s) { delete s; }
 
-static int scale_mode_ok(int m) { return m == FM_SCALE_TENSOR || m == FM_SCALE_ROWCOL; }
+static int scale_mode_ok(int m) {
+  return m == FM_SCALE_TENSOR || m == FM_SCALE_ROWCOL || m == FM_SCALE_GROUP;
+}
 
 size_t fm_workspace_size_scaled(const fm_scheme* s, int M, int N, int K, int levels, int G,
                                 int chunk, fm_scale_mode scale_mode) {
   Geometry g;
-  if (G < 1 || !scale_mode_ok(scale_mode) || check_geometry(s, levels, M, N, K, g) != FM_OK)
+  if (G < 1 || !scale_mode_ok(scale_mode) || check_geometry(s, levels, M, N, K, g) != FM_OK ||
+      scale_shape_ok(g.Mb, g.Nb, g.Kb, scale_mode) != FM_OK)
     return 0;
   if (chunk <= 0 || chunk > G) chunk = G;
   return make_layout(g, G, chunk, true, scale_mode).total;
@@ -664,6 +691,7 @@ int fm_form_operands_scaled(const fm_scheme* s, int levels, const float* A, cons
   if (!scale_mode_ok(scale_mode)) return fail(FM_E_ARG, "bad scale mode");
   Geometry geo;
   if (int rc = check_geometry(s, levels, M, N, K, geo)) return rc;
+  if (int rc = scale_shape_ok(geo.Mb, geo.Nb, geo.Kb, scale_mode)) return rc;
   const Layout L = make_layout(geo, 1, 1, true, scale_mode);
   if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
   hipStream_t st = (hipStream_t)hip_stream;
@@ -737,6 +765,7 @@ int fm_matmul_lowp_scaled(const fm_scheme* s, const float* A, const float* B, fl
   if (!scale_mode_ok(scale_mode)) return fail(FM_E_ARG, "bad scale mode");
   Geometry geo;
   if (int rc = check_geometry(s, levels, M, N, K, geo)) return rc;
+  if (int rc = scale_shape_ok(geo.Mb, geo.Nb, geo.Kb, scale_mode)) return rc;
   const Layout L = make_layout(geo, 1, 1, true, scale_mode);
   if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
   hipStream_t st = (hipStream_t)hip_stream;
@@ -816,6 +845,7 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   if (!scale_mode_ok(scale_mode)) return fail(FM_E_ARG, "bad scale mode");
   Geometry geo;
   if (int rc = check_geometry(gauged[0], levels, M, N, K, geo)) return rc;
+  if (int rc = scale_shape_ok(geo.Mb, geo.Nb, geo.Kb, scale_mode)) return rc;
   int chunk = G;
   Layout L = make_layout(geo, G, chunk, true, scale_mode);
   while (chunk > 1 && L.total > ws_bytes) {

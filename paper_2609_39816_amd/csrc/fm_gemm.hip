@@ -212,7 +212,11 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
                                                        const float* __restrict__ dS,
                                                        float* __restrict__ Mout, int Mb, int Nb,
                                                        int Kb, int tiles_m, int tiles_n, int total) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[DNS * DSTAGE];
+  // SC = 2 (group scales): every K step is one group of 128; its scales ride
+  // the ring in a 2 KB slot after the stage (dT of the tile's 256 rows, then
+  // the tile's one dS)
+  constexpr int STG = SC == 2 ? DSTAGE + 2048 : DSTAGE;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[DNS * STG];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -251,7 +255,23 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
         row = row < Nb ? row : 0;
         src = Bb + (size_t)row * Kb + ch * 16;
       }
-      dma16(src, lds_base + (uint32_t)(buf * DSTAGE + r0 * GK));
+      dma16(src, lds_base + (uint32_t)(buf * STG + r0 * GK));
+    }
+    if constexpr (SC == 2) {
+      // wave 0: dT[b][kt][m0 + 4 lane .. + 3] (Mb a multiple of 4); wave 1:
+      // the 16-byte-aligned chunk holding dS[b][kt][n0 / 128] (the scale
+      // arrays are padded to whole chunks)
+      if (wave < 2) {
+        const size_t grp = (size_t)b * nk + kt;
+        const float* src;
+        if (wave == 0) {
+          const int row = m0 + 4 * lane;
+          src = dT + grp * Mb + (row < Mb ? row : 0);
+        } else {
+          src = dS + ((grp * (Nb / 128) + n0 / 128) & ~(size_t)3);
+        }
+        dma16(src, lds_base + (uint32_t)(buf * STG + DSTAGE + wave * 1024));
+      }
     }
   };
   // Half h of a K step: lane (l16, q) of fragment i holds bytes
@@ -262,22 +282,48 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = wm * 64 + i * 16 + l16;
-      fa[h][i] = *reinterpret_cast<const uint4*>(lds + buf * DSTAGE + row * GK +
+      fa[h][i] = *reinterpret_cast<const uint4*>(lds + buf * STG + row * GK +
                                                  (((2 * q + h) ^ swz(row)) << 4));
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int row = DBM + wn * 64 + j * 16 + l16;
-      fb[h][j] = *reinterpret_cast<const uint4*>(lds + buf * DSTAGE + row * GK +
+      fb[h][j] = *reinterpret_cast<const uint4*>(lds + buf * STG + row * GK +
                                                  (((2 * q + h) ^ swz(row)) << 4));
     }
   };
 
   v4f acc[4][4];
+  v4f ofl[4][4];  // SC = 2: the fp32 sum over the groups so far
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) {
+      acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
+      ofl[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
+    }
+  // SC = 2: the step's scales, read from its ring slot before the barrier
+  float gs[4];
+  auto read_scales = [&](int buf, int tile, int kt) {
+    const float* sA = reinterpret_cast<const float*>(lds + buf * STG + DSTAGE);
+    const float* sB = reinterpret_cast<const float*>(lds + buf * STG + DSTAGE + 1024);
+    const int b = tile / tiles, tt = tile - b * tiles;
+    const int n0 = (tt - (tt / tiles_n) * tiles_n) * DBN;
+    const float ds = sB[(((size_t)b * nk + kt) * (Nb / 128) + n0 / 128) & 3];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) gs[i] = sA[wm * 64 + i * 16 + l16] * ds;
+  };
+  // out = fmaf(group sum, dT dS, out), then the next group starts from zero
+  auto rescale = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) ofl[i][j][v] = __builtin_fmaf(acc[i][j][v], gs[i], ofl[i][j][v]);
+        acc[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
+      }
+  };
 
   // acc[i][j] holds the transposed 16 x 16 product: element (4q+v, l16) is
   // output row i*16 + l16, column j*16 + 4q + v of the wave's 64 x 64 block
@@ -326,7 +372,40 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
     float* Mo = Mout + (size_t)b * Mb * Nb;
     const int r_base = m0 + wm * 64 + l16, c_base = n0 + wn * 64 + 4 * q;
     int counted = 0;
-    if (vec_store && m0 + DBM <= Mb && n0 + DBN <= Nb) {
+    if constexpr (SC == 2) {
+      // products returned in bf16 (nearest even), held as fp32
+      auto bf = [](float x) {
+        const uint32_t u = __float_as_uint(x);
+        return __uint_as_float((u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u);
+      };
+      if (m0 + DBM <= Mb && n0 + DBN <= Nb) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float* prow = Mo + (size_t)(r_base + i * 16) * Nb + c_base;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            *reinterpret_cast<float4*>(prow + j * 16) =
+                make_float4(bf(ofl[i][j][0]), bf(ofl[i][j][1]), bf(ofl[i][j][2]), bf(ofl[i][j][3]));
+        }
+        counted = DSTORES;
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = r_base + i * 16;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int col = c_base + j * 16 + v;
+              if (row < Mb && col < Nb) Mo[(size_t)row * Nb + col] = bf(ofl[i][j][v]);
+            }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) ofl[i][j] = (v4f){0.f, 0.f, 0.f, 0.f};
+    } else if (vec_store && m0 + DBM <= Mb && n0 + DBN <= Nb) {
       float sT[4];
       float4 sS[4];
       if constexpr (SC) {
@@ -414,6 +493,7 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
   int cb = 0;  // buffer of p_s
   while (true) {
     read_half(1, cb);
+    if constexpr (SC == 2) read_scales(cb, ct, ck);
     compute_half(0);
     wait_vm(after1);                     // p_{s+1} has landed (this wave's share)
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of p_s are done
@@ -430,6 +510,7 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
     const bool more = t1 < t_end;
     if (more) read_half(0, nb);
     compute_half(1);
+    if constexpr (SC == 2) rescale();
     if (ck == nk - 1) after2 += epilogue(ct);
     FM_COMPILER_FENCE();
     if (!more) break;
@@ -478,6 +559,9 @@ int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, 
     }
     return launched("gemm_dma_kernel");
   }
+  if constexpr (SC == 2) {
+    return fail(FM_E_SHAPE, "group scales need inner blocks of a multiple of 128");
+  } else {
   // inner length a multiple of 16 only: one 128 x 128 tile per workgroup
   const int tm = (Mb + GT - 1) / GT, tn = (Nb + GT - 1) / GT;
   const long long total = (long long)batch * tm * tn;
@@ -491,6 +575,7 @@ int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, 
     else gemm_tile_kernel<FM_E5M2, 0, SC><<<T, kThreads, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
   }
   return launched("gemm_tile_kernel");
+  }
 }
 }  // namespace
 
@@ -499,6 +584,11 @@ int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, con
                       hipStream_t st) {
   if (scale_mode == FM_SCALE_ROWCOL)
     return launch_block_gemm_sc<1>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
+  if (scale_mode == FM_SCALE_GROUP) {
+    if (Kb % 128 || Nb % 128 || Mb % 4)
+      return fail(FM_E_SHAPE, "group scales need Kb, Nb multiples of 128 and Mb of 4");
+    return launch_block_gemm_sc<2>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
+  }
   return launch_block_gemm_sc<0>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
 }
 

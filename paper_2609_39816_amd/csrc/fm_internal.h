@@ -116,6 +116,10 @@ struct FormArgs {
 // pattern: family id from match_pattern (side A or B), or -1 for the
 // generic kernel.
 int launch_form(const FormArgs& a, int mode, int pattern, int side, hipStream_t st);
+// Group scales in one pass (side 0: 1 x 128 groups of A's block sums; side
+// 1: 128 x 128 blocks of B's bf16-rounded block sums): codes into a.codes,
+// scales d[(g R + r) (Kb/128) + kg][x] or [..][zb]; non-finite sets *flag |= 1.
+int launch_form_group(const FormArgs& a, int side, float* d, uint32_t* flag, hipStream_t st);
 
 // Scales from amax: for i < n: q[i] = FMAX/amax, d[i] = amax/FMAX (1, 1 for
 // amax = 0); a non-finite amax sets *flag |= 1.

@@ -25,7 +25,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "fm.h")
 
 E4M3, E5M2 = 0, 1
 ACC_BF16, ACC_FP8 = 0, 1
-SCALE_TENSOR, SCALE_ROWCOL = 0, 1  # fm_scale_mode
+SCALE_TENSOR, SCALE_ROWCOL, SCALE_GROUP = 0, 1, 2  # fm_scale_mode
 FMTS = {"e4m3": E4M3, "e5m2": E5M2}
 ERRORS = {0: "FM_OK", -1: "FM_E_ARG", -2: "FM_E_SHAPE", -3: "FM_E_BRENT", -4: "FM_E_SINGULAR",
           -5: "FM_E_NONFINITE", -6: "FM_E_WORKSPACE", -7: "FM_E_HIP", -8: "FM_E_MISMATCH",
@@ -236,7 +236,8 @@ def workspace(nbytes: int, device=None):
 def form_operands(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, stream=None,
                   scale_mode: int = SCALE_TENSOR):
     """Quantized block sums: Tq (R, Mb, Kb) u8, Sq (R, Nb, Kb) u8 (transposed),
-    dT (R,) and dS (R,) fp32, or (R, Mb) and (R, Nb) with SCALE_ROWCOL."""
+    dT (R,) and dS (R,) fp32, or (R, Mb) and (R, Nb) with SCALE_ROWCOL, or
+    (R, Kb/128, Mb) and (R, Kb/128, Nb/128) with SCALE_GROUP."""
     _cuda(A, torch.float32), _cuda(B, torch.float32)
     M, K = A.shape
     N = B.shape[1]
@@ -244,9 +245,12 @@ def form_operands(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, st
     Mb, Nb = M // gm, N // gn
     Tq = torch.empty((R, Mb, K // gk), dtype=torch.uint8, device=A.device)
     Sq = torch.empty((R, Nb, K // gk), dtype=torch.uint8, device=A.device)
-    rc = scale_mode == SCALE_ROWCOL
-    dT = torch.empty((R, Mb) if rc else (R,), dtype=torch.float32, device=A.device)
-    dS = torch.empty((R, Nb) if rc else (R,), dtype=torch.float32, device=A.device)
+    Kb = K // gk
+    shp = {SCALE_ROWCOL: ((R, Mb), (R, Nb)),
+           SCALE_GROUP: ((R, Kb // 128, Mb), (R, Kb // 128, Nb // 128))}.get(scale_mode,
+                                                                           ((R,), (R,)))
+    dT = torch.empty(shp[0], dtype=torch.float32, device=A.device)
+    dS = torch.empty(shp[1], dtype=torch.float32, device=A.device)
     if ws is None:
         ws = workspace(workspace_size(s, M, N, K, levels, 1, 1, scale_mode), A.device)
     _check(lib.fm_form_operands_scaled(s.handle, levels, _dptr(A), _dptr(B), M, N, K, fmt,
@@ -258,14 +262,28 @@ def form_operands(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, st
 def block_products(Tq, Sq, dT, dS, fmt: int = E4M3, out=None, stream=None,
                    scale_mode: int = SCALE_TENSOR):
     """Mout[b] = ((Tq[b] Sq[b]^T) * dT) * dS; dT, dS per product (batch,) or,
-    with SCALE_ROWCOL, per row (batch, Mb) and per column (batch, Nb)."""
+    with SCALE_ROWCOL, per row (batch, Mb) and per column (batch, Nb); with
+    SCALE_GROUP per group (batch, Kb/128, Mb) and (batch, Kb/128, Nb/128),
+    products returned in bf16 (as fp32 values)."""
     _cuda(Tq, torch.uint8), _cuda(Sq, torch.uint8)
     batch, Mb, Kb = Tq.shape
     Nb = Sq.shape[1]
-    want = (batch * Mb, batch * Nb) if scale_mode == SCALE_ROWCOL else (batch, batch)
+    want = {SCALE_ROWCOL: (batch * Mb, batch * Nb),
+            SCALE_GROUP: (batch * (Kb // 128) * Mb, batch * (Kb // 128) * (Nb // 128))
+            }.get(scale_mode, (batch, batch))
     if (dT.numel(), dS.numel()) != want:
         raise ValueError(f"scale arrays hold {dT.numel()} and {dS.numel()} values, need {want}")
     _cuda(dT, torch.float32), _cuda(dS, torch.float32)
+    if scale_mode == SCALE_GROUP:
+        # the kernel reads scales in aligned 16-byte chunks: give it a fresh,
+        # padded copy whenever the caller's arrays are not such
+        def padded(t):
+            if t.data_ptr() % 16 == 0 and t.numel() % 4 == 0:
+                return t
+            p = torch.zeros((t.numel() + 3) // 4 * 4, dtype=torch.float32, device=t.device)
+            p[:t.numel()] = t.reshape(-1)
+            return p
+        dT, dS = padded(dT), padded(dS)
     if out is None:
         out = torch.empty((batch, Mb, Nb), dtype=torch.float32, device=Tq.device)
     _check(lib.fm_block_products_scaled(_dptr(Tq), _dptr(Sq), _dptr(dT), _dptr(dS), batch, Mb, Nb,

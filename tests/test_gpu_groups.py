@@ -1,0 +1,183 @@
+"""GPU parity of the group-scale granularity (App. B.1, the models' schedule:
+1 x 128 scales on A's block sums, bf16 rounding then 128 x 128 scales on B's,
+products returned in bf16) through the C ABI, against the CPU oracle on the
+same seeded inputs.
+
+Bars: FP8 codes and every group scale bit-exact.  Block products: each
+within one bf16 step of the oracle's and different from it in at most 1% of
+positions.  The products' last fp32 bits depend on the order of the fp32
+sums over a group (the oracle rounds the exact sum once), and a bf16
+rounding flips when the fp32 value lies that close to a rounding midpoint,
+about once per 1e3 positions; one flip is 2^-8 relative, so the products and
+C stay within 5e-4 relative Frobenius of the oracle's.  Orbit errors within
+1% of the oracle's.  Structural pins (App. C.3's row map, Sec. 4.2's 48 of
+496 pairs) hold exactly on the device.
+"""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import scheme_ops as so
+from oracle import schemes as osch
+import synthetic as sy
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU-only machines, never run
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2609_39816_amd import fm  # noqa: E402
+
+DEV = torch.device("cuda:0")
+SG_H, SG_O = fm.SCALE_GROUP, oracle.SCALE_GROUP
+FMT = {"e4m3": (fm.E4M3, oracle.E4M3), "e5m2": (fm.E5M2, oracle.E5M2)}
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_values.json")))
+TOL = 5e-4
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    nb = np.linalg.norm(b)
+    return np.linalg.norm(a - b) / (nb if nb > 0 else 1.0)
+
+
+def gpu(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def bits(x):
+    return np.ascontiguousarray(x, np.float32).view(np.uint32)
+
+
+def within_one_bf16_step(got, want):
+    """|got - want| at most one bf16 spacing of want, and few positions differ."""
+    got = np.asarray(got, np.float32)
+    want = np.asarray(want, np.float32)
+    step = np.ldexp(1.0, np.frexp(np.abs(want).astype(np.float64))[1] - 8)
+    diff = np.abs(got.astype(np.float64) - want)
+    assert np.all(diff <= step + 1e-30), float(np.max(diff / (step + 1e-30)))
+    return float(np.mean(got != want))
+
+
+CASES = [
+    # name, base scheme, levels, gauge kind, M, K, N, fmt
+    ("strassen1_gl", "strassen", 1, "gl", 256, 256, 256, "e4m3"),
+    ("strassen2_sign_two_groups", "strassen", 2, "sign", 256, 1024, 512, "e4m3"),
+    ("strassen2_sign_ragged_rows", "strassen", 2, "sign", 208, 512, 512, "e4m3"),
+    ("laderman_gl_e5m2", "laderman", 1, "gl", 192, 768, 384, "e5m2"),
+    ("classical_four_groups", "classical", 1, "gl", 136, 512, 256, "e4m3"),
+]
+
+
+def gauges_for(base, levels, kind, count, seed):
+    if base == "classical":
+        return [(np.eye(1), np.eye(1), np.eye(1))]
+    if kind == "gl":
+        m = {"strassen": 2, "laderman": 3}[base]
+        return sy.gl_gauges(m, m, m, count, seed=seed)
+    g = 2 ** levels
+    sv = sy.sample_sign_orbit(g, g, g, count, seed=seed)
+    return [(np.diag(d), np.diag(e), np.diag(f)) for d, e, f in sv]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_group_scale_parity(case):
+    name, base, levels, kind, M, K, N, fmt = case
+    fh, fo = FMT[fmt]
+    say(f"[groups] {name} {M}x{K}x{N} {fmt}")
+    rng = np.random.default_rng(sum(name.encode()))
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    A[:, rng.choice(K, 4, replace=False)] *= 50.0
+    B = (0.02 * rng.standard_normal((K, N))).astype(np.float32)
+    At, Bt = gpu(A), gpu(B)
+    gauges = gauges_for(base, levels, kind, 4, seed=17)
+    hb = fm.Scheme.base(base)
+    ob = osch.BASE_SCHEMES[base]()
+    if kind == "sign":
+        hflat = hb.kron(levels) if levels > 1 else hb
+        hips = [hflat.gauge(*g) for g in gauges]
+        orcs = [so.gauge(so.power(ob, levels), *g) for g in gauges]
+        lv = 1
+    else:
+        hips = [hb.gauge(*g) for g in gauges]
+        orcs = [so.power(so.gauge(ob, *g), levels) for g in gauges]
+        lv = levels
+    Cref = fm.reference_f64(At, Bt)
+    Cref_o = oracle.reference_f64(A, B)
+    errs = fm.orbit_eval(hips, At, Bt, Cref, lv, fh, scale_mode=SG_H)
+    for gi in sorted({0, len(hips) - 1}):
+        h, o = hips[gi], orcs[gi]
+        tabs, dims = oracle.flatten_f32(o)
+        gm, gk, gn, R = dims
+        Tq, Sq, dT, dS = fm.form_operands(h, At, Bt, lv, fh, scale_mode=SG_H)
+        tq, dt = oracle.form_operands(A, gm, gk, tabs[0], fo, scale_mode=SG_O, side=0)
+        sq, ds = oracle.form_operands(B, gk, gn, tabs[1], fo, scale_mode=SG_O, side=1)
+        assert np.array_equal(Tq.cpu().numpy(), tq), "Tq"
+        assert np.array_equal(Sq.cpu().numpy(), sq.transpose(0, 2, 1)), "Sq"
+        assert np.array_equal(bits(dT.cpu().numpy()), bits(dt)), "dT"
+        assert np.array_equal(bits(dS.cpu().numpy()), bits(ds)), "dS"
+        Mg = fm.block_products(Tq, Sq, dT, dS, fh, scale_mode=SG_H).cpu().numpy()
+        assert np.all(bits(Mg) & 0xffff == 0), "products are bf16 values"
+        for r in sorted({0, R - 1}):
+            Mo = oracle.block_product_groups(tq[r], sq[r], dt[r], ds[r], fo)
+            frac = within_one_bf16_step(Mg[r], Mo)
+            assert frac <= 1e-2, f"block product {r}: {frac:.2e} of positions differ"
+            assert rel(Mg[r], Mo) <= TOL
+        Co = oracle.lowp_matmul(A, B, tabs, dims, fo, scale_mode=SG_O)
+        Cg = fm.matmul_lowp(h, At, Bt, lv, fh, scale_mode=SG_H).cpu().numpy()
+        assert rel(Cg, Co) <= TOL, f"C: {rel(Cg, Co):.2e}"
+        want = oracle.rel_fro(Co, Cref_o)
+        assert abs(errs[gi] / want - 1) <= 1e-2, (gi, errs[gi], want)
+
+
+def changed_rows(C0, C1):
+    return [int(r) for r in np.nonzero(np.any(C0 != C1, axis=1))[0]]
+
+
+def test_row_map_and_prefix_pairs_on_the_device():
+    """App. C.3 and Sec. 4.2 under group scales on the device: replacing row 40
+    of 48 moves output rows 4, 16, 28, 40 only; 48 of 496 pairs move, exactly
+    those sharing a block offset."""
+    s2 = fm.Scheme.base("strassen")
+    rng = np.random.default_rng(40)
+    A = np.zeros((48, 512), np.float32)
+    A[:40] = rng.standard_normal((40, 512))
+    B = gpu(rng.standard_normal((512, 512)).astype(np.float32))
+    A1 = A.copy()
+    A1[39] = rng.standard_normal(512)
+    C0 = fm.matmul_lowp(s2, gpu(A), B, 2, scale_mode=SG_H).cpu().numpy()
+    C1 = fm.matmul_lowp(s2, gpu(A1), B, 2, scale_mode=SG_H).cpu().numpy()
+    assert [r + 1 for r in changed_rows(C0, C1)] == GOLD["rowmap_changed_rows_1based"]["value"]
+    rng = np.random.default_rng(32)
+    A = rng.standard_normal((32, 512)).astype(np.float32)
+    B = gpu(rng.standard_normal((512, 512)).astype(np.float32))
+    base = fm.matmul_lowp(s2, gpu(A), B, 2, scale_mode=SG_H).cpu().numpy()
+    rng2 = np.random.default_rng(33)
+    moved = set()
+    for j in range(1, 32):
+        A1 = A.copy()
+        A1[j] = rng2.standard_normal(512)
+        C1 = fm.matmul_lowp(s2, gpu(A1), B, 2, scale_mode=SG_H).cpu().numpy()
+        moved |= {(i, j) for i in range(j) if np.any(base[i] != C1[i])}
+    assert len(moved) == GOLD["prefix_pairs_moved_fp8"]["value"]
+    assert moved == {(i, j) for j in range(32) for i in range(j) if i % 8 == j % 8}
+
+
+def test_shapes_the_group_scales_cannot_take():
+    s = fm.Scheme.base("strassen")
+    A = gpu(np.ones((64, 192), np.float32))  # Kb = 96: not a multiple of 128
+    B = gpu(np.ones((192, 256), np.float32))
+    with pytest.raises(fm.FmError) as e:
+        fm.matmul_lowp(s, A, B, 1, scale_mode=SG_H, ws=fm.workspace(1 << 24))
+    assert e.value.name == "FM_E_SHAPE"
