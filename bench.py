@@ -100,7 +100,7 @@ def gemm_bytes(w, geo, G):
     return G * R * (Mb * Kb + Nb * Kb + 4.0 * Mb * Nb) + (w.M * w.K + w.N * w.K + 4.0 * w.M * w.N)
 
 
-def cpu_baseline(w, A, B, gauge):
+def cpu_baseline(w, A, B, gauge, scale_mode=0):
     """The oracle (plain C, OpenMP) on one gauge of the workload."""
     import oracle
     from oracle import scheme_ops as so
@@ -111,7 +111,7 @@ def cpu_baseline(w, A, B, gauge):
         so.power(so.gauge(base, *gauge), w.levels)
     tabs, dims = oracle.flatten_f32(s)
     t0 = time.perf_counter()
-    oracle.lowp_matmul(A, B, tabs, dims)
+    oracle.lowp_matmul(A, B, tabs, dims, scale_mode=scale_mode)
     t = time.perf_counter() - t0
     cores = oracle.default_threads()
     return dict(value=2.0 * w.M * w.N * w.K / t / 1e12, unit="TFLOP/s (classical-equivalent)",
@@ -203,6 +203,8 @@ def main():
     ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--chunk", type=int, default=32, help="gauges per launch batch")
     ap.add_argument("--fmt", default=None)
+    ap.add_argument("--scale-mode", default="tensor", choices=["tensor", "rowcol", "group"],
+                    help="scale granularity of the FP8 rounding of block sums")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="do not bracket kernels with events")
     ap.add_argument("--int8", action="store_true",
@@ -230,6 +232,8 @@ def main():
     w = sy.WORKLOADS[args.workload]
     fmt_name = args.fmt or w.fmts[0]
     fmt = fm.FMTS[fmt_name]
+    smode = {"tensor": fm.SCALE_TENSOR, "rowcol": fm.SCALE_ROWCOL, "group": fm.SCALE_GROUP}[
+        args.scale_mode]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     log(f"[bench] workload {w.name}: generating inputs")
@@ -249,8 +253,8 @@ def main():
     classical = fm.Scheme.base("classical")
     geo = flat.flat_dims(levels)
     chunk = min(args.chunk, G) if args.chunk > 0 else G
-    ws = fm.workspace(fm.workspace_size(flat, w.M, w.N, w.K, levels, G, chunk))
-    ws_cl = fm.workspace(fm.workspace_size(classical, w.M, w.N, w.K, 1, 1, 1))
+    ws = fm.workspace(fm.workspace_size(flat, w.M, w.N, w.K, levels, G, chunk, smode))
+    ws_cl = fm.workspace(fm.workspace_size(classical, w.M, w.N, w.K, 1, 1, 1, smode))
     ws_err = fm.workspace(fm.lib.fm_error_workspace_size(w.M, w.N))
     Cref = torch.empty((w.M, w.N), dtype=torch.float64, device=dev)
     C_cl = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
@@ -261,9 +265,9 @@ def main():
         # device work that needs no host preparation goes first, so the host
         # gauge action below overlaps it
         fm.reference_f64(At, Bt, out=Cref)
-        fm.matmul_lowp(classical, At, Bt, 1, fmt, ws=ws_cl, out=C_cl)
+        fm.matmul_lowp(classical, At, Bt, 1, fmt, ws=ws_cl, out=C_cl, scale_mode=smode)
         hips = (flat if w.gauge_kind == "sign" else base).gauge_orbit(gauges)
-        errs = fm.orbit_eval(hips, At, Bt, Cref, levels, fmt, ws=ws)
+        errs = fm.orbit_eval(hips, At, Bt, Cref, levels, fmt, ws=ws, scale_mode=smode)
         st = fm.error_stats(C_cl, Cref, ws=ws_err)
         return errs / st["rel_fro"], st["rel_fro"]
 
@@ -315,7 +319,9 @@ def main():
                              frac_of_fp8_peak=round(achieved / PEAK_FP8_TFLOPS, 4))
         else:
             achieved, peak = work / tot_s / 1e9, PEAK_HBM_GBS
-        traffic = profiled_traffic(dom, w.name, gemm_bytes(w, geo, G)) if dom == "block_gemm" else None
+        # the byte counters were taken for the per-tensor schedule only
+        traffic = (profiled_traffic(dom, w.name, gemm_bytes(w, geo, G))
+                   if dom == "block_gemm" and smode == fm.SCALE_TENSOR else None)
         roof = dict(bound=bound, kernel=dom, achieved=round(achieved, 2), peak=peak, unit=unit,
                     frac=round(achieved / peak, 4),
                     traffic=traffic["bytes_per_step"] if traffic else None,
@@ -345,7 +351,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "M": w.M, "K": w.K, "N": w.N, "scheme": w.scheme,
                    "levels": w.levels, "gauges": G, "gauge_kind": w.gauge_kind, "fmt": fmt_name,
-                   "chunk": chunk, "parallelism": "none (1 GPU)"},
+                   "chunk": chunk, "scale_mode": args.scale_mode, "parallelism": "none (1 GPU)"},
         "evals_per_s": round(G / t, 1),
         "pct_mfma_peak_classical_equiv": round(100 * value / PEAK_FP8_TFLOPS, 2),
         "pct_mfma_peak_actual": round(100 * mfma_flops / t / 1e12 / PEAK_FP8_TFLOPS, 2),
@@ -356,7 +362,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("[bench] oracle baseline on the host cores")
-        out["cpu_baseline"] = cpu_baseline(w, A, B, gauges[0])
+        out["cpu_baseline"] = cpu_baseline(w, A, B, gauges[0], smode)
     print(json.dumps(out), flush=True)
 
 
