@@ -88,6 +88,11 @@ def lib():
             "orc_block_product_groups": (None, [p, p, p, p, i, i, i, i, p]),
             "orc_block_product_groups_acc": (None, [p, p, p, p, i, i, i, i, i, p]),
             "orc_bf16_round": (f, [f]),
+            "orc_row_exponent": (i, [p, i]),
+            "orc_joint_round_position": (i, [p, p, p, p, i, i, i, p]),
+            "orc_repair_gram": (None, [p, p, i, i, i, p]),
+            "orc_lowp_matmul_repaired": (i, [p, p, i, i, i, i, i, i, i, p, p, p, i, i, p, p, p, p,
+                                             p, p, p]),
             "orc_int8_group_product_corrected": (None, [p, p, i, i, i, i, i, i, i, i, i, i, p, p,
                                                         p, p, p, p]),
             "orc_int8_fast_corrected": (i, [p, p, p, p, i, i, i, i, i, i, i, i, i, p, p, p, p,
@@ -339,6 +344,67 @@ def lowp_matmul(A, B, scheme_f32, dims, fmt: int = E4M3, keep: bool = False,
         raise ValueError("orc_lowp_matmul failed")
     if keep:
         return dict(C=C, Tq=Tq, dT=dT, Sq=Sq, dS=dS, Mr=Mr)
+    return C
+
+
+# --------------------------------------------------------------------------
+# Repairs (App. C, the repair rules) on the group-scale schedule
+# --------------------------------------------------------------------------
+REPAIR_ROWS, REPAIR_WEIGHTS = 1, 2
+REPAIR_SWEEPS = 12
+
+
+def row_exponents(A) -> np.ndarray:
+    """k_t with d_t = 2^k_t = 2^ceil(log2(max(RMS(row t), 1e-3)))."""
+    A = _f32(A)
+    return np.array([lib().orc_row_exponent(_ptr(A[t]), A.shape[1]) for t in range(A.shape[0])],
+                    np.int32)
+
+
+def repair_gram(U, W) -> np.ndarray:
+    """H_rs = <w_r, w_s> <u_r, u_s> (float64 inner products, one fp32 rounding)."""
+    U, W = _f32(U), _f32(W)
+    R = U.shape[0]
+    H = np.empty((R, R), np.float32)
+    lib().orc_repair_gram(_ptr(U), _ptr(W), R, U.shape[1], W.shape[1], _ptr(H))
+    return H
+
+
+def joint_round_position(s, q, d, H, fmt: int = E4M3, max_sweeps: int = REPAIR_SWEEPS):
+    """Joint rounding of one position: (codes (R,), sweeps made)."""
+    s, q, d, H = _f32(s), _f32(q), _f32(d), _f32(H)
+    R = s.size
+    codes = np.empty(R, np.uint8)
+    n = lib().orc_joint_round_position(_ptr(s), _ptr(q), _ptr(d), _ptr(H), R, fmt, max_sweeps,
+                                       _ptr(codes))
+    return codes, int(n)
+
+
+def lowp_matmul_repaired(A, B, scheme_f32, dims, fmt: int = E4M3, flags: int = 3,
+                         keep: bool = False):
+    """The group-scale schedule with repairs (flags: REPAIR_ROWS,
+    REPAIR_WEIGHTS).  Returns C, or with keep=True a dict with C, Tq, dT,
+    Sq, dS, Mr and the row exponents."""
+    U, V, W = (_f32(t) for t in scheme_f32)
+    gm, gk, gn, R = dims
+    A, B = _f32(A), _f32(B)
+    M, K = A.shape
+    N = B.shape[1]
+    br, bk, bc = M // gm, K // gk, N // gn
+    C = np.empty((M, N), np.float32)
+    Tq = np.empty((R, br, bk), np.uint8)
+    Sq = np.empty((R, bk, bc), np.uint8)
+    dT = np.empty((R, bk // GROUP, br), np.float32)
+    dS = np.empty((R, bk // GROUP, bc // GROUP), np.float32)
+    Mr = np.empty((R, br, bc), np.float32)
+    kx = np.empty(M, np.int32)
+    rc = lib().orc_lowp_matmul_repaired(_ptr(A), _ptr(B), M, N, K, gm, gk, gn, R, _ptr(U), _ptr(V),
+                                        _ptr(W), fmt, flags, _ptr(C), _ptr(Tq), _ptr(dT), _ptr(Sq),
+                                        _ptr(dS), _ptr(Mr), _ptr(kx))
+    if rc != 0:
+        raise ValueError("shape not supported by the group-scale schedule")
+    if keep:
+        return dict(C=C, Tq=Tq, dT=dT, Sq=Sq, dS=dS, Mr=Mr, rowexp=kx)
     return C
 
 

@@ -956,3 +956,263 @@ int orc_int8_fast_corrected(const int8_t* Ac, const float* dA, const int8_t* Bc,
   free(P);
   return 0;
 }
+
+/* ======================================================================== */
+/* Repairs (App. C, the repair rules), options of the group-scale schedule. */
+/* ======================================================================== */
+
+/* Exponent k of the outside row scale d_t = 2^k, k = ceil(log2(max(RMS(x_t), */
+/* 1e-3))), RMS over the full row.  The sum of squares is formed in float64   */
+/* in a fixed order: partial sums over the residues of the index mod 64, in   */
+/* ascending index, combined pairwise as v[l] + v[l ^ off] for off = 32, 16, */
+/* ..., 1; then m2 = sum / K (one float64 division).  k is the least integer */
+/* with 4^k >= m2 (so 2^k >= RMS), found exactly from m2's binary exponent,  */
+/* and at least -9 (2^-9 is the least power of two >= 1e-3).  A non-finite  */
+/* row gets k = 0.                                                           */
+int orc_row_exponent(const float* x, int K) {
+  double v[64];
+  for (int l = 0; l < 64; ++l) v[l] = 0.0;
+  for (int i = 0; i < K; ++i) v[i & 63] += (double)x[i] * (double)x[i];
+  for (int off = 32; off >= 1; off >>= 1) {
+    double w[64];
+    for (int l = 0; l < 64; ++l) w[l] = v[l] + v[l ^ off];
+    memcpy(v, w, sizeof v);
+  }
+  double m2 = v[0] / (double)K;
+  if (!isfinite(m2)) return 0;
+  if (m2 == 0.0) return -9;
+  int e;
+  double fr = frexp(m2, &e); /* m2 = fr 2^e, fr in [0.5, 1) */
+  int c = fr == 0.5 ? e - 1 : e; /* ceil(log2 m2) */
+  int k = c >= 0 ? (c + 1) / 2 : -((-c) / 2); /* ceil(c / 2) */
+  return k < -9 ? -9 : k;
+}
+
+/* Joint rounding of one position of B's block sums (the repair rules): for   */
+/* every product r, s[r] is the bf16 block-sum entry, q[r] and d[r] its       */
+/* block's scales.  The candidates are the two codes whose values bracket     */
+/* y = s q (one fp32 multiply) -- the nearest (the ordinary rounding) and its */
+/* neighbour on the other side of y (none when y is a code value, or beyond   */
+/* the largest finite one) -- valued fl(dec(code) d); the start is the one    */
+/* whose value is nearer s (fp32 distances fl(value - s); on equal distances  */
+/* the nearest-even code).  With e_r = fl(value - s[r]) and g = H e (g_r =    */
+/* fmaf over s ascending from +0), sweep r = 0..R-1:                          */
+/* delta = fl(alt value - current value), change = fl(fl(fl(2 delta) g_r) +  */
+/* fl(fl(delta delta) H_rr)); if change < 0 the alternative is taken,        */
+/* e_r = fl(new value - s[r]) and g_t = fmaf(H_tr, delta, g_t) for every t   */
+/* ascending.  Stop after a sweep with no change or after max_sweeps.        */
+/* Returns the number of sweeps made.                                         */
+static uint8_t code_step(uint8_t c, int up, int fmt) {
+  /* the neighbouring code one step larger (up) or smaller in magnitude,    */
+  /* 0xff when none (beyond the largest finite or below zero)              */
+  uint8_t mag = c & 0x7f, sign = c & 0x80;
+  uint8_t maxmag = (uint8_t)(fmt == ORC_E4M3 ? 0x7e : 0x7b);
+  if (up) return mag >= maxmag ? 0xff : (uint8_t)(sign | (mag + 1));
+  return mag == 0 ? 0xff : (uint8_t)(sign | (mag - 1));
+}
+
+int orc_joint_round_position(const float* s, const float* q, const float* d, const float* H,
+                             int R, int fmt, int max_sweeps, uint8_t* codes) {
+  uint8_t cur[512], alt[512];
+  float e[512], g[512], val[512], aval[512];
+  if (R > 512) return -1;
+  for (int r = 0; r < R; ++r) {
+    float y = s[r] * q[r];
+    uint8_t c = orc_fp8_encode(y, fmt);
+    double dv = orc_fp8_decode(c, fmt);
+    uint8_t a = 0xff;
+    if (dv != (double)y) {
+      /* the neighbour on the other side of y, in magnitude */
+      int away = fabs((double)y) > fabs(dv); /* y beyond the code: step up */
+      a = code_step(c, away, fmt);
+      if (a != 0xff && (c & 0x7f) == 0) a = (uint8_t)((y < 0 ? 0x80 : 0x00) | (a & 0x7f));
+    }
+    cur[r] = c;
+    alt[r] = a;
+    val[r] = (float)dv * d[r];
+    aval[r] = a == 0xff ? 0.0f : (float)orc_fp8_decode(a, fmt) * d[r];
+    e[r] = val[r] - s[r];
+    if (a != 0xff) {
+      /* start at the candidate whose value is nearer s (fp32 distances; on */
+      /* equal distances the nearest-even code)                            */
+      float ea = aval[r] - s[r];
+      if (fabsf(ea) < fabsf(e[r])) {
+        cur[r] = a;
+        alt[r] = c;
+        float tv = val[r];
+        val[r] = aval[r];
+        aval[r] = tv;
+        e[r] = ea;
+      }
+    }
+  }
+  for (int r = 0; r < R; ++r) {
+    float acc = 0.0f;
+    for (int t = 0; t < R; ++t) acc = fmaf(H[(int64_t)r * R + t], e[t], acc);
+    g[r] = acc;
+  }
+  int sweeps = 0;
+  for (int sw = 0; sw < max_sweeps; ++sw) {
+    ++sweeps;
+    int changed = 0;
+    for (int r = 0; r < R; ++r) {
+      if (alt[r] == 0xff) continue;
+      float delta = aval[r] - val[r];
+      float two = 2.0f * delta;
+      float lin = two * g[r];
+      float sq = delta * delta;
+      float quad = sq * H[(int64_t)r * R + r];
+      float change = lin + quad;
+      if (change < 0.0f) {
+        uint8_t tc = cur[r];
+        cur[r] = alt[r];
+        alt[r] = tc;
+        float tv = val[r];
+        val[r] = aval[r];
+        aval[r] = tv;
+        e[r] = val[r] - s[r];
+        for (int t = 0; t < R; ++t) g[t] = fmaf(H[(int64_t)t * R + r], delta, g[t]);
+        changed = 1;
+      }
+    }
+    if (!changed) break;
+  }
+  for (int r = 0; r < R; ++r) codes[r] = cur[r];
+  return sweeps;
+}
+
+/* H_rs = <w_r, w_s> <u_r, u_s> from the fp32 coefficient tables: each inner */
+/* product in float64 over ascending index, their product rounded once to   */
+/* fp32.  U is R x nu, W is R x nw.                                          */
+void orc_repair_gram(const float* U, const float* W, int R, int nu, int nw, float* H) {
+  for (int r = 0; r < R; ++r)
+    for (int t = 0; t < R; ++t) {
+      double uu = 0.0, ww = 0.0;
+      for (int i = 0; i < nu; ++i) uu += (double)U[(int64_t)r * nu + i] * U[(int64_t)t * nu + i];
+      for (int i = 0; i < nw; ++i) ww += (double)W[(int64_t)r * nw + i] * W[(int64_t)t * nw + i];
+      H[(int64_t)r * R + t] = (float)(ww * uu);
+    }
+}
+
+/* Scales of B's bf16 block sums in 128 x 128 blocks, as                   */
+/* orc_quantize_bf16_blocks computes them: q[kg * nzb + zb], d[...] .        */
+static void bf16_block_scales(const float* Tb, int rows, int cols, int fmt, float* q, float* d) {
+  int nkg = rows / ORC_GROUP, nzb = cols / ORC_GROUP;
+  for (int kg = 0; kg < nkg; ++kg)
+    for (int zb = 0; zb < nzb; ++zb) {
+      float amax = 0.0f;
+      for (int y = kg * ORC_GROUP; y < (kg + 1) * ORC_GROUP; ++y)
+        for (int z = zb * ORC_GROUP; z < (zb + 1) * ORC_GROUP; ++z) {
+          float a = fabsf(Tb[(int64_t)y * cols + z]);
+          if (a > amax) amax = a;
+        }
+      float r;
+      d[(int64_t)kg * nzb + zb] = scale_from_amax(amax, fmt, &r);
+      q[(int64_t)kg * nzb + zb] = r;
+    }
+}
+
+/* The group-scale schedule with repairs (flags: 1 = outside power-of-two   */
+/* row scaling of A, 2 = joint rounding of B's block sums, 12 sweeps at     */
+/* most).  Row scaling: A's row t is multiplied by 2^-k_t (exact) before    */
+/* the block sums and C's row t by 2^k_t after the reconstruction.  Joint   */
+/* rounding replaces the nearest-code rounding of B's bf16 block sums; the  */
+/* block scales are those of the ordinary schedule.  Outputs as             */
+/* orc_lowp_matmul_sm (mode 2), plus the row exponents (M ints) if asked.   */
+#define ORC_REPAIR_SWEEPS 12
+int orc_lowp_matmul_repaired(const float* A, const float* B, int M, int N, int K, int gm, int gk,
+                             int gn, int R, const float* U, const float* V, const float* W,
+                             int fmt, int flags, float* C, uint8_t* Tq_out, float* dT_out,
+                             uint8_t* Sq_out, float* dS_out, float* Mr_out, int* rowexp_out) {
+  if (M % gm || K % gk || N % gn) return -1;
+  int br = M / gm, bk = K / gk, bc = N / gn;
+  if (bk % ORC_GROUP || bc % ORC_GROUP) return -1;
+  int nkg = bk / ORC_GROUP, nzb = bc / ORC_GROUP;
+  int64_t nta = (int64_t)nkg * br, nsb = (int64_t)nkg * nzb;
+  int64_t tsz = (int64_t)br * bk, ssz = (int64_t)bk * bc, msz = (int64_t)br * bc;
+  /* row scaling */
+  int* kx = (int*)malloc(sizeof(int) * (size_t)M);
+  const float* Ause = A;
+  float* As = NULL;
+  for (int t = 0; t < M; ++t) kx[t] = (flags & 1) ? orc_row_exponent(A + (int64_t)t * K, K) : 0;
+  if (flags & 1) {
+    As = (float*)malloc(sizeof(float) * (size_t)M * K);
+    for (int t = 0; t < M; ++t) {
+      float f = ldexpf(1.0f, -kx[t]);
+      for (int i = 0; i < K; ++i) As[(int64_t)t * K + i] = A[(int64_t)t * K + i] * f;
+    }
+    Ause = As;
+  }
+  if (rowexp_out) memcpy(rowexp_out, kx, sizeof(int) * (size_t)M);
+  /* B side for every product first: joint rounding looks across r */
+  float* S = (float*)malloc(sizeof(float) * (size_t)ssz);
+  float* Sb = (float*)malloc(sizeof(float) * (size_t)(ssz * R));
+  float* qS = (float*)malloc(sizeof(float) * (size_t)(nsb * R));
+  float* dS = (float*)malloc(sizeof(float) * (size_t)(nsb * R));
+  uint8_t* sq = (uint8_t*)malloc((size_t)(ssz * R));
+  for (int r = 0; r < R; ++r) {
+    orc_block_sum(B, K, N, gk, gn, V + (int64_t)r * gk * gn, S);
+    for (int64_t i = 0; i < ssz; ++i) Sb[r * ssz + i] = orc_bf16_round(S[i]);
+    bf16_block_scales(Sb + r * ssz, bk, bc, fmt, qS + r * nsb, dS + r * nsb);
+    for (int y = 0; y < bk; ++y)
+      for (int z = 0; z < bc; ++z) {
+        int64_t blk = (int64_t)(y / ORC_GROUP) * nzb + z / ORC_GROUP;
+        sq[r * ssz + (int64_t)y * bc + z] =
+            orc_fp8_encode(Sb[r * ssz + (int64_t)y * bc + z] * qS[r * nsb + blk], fmt);
+      }
+  }
+  if (flags & 2) {
+    float* H = (float*)malloc(sizeof(float) * (size_t)R * R);
+    orc_repair_gram(U, W, R, gm * gk, gm * gn, H);
+    float* sv = (float*)malloc(sizeof(float) * (size_t)R * 3);
+    float *qv = sv + R, *dv = sv + 2 * R;
+    uint8_t* cv = (uint8_t*)malloc((size_t)R);
+    for (int y = 0; y < bk; ++y)
+      for (int z = 0; z < bc; ++z) {
+        int64_t pos = (int64_t)y * bc + z;
+        int64_t blk = (int64_t)(y / ORC_GROUP) * nzb + z / ORC_GROUP;
+        for (int r = 0; r < R; ++r) {
+          sv[r] = Sb[r * ssz + pos];
+          qv[r] = qS[r * nsb + blk];
+          dv[r] = dS[r * nsb + blk];
+        }
+        orc_joint_round_position(sv, qv, dv, H, R, fmt, ORC_REPAIR_SWEEPS, cv);
+        for (int r = 0; r < R; ++r) sq[r * ssz + pos] = cv[r];
+      }
+    free(H);
+    free(sv);
+    free(cv);
+  }
+  /* A side, products, reconstruction */
+  float* T = (float*)malloc(sizeof(float) * (size_t)tsz);
+  uint8_t* tq = (uint8_t*)malloc((size_t)tsz);
+  float* dT = (float*)malloc(sizeof(float) * (size_t)nta);
+  float* Mr = Mr_out ? Mr_out : (float*)malloc(sizeof(float) * (size_t)(msz * R));
+  for (int r = 0; r < R; ++r) {
+    orc_block_sum(Ause, M, K, gm, gk, U + (int64_t)r * gm * gk, T);
+    orc_quantize_row_groups(T, br, bk, fmt, tq, dT);
+    if (Tq_out) memcpy(Tq_out + r * tsz, tq, (size_t)tsz);
+    if (dT_out) memcpy(dT_out + (int64_t)r * nta, dT, sizeof(float) * (size_t)nta);
+    orc_block_product_groups(tq, sq + r * ssz, dT, dS + r * nsb, br, bc, bk, fmt, Mr + r * msz);
+  }
+  if (Sq_out) memcpy(Sq_out, sq, (size_t)(ssz * R));
+  if (dS_out) memcpy(dS_out, dS, sizeof(float) * (size_t)(nsb * R));
+  orc_reconstruct(Mr, W, R, gm, gn, br, bc, C);
+  if (flags & 1)
+    for (int t = 0; t < M; ++t) {
+      float f = ldexpf(1.0f, kx[t]);
+      for (int j = 0; j < N; ++j) C[(int64_t)t * N + j] = C[(int64_t)t * N + j] * f;
+    }
+  if (!Mr_out) free(Mr);
+  free(T);
+  free(tq);
+  free(dT);
+  free(S);
+  free(Sb);
+  free(qS);
+  free(dS);
+  free(sq);
+  free(As);
+  free(kx);
+  return 0;
+}
