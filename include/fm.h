@@ -84,7 +84,33 @@ typedef enum { FM_ACC_BF16 = 0, FM_ACC_FP8 = 1 } fm_accum;
  *     first rounded to bf16, then get one scale per 128 x 128 block; block
  *     products are returned in bf16 (as fp32 values).  Scale arrays hold
  *     R x (Kb/128) x Mb (A) and R x (Kb/128) x (Nb/128) (B) per gauge. */
-typedef enum { FM_SCALE_TENSOR = 0, FM_SCALE_ROWCOL = 1, FM_SCALE_GROUP = 2 } fm_scale_mode;
+/* Repairs (App. C, the repair rules), OR-ed into the fm_scale_mode argument
+ * of the *_scaled calls (except fm_block_products_scaled), with
+ * FM_SCALE_GROUP only (FM_E_ARG otherwise):
+ *   FM_REPAIR_ROWS: every row t of A is divided by d_t = 2^k_t before the
+ *     block sums and the output row t multiplied by d_t afterwards, k_t the
+ *     least integer with 4^k_t >= m2_t and k_t >= -9, where m2_t is the
+ *     float64 mean of the squares of the row (partial sums over the indices
+ *     mod 64 in ascending order, combined pairwise as v[l] + v[l ^ off] for
+ *     off = 32, ..., 1, then divided by K): 2^k_t is the least power of two
+ *     at least max(RMS, 1e-3);
+ *   FM_REPAIR_WEIGHTS: the FP8 codes of B's bf16 block sums are chosen
+ *     jointly at every position: each product's two codes whose values
+ *     bracket s q (its block's scales q, d), starting at the value nearer s
+ *     (fp32 distances), then sweeps r = 0..R-1 taking the other code when
+ *     fl(fl(2 delta) g_r) + fl(fl(delta delta) H_rr) < 0, where e_r =
+ *     fl(fl(code value * d) - s), g = H e (fmaf, ascending), updated by
+ *     g_t = fmaf(H_tr, delta, g_t) on each change, and H_rs =
+ *     fl32(<w_r, w_s> <u_r, u_s>) in float64; at most 12 sweeps, stopping
+ *     after one with no change.  Built for R <= 64 (FM_E_UNSUPPORTED
+ *     otherwise). */
+typedef enum {
+  FM_SCALE_TENSOR = 0,
+  FM_SCALE_ROWCOL = 1,
+  FM_SCALE_GROUP = 2,
+  FM_REPAIR_ROWS = 0x100,
+  FM_REPAIR_WEIGHTS = 0x200
+} fm_scale_mode;
 
 typedef struct {
   double rel_fro; /* ||C - C_ref||_F / ||C_ref||_F (0 if C_ref = 0)         */

@@ -107,24 +107,31 @@ int chunk_pattern(const Tables& T, int side, int g0, int n) {
 // Workspace layout for G gauges processed `chunk` at a time.
 struct Layout {
   size_t flags, bt, off[3], idx[3], coef[3], amax, q, d, tq, sq, mprod, partial, errsq, out3,
-      total;
+      arow, rowup, qb, hg, total;
   int recon_nblk;
 };
+
+// Scale-mode word: the granularity in the low byte, repair flags above it
+// (FM_REPAIR_ROWS, FM_REPAIR_WEIGHTS; only with FM_SCALE_GROUP).
+int base_mode(int scale_mode) { return scale_mode & 0xff; }
+bool repair_rows(int scale_mode) { return (scale_mode & FM_REPAIR_ROWS) != 0; }
+bool repair_weights(int scale_mode) { return (scale_mode & FM_REPAIR_WEIGHTS) != 0; }
 
 // Scales per (gauge, product) on each side: 1, or one per block-sum row
 // (A side, Mb) and per block-sum column (B side, Nb), or per group: (Kb/128)
 // Mb on A's side and (Kb/128) (Nb/128) on B's.
 int scales_a(const Geometry& g, int scale_mode) {
-  return scale_mode == FM_SCALE_ROWCOL ? g.Mb : scale_mode == FM_SCALE_GROUP ? g.Kb / 128 * g.Mb : 1;
+  const int m = base_mode(scale_mode);
+  return m == FM_SCALE_ROWCOL ? g.Mb : m == FM_SCALE_GROUP ? g.Kb / 128 * g.Mb : 1;
 }
 int scales_b(const Geometry& g, int scale_mode) {
-  return scale_mode == FM_SCALE_ROWCOL ? g.Nb
-                                       : scale_mode == FM_SCALE_GROUP ? g.Kb / 128 * (g.Nb / 128) : 1;
+  const int m = base_mode(scale_mode);
+  return m == FM_SCALE_ROWCOL ? g.Nb : m == FM_SCALE_GROUP ? g.Kb / 128 * (g.Nb / 128) : 1;
 }
 // Block shapes a scale mode needs (group scales: Kb, Nb multiples of 128,
 // Mb of 4).
 int scale_shape_ok(int Mb, int Nb, int Kb, int scale_mode) {
-  if (scale_mode == FM_SCALE_GROUP && (Kb % 128 || Nb % 128 || Mb % 4))
+  if (base_mode(scale_mode) == FM_SCALE_GROUP && (Kb % 128 || Nb % 128 || Mb % 4))
     return fail(FM_E_SHAPE, "group scales need Kb, Nb multiples of 128 and Mb of 4");
   return FM_OK;
 }
@@ -165,8 +172,64 @@ Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
   L.partial = take((size_t)chunk * L.recon_nblk * 8);
   L.errsq = take((size_t)G * 8);
   L.out3 = take(3 * 8);
+  // repairs: A's rescaled rows and the row factors; B's block scales q and
+  // every gauge's H
+  L.arow = take(repair_rows(scale_mode) ? (size_t)g.M * g.K * 4 : 0);
+  L.rowup = take(repair_rows(scale_mode) ? (size_t)g.M * 4 : 0);
+  L.qb = take(repair_weights(scale_mode) ? (size_t)chunk * R * scales_b(g, scale_mode) * 4 : 0);
+  L.hg = take(repair_weights(scale_mode) ? (size_t)G * R * R * 4 : 0);
   L.total = o;
   return L;
+}
+
+// H_rs = <w_r, w_s> <u_r, u_s> for every gauge (the repair rules), from the
+// fp32 coefficient lists: each inner product in float64 over ascending block
+// index, their product rounded once to fp32.
+std::vector<float> repair_grams(const Tables& T, const Geometry& geo) {
+  const int R = T.R, nu = geo.NBa(), nw = geo.NC();
+  std::vector<float> H((size_t)T.G * R * R);
+  std::vector<double> u((size_t)R * nu), w((size_t)R * nw);
+  for (int g = 0; g < T.G; ++g) {
+    std::fill(u.begin(), u.end(), 0.0);
+    std::fill(w.begin(), w.end(), 0.0);
+    for (int k : {0, 2}) {
+      const Side& sd = T.s[k];
+      std::vector<double>& dst = k == 0 ? u : w;
+      const int n = k == 0 ? nu : nw;
+      for (int r = 0; r < R; ++r)
+        for (int e = sd.off[(size_t)g * (R + 1) + r]; e < sd.off[(size_t)g * (R + 1) + r + 1]; ++e)
+          dst[(size_t)r * n + sd.idx[e]] = sd.coef[e];
+    }
+    for (int r = 0; r < R; ++r)
+      for (int t = 0; t < R; ++t) {
+        double uu = 0.0, ww = 0.0;
+        for (int i = 0; i < nu; ++i) uu += u[(size_t)r * nu + i] * u[(size_t)t * nu + i];
+        for (int i = 0; i < nw; ++i) ww += w[(size_t)r * nw + i] * w[(size_t)t * nw + i];
+        H[((size_t)g * R + r) * R + t] = (float)(ww * uu);
+      }
+  }
+  return H;
+}
+
+// Repairs that act once per call: A's rows rescaled (returns the operand the
+// formation reads and the row factors) and every gauge's H uploaded.
+int prepare_repairs(const Geometry& geo, const Tables& T, char* ws, const Layout& L,
+                    int scale_mode, const float* A, const float*& Aform, const float*& rowup,
+                    hipStream_t st) {
+  Aform = A;
+  rowup = nullptr;
+  if (repair_rows(scale_mode)) {
+    float* As = (float*)(ws + L.arow);
+    float* up = (float*)(ws + L.rowup);
+    if (int rc = launch_row_repair(A, geo.M, geo.K, As, up, st)) return rc;
+    Aform = As;
+    rowup = up;
+  }
+  if (repair_weights(scale_mode)) {
+    const std::vector<float> H = repair_grams(T, geo);
+    if (int rc = upload(ws + L.hg, {{H.data(), H.size() * 4}}, {0}, H.size() * 4, st)) return rc;
+  }
+  return FM_OK;
 }
 
 int check_geometry(const fm_scheme* s, int levels, int M, int N, int K, Geometry& g) {
@@ -274,12 +337,20 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
               amax, q,     Tq,    fmt,    per_row};
   FormArgs fb{Bt, geo.N, geo.K, geo.gn, geo.gk, geo.Nb, geo.Kb, off(1), idx(1), coef(1), R, n,
               amax + na, q + na, Sq, fmt, per_row};
-  if (scale_mode == FM_SCALE_GROUP) {
+  if (base_mode(scale_mode) == FM_SCALE_GROUP) {
     // one pass per side: every group's maximum is local to its wave or workgroup
+    float* qb = repair_weights(scale_mode) ? (float*)(ws + L.qb) : nullptr;
     for (int side = 0; side < 2; ++side) {
       timing_begin(T_FORM_QUANT, st);
       if (int rc = launch_form_group(side ? fb : fa, side, side ? dd + na : dd,
-                                     (uint32_t*)(ws + L.flags), st))
+                                     (uint32_t*)(ws + L.flags), st, side ? qb : nullptr))
+        return rc;
+      timing_end(T_FORM_QUANT, st);
+    }
+    if (qb) {  // joint rounding of B's block sums replaces their nearest codes
+      timing_begin(T_FORM_QUANT, st);
+      if (int rc = launch_joint_round(fb, qb, dd + na,
+                                      (const float*)(ws + L.hg) + (size_t)g0 * R * R, st))
         return rc;
       timing_end(T_FORM_QUANT, st);
     }
@@ -658,7 +729,10 @@ int fm_scheme_coeffs_f32(const fm_scheme* s, int levels, float* U, float* V, flo
 void fm_scheme_free(fm_scheme* s) { delete s; }
 
 static int scale_mode_ok(int m) {
-  return m == FM_SCALE_TENSOR || m == FM_SCALE_ROWCOL || m == FM_SCALE_GROUP;
+  const int b = m & 0xff, flags = m & ~0xff;
+  if (b != FM_SCALE_TENSOR && b != FM_SCALE_ROWCOL && b != FM_SCALE_GROUP) return 0;
+  if (flags & ~(FM_REPAIR_ROWS | FM_REPAIR_WEIGHTS)) return 0;
+  return !flags || b == FM_SCALE_GROUP;  // the repairs belong to the group schedule
 }
 
 size_t fm_workspace_size_scaled(const fm_scheme* s, int M, int N, int K, int levels, int G,
@@ -703,7 +777,9 @@ int fm_form_operands_scaled(const fm_scheme* s, int levels, const float* A, cons
   if ((rc = upload_tables(T, ws, L, st))) return rc;
   float* Bt = (float*)(ws + L.bt);
   if ((rc = launch_transpose(B, Bt, K, N, st))) return rc;
-  return form_chunk(geo, A, Bt, ws, L, T, 0, 1, fmt, scale_mode, Tq, Sq, dT, dS, st);
+  const float *Aform, *rowup;
+  if ((rc = prepare_repairs(geo, T, ws, L, scale_mode, A, Aform, rowup, st))) return rc;
+  return form_chunk(geo, Aform, Bt, ws, L, T, 0, 1, fmt, scale_mode, Tq, Sq, dT, dS, st);
 }
 
 int fm_form_operands(const fm_scheme* s, int levels, const float* A, const float* B, int M, int N,
@@ -719,7 +795,8 @@ int fm_block_products_scaled(const uint8_t* Tq, const uint8_t* Sq, const float* 
   clear_error();
   if (!Tq || !Sq || !dT || !dS || !Mout) return fail(FM_E_ARG, "null pointer");
   if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
-  if (!scale_mode_ok(scale_mode)) return fail(FM_E_ARG, "bad scale mode");
+  if (!scale_mode_ok(scale_mode) || (scale_mode & ~0xff))
+    return fail(FM_E_ARG, "bad scale mode (the repairs act on the operands, not on the products)");
   if (batch < 1 || Mb < 1 || Nb < 1 || Kb < 1) return fail(FM_E_ARG, "sizes must be positive");
   if (Kb % 16) return fail(FM_E_SHAPE, "Kb must be a multiple of 16");
   return launch_block_gemm(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, scale_mode,
@@ -779,16 +856,20 @@ int fm_matmul_lowp_scaled(const fm_scheme* s, const float* A, const float* B, fl
   if ((rc = launch_transpose(B, Bt, K, N, st))) return rc;
   uint8_t* Tq = (uint8_t*)(ws + L.tq);
   uint8_t* Sq = (uint8_t*)(ws + L.sq);
-  if ((rc = form_chunk(geo, A, Bt, ws, L, T, 0, 1, fmt, scale_mode, Tq, Sq, nullptr, nullptr, st)))
+  const float *Aform, *rowup;
+  if ((rc = prepare_repairs(geo, T, ws, L, scale_mode, A, Aform, rowup, st))) return rc;
+  if ((rc = form_chunk(geo, Aform, Bt, ws, L, T, 0, 1, fmt, scale_mode, Tq, Sq, nullptr, nullptr,
+                       st)))
     return rc;
   const float* dd = (const float*)(ws + L.d);
   float* Mp = (float*)(ws + L.mprod);
   timing_begin(T_BLOCK_GEMM, st);
   if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)geo.R * scales_a(geo, scale_mode), Mp,
-                              geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, scale_mode, st)))
+                              geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, base_mode(scale_mode), st)))
     return rc;
   timing_end(T_BLOCK_GEMM, st);
-  const ReconArgs ra = recon_args(geo, ws, L, 0, 1, Mp, C, nullptr);
+  ReconArgs ra = recon_args(geo, ws, L, 0, 1, Mp, C, nullptr);
+  ra.rowscale = rowup;
   return launch_recon(ra, chunk_pattern(T, 2, 0, 1), st);
 }
 
@@ -867,17 +948,21 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   float* Mp = (float*)(ws + L.mprod);
   const float* dd = (const float*)(ws + L.d);
   double* errsq = (double*)(ws + L.errsq);
+  const float *Aform, *rowup;
+  if ((rc = prepare_repairs(geo, T, ws, L, scale_mode, A, Aform, rowup, st))) return rc;
   for (int g0 = 0; g0 < G; g0 += chunk) {
     const int n = std::min(chunk, G - g0);
-    if ((rc = form_chunk(geo, A, Bt, ws, L, T, g0, n, fmt, scale_mode, Tq, Sq, nullptr, nullptr,
-                         st)))
+    if ((rc = form_chunk(geo, Aform, Bt, ws, L, T, g0, n, fmt, scale_mode, Tq, Sq, nullptr,
+                         nullptr, st)))
       return rc;
     timing_begin(T_BLOCK_GEMM, st);
     if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)n * geo.R * scales_a(geo, scale_mode), Mp,
-                                n * geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, scale_mode, st)))
+                                n * geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, base_mode(scale_mode),
+                                st)))
       return rc;
     timing_end(T_BLOCK_GEMM, st);
-    const ReconArgs ra = recon_args(geo, ws, L, g0, n, Mp, nullptr, C_ref);
+    ReconArgs ra = recon_args(geo, ws, L, g0, n, Mp, nullptr, C_ref);
+    ra.rowscale = rowup;
     const int nblk = recon_blocks(ra);
     timing_begin(T_RECON, st);
     if ((rc = launch_recon(ra, chunk_pattern(T, 2, g0, n), st))) return rc;

@@ -450,14 +450,18 @@ __device__ __forceinline__ void recon_emit(const ReconArgs& a, int c, int x, int
                                            const float (&acc)[VW], double& esq) {
   const int i = c / a.gn, j = c - (c / a.gn) * a.gn;
   const size_t o = (size_t)(i * a.Mb + x) * a.N + (size_t)j * a.Nb + z0;
+  float out[VW];
+  const float f = a.rowscale ? a.rowscale[i * a.Mb + x] : 1.0f;
+#pragma unroll
+  for (int v = 0; v < VW; ++v) out[v] = a.rowscale ? acc[v] * f : acc[v];
   if (a.C) {
 #pragma unroll
-    for (int v = 0; v < VW; ++v) a.C[o + v] = acc[v];
+    for (int v = 0; v < VW; ++v) a.C[o + v] = out[v];
   }
   if (a.Cref) {
 #pragma unroll
     for (int v = 0; v < VW; ++v) {
-      const double dlt = (double)acc[v] - a.Cref[o + v];
+      const double dlt = (double)out[v] - a.Cref[o + v];
       esq = __fma_rn(dlt, dlt, esq);
     }
   }

@@ -119,7 +119,14 @@ int launch_form(const FormArgs& a, int mode, int pattern, int side, hipStream_t 
 // Group scales in one pass (side 0: 1 x 128 groups of A's block sums; side
 // 1: 128 x 128 blocks of B's bf16-rounded block sums): codes into a.codes,
 // scales d[(g R + r) (Kb/128) + kg][x] or [..][zb]; non-finite sets *flag |= 1.
-int launch_form_group(const FormArgs& a, int side, float* d, uint32_t* flag, hipStream_t st);
+int launch_form_group(const FormArgs& a, int side, float* d, uint32_t* flag, hipStream_t st,
+                      float* qout = nullptr);
+// Repairs: row exponents of A (As = A 2^-k row by row, up = 2^k), and the
+// joint rounding of B's bf16 block sums (a is B's FormArgs; codes into
+// a.codes; qS, dS the block scales from launch_form_group; H G x R x R).
+int launch_row_repair(const float* A, int M, int K, float* As, float* up, hipStream_t st);
+int launch_joint_round(const FormArgs& a, const float* qS, const float* dS, const float* H,
+                       hipStream_t st);
 
 // Scales from amax: for i < n: q[i] = FMAX/amax, d[i] = amax/FMAX (1, 1 for
 // amax = 0); a non-finite amax sets *flag |= 1.
@@ -148,6 +155,7 @@ struct ReconArgs {
   float* C;            // optional
   const double* Cref;  // optional
   double* partial;     // G x nblk (if Cref)
+  const float* rowscale = nullptr;  // optional: output row i*Mb + x times rowscale[i*Mb + x]
 };
 // Positions per thread in the reconstruction kernels (4 or 1) and the
 // number of workgroups per gauge (one position group per thread).

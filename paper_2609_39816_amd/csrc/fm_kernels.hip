@@ -71,6 +71,7 @@ __global__ __launch_bounds__(256) void transpose_kernel(const float* __restrict_
 // block sums are formed, scaled and encoded in a single pass.  Scales use the
 // tensor rule (q = FMAX / amax, d = amax / FMAX, both 1 for amax = 0).
 constexpr int kGroup = 128;
+constexpr int kRepairSweeps = 12;  // the repair rules' bound on the sweeps
 
 __device__ __forceinline__ float bf16_rne(float x) {
   // nearest bf16, ties to even (finite inputs; non-finite values are flagged)
@@ -130,7 +131,8 @@ __global__ __launch_bounds__(kThreads) void form_rowgroup_kernel(FormArgs a, flo
 // of product r of gauge g; thread t forms row t / 2, entries 64 (t & 1) ..
 // + 63, rounded to bf16.  grid (nzb * nkg, R, G).
 __global__ __launch_bounds__(kThreads) void form_bf16block_kernel(FormArgs a, float* __restrict__ d,
-                                                                  uint32_t* flag, float fmax) {
+                                                                  uint32_t* flag, float fmax,
+                                                                  float* __restrict__ qout) {
   __shared__ uint32_t wmax[kThreads / 64];
   const int nkg = a.bc / kGroup, nzb = a.br / kGroup;
   const int zb = blockIdx.x / nkg, kg = blockIdx.x - (blockIdx.x / nkg) * nkg;
@@ -181,7 +183,166 @@ __global__ __launch_bounds__(kThreads) void form_bf16block_kernel(FormArgs a, fl
       64 * half);
 #pragma unroll
   for (int i = 0; i < 4; ++i) dst[i] = make_uint4(w32[4 * i], w32[4 * i + 1], w32[4 * i + 2], w32[4 * i + 3]);
-  if (threadIdx.x == 0) d[((size_t)((size_t)g * a.R + r) * nkg + kg) * nzb + zb] = dv;
+  if (threadIdx.x == 0) {
+    d[((size_t)((size_t)g * a.R + r) * nkg + kg) * nzb + zb] = dv;
+    if (qout) qout[((size_t)((size_t)g * a.R + r) * nkg + kg) * nzb + zb] = qv;
+  }
+}
+
+// ------------------------------------------------------------- repairs
+// Outside power-of-two row scaling (the repair rules): one wave per row t of
+// A computes the float64 sum of squares (lane l over the indices = l mod 64
+// in ascending order, then the fixed butterfly), m2 = sum / K, the least k
+// with 4^k >= m2 (at least -9; a non-finite row gets 0), writes
+// As[t] = A[t] * 2^-k and up[t] = 2^k.
+__global__ __launch_bounds__(kThreads) void row_repair_kernel(const float* __restrict__ A, int M,
+                                                              int K, float* __restrict__ As,
+                                                              float* __restrict__ up) {
+  const int lane = threadIdx.x & 63;
+  const long long t = (long long)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (t >= M) return;
+  const float* x = A + (size_t)t * K;
+  double s = 0.0;
+  for (int i = lane; i < K; i += 64) s += (double)x[i] * (double)x[i];
+  for (int off = 32; off > 0; off >>= 1) s = s + __shfl_xor(s, off, 64);
+  const double m2 = s / (double)K;
+  int k;
+  if (!isfinite(m2)) {
+    k = 0;
+  } else if (m2 == 0.0) {
+    k = -9;
+  } else {
+    int e;
+    const double fr = frexp(m2, &e);
+    const int c = fr == 0.5 ? e - 1 : e;
+    k = c >= 0 ? (c + 1) / 2 : -((-c) / 2);
+    k = k < -9 ? -9 : k;
+  }
+  const float down = ldexpf(1.0f, -k);
+  float* y = As + (size_t)t * K;
+  for (int i = lane; i < K; i += 64) y[i] = x[i] * down;
+  if (lane == 0) up[t] = ldexpf(1.0f, k);
+}
+
+// Joint rounding of B's bf16 block sums (the repair rules), one thread per
+// position (z, k) of the block sums (B^T orientation) of gauge g: every
+// product's block sum there (the formation's fmaf order, then bf16), the
+// two codes bracketing s q, the start at the value-nearer one, then sweeps
+// over r with the fp32 decisions of the definition; writes all R codes.  A
+// workgroup (one wave) covers 64 consecutive k of one row z, inside one
+// 128 x 128 block.  LDS: the gauge's H, the block's scales q and d per
+// product, and per thread (column `lane` of R x 64 arrays) its block sums,
+// errors, H e and the candidate codes.
+__device__ __forceinline__ float fp8_value(uint32_t code, int fmt) {
+  return fmt == FM_E4M3 ? __builtin_amdgcn_cvt_f32_fp8((int)code, 0)
+                        : __builtin_amdgcn_cvt_f32_bf8((int)code, 0);
+}
+
+__device__ __forceinline__ uint32_t fp8_neighbour(uint32_t c, bool up, int fmt) {
+  // one step larger (up) or smaller in magnitude; 0x100 when there is none
+  const uint32_t mag = c & 0x7fu, sign = c & 0x80u;
+  const uint32_t maxmag = fmt == FM_E4M3 ? 0x7eu : 0x7bu;
+  if (up) return mag >= maxmag ? 0x100u : (sign | (mag + 1u));
+  return mag == 0u ? 0x100u : (sign | (mag - 1u));
+}
+
+constexpr int kJointLanes = 64;
+constexpr int kJointMaxR = 64;
+
+__global__ __launch_bounds__(kJointLanes) void joint_round_kernel(FormArgs a,
+                                                                  const float* __restrict__ qS,
+                                                                  const float* __restrict__ dS,
+                                                                  const float* __restrict__ Hg,
+                                                                  int max_sweeps) {
+  extern __shared__ float sm[];
+  const int R = a.R;
+  float* H = sm;                          // R x R
+  float* qs = H + R * R;                  // R
+  float* dsc = qs + R;                    // R
+  float* sv = dsc + R;                    // R x 64
+  float* ev = sv + R * kJointLanes;       // R x 64
+  float* gv = ev + R * kJointLanes;       // R x 64
+  uint32_t* pk = reinterpret_cast<uint32_t*>(gv + R * kJointLanes);  // R x 64
+  const int lane = threadIdx.x;
+  const int nkg = a.bc / kGroup, nzb = a.br / kGroup;
+  const int per_row = a.bc / kJointLanes;
+  const int z = blockIdx.x / per_row, k = (blockIdx.x - z * per_row) * kJointLanes + lane;
+  const int kg = k / kGroup, zb = z / kGroup;
+  const int g = blockIdx.y;
+  for (int i = lane; i < R * R; i += kJointLanes) H[i] = Hg[(size_t)g * R * R + i];
+  for (int r = lane; r < R; r += kJointLanes) {
+    const size_t o = ((size_t)((size_t)g * a.R + r) * nkg + kg) * nzb + zb;
+    qs[r] = qS[o];
+    dsc[r] = dS[o];
+  }
+  __syncthreads();
+  const auto off = ro(a.off);
+  // pk: bits 0-7 the nearest code, 8-15 its neighbour (bit 16: none),
+  // bit 17: the neighbour is the current choice
+  for (int r = 0; r < R; ++r) {
+    const int e0 = off[(size_t)g * (a.R + 1) + r], e1 = off[(size_t)g * (a.R + 1) + r + 1];
+    float acc = 0.0f;
+    for (int i = e0; i < e1; ++i) {
+      const float c = ro(a.coef)[i];
+      const int b = ro(a.idx)[i];
+      const int p = b / a.gc, qb = b - (b / a.gc) * a.gc;
+      acc = __builtin_fmaf(c, a.X[(size_t)(p * a.br + z) * a.cols + (size_t)qb * a.bc + k], acc);
+    }
+    const float s = bf16_rne(acc);
+    const float y = s * qs[r];
+    const uint32_t c0 = enc2d(y, 0.0f, a.fmt) & 0xffu;
+    const float v0 = fp8_value(c0, a.fmt);
+    uint32_t c1 = 0x100u;
+    if (v0 != y) c1 = fp8_neighbour(c0, fabsf(y) > fabsf(v0), a.fmt);
+    float er = v0 * dsc[r] - s;
+    uint32_t word = c0 | (c1 << 8);
+    if (c1 != 0x100u) {
+      const float ea = fp8_value(c1, a.fmt) * dsc[r] - s;
+      if (fabsf(ea) < fabsf(er)) {
+        er = ea;
+        word |= 1u << 17;
+      }
+    }
+    sv[r * kJointLanes + lane] = s;
+    ev[r * kJointLanes + lane] = er;
+    pk[r * kJointLanes + lane] = word;
+  }
+  for (int r = 0; r < R; ++r) {
+    float acc = 0.0f;
+    for (int t = 0; t < R; ++t) acc = __builtin_fmaf(H[r * R + t], ev[t * kJointLanes + lane], acc);
+    gv[r * kJointLanes + lane] = acc;
+  }
+  for (int sw = 0; sw < max_sweeps; ++sw) {
+    bool changed = false;
+    for (int r = 0; r < R; ++r) {
+      const uint32_t word = pk[r * kJointLanes + lane];
+      if (word & (1u << 16)) continue;  // no second candidate
+      const bool on_alt = (word >> 17) & 1u;
+      const uint32_t ccur = on_alt ? (word >> 8) & 0xffu : word & 0xffu;
+      const uint32_t calt = on_alt ? word & 0xffu : (word >> 8) & 0xffu;
+      const float vcur = fp8_value(ccur, a.fmt) * dsc[r];
+      const float valt = fp8_value(calt, a.fmt) * dsc[r];
+      const float delta = valt - vcur;
+      const float two = 2.0f * delta;
+      const float lin = two * gv[r * kJointLanes + lane];
+      const float sq = delta * delta;
+      const float quad = sq * H[r * R + r];
+      const float change = lin + quad;
+      if (change < 0.0f) {
+        pk[r * kJointLanes + lane] = word ^ (1u << 17);
+        for (int t = 0; t < R; ++t)
+          gv[t * kJointLanes + lane] =
+              __builtin_fmaf(H[t * R + r], delta, gv[t * kJointLanes + lane]);
+        changed = true;
+      }
+    }
+    if (!__builtin_amdgcn_ballot_w64(changed)) break;
+  }
+  for (int r = 0; r < R; ++r) {
+    const uint32_t word = pk[r * kJointLanes + lane];
+    const uint32_t c = ((word >> 17) & 1u) ? (word >> 8) & 0xffu : word & 0xffu;
+    a.codes[((size_t)((size_t)g * a.R + r) * a.br + z) * a.bc + k] = (uint8_t)c;
+  }
 }
 
 // --------------------------------------------------------------- scales
@@ -423,7 +584,8 @@ int launch_fp8_encode(const float* x, uint8_t* out, size_t n, int fmt, int impl,
   return launched("fp8_encode_kernel");
 }
 
-int launch_form_group(const FormArgs& a, int side, float* d, uint32_t* flag, hipStream_t st) {
+int launch_form_group(const FormArgs& a, int side, float* d, uint32_t* flag, hipStream_t st,
+                      float* qout) {
   if (a.bc % kGroup || (side == 1 && a.br % kGroup))
     return fail(FM_E_SHAPE, "group scales need inner blocks (and B's blocks) of multiples of 128");
   if (a.R > 65535 || a.G > 65535) return fail(FM_E_SHAPE, "too many products or gauges");
@@ -438,8 +600,34 @@ int launch_form_group(const FormArgs& a, int side, float* d, uint32_t* flag, hip
   }
   const long long blocks = (long long)(a.br / kGroup) * nkg;
   if (blocks > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many groups");
-  form_bf16block_kernel<<<dim3((unsigned)blocks, a.R, a.G), kThreads, 0, st>>>(a, d, flag, fmax);
+  form_bf16block_kernel<<<dim3((unsigned)blocks, a.R, a.G), kThreads, 0, st>>>(a, d, flag, fmax,
+                                                                              qout);
   return launched("form_bf16block_kernel");
+}
+
+int launch_row_repair(const float* A, int M, int K, float* As, float* up, hipStream_t st) {
+  const long long blocks = ((long long)M + kThreads / 64 - 1) / (kThreads / 64);
+  if (M < 1 || K < 1 || blocks > 0x7fffffffLL) return fail(FM_E_SHAPE, "row repair shape");
+  row_repair_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(A, M, K, As, up);
+  return launched("row_repair_kernel");
+}
+
+int launch_joint_round(const FormArgs& a, const float* qS, const float* dS, const float* H,
+                       hipStream_t st) {
+  if (a.bc % kGroup || a.br % kGroup) return fail(FM_E_SHAPE, "joint rounding needs 128 x 128 blocks");
+  if (a.R > kJointMaxR)
+    return fail(FM_E_UNSUPPORTED, "joint rounding is built for at most 64 products");
+  if (a.G > 65535) return fail(FM_E_SHAPE, "too many gauges");
+  const long long blocks = (long long)a.br * (a.bc / kJointLanes);
+  if (blocks > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many positions");
+  const size_t shm = ((size_t)a.R * a.R + 2 * a.R + 4 * (size_t)a.R * kJointLanes) * 4;
+  if (int rc = hip_check(hipFuncSetAttribute(reinterpret_cast<const void*>(&joint_round_kernel),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm),
+                         "hipFuncSetAttribute"))
+    return rc;
+  joint_round_kernel<<<dim3((unsigned)blocks, a.G), kJointLanes, shm, st>>>(a, qS, dS, H,
+                                                                           kRepairSweeps);
+  return launched("joint_round_kernel");
 }
 
 }  // namespace fm

@@ -26,6 +26,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "fm.h")
 E4M3, E5M2 = 0, 1
 ACC_BF16, ACC_FP8 = 0, 1
 SCALE_TENSOR, SCALE_ROWCOL, SCALE_GROUP = 0, 1, 2  # fm_scale_mode
+REPAIR_ROWS, REPAIR_WEIGHTS = 0x100, 0x200  # OR-ed into SCALE_GROUP
 FMTS = {"e4m3": E4M3, "e5m2": E5M2}
 ERRORS = {0: "FM_OK", -1: "FM_E_ARG", -2: "FM_E_SHAPE", -3: "FM_E_BRENT", -4: "FM_E_SINGULAR",
           -5: "FM_E_NONFINITE", -6: "FM_E_WORKSPACE", -7: "FM_E_HIP", -8: "FM_E_MISMATCH",
@@ -247,7 +248,7 @@ def form_operands(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, st
     Sq = torch.empty((R, Nb, K // gk), dtype=torch.uint8, device=A.device)
     Kb = K // gk
     shp = {SCALE_ROWCOL: ((R, Mb), (R, Nb)),
-           SCALE_GROUP: ((R, Kb // 128, Mb), (R, Kb // 128, Nb // 128))}.get(scale_mode,
+           SCALE_GROUP: ((R, Kb // 128, Mb), (R, Kb // 128, Nb // 128))}.get(scale_mode & 0xff,
                                                                            ((R,), (R,)))
     dT = torch.empty(shp[0], dtype=torch.float32, device=A.device)
     dS = torch.empty(shp[1], dtype=torch.float32, device=A.device)
