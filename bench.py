@@ -111,7 +111,10 @@ def cpu_baseline(w, A, B, gauge, scale_mode=0):
         so.power(so.gauge(base, *gauge), w.levels)
     tabs, dims = oracle.flatten_f32(s)
     t0 = time.perf_counter()
-    oracle.lowp_matmul(A, B, tabs, dims, scale_mode=scale_mode)
+    if scale_mode & ~0xff:  # the repairs (group schedule)
+        oracle.lowp_matmul_repaired(A, B, tabs, dims, flags=(scale_mode >> 8) & 3)
+    else:
+        oracle.lowp_matmul(A, B, tabs, dims, scale_mode=scale_mode)
     t = time.perf_counter() - t0
     cores = oracle.default_threads()
     return dict(value=2.0 * w.M * w.N * w.K / t / 1e12, unit="TFLOP/s (classical-equivalent)",
@@ -205,6 +208,8 @@ def main():
     ap.add_argument("--fmt", default=None)
     ap.add_argument("--scale-mode", default="tensor", choices=["tensor", "rowcol", "group"],
                     help="scale granularity of the FP8 rounding of block sums")
+    ap.add_argument("--repair", default="none", choices=["none", "rows", "weights", "both"],
+                    help="repairs of the group schedule (with --scale-mode group)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="do not bracket kernels with events")
     ap.add_argument("--int8", action="store_true",
@@ -234,6 +239,11 @@ def main():
     fmt = fm.FMTS[fmt_name]
     smode = {"tensor": fm.SCALE_TENSOR, "rowcol": fm.SCALE_ROWCOL, "group": fm.SCALE_GROUP}[
         args.scale_mode]
+    if args.repair != "none":
+        if smode != fm.SCALE_GROUP:
+            sys.exit("the repairs belong to the group schedule: add --scale-mode group")
+        smode |= {"rows": fm.REPAIR_ROWS, "weights": fm.REPAIR_WEIGHTS,
+                  "both": fm.REPAIR_ROWS | fm.REPAIR_WEIGHTS}[args.repair]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     log(f"[bench] workload {w.name}: generating inputs")
@@ -351,7 +361,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "M": w.M, "K": w.K, "N": w.N, "scheme": w.scheme,
                    "levels": w.levels, "gauges": G, "gauge_kind": w.gauge_kind, "fmt": fmt_name,
-                   "chunk": chunk, "scale_mode": args.scale_mode, "parallelism": "none (1 GPU)"},
+                   "chunk": chunk, "scale_mode": args.scale_mode, "repair": args.repair,
+                   "parallelism": "none (1 GPU)"},
         "evals_per_s": round(G / t, 1),
         "pct_mfma_peak_classical_equiv": round(100 * value / PEAK_FP8_TFLOPS, 2),
         "pct_mfma_peak_actual": round(100 * mfma_flops / t / 1e12 / PEAK_FP8_TFLOPS, 2),
