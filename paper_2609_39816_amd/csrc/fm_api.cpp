@@ -107,7 +107,7 @@ int chunk_pattern(const Tables& T, int side, int g0, int n) {
 // Workspace layout for G gauges processed `chunk` at a time.
 struct Layout {
   size_t flags, bt, off[3], idx[3], coef[3], amax, q, d, tq, sq, mprod, partial, errsq, out3,
-      arow, rowup, qb, hg, total;
+      arow, rowup, hg, total;
   int recon_nblk;
 };
 
@@ -172,11 +172,9 @@ Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
   L.partial = take((size_t)chunk * L.recon_nblk * 8);
   L.errsq = take((size_t)G * 8);
   L.out3 = take(3 * 8);
-  // repairs: A's rescaled rows and the row factors; B's block scales q and
-  // every gauge's H
+  // repairs: A's rescaled rows and the row factors; every gauge's H
   L.arow = take(repair_rows(scale_mode) ? (size_t)g.M * g.K * 4 : 0);
   L.rowup = take(repair_rows(scale_mode) ? (size_t)g.M * 4 : 0);
-  L.qb = take(repair_weights(scale_mode) ? (size_t)chunk * R * scales_b(g, scale_mode) * 4 : 0);
   L.hg = take(repair_weights(scale_mode) ? (size_t)G * R * R * 4 : 0);
   L.total = o;
   return L;
@@ -323,7 +321,11 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
                const Tables& T, int g0, int n, int fmt, int scale_mode, uint8_t* Tq, uint8_t* Sq,
                float* dT, float* dS, hipStream_t st) {
   const int R = geo.R;
-  const int per_row = scale_mode == FM_SCALE_ROWCOL ? 1 : 0;
+  // finer granularities fold their maxima into global memory by group:
+  // rows (per-row form), or 1 x 128 groups on A's side and bf16-rounded
+  // 128 x 128 blocks on B's (group schedule)
+  const int mode = base_mode(scale_mode);
+  const int per_row = mode == FM_SCALE_TENSOR ? 0 : 1;
   const size_t na = (size_t)n * R * scales_a(geo, scale_mode);
   const size_t nb = (size_t)n * R * scales_b(geo, scale_mode);
   uint32_t* amax = (uint32_t*)(ws + L.amax);
@@ -334,27 +336,9 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
   auto coef = [&](int k) { return (const float*)(ws + L.coef[k]); };
   const int pa = chunk_pattern(T, 0, g0, n), pb = chunk_pattern(T, 1, g0, n);
   FormArgs fa{A,    geo.M, geo.K, geo.gm, geo.gk, geo.Mb, geo.Kb, off(0), idx(0), coef(0), R, n,
-              amax, q,     Tq,    fmt,    per_row};
+              amax, q,     Tq,    fmt,    per_row, mode == FM_SCALE_GROUP ? 2 : 1};
   FormArgs fb{Bt, geo.N, geo.K, geo.gn, geo.gk, geo.Nb, geo.Kb, off(1), idx(1), coef(1), R, n,
-              amax + na, q + na, Sq, fmt, per_row};
-  if (base_mode(scale_mode) == FM_SCALE_GROUP) {
-    // one pass per side: every group's maximum is local to its wave or workgroup
-    float* qb = repair_weights(scale_mode) ? (float*)(ws + L.qb) : nullptr;
-    for (int side = 0; side < 2; ++side) {
-      timing_begin(T_FORM_QUANT, st);
-      if (int rc = launch_form_group(side ? fb : fa, side, side ? dd + na : dd,
-                                     (uint32_t*)(ws + L.flags), st, side ? qb : nullptr))
-        return rc;
-      timing_end(T_FORM_QUANT, st);
-    }
-    if (qb) {  // joint rounding of B's block sums replaces their nearest codes
-      timing_begin(T_FORM_QUANT, st);
-      if (int rc = launch_joint_round(fb, qb, dd + na,
-                                      (const float*)(ws + L.hg) + (size_t)g0 * R * R, st))
-        return rc;
-      timing_end(T_FORM_QUANT, st);
-    }
-  } else {
+              amax + na, q + na, Sq, fmt, per_row, mode == FM_SCALE_GROUP ? 3 : 1};
   if (int rc = launch_fill_u32(amax, na + nb, 0u, st)) return rc;
   for (int side = 0; side < 2; ++side) {
     timing_begin(T_FORM_AMAX, st);
@@ -368,6 +352,13 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
     if (int rc = launch_form(side ? fb : fa, 1, side ? pb : pa, side, st)) return rc;
     timing_end(T_FORM_QUANT, st);
   }
+  if (repair_weights(scale_mode)) {
+    // joint rounding of B's bf16 block sums replaces their nearest codes
+    timing_begin(T_FORM_QUANT, st);
+    if (int rc = launch_joint_round(fb, q + na, dd + na,
+                                    (const float*)(ws + L.hg) + (size_t)g0 * R * R, st))
+      return rc;
+    timing_end(T_FORM_QUANT, st);
   }
   if (dT)
     if (int rc = hip_check(hipMemcpyAsync(dT, dd, na * 4, hipMemcpyDeviceToDevice, st),

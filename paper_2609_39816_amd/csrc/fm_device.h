@@ -144,24 +144,48 @@ __device__ __forceinline__ void form_load(const FormArgs& a, float (&xv)[NB][VW]
   }
 }
 
+// Index of the maximum / scale that covers entries (x, y0..) of product r
+// of gauge g, for the finer granularities (a.per_row set).
+__device__ __forceinline__ size_t group_index(const FormArgs& a, int g, int r, int x, int y0) {
+  const size_t gr = (size_t)g * a.R + r;
+  if (a.gran == 1) return gr * a.br + x;
+  const size_t kg = gr * (a.bc / 128) + (y0 >> 7);
+  return a.gran == 2 ? kg * a.br + x : kg * (a.br / 128) + (x >> 7);
+}
+
+// The B side of the group schedule rounds block sums to bf16 (nearest even)
+// before their maxima and codes.
+template <int VW>
+__device__ __forceinline__ void round_bf16(float (&acc)[VW]) {
+#pragma unroll
+  for (int v = 0; v < VW; ++v) {
+    const uint32_t u = __float_as_uint(acc[v]);
+    acc[v] = __uint_as_float((u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u);
+  }
+}
+
 template <int VW, int MODE>
-__device__ __forceinline__ void form_finish(const FormArgs& a, const float (&acc)[VW], int g,
+__device__ __forceinline__ void form_finish(const FormArgs& a, const float (&acc0)[VW], int g,
                                             int g0, int r, bool active, int x, int y0,
                                             uint32_t* smax, int lane) {
+  float acc[VW];
+#pragma unroll
+  for (int v = 0; v < VW; ++v) acc[v] = acc0[v];
+  if (a.per_row && a.gran == 3) round_bf16<VW>(acc);
   if constexpr (MODE == 0) {
     uint32_t mx = 0u;
 #pragma unroll
     for (int v = 0; v < VW; ++v) mx = max(mx, __float_as_uint(acc[v]) & 0x7fffffffu);
     if (!active) mx = 0u;
-    if (a.per_row) {  // one maximum per block-sum row: straight to global memory
-      if (mx) atomicMax(&a.amax[((size_t)g * a.R + r) * a.br + x], mx);
+    if (a.per_row) {  // one maximum per group: straight to global memory
+      if (mx) atomicMax(&a.amax[group_index(a, g, r, x, y0)], mx);
       return;
     }
     mx = wave_max_u32(mx);
     if (lane == 0 && mx) atomicMax(&smax[(g - g0) * a.R + r], mx);
   } else {
     if (!active) return;
-    const float q = a.per_row ? a.q[((size_t)g * a.R + r) * a.br + x] : a.q[(size_t)g * a.R + r];
+    const float q = a.per_row ? a.q[group_index(a, g, r, x, y0)] : a.q[(size_t)g * a.R + r];
     uint8_t* dst =
         a.codes + ((size_t)g * a.R + r) * ((size_t)a.br * a.bc) + (size_t)x * a.bc + y0;
     if constexpr (VW >= 4) {
@@ -282,25 +306,27 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
 #pragma unroll
               for (int v = 0; v < VW; ++v) acc[v] = __builtin_fmaf(c, xv[b][v], acc[v]);
             });
+            if (ROWS && a.gran == 3) round_bf16<VW>(acc);
             if constexpr (MODE == 0) {
               uint32_t mx = 0u;
 #pragma unroll
               for (int v = 0; v < VW; ++v) mx = max(mx, __float_as_uint(acc[v]) & 0x7fffffffu);
               lm[j] = active ? mx : 0u;
             } else {
-              const float q = ROWS ? ro(a.q)[((size_t)g * P::R + r) * a.br + x]
+              const float q = ROWS ? ro(a.q)[group_index(a, g, r, x, y0)]
                                    : ro(a.q)[(size_t)g * P::R + r];
               form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, acc, q);
             }
           }
         });
         if constexpr (MODE == 0 && ROWS) {
-          // one maximum per block-sum row, folded into global memory: when a
-          // row spans whole 16-lane DPP rows (bcv a multiple of 16) they are
-          // reduced first and their last lane folds the result; otherwise
-          // every lane folds its own
+          // one maximum per group, folded into global memory: when a group
+          // spans whole 16-lane DPP rows (bcv a multiple of 16, and 16 VW
+          // entries within one group of 128 for the finer granularities)
+          // they are reduced first and their last lane folds the result;
+          // otherwise every lane folds its own
           constexpr int NJ = (gi * GR + GR <= P::R) ? GR : P::R - gi * GR;
-          if (bcv % 16 == 0) {
+          if (bcv % 16 == 0 && (a.gran == 1 || 16 * VW <= 128)) {
             sfor<0, 4>([&](auto sc) {
               constexpr int ctl = 0x111 + (1 << decltype(sc)::value) - 1;  // row_shr:1,2,4,8
               uint32_t sh[NJ];
@@ -313,12 +339,12 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
             if ((lane & 15) == 15 && active) {
 #pragma unroll
               for (int j = 0; j < NJ; ++j)
-                if (lm[j]) atomicMax(&a.amax[((size_t)g * P::R + gi * GR + j) * a.br + x], lm[j]);
+                if (lm[j]) atomicMax(&a.amax[group_index(a, g, gi * GR + j, x, y0)], lm[j]);
             }
           } else if (active) {
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
-              if (lm[j]) atomicMax(&a.amax[((size_t)g * P::R + gi * GR + j) * a.br + x], lm[j]);
+              if (lm[j]) atomicMax(&a.amax[group_index(a, g, gi * GR + j, x, y0)], lm[j]);
           }
         }
         if constexpr (MODE == 0 && !ROWS) {

@@ -109,21 +109,20 @@ struct FormArgs {
   const float* q;   // mode 1
   uint8_t* codes;   // mode 1
   int fmt;
-  int per_row;      // 0: one amax/scale per (gauge, product); 1: one per row
-                    // of the block-sum tensor as stored (br rows), at
-                    // amax/q[(g*R + r)*br + x]
+  int per_row;      // 0: one amax/scale per (gauge, product); 1: one per
+                    // group of entries, gran below, folded by atomics
+  int gran = 1;     // with per_row: 1 one per row of the block-sum tensor as
+                    // stored, at [(g R + r) br + x]; 2 one per row and 128
+                    // consecutive entries, at [((g R + r) (bc/128) + y/128) br + x];
+                    // 3 the same values rounded to bf16 first, one per 128 x 128
+                    // block, at [((g R + r) (bc/128) + y/128) (br/128) + x/128]
 };
 // pattern: family id from match_pattern (side A or B), or -1 for the
 // generic kernel.
 int launch_form(const FormArgs& a, int mode, int pattern, int side, hipStream_t st);
-// Group scales in one pass (side 0: 1 x 128 groups of A's block sums; side
-// 1: 128 x 128 blocks of B's bf16-rounded block sums): codes into a.codes,
-// scales d[(g R + r) (Kb/128) + kg][x] or [..][zb]; non-finite sets *flag |= 1.
-int launch_form_group(const FormArgs& a, int side, float* d, uint32_t* flag, hipStream_t st,
-                      float* qout = nullptr);
 // Repairs: row exponents of A (As = A 2^-k row by row, up = 2^k), and the
-// joint rounding of B's bf16 block sums (a is B's FormArgs; codes into
-// a.codes; qS, dS the block scales from launch_form_group; H G x R x R).
+// joint rounding of B's bf16 block sums (a is B's FormArgs with gran 3;
+// codes into a.codes; qS, dS the block scales; H G x R x R).
 int launch_row_repair(const float* A, int M, int K, float* As, float* up, hipStream_t st);
 int launch_joint_round(const FormArgs& a, const float* qS, const float* dS, const float* H,
                        hipStream_t st);

@@ -63,13 +63,7 @@ __global__ __launch_bounds__(256) void transpose_kernel(const float* __restrict_
   }
 }
 
-// ------------------------------------------------- group-scale formation
-// The models' schedule (App. B.1): A's block sums get one scale per row and
-// 128 consecutive inner entries; B's block sums (formed from B^T, rows =
-// output columns) are rounded to bf16 and get one scale per 128 x 128 block.
-// Each group's maximum is local to one wave (A) or one workgroup (B), so the
-// block sums are formed, scaled and encoded in a single pass.  Scales use the
-// tensor rule (q = FMAX / amax, d = amax / FMAX, both 1 for amax = 0).
+// ------------------------------------------------- group-scale schedule
 constexpr int kGroup = 128;
 constexpr int kRepairSweeps = 12;  // the repair rules' bound on the sweeps
 
@@ -77,116 +71,6 @@ __device__ __forceinline__ float bf16_rne(float x) {
   // nearest bf16, ties to even (finite inputs; non-finite values are flagged)
   const uint32_t u = __float_as_uint(x);
   return __uint_as_float((u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u);
-}
-
-__device__ __forceinline__ void group_scale(uint32_t m, float fmax, float& qv, float& dv,
-                                            uint32_t* flag, bool leader) {
-  if (m >= 0x7f800000u) {
-    if (leader) atomicOr(flag, 1u);
-    qv = dv = 1.0f;
-    return;
-  }
-  const float amax = __uint_as_float(m);
-  if (amax == 0.0f) {
-    qv = dv = 1.0f;
-  } else {
-    qv = __fdiv_rn(fmax, amax);
-    dv = __fdiv_rn(amax, fmax);
-  }
-}
-
-// A side: one wave per (row x, group kg) of product r of gauge g; lane l
-// forms entries 2l, 2l + 1 of the group.  grid (ceil(br * nkg / 4), R, G).
-__global__ __launch_bounds__(kThreads) void form_rowgroup_kernel(FormArgs a, float* __restrict__ d,
-                                                                 uint32_t* flag, float fmax) {
-  const int lane = threadIdx.x & 63;
-  const int nkg = a.bc / kGroup;
-  const long long grp = (long long)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
-  if (grp >= (long long)a.br * nkg) return;
-  const int x = (int)(grp / nkg), kg = (int)(grp - (long long)x * nkg);
-  const int r = blockIdx.y, g = blockIdx.z;
-  const auto off = ro(a.off);
-  const int e0 = off[(size_t)g * (a.R + 1) + r], e1 = off[(size_t)g * (a.R + 1) + r + 1];
-  float v0 = 0.0f, v1 = 0.0f;
-  for (int e = e0; e < e1; ++e) {
-    const float c = ro(a.coef)[e];
-    const int b = ro(a.idx)[e];
-    const int p = b / a.gc, qb = b - (b / a.gc) * a.gc;
-    const float2 xv = *reinterpret_cast<const float2*>(
-        a.X + (size_t)(p * a.br + x) * a.cols + (size_t)qb * a.bc + kg * kGroup + 2 * lane);
-    v0 = __builtin_fmaf(c, xv.x, v0);
-    v1 = __builtin_fmaf(c, xv.y, v1);
-  }
-  const uint32_t m = wave_max_u32(max(__float_as_uint(v0) & 0x7fffffffu,
-                                      __float_as_uint(v1) & 0x7fffffffu));
-  float qv, dv;
-  group_scale(m, fmax, qv, dv, flag, lane == 0);
-  const uint32_t c2 = enc2d(v0 * qv, v1 * qv, a.fmt);
-  const size_t o = ((size_t)((size_t)g * a.R + r) * a.br + x) * a.bc + kg * kGroup + 2 * lane;
-  *reinterpret_cast<uint16_t*>(a.codes + o) = (uint16_t)c2;
-  if (lane == 0) d[((size_t)((size_t)g * a.R + r) * nkg + kg) * a.br + x] = dv;
-}
-
-// B side: one workgroup per 128 x 128 block (rows zb*128.., inner kg*128..)
-// of product r of gauge g; thread t forms row t / 2, entries 64 (t & 1) ..
-// + 63, rounded to bf16.  grid (nzb * nkg, R, G).
-__global__ __launch_bounds__(kThreads) void form_bf16block_kernel(FormArgs a, float* __restrict__ d,
-                                                                  uint32_t* flag, float fmax,
-                                                                  float* __restrict__ qout) {
-  __shared__ uint32_t wmax[kThreads / 64];
-  const int nkg = a.bc / kGroup, nzb = a.br / kGroup;
-  const int zb = blockIdx.x / nkg, kg = blockIdx.x - (blockIdx.x / nkg) * nkg;
-  const int r = blockIdx.y, g = blockIdx.z;
-  const int zz = threadIdx.x >> 1, half = threadIdx.x & 1;
-  const auto off = ro(a.off);
-  const int e0 = off[(size_t)g * (a.R + 1) + r], e1 = off[(size_t)g * (a.R + 1) + r + 1];
-  float v[64];
-#pragma unroll
-  for (int i = 0; i < 64; ++i) v[i] = 0.0f;
-  for (int e = e0; e < e1; ++e) {
-    const float c = ro(a.coef)[e];
-    const int b = ro(a.idx)[e];
-    const int p = b / a.gc, qb = b - (b / a.gc) * a.gc;
-    const float4* src = reinterpret_cast<const float4*>(
-        a.X + (size_t)(p * a.br + zb * kGroup + zz) * a.cols + (size_t)qb * a.bc + kg * kGroup +
-        64 * half);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float4 xv = src[i];
-      v[4 * i] = __builtin_fmaf(c, xv.x, v[4 * i]);
-      v[4 * i + 1] = __builtin_fmaf(c, xv.y, v[4 * i + 1]);
-      v[4 * i + 2] = __builtin_fmaf(c, xv.z, v[4 * i + 2]);
-      v[4 * i + 3] = __builtin_fmaf(c, xv.w, v[4 * i + 3]);
-    }
-  }
-  uint32_t m = 0u;
-#pragma unroll
-  for (int i = 0; i < 64; ++i) {
-    v[i] = bf16_rne(v[i]);
-    m = max(m, __float_as_uint(v[i]) & 0x7fffffffu);
-  }
-  m = wave_max_u32(m);
-  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = m;
-  __syncthreads();
-  m = wmax[0];
-#pragma unroll
-  for (int w = 1; w < kThreads / 64; ++w) m = max(m, wmax[w]);
-  float qv, dv;
-  group_scale(m, fmax, qv, dv, flag, threadIdx.x == 0);
-  uint32_t w32[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i)
-    w32[i] = enc2d(v[4 * i] * qv, v[4 * i + 1] * qv, a.fmt) |
-             (enc2d(v[4 * i + 2] * qv, v[4 * i + 3] * qv, a.fmt) << 16);
-  uint4* dst = reinterpret_cast<uint4*>(
-      a.codes + ((size_t)((size_t)g * a.R + r) * a.br + zb * kGroup + zz) * a.bc + kg * kGroup +
-      64 * half);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) dst[i] = make_uint4(w32[4 * i], w32[4 * i + 1], w32[4 * i + 2], w32[4 * i + 3]);
-  if (threadIdx.x == 0) {
-    d[((size_t)((size_t)g * a.R + r) * nkg + kg) * nzb + zb] = dv;
-    if (qout) qout[((size_t)((size_t)g * a.R + r) * nkg + kg) * nzb + zb] = qv;
-  }
 }
 
 // ------------------------------------------------------------- repairs
@@ -582,27 +466,6 @@ int launch_fp8_encode(const float* x, uint8_t* out, size_t n, int fmt, int impl,
   fp8_encode_kernel<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, st>>>(x, out, n, fmt,
                                                                                    impl);
   return launched("fp8_encode_kernel");
-}
-
-int launch_form_group(const FormArgs& a, int side, float* d, uint32_t* flag, hipStream_t st,
-                      float* qout) {
-  if (a.bc % kGroup || (side == 1 && a.br % kGroup))
-    return fail(FM_E_SHAPE, "group scales need inner blocks (and B's blocks) of multiples of 128");
-  if (a.R > 65535 || a.G > 65535) return fail(FM_E_SHAPE, "too many products or gauges");
-  const float fmax = a.fmt == FM_E4M3 ? 448.0f : 57344.0f;
-  const int nkg = a.bc / kGroup;
-  if (side == 0) {
-    const long long groups = (long long)a.br * nkg;
-    const long long blocks = (groups + kThreads / 64 - 1) / (kThreads / 64);
-    if (blocks > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many groups");
-    form_rowgroup_kernel<<<dim3((unsigned)blocks, a.R, a.G), kThreads, 0, st>>>(a, d, flag, fmax);
-    return launched("form_rowgroup_kernel");
-  }
-  const long long blocks = (long long)(a.br / kGroup) * nkg;
-  if (blocks > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many groups");
-  form_bf16block_kernel<<<dim3((unsigned)blocks, a.R, a.G), kThreads, 0, st>>>(a, d, flag, fmax,
-                                                                              qout);
-  return launched("form_bf16block_kernel");
 }
 
 int launch_row_repair(const float* A, int M, int K, float* As, float* up, hipStream_t st) {
