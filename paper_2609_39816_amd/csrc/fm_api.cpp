@@ -107,7 +107,7 @@ int chunk_pattern(const Tables& T, int side, int g0, int n) {
 // Workspace layout for G gauges processed `chunk` at a time.
 struct Layout {
   size_t flags, bt, off[3], idx[3], coef[3], amax, q, d, tq, sq, mprod, partial, errsq, out3,
-      arow, rowup, hg, total;
+      arow, rowup, hg, hgc, hgp, total;
   int recon_nblk;
 };
 
@@ -175,7 +175,10 @@ Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
   // repairs: A's rescaled rows and the row factors; every gauge's H
   L.arow = take(repair_rows(scale_mode) ? (size_t)g.M * g.K * 4 : 0);
   L.rowup = take(repair_rows(scale_mode) ? (size_t)g.M * 4 : 0);
+  // every gauge's H in compressed rows: values, columns, row pointers
   L.hg = take(repair_weights(scale_mode) ? (size_t)G * R * R * 4 : 0);
+  L.hgc = take(repair_weights(scale_mode) ? (size_t)G * R * R * 2 : 0);
+  L.hgp = take(repair_weights(scale_mode) ? (size_t)G * (R + 1) * 4 : 0);
   L.total = o;
   return L;
 }
@@ -225,7 +228,30 @@ int prepare_repairs(const Geometry& geo, const Tables& T, char* ws, const Layout
   }
   if (repair_weights(scale_mode)) {
     const std::vector<float> H = repair_grams(T, geo);
-    if (int rc = upload(ws + L.hg, {{H.data(), H.size() * 4}}, {0}, H.size() * 4, st)) return rc;
+    const int R = T.R;
+    std::vector<float> hv((size_t)T.G * R * R, 0.0f);
+    std::vector<uint16_t> hc((size_t)T.G * R * R, 0);
+    std::vector<int32_t> hp((size_t)T.G * (R + 1), 0);
+    for (int g = 0; g < T.G; ++g) {
+      int n = 0;
+      for (int r = 0; r < R; ++r) {
+        hp[(size_t)g * (R + 1) + r] = n;
+        for (int t = 0; t < R; ++t) {
+          const float h = H[((size_t)g * R + r) * R + t];
+          if (h == 0.0f) continue;
+          hv[(size_t)g * R * R + n] = h;
+          hc[(size_t)g * R * R + n] = (uint16_t)t;
+          ++n;
+        }
+      }
+      hp[(size_t)g * (R + 1) + R] = n;
+    }
+    // the three tables are adjacent in the workspace: one staged copy
+    if (int rc = upload(ws + L.hg,
+                        {{hv.data(), hv.size() * 4}, {hc.data(), hc.size() * 2},
+                         {hp.data(), hp.size() * 4}},
+                        {0, L.hgc - L.hg, L.hgp - L.hg}, L.hgp - L.hg + hp.size() * 4, st))
+      return rc;
   }
   return FM_OK;
 }
@@ -356,7 +382,9 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
     // joint rounding of B's bf16 block sums replaces their nearest codes
     timing_begin(T_FORM_QUANT, st);
     if (int rc = launch_joint_round(fb, q + na, dd + na,
-                                    (const float*)(ws + L.hg) + (size_t)g0 * R * R, st))
+                                    (const float*)(ws + L.hg) + (size_t)g0 * R * R,
+                                    (const uint16_t*)(ws + L.hgc) + (size_t)g0 * R * R,
+                                    (const int32_t*)(ws + L.hgp) + (size_t)g0 * (R + 1), st))
       return rc;
     timing_end(T_FORM_QUANT, st);
   }

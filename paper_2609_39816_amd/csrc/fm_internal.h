@@ -122,10 +122,12 @@ struct FormArgs {
 int launch_form(const FormArgs& a, int mode, int pattern, int side, hipStream_t st);
 // Repairs: row exponents of A (As = A 2^-k row by row, up = 2^k), and the
 // joint rounding of B's bf16 block sums (a is B's FormArgs with gran 3;
-// codes into a.codes; qS, dS the block scales; H G x R x R).
+// codes into a.codes; qS, dS the block scales; H of every gauge in
+// compressed rows: hv values, hc columns (G x R x R each), hp pointers
+// (G x (R + 1))).
 int launch_row_repair(const float* A, int M, int K, float* As, float* up, hipStream_t st);
-int launch_joint_round(const FormArgs& a, const float* qS, const float* dS, const float* H,
-                       hipStream_t st);
+int launch_joint_round(const FormArgs& a, const float* qS, const float* dS, const float* hv,
+                       const uint16_t* hc, const int32_t* hp, hipStream_t st);
 
 // Scales from amax: for i < n: q[i] = FMAX/amax, d[i] = amax/FMAX (1, 1 for
 // amax = 0); a non-finite amax sets *flag |= 1.

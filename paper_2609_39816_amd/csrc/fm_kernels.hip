@@ -133,31 +133,55 @@ __device__ __forceinline__ uint32_t fp8_neighbour(uint32_t c, bool up, int fmt) 
 constexpr int kJointLanes = 64;
 constexpr int kJointMaxR = 64;
 
+// H of a gauge in compressed rows (symmetric, so a row is also a column):
+// hv values and hc columns of the nonzeros of row r at [hp[r], hp[r + 1]),
+// ascending columns; a zero entry contributes nothing to a fused
+// multiply-add, so skipping it leaves every sum bit-identical.
+struct JointH {
+  const float* hv;       // G x R*R (per gauge, the first nnz used)
+  const uint16_t* hc;    // G x R*R
+  const int32_t* hp;     // G x (R + 1)
+};
+
 __global__ __launch_bounds__(kJointLanes) void joint_round_kernel(FormArgs a,
                                                                   const float* __restrict__ qS,
                                                                   const float* __restrict__ dS,
-                                                                  const float* __restrict__ Hg,
-                                                                  int max_sweeps) {
+                                                                  JointH hg, int max_sweeps) {
   extern __shared__ float sm[];
   const int R = a.R;
-  float* H = sm;                          // R x R
-  float* qs = H + R * R;                  // R
-  float* dsc = qs + R;                    // R
-  float* sv = dsc + R;                    // R x 64
-  float* ev = sv + R * kJointLanes;       // R x 64
-  float* gv = ev + R * kJointLanes;       // R x 64
-  uint32_t* pk = reinterpret_cast<uint32_t*>(gv + R * kJointLanes);  // R x 64
   const int lane = threadIdx.x;
+  const int g = blockIdx.y;
+  const int32_t* hpg = hg.hp + (size_t)g * (R + 1);
+  const int nnz = hpg[R];
+  float* hv = sm;                                              // nnz
+  float* qs = hv + R * R;                                      // R
+  float* dsc = qs + R;                                         // R
+  float* hd = dsc + R;                                         // R: the diagonal
+  float* ev = hd + R;                                          // R x 64
+  float* gv = ev + R * kJointLanes;                            // R x 64
+  uint32_t* pk = reinterpret_cast<uint32_t*>(gv + R * kJointLanes);  // R x 64
+  int32_t* hp = reinterpret_cast<int32_t*>(pk + R * kJointLanes);    // R + 1
+  uint16_t* hc = reinterpret_cast<uint16_t*>(hp + R + 1);            // nnz
   const int nkg = a.bc / kGroup, nzb = a.br / kGroup;
   const int per_row = a.bc / kJointLanes;
   const int z = blockIdx.x / per_row, k = (blockIdx.x - z * per_row) * kJointLanes + lane;
   const int kg = k / kGroup, zb = z / kGroup;
-  const int g = blockIdx.y;
-  for (int i = lane; i < R * R; i += kJointLanes) H[i] = Hg[(size_t)g * R * R + i];
+  for (int i = lane; i < nnz; i += kJointLanes) {
+    hv[i] = hg.hv[(size_t)g * R * R + i];
+    hc[i] = hg.hc[(size_t)g * R * R + i];
+  }
+  for (int i = lane; i <= R; i += kJointLanes) hp[i] = hpg[i];
   for (int r = lane; r < R; r += kJointLanes) {
     const size_t o = ((size_t)((size_t)g * a.R + r) * nkg + kg) * nzb + zb;
     qs[r] = qS[o];
     dsc[r] = dS[o];
+  }
+  __syncthreads();
+  for (int r = lane; r < R; r += kJointLanes) {
+    float h = 0.0f;
+    for (int i = hp[r]; i < hp[r + 1]; ++i)
+      if (hc[i] == r) h = hv[i];
+    hd[r] = h;
   }
   __syncthreads();
   const auto off = ro(a.off);
@@ -187,36 +211,41 @@ __global__ __launch_bounds__(kJointLanes) void joint_round_kernel(FormArgs a,
         word |= 1u << 17;
       }
     }
-    sv[r * kJointLanes + lane] = s;
     ev[r * kJointLanes + lane] = er;
     pk[r * kJointLanes + lane] = word;
   }
   for (int r = 0; r < R; ++r) {
     float acc = 0.0f;
-    for (int t = 0; t < R; ++t) acc = __builtin_fmaf(H[r * R + t], ev[t * kJointLanes + lane], acc);
+    for (int i = hp[r]; i < hp[r + 1]; ++i)
+      acc = __builtin_fmaf(hv[i], ev[hc[i] * kJointLanes + lane], acc);
     gv[r * kJointLanes + lane] = acc;
   }
   for (int sw = 0; sw < max_sweeps; ++sw) {
     bool changed = false;
     for (int r = 0; r < R; ++r) {
       const uint32_t word = pk[r * kJointLanes + lane];
-      if (word & (1u << 16)) continue;  // no second candidate
-      const bool on_alt = (word >> 17) & 1u;
-      const uint32_t ccur = on_alt ? (word >> 8) & 0xffu : word & 0xffu;
-      const uint32_t calt = on_alt ? word & 0xffu : (word >> 8) & 0xffu;
-      const float vcur = fp8_value(ccur, a.fmt) * dsc[r];
-      const float valt = fp8_value(calt, a.fmt) * dsc[r];
-      const float delta = valt - vcur;
-      const float two = 2.0f * delta;
-      const float lin = two * gv[r * kJointLanes + lane];
-      const float sq = delta * delta;
-      const float quad = sq * H[r * R + r];
-      const float change = lin + quad;
-      if (change < 0.0f) {
+      bool flip = false;
+      float delta = 0.0f;
+      if (!(word & (1u << 16))) {
+        const bool on_alt = (word >> 17) & 1u;
+        const uint32_t ccur = on_alt ? (word >> 8) & 0xffu : word & 0xffu;
+        const uint32_t calt = on_alt ? word & 0xffu : (word >> 8) & 0xffu;
+        const float vcur = fp8_value(ccur, a.fmt) * dsc[r];
+        const float valt = fp8_value(calt, a.fmt) * dsc[r];
+        delta = valt - vcur;
+        const float two = 2.0f * delta;
+        const float lin = two * gv[r * kJointLanes + lane];
+        const float sq = delta * delta;
+        const float quad = sq * hd[r];
+        const float change = lin + quad;
+        flip = change < 0.0f;
+      }
+      if (flip) {
         pk[r * kJointLanes + lane] = word ^ (1u << 17);
-        for (int t = 0; t < R; ++t)
-          gv[t * kJointLanes + lane] =
-              __builtin_fmaf(H[t * R + r], delta, gv[t * kJointLanes + lane]);
+        for (int i = hp[r]; i < hp[r + 1]; ++i) {
+          const int t = hc[i];
+          gv[t * kJointLanes + lane] = __builtin_fmaf(hv[i], delta, gv[t * kJointLanes + lane]);
+        }
         changed = true;
       }
     }
@@ -475,21 +504,24 @@ int launch_row_repair(const float* A, int M, int K, float* As, float* up, hipStr
   return launched("row_repair_kernel");
 }
 
-int launch_joint_round(const FormArgs& a, const float* qS, const float* dS, const float* H,
-                       hipStream_t st) {
+int launch_joint_round(const FormArgs& a, const float* qS, const float* dS, const float* hv,
+                       const uint16_t* hc, const int32_t* hp, hipStream_t st) {
   if (a.bc % kGroup || a.br % kGroup) return fail(FM_E_SHAPE, "joint rounding needs 128 x 128 blocks");
   if (a.R > kJointMaxR)
     return fail(FM_E_UNSUPPORTED, "joint rounding is built for at most 64 products");
   if (a.G > 65535) return fail(FM_E_SHAPE, "too many gauges");
   const long long blocks = (long long)a.br * (a.bc / kJointLanes);
   if (blocks > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many positions");
-  const size_t shm = ((size_t)a.R * a.R + 2 * a.R + 4 * (size_t)a.R * kJointLanes) * 4;
+  // H values (room for R x R), q, d, diagonal, three R x 64 lane arrays,
+  // row pointers, then the columns (R x R halves)
+  const size_t shm = ((size_t)a.R * a.R + 3 * a.R + 3 * (size_t)a.R * kJointLanes + a.R + 1) * 4 +
+                     (size_t)a.R * a.R * 2;
   if (int rc = hip_check(hipFuncSetAttribute(reinterpret_cast<const void*>(&joint_round_kernel),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm),
                          "hipFuncSetAttribute"))
     return rc;
-  joint_round_kernel<<<dim3((unsigned)blocks, a.G), kJointLanes, shm, st>>>(a, qS, dS, H,
-                                                                           kRepairSweeps);
+  joint_round_kernel<<<dim3((unsigned)blocks, a.G), kJointLanes, shm, st>>>(
+      a, qS, dS, JointH{hv, hc, hp}, kRepairSweeps);
   return launched("joint_round_kernel");
 }
 
