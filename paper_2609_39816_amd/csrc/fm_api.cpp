@@ -373,18 +373,22 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
   }
   if (int rc = launch_scales(amax, q, dd, (int)(na + nb), fmt, (uint32_t*)(ws + L.flags), st))
     return rc;
-  for (int side = 0; side < 2; ++side) {
+  // with joint rounding B's codes come from it alone (it writes every one)
+  const int quant_sides = repair_weights(scale_mode) ? 1 : 2;
+  for (int side = 0; side < quant_sides; ++side) {
     timing_begin(T_FORM_QUANT, st);
     if (int rc = launch_form(side ? fb : fa, 1, side ? pb : pa, side, st)) return rc;
     timing_end(T_FORM_QUANT, st);
   }
   if (repair_weights(scale_mode)) {
-    // joint rounding of B's bf16 block sums replaces their nearest codes
+    // H's structure follows A's and C's lists, the block sums B's
+    const int pw = chunk_pattern(T, 2, g0, n);
     timing_begin(T_FORM_QUANT, st);
     if (int rc = launch_joint_round(fb, q + na, dd + na,
                                     (const float*)(ws + L.hg) + (size_t)g0 * R * R,
                                     (const uint16_t*)(ws + L.hgc) + (size_t)g0 * R * R,
-                                    (const int32_t*)(ws + L.hgp) + (size_t)g0 * (R + 1), st))
+                                    (const int32_t*)(ws + L.hgp) + (size_t)g0 * (R + 1),
+                                    pa == pb && pb == pw ? pb : -1, st))
       return rc;
     timing_end(T_FORM_QUANT, st);
   }

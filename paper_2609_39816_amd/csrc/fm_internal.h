@@ -124,10 +124,11 @@ int launch_form(const FormArgs& a, int mode, int pattern, int side, hipStream_t 
 // joint rounding of B's bf16 block sums (a is B's FormArgs with gran 3;
 // codes into a.codes; qS, dS the block scales; H of every gauge in
 // compressed rows: hv values, hc columns (G x R x R each), hp pointers
-// (G x (R + 1))).
+// (G x (R + 1)); pattern: the family id shared by all three sides of every
+// gauge, or -1 for the generic kernel).
 int launch_row_repair(const float* A, int M, int K, float* As, float* up, hipStream_t st);
 int launch_joint_round(const FormArgs& a, const float* qS, const float* dS, const float* hv,
-                       const uint16_t* hc, const int32_t* hp, hipStream_t st);
+                       const uint16_t* hc, const int32_t* hp, int pattern, hipStream_t st);
 
 // Scales from amax: for i < n: q[i] = FMAX/amax, d[i] = amax/FMAX (1, 1 for
 // amax = 0); a non-finite amax sets *flag |= 1.

@@ -63,16 +63,6 @@ __global__ __launch_bounds__(256) void transpose_kernel(const float* __restrict_
   }
 }
 
-// ------------------------------------------------- group-scale schedule
-constexpr int kGroup = 128;
-constexpr int kRepairSweeps = 12;  // the repair rules' bound on the sweeps
-
-__device__ __forceinline__ float bf16_rne(float x) {
-  // nearest bf16, ties to even (finite inputs; non-finite values are flagged)
-  const uint32_t u = __float_as_uint(x);
-  return __uint_as_float((u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u);
-}
-
 // ------------------------------------------------------------- repairs
 // Outside power-of-two row scaling (the repair rules): one wave per row t of
 // A computes the float64 sum of squares (lane l over the indices = l mod 64
@@ -117,32 +107,6 @@ __global__ __launch_bounds__(kThreads) void row_repair_kernel(const float* __res
 // 128 x 128 block.  LDS: the gauge's H, the block's scales q and d per
 // product, and per thread (column `lane` of R x 64 arrays) its block sums,
 // errors, H e and the candidate codes.
-__device__ __forceinline__ float fp8_value(uint32_t code, int fmt) {
-  return fmt == FM_E4M3 ? __builtin_amdgcn_cvt_f32_fp8((int)code, 0)
-                        : __builtin_amdgcn_cvt_f32_bf8((int)code, 0);
-}
-
-__device__ __forceinline__ uint32_t fp8_neighbour(uint32_t c, bool up, int fmt) {
-  // one step larger (up) or smaller in magnitude; 0x100 when there is none
-  const uint32_t mag = c & 0x7fu, sign = c & 0x80u;
-  const uint32_t maxmag = fmt == FM_E4M3 ? 0x7eu : 0x7bu;
-  if (up) return mag >= maxmag ? 0x100u : (sign | (mag + 1u));
-  return mag == 0u ? 0x100u : (sign | (mag - 1u));
-}
-
-constexpr int kJointLanes = 64;
-constexpr int kJointMaxR = 64;
-
-// H of a gauge in compressed rows (symmetric, so a row is also a column):
-// hv values and hc columns of the nonzeros of row r at [hp[r], hp[r + 1]),
-// ascending columns; a zero entry contributes nothing to a fused
-// multiply-add, so skipping it leaves every sum bit-identical.
-struct JointH {
-  const float* hv;       // G x R*R (per gauge, the first nnz used)
-  const uint16_t* hc;    // G x R*R
-  const int32_t* hp;     // G x (R + 1)
-};
-
 __global__ __launch_bounds__(kJointLanes) void joint_round_kernel(FormArgs a,
                                                                   const float* __restrict__ qS,
                                                                   const float* __restrict__ dS,
@@ -505,8 +469,17 @@ int launch_row_repair(const float* A, int M, int K, float* As, float* up, hipStr
 }
 
 int launch_joint_round(const FormArgs& a, const float* qS, const float* dS, const float* hv,
-                       const uint16_t* hc, const int32_t* hp, hipStream_t st) {
+                       const uint16_t* hc, const int32_t* hp, int pattern, hipStream_t st) {
   if (a.bc % kGroup || a.br % kGroup) return fail(FM_E_SHAPE, "joint rounding needs 128 x 128 blocks");
+  int id = 0;
+#define FM_JOINT_CASE(P)                                            \
+  if (pattern == id) {                                              \
+    const int rc = joint_family_##P(a, qS, dS, hv, hc, hp, st);     \
+    if (rc != 1) return rc;                                         \
+  }                                                                 \
+  ++id;
+  FM_PATTERN_FAMILIES(FM_JOINT_CASE)
+#undef FM_JOINT_CASE
   if (a.R > kJointMaxR)
     return fail(FM_E_UNSUPPORTED, "joint rounding is built for at most 64 products");
   if (a.G > 65535) return fail(FM_E_SHAPE, "too many gauges");

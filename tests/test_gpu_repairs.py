@@ -64,35 +64,62 @@ def operands(M, K, N, seed):
 
 
 CASES = [
-    # name, levels, M, K, N, which
-    ("strassen2_rows", 2, 256, 512, 512, "rows"),
-    ("strassen2_weights", 2, 256, 512, 512, "weights"),
-    ("strassen2_both_two_groups", 2, 128, 1024, 512, "both"),
-    ("strassen1_both", 1, 192, 256, 256, "both"),
+    # name, base, levels, gauge, M, K, N, fmt, which.  Kronecker powers and
+    # sign gauges keep a family's structure (the kernel specialized for it);
+    # a GL gauge on A's side alone leaves B's lists as they were but not A's
+    # and C's, so the joint rounding takes the generic kernel
+    ("strassen2_rows", "strassen", 2, None, 256, 512, 512, "e4m3", "rows"),
+    ("strassen2_weights", "strassen", 2, None, 256, 512, 512, "e4m3", "weights"),
+    ("strassen2_both_two_groups", "strassen", 2, None, 128, 1024, 512, "e4m3", "both"),
+    ("strassen1_both", "strassen", 1, None, 192, 256, 256, "e4m3", "both"),
+    ("strassen2_sign_weights_e5m2", "strassen", 2, "sign", 128, 512, 512, "e5m2", "weights"),
+    ("laderman_both", "laderman", 1, None, 192, 384, 384, "e4m3", "both"),
+    ("strassen1_gl_on_a_generic", "strassen", 1, "gl_a", 128, 256, 512, "e4m3", "weights"),
 ]
+FMT = {"e4m3": (fm.E4M3, oracle.E4M3), "e5m2": (fm.E5M2, oracle.E5M2)}
+
+
+def schemes_for(base, levels, gauge, seed):
+    """The library's scheme and the oracle's, flattened when gauged by signs
+    (then evaluated at one level)."""
+    hb, ob = fm.Scheme.base(base), osch.BASE_SCHEMES[base]()
+    if gauge is None:
+        return hb, so.power(ob, levels), levels
+    if gauge == "sign":
+        g = 2 ** levels
+        d, e, f = sy.sample_sign_orbit(g, g, g, 3, seed=seed)[-1]  # not the identity
+        D, E, F = np.diag(d), np.diag(e), np.diag(f)
+        return hb.kron(levels).gauge(D, E, F), so.gauge(so.power(ob, levels), D, E, F), 1
+    X = sy.gl_gauges(2, 2, 2, 1, seed=seed)[0][0]
+    I2 = np.eye(2)
+    assert levels == 1
+    return hb.gauge(X, I2, I2), so.gauge(ob, X, I2, I2), 1
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_repair_parity(case):
-    name, levels, M, K, N, which = case
+    name, base, levels, gauge, M, K, N, fmt, which = case
     fh, fo = FLAGS[which]
-    say(f"[repairs] {name} {M}x{K}x{N}")
+    th, to = FMT[fmt]
+    say(f"[repairs] {name} {M}x{K}x{N} {fmt}")
     A, B = operands(M, K, N, sum(name.encode()))
     At, Bt = gpu(A), gpu(B)
-    s = fm.Scheme.base("strassen")
-    tabs, dims = oracle.flatten_f32(so.power(osch.strassen(), levels))
-    want = oracle.lowp_matmul_repaired(A, B, tabs, dims, flags=fo, keep=True)
-    Tq, Sq, dT, dS = fm.form_operands(s, At, Bt, levels, scale_mode=SG | fh)
+    s, o, lv = schemes_for(base, levels, gauge, seed=sum(name.encode()))
+    fam = s.kernel_family(lv)
+    assert (fam == "generic") == (gauge == "gl_a"), fam
+    tabs, dims = oracle.flatten_f32(o)
+    want = oracle.lowp_matmul_repaired(A, B, tabs, dims, fmt=to, flags=fo, keep=True)
+    Tq, Sq, dT, dS = fm.form_operands(s, At, Bt, lv, th, scale_mode=SG | fh)
     assert np.array_equal(Tq.cpu().numpy(), want["Tq"]), "Tq"
     assert np.array_equal(bits(dT.cpu().numpy()), bits(want["dT"])), "dT"
     assert np.array_equal(Sq.cpu().numpy(), want["Sq"].transpose(0, 2, 1)), "Sq"
     assert np.array_equal(bits(dS.cpu().numpy()), bits(want["dS"])), "dS"
-    C = fm.matmul_lowp(s, At, Bt, levels, scale_mode=SG | fh).cpu().numpy()
+    C = fm.matmul_lowp(s, At, Bt, lv, th, scale_mode=SG | fh).cpu().numpy()
     assert rel(C, want["C"]) <= TOL, f"C: {rel(C, want['C']):.2e}"
     # the orbit path (errors fused in the reconstruction) agrees with C
     Cref = fm.reference_f64(At, Bt)
-    err = fm.orbit_eval([s.kron(levels) if levels > 1 else s], At, Bt, Cref,
-                        1, scale_mode=SG | fh)[0]
+    err = fm.orbit_eval([s.kron(lv) if lv > 1 else s], At, Bt, Cref, 1, th,
+                        scale_mode=SG | fh)[0]
     assert abs(err / oracle.rel_fro(want["C"], oracle.reference_f64(A, B)) - 1) <= 1e-2
 
 
