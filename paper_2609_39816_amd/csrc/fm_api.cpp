@@ -81,6 +81,7 @@ struct Tables {
   int G = 0, R = 0;
   Side s[3];
   std::vector<int> pat[3];
+  std::vector<int> hpat;  // family of each gauge's H support (joint rounding only)
 };
 
 void append(Tables& T, const Lists& L, int R, const int nb[3]) {
@@ -186,9 +187,13 @@ Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
 // H_rs = <w_r, w_s> <u_r, u_s> for every gauge (the repair rules), from the
 // fp32 coefficient lists: each inner product in float64 over ascending block
 // index, their product rounded once to fp32.
-std::vector<float> repair_grams(const Tables& T, const Geometry& geo) {
+// H of every gauge (G x R x R) and its support: the pairs whose products
+// share a block of A and a block of C, where H can be nonzero (an entry of
+// the support may still cancel to zero).
+std::vector<float> repair_grams(const Tables& T, const Geometry& geo, std::vector<uint8_t>& sup) {
   const int R = T.R, nu = geo.NBa(), nw = geo.NC();
   std::vector<float> H((size_t)T.G * R * R);
+  sup.assign((size_t)T.G * R * R, 0);
   std::vector<double> u((size_t)R * nu), w((size_t)R * nw);
   for (int g = 0; g < T.G; ++g) {
     std::fill(u.begin(), u.end(), 0.0);
@@ -204,9 +209,17 @@ std::vector<float> repair_grams(const Tables& T, const Geometry& geo) {
     for (int r = 0; r < R; ++r)
       for (int t = 0; t < R; ++t) {
         double uu = 0.0, ww = 0.0;
-        for (int i = 0; i < nu; ++i) uu += u[(size_t)r * nu + i] * u[(size_t)t * nu + i];
-        for (int i = 0; i < nw; ++i) ww += w[(size_t)r * nw + i] * w[(size_t)t * nw + i];
+        bool su = false, sw = false;
+        for (int i = 0; i < nu; ++i) {
+          uu += u[(size_t)r * nu + i] * u[(size_t)t * nu + i];
+          su |= u[(size_t)r * nu + i] != 0.0 && u[(size_t)t * nu + i] != 0.0;
+        }
+        for (int i = 0; i < nw; ++i) {
+          ww += w[(size_t)r * nw + i] * w[(size_t)t * nw + i];
+          sw |= w[(size_t)r * nw + i] != 0.0 && w[(size_t)t * nw + i] != 0.0;
+        }
         H[((size_t)g * R + r) * R + t] = (float)(ww * uu);
+        sup[((size_t)g * R + r) * R + t] = su && sw;
       }
   }
   return H;
@@ -214,7 +227,7 @@ std::vector<float> repair_grams(const Tables& T, const Geometry& geo) {
 
 // Repairs that act once per call: A's rows rescaled (returns the operand the
 // formation reads and the row factors) and every gauge's H uploaded.
-int prepare_repairs(const Geometry& geo, const Tables& T, char* ws, const Layout& L,
+int prepare_repairs(const Geometry& geo, Tables& T, char* ws, const Layout& L,
                     int scale_mode, const float* A, const float*& Aform, const float*& rowup,
                     hipStream_t st) {
   Aform = A;
@@ -227,24 +240,29 @@ int prepare_repairs(const Geometry& geo, const Tables& T, char* ws, const Layout
     rowup = up;
   }
   if (repair_weights(scale_mode)) {
-    const std::vector<float> H = repair_grams(T, geo);
+    // H in compressed rows over its support (an entry outside it is an
+    // exact zero and is left out; one inside that cancels adds an exact
+    // zero), so the rows of a family's gauges follow the family's H pattern
+    std::vector<uint8_t> sup;
+    const std::vector<float> H = repair_grams(T, geo, sup);
     const int R = T.R;
     std::vector<float> hv((size_t)T.G * R * R, 0.0f);
     std::vector<uint16_t> hc((size_t)T.G * R * R, 0);
     std::vector<int32_t> hp((size_t)T.G * (R + 1), 0);
+    T.hpat.assign(T.G, -1);
     for (int g = 0; g < T.G; ++g) {
       int n = 0;
       for (int r = 0; r < R; ++r) {
         hp[(size_t)g * (R + 1) + r] = n;
         for (int t = 0; t < R; ++t) {
-          const float h = H[((size_t)g * R + r) * R + t];
-          if (h == 0.0f) continue;
-          hv[(size_t)g * R * R + n] = h;
+          if (!sup[((size_t)g * R + r) * R + t]) continue;
+          hv[(size_t)g * R * R + n] = H[((size_t)g * R + r) * R + t];
           hc[(size_t)g * R * R + n] = (uint16_t)t;
           ++n;
         }
       }
       hp[(size_t)g * (R + 1) + R] = n;
+      T.hpat[g] = match_h_pattern(hp.data() + (size_t)g * (R + 1), hc.data() + (size_t)g * R * R, R);
     }
     // the three tables are adjacent in the workspace: one staged copy
     if (int rc = upload(ws + L.hg,
@@ -381,14 +399,16 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
     timing_end(T_FORM_QUANT, st);
   }
   if (repair_weights(scale_mode)) {
-    // H's structure follows A's and C's lists, the block sums B's
-    const int pw = chunk_pattern(T, 2, g0, n);
+    // the family kernel needs B's lists and H's support both of its family
+    int ph = T.hpat.empty() ? -1 : T.hpat[g0];
+    for (int g = g0 + 1; g < g0 + n && ph >= 0; ++g)
+      if (T.hpat[g] != ph) ph = -1;
     timing_begin(T_FORM_QUANT, st);
     if (int rc = launch_joint_round(fb, q + na, dd + na,
                                     (const float*)(ws + L.hg) + (size_t)g0 * R * R,
                                     (const uint16_t*)(ws + L.hgc) + (size_t)g0 * R * R,
                                     (const int32_t*)(ws + L.hgp) + (size_t)g0 * (R + 1),
-                                    pa == pb && pb == pw ? pb : -1, st))
+                                    pb >= 0 && pb == ph ? pb : -1, st))
       return rc;
     timing_end(T_FORM_QUANT, st);
   }

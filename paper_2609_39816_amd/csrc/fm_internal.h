@@ -64,6 +64,9 @@ void build_lists(const fm_scheme& flat, Lists& out);
 // Pattern family of one side of a list (compiled specializations), or -1.
 int match_pattern(int side, const Side& s, int R, int NB);
 // Number of pattern families; side: 0 = A, 1 = B, 2 = W.
+// Family whose H pattern (pairs of products sharing a block of A and a
+// block of C) equals one gauge's H support in compressed rows, or -1.
+int match_h_pattern(const int32_t* rowptr, const uint16_t* cols, int R);
 int pattern_count();
 const char* pattern_name(int id);
 

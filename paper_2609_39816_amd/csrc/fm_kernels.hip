@@ -18,6 +18,7 @@
 #include <hip/hip_runtime.h>
 
 #include "fm_device.h"
+#include "fm_joint.h"
 
 
 namespace fm {

@@ -15,6 +15,10 @@ struct PatternRef {
   int nnz[3];
   const int16_t* rowptr[3];
   const int16_t* idx[3];
+  bool joint;  // H pattern generated (at most 64 products)
+  int hnnz;
+  const int16_t* hrowptr;
+  const int16_t* hidx;
 };
 
 #define FM_PATTERN_REF(P)                                                    \
@@ -23,7 +27,11 @@ struct PatternRef {
              {pat::P::A::NB, pat::P::B::NB, pat::P::W::NB},                  \
              {pat::P::A::NNZ, pat::P::B::NNZ, pat::P::W::NNZ},               \
              {pat::P::A::rowptr, pat::P::B::rowptr, pat::P::W::rowptr},      \
-             {pat::P::A::idx, pat::P::B::idx, pat::P::W::idx}},
+             {pat::P::A::idx, pat::P::B::idx, pat::P::W::idx},                \
+             pat::P::H::JOINT,                                               \
+             pat::P::H::NNZ,                                                 \
+             pat::P::H::rowptr,                                              \
+             pat::P::H::idx},
 
 const PatternRef kPatterns[] = {FM_PATTERN_FAMILIES(FM_PATTERN_REF)};
 constexpr int kNumPatterns = sizeof(kPatterns) / sizeof(kPatterns[0]);
@@ -43,6 +51,18 @@ int match_pattern(int side, const Side& s, int R, int NB) {
     bool ok = true;
     for (int r = 0; r <= R && ok; ++r) ok = (P.rowptr[side][r] == s.off[r] - s.off[0]);
     for (size_t e = 0; e < s.idx.size() && ok; ++e) ok = (P.idx[side][e] == s.idx[e]);
+    if (ok) return p;
+  }
+  return -1;
+}
+
+int match_h_pattern(const int32_t* rowptr, const uint16_t* cols, int R) {
+  for (int p = 0; p < kNumPatterns; ++p) {
+    const PatternRef& P = kPatterns[p];
+    if (!P.joint || P.R != R || P.hnnz != rowptr[R]) continue;
+    bool ok = true;
+    for (int r = 0; r <= R && ok; ++r) ok = P.hrowptr[r] == rowptr[r];
+    for (int e = 0; e < P.hnnz && ok; ++e) ok = P.hidx[e] == (int)cols[e];
     if (ok) return p;
   }
   return -1;
