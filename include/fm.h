@@ -460,6 +460,15 @@ int fm_set_block_product_arithmetic(fm_accum a);
 int fm_fp8_encode(const float* x, int64_t n, fm_fmt fmt, int impl, uint8_t* out,
                   void* hip_stream);
 
+/* The bf16 rounding of the group schedule (App. B.1: B's block sums are
+ * rounded to bf16 before their scales and codes) applied to n fp32 device
+ * values x; out (device, n floats) holds the bf16 values as fp32:
+ * impl 0 = the rounding the formation kernels use, 1 = the gfx950
+ * conversion instruction (v_cvt_pk_bf16_f32), 2 = the integer rounding
+ * (add 0x7fff plus the kept low bit, truncate).  Nearest, ties to even;
+ * finite inputs (the formation flags non-finite ones).  Async. */
+int fm_bf16_round(const float* x, int64_t n, int impl, float* out, void* hip_stream);
+
 /* Name of the kernel family that evaluates `s` flattened to `levels`
  * ("Strassen2", "DenseR7G2", ... or "generic"): families have formation and
  * reconstruction kernels compiled for their nonzero structure.  Static

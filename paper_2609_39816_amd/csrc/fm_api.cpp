@@ -1055,6 +1055,14 @@ int fm_fp8_encode(const float* x, int64_t n, fm_fmt fmt, int impl, uint8_t* out,
   return launch_fp8_encode(x, out, (size_t)n, fmt, impl, (hipStream_t)hip_stream);
 }
 
+int fm_bf16_round(const float* x, int64_t n, int impl, float* out, void* hip_stream) {
+  clear_error();
+  if (!x || !out) return fail(FM_E_ARG, "null pointer");
+  if (n < 0 || impl < 0 || impl > 2) return fail(FM_E_ARG, "bad argument");
+  if ((uint64_t)n > ((uint64_t)0xffffffffu) * 256u) return fail(FM_E_SHAPE, "too many values");
+  return launch_bf16_round(x, out, (size_t)n, impl, (hipStream_t)hip_stream);
+}
+
 const char* fm_scheme_kernel_family(const fm_scheme* s, int levels) {
   clear_error();
   if (!s || levels < 1 || levels > 8) {

@@ -154,14 +154,27 @@ __device__ __forceinline__ size_t group_index(const FormArgs& a, int g, int r, i
 }
 
 // The B side of the group schedule rounds block sums to bf16 (nearest even)
-// before their maxima and codes.
+// before their maxima and codes: two at a time with the gfx950 conversion
+// (v_cvt_pk_bf16_f32, checked against the integer rounding on every fp32
+// high half with low halves around each tie), back to fp32 exactly.
+__device__ __forceinline__ float bf16_round_int(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return __uint_as_float((u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u);
+}
+
+__device__ __forceinline__ void bf16_round_pair(float& x0, float& x1) {
+  typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  const bf2 b = __builtin_convertvector((f2){x0, x1}, bf2);
+  x0 = (float)b[0];
+  x1 = (float)b[1];
+}
+
 template <int VW>
 __device__ __forceinline__ void round_bf16(float (&acc)[VW]) {
 #pragma unroll
-  for (int v = 0; v < VW; ++v) {
-    const uint32_t u = __float_as_uint(acc[v]);
-    acc[v] = __uint_as_float((u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u);
-  }
+  for (int v = 0; v + 1 < VW; v += 2) bf16_round_pair(acc[v], acc[v + 1]);
+  if constexpr (VW % 2) acc[VW - 1] = bf16_round_int(acc[VW - 1]);
 }
 
 template <int VW, int MODE>
@@ -293,6 +306,14 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
       sfor<0, NG>([&](auto gc) {
         constexpr int gi = decltype(gc)::value;
         uint32_t lm[GR];
+        // finer scales: the group's scale loads go out before its block
+        // sums, so their latency hides under the fused multiply-adds
+        [[maybe_unused]] float qv[GR];
+        if constexpr (MODE == 1 && ROWS)
+          sfor<0, GR>([&](auto jc) {
+            constexpr int j = decltype(jc)::value, r = gi * GR + j;
+            if constexpr (r < P::R) qv[j] = ro(a.q)[group_index(a, g, r, x, y0)];
+          });
         sfor<0, GR>([&](auto jc) {
           constexpr int j = decltype(jc)::value, r = gi * GR + j;
           if constexpr (r < P::R) {
@@ -313,8 +334,7 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
               for (int v = 0; v < VW; ++v) mx = max(mx, __float_as_uint(acc[v]) & 0x7fffffffu);
               lm[j] = active ? mx : 0u;
             } else {
-              const float q = ROWS ? ro(a.q)[group_index(a, g, r, x, y0)]
-                                   : ro(a.q)[(size_t)g * P::R + r];
+              const float q = ROWS ? qv[j] : ro(a.q)[(size_t)g * P::R + r];
               form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, acc, q);
             }
           }

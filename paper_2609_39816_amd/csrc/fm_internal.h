@@ -205,5 +205,6 @@ int launch_error_finalize(const double* partial, int nblk, double* out3, hipStre
 
 // Diagnostic encoder: codes for n fp32 values with the kernels' encoder.
 int launch_fp8_encode(const float* x, uint8_t* out, size_t n, int fmt, int impl, hipStream_t st);
+int launch_bf16_round(const float* x, float* out, size_t n, int impl, hipStream_t st);
 
 }  // namespace fm

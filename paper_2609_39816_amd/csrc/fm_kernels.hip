@@ -38,6 +38,19 @@ __global__ void fp8_encode_kernel(const float* x, uint8_t* out, size_t n, int fm
   out[i] = (uint8_t)(c & 0xffu);
 }
 
+__global__ void bf16_round_kernel(const float* x, float* out, size_t n, int impl) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float v = x[i];
+  if (impl == 2) {
+    v = bf16_round_int(v);
+  } else {
+    float w = v;
+    bf16_round_pair(v, w);
+  }
+  out[i] = v;
+}
+
 // ------------------------------------------------------------------ fill
 __global__ void fill_u32_kernel(uint32_t* p, size_t n, uint32_t v) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
@@ -460,6 +473,12 @@ int launch_fp8_encode(const float* x, uint8_t* out, size_t n, int fmt, int impl,
   fp8_encode_kernel<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, st>>>(x, out, n, fmt,
                                                                                    impl);
   return launched("fp8_encode_kernel");
+}
+
+int launch_bf16_round(const float* x, float* out, size_t n, int impl, hipStream_t st) {
+  if (n == 0) return FM_OK;
+  bf16_round_kernel<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, st>>>(x, out, n, impl);
+  return launched("bf16_round_kernel");
 }
 
 int launch_row_repair(const float* A, int M, int K, float* As, float* up, hipStream_t st) {

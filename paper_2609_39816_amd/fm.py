@@ -90,6 +90,7 @@ def _load():
         "fm_int8_plan_run": (i, [p, p, p, p, p, p, p]),
         "fm_int8_plan_free": (None, [p]),
         "fm_fp8_encode": (i, [p, i64, i, i, p, p]),
+        "fm_bf16_round": (i, [p, i64, i, p, p]),
         "fm_scheme_kernel_family": (ct.c_char_p, [p, i]),
         "fm_status": (i, [p, sz, p]),
         "fm_set_block_product_arithmetic": (i, [i]),
@@ -359,6 +360,13 @@ def fp8_encode(x, fmt: int = E4M3, impl: int = 0, stream=None):
     _cuda(x, torch.float32)
     out = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
     _check(lib.fm_fp8_encode(_dptr(x), x.numel(), fmt, impl, _dptr(out), _stream(stream)))
+    return out
+
+
+def bf16_round(x, impl: int = 0, stream=None):
+    _cuda(x, torch.float32)
+    out = torch.empty_like(x)
+    _check(lib.fm_bf16_round(_dptr(x), x.numel(), impl, _dptr(out), _stream(stream)))
     return out
 
 

@@ -50,6 +50,10 @@ def gpu(x):
     return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
 
 
+def bits(x):
+    return np.ascontiguousarray(x, np.float32).view(np.uint32)
+
+
 class OracleSchemes:
     """Oracle-side gauged schemes, built on first use (pure-Python float64)."""
 
@@ -168,6 +172,23 @@ def test_fp8_hardware_conversion_report(fmt):
     bad = np.nonzero(got != want)[0]
     say(f"[codec] hardware {fmt}: {bad.size} of {x.size} differ; first: "
         f"{[(float(x[i]), int(got[i]), int(want[i])) for i in bad[:6]]}")
+
+
+def test_bf16_rounding_bit_exact():
+    """The group schedule's bf16 rounding on the device (the gfx950
+    conversion the formation kernels use, and the integer rounding) equals
+    the oracle's on every finite fp32 high half with low halves on, above and
+    below each tie, subnormals included."""
+    hi = np.arange(1 << 16, dtype=np.uint32) << 16
+    lows = np.array([0, 1, 0x7FFF, 0x8000, 0x8001, 0xFFFF], dtype=np.uint32)
+    x = (hi[:, None] | lows[None, :]).reshape(-1).view(np.float32)
+    x = x[np.isfinite(oracle.bf16_round(x))]
+    want = bits(oracle.bf16_round(x))
+    xg = gpu(x)
+    for impl in (0, 1, 2):
+        got = bits(fm.bf16_round(xg, impl).cpu().numpy())
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, (impl, x[bad[:8]], got[bad[:8]], want[bad[:8]])
 
 
 # ------------------------------------------------------------ workloads
