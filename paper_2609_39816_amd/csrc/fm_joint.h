@@ -35,12 +35,15 @@ __device__ __forceinline__ uint32_t fp8_neighbour(uint32_t c, bool up, int fmt) 
   return mag == 0u ? 0x100u : (sign | (mag - 1u));
 }
 
-// H of a gauge in compressed rows (symmetric, so a row is also a column):
-// hv values and hc columns of the nonzeros of row r at [hp[r], hp[r + 1]),
-// ascending columns; a zero entry contributes nothing to a fused
-// multiply-add, so skipping it leaves every sum bit-identical.
+// H of a gauge in compressed rows over its support, the pairs of products
+// that share a block of A and a block of C (symmetric, so a row is also a
+// column): hv values and hc columns of row r at [hp[r], hp[r + 1]),
+// ascending columns.  Outside the support H is an exact zero and is
+// skipped; an entry inside it may still be zero and adds an exact zero to a
+// fused multiply-add; either way every sum equals the dense one (up to the
+// sign of a zero sum, which no decision can see).
 struct JointH {
-  const float* hv;       // G x R*R (per gauge, the first nnz used)
+  const float* hv;       // G x R*R (per gauge, the first hp[R] used)
   const uint16_t* hc;    // G x R*R
   const int32_t* hp;     // G x (R + 1)
 };
