@@ -131,9 +131,12 @@ int scales_b(const Geometry& g, int scale_mode) {
 }
 // Block shapes a scale mode needs (group scales: Kb, Nb multiples of 128,
 // Mb of 4).
-int scale_shape_ok(int Mb, int Nb, int Kb, int scale_mode) {
+int scale_shape_ok(int Mb, int Nb, int Kb, int R, int scale_mode) {
   if (base_mode(scale_mode) == FM_SCALE_GROUP && (Kb % 128 || Nb % 128 || Mb % 4))
     return fail(FM_E_SHAPE, "group scales need Kb, Nb multiples of 128 and Mb of 4");
+  // checked before any device work (the joint rounding keeps R-long state)
+  if (repair_weights(scale_mode) && R > 64)
+    return fail(FM_E_UNSUPPORTED, "joint rounding is built for at most 64 products");
   return FM_OK;
 }
 
@@ -782,7 +785,7 @@ size_t fm_workspace_size_scaled(const fm_scheme* s, int M, int N, int K, int lev
                                 int chunk, fm_scale_mode scale_mode) {
   Geometry g;
   if (G < 1 || !scale_mode_ok(scale_mode) || check_geometry(s, levels, M, N, K, g) != FM_OK ||
-      scale_shape_ok(g.Mb, g.Nb, g.Kb, scale_mode) != FM_OK)
+      scale_shape_ok(g.Mb, g.Nb, g.Kb, g.R, scale_mode) != FM_OK)
     return 0;
   if (chunk <= 0 || chunk > G) chunk = G;
   return make_layout(g, G, chunk, true, scale_mode).total;
@@ -808,7 +811,7 @@ int fm_form_operands_scaled(const fm_scheme* s, int levels, const float* A, cons
   if (!scale_mode_ok(scale_mode)) return fail(FM_E_ARG, "bad scale mode");
   Geometry geo;
   if (int rc = check_geometry(s, levels, M, N, K, geo)) return rc;
-  if (int rc = scale_shape_ok(geo.Mb, geo.Nb, geo.Kb, scale_mode)) return rc;
+  if (int rc = scale_shape_ok(geo.Mb, geo.Nb, geo.Kb, geo.R, scale_mode)) return rc;
   const Layout L = make_layout(geo, 1, 1, true, scale_mode);
   if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
   hipStream_t st = (hipStream_t)hip_stream;
@@ -885,7 +888,7 @@ int fm_matmul_lowp_scaled(const fm_scheme* s, const float* A, const float* B, fl
   if (!scale_mode_ok(scale_mode)) return fail(FM_E_ARG, "bad scale mode");
   Geometry geo;
   if (int rc = check_geometry(s, levels, M, N, K, geo)) return rc;
-  if (int rc = scale_shape_ok(geo.Mb, geo.Nb, geo.Kb, scale_mode)) return rc;
+  if (int rc = scale_shape_ok(geo.Mb, geo.Nb, geo.Kb, geo.R, scale_mode)) return rc;
   const Layout L = make_layout(geo, 1, 1, true, scale_mode);
   if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
   hipStream_t st = (hipStream_t)hip_stream;
@@ -969,7 +972,7 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   if (!scale_mode_ok(scale_mode)) return fail(FM_E_ARG, "bad scale mode");
   Geometry geo;
   if (int rc = check_geometry(gauged[0], levels, M, N, K, geo)) return rc;
-  if (int rc = scale_shape_ok(geo.Mb, geo.Nb, geo.Kb, scale_mode)) return rc;
+  if (int rc = scale_shape_ok(geo.Mb, geo.Nb, geo.Kb, geo.R, scale_mode)) return rc;
   int chunk = G;
   Layout L = make_layout(geo, G, chunk, true, scale_mode);
   while (chunk > 1 && L.total > ws_bytes) {

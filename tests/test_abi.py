@@ -257,3 +257,20 @@ def test_corrected_certificate_from_the_library():
     rc = fm.lib.fm_int8_plan_create(s.handle, 2, 64, 64, 256, 256, 32, 127, 127, 1, None, 0, None,
                                     ct.byref(out))
     assert rc == ERR["FM_E_UNSUPPORTED"] and not out.value
+
+
+def test_joint_rounding_beyond_64_products_is_refused_up_front():
+    """The joint rounding keeps R-long state per position and is built for at
+    most 64 products: three-level Strassen (343) is refused before any
+    device work (stand-in pointers are never touched)."""
+    s = fm.Scheme.base("strassen")
+    fake = ct.c_void_p(256)
+    mode = fm.SCALE_GROUP | fm.REPAIR_WEIGHTS
+    rc = fm.lib.fm_form_operands_scaled(s.handle, 3, fake, fake, 32, 1024, 1024, fm.E4M3, mode,
+                                        fake, fake, fake, fake, fake, 1 << 40, None)
+    assert rc == ERR["FM_E_UNSUPPORTED"]
+    assert "64 products" in fm.lib.fm_last_error().decode()
+    rc = fm.lib.fm_form_operands_scaled(s.handle, 3, fake, fake, 32, 1024, 1024, fm.E4M3,
+                                        fm.SCALE_GROUP | fm.REPAIR_ROWS, fake, fake, fake, fake,
+                                        fake, 0, None)
+    assert rc == ERR["FM_E_WORKSPACE"]  # rows alone pass the check, then the workspace is short
