@@ -910,12 +910,16 @@ int fm_matmul_lowp_scaled(const fm_scheme* s, const float* A, const float* B, fl
   const float* dd = (const float*)(ws + L.d);
   float* Mp = (float*)(ws + L.mprod);
   timing_begin(T_BLOCK_GEMM, st);
+  // group scales return bf16 products: stored as bf16 on the way to the
+  // reconstruction (half the bytes, the same values)
+  const bool bf = base_mode(scale_mode) == FM_SCALE_GROUP;
   if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)geo.R * scales_a(geo, scale_mode), Mp,
-                              geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, base_mode(scale_mode), st)))
+                              geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, base_mode(scale_mode), st, bf)))
     return rc;
   timing_end(T_BLOCK_GEMM, st);
   ReconArgs ra = recon_args(geo, ws, L, 0, 1, Mp, C, nullptr);
   ra.rowscale = rowup;
+  ra.prod_bf16 = bf;
   return launch_recon(ra, chunk_pattern(T, 2, 0, 1), st);
 }
 
@@ -996,6 +1000,9 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   double* errsq = (double*)(ws + L.errsq);
   const float *Aform, *rowup;
   if ((rc = prepare_repairs(geo, T, ws, L, scale_mode, A, Aform, rowup, st))) return rc;
+  // group scales return bf16 products: stored as bf16 on the way to the
+  // reconstruction (half the bytes, the same values)
+  const bool bf = base_mode(scale_mode) == FM_SCALE_GROUP;
   for (int g0 = 0; g0 < G; g0 += chunk) {
     const int n = std::min(chunk, G - g0);
     if ((rc = form_chunk(geo, Aform, Bt, ws, L, T, g0, n, fmt, scale_mode, Tq, Sq, nullptr,
@@ -1004,11 +1011,12 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
     timing_begin(T_BLOCK_GEMM, st);
     if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)n * geo.R * scales_a(geo, scale_mode), Mp,
                                 n * geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, base_mode(scale_mode),
-                                st)))
+                                st, bf)))
       return rc;
     timing_end(T_BLOCK_GEMM, st);
     ReconArgs ra = recon_args(geo, ws, L, g0, n, Mp, nullptr, C_ref);
     ra.rowscale = rowup;
+    ra.prod_bf16 = bf;
     const int nblk = recon_blocks(ra);
     timing_begin(T_RECON, st);
     if ((rc = launch_recon(ra, chunk_pattern(T, 2, g0, n), st))) return rc;

@@ -475,6 +475,24 @@ __global__ __launch_bounds__(kThreads) void form_generic_kernel(FormArgs a, int 
 // blocks the product feeds (ascending r for every block, fmaf from +0), and
 // then writes C and/or accumulates (C - Cref)^2 in float64.
 template <int VW>
+__device__ __forceinline__ void recon_load_bf16(const uint16_t* src, float (&m)[VW]) {
+  // bf16 products: each value is its fp32 high half
+  if constexpr (VW % 4 == 0) {
+#pragma unroll
+    for (int v = 0; v < VW; v += 4) {
+      const uint2 t = *reinterpret_cast<const uint2*>(src + v);
+      m[v] = __uint_as_float(t.x << 16);
+      m[v + 1] = __uint_as_float(t.x & 0xffff0000u);
+      m[v + 2] = __uint_as_float(t.y << 16);
+      m[v + 3] = __uint_as_float(t.y & 0xffff0000u);
+    }
+  } else {
+#pragma unroll
+    for (int v = 0; v < VW; ++v) m[v] = __uint_as_float((uint32_t)src[v] << 16);
+  }
+}
+
+template <int VW>
 __device__ __forceinline__ void recon_load(const float* src, float (&m)[VW]) {
   if constexpr (VW % 4 == 0) {
 #pragma unroll
@@ -565,10 +583,21 @@ __device__ __forceinline__ void pin_acc(float (&acc)[NB][VW]) {
     for (int v = 0; v < VW; ++v) asm volatile("" : "+v"(acc[c][v]));
 }
 
-template <int VW>
+template <int VW, bool BF>
 __device__ __forceinline__ void recon_load_buf(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff,
                                                uint32_t soff, float (&m)[VW]) {
-  if constexpr (VW == 4) {
+  if constexpr (BF && VW == 4) {
+    const auto t = __builtin_amdgcn_raw_buffer_load_b64(rsrc, (int)voff, (int)soff, 0);
+    m[0] = __uint_as_float(t[0] << 16);
+    m[1] = __uint_as_float(t[0] & 0xffff0000u);
+    m[2] = __uint_as_float(t[1] << 16);
+    m[3] = __uint_as_float(t[1] & 0xffff0000u);
+  } else if constexpr (BF) {
+#pragma unroll
+    for (int v = 0; v < VW; ++v)
+      m[v] = __uint_as_float(
+          (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rsrc, (int)(voff + 2 * v), (int)soff, 0) << 16);
+  } else if constexpr (VW == 4) {
     const auto t = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)voff, (int)soff, 0);
 #pragma unroll
     for (int v = 0; v < 4; ++v) m[v] = __uint_as_float(t[v]);
@@ -579,7 +608,7 @@ __device__ __forceinline__ void recon_load_buf(__amdgpu_buffer_rsrc_t rsrc, uint
   }
 }
 
-template <class P, int VW>
+template <class P, int VW, bool BF>
 __global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a, int nblk) {
   constexpr int NNZ = P::rowptr[P::R];
   constexpr int GR = 8, NG = (P::R + GR - 1) / GR;
@@ -593,15 +622,16 @@ __global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a, int
   const int bcv = a.Nb / VW;
   const int Ptot = a.Mb * bcv;
   const size_t bsz = (size_t)a.Mb * a.Nb;
-  const uint32_t bbytes = (uint32_t)(bsz * 4);
+  constexpr uint32_t esz = BF ? 2u : 4u;  // bytes per product value
+  const uint32_t bbytes = (uint32_t)(bsz * esz);
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(a.Mprod + (size_t)g * P::R * bsz), (short)0, (int)(P::R * bbytes),
-      0x00020000);
+      const_cast<char*>(reinterpret_cast<const char*>(a.Mprod) + (size_t)g * P::R * bbytes),
+      (short)0, (int)(P::R * bbytes), 0x00020000);
   double esq = 0.0;
   const int p = blk * kThreads + threadIdx.x;
   if (p < Ptot) {
     const int x = p / bcv, z0 = (p - x * bcv) * VW;
-    const uint32_t voff = (uint32_t)(x * a.Nb + z0) * 4u;
+    const uint32_t voff = (uint32_t)(x * a.Nb + z0) * esz;
     float acc[P::NB][VW];
 #pragma unroll
     for (int c = 0; c < P::NB; ++c)
@@ -614,7 +644,7 @@ __global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a, int
         constexpr int j = decltype(jc)::value, r = gi * GR + j;
         if constexpr (r < P::R) {
           if constexpr (P::rowptr[r + 1] > P::rowptr[r])
-            recon_load_buf<VW>(rsrc, voff, (uint32_t)r * bbytes, mb[gi & 1][j]);
+            recon_load_buf<VW, BF>(rsrc, voff, (uint32_t)r * bbytes, mb[gi & 1][j]);
         }
       });
     };
@@ -647,7 +677,7 @@ __global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a, int
   recon_reduce(a, esq, red, g, nblk, blk);
 }
 
-template <int VW>
+template <int VW, bool BF>
 __global__ __launch_bounds__(kThreads) void recon_generic_kernel(ReconArgs a, int nblk) {
   __shared__ double red[kThreads];
   extern __shared__ float lacc[];  // [NC][thread][VW]
@@ -666,12 +696,15 @@ __global__ __launch_bounds__(kThreads) void recon_generic_kernel(ReconArgs a, in
     for (int c = 0; c < NC; ++c)
 #pragma unroll
       for (int v = 0; v < VW; ++v) lacc[((size_t)c * kThreads + threadIdx.x) * VW + v] = 0.0f;
-    const float* mb = a.Mprod + (size_t)g * R * bsz + (size_t)x * a.Nb + z0;
+    const size_t o = (size_t)g * R * bsz + (size_t)x * a.Nb + z0;
     for (int r = 0; r < R; ++r) {
       const int e0 = off[r], e1 = off[r + 1];
       if (e0 == e1) continue;
       float m[VW];
-      recon_load<VW>(mb + (size_t)r * bsz, m);
+      if constexpr (BF)
+        recon_load_bf16<VW>(reinterpret_cast<const uint16_t*>(a.Mprod) + o + (size_t)r * bsz, m);
+      else
+        recon_load<VW>(a.Mprod + o + (size_t)r * bsz, m);
       for (int e = e0; e < e1; ++e) {
         const float w = a.coef[e];
         float* s = lacc + ((size_t)a.idx[e] * kThreads + threadIdx.x) * VW;
@@ -774,7 +807,10 @@ int launch_recon_static(const ReconArgs& a, hipStream_t st) {
   // the kernel gives each thread exactly one position group
   if (recon_width(a) != VW || (long long)nblk * kThreads < (long long)a.Mb * (a.Nb / VW))
     return fail(FM_E_UNSUPPORTED, "reconstruction grid does not cover the block");
-  recon_static_kernel<P, VW><<<nblk * a.G, kThreads, 0, st>>>(a, nblk);
+  if (a.prod_bf16)
+    recon_static_kernel<P, VW, true><<<nblk * a.G, kThreads, 0, st>>>(a, nblk);
+  else
+    recon_static_kernel<P, VW, false><<<nblk * a.G, kThreads, 0, st>>>(a, nblk);
   return launched("recon_static_kernel");
 }
 
@@ -784,17 +820,23 @@ inline int launch_recon_generic(const ReconArgs& a, hipStream_t st) {
   const int grid = nblk * a.G;
   const bool wide = recon_width(a) == 4;
   const size_t shm = (size_t)nc * kThreads * 4 * (wide ? 4 : 1);
-  const void* fn = wide ? reinterpret_cast<const void*>(&recon_generic_kernel<4>)
-                        : reinterpret_cast<const void*>(&recon_generic_kernel<1>);
+  const bool bf = a.prod_bf16 != 0;
+  const void* fn = wide ? (bf ? reinterpret_cast<const void*>(&recon_generic_kernel<4, true>)
+                              : reinterpret_cast<const void*>(&recon_generic_kernel<4, false>))
+                        : (bf ? reinterpret_cast<const void*>(&recon_generic_kernel<1, true>)
+                              : reinterpret_cast<const void*>(&recon_generic_kernel<1, false>));
   if (int rc = hip_check(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
                                              (int)shm),
                          "hipFuncSetAttribute"))
     return rc;
-  if (wide) {
-    recon_generic_kernel<4><<<grid, kThreads, shm, st>>>(a, nblk);
-  } else {
-    recon_generic_kernel<1><<<grid, kThreads, shm, st>>>(a, nblk);
-  }
+  if (wide && bf)
+    recon_generic_kernel<4, true><<<grid, kThreads, shm, st>>>(a, nblk);
+  else if (wide)
+    recon_generic_kernel<4, false><<<grid, kThreads, shm, st>>>(a, nblk);
+  else if (bf)
+    recon_generic_kernel<1, true><<<grid, kThreads, shm, st>>>(a, nblk);
+  else
+    recon_generic_kernel<1, false><<<grid, kThreads, shm, st>>>(a, nblk);
   return launched("recon_generic_kernel");
 }
 

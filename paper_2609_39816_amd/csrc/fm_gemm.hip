@@ -205,7 +205,7 @@ __global__ __launch_bounds__(kThreads) void gemm_tile_kernel(const uint8_t* __re
 // fm_lds_ring.h.  The products are accumulated transposed (operands swapped
 // in the MFMA) so that each lane holds 4 consecutive output columns and the
 // epilogue writes 16-byte stores.
-template <int FMT, int ACC, int SC>
+template <int FMT, int ACC, int SC, bool OB = false>
 __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict__ Tq,
                                                        const uint8_t* __restrict__ Sq,
                                                        const float* __restrict__ dT,
@@ -378,14 +378,23 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
         const uint32_t u = __float_as_uint(x);
         return __uint_as_float((u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u);
       };
+      // OB: stored as bf16 (the values' high halves, 8-byte stores)
+      uint16_t* Mh = reinterpret_cast<uint16_t*>(Mout) + (size_t)b * Mb * Nb;
+      auto hi = [](float x) { return __float_as_uint(x) >> 16; };
       if (m0 + DBM <= Mb && n0 + DBN <= Nb) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float* prow = Mo + (size_t)(r_base + i * 16) * Nb + c_base;
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            *reinterpret_cast<float4*>(prow + j * 16) =
-                make_float4(bf(ofl[i][j][0]), bf(ofl[i][j][1]), bf(ofl[i][j][2]), bf(ofl[i][j][3]));
+          for (int j = 0; j < 4; ++j) {
+            const float v0 = bf(ofl[i][j][0]), v1 = bf(ofl[i][j][1]);
+            const float v2 = bf(ofl[i][j][2]), v3 = bf(ofl[i][j][3]);
+            if constexpr (OB)
+              *reinterpret_cast<uint2*>(Mh + (size_t)(r_base + i * 16) * Nb + c_base + j * 16) =
+                  make_uint2(hi(v0) | (hi(v1) << 16), hi(v2) | (hi(v3) << 16));
+            else
+              *reinterpret_cast<float4*>(Mo + (size_t)(r_base + i * 16) * Nb + c_base + j * 16) =
+                  make_float4(v0, v1, v2, v3);
+          }
         }
         counted = DSTORES;
       } else {
@@ -397,7 +406,10 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
               const int col = c_base + j * 16 + v;
-              if (row < Mb && col < Nb) Mo[(size_t)row * Nb + col] = bf(ofl[i][j][v]);
+              if (row < Mb && col < Nb) {
+                if constexpr (OB) Mh[(size_t)row * Nb + col] = (uint16_t)hi(bf(ofl[i][j][v]));
+                else Mo[(size_t)row * Nb + col] = bf(ofl[i][j][v]);
+              }
             }
         }
       }
@@ -539,7 +551,7 @@ int set_block_product_arith(int a) {
 }
 
 namespace {
-template <int SC>
+template <int SC, bool OB = false>
 int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
                          float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, hipStream_t st) {
   const bool fp8acc = g_block_product_arith == FM_ACC_FP8;
@@ -551,11 +563,11 @@ int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, 
     const int T = (int)total;
     const int grid = (int)std::min<long long>(total, 256);
     if (fmt == FM_E4M3) {
-      if (fp8acc) gemm_dma_kernel<FM_E4M3, 1, SC><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-      else gemm_dma_kernel<FM_E4M3, 0, SC><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+      if (fp8acc) gemm_dma_kernel<FM_E4M3, 1, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+      else gemm_dma_kernel<FM_E4M3, 0, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
     } else {
-      if (fp8acc) gemm_dma_kernel<FM_E5M2, 1, SC><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-      else gemm_dma_kernel<FM_E5M2, 0, SC><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+      if (fp8acc) gemm_dma_kernel<FM_E5M2, 1, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+      else gemm_dma_kernel<FM_E5M2, 0, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
     }
     return launched("gemm_dma_kernel");
   }
@@ -581,12 +593,14 @@ int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, 
 
 int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
                       float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, int scale_mode,
-                      hipStream_t st) {
+                      hipStream_t st, bool out_bf16) {
   if (scale_mode == FM_SCALE_ROWCOL)
     return launch_block_gemm_sc<1>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
   if (scale_mode == FM_SCALE_GROUP) {
     if (Kb % 128 || Nb % 128 || Mb % 4)
       return fail(FM_E_SHAPE, "group scales need Kb, Nb multiples of 128 and Mb of 4");
+    if (out_bf16)
+      return launch_block_gemm_sc<2, true>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
     return launch_block_gemm_sc<2>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
   }
   return launch_block_gemm_sc<0>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);

@@ -144,15 +144,17 @@ int set_block_product_arith(int a);
 // Batched FP8 block products: Mout[b] = ((Tq[b] Sq[b]^T) * dT) * dS with
 // dT = dT[b], dS = dS[b] (FM_SCALE_TENSOR) or dT[b*Mb + x], dS[b*Nb + z]
 // (FM_SCALE_ROWCOL).
+// out_bf16 (group scales only): the products, bf16 values, are stored as
+// bf16 (2 bytes each, uint16_t at Mout) instead of fp32.
 int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
                       float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, int scale_mode,
-                      hipStream_t st);
+                      hipStream_t st, bool out_bf16 = false);
 
 // Reconstruction + error: for gauge g < G, C_g = sum_r w M_{g,r}; if C is not
 // null it is written (G must be 1); if Cref is not null, partial sums of
 // (C - Cref)^2 go to partial[g*nblk + blk].  Returns nblk through *nblk_out.
 struct ReconArgs {
-  const float* Mprod;  // G x R x Mb x Nb
+  const float* Mprod;  // G x R x Mb x Nb (fp32, or bf16 when prod_bf16)
   const int32_t* off;  // G*(R+1)
   const int32_t* idx;
   const float* coef;
@@ -161,6 +163,7 @@ struct ReconArgs {
   const double* Cref;  // optional
   double* partial;     // G x nblk (if Cref)
   const float* rowscale = nullptr;  // optional: output row i*Mb + x times rowscale[i*Mb + x]
+  int prod_bf16 = 0;  // products stored as bf16 (uint16_t at Mprod; group scales)
 };
 // Positions per thread in the reconstruction kernels (4 or 1) and the
 // number of workgroups per gauge (one position group per thread).
