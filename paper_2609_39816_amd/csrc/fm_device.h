@@ -146,11 +146,23 @@ __device__ __forceinline__ void form_load(const FormArgs& a, float (&xv)[NB][VW]
 
 // Index of the maximum / scale that covers entries (x, y0..) of product r
 // of gauge g, for the finer granularities (a.per_row set).
+// The index splits into a part shared by a product's whole tensor,
+// (g R + r) group_span, and a part of the position alone, group_local:
+// the static kernels form the local part once per position group, so the
+// per-product address is one scalar product plus that offset.
+__device__ __forceinline__ uint32_t group_span(const FormArgs& a) {
+  if (a.gran == 1) return (uint32_t)a.br;
+  return (uint32_t)(a.bc / 128) * (uint32_t)(a.gran == 2 ? a.br : a.br / 128);
+}
+
+__device__ __forceinline__ uint32_t group_local(const FormArgs& a, int x, int y0) {
+  if (a.gran == 1) return (uint32_t)x;
+  if (a.gran == 2) return (uint32_t)(y0 >> 7) * (uint32_t)a.br + (uint32_t)x;
+  return (uint32_t)(y0 >> 7) * (uint32_t)(a.br / 128) + (uint32_t)(x >> 7);
+}
+
 __device__ __forceinline__ size_t group_index(const FormArgs& a, int g, int r, int x, int y0) {
-  const size_t gr = (size_t)g * a.R + r;
-  if (a.gran == 1) return gr * a.br + x;
-  const size_t kg = gr * (a.bc / 128) + (y0 >> 7);
-  return a.gran == 2 ? kg * a.br + x : kg * (a.br / 128) + (x >> 7);
+  return ((size_t)g * a.R + r) * group_span(a) + group_local(a, x, y0);
 }
 
 // The B side of the group schedule rounds block sums to bf16 (nearest even)
@@ -295,6 +307,10 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
     const int x = active ? p / bcv : 0;
     const int y0 = active ? (p - x * bcv) * VW : 0;
     const uint32_t voff = active ? (uint32_t)(x * a.bc + y0) : 0x80000000u;
+    // finer granularities: the position's offset among a product's groups
+    [[maybe_unused]] const uint32_t gspan = ROWS ? group_span(a) : 0u;
+    [[maybe_unused]] const uint32_t gloc = ROWS ? group_local(a, x, y0) : 0u;
+    auto gidx = [&](int gg, int rr) { return ((size_t)gg * P::R + rr) * gspan + gloc; };
     float xv[P::NB][VW];
     form_load<P::NB, VW>(a, xv, active, x, y0);
     for (int g = g0; g < g1; ++g) {
@@ -306,13 +322,19 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
       sfor<0, NG>([&](auto gc) {
         constexpr int gi = decltype(gc)::value;
         uint32_t lm[GR];
+        // the group's coefficients and per-tensor scales are read through
+        // an offset the compiler cannot see through, so their scalar loads
+        // stay with the group instead of all going out at the top of the
+        // gauge (which needs more scalar registers than there are)
+        int so = 0;
+        asm volatile("" : "+s"(so));
         // finer scales: the group's scale loads go out before its block
         // sums, so their latency hides under the fused multiply-adds
         [[maybe_unused]] float qv[GR];
         if constexpr (MODE == 1 && ROWS)
           sfor<0, GR>([&](auto jc) {
             constexpr int j = decltype(jc)::value, r = gi * GR + j;
-            if constexpr (r < P::R) qv[j] = ro(a.q)[group_index(a, g, r, x, y0)];
+            if constexpr (r < P::R) qv[j] = ro(a.q)[gidx(g, r)];
           });
         sfor<0, GR>([&](auto jc) {
           constexpr int j = decltype(jc)::value, r = gi * GR + j;
@@ -323,7 +345,7 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
             sfor<P::rowptr[r], P::rowptr[r + 1]>([&](auto ec) {
               constexpr int e = decltype(ec)::value;
               constexpr int b = P::idx[e];
-              const float c = coef[e];
+              const float c = coef[e + so];
 #pragma unroll
               for (int v = 0; v < VW; ++v) acc[v] = __builtin_fmaf(c, xv[b][v], acc[v]);
             });
@@ -334,7 +356,7 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
               for (int v = 0; v < VW; ++v) mx = max(mx, __float_as_uint(acc[v]) & 0x7fffffffu);
               lm[j] = active ? mx : 0u;
             } else {
-              const float q = ROWS ? qv[j] : ro(a.q)[(size_t)g * P::R + r];
+              const float q = ROWS ? qv[j] : ro(a.q)[(size_t)g * P::R + r + so];
               form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, acc, q);
             }
           }
@@ -344,9 +366,26 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
           // spans whole 16-lane DPP rows (bcv a multiple of 16, and 16 VW
           // entries within one group of 128 for the finer granularities)
           // they are reduced first and their last lane folds the result;
-          // otherwise every lane folds its own
+          // the same with 8-lane halves of a row when 8 VW = 128 (the
+          // shifts by 1, 2, 4 leave lanes 7 and 15 with their half's
+          // maximum); otherwise every lane folds its own
           constexpr int NJ = (gi * GR + GR <= P::R) ? GR : P::R - gi * GR;
-          if (bcv % 16 == 0 && (a.gran == 1 || 16 * VW <= 128)) {
+          if (VW == 16 && a.gran != 1 && bcv % 8 == 0) {
+            sfor<0, 3>([&](auto sc) {
+              constexpr int ctl = 0x111 + (1 << decltype(sc)::value) - 1;  // row_shr:1,2,4
+              uint32_t sh[NJ];
+#pragma unroll
+              for (int j = 0; j < NJ; ++j)
+                sh[j] = (uint32_t)__builtin_amdgcn_mov_dpp((int)lm[j], ctl, 0xf, 0xf, true);
+#pragma unroll
+              for (int j = 0; j < NJ; ++j) lm[j] = max(lm[j], sh[j]);
+            });
+            if ((lane & 7) == 7 && active) {
+#pragma unroll
+              for (int j = 0; j < NJ; ++j)
+                if (lm[j]) atomicMax(&a.amax[gidx(g, gi * GR + j)], lm[j]);
+            }
+          } else if (bcv % 16 == 0 && (a.gran == 1 || 16 * VW <= 128)) {
             sfor<0, 4>([&](auto sc) {
               constexpr int ctl = 0x111 + (1 << decltype(sc)::value) - 1;  // row_shr:1,2,4,8
               uint32_t sh[NJ];
@@ -359,12 +398,12 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
             if ((lane & 15) == 15 && active) {
 #pragma unroll
               for (int j = 0; j < NJ; ++j)
-                if (lm[j]) atomicMax(&a.amax[group_index(a, g, gi * GR + j, x, y0)], lm[j]);
+                if (lm[j]) atomicMax(&a.amax[gidx(g, gi * GR + j)], lm[j]);
             }
           } else if (active) {
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
-              if (lm[j]) atomicMax(&a.amax[group_index(a, g, gi * GR + j, x, y0)], lm[j]);
+              if (lm[j]) atomicMax(&a.amax[gidx(g, gi * GR + j)], lm[j]);
           }
         }
         if constexpr (MODE == 0 && !ROWS) {
