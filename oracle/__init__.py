@@ -269,6 +269,26 @@ def block_product_at(Tq, Sq, dT, dS, xs, zs, fmt: int = E4M3) -> np.ndarray:
     return out
 
 
+def lowp_matmul_at(Tq, dT, Sq, dS, W, gm: int, gn: int, xs, zs, fmt: int = E4M3) -> np.ndarray:
+    """The FP8 schedule's output at sampled positions, for shapes where the
+    whole output is too slow to compute here.  From the quantized operands
+    of every product (Tq (R, Mb, Kb), Sq (R, Kb, Nb), per-tensor scales dT,
+    dS (R,)), the block products M_r at the in-block positions (xs[t], zs[t])
+    and, from them, eq. (1)'s reconstruction of every output block at those
+    positions, with the same arithmetic as the whole-output schedule.
+    Returns C (gm, gn, S): C[i, j, t] is output entry
+    (i Mb + xs[t], j Nb + zs[t])."""
+    W = _f32(W)
+    R = W.shape[0]
+    xs = np.ascontiguousarray(xs, np.int32)
+    zs = np.ascontiguousarray(zs, np.int32)
+    S = xs.size
+    Mr = np.empty((R, 1, S), np.float32)
+    for r in range(R):
+        Mr[r, 0] = block_product_at(Tq[r], Sq[r], dT[r], dS[r], xs, zs, fmt)
+    return reconstruct(Mr, W, gm, gn).reshape(gm, gn, S)
+
+
 def reconstruct(Mr, W, gm: int, gn: int) -> np.ndarray:
     Mr = _f32(Mr)
     R, br, bc = Mr.shape

@@ -135,18 +135,21 @@ void orc_fp8_decode_array(const uint8_t* c, int64_t n, int fmt, double* out) {
 void orc_block_sum(const float* X, int rows, int cols, int gr, int gc,
                    const float* c, float* T) {
   int br = rows / gr, bc = cols / gc;
-  for (int x = 0; x < br; ++x) {
-    for (int y = 0; y < bc; ++y) {
-      float acc = 0.0f;
-      for (int p = 0; p < gr; ++p)
-        for (int q = 0; q < gc; ++q) {
-          float u = c[p * gc + q];
-          if (u == 0.0f) continue;
-          acc = fmaf(u, X[(int64_t)(p * br + x) * cols + (q * bc + y)], acc);
-        }
-      T[(int64_t)x * bc + y] = acc;
+  int64_t n = (int64_t)br * bc;
+  for (int64_t e = 0; e < n; ++e) T[e] = 0.0f;
+  /* block by block, so every entry sees the nonzero coefficients in the   */
+  /* order stated above; rows of T are independent                         */
+  for (int p = 0; p < gr; ++p)
+    for (int q = 0; q < gc; ++q) {
+      float u = c[p * gc + q];
+      if (u == 0.0f) continue;
+#pragma omp parallel for schedule(static)
+      for (int x = 0; x < br; ++x) {
+        const float* src = X + (int64_t)(p * br + x) * cols + (int64_t)q * bc;
+        float* dst = T + (int64_t)x * bc;
+        for (int y = 0; y < bc; ++y) dst[y] = fmaf(u, src[y], dst[y]);
+      }
     }
-  }
 }
 
 /* ------------------------------------------------------------------------ */
@@ -166,6 +169,8 @@ static float scale_from_amax(float amax, int fmt, float* r_out) {
 
 float orc_tensor_scale(const float* T, int64_t n, int fmt, float* r_out) {
   float amax = 0.0f;
+  /* the largest magnitude does not depend on the order it is searched in */
+#pragma omp parallel for reduction(max : amax) schedule(static) if (n > 65536)
   for (int64_t i = 0; i < n; ++i) {
     float a = fabsf(T[i]);
     if (a > amax) amax = a;
@@ -176,6 +181,7 @@ float orc_tensor_scale(const float* T, int64_t n, int fmt, float* r_out) {
 float orc_quantize_tensor(const float* T, int64_t n, int fmt, uint8_t* codes) {
   float r;
   float d = orc_tensor_scale(T, n, fmt, &r);
+#pragma omp parallel for schedule(static) if (n > 65536)
   for (int64_t i = 0; i < n; ++i) {
     float y = T[i] * r;
     codes[i] = orc_fp8_encode(y, fmt);

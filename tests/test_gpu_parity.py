@@ -384,3 +384,54 @@ def test_full_size_headline_workload_sampled():
         e_want = oracle.rel_fro(Co, Cref_o)
         say(f"[parity] gauge {gi}: gpu {errs[gi]:.6e} oracle {e_want:.6e}")
         assert abs(errs[gi] / e_want - 1) <= 1e-2
+
+
+FULL_SIZE = [("laderman1_3072x4608x12288_gl512", "e4m3"), ("laderman1_3072x4608x12288_gl512", "e5m2"),
+             ("strassen2_4096x4096x14336_sign512", "e4m3"),
+             ("strassen3_8192x27648x5120_sign512", "e4m3")]
+
+
+@pytest.mark.parametrize("name,fmt", FULL_SIZE)
+def test_full_size_workloads_sampled(name, fmt):
+    """The other full-size workloads, every gauge of the orbit in the launch
+    configuration the benchmark times (32 gauges per chunk).  The oracle
+    checks one gauge's operands bit for bit over the whole tensors, that
+    gauge's output at sampled positions of every output block (the block
+    products at those positions, then the reconstruction), and the float64
+    reference at sampled entries; the orbit's error for that gauge must
+    equal the error of the stand-alone output against the same reference."""
+    w = sy.WORKLOADS[name]
+    say(f"[parity] {name} fmt={fmt} full size")
+    A, B = sy.operands(w)
+    At, Bt = gpu(A), gpu(B)
+    gauges = sy.gauges(w)
+    hips, orcs, levels = schemes_for(w, gauges)
+    Cref = fm.reference_f64(At, Bt)
+    errs = fm.orbit_eval(hips, At, Bt, Cref, levels, FMT[fmt], chunk=32)
+    assert errs.shape == (w.G,) and np.all(np.isfinite(errs)) and np.all(errs > 0)
+    say(f"[parity] orbit done: errors {errs.min():.4e} .. {errs.max():.4e}")
+
+    ri, rj = sy.ratio_sample_positions(w.M, w.N, 48, seed=11)
+    want = np.array([oracle.reference_f64_at(A, B, int(i), int(j)) for i, j in zip(ri, rj)])
+    got = Cref[torch.from_numpy(ri).to(DEV), torch.from_numpy(rj).to(DEV)].cpu().numpy()
+    assert rel(got, want) <= 1e-12
+
+    gi = 1
+    _, _, _, _, tq, sq, dt, ds = check_operands(hips[gi], orcs[gi], levels, A, B, At, Bt, fmt)
+    say(f"[parity] gauge {gi}: operands bit-exact")
+    tabs, dims = oracle.flatten_f32(orcs[gi])
+    gm, gk, gn, R = dims
+    Mb, Nb = w.M // gm, w.N // gn
+    rng = np.random.default_rng(5)
+    xs, zs = rng.integers(0, Mb, 24), rng.integers(0, Nb, 24)
+    C_o = oracle.lowp_matmul_at(tq, dt, sq, ds, tabs[2], gm, gn, xs, zs, OFMT[fmt])
+    C = fm.matmul_lowp(hips[gi], At, Bt, levels, FMT[fmt])
+    rows = (np.arange(gm)[:, None, None] * Mb + xs[None, None, :]).repeat(gn, 1)
+    cols = (np.arange(gn)[None, :, None] * Nb + zs[None, None, :]).repeat(gm, 0)
+    C_s = C[torch.from_numpy(rows.ravel()).to(DEV), torch.from_numpy(cols.ravel()).to(DEV)]
+    r_c = rel(C_s.cpu().numpy(), C_o.ravel())
+    st = fm.error_stats(C, Cref)
+    say(f"[parity] gauge {gi}: sampled C rel {r_c:.3e}; orbit error {errs[gi]:.6e}, "
+        f"stand-alone {st['rel_fro']:.6e}")
+    assert r_c <= 1e-5
+    assert abs(errs[gi] / st["rel_fro"] - 1) <= 1e-6

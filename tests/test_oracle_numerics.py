@@ -457,3 +457,25 @@ def test_levels_equal_kron_power_bit_for_bit():
     s2b = so.kron(schemes.strassen(), schemes.strassen())
     for a, b in ((s2.U, s2b.U), (s2.V, s2b.V), (s2.W, s2b.W)):
         assert np.array_equal(a, b)
+
+
+def test_sampled_outputs_equal_whole_schedule():
+    """The sampled form used at full size gives the whole-output schedule's
+    bits at every sampled position, for a GL-gauged two-level Strassen with
+    ragged in-block positions."""
+    w = sy.scaled(sy.WORKLOADS["strassen1_256_gl64"], 48, 80, 64, G=2)
+    A, B = sy.operands(w)
+    P, Q, S = sy.gauges(w)[1]
+    tabs, dims = oracle.flatten_f32(so.power(so.gauge(schemes.strassen(), P, Q, S), 2))
+    U, V, W = tabs
+    gm, gk, gn, R = dims
+    for fmt in (E4M3, E5M2):
+        full = oracle.lowp_matmul(A, B, tabs, dims, fmt, keep=True)
+        tq, dt = oracle.form_operands(A, gm, gk, U, fmt)
+        sq, ds = oracle.form_operands(B, gk, gn, V, fmt)
+        assert np.array_equal(tq, full["Tq"]) and np.array_equal(sq, full["Sq"])
+        Mb, Nb = A.shape[0] // gm, B.shape[1] // gn
+        xs, zs = np.meshgrid(np.arange(Mb), np.arange(Nb), indexing="ij")
+        got = oracle.lowp_matmul_at(tq, dt, sq, ds, W, gm, gn, xs.ravel(), zs.ravel(), fmt)
+        want = full["C"].reshape(gm, Mb, gn, Nb).transpose(0, 2, 1, 3).reshape(gm, gn, -1)
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
