@@ -88,8 +88,11 @@ def profiled_traffic(cls, workload, steps_work):
     if h.hexdigest() != kv.get("sources_sha256"):
         return None
     rd, wr = float(kv["read_bytes_per_step"]), float(kv["write_bytes_per_step"])
+    launches = float(kv["dispatches_per_step"])
     return dict(bytes_per_step=rd + wr, read_bytes_per_step=rd, write_bytes_per_step=wr,
-                algorithmic_bytes_per_step=steps_work, source=os.path.relpath(path, ROOT))
+                algorithmic_bytes_per_step=steps_work, bytes_per_launch=(rd + wr) / launches,
+                algorithmic_bytes_per_launch=steps_work / launches,
+                source=os.path.relpath(path, ROOT))
 
 
 def gemm_bytes(w, geo, G):
@@ -334,7 +337,8 @@ def main():
                    if dom == "block_gemm" and smode == fm.SCALE_TENSOR else None)
         roof = dict(bound=bound, kernel=dom, achieved=round(achieved, 2), peak=peak, unit=unit,
                     frac=round(achieved / peak, 4),
-                    traffic=traffic["bytes_per_step"] if traffic else None,
+                    traffic=(round(traffic["bytes_per_step"] / (n / args.steps))
+                             if traffic else None),
                     traffic_detail=traffic, peak_basis=peak_note,
                     avg_launch_ms=round(avg_s * 1e3, 4), launches_per_step=n / args.steps)
         log("[bench] per-class kernel time per step (ms): " +
