@@ -186,6 +186,8 @@ void fm_scheme_free(fm_scheme* s);
 /* Bytes of device workspace needed to evaluate G gauged copies of `s`
  * (flattened to `levels`) at M x K times K x N, `chunk` copies at a time
  * (chunk <= 0 means all G at once).  0 if the arguments are invalid.
+ * With chunk < G the size includes a second buffer of block products, so
+ * that fm_orbit_eval can reconstruct one chunk while the next is formed.
  * fm_matmul_lowp and fm_form_operands need fm_workspace_size(s,M,N,K,L,1,1).
  * The workspace must be 256-byte aligned. */
 size_t fm_workspace_size(const fm_scheme* s, int M, int N, int K, int levels,
@@ -265,7 +267,12 @@ int fm_error_stats(const float* C, const double* C_ref, int M, int N,
  * relative Frobenius error against C_ref (M x N float64, device), reduced on
  * the device; rel_fro_out (host, G doubles) receives the errors.  C is not
  * materialized.  Works through the gauges in chunks that fit `ws_bytes`
- * (fm_workspace_size(.., G, chunk)).  Synchronizes. */
+ * (fm_workspace_size(.., G, chunk)): the largest chunk reached by halving G
+ * that fits.  With several chunks and room for two product buffers, each
+ * chunk's reconstruction runs on a second stream of the library's (one per
+ * device, default priority), ordered by events against the caller's stream,
+ * beside the next chunk's formation; the results are the same bits as with
+ * one buffer.  Synchronizes. */
 int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A,
                   const float* B, const double* C_ref, int M, int N, int K,
                   int levels, fm_fmt fmt, double* rel_fro_out,

@@ -7,6 +7,7 @@
 #include <cstring>
 #include <memory>
 #include <string>
+#include <mutex>
 #include <vector>
 
 #include "fm_internal.h"
@@ -107,8 +108,10 @@ int chunk_pattern(const Tables& T, int side, int g0, int n) {
 
 // Workspace layout for G gauges processed `chunk` at a time.
 struct Layout {
-  size_t flags, bt, off[3], idx[3], coef[3], amax, q, d, tq, sq, mprod, partial, errsq, out3,
-      arow, rowup, hg, hgc, hgp, total;
+  // mprod2: a second product buffer when the orbit runs in several chunks
+  // (equal to mprod otherwise)
+  size_t flags, bt, off[3], idx[3], coef[3], amax, q, d, tq, sq, mprod, mprod2, partial, errsq,
+      out3, arow, rowup, hg, hgc, hgp, total;
   int recon_nblk;
 };
 
@@ -141,7 +144,7 @@ int scale_shape_ok(int Mb, int Nb, int Kb, int R, int scale_mode) {
 }
 
 Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
-                   int scale_mode = FM_SCALE_TENSOR) {
+                   int scale_mode = FM_SCALE_TENSOR, bool two_products = false) {
   Layout L{};
   const size_t R = (size_t)g.R;
   size_t o = 0;
@@ -165,6 +168,7 @@ Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
   L.tq = take((size_t)chunk * R * g.Mb * g.Kb);
   L.sq = take((size_t)chunk * R * g.Nb * g.Kb);
   L.mprod = take((size_t)chunk * R * g.Mb * g.Nb * 4);
+  L.mprod2 = two_products ? take((size_t)chunk * R * g.Mb * g.Nb * 4) : L.mprod;
   ReconArgs ra{};
   ra.G = chunk;
   ra.gm = g.gm;
@@ -425,6 +429,78 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
       return rc;
   return FM_OK;
 }
+
+// Two-stream schedule of an orbit in several chunks: the caller's stream
+// forms operands and runs the block products; a second stream of the same
+// (default) priority reconstructs each chunk from its product buffer, so
+// that work runs beside the next chunk's formation.  Events order the two:
+// a chunk's reconstruction waits for its products, products of chunk c wait
+// until chunk c - 2 has been reconstructed from the same buffer, and the
+// caller's stream waits for every reconstruction at the end (also on an
+// early return, so no work is left running on the workspace).
+hipStream_t side_stream(int& rc) {
+  static std::mutex mu;
+  static hipStream_t streams[64] = {};
+  int dev = 0;
+  if ((rc = hip_check(hipGetDevice(&dev), "hipGetDevice"))) return nullptr;
+  if (dev < 0 || dev >= 64) {
+    rc = fail(FM_E_HIP, "device index out of range");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!streams[dev] &&
+      (rc = hip_check(hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking),
+                      "hipStreamCreateWithFlags")))
+    return nullptr;
+  return streams[dev];
+}
+
+struct Pipeline {
+  bool on = false;
+  hipStream_t main = nullptr, side = nullptr;
+  hipEvent_t made[2] = {}, read[2] = {}, done = nullptr;
+
+  int open(hipStream_t st) {
+    int rc = FM_OK;
+    main = st;
+    side = side_stream(rc);
+    if (rc) return rc;
+    for (hipEvent_t* e : {&made[0], &made[1], &read[0], &read[1], &done})
+      if ((rc = hip_check(hipEventCreateWithFlags(e, hipEventDisableTiming), "hipEventCreate")))
+        return rc;
+    on = true;
+    return FM_OK;
+  }
+  // products of the buffer are written: the side stream takes over
+  int hand_over(int buf, hipStream_t& rs) {
+    if (int rc = hip_check(hipEventRecord(made[buf], main), "hipEventRecord")) return rc;
+    if (int rc = hip_check(hipStreamWaitEvent(side, made[buf], 0), "hipStreamWaitEvent")) return rc;
+    rs = side;
+    return FM_OK;
+  }
+  int reconstructed(int buf) {
+    return hip_check(hipEventRecord(read[buf], side), "hipEventRecord");
+  }
+  int wait_reconstructed(int buf) {
+    if (!on) return FM_OK;
+    return hip_check(hipStreamWaitEvent(main, read[buf], 0), "hipStreamWaitEvent");
+  }
+  int join() {
+    if (!on) return FM_OK;
+    on = false;
+    if (int rc = hip_check(hipEventRecord(done, side), "hipEventRecord")) return rc;
+    return hip_check(hipStreamWaitEvent(main, done, 0), "hipStreamWaitEvent");
+  }
+  ~Pipeline() {
+    if (on) {
+      (void)hipEventRecord(done, side);
+      (void)hipStreamWaitEvent(main, done, 0);
+      (void)hipStreamSynchronize(side);
+    }
+    for (hipEvent_t e : {made[0], made[1], read[0], read[1], done})
+      if (e) (void)hipEventDestroy(e);
+  }
+};
 
 ReconArgs recon_args(const Geometry& geo, const char* ws, const Layout& L, int g0, int n,
                      const float* Mp, float* C, const double* Cref) {
@@ -788,7 +864,7 @@ size_t fm_workspace_size_scaled(const fm_scheme* s, int M, int N, int K, int lev
       scale_shape_ok(g.Mb, g.Nb, g.Kb, g.R, scale_mode) != FM_OK)
     return 0;
   if (chunk <= 0 || chunk > G) chunk = G;
-  return make_layout(g, G, chunk, true, scale_mode).total;
+  return make_layout(g, G, chunk, true, scale_mode, chunk < G).total;
 }
 
 size_t fm_workspace_size(const fm_scheme* s, int M, int N, int K, int levels, int G, int chunk) {
@@ -977,14 +1053,22 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   Geometry geo;
   if (int rc = check_geometry(gauged[0], levels, M, N, K, geo)) return rc;
   if (int rc = scale_shape_ok(geo.Mb, geo.Nb, geo.Kb, geo.R, scale_mode)) return rc;
+  // the largest chunk of gauges that fits, halving from G; with several
+  // chunks, two product buffers if they fit (the reconstruction of one chunk
+  // then runs beside the next chunk's formation and block products)
   int chunk = G;
   Layout L = make_layout(geo, G, chunk, true, scale_mode);
   while (chunk > 1 && L.total > ws_bytes) {
     chunk = std::max(1, chunk / 2);
-    L = make_layout(geo, G, chunk, true, scale_mode);
+    L = make_layout(geo, G, chunk, true, scale_mode, true);
+    if (L.total > ws_bytes) L = make_layout(geo, G, chunk, true, scale_mode);
   }
   if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
   hipStream_t st = (hipStream_t)hip_stream;
+  Pipeline pipe;
+  if (L.mprod2 != L.mprod) {
+    if (int rc = pipe.open(st)) return rc;
+  }
   char* ws = (char*)workspace;
   int rc = FM_OK;
   Tables T = make_tables(gauged, G, levels, geo, rc);
@@ -1003,26 +1087,35 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   // group scales return bf16 products: stored as bf16 on the way to the
   // reconstruction (half the bytes, the same values)
   const bool bf = base_mode(scale_mode) == FM_SCALE_GROUP;
-  for (int g0 = 0; g0 < G; g0 += chunk) {
+  for (int g0 = 0, c = 0; g0 < G; g0 += chunk, ++c) {
     const int n = std::min(chunk, G - g0);
+    // products of chunk c go to buffer c mod 2 when there are two
+    const int buf = pipe.on ? (c & 1) : 0;
+    float* Mc = buf ? (float*)(ws + L.mprod2) : Mp;
     if ((rc = form_chunk(geo, Aform, Bt, ws, L, T, g0, n, fmt, scale_mode, Tq, Sq, nullptr,
                          nullptr, st)))
       return rc;
+    // the buffer's previous products (chunk c - 2) must have been read
+    if (c >= 2 && (rc = pipe.wait_reconstructed(buf))) return rc;
     timing_begin(T_BLOCK_GEMM, st);
-    if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)n * geo.R * scales_a(geo, scale_mode), Mp,
+    if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)n * geo.R * scales_a(geo, scale_mode), Mc,
                                 n * geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, base_mode(scale_mode),
                                 st, bf)))
       return rc;
     timing_end(T_BLOCK_GEMM, st);
-    ReconArgs ra = recon_args(geo, ws, L, g0, n, Mp, nullptr, C_ref);
+    hipStream_t rs = st;
+    if (pipe.on && (rc = pipe.hand_over(buf, rs))) return rc;
+    ReconArgs ra = recon_args(geo, ws, L, g0, n, Mc, nullptr, C_ref);
     ra.rowscale = rowup;
     ra.prod_bf16 = bf;
     const int nblk = recon_blocks(ra);
-    timing_begin(T_RECON, st);
-    if ((rc = launch_recon(ra, chunk_pattern(T, 2, g0, n), st))) return rc;
-    timing_end(T_RECON, st);
-    if ((rc = launch_reduce_rows((double*)(ws + L.partial), nblk, n, errsq + g0, st))) return rc;
+    timing_begin(T_RECON, rs);
+    if ((rc = launch_recon(ra, chunk_pattern(T, 2, g0, n), rs))) return rc;
+    timing_end(T_RECON, rs);
+    if ((rc = launch_reduce_rows((double*)(ws + L.partial), nblk, n, errsq + g0, rs))) return rc;
+    if (pipe.on && (rc = pipe.reconstructed(buf))) return rc;
   }
+  if ((rc = pipe.join())) return rc;
   // sum of squares of the reference (err_sq of a zero output)
   {
     const size_t nel = (size_t)M * N;

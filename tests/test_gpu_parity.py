@@ -356,10 +356,15 @@ def test_chunked_orbit_equals_single_launch_and_is_deterministic():
     Cref = fm.reference_f64(At, Bt)
     e1 = fm.orbit_eval(hips, At, Bt, Cref, levels)
     e2 = fm.orbit_eval(hips, At, Bt, Cref, levels)
-    ws = fm.workspace(fm.workspace_size(hips[0], w.M, w.N, w.K, levels, len(hips), 5))
-    e3 = fm.orbit_eval(hips, At, Bt, Cref, levels, ws=ws)
     assert np.array_equal(e1.view(np.uint64), e2.view(np.uint64))
-    assert np.array_equal(e1.view(np.uint64), e3.view(np.uint64))
+    # chunks of 6 and 3 (halving 24) with two product buffers: the
+    # reconstruction runs on the second stream and each buffer is reused;
+    # a workspace sized for chunks of 5 takes chunks of 6 with one buffer,
+    # one sized for 7 (not reached by halving) chunks of 6 with two
+    for ch in (6, 3, 5, 7):
+        ws = fm.workspace(fm.workspace_size(hips[0], w.M, w.N, w.K, levels, len(hips), ch))
+        e3 = fm.orbit_eval(hips, At, Bt, Cref, levels, ws=ws)
+        assert np.array_equal(e1.view(np.uint64), e3.view(np.uint64)), ch
     c1 = fm.matmul_lowp(hips[3], At, Bt, levels).cpu().numpy()
     c2 = fm.matmul_lowp(hips[3], At, Bt, levels).cpu().numpy()
     assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
