@@ -108,6 +108,12 @@ __device__ __forceinline__ void sfor(F&& f) {
   if constexpr (E > B) sfor_impl<B>(f, std::make_integer_sequence<int, E - B>{});
 }
 
+// Cache policy of the streams written or read once per launch (the FP8
+// codes, the block products on their way to the reconstruction): the
+// non-temporal bit of the buffer instructions' cache-policy operand.
+constexpr int kStreamOut = 2;
+constexpr int kStreamIn = 2;
+
 // ------------------------------------------------------- operand formation
 // A thread owns VW consecutive positions (x, y0..y0+VW-1) of the block-sum
 // tensors and reads the matching entries of every grid block once per
@@ -277,18 +283,18 @@ __device__ __forceinline__ void form_encode_store(__amdgpu_buffer_rsrc_t rsrc, u
     }
   }
   if constexpr (VW == 2) {
-    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)(w[0] & 0xffffu), rsrc, (int)voff, (int)soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b16((unsigned short)(w[0] & 0xffffu), rsrc, (int)voff, (int)soff, kStreamOut);
   } else if constexpr (VW == 4) {
-    __builtin_amdgcn_raw_buffer_store_b32(w[0], rsrc, (int)voff, (int)soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b32(w[0], rsrc, (int)voff, (int)soff, kStreamOut);
   } else if constexpr (VW == 8) {
     __builtin_amdgcn_raw_buffer_store_b64((__attribute__((ext_vector_type(2))) unsigned){w[0], w[1]},
-                                          rsrc, (int)voff, (int)soff, 0);
+                                          rsrc, (int)voff, (int)soff, kStreamOut);
   } else {
 #pragma unroll
     for (int t = 0; t < VW / 4; t += 4)
       __builtin_amdgcn_raw_buffer_store_b128(
           (__attribute__((ext_vector_type(4))) unsigned){w[t], w[t + 1], w[t + 2], w[t + 3]}, rsrc,
-          (int)(voff + 4 * t), (int)soff, 0);
+          (int)(voff + 4 * t), (int)soff, kStreamOut);
   }
 }
 
@@ -626,7 +632,7 @@ template <int VW, bool BF>
 __device__ __forceinline__ void recon_load_buf(__amdgpu_buffer_rsrc_t rsrc, uint32_t voff,
                                                uint32_t soff, float (&m)[VW]) {
   if constexpr (BF && VW == 4) {
-    const auto t = __builtin_amdgcn_raw_buffer_load_b64(rsrc, (int)voff, (int)soff, 0);
+    const auto t = __builtin_amdgcn_raw_buffer_load_b64(rsrc, (int)voff, (int)soff, kStreamIn);
     m[0] = __uint_as_float(t[0] << 16);
     m[1] = __uint_as_float(t[0] & 0xffff0000u);
     m[2] = __uint_as_float(t[1] << 16);
@@ -635,15 +641,15 @@ __device__ __forceinline__ void recon_load_buf(__amdgpu_buffer_rsrc_t rsrc, uint
 #pragma unroll
     for (int v = 0; v < VW; ++v)
       m[v] = __uint_as_float(
-          (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rsrc, (int)(voff + 2 * v), (int)soff, 0) << 16);
+          (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rsrc, (int)(voff + 2 * v), (int)soff, kStreamIn) << 16);
   } else if constexpr (VW == 4) {
-    const auto t = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)voff, (int)soff, 0);
+    const auto t = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)voff, (int)soff, kStreamIn);
 #pragma unroll
     for (int v = 0; v < 4; ++v) m[v] = __uint_as_float(t[v]);
   } else {
 #pragma unroll
     for (int v = 0; v < VW; ++v)
-      m[v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, (int)(voff + 4 * v), (int)soff, 0));
+      m[v] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsrc, (int)(voff + 4 * v), (int)soff, kStreamIn));
   }
 }
 
