@@ -108,11 +108,23 @@ int chunk_pattern(const Tables& T, int side, int g0, int n) {
 
 // Workspace layout for G gauges processed `chunk` at a time.
 struct Layout {
-  // mprod2: a second product buffer when the orbit runs in several chunks
-  // (equal to mprod otherwise)
-  size_t flags, bt, off[3], idx[3], coef[3], amax, q, d, tq, sq, mprod, mprod2, partial, errsq,
-      out3, arow, rowup, hg, hgc, hgp, total;
+  // *2: a second set of a chunk's maxima, scales and block products when the
+  // orbit runs in several chunks (equal to the first set otherwise)
+  size_t flags, bt, off[3], idx[3], coef[3], amax, q, d, tq, sq, mprod, amax2, q2, d2, mprod2,
+      partial, errsq, out3, arow, rowup, hg, hgc, hgp, total;
   int recon_nblk;
+  bool two_sets() const { return mprod2 != mprod; }
+  // the layout with set k in the first slots
+  Layout set(int k) const {
+    Layout o = *this;
+    if (k) {
+      o.amax = amax2;
+      o.q = q2;
+      o.d = d2;
+      o.mprod = mprod2;
+    }
+    return o;
+  }
 };
 
 // Scale-mode word: the granularity in the low byte, repair flags above it
@@ -144,7 +156,7 @@ int scale_shape_ok(int Mb, int Nb, int Kb, int R, int scale_mode) {
 }
 
 Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
-                   int scale_mode = FM_SCALE_TENSOR, bool two_products = false) {
+                   int scale_mode = FM_SCALE_TENSOR, bool two_sets = false) {
   Layout L{};
   const size_t R = (size_t)g.R;
   size_t o = 0;
@@ -168,7 +180,17 @@ Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
   L.tq = take((size_t)chunk * R * g.Mb * g.Kb);
   L.sq = take((size_t)chunk * R * g.Nb * g.Kb);
   L.mprod = take((size_t)chunk * R * g.Mb * g.Nb * 4);
-  L.mprod2 = two_products ? take((size_t)chunk * R * g.Mb * g.Nb * 4) : L.mprod;
+  if (two_sets) {
+    L.amax2 = take(nsc * 4);
+    L.q2 = take(nsc * 4);
+    L.d2 = take(nsc * 4 + 16);
+    L.mprod2 = take((size_t)chunk * R * g.Mb * g.Nb * 4);
+  } else {
+    L.amax2 = L.amax;
+    L.q2 = L.q;
+    L.d2 = L.d;
+    L.mprod2 = L.mprod;
+  }
   ReconArgs ra{};
   ra.G = chunk;
   ra.gm = g.gm;
@@ -368,6 +390,63 @@ int upload_tables(const Tables& T, char* ws, const Layout& L, hipStream_t st) {
 }
 
 // Operand formation for gauges [g0, g0 + n) of the uploaded tables.
+// Formation arguments of both sides of the gauges [g0, g0 + n) with one
+// scale per block-sum tensor, maxima and scales in the first set of L.
+void tensor_form_args(const Geometry& geo, const float* A, const float* Bt, char* ws,
+                      const Layout& L, int g0, int n, int fmt, uint8_t* Tq, uint8_t* Sq,
+                      FormArgs& fa, FormArgs& fb) {
+  const int R = geo.R;
+  const size_t na = (size_t)n * R;
+  uint32_t* amax = (uint32_t*)(ws + L.amax);
+  float* q = (float*)(ws + L.q);
+  auto off = [&](int k) { return (const int32_t*)(ws + L.off[k]) + (size_t)g0 * (R + 1); };
+  auto idx = [&](int k) { return (const int32_t*)(ws + L.idx[k]); };
+  auto coef = [&](int k) { return (const float*)(ws + L.coef[k]); };
+  fa = FormArgs{A,    geo.M, geo.K, geo.gm, geo.gk, geo.Mb, geo.Kb, off(0), idx(0), coef(0), R, n,
+                amax, q,     Tq,    fmt,    0,      1};
+  fb = FormArgs{Bt,       geo.N,    geo.K, geo.gn, geo.gk, geo.Nb, geo.Kb, off(1), idx(1), coef(1),
+                R,        n,        amax + na, q + na, Sq, fmt, 0, 1};
+}
+
+// Per-tensor scales of an orbit in several chunks: the FP8 codes of chunk c
+// and the maxima of chunk c + 1 are formed in one pass per side (the merged
+// kernel, when both chunks are of one kernel family; otherwise the two passes
+// separately), then the scales of chunk c + 1 (the other set of L).  The
+// maxima and scales of chunk 0 are formed first, by the caller.
+int form_codes_and_next_maxima(const Geometry& geo, const float* A, const float* Bt, char* ws,
+                               const Layout& L, const Tables& T, int c, int g0, int n, int n1,
+                               int fmt, uint8_t* Tq, uint8_t* Sq, hipStream_t st) {
+  FormArgs qa, qb, ma, mb;
+  tensor_form_args(geo, A, Bt, ws, L.set(c & 1), g0, n, fmt, Tq, Sq, qa, qb);
+  const Layout Ln = L.set((c + 1) & 1);
+  if (n1 > 0) {
+    tensor_form_args(geo, A, Bt, ws, Ln, g0 + n, n1, fmt, Tq, Sq, ma, mb);
+    if (int rc = launch_fill_u32(ma.amax, (size_t)2 * n1 * geo.R, 0u, st)) return rc;
+  }
+  for (int side = 0; side < 2; ++side) {
+    const int pq = chunk_pattern(T, side, g0, n);
+    const int pm = n1 > 0 ? chunk_pattern(T, side, g0 + n, n1) : -1;
+    const FormArgs& aq = side ? qb : qa;
+    const FormArgs& am = side ? mb : ma;
+    timing_begin(T_FORM_QUANT, st);
+    const bool merge = n1 > 0 && pq >= 0 && pq == pm;
+    int rc = merge ? launch_form_merged(aq, am, pq, side, st) : 1;
+    const bool merged = merge && rc != 1;
+    if (!merged) rc = launch_form(aq, 1, pq, side, st);
+    if (rc) return rc;
+    timing_end(T_FORM_QUANT, st);
+    if (n1 > 0 && !merged) {
+      timing_begin(T_FORM_AMAX, st);
+      if ((rc = launch_form(am, 0, pm, side, st))) return rc;
+      timing_end(T_FORM_AMAX, st);
+    }
+  }
+  if (n1 > 0)
+    return launch_scales(ma.amax, (float*)(ws + Ln.q), (float*)(ws + Ln.d), 2 * n1 * geo.R, fmt,
+                         (uint32_t*)(ws + L.flags), st);
+  return FM_OK;
+}
+
 int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, const Layout& L,
                const Tables& T, int g0, int n, int fmt, int scale_mode, uint8_t* Tq, uint8_t* Sq,
                float* dT, float* dS, hipStream_t st) {
@@ -1054,8 +1133,9 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   if (int rc = check_geometry(gauged[0], levels, M, N, K, geo)) return rc;
   if (int rc = scale_shape_ok(geo.Mb, geo.Nb, geo.Kb, geo.R, scale_mode)) return rc;
   // the largest chunk of gauges that fits, halving from G; with several
-  // chunks, two product buffers if they fit (the reconstruction of one chunk
-  // then runs beside the next chunk's formation and block products)
+  // chunks, two sets of maxima, scales and block products if they fit (the
+  // reconstruction of one chunk then runs beside the next chunk's formation,
+  // and per-tensor maxima are formed a chunk ahead)
   int chunk = G;
   Layout L = make_layout(geo, G, chunk, true, scale_mode);
   while (chunk > 1 && L.total > ws_bytes) {
@@ -1066,7 +1146,7 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
   hipStream_t st = (hipStream_t)hip_stream;
   Pipeline pipe;
-  if (L.mprod2 != L.mprod) {
+  if (L.two_sets()) {
     if (int rc = pipe.open(st)) return rc;
   }
   char* ws = (char*)workspace;
@@ -1080,21 +1160,45 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   uint8_t* Tq = (uint8_t*)(ws + L.tq);
   uint8_t* Sq = (uint8_t*)(ws + L.sq);
   float* Mp = (float*)(ws + L.mprod);
-  const float* dd = (const float*)(ws + L.d);
   double* errsq = (double*)(ws + L.errsq);
   const float *Aform, *rowup;
   if ((rc = prepare_repairs(geo, T, ws, L, scale_mode, A, Aform, rowup, st))) return rc;
   // group scales return bf16 products: stored as bf16 on the way to the
   // reconstruction (half the bytes, the same values)
   const bool bf = base_mode(scale_mode) == FM_SCALE_GROUP;
+  // per-tensor scales over several chunks: each chunk's codes are formed
+  // together with the next chunk's maxima (chunk 0's maxima first)
+  const bool fuse = L.two_sets() && scale_mode == FM_SCALE_TENSOR;
+  if (fuse) {
+    const int n0 = std::min(chunk, G);
+    FormArgs fa, fb;
+    tensor_form_args(geo, Aform, Bt, ws, L, 0, n0, fmt, Tq, Sq, fa, fb);
+    if ((rc = launch_fill_u32(fa.amax, (size_t)2 * n0 * geo.R, 0u, st))) return rc;
+    for (int side = 0; side < 2; ++side) {
+      timing_begin(T_FORM_AMAX, st);
+      if ((rc = launch_form(side ? fb : fa, 0, chunk_pattern(T, side, 0, n0), side, st))) return rc;
+      timing_end(T_FORM_AMAX, st);
+    }
+    if ((rc = launch_scales(fa.amax, (float*)(ws + L.q), (float*)(ws + L.d), 2 * n0 * geo.R, fmt,
+                            (uint32_t*)(ws + L.flags), st)))
+      return rc;
+  }
   for (int g0 = 0, c = 0; g0 < G; g0 += chunk, ++c) {
     const int n = std::min(chunk, G - g0);
-    // products of chunk c go to buffer c mod 2 when there are two
-    const int buf = pipe.on ? (c & 1) : 0;
-    float* Mc = buf ? (float*)(ws + L.mprod2) : Mp;
-    if ((rc = form_chunk(geo, Aform, Bt, ws, L, T, g0, n, fmt, scale_mode, Tq, Sq, nullptr,
-                         nullptr, st)))
+    // chunk c uses set c mod 2 (maxima, scales, products) when there are two
+    const int buf = L.two_sets() ? (c & 1) : 0;
+    const Layout Lc = L.set(buf);
+    float* Mc = (float*)(ws + Lc.mprod);
+    const float* dd = (const float*)(ws + Lc.d);
+    if (fuse) {
+      const int n1 = std::min(chunk, std::max(0, G - g0 - n));
+      if ((rc = form_codes_and_next_maxima(geo, Aform, Bt, ws, L, T, c, g0, n, n1, fmt, Tq, Sq,
+                                           st)))
+        return rc;
+    } else if ((rc = form_chunk(geo, Aform, Bt, ws, Lc, T, g0, n, fmt, scale_mode, Tq, Sq,
+                                nullptr, nullptr, st))) {
       return rc;
+    }
     // the buffer's previous products (chunk c - 2) must have been read
     if (c >= 2 && (rc = pipe.wait_reconstructed(buf))) return rc;
     timing_begin(T_BLOCK_GEMM, st);
@@ -1105,7 +1209,7 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
     timing_end(T_BLOCK_GEMM, st);
     hipStream_t rs = st;
     if (pipe.on && (rc = pipe.hand_over(buf, rs))) return rc;
-    ReconArgs ra = recon_args(geo, ws, L, g0, n, Mc, nullptr, C_ref);
+    ReconArgs ra = recon_args(geo, ws, Lc, g0, n, Mc, nullptr, C_ref);
     ra.rowscale = rowup;
     ra.prod_bf16 = bf;
     const int nblk = recon_blocks(ra);

@@ -298,27 +298,21 @@ __device__ __forceinline__ void form_encode_store(__amdgpu_buffer_rsrc_t rsrc, u
   }
 }
 
+// Gauges g0 <= g < g1 of a at one position group (operand values xv); mode
+// 0 keeps its maxima in the LDS slots of gauge g - g0.
 template <class P, int VW, int MODE, int FMT, bool ROWS>
-__device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uint32_t* smax) {
+__device__ __forceinline__ void form_static_gauges(const FormArgs& a, int g0, int g1,
+                                                   const float (&xv)[P::NB][VW], bool active,
+                                                   int x, int y0, uint32_t voff, uint32_t* smax) {
   constexpr int GR = 8, NG = (P::R + GR - 1) / GR;
-  const int bcv = a.bc / VW;
-  const int Ptot = a.br * bcv;
-  const int g0 = blockIdx.y * gpb;
-  const int g1 = min(a.G, g0 + gpb);
   const int lane = threadIdx.x & 63;
   const uint32_t bsz = (uint32_t)a.br * (uint32_t)a.bc;
-  for (int base = blockIdx.x * kThreads; base < Ptot; base += gridDim.x * kThreads) {
-    const int p = base + threadIdx.x;
-    const bool active = p < Ptot;
-    const int x = active ? p / bcv : 0;
-    const int y0 = active ? (p - x * bcv) * VW : 0;
-    const uint32_t voff = active ? (uint32_t)(x * a.bc + y0) : 0x80000000u;
+  [[maybe_unused]] const int bcv = a.bc / VW;
+  {
     // finer granularities: the position's offset among a product's groups
     [[maybe_unused]] const uint32_t gspan = ROWS ? group_span(a) : 0u;
     [[maybe_unused]] const uint32_t gloc = ROWS ? group_local(a, x, y0) : 0u;
     auto gidx = [&](int gg, int rr) { return ((size_t)gg * P::R + rr) * gspan + gloc; };
-    float xv[P::NB][VW];
-    form_load<P::NB, VW>(a, xv, active, x, y0);
     for (int g = g0; g < g1; ++g) {
       const auto coef = ro(a.coef) + ro(a.off)[(size_t)g * (P::R + 1)];
       __amdgpu_buffer_rsrc_t rsrc;
@@ -439,6 +433,25 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
   }
 }
 
+
+template <class P, int VW, int MODE, int FMT, bool ROWS>
+__device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uint32_t* smax) {
+  const int bcv = a.bc / VW;
+  const int Ptot = a.br * bcv;
+  const int g0 = blockIdx.y * gpb;
+  const int g1 = min(a.G, g0 + gpb);
+  for (int base = blockIdx.x * kThreads; base < Ptot; base += gridDim.x * kThreads) {
+    const int p = base + threadIdx.x;
+    const bool active = p < Ptot;
+    const int x = active ? p / bcv : 0;
+    const int y0 = active ? (p - x * bcv) * VW : 0;
+    const uint32_t voff = active ? (uint32_t)(x * a.bc + y0) : 0x80000000u;
+    float xv[P::NB][VW];
+    form_load<P::NB, VW>(a, xv, active, x, y0);
+    form_static_gauges<P, VW, MODE, FMT, ROWS>(a, g0, g1, xv, active, x, y0, voff, smax);
+  }
+}
+
 template <class P, int VW, int MODE, bool ROWS>
 __global__ __launch_bounds__(kThreads) void form_static_kernel(FormArgs a, int gpb) {
   extern __shared__ uint32_t smax[];  // mode 0: [gauge][product][wave * 4 + row]
@@ -461,6 +474,44 @@ __global__ __launch_bounds__(kThreads) void form_static_kernel(FormArgs a, int g
   } else {
     if (a.fmt == FM_E4M3) form_static_body<P, VW, 1, FM_E4M3, ROWS>(a, gpb, smax);
     else form_static_body<P, VW, 1, FM_E5M2, ROWS>(a, gpb, smax);
+  }
+}
+
+// One operand side of two consecutive chunks of an orbit in one pass: the
+// FP8 codes of chunk c (aq, mode 1, scales known) and the per-tensor maxima
+// of chunk c + 1 (am, mode 0), from one load of the operand blocks per
+// position group.  The encoding is bound by its code stores and the maxima
+// by vector arithmetic, so each fills the other's idle time.  Gauges split
+// over grid.y as in the separate kernels: slice y encodes gauges
+// [y gpbq, (y + 1) gpbq) of aq and folds the maxima of [y gpbm, ..) of am.
+template <class P, int VW, int FMT>
+__global__ __launch_bounds__(kThreads) void form_merged_kernel(FormArgs aq, FormArgs am, int gpbq,
+                                                               int gpbm) {
+  extern __shared__ uint32_t smax[];  // am's [gauge][product][wave * 4 + row]
+  const int g0q = blockIdx.y * gpbq, g1q = min(aq.G, g0q + gpbq);
+  const int g0m = blockIdx.y * gpbm, g1m = min(am.G, g0m + gpbm);
+  for (int i = threadIdx.x; i < gpbm * P::R * 16; i += kThreads) smax[i] = 0u;
+  __syncthreads();
+  const int bcv = aq.bc / VW;
+  const int Ptot = aq.br * bcv;
+  for (int base = blockIdx.x * kThreads; base < Ptot; base += gridDim.x * kThreads) {
+    const int p = base + threadIdx.x;
+    const bool active = p < Ptot;
+    const int x = active ? p / bcv : 0;
+    const int y0 = active ? (p - x * bcv) * VW : 0;
+    const uint32_t voff = active ? (uint32_t)(x * aq.bc + y0) : 0x80000000u;
+    float xv[P::NB][VW];
+    form_load<P::NB, VW>(aq, xv, active, x, y0);
+    form_static_gauges<P, VW, 1, FMT, false>(aq, g0q, g1q, xv, active, x, y0, voff, smax);
+    form_static_gauges<P, VW, 0, FM_E4M3, false>(am, g0m, g1m, xv, active, x, y0, voff, smax);
+  }
+  __syncthreads();
+  const int n = max(0, g1m - g0m) * P::R;
+  for (int k = threadIdx.x; k < n; k += kThreads) {
+    uint32_t m = 0u;
+#pragma unroll
+    for (int t = 0; t < 16; ++t) m = max(m, smax[k * 16 + t]);
+    if (m) atomicMax(&am.amax[(size_t)g0m * P::R + k], m);
   }
 }
 
@@ -808,6 +859,24 @@ int launch_form_static(const FormArgs& a, hipStream_t st) {
   return launched("form_static_kernel");
 }
 
+// The merged pass (form_merged_kernel): the encoding's grid, the maxima's
+// gauges spread over the same slices.  Returns 1 if the maxima's LDS slots
+// would not fit (the caller then launches the two passes separately).
+template <class P>
+int launch_form_merged(const FormArgs& aq, const FormArgs& am, hipStream_t st) {
+  constexpr int VW = static_vw<P>();
+  int gpbq;
+  const dim3 grid = form_grid(aq, VW, aq.G, gpbq);
+  const int gpbm = (am.G + (int)grid.y - 1) / (int)grid.y;
+  if (gpbm * P::R * 16 > 12288) return 1;
+  const size_t shm = (size_t)gpbm * P::R * 16 * 4;
+  if (aq.fmt == FM_E4M3)
+    form_merged_kernel<P, VW, FM_E4M3><<<grid, kThreads, shm, st>>>(aq, am, gpbq, gpbm);
+  else
+    form_merged_kernel<P, VW, FM_E5M2><<<grid, kThreads, shm, st>>>(aq, am, gpbq, gpbm);
+  return launched("form_merged_kernel");
+}
+
 template <class P>
 bool static_ok(const FormArgs& a) {
   constexpr int VW = static_vw<P>();
@@ -893,6 +962,8 @@ inline int launch_recon_generic(const ReconArgs& a, hipStream_t st) {
 // then uses the generic kernels), else FM_OK or an error code.
 #define FM_DECLARE_FAMILY(P)                                                  \
   int form_family_##P(const FormArgs& a, int mode, int side, hipStream_t st); \
+  int form_merged_family_##P(const FormArgs& aq, const FormArgs& am, int side,  \
+                             hipStream_t st);                                  \
   int recon_family_##P(const ReconArgs& a, hipStream_t st);
 FM_PATTERN_FAMILIES(FM_DECLARE_FAMILY)
 #undef FM_DECLARE_FAMILY
@@ -908,6 +979,17 @@ FM_PATTERN_FAMILIES(FM_DECLARE_FAMILY)
     if (!static_ok<pat::P::B>(a)) return 1;                                          \
     return mode ? launch_form_static<pat::P::B, 1>(a, st)                            \
                 : launch_form_static<pat::P::B, 0>(a, st);                           \
+  }                                                                                  \
+  int form_merged_family_##P(const FormArgs& aq, const FormArgs& am, int side,       \
+                             hipStream_t st) {                                       \
+    using namespace dev;                                                             \
+    if (aq.per_row || am.per_row) return 1;                                          \
+    if (side == 0) {                                                                 \
+      if (!static_ok<pat::P::A>(aq) || !static_ok<pat::P::A>(am)) return 1;          \
+      return launch_form_merged<pat::P::A>(aq, am, st);                              \
+    }                                                                                \
+    if (!static_ok<pat::P::B>(aq) || !static_ok<pat::P::B>(am)) return 1;            \
+    return launch_form_merged<pat::P::B>(aq, am, st);                                \
   }                                                                                  \
   int recon_family_##P(const ReconArgs& a, hipStream_t st) {                         \
     using namespace dev;                                                             \

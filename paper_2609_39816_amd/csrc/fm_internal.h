@@ -123,6 +123,12 @@ struct FormArgs {
 // pattern: family id from match_pattern (side A or B), or -1 for the
 // generic kernel.
 int launch_form(const FormArgs& a, int mode, int pattern, int side, hipStream_t st);
+// One side's FP8 codes of one chunk (aq, scales known) and per-tensor maxima
+// of the next (am) in one pass; both of the family `pattern` (no generic
+// form).  Returns 1, launching nothing, when the pair does not fit the
+// merged kernel.
+int launch_form_merged(const FormArgs& aq, const FormArgs& am, int pattern, int side,
+                       hipStream_t st);
 // Repairs: row exponents of A (As = A 2^-k row by row, up = 2^k), and the
 // joint rounding of B's bf16 block sums (a is B's FormArgs with gran 3;
 // codes into a.codes; qS, dS the block scales; H of every gauge in

@@ -410,6 +410,17 @@ int launch_form(const FormArgs& a, int mode, int pattern, int side, hipStream_t 
   return launch_form_generic(a, mode, st);
 }
 
+int launch_form_merged(const FormArgs& aq, const FormArgs& am, int pattern, int side,
+                       hipStream_t st) {
+  int id = 0;
+#define FM_MERGED_CASE(P)                                            \
+  if (pattern == id) return form_merged_family_##P(aq, am, side, st); \
+  ++id;
+  FM_PATTERN_FAMILIES(FM_MERGED_CASE)
+#undef FM_MERGED_CASE
+  return 1;
+}
+
 int launch_scales(const uint32_t* amax, float* q, float* d, int n, int fmt, uint32_t* flag,
                   hipStream_t st) {
   const float fmax = fmt == FM_E4M3 ? 448.0f : 57344.0f;
