@@ -860,15 +860,24 @@ int launch_form_static(const FormArgs& a, hipStream_t st) {
 }
 
 // The merged pass (form_merged_kernel): the encoding's grid, the maxima's
-// gauges spread over the same slices.  Returns 1 if the maxima's LDS slots
-// would not fit (the caller then launches the two passes separately).
+// gauges spread over the same slices, with more slices when a slice's
+// maxima would not fit their LDS slots (at most 48 KB, as the separate
+// maxima pass).
 template <class P>
 int launch_form_merged(const FormArgs& aq, const FormArgs& am, hipStream_t st) {
   constexpr int VW = static_vw<P>();
+  constexpr int max_gpbm = 12288 / (P::R * 16);
+  if (max_gpbm < 1) return 1;
   int gpbq;
-  const dim3 grid = form_grid(aq, VW, aq.G, gpbq);
+  dim3 grid = form_grid(aq, VW, aq.G, gpbq);
+  if ((am.G + (int)grid.y - 1) / (int)grid.y > max_gpbm) {
+    const int gy = (am.G + max_gpbm - 1) / max_gpbm;
+    gpbq = (aq.G + gy - 1) / gy;
+    grid.y = (unsigned)std::max(gy, (aq.G + gpbq - 1) / gpbq);
+    if ((long long)grid.x * grid.y > 4 * 2048) grid.x = (unsigned)std::max(1, 4 * 2048 / (int)grid.y);
+  }
   const int gpbm = (am.G + (int)grid.y - 1) / (int)grid.y;
-  if (gpbm * P::R * 16 > 12288) return 1;
+  if (gpbm > max_gpbm || (long long)gpbq * grid.y < aq.G) return 1;
   const size_t shm = (size_t)gpbm * P::R * 16 * 4;
   if (aq.fmt == FM_E4M3)
     form_merged_kernel<P, VW, FM_E4M3><<<grid, kThreads, shm, st>>>(aq, am, gpbq, gpbm);

@@ -368,6 +368,20 @@ def test_chunked_orbit_equals_single_launch_and_is_deterministic():
     c1 = fm.matmul_lowp(hips[3], At, Bt, levels).cpu().numpy()
     c2 = fm.matmul_lowp(hips[3], At, Bt, levels).cpu().numpy()
     assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
+    # chunks whose kernel families differ (the identity's sparse Strassen
+    # beside dense GL-gauged copies, and a chunk mixing both, formed by the
+    # generic kernels): the codes of one chunk and the maxima of the next
+    # are then formed in separate passes; same bits as one chunk
+    wg = sy.scaled(sy.WORKLOADS["strassen1_256_gl64"], 192, 256, 160, G=11)
+    A, B = sy.operands(wg)
+    At, Bt = gpu(A), gpu(B)
+    hips, _, levels = schemes_for(wg, [sy.identity_gauge(wg)] + sy.gauges(wg))
+    Cref = fm.reference_f64(At, Bt)
+    e1 = fm.orbit_eval(hips, At, Bt, Cref, levels)
+    for ch in (1, 3):
+        ws = fm.workspace(fm.workspace_size(hips[0], wg.M, wg.N, wg.K, levels, len(hips), ch))
+        e3 = fm.orbit_eval(hips, At, Bt, Cref, levels, ws=ws)
+        assert np.array_equal(e1.view(np.uint64), e3.view(np.uint64)), ch
 
 
 def test_full_size_headline_workload_sampled():
