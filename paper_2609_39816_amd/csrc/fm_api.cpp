@@ -1201,10 +1201,17 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
     }
     // the buffer's previous products (chunk c - 2) must have been read
     if (c >= 2 && (rc = pipe.wait_reconstructed(buf))) return rc;
+    // products of whole tiles go to the reconstruction in the tiled layout
+    // (contiguous stores) when a family kernel with 4 positions per thread
+    // reconstructs them
+    const int rpat = chunk_pattern(T, 2, g0, n);
+    const bool tiled = scale_mode == FM_SCALE_TENSOR && rpat >= 0 && geo.Mb % 256 == 0 &&
+                       geo.Nb % 128 == 0 && geo.Kb % 128 == 0 && geo.N % 4 == 0 &&
+                       geo.gm * geo.gn <= 16 && (size_t)geo.R * geo.Mb * geo.Nb * 4 < ((size_t)1 << 32);
     timing_begin(T_BLOCK_GEMM, st);
     if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)n * geo.R * scales_a(geo, scale_mode), Mc,
                                 n * geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, base_mode(scale_mode),
-                                st, bf)))
+                                st, bf, tiled)))
       return rc;
     timing_end(T_BLOCK_GEMM, st);
     hipStream_t rs = st;
@@ -1212,9 +1219,10 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
     ReconArgs ra = recon_args(geo, ws, Lc, g0, n, Mc, nullptr, C_ref);
     ra.rowscale = rowup;
     ra.prod_bf16 = bf;
+    ra.tiled = tiled;
     const int nblk = recon_blocks(ra);
     timing_begin(T_RECON, rs);
-    if ((rc = launch_recon(ra, chunk_pattern(T, 2, g0, n), rs))) return rc;
+    if ((rc = launch_recon(ra, rpat, rs))) return rc;
     timing_end(T_RECON, rs);
     if ((rc = launch_reduce_rows((double*)(ws + L.partial), nblk, n, errsq + g0, rs))) return rc;
     if (pipe.on && (rc = pipe.reconstructed(buf))) return rc;

@@ -726,8 +726,16 @@ __global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a, int
   double esq = 0.0;
   const int p = blk * kThreads + threadIdx.x;
   if (p < Ptot) {
-    const int x = p / bcv, z0 = (p - x * bcv) * VW;
-    const uint32_t voff = (uint32_t)(x * a.Nb + z0) * esz;
+    // products in the tiled layout: thread p takes the p-th 16-byte piece
+    const bool tl = VW == 4 && !BF && a.tiled;
+    int x, z0;
+    if (tl) {
+      tile_layout_position(p, a.Nb, x, z0);
+    } else {
+      x = p / bcv;
+      z0 = (p - x * bcv) * VW;
+    }
+    const uint32_t voff = tl ? (uint32_t)p * 16u : (uint32_t)(x * a.Nb + z0) * esz;
     float acc[P::NB][VW];
 #pragma unroll
     for (int c = 0; c < P::NB; ++c)
@@ -930,6 +938,8 @@ int launch_recon_static(const ReconArgs& a, hipStream_t st) {
   // the kernel gives each thread exactly one position group
   if (recon_width(a) != VW || (long long)nblk * kThreads < (long long)a.Mb * (a.Nb / VW))
     return fail(FM_E_UNSUPPORTED, "reconstruction grid does not cover the block");
+  if (a.tiled && (VW != 4 || a.prod_bf16))
+    return fail(FM_E_UNSUPPORTED, "tiled products need fp32 values and 4 positions per thread");
   if (a.prod_bf16)
     recon_static_kernel<P, VW, true><<<nblk * a.G, kThreads, 0, st>>>(a, nblk);
   else
@@ -1005,7 +1015,7 @@ FM_PATTERN_FAMILIES(FM_DECLARE_FAMILY)
     using W = pat::P::W;                                                             \
     if (a.gm * a.gn != W::NB || a.R != W::R || a.Nb % recon_vw<W>() != 0 || a.N % 4 || \
         (size_t)a.R * a.Mb * a.Nb * 4 >= ((size_t)1 << 32))                          \
-      return 1;                                                                      \
+      return a.tiled ? fail(FM_E_UNSUPPORTED, "tiled products need the family kernel") : 1; \
     return launch_recon_static<W>(a, st);                                            \
   }
 

@@ -211,7 +211,8 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
                                                        const float* __restrict__ dT,
                                                        const float* __restrict__ dS,
                                                        float* __restrict__ Mout, int Mb, int Nb,
-                                                       int Kb, int tiles_m, int tiles_n, int total) {
+                                                       int Kb, int tiles_m, int tiles_n, int total,
+                                                       int tiled) {
   // SC = 2 (group scales): every K step is one group of 128; its scales ride
   // the ring in a 2 KB slot after the stage (dT of the tile's 256 rows, then
   // the tile's one dS)
@@ -433,6 +434,10 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
 #pragma unroll
         for (int j = 0; j < 4; ++j) sS[j] = make_float4(u, u, u, u);
       }
+      // tiled layout (full tiles only): the 16-byte pieces of a tile in
+      // the order (wave, i, j, row l16, column group q), so each store of a
+      // wave is one contiguous kilobyte
+      float* tbase = Mo + (size_t)tt * (DBM * DBN) + (size_t)wave * 4096 + (l16 * 4 + q) * 4;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float* prow = Mo + (size_t)(r_base + i * 16) * Nb + c_base;
@@ -443,7 +448,8 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
           o.y = (acc[i][j][1] * sT[i]) * sS[j].y;
           o.z = (acc[i][j][2] * sT[i]) * sS[j].z;
           o.w = (acc[i][j][3] * sT[i]) * sS[j].w;
-          *reinterpret_cast<float4*>(prow + j * 16) = o;
+          float* dst = tiled ? tbase + (i * 4 + j) * 256 : prow + j * 16;
+          *reinterpret_cast<float4*>(dst) = o;
         }
       }
       counted = DSTORES;
@@ -553,7 +559,8 @@ int set_block_product_arith(int a) {
 namespace {
 template <int SC, bool OB = false>
 int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
-                         float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, hipStream_t st) {
+                         float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, hipStream_t st,
+                         int tiled = 0) {
   const bool fp8acc = g_block_product_arith == FM_ACC_FP8;
   if (Kb % GK == 0) {
     // pipelined persistent kernel: one 144 KB-LDS workgroup per CU
@@ -562,15 +569,18 @@ int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, 
     if (total > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many GEMM tiles in one launch");
     const int T = (int)total;
     const int grid = (int)std::min<long long>(total, 256);
+    if (tiled && (SC != 0 || Mb % DBM || Nb % DBN))
+      return fail(FM_E_UNSUPPORTED, "the tiled product layout needs whole tiles and tensor scales");
     if (fmt == FM_E4M3) {
-      if (fp8acc) gemm_dma_kernel<FM_E4M3, 1, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-      else gemm_dma_kernel<FM_E4M3, 0, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+      if (fp8acc) gemm_dma_kernel<FM_E4M3, 1, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
+      else gemm_dma_kernel<FM_E4M3, 0, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
     } else {
-      if (fp8acc) gemm_dma_kernel<FM_E5M2, 1, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
-      else gemm_dma_kernel<FM_E5M2, 0, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T);
+      if (fp8acc) gemm_dma_kernel<FM_E5M2, 1, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
+      else gemm_dma_kernel<FM_E5M2, 0, SC, OB><<<grid, DNT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
     }
     return launched("gemm_dma_kernel");
   }
+  if (tiled) return fail(FM_E_UNSUPPORTED, "the tiled product layout needs inner blocks of 128");
   if constexpr (SC == 2) {
     return fail(FM_E_SHAPE, "group scales need inner blocks of a multiple of 128");
   } else {
@@ -593,7 +603,9 @@ int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, 
 
 int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
                       float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, int scale_mode,
-                      hipStream_t st, bool out_bf16) {
+                      hipStream_t st, bool out_bf16, bool tiled) {
+  if (tiled && scale_mode != FM_SCALE_TENSOR)
+    return fail(FM_E_UNSUPPORTED, "the tiled product layout needs tensor scales");
   if (scale_mode == FM_SCALE_ROWCOL)
     return launch_block_gemm_sc<1>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
   if (scale_mode == FM_SCALE_GROUP) {
@@ -603,7 +615,7 @@ int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, con
       return launch_block_gemm_sc<2, true>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
     return launch_block_gemm_sc<2>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
   }
-  return launch_block_gemm_sc<0>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st);
+  return launch_block_gemm_sc<0>(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, st, tiled ? 1 : 0);
 }
 
 }  // namespace fm

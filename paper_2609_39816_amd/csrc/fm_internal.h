@@ -152,9 +152,26 @@ int set_block_product_arith(int a);
 // (FM_SCALE_ROWCOL).
 // out_bf16 (group scales only): the products, bf16 values, are stored as
 // bf16 (2 bytes each, uint16_t at Mout) instead of fp32.
+// tiled (tensor scales, Mb a multiple of 256, Nb of 128, Kb of 128): each
+// product is stored tile by tile (tile_layout_offset below) instead of row
+// by row.
 int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
                       float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, int scale_mode,
-                      hipStream_t st, bool out_bf16 = false);
+                      hipStream_t st, bool out_bf16 = false, bool tiled = false);
+
+// The tiled layout of a product block (Mb x Nb, whole 256 x 128 tiles): the
+// 16-byte piece p (4 consecutive columns of one row) sits at byte 16 p, with
+// p = (((t 8 + w) 4 + i) 4 + j) 64 + 4 l + c for the tile t (row-major over
+// the block's tiles), the 64 x 64 quarter w = 2 (row / 64 % 4) + (column / 64
+// % 2), i = row / 16 % 4, j = column / 16 % 4, l = row % 16 and c = column /
+// 4 % 4.  The block-product kernel stores each wave's piece of a tile as one
+// contiguous kilobyte; the reconstruction reads pieces in this order.
+__host__ __device__ inline void tile_layout_position(int p, int Nb, int& row, int& col) {
+  const int l = (p >> 2) & 15, c = p & 3, j = (p >> 6) & 3, i = (p >> 8) & 3, w = (p >> 10) & 7;
+  const int t = p >> 13, tn = Nb / 128, tm = t / tn;
+  row = tm * 256 + (w >> 1) * 64 + i * 16 + l;
+  col = (t - tm * tn) * 128 + (w & 1) * 64 + j * 16 + 4 * c;
+}
 
 // Reconstruction + error: for gauge g < G, C_g = sum_r w M_{g,r}; if C is not
 // null it is written (G must be 1); if Cref is not null, partial sums of
@@ -170,6 +187,7 @@ struct ReconArgs {
   double* partial;     // G x nblk (if Cref)
   const float* rowscale = nullptr;  // optional: output row i*Mb + x times rowscale[i*Mb + x]
   int prod_bf16 = 0;  // products stored as bf16 (uint16_t at Mprod; group scales)
+  int tiled = 0;      // products in the tiled layout (fp32, 4 positions per thread)
 };
 // Positions per thread in the reconstruction kernels (4 or 1) and the
 // number of workgroups per gauge (one position group per thread).

@@ -448,6 +448,7 @@ int launch_recon(const ReconArgs& a, int pattern, hipStream_t st) {
   ++id;
   FM_PATTERN_FAMILIES(FM_RECON_CASE)
 #undef FM_RECON_CASE
+  if (a.tiled) return fail(FM_E_UNSUPPORTED, "tiled products need a family kernel");
   return launch_recon_generic(a, st);
 }
 

@@ -382,6 +382,21 @@ def test_chunked_orbit_equals_single_launch_and_is_deterministic():
         ws = fm.workspace(fm.workspace_size(hips[0], wg.M, wg.N, wg.K, levels, len(hips), ch))
         e3 = fm.orbit_eval(hips, At, Bt, Cref, levels, ws=ws)
         assert np.array_equal(e1.view(np.uint64), e3.view(np.uint64)), ch
+    # blocks of whole 256 x 128 tiles: the orbit passes its products to the
+    # reconstruction in the tiled layout; its errors equal those of the
+    # stand-alone row-major path (the same output bits, sums in another order)
+    wt = sy.scaled(sy.WORKLOADS["strassen1_256_gl64"], 512, 512, 256, G=6)
+    A, B = sy.operands(wt)
+    At, Bt = gpu(A), gpu(B)
+    hips, _, levels = schemes_for(wt, sy.gauges(wt))
+    Cref = fm.reference_f64(At, Bt)
+    for ch in (0, 2):
+        ws = None if ch == 0 else fm.workspace(
+            fm.workspace_size(hips[0], wt.M, wt.N, wt.K, levels, len(hips), ch))
+        errs = fm.orbit_eval(hips, At, Bt, Cref, levels, ws=ws)
+        for gi, h in enumerate(hips):
+            st = fm.error_stats(fm.matmul_lowp(h, At, Bt, levels), Cref)
+            assert abs(errs[gi] / st["rel_fro"] - 1) <= 1e-9, (ch, gi, errs[gi], st["rel_fro"])
 
 
 def test_full_size_headline_workload_sampled():
