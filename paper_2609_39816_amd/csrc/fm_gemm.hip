@@ -448,8 +448,13 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
           o.y = (acc[i][j][1] * sT[i]) * sS[j].y;
           o.z = (acc[i][j][2] * sT[i]) * sS[j].z;
           o.w = (acc[i][j][3] * sT[i]) * sS[j].w;
-          float* dst = tiled ? tbase + (i * 4 + j) * 256 : prow + j * 16;
-          *reinterpret_cast<float4*>(dst) = o;
+          // whole lines of products read once, by the reconstruction:
+          // non-temporal
+          if (tiled)
+            __builtin_nontemporal_store((v4f){o.x, o.y, o.z, o.w},
+                                        reinterpret_cast<v4f*>(tbase + (i * 4 + j) * 256));
+          else
+            *reinterpret_cast<float4*>(prow + j * 16) = o;
         }
       }
       counted = DSTORES;
