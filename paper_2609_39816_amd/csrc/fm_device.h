@@ -484,17 +484,33 @@ __global__ __launch_bounds__(kThreads) void form_static_kernel(FormArgs a, int g
 // by vector arithmetic, so each fills the other's idle time.  Gauges split
 // over grid.y as in the separate kernels: slice y encodes gauges
 // [y gpbq, (y + 1) gpbq) of aq and folds the maxima of [y gpbm, ..) of am.
+//
+// The grid is one-dimensional over gx position blocks x gy slices.  With gx
+// a multiple of 8, workgroup w takes position block 8 ((w / 8) / gy) + w % 8
+// and slice (w / 8) % gy: the gy slices of a position block run on one XCD
+// (workgroups go round-robin over the 8 XCDs) within a few dispatch rounds,
+// so the block's operand values are read from memory once and from that
+// XCD's L2 by the other slices.
 template <class P, int VW, int FMT>
 __global__ __launch_bounds__(kThreads) void form_merged_kernel(FormArgs aq, FormArgs am, int gpbq,
-                                                               int gpbm) {
+                                                               int gpbm, int gx, int gy) {
   extern __shared__ uint32_t smax[];  // am's [gauge][product][wave * 4 + row]
-  const int g0q = blockIdx.y * gpbq, g1q = min(aq.G, g0q + gpbq);
-  const int g0m = blockIdx.y * gpbm, g1m = min(am.G, g0m + gpbm);
+  const int w = blockIdx.x;
+  int bx, by;
+  if ((gx & 7) == 0) {
+    by = (w >> 3) % gy;
+    bx = ((w >> 3) / gy) * 8 + (w & 7);
+  } else {
+    by = w / gx;
+    bx = w - by * gx;
+  }
+  const int g0q = by * gpbq, g1q = min(aq.G, g0q + gpbq);
+  const int g0m = by * gpbm, g1m = min(am.G, g0m + gpbm);
   for (int i = threadIdx.x; i < gpbm * P::R * 16; i += kThreads) smax[i] = 0u;
   __syncthreads();
   const int bcv = aq.bc / VW;
   const int Ptot = aq.br * bcv;
-  for (int base = blockIdx.x * kThreads; base < Ptot; base += gridDim.x * kThreads) {
+  for (int base = bx * kThreads; base < Ptot; base += gx * kThreads) {
     const int p = base + threadIdx.x;
     const bool active = p < Ptot;
     const int x = active ? p / bcv : 0;
@@ -887,10 +903,11 @@ int launch_form_merged(const FormArgs& aq, const FormArgs& am, hipStream_t st) {
   const int gpbm = (am.G + (int)grid.y - 1) / (int)grid.y;
   if (gpbm > max_gpbm || (long long)gpbq * grid.y < aq.G) return 1;
   const size_t shm = (size_t)gpbm * P::R * 16 * 4;
+  const int gx = (int)grid.x, gy = (int)grid.y;
   if (aq.fmt == FM_E4M3)
-    form_merged_kernel<P, VW, FM_E4M3><<<grid, kThreads, shm, st>>>(aq, am, gpbq, gpbm);
+    form_merged_kernel<P, VW, FM_E4M3><<<gx * gy, kThreads, shm, st>>>(aq, am, gpbq, gpbm, gx, gy);
   else
-    form_merged_kernel<P, VW, FM_E5M2><<<grid, kThreads, shm, st>>>(aq, am, gpbq, gpbm);
+    form_merged_kernel<P, VW, FM_E5M2><<<gx * gy, kThreads, shm, st>>>(aq, am, gpbq, gpbm, gx, gy);
   return launched("form_merged_kernel");
 }
 
