@@ -389,7 +389,6 @@ int upload_tables(const Tables& T, char* ws, const Layout& L, hipStream_t st) {
   return upload(ws + base, pieces, offs, total, st);
 }
 
-// Operand formation for gauges [g0, g0 + n) of the uploaded tables.
 // Formation arguments of both sides of the gauges [g0, g0 + n) with one
 // scale per block-sum tensor, maxima and scales in the first set of L.
 void tensor_form_args(const Geometry& geo, const float* A, const float* Bt, char* ws,
@@ -447,6 +446,7 @@ int form_codes_and_next_maxima(const Geometry& geo, const float* A, const float*
   return FM_OK;
 }
 
+// Operand formation for gauges [g0, g0 + n) of the uploaded tables.
 int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, const Layout& L,
                const Tables& T, int g0, int n, int fmt, int scale_mode, uint8_t* Tq, uint8_t* Sq,
                float* dT, float* dS, hipStream_t st) {
