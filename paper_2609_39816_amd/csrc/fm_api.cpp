@@ -348,6 +348,65 @@ int check_ws(void* ws, size_t ws_bytes, size_t need) {
   return FM_OK;
 }
 
+// Appends the lists of gauges [g_from, g_to) to T.
+int extend_tables(Tables& T, const fm_scheme* const* schemes, int g_from, int g_to, int levels,
+                  const Geometry& geo) {
+  T.R = geo.R;
+  for (int g = g_from; g < g_to; ++g) {
+    const fm_scheme* s = schemes[g];
+    if (!s) return fail(FM_E_ARG, "null scheme in orbit");
+    fm_scheme flat = power(*s, levels);
+    if (flat.m != geo.gm || flat.k != geo.gk || flat.n != geo.gn || flat.R != geo.R)
+      return fail(FM_E_MISMATCH, "schemes of one orbit must share grid and rank");
+    Lists L;
+    build_lists(flat, L);
+    const int nb[3] = {geo.NBa(), geo.NBb(), geo.NC()};
+    append(T, L, geo.R, nb);
+  }
+  return FM_OK;
+}
+
+// Uploads the tables of gauges [g_from, g_to) (already in T) to their
+// places in the workspace: one asynchronous copy per table region.  The
+// staging buffer must hold them (stage_reserve).
+int upload_table_range(const Tables& T, char* ws, const Layout& L, int g_from, int g_to,
+                       hipStream_t st) {
+  const size_t R1 = (size_t)T.R + 1;
+  std::vector<std::pair<const void*, size_t>> pieces;
+  std::vector<size_t> dst;
+  for (int k = 0; k < 3; ++k) {
+    const Side& sd = T.s[k];
+    const size_t e0 = (size_t)sd.off[(size_t)g_from * R1];
+    const size_t e1 = (size_t)sd.off[(size_t)(g_to - 1) * R1 + T.R];
+    pieces.push_back({sd.off.data() + (size_t)g_from * R1, (size_t)(g_to - g_from) * R1 * 4});
+    dst.push_back(L.off[k] + (size_t)g_from * R1 * 4);
+    pieces.push_back({sd.idx.data() + e0, (e1 - e0) * 4});
+    dst.push_back(L.idx[k] + e0 * 4);
+    pieces.push_back({sd.coef.data() + e0, (e1 - e0) * 4});
+    dst.push_back(L.coef[k] + e0 * 4);
+  }
+  size_t total = 0;
+  for (auto& p : pieces) total += p.second;
+  if (int rc = stage_reserve(total)) return rc;
+  size_t at = 0;
+  for (size_t i = 0; i < pieces.size(); ++i) {
+    if (!pieces[i].second) continue;
+    std::memcpy((char*)g_stage.host + at, pieces[i].first, pieces[i].second);
+    if (int rc = hip_check(hipMemcpyAsync(ws + dst[i], (char*)g_stage.host + at, pieces[i].second,
+                                          hipMemcpyHostToDevice, st),
+                           "hipMemcpyAsync(H2D)"))
+      return rc;
+    at += pieces[i].second;
+  }
+  if (!g_stage.ev)
+    if (int rc = hip_check(hipEventCreateWithFlags(&g_stage.ev, hipEventDisableTiming),
+                           "hipEventCreate"))
+      return rc;
+  if (int rc = hip_check(hipEventRecord(g_stage.ev, st), "hipEventRecord")) return rc;
+  g_stage.pending = true;
+  return FM_OK;
+}
+
 Tables make_tables(const fm_scheme* const* schemes, int G, int levels, const Geometry& geo,
                    int& rc) {
   Tables T;
@@ -1151,9 +1210,36 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   }
   char* ws = (char*)workspace;
   int rc = FM_OK;
-  Tables T = make_tables(gauged, G, levels, geo, rc);
-  if (rc) return rc;
-  if ((rc = upload_tables(T, ws, L, st))) return rc;
+  // Coefficient tables: with several chunks (and no joint rounding, whose
+  // set-up needs every gauge's tables), those of the first two chunks are
+  // built and uploaded first, the rest while the first chunk runs on the
+  // device.  Every gauge's grid and rank are checked before any device work.
+  for (int g = 0; g < G; ++g) {
+    const fm_scheme* s = gauged[g];
+    if (!s) return fail(FM_E_ARG, "null scheme in orbit");
+    long long m = 1, k = 1, n = 1, R = 1;
+    for (int l = 0; l < levels; ++l) {
+      m *= s->m;
+      k *= s->k;
+      n *= s->n;
+      R *= s->R;
+    }
+    if (m != geo.gm || k != geo.gk || n != geo.gn || R != geo.R)
+      return fail(FM_E_MISMATCH, "schemes of one orbit must share grid and rank");
+  }
+  const int G1 = (L.two_sets() && !repair_weights(scale_mode)) ? std::min(G, 2 * chunk) : G;
+  Tables T;
+  if ((rc = extend_tables(T, gauged, 0, G1, levels, geo))) return rc;
+  if (G1 < G) {
+    // staging for the largest upload (dense lists) up front: no pinned
+    // allocation while the orbit runs
+    const size_t per_gauge = (size_t)(geo.R + 1) * 4 * 3 +
+                             (size_t)geo.R * (geo.NBa() + geo.NBb() + geo.NC()) * 8;
+    if ((rc = stage_reserve(per_gauge * (size_t)G))) return rc;
+    if ((rc = upload_table_range(T, ws, L, 0, G1, st))) return rc;
+  } else if ((rc = upload_tables(T, ws, L, st))) {
+    return rc;
+  }
   if ((rc = launch_fill_u32((uint32_t*)(ws + L.flags), 1, 0u, st))) return rc;
   float* Bt = (float*)(ws + L.bt);
   if ((rc = launch_transpose(B, Bt, K, N, st))) return rc;
@@ -1226,6 +1312,14 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
     timing_end(T_RECON, rs);
     if ((rc = launch_reduce_rows((double*)(ws + L.partial), nblk, n, errsq + g0, rs))) return rc;
     if (pipe.on && (rc = pipe.reconstructed(buf))) return rc;
+    // the remaining gauges' tables, built while the first chunk runs; they
+    // are uploaded on the caller's stream ahead of the next formation pass,
+    // the first to read them (chunk 2's maxima)
+    if (c == 0 && T.G < G) {
+      const int Gd = T.G;
+      if ((rc = extend_tables(T, gauged, Gd, G, levels, geo))) return rc;
+      if ((rc = upload_table_range(T, ws, L, Gd, G, st))) return rc;
+    }
   }
   if ((rc = pipe.join())) return rc;
   // sum of squares of the reference (err_sq of a zero output)
