@@ -7,7 +7,8 @@
 //  (block products: fm_gemm.hip)
 //  recon_kernel     C_ij = sum_r w_{r,ij} M_r (eq. (1)) with the squared
 //                   error against the float64 reference reduced on chip.
-//  ref_f64_kernel   float64 reference product (App. F).
+//  ref_f64_mfma_kernel  float64 reference product (App. F) on the float64
+//                   matrix cores.
 // plus small kernels: fill, transpose, scales, fixed-order reductions.
 //
 // Arithmetic contract (matched bit for bit by the CPU oracle for everything
@@ -277,54 +278,87 @@ __global__ __launch_bounds__(64) void reduce_rows_kernel(const double* partial, 
 }
 
 // ----------------------------------------------------- float64 reference
-// 64 x 64 output tile per workgroup, 4 x 4 per thread, K step 16; operands
-// staged in LDS as fp32 and widened to float64 (products of two fp32 values
-// are exact in float64).
-__global__ __launch_bounds__(kThreads) void ref_f64_kernel(const float* __restrict__ A,
-                                                           const float* __restrict__ B,
-                                                           double* __restrict__ C, int M, int N,
-                                                           int K) {
-  __shared__ float As[16][64 + 4];
-  __shared__ float Bs[16][64 + 4];
-  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  double c[4][4] = {};
-  for (int k0 = 0; k0 < K; k0 += 16) {
+// On the float64 matrix cores: 128 x 128 output tile per workgroup of 4
+// waves (64 x 64 each: 4 x 4 blocks of v_mfma_f64_16x16x4_f64), K step 32;
+// operands staged in LDS as fp32 and widened to float64 when read (products
+// of two fp32 values are exact in float64; the sums are float64).
+// Lane l of a 16 x 16 x 4 step holds A[l % 16][l / 16] and B[l / 16][l % 16];
+// its four results v = 0..3 are rows l / 16 + 4 v, column l % 16 of the block
+// (checked on the device with small integer operands).
+typedef double v4d __attribute__((ext_vector_type(4)));
+__global__ __launch_bounds__(kThreads) void ref_f64_mfma_kernel(const float* __restrict__ A,
+                                                                const float* __restrict__ B,
+                                                                double* __restrict__ C, int M,
+                                                                int N, int K) {
+  constexpr int KS = 32;  // K step
+  __shared__ float As[128][KS + 1];
+  __shared__ float Bs[KS][128 + 4];
+  const int m0 = blockIdx.y * 128, n0 = blockIdx.x * 128;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l16 = lane & 15, lq = lane >> 4;
+  v4d acc[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int idx = threadIdx.x + kThreads * i;
-      const int row = idx >> 4, kk = idx & 15;
-      const int gr = m0 + row, gk = k0 + kk;
-      As[kk][row] = (gr < M && gk < K) ? A[(size_t)gr * K + gk] : 0.0f;
-      const int kb = idx >> 6, col = idx & 63;
-      const int gkb = k0 + kb, gc = n0 + col;
-      Bs[kb][col] = (gkb < K && gc < N) ? B[(size_t)gkb * N + gc] : 0.0f;
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = (v4d){0.0, 0.0, 0.0, 0.0};
+  // the next step's operands are loaded into registers while this step's
+  // products run
+  float ra[16], rb[16];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int idx = tid + kThreads * i;  // 0 .. 4095
+      const int r = idx >> 5, kk = idx & 31;
+      const int gr = m0 + r, gk = k0 + kk;
+      ra[i] = (gr < M && gk < K) ? A[(size_t)gr * K + gk] : 0.0f;
+      const int kb = idx >> 7, c = idx & 127;
+      const int gkb = k0 + kb, gc = n0 + c;
+      rb[i] = (gkb < K && gc < N) ? B[(size_t)gkb * N + gc] : 0.0f;
     }
-    __syncthreads();
+  };
+  auto store = [&]() {
 #pragma unroll
-    for (int kk = 0; kk < 16; ++kk) {
-      const float4 av = *reinterpret_cast<const float4*>(&As[kk][ty * 4]);
-      const float4 bv = *reinterpret_cast<const float4*>(&Bs[kk][tx * 4]);
-      const double a4[4] = {(double)av.x, (double)av.y, (double)av.z, (double)av.w};
-      const double b4[4] = {(double)bv.x, (double)bv.y, (double)bv.z, (double)bv.w};
+    for (int i = 0; i < 16; ++i) {
+      const int idx = tid + kThreads * i;
+      As[idx >> 5][idx & 31] = ra[i];
+      Bs[idx >> 7][idx & 127] = rb[i];
+    }
+  };
+  load(0);
+  for (int k0 = 0; k0 < K; k0 += KS) {
+    store();
+    __syncthreads();
+    if (k0 + KS < K) load(k0 + KS);
+#pragma unroll
+    for (int kk = 0; kk < KS; kk += 4) {
+      double a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = (double)As[wm * 64 + i * 16 + l16][kk + lq];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = (double)Bs[kk + lq][wn * 64 + j * 16 + l16];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) c[i][j] = __fma_rn(a4[i], b4[j], c[i][j]);
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = m0 + ty * 4 + i;
-    if (row >= M) continue;
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = n0 + tx * 4 + j;
-      if (col < N) C[(size_t)row * N + col] = c[i][j];
+    for (int v = 0; v < 4; ++v) {
+      const int row = m0 + wm * 64 + i * 16 + lq + 4 * v;
+      if (row >= M) continue;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int col = n0 + wn * 64 + j * 16 + l16;
+        if (col < N) C[(size_t)row * N + col] = acc[i][j][v];
+      }
     }
-  }
 }
+
 
 // --------------------------------------------------------- error stats
 __global__ __launch_bounds__(kThreads) void error_stats_kernel(const float* __restrict__ C,
@@ -460,9 +494,9 @@ int launch_reduce_rows(const double* partial, int nblk, int G, double* out, hipS
 
 int launch_reference_f64(const float* A, const float* B, double* C, int M, int N, int K,
                          hipStream_t st) {
-  dim3 grid((N + 63) / 64, (M + 63) / 64);
-  ref_f64_kernel<<<grid, kThreads, 0, st>>>(A, B, C, M, N, K);
-  return launched("ref_f64_kernel");
+  dim3 grid((N + 127) / 128, (M + 127) / 128);
+  ref_f64_mfma_kernel<<<grid, kThreads, 0, st>>>(A, B, C, M, N, K);
+  return launched("ref_f64_mfma_kernel");
 }
 
 int error_stats_blocks(size_t n) {
