@@ -351,10 +351,14 @@ __device__ __forceinline__ void form_static_gauges(const FormArgs& a, int g0, in
             });
             if (ROWS && a.gran == 3) round_bf16<VW>(acc);
             if constexpr (MODE == 0) {
-              uint32_t mx = 0u;
+              // largest magnitude, NaN-propagating (v_maximum3_f32 on
+              // absolute values: half an instruction per value); as bits it
+              // orders like the magnitudes, and a NaN or infinity stays at
+              // or above the bits of infinity, as the scales check expects
+              float mf = 0.0f;
 #pragma unroll
-              for (int v = 0; v < VW; ++v) mx = max(mx, __float_as_uint(acc[v]) & 0x7fffffffu);
-              lm[j] = active ? mx : 0u;
+              for (int v = 0; v < VW; ++v) mf = __builtin_elementwise_maximum(mf, __builtin_fabsf(acc[v]));
+              lm[j] = active ? __float_as_uint(mf) : 0u;
             } else {
               const float q = ROWS ? qv[j] : ro(a.q)[(size_t)g * P::R + r + so];
               form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, acc, q);
