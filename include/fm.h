@@ -186,8 +186,10 @@ void fm_scheme_free(fm_scheme* s);
 /* Bytes of device workspace needed to evaluate G gauged copies of `s`
  * (flattened to `levels`) at M x K times K x N, `chunk` copies at a time
  * (chunk <= 0 means all G at once).  0 if the arguments are invalid.
- * With chunk < G the size includes a second buffer of block products, so
- * that fm_orbit_eval can reconstruct one chunk while the next is formed.
+ * With chunk < G the size includes a second set of a chunk's block
+ * products, maxima and scales, so that fm_orbit_eval can reconstruct one
+ * chunk while the next is formed (and, with one scale per tensor, form a
+ * chunk's maxima one chunk ahead).
  * fm_matmul_lowp and fm_form_operands need fm_workspace_size(s,M,N,K,L,1,1).
  * The workspace must be 256-byte aligned. */
 size_t fm_workspace_size(const fm_scheme* s, int M, int N, int K, int levels,
@@ -271,8 +273,11 @@ int fm_error_stats(const float* C, const double* C_ref, int M, int N,
  * that fits.  With several chunks and room for two product buffers, each
  * chunk's reconstruction runs on a second stream of the library's (one per
  * device, default priority), ordered by events against the caller's stream,
- * beside the next chunk's formation; the results are the same bits as with
- * one buffer.  Synchronizes. */
+ * beside the next chunk's formation; concurrent calls on one device share
+ * that stream (their reconstructions then run one after another).  The
+ * results are the bits of the one-buffer schedule; within a chunk the
+ * products may be stored in a tiled order internally (whole 256 x 128
+ * tiles, tensor scales).  Synchronizes. */
 int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A,
                   const float* B, const double* C_ref, int M, int N, int K,
                   int levels, fm_fmt fmt, double* rel_fro_out,
