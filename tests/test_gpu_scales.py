@@ -98,6 +98,11 @@ def test_rowcol_parity(case):
     Cref = fm.reference_f64(At, Bt)
     Cref_o = oracle.reference_f64(A, B)
     errs = fm.orbit_eval(hips, At, Bt, Cref, lv, fh, scale_mode=RC_H)
+    # one gauge per chunk: each chunk's codes are formed together with the
+    # next chunk's maxima, on two sets of scales; the same bits
+    ws1 = fm.workspace(fm.workspace_size(hips[0], M, N, K, lv, len(hips), 1, RC_H))
+    errs1 = fm.orbit_eval(hips, At, Bt, Cref, lv, fh, ws=ws1, scale_mode=RC_H)
+    assert np.array_equal(errs.view(np.uint64), errs1.view(np.uint64)), (errs, errs1)
     for gi in (0, len(hips) - 1):
         h, o = hips[gi], orcs[gi]
         tabs, dims = oracle.flatten_f32(o)
