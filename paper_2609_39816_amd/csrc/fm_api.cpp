@@ -573,9 +573,9 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
 // (default) priority reconstructs each chunk from its product buffer, so
 // that work runs beside the next chunk's formation.  Events order the two:
 // a chunk's reconstruction waits for its products, products of chunk c wait
-// until chunk c - 2 has been reconstructed from the same buffer, and the
-// caller's stream waits for every reconstruction at the end (also on an
-// early return, so no work is left running on the workspace).
+// until chunk c - 1 has been reconstructed, and the caller's stream waits
+// for every reconstruction at the end (also on an early return, so no work
+// is left running on the workspace).
 hipStream_t side_stream(int& rc) {
   static std::mutex mu;
   static hipStream_t streams[64] = {};
@@ -1285,8 +1285,11 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
                                 nullptr, nullptr, st))) {
       return rc;
     }
-    // the buffer's previous products (chunk c - 2) must have been read
-    if (c >= 2 && (rc = pipe.wait_reconstructed(buf))) return rc;
+    // the previous chunk's reconstruction runs beside this chunk's
+    // formation and is done before these products start: the block
+    // products, the bulk of the work, then have the GPU to themselves (a
+    // reconstruction running beside them slows them more than it gains)
+    if (c >= 1 && (rc = pipe.wait_reconstructed(buf ^ 1))) return rc;
     // products of whole tiles go to the reconstruction in the tiled layout
     // (contiguous stores) when a family kernel with 4 positions per thread
     // reconstructs them
