@@ -203,3 +203,40 @@ def test_joint_rounding_lowers_the_quadratic_error():
                     assert float(exact_energy(c2, s, d, H)) >= float(E1) - noise
         improved += int(float(E1) < float(E0) - noise)
     assert improved >= 6
+
+
+def test_joint_rounding_sweeps_in_ascending_order_hand_example():
+    """App. C's joint rounding sweeps r = 1, ..., R in order.  A hand-worked
+    position (E4M3, q = d = 1, so values are codes' values) where the sweep
+    order decides the outcome:
+
+      s = (343/256, 151/128, 103/64), H = [[6, -6, 0], [-6, 9, 0], [0, 0, 8]].
+
+    Brackets: s0 in (5/4, 11/8), s1 in (9/8, 5/4), s2 in (3/2, 13/8); the
+    nearer values start: (11/8, 9/8, 13/8), e = (9, -14, 4)/256, so
+    g = H e = (138, -180, 32)/256.  Sweep 1, r = 0: delta = -1/8, change =
+    2 delta g0 + delta^2 H00 = -276/2048 + 6/64 < 0, flip to 5/4; g becomes
+    (-54, 12, 32)/256.  r = 1: delta = 1/8, change = 24/2048 + 9/64 > 0.
+    r = 2: delta = -1/8, change = -64/2048 + 8/64 > 0.  Sweep 2 changes
+    nothing (r = 0: 2 (1/8)(-54/256) + 6/64 > 0), so two sweeps end at
+    (5/4, 9/8, 13/8) = codes (0x3A, 0x39, 0x3D).
+
+    Swept in reverse (r = 2, 1, 0) the same start flips product 1 first
+    (change 2 (1/8)(-180/256) + 9/64 < 0), after which g0 = -54/256 keeps
+    product 0 at 11/8: (11/8, 5/4, 13/8) = (0x3B, 0x3A, 0x3D).  Every value
+    here is exact in fp32 and no decision is within 1/64 of zero, so the
+    fp32 arithmetic cannot change a decision."""
+    s = np.array([343 / 256, 151 / 128, 103 / 64], np.float32)
+    H = np.array([[6, -6, 0], [-6, 9, 0], [0, 0, 8]], np.float32)
+    one = np.ones(3, np.float32)
+    codes, sweeps = oracle.joint_round_position(s, one, one, H)
+    assert [int(c) for c in codes] == [0x3A, 0x39, 0x3D]
+    assert sweeps == 2
+    assert list(oracle.fp8_decode(codes)) == [1.25, 1.125, 1.625]
+    # the reversed sweep's result, from the oracle on the mirrored problem
+    # (reverse the product order, so that its ascending sweep visits the
+    # original products from the last): it must differ
+    p = [2, 1, 0]
+    rcodes, rsweeps = oracle.joint_round_position(s[p], one, one, H[np.ix_(p, p)])
+    assert [int(c) for c in rcodes[p]] == [0x3B, 0x3A, 0x3D]
+    assert rsweeps == 2
