@@ -264,6 +264,21 @@ int fm_error_stats(const float* C, const double* C_ref, int M, int N,
                    fm_stats* out, void* workspace, size_t ws_bytes,
                    void* hip_stream);
 
+/* fm_error_stats without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same kernels, sums and result,
+ * with the reduction's partial sums in a static device array of the
+ * library (32768 bytes per device, held until the process ends) instead of
+ * a caller's workspace.  Allocates nothing (no hipMalloc, hipFree or pinned
+ * host memory; the 24-byte result is copied straight into a host local).
+ * Every output size fits the array (the reduction uses at most 1024
+ * workgroups); FM_E_WORKSPACE would report one that did not.  All calls on
+ * one device share that device's array: calls that overlap in time on one
+ * device (several host threads, or several streams) race and must be
+ * serialized by the caller.  Synchronizes; writes *out. */
+int fm_error_stats_noalloc(const float* C, const double* C_ref, int M, int N,
+                           fm_stats* out, void* hip_stream);
+
 /* Orbit evaluation: for each of G gauged schemes (same grid and rank after
  * flattening to `levels`), the whole FP8 schedule on A, B and the float64
  * relative Frobenius error against C_ref (M x N float64, device), reduced on

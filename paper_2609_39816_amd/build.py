@@ -26,7 +26,8 @@ FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-ffp-contract=o
 
 
 def sources():
-    fixed = ["fm_scheme.cpp", "fm_patterns.cpp", "fm_api.cpp", "fm_kernels.hip", "fm_gemm.hip", "fm_int8.hip"]
+    fixed = ["fm_scheme.cpp", "fm_patterns.cpp", "fm_api.cpp", "fm_kernels.hip", "fm_gemm.hip", "fm_int8.hip",
+             "fm_noalloc.hip"]
     fams = sorted(os.path.basename(p) for p in glob.glob(os.path.join(CSRC, "fm_fam_*.hip")))
     return fixed + fams
 

@@ -72,6 +72,7 @@ def _load():
         "fm_matmul_lowp": (i, [p, p, p, p, i, i, i, i, i, p, sz, p]),
         "fm_reference_f64": (i, [p, p, p, i, i, i, p]),
         "fm_error_stats": (i, [p, p, i, i, ct.POINTER(_Stats), p, sz, p]),
+        "fm_error_stats_noalloc": (i, [p, p, i, i, ct.POINTER(_Stats), p]),
         "fm_orbit_eval": (i, [p, i, p, p, p, i, i, i, i, i, p, p, sz, p]),
         "fm_workspace_size_scaled": (sz, [p, i, i, i, i, i, i, i]),
         "fm_form_operands_scaled": (i, [p, i, p, p, i, i, i, i, i, p, p, p, p, p, sz, p]),
@@ -336,6 +337,16 @@ def error_stats(C, Cref, ws=None, stream=None) -> dict:
     st = _Stats()
     _check(lib.fm_error_stats(_dptr(C), _dptr(Cref), M, N, ct.byref(st), _dptr(ws), ws.numel(),
                               _stream(stream)))
+    return dict(rel_fro=st.rel_fro, err_sq=st.err_sq, ref_sq=st.ref_sq, max_abs=st.max_abs)
+
+
+def error_stats_noalloc(C, Cref, stream=None) -> dict:
+    """error_stats without a workspace: the library's static device scratch
+    holds the partial sums (calls overlapping on one device race)."""
+    _cuda(C, torch.float32), _cuda(Cref, torch.float64)
+    M, N = C.shape
+    st = _Stats()
+    _check(lib.fm_error_stats_noalloc(_dptr(C), _dptr(Cref), M, N, ct.byref(st), _stream(stream)))
     return dict(rel_fro=st.rel_fro, err_sq=st.err_sq, ref_sq=st.ref_sq, max_abs=st.max_abs)
 
 
