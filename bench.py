@@ -1,19 +1,23 @@
 #!/usr/bin/env python3
 """Benchmark of the FP8 gauge-orbit evaluation on one MI355X.
 
-One step = the whole hot path once for the headline workload: two-level
-Strassen (4x4x4, 49 products) on A 2048x4096 (N(0,1), 8 outlier channels
-x100) times B 4096x4096 (N(0, 0.02^2)), for every one of its 512 sign
-variants: scheme preparation (the gauge action on the host), the float64
-reference, the classical FP8 baseline with its error, and for every variant
-the FP8 operands, the 49 block products, the reconstruction and its error on
-the device.  Inputs are resident in HBM before timing starts.
+One step = the whole hot path once for the headline workload, the largest
+projection shape: three-level Strassen (8x8x8, 343 products) on A
+8192x27648 (Student-t(3), 32 outlier channels x1000) times B 27648x5120
+(N(0, 0.015^2)), for 512 sign variants sampled from its orbit: scheme
+preparation (the gauge action on the host), the float64 reference, the
+classical FP8 baseline with its error, and for every variant the FP8
+operands, the 343 block products, the reconstruction and its error on the
+device.  Inputs are resident in HBM before timing starts.  Other workloads
+(--workload) are the smaller projection shapes.
 
 Prints one JSON line on stdout (progress goes to stderr):
   value  = classical-equivalent FP8 TFLOP/s = G * 2MNK / t,
   roofline = the kernel class with the most time in the timed region, its
              achieved rate from HIP events around each of its launches,
-  cpu_baseline = the oracle on one variant of the same workload.
+  pipeline = the whole orbit against the matrix-core and HBM ceilings
+             (algorithmic flops and bytes per step over the step time),
+  cpu_baseline = the oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -26,7 +30,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-HEADLINE = "strassen2_2048x4096x4096_sign512"
+HEADLINE = "strassen3_8192x27648x5120_sign512"
 PEAK_FP8_TFLOPS = 5000.0     # MI355X dense FP8 matrix peak
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix peak
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
@@ -103,15 +107,47 @@ def gemm_bytes(w, geo, G):
     return G * R * (Mb * Kb + Nb * Kb + 4.0 * Mb * Nb) + (w.M * w.K + w.N * w.K + 4.0 * w.M * w.N)
 
 
+def cpu_model():
+    """The host CPU's model name (first entry of /proc/cpuinfo), or None."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+# Classical-equivalent flops the oracle is given per gauge in the CPU sample:
+# at about 0.04 TFLOP/s on 16 host cores this is about 8 s per gauge.
+CPU_SAMPLE_FLOPS = 4e11
+
+
+def cpu_sample_rows(w, gm):
+    """Rows of A the CPU sample uses: all of them, or the first M / f for the
+    least power of two f that brings 2 (M / f) N K under CPU_SAMPLE_FLOPS
+    while M / f stays a multiple of the grid's m^L."""
+    rows = w.M
+    while 2.0 * rows * w.N * w.K > CPU_SAMPLE_FLOPS and rows % (2 * gm) == 0:
+        rows //= 2
+    return rows
+
+
 def cpu_baseline(w, A, B, gauges, scale_mode=0, budget_s=10.0):
     """The oracle (plain C, OpenMP) on the first gauges of the workload's
     orbit, one after another until about budget_s seconds have passed (at
-    least one, at most 16)."""
+    least one, at most 16).  On the largest shapes one gauge would take
+    about a minute, so the sample keeps the workload's K, N, scheme and
+    gauges and takes the first rows of A (cpu_sample_rows); the rate is
+    classical-equivalent flops of the sample over its time."""
     import oracle
     from oracle import scheme_ops as so
     from oracle import schemes as osch
 
     base = osch.BASE_SCHEMES[w.scheme]()
+    gm = base.m ** w.levels
+    rows = cpu_sample_rows(w, gm)
+    As = A[:rows]
     t = 0.0
     n = 0
     dims = None
@@ -122,17 +158,33 @@ def cpu_baseline(w, A, B, gauges, scale_mode=0, budget_s=10.0):
         tabs, dims = oracle.flatten_f32(s)
         t0 = time.perf_counter()
         if scale_mode & ~0xff:  # the repairs (group schedule)
-            oracle.lowp_matmul_repaired(A, B, tabs, dims, flags=(scale_mode >> 8) & 3)
+            oracle.lowp_matmul_repaired(As, B, tabs, dims, flags=(scale_mode >> 8) & 3)
         else:
-            oracle.lowp_matmul(A, B, tabs, dims, scale_mode=scale_mode)
+            oracle.lowp_matmul(As, B, tabs, dims, scale_mode=scale_mode)
         t += time.perf_counter() - t0
         n += 1
     cores = oracle.default_threads()
-    return dict(value=n * 2.0 * w.M * w.N * w.K / t / 1e12, unit="TFLOP/s (classical-equivalent)",
-                cores=cores, kind="oracle",
-                sample=f"the first {n} of {w.G} gauge variants at the full "
-                       f"{w.M}x{w.K}x{w.N} shape: FP8 operands, {dims[3]} block products, "
-                       f"reconstruction each; {t:.2f} s; the float64 reference is not included")
+    shape = (f"the full {w.M}x{w.K}x{w.N} shape" if rows == w.M else
+             f"the first {rows} of the {w.M} rows of A ({rows}x{w.K}x{w.N}; same B, scheme "
+             f"and gauges)")
+    return dict(value=n * 2.0 * rows * w.N * w.K / t / 1e12, unit="TFLOP/s (classical-equivalent)",
+                cores=cores, cpu_model=cpu_model(), kind="oracle",
+                sample=f"the first {n} of {w.G} gauge variants on {shape}: FP8 operands, "
+                       f"{dims[3]} block products, reconstruction each; {t:.2f} s; the float64 "
+                       f"reference is not included")
+
+
+def pipeline_work(w, geo, G):
+    """Algorithmic work of one step's orbit (all G gauges): the block
+    products' matrix flops, and the least HBM traffic of the schedule with
+    materialized products: per gauge the FP8 operands written and read once,
+    the fp32 products written and read once, the float64 reference read once
+    (operand inputs, read once per chunk, are left out)."""
+    gm, gk, gn, R = geo
+    Mb, Kb, Nb = w.M // gm, w.K // gk, w.N // gn
+    flops = G * R * 2.0 * Mb * Nb * Kb
+    hbm = G * (2.0 * R * (Mb * Kb + Nb * Kb) + 2.0 * 4.0 * R * Mb * Nb + 8.0 * w.M * w.N)
+    return flops, hbm
 
 
 # The paper's integer timings (App. E, one H20 at 4096 x 4096 x 4096 from
@@ -355,7 +407,33 @@ def main():
 
     flops = G * 2.0 * w.M * w.N * w.K
     value = flops / t / 1e12
-    mfma_flops = G * geo[3] * 2.0 * (w.M // geo[0]) * (w.N // geo[2]) * (w.K // geo[1])
+    mfma_flops, hbm_bytes = pipeline_work(w, geo, G)
+    # the whole orbit against both ceilings: its block products' matrix
+    # flops over the step time against the matrix peak of the instruction
+    # issued (and the FP8 peak), and its least HBM traffic over the step time
+    # against the HBM peak; per kernel class, achieved rates from the HIP
+    # event times of its launches
+    fp8_mfma = fm.get_block_product_arithmetic() == fm.ACC_FP8
+    pipe = dict(mfma_flops_per_step=mfma_flops, hbm_bytes_per_step=hbm_bytes,
+                mfma_tflops=round(mfma_flops / t / 1e12, 2),
+                frac_of_mfma_peak=round(mfma_flops / t / 1e12 /
+                                        (PEAK_FP8_TFLOPS if fp8_mfma else PEAK_BF16_TFLOPS), 4),
+                frac_of_fp8_peak=round(mfma_flops / t / 1e12 / PEAK_FP8_TFLOPS, 4),
+                hbm_gbs=round(hbm_bytes / t / 1e9, 1),
+                frac_of_hbm_peak=round(hbm_bytes / t / 1e9 / PEAK_HBM_GBS, 4))
+    per_class_rate = {}
+    for cls, v in per_class.items():
+        if v["total_ms"] <= 0:
+            continue
+        bound, work, unit = kernel_work(cls, w, geo, chunk, G)
+        secs = v["total_ms"] / 1e3 / args.steps
+        if unit == "TFLOP/s":
+            per_class_rate[cls] = dict(ms_per_step=round(secs * 1e3, 3),
+                                       tflops=round(work / secs / 1e12, 1))
+        else:
+            per_class_rate[cls] = dict(ms_per_step=round(secs * 1e3, 3),
+                                       gbs=round(work / secs / 1e9, 1),
+                                       frac_of_hbm_peak=round(work / secs / 1e9 / PEAK_HBM_GBS, 4))
     st = dict(min=float(ratios.min()), median=float(np.sort(ratios)[len(ratios) // 2]),
               max=float(ratios.max()), identity=float(ratios[0]))
     out = {
@@ -381,7 +459,8 @@ def main():
         "classical_fp8_rel_fro": err_cl,
         "ratio_stats": st,
         "roofline": roof,
-        "kernel_ms_per_step": {c: round(v["total_ms"] / args.steps, 3) for c, v in per_class.items()},
+        "pipeline": pipe,
+        "kernel_classes": per_class_rate,
     }
     if not args.no_cpu_baseline:
         log("[bench] oracle baseline on the host cores")
