@@ -334,7 +334,11 @@ int fm_form_operands_scaled(const fm_scheme* s, int levels, const float* A,
                             void* workspace, size_t ws_bytes,
                             void* hip_stream);
 
-/* fm_block_products with a scale granularity.  Async. */
+/* fm_block_products with a scale granularity.  Async.  The kernels read the
+ * scale arrays in aligned 16-byte chunks: with FM_SCALE_ROWCOL dS must be
+ * 16-byte aligned; with FM_SCALE_GROUP dT and dS must be 16-byte aligned
+ * and readable up to the next multiple of 4 floats past their last entry
+ * (pad the allocation).  FM_E_ARG for a misaligned scale array. */
 int fm_block_products_scaled(const uint8_t* Tq, const uint8_t* Sq,
                              const float* dT, const float* dS, int batch,
                              int Mb, int Nb, int Kb, fm_fmt fmt,

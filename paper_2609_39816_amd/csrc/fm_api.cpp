@@ -1059,6 +1059,13 @@ int fm_block_products_scaled(const uint8_t* Tq, const uint8_t* Sq, const float* 
     return fail(FM_E_ARG, "bad scale mode (the repairs act on the operands, not on the products)");
   if (batch < 1 || Mb < 1 || Nb < 1 || Kb < 1) return fail(FM_E_ARG, "sizes must be positive");
   if (Kb % 16) return fail(FM_E_SHAPE, "Kb must be a multiple of 16");
+  // scales read in aligned 16-byte chunks (float4 column scales; group
+  // scales as the chunk holding the entry)
+  auto aligned16 = [](const void* p) { return ((uintptr_t)p & 15u) == 0; };
+  if (scale_mode == FM_SCALE_ROWCOL && !aligned16(dS))
+    return fail(FM_E_ARG, "per-column scales must be 16-byte aligned");
+  if (scale_mode == FM_SCALE_GROUP && (!aligned16(dT) || !aligned16(dS)))
+    return fail(FM_E_ARG, "group scales must be 16-byte aligned (and padded to 4 floats)");
   return launch_block_gemm(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, scale_mode,
                            (hipStream_t)hip_stream);
 }
@@ -1291,12 +1298,12 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
     // reconstruction running beside them slows them more than it gains)
     if (c >= 1 && (rc = pipe.wait_reconstructed(buf ^ 1))) return rc;
     // products of whole tiles go to the reconstruction in the tiled layout
-    // (contiguous stores) when a family kernel with 4 positions per thread
-    // reconstructs them
+    // (contiguous stores) when a family kernel reconstructs them
     const int rpat = chunk_pattern(T, 2, g0, n);
-    const bool tiled = scale_mode == FM_SCALE_TENSOR && rpat >= 0 && geo.Mb % 256 == 0 &&
-                       geo.Nb % 128 == 0 && geo.Kb % 128 == 0 && geo.N % 4 == 0 &&
-                       geo.gm * geo.gn <= 16 && (size_t)geo.R * geo.Mb * geo.Nb * 4 < ((size_t)1 << 32);
+    const int trows = block_gemm_tile_rows(geo.Mb, geo.Nb, geo.Kb, base_mode(scale_mode), bf);
+    const bool tiled = scale_mode == FM_SCALE_TENSOR && rpat >= 0 && trows > 0 &&
+                       geo.Mb % trows == 0 && geo.Nb % 128 == 0 && geo.N % 4 == 0 &&
+                       geo.gm * geo.gn <= 64 && (size_t)geo.R * geo.Mb * geo.Nb * 4 < ((size_t)1 << 32);
     timing_begin(T_BLOCK_GEMM, st);
     if ((rc = launch_block_gemm(Tq, Sq, dd, dd + (size_t)n * geo.R * scales_a(geo, scale_mode), Mc,
                                 n * geo.R, geo.Mb, geo.Nb, geo.Kb, fmt, base_mode(scale_mode),
@@ -1308,7 +1315,7 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
     ReconArgs ra = recon_args(geo, ws, Lc, g0, n, Mc, nullptr, C_ref);
     ra.rowscale = rowup;
     ra.prod_bf16 = bf;
-    ra.tiled = tiled;
+    ra.tiled = tiled ? trows : 0;
     const int nblk = recon_blocks(ra);
     timing_begin(T_RECON, rs);
     if ((rc = launch_recon(ra, rpat, rs))) return rc;

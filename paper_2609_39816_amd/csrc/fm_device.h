@@ -747,15 +747,20 @@ __global__ __launch_bounds__(kThreads) void recon_static_kernel(ReconArgs a, int
   const int p = blk * kThreads + threadIdx.x;
   if (p < Ptot) {
     // products in the tiled layout: thread p takes the p-th 16-byte piece
-    const bool tl = VW == 4 && !BF && a.tiled;
+    // (4 positions per thread) or the p-th value (one position: value p % 4
+    // of piece p / 4), so a wave reads contiguous bytes either way
+    const bool tl = (VW == 4 || VW == 1) && !BF && a.tiled;
     int x, z0;
-    if (tl) {
-      tile_layout_position(p, a.Nb, x, z0);
+    if (tl && VW == 4) {
+      tile_layout_position(p, a.Nb, a.tiled, x, z0);
+    } else if (tl) {
+      tile_layout_position(p >> 2, a.Nb, a.tiled, x, z0);
+      z0 += p & 3;
     } else {
       x = p / bcv;
       z0 = (p - x * bcv) * VW;
     }
-    const uint32_t voff = tl ? (uint32_t)p * 16u : (uint32_t)(x * a.Nb + z0) * esz;
+    const uint32_t voff = tl ? (uint32_t)p * (uint32_t)(VW * 4) : (uint32_t)(x * a.Nb + z0) * esz;
     float acc[P::NB][VW];
 #pragma unroll
     for (int c = 0; c < P::NB; ++c)
@@ -959,8 +964,7 @@ int launch_recon_static(const ReconArgs& a, hipStream_t st) {
   // the kernel gives each thread exactly one position group
   if (recon_width(a) != VW || (long long)nblk * kThreads < (long long)a.Mb * (a.Nb / VW))
     return fail(FM_E_UNSUPPORTED, "reconstruction grid does not cover the block");
-  if (a.tiled && (VW != 4 || a.prod_bf16))
-    return fail(FM_E_UNSUPPORTED, "tiled products need fp32 values and 4 positions per thread");
+  if (a.tiled && a.prod_bf16) return fail(FM_E_UNSUPPORTED, "tiled products need fp32 values");
   if (a.prod_bf16)
     recon_static_kernel<P, VW, true><<<nblk * a.G, kThreads, 0, st>>>(a, nblk);
   else

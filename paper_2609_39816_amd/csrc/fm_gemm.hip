@@ -9,6 +9,9 @@
 //                    any inner length that is a multiple of 16.
 #include <hip/hip_runtime.h>
 
+#include <cstdlib>
+#include <cstring>
+
 #include "fm_device.h"
 #include "fm_lds_ring.h"
 
@@ -549,10 +552,375 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
   }
 }
 
+
+// Wide-wave persistent kernel (tensor or row/column scales, bf16 products,
+// Mb a multiple of 512, Nb of 128, Kb of 64): workgroup tile 512 x 128, 4
+// waves (one per SIMD), each wave 128 rows x 128 columns = 4 x 4 tiles of
+// 32 x 32 (v_mfma_f32_32x32x16_bf16), K step 64 bytes, a ring of 4 LDS
+// stages of 40 KB (512 + 128 rows of 64 bytes; all 160 KB of the CU's LDS)
+// filled by direct global-to-LDS loads, three K steps ahead.  A wave's tile shares every widened A fragment among
+// 4 column tiles and every B fragment among 4 row tiles: per flop half the
+// widening conversions of the 64 x 64 waves of gemm_dma_kernel.  With one
+// wave per SIMD the accumulators (256 per lane) live in the accumulation
+// registers, and the conversions of the next sub-step and the fragment reads
+// of the next stage sit between the matrix instructions of this one.
+//
+// Within a K step, lane (r, h) = (lane % 32, lane / 32) of a 32-row fragment
+// holds the 32 bytes [32h, 32h + 32) of row r; sub-step t (16 k values)
+// takes bytes [8t, 8t + 8) of them, for both operands alike (the 64 k values
+// of the step are summed in another order than in gemm_dma_kernel: the
+// products are exact, the fp32 sums differ only by rounding).  Rows of 64
+// bytes hold their 4 chunks XOR-swizzled by (row / 4) % 4: the 16 lanes
+// served per LDS cycle of a 16-byte fragment read (16 consecutive rows, 4
+// rows per 256-byte bank window) then hit 16 distinct 16-byte bank groups.
+namespace wide {
+constexpr int BM = 512, BN = 128, KS = 64, NT = 256, NSTG = 4;
+constexpr int ROWS = BM + BN;         // rows of KS bytes per stage
+constexpr int STAGE = ROWS * KS;      // 40 KB
+constexpr int LOADS = ROWS / 16 / 4;  // 1 KB wave-loads per wave per stage (10)
+constexpr int STORES = 64;            // 16-byte stores per lane per tile
+
+// global_load_lds_dwordx4 with a scalar base and a 32-bit per-lane offset:
+// lane L writes the 16 bytes it fetched at M0 + 16 L (M0 written by SALU
+// then read by an LDS-DMA load needs one wait state)
+__device__ __forceinline__ void dma16s(const void* sbase, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds_addr)
+               : "memory", "m0");
+}
+
+// s_waitcnt on the vector-memory counter only, for the few counts used (a
+// count above the largest encodable, 63, waits for more than needed)
+__device__ __forceinline__ void wait_vm(int n) {
+  if (n >= 63) ring::wait_vm_n<63>();
+  else if (n >= 2 * LOADS) ring::wait_vm_n<2 * LOADS>();
+  else if (n >= LOADS) ring::wait_vm_n<LOADS>();
+  else ring::wait_vm_n<0>();
+}
+}  // namespace wide
+
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+// Scheduling-group barriers for one region: 16 times one matrix
+// instruction followed by N instructions of class MASK (0x002 vector ALU,
+// 0x100 LDS reads).
+template <int MASK, int N>
+__device__ __forceinline__ void interleave() {
+  sfor<0, 16>([&](auto) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(MASK, N, 0);
+  });
+}
+
+template <int FMT, int SC>
+__global__ __launch_bounds__(wide::NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemm_wide_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict__ Sq,
+                      const float* __restrict__ dT, const float* __restrict__ dS,
+                      float* __restrict__ Mout, int Mb, int Nb, int Kb, int tiles_m, int tiles_n,
+                      int total, int tiled) {
+  using namespace wide;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[NSTG * STAGE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r32 = lane & 31, h = lane >> 5;
+  const int tiles = tiles_m * tiles_n;
+  const int nk = Kb / KS;
+
+  // workgroups go round-robin over the 8 XCDs: give each XCD a contiguous
+  // range of tiles (whole products), so a product's operand panels stay in
+  // one L2
+  const int G = gridDim.x;
+  const bool xcd_split = (G & 7) == 0 && (total & 7) == 0;
+  const int t = xcd_split ? (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+  const int tstep = xcd_split ? (G >> 3) : G;
+  const int t_end = xcd_split ? ((blockIdx.x & 7) + 1) * (total >> 3) : total;
+  if (t >= t_end) return;
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)lds;
+
+  // A wave-load fills 16 rows of 64 bytes: lane L writes row L / 4, slot L %
+  // 4, and fetches the chunk (L % 4) ^ ((row / 4) % 4); rows start at
+  // multiples of 16, so the chunk and the row's offset in the operand depend
+  // on the lane alone (one 32-bit offset), and the row block's address is
+  // uniform (a scalar base).  Wave w loads its own 128 A rows (8 wave-loads)
+  // and B rows [32 w, 32 w + 32) (2 wave-loads).
+  const uint32_t dma_off =
+      (uint32_t)(lane >> 2) * (uint32_t)Kb + (uint32_t)(((lane & 3) ^ ((lane >> 4) & 3)) << 4);
+  const size_t kb16 = (size_t)16 * Kb;
+  // first rows of a tile's A and B panels
+  auto tile_base = [&](int tile, const uint8_t*& Ab, const uint8_t*& Bb) {
+    const int b = tile / tiles, tt = tile - b * tiles;
+    const int tmi = tt / tiles_n;
+    Ab = Tq + ((size_t)b * Mb + (size_t)tmi * BM + (size_t)wave * 128) * Kb;
+    Bb = Sq + ((size_t)b * Nb + (size_t)(tt - tmi * tiles_n) * BN + (size_t)wave * 32) * Kb;
+  };
+  auto issue = [&](const uint8_t* Ab, const uint8_t* Bb, int kt, int buf) {
+    const uint32_t l0 = lds_base + (uint32_t)(buf * STAGE);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      dma16s(Ab + j * kb16 + kt * KS, dma_off, l0 + (uint32_t)((wave * 128 + 16 * j) * KS));
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      dma16s(Bb + j * kb16 + kt * KS, dma_off, l0 + (uint32_t)((BM + wave * 32 + 16 * j) * KS));
+  };
+
+  // one stage's raw codes: A rows 128 wave + 32 i + r32, B rows 32 j + r32,
+  // 32 bytes each (two 16-byte chunks)
+  uint4 ra[4][2], rb[4][2];
+  // the swizzle of rows 32 i + r32 is (r32 / 4) % 4 for every i: per-lane
+  // offsets of the two chunks, plus compile-time row-block offsets
+  const uint32_t rd0 = (uint32_t)r32 * KS + (uint32_t)(((2 * h) ^ ((r32 >> 2) & 3)) << 4);
+  const uint32_t rd1 = (uint32_t)r32 * KS + (uint32_t)(((2 * h + 1) ^ ((r32 >> 2) & 3)) << 4);
+  auto read_stage = [&](int buf) {
+    const uint8_t* sa = lds + buf * STAGE + wave * 128 * KS;
+    const uint8_t* sb = lds + buf * STAGE + BM * KS;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ra[i][0] = *reinterpret_cast<const uint4*>(sa + i * 32 * KS + rd0);
+      ra[i][1] = *reinterpret_cast<const uint4*>(sa + i * 32 * KS + rd1);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      rb[j][0] = *reinterpret_cast<const uint4*>(sb + j * 32 * KS + rd0);
+      rb[j][1] = *reinterpret_cast<const uint4*>(sb + j * 32 * KS + rd1);
+    }
+  };
+  auto sel = [](const uint4 (&r)[2], int t, int d) -> int {
+    const uint4& c = r[t >> 1];
+    return (t & 1) ? (d ? (int)c.w : (int)c.z) : (d ? (int)c.y : (int)c.x);
+  };
+  v8bf wa[3][4], wb[3][4];  // widened fragments of three sub-steps
+  auto widen_sub = [&](int t, int slot) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) wa[slot][i] = widen8<FMT>(sel(ra[i], t, 0), sel(ra[i], t, 1));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) wb[slot][j] = widen8<FMT>(sel(rb[j], t, 0), sel(rb[j], t, 1));
+  };
+  // makes a slot's values appear used here, so their conversions stay in
+  // the phase that computes them (instead of sinking towards their use)
+  auto pin = [&](int slot) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      asm volatile("" : "+v"(wa[slot][i]));
+      asm volatile("" : "+v"(wb[slot][i]));
+    }
+  };
+
+  // acc[i][j] holds the transposed 32 x 32 product: element v of lane
+  // (r32, h) is output row i*32 + r32, column j*32 + 8 (v / 4) + 4 h + v % 4
+  // of the wave's 128 x 128 block
+  v16f acc[4][4];
+  auto mma = [&](int slot) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb[slot][j], wa[slot][i], acc[i][j], 0, 0, 0);
+  };
+
+  auto epilogue = [&](int tile) {
+    const int b = tile / tiles, tt = tile - b * tiles;
+    const int tmi = tt / tiles_n;
+    const int m0 = tmi * BM, n0 = (tt - tmi * tiles_n) * BN;
+    float* Mo = Mout + (size_t)b * Mb * Nb;
+    const int r_base = m0 + wave * 128 + r32, c_base = n0 + 4 * h;
+    // tiled layout: the 16-byte pieces of a tile in the order (wave, i, j,
+    // column group g, lane), so each store of a wave is one contiguous
+    // kilobyte
+    float* tbase = Mo + (size_t)tt * (BM * BN) + (size_t)wave * (128 * 128) + lane * 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = r_base + i * 32;
+      const float sT = SC == 1 ? dT[(size_t)b * Mb + row] : dT[b];
+      float* prow = Mo + (size_t)row * Nb + c_base;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          float4 sS;
+          if constexpr (SC == 1) {
+            sS = *reinterpret_cast<const float4*>(dS + (size_t)b * Nb + c_base + j * 32 + 8 * g);
+          } else {
+            const float u = dS[b];
+            sS = make_float4(u, u, u, u);
+          }
+          v4f o;
+          o[0] = (acc[i][j][4 * g + 0] * sT) * sS.x;
+          o[1] = (acc[i][j][4 * g + 1] * sT) * sS.y;
+          o[2] = (acc[i][j][4 * g + 2] * sT) * sS.z;
+          o[3] = (acc[i][j][4 * g + 3] * sT) * sS.w;
+          if (tiled)
+            __builtin_nontemporal_store(o, reinterpret_cast<v4f*>(tbase + ((i * 4 + j) * 4 + g) * 256));
+          else
+            *reinterpret_cast<v4f*>(prow + j * 32 + 8 * g) = o;
+        }
+      }
+    }
+  };
+
+  // Sequence of (tile, K-step) pairs p_0, p_1, ...; p_s lives in LDS buffer
+  // s mod 4, and its 4 sub-steps run in order.  Iteration s, in four phases
+  // whose instructions are interleaved with the matrix instructions (each
+  // region's order fixed by scheduling-group barriers or program order):
+  //   A: sub-step 0 of p_s, widening sub-step 1;
+  //   B: sub-step 1, widening sub-steps 2 and 3 (the raw codes of p_s are
+  //      then dead);
+  //   wait until p_{s+1} has landed and every wave is done reading p_s;
+  //   C: sub-step 2, reading p_{s+1} from LDS and starting the loads of
+  //      p_{s+4} into the buffer of p_s;
+  //   D: sub-step 3, widening sub-step 0 of p_{s+1}.
+  // The loads run ahead across tile boundaries; the accumulators are
+  // cleared at the start of a tile and stored after its last K step.
+  auto advance = [&](int& tt, int& kk) {
+    if (++kk == nk) {
+      kk = 0;
+      tt += tstep;
+    }
+  };
+  int t1 = t, k1 = 0;  // p_{s+1}
+  advance(t1, k1);
+  int t2 = t1, k2 = k1;  // p_{s+2}
+  advance(t2, k2);
+  int t3 = t2, k3 = k2;  // p_{s+3}
+  advance(t3, k3);
+  int t4 = t3, k4 = k3;  // p_{s+4}
+  advance(t4, k4);
+  const uint8_t *A0, *B0;  // panels of the tile being issued
+  tile_base(t, A0, B0);
+  issue(A0, B0, 0, 0);
+  int after1 = 0;  // vector-memory operations issued after the group of p_{s+1}
+  if (t1 < t_end) {
+    if (t1 != t) tile_base(t1, A0, B0);
+    issue(A0, B0, k1, 1);
+  }
+  if (t2 < t_end) {
+    if (t2 != t1) tile_base(t2, A0, B0);
+    issue(A0, B0, k2, 2);
+    after1 += LOADS;
+  }
+  if (t3 < t_end) {
+    if (t3 != t2) tile_base(t3, A0, B0);
+    issue(A0, B0, k3, 3);
+    after1 += LOADS;
+  }
+  int after2 = t3 < t_end ? LOADS : 0;  // operations issued after the group of p_{s+2}
+  const uint8_t *A4 = A0, *B4 = B0;  // panels of the tile of p_{s+4}
+  if (t4 < t_end && t4 != t3) tile_base(t4, A4, B4);
+  wait_vm(t1 < t_end ? after1 + LOADS : 0);  // p_0 has landed
+  FM_COMPILER_FENCE();
+  __builtin_amdgcn_s_barrier();
+  FM_COMPILER_FENCE();
+  read_stage(0);
+  widen_sub(0, 0);
+  int cb = 0;  // buffer of p_s
+  bool more = true;
+  for (int tile = t; more; tile += tstep) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+    for (int kk = 0; kk < nk; ++kk) {
+      // A
+      mma(0);
+      widen_sub(1, 1);
+      interleave<0x002, 2>();
+      pin(1);
+      __builtin_amdgcn_sched_barrier(0);
+      // B
+      mma(1);
+      widen_sub(2, 2);
+      widen_sub(3, 0);
+      interleave<0x002, 4>();
+      pin(2);
+      pin(0);
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vm(after1);                     // p_{s+1} has landed (this wave's share)
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of p_s are done
+      FM_COMPILER_FENCE();
+      __builtin_amdgcn_s_barrier();
+      FM_COMPILER_FENCE();
+      const int nb = cb == NSTG - 1 ? 0 : cb + 1;
+      const bool iss = t4 < t_end;
+      const int after3 = iss ? LOADS : 0;  // operations issued after the group of p_{s+3}
+      FM_COMPILER_FENCE();
+      more = t1 < t_end;
+      // C: the reads of p_{s+1} (after the last pair a stale stage, never
+      // used), then the loads of p_{s+4} into the buffer of p_s, one after
+      // each of the first ten matrix instructions
+      read_stage(nb);
+      {
+        const uint32_t l0 = lds_base + (uint32_t)(cb * STAGE);
+        const uint8_t* pa = A4 + k4 * KS;
+        const uint8_t* pb = B4 + k4 * KS;
+        sfor<0, 16>([&](auto qc) {
+          constexpr int q = decltype(qc)::value;
+          acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb[2][q & 3], wa[2][q >> 2], acc[q >> 2][q & 3], 0, 0, 0);
+          if constexpr (q < 8) {
+            if (iss) dma16s(pa + q * kb16, dma_off, l0 + (uint32_t)((wave * 128 + 16 * q) * KS));
+          } else if constexpr (q < 10) {
+            if (iss) dma16s(pb + (q - 8) * kb16, dma_off, l0 + (uint32_t)((BM + wave * 32 + 16 * (q - 8)) * KS));
+          }
+        });
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      // D
+      mma(0);
+      widen_sub(0, 1);
+      interleave<0x002, 2>();
+      pin(1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        wa[0][i] = wa[1][i];
+        wb[0][i] = wb[1][i];
+      }
+      t1 = t2;
+      k1 = k2;
+      t2 = t3;
+      k2 = k3;
+      t3 = t4;
+      k3 = k4;
+      advance(t4, k4);
+      if (k4 == 0 && t4 < t_end) tile_base(t4, A4, B4);
+      after1 = after2 + after3;
+      after2 = after3;
+      cb = nb;
+    }
+    epilogue(tile);
+    after1 += STORES;
+    after2 += STORES;
+  }
+}
+
 }  // namespace
 
 namespace {
 int g_block_product_arith = FM_ACC_BF16;
+
+// The wide-wave kernel is the default where it applies; FM_BLOCK_GEMM=dma
+// in the environment selects gemm_dma_kernel instead (for comparisons).
+bool wide_enabled() {
+  static const bool on = [] {
+    const char* e = std::getenv("FM_BLOCK_GEMM");
+    return !(e && std::strcmp(e, "dma") == 0);
+  }();
+  return on;
+}
+
+bool use_wide(int Mb, int Nb, int Kb, int sc, bool out_bf16) {
+  return wide_enabled() && g_block_product_arith == FM_ACC_BF16 && (sc == 0 || sc == 1) &&
+         !out_bf16 && Mb % wide::BM == 0 && Nb % wide::BN == 0 && Kb % wide::KS == 0;
+}
+}  // namespace
+
+int block_gemm_tile_rows(int Mb, int Nb, int Kb, int scale_mode, bool out_bf16) {
+  const int sc = scale_mode == FM_SCALE_ROWCOL ? 1 : (scale_mode == FM_SCALE_GROUP ? 2 : 0);
+  if (use_wide(Mb, Nb, Kb, sc, out_bf16)) return wide::BM;
+  if (Kb % GK == 0) return DBM;
+  return 0;
 }
 
 int set_block_product_arith(int a) {
@@ -567,6 +935,23 @@ int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, 
                          float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, hipStream_t st,
                          int tiled = 0) {
   const bool fp8acc = g_block_product_arith == FM_ACC_FP8;
+  if (use_wide(Mb, Nb, Kb, SC, OB)) {
+    if constexpr (SC == 0 || SC == 1) {
+      // persistent: one 160 KB-LDS workgroup of 4 waves per CU
+      const int tm = Mb / wide::BM, tn = Nb / wide::BN;
+      const long long total = (long long)batch * tm * tn;
+      if (total > 0x7fffffffLL) return fail(FM_E_SHAPE, "too many GEMM tiles in one launch");
+      const int T = (int)total;
+      const int grid = (int)std::min<long long>(total, 256);
+      if (tiled && SC != 0)
+        return fail(FM_E_UNSUPPORTED, "the tiled product layout needs tensor scales");
+      if (fmt == FM_E4M3)
+        gemm_wide_kernel<FM_E4M3, SC><<<grid, wide::NT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
+      else
+        gemm_wide_kernel<FM_E5M2, SC><<<grid, wide::NT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
+      return launched("gemm_wide_kernel");
+    }
+  }
   if (Kb % GK == 0) {
     // pipelined persistent kernel: one 144 KB-LDS workgroup per CU
     const int tm = (Mb + DBM - 1) / DBM, tn = (Nb + DBN - 1) / DBN;

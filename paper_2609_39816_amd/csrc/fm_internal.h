@@ -152,25 +152,46 @@ int set_block_product_arith(int a);
 // (FM_SCALE_ROWCOL).
 // out_bf16 (group scales only): the products, bf16 values, are stored as
 // bf16 (2 bytes each, uint16_t at Mout) instead of fp32.
-// tiled (tensor scales, Mb a multiple of 256, Nb of 128, Kb of 128): each
-// product is stored tile by tile (tile_layout_offset below) instead of row
-// by row.
+// tiled (tensor scales, whole tiles of the kernel that runs, see
+// block_gemm_tile_rows): each product is stored tile by tile
+// (tile_layout_position below) instead of row by row.
 int launch_block_gemm(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
                       float* Mout, int batch, int Mb, int Nb, int Kb, int fmt, int scale_mode,
                       hipStream_t st, bool out_bf16 = false, bool tiled = false);
 
-// The tiled layout of a product block (Mb x Nb, whole 256 x 128 tiles): the
-// 16-byte piece p (4 consecutive columns of one row) sits at byte 16 p, with
-// p = (((t 8 + w) 4 + i) 4 + j) 64 + 4 l + c for the tile t (row-major over
-// the block's tiles), the 64 x 64 quarter w = 2 (row / 64 % 4) + (column / 64
-// % 2), i = row / 16 % 4, j = column / 16 % 4, l = row % 16 and c = column /
-// 4 % 4.  The block-product kernel stores each wave's piece of a tile as one
-// contiguous kilobyte; the reconstruction reads pieces in this order.
-__host__ __device__ inline void tile_layout_position(int p, int Nb, int& row, int& col) {
-  const int l = (p >> 2) & 15, c = p & 3, j = (p >> 6) & 3, i = (p >> 8) & 3, w = (p >> 10) & 7;
-  const int t = p >> 13, tn = Nb / 128, tm = t / tn;
-  row = tm * 256 + (w >> 1) * 64 + i * 16 + l;
-  col = (t - tm * tn) * 128 + (w & 1) * 64 + j * 16 + 4 * c;
+// Rows of the output tile of the block-product kernel launch_block_gemm
+// runs for these arguments: 512 (gemm_wide_kernel: bf16 arithmetic, tensor
+// or row/column scales, fp32 products, Mb a multiple of 512, Nb of 128, Kb
+// of 64), 256 (gemm_dma_kernel: Kb a multiple of 128), 0 otherwise.  Tiles
+// are 128 columns wide.
+int block_gemm_tile_rows(int Mb, int Nb, int Kb, int scale_mode, bool out_bf16);
+
+// The tiled layout of a product block (Mb x Nb, whole TR x 128 tiles, TR =
+// 256 or 512): the 16-byte piece p (4 consecutive columns of one row) sits
+// at byte 16 p, t being the tile (row-major over the block's tiles).  For
+// TR = 256, p = (((t 8 + w) 4 + i) 4 + j) 64 + 4 l + c with the 64 x 64
+// quarter w = 2 (row / 64 % 4) + (column / 64 % 2), i = row / 16 % 4, j =
+// column / 16 % 4, l = row % 16 and c = column / 4 % 4.  For TR = 512, p =
+// ((((t 4 + w) 4 + i) 4 + j) 4 + g) 64 + 32 h + r with the 128-row quarter
+// w = row / 128 % 4, i = row / 32 % 4, r = row % 32, j = column / 32 % 4,
+// g = column / 8 % 4 and h = column / 4 % 2.  The block-product kernel
+// stores each wave's piece of a tile as one contiguous kilobyte; the
+// reconstruction reads pieces in this order.
+__host__ __device__ inline void tile_layout_position(int p, int Nb, int TR, int& row, int& col) {
+  const int tn = Nb / 128;
+  if (TR == 512) {
+    const int r = p & 31, h = (p >> 5) & 1, g = (p >> 6) & 3, j = (p >> 8) & 3;
+    const int i = (p >> 10) & 3, w = (p >> 12) & 3;
+    const int t = p >> 14, tm = t / tn;
+    row = tm * 512 + w * 128 + i * 32 + r;
+    col = (t - tm * tn) * 128 + j * 32 + 8 * g + 4 * h;
+  } else {
+    const int l = (p >> 2) & 15, c = p & 3;
+    const int j = (p >> 6) & 3, i = (p >> 8) & 3, w = (p >> 10) & 7;
+    const int t = p >> 13, tm = t / tn;
+    row = tm * 256 + (w >> 1) * 64 + i * 16 + l;
+    col = (t - tm * tn) * 128 + (w & 1) * 64 + j * 16 + 4 * c;
+  }
 }
 
 // Reconstruction + error: for gauge g < G, C_g = sum_r w M_{g,r}; if C is not
@@ -187,7 +208,8 @@ struct ReconArgs {
   double* partial;     // G x nblk (if Cref)
   const float* rowscale = nullptr;  // optional: output row i*Mb + x times rowscale[i*Mb + x]
   int prod_bf16 = 0;  // products stored as bf16 (uint16_t at Mprod; group scales)
-  int tiled = 0;      // products in the tiled layout (fp32, 4 positions per thread)
+  int tiled = 0;      // products in the tiled layout of tiles of this many rows
+                      // (256 or 512; fp32, 4 positions per thread), or 0
 };
 // Positions per thread in the reconstruction kernels (4 or 1) and the
 // number of workgroups per gauge (one position group per thread).

@@ -277,9 +277,9 @@ def block_products(Tq, Sq, dT, dS, fmt: int = E4M3, out=None, stream=None,
     if (dT.numel(), dS.numel()) != want:
         raise ValueError(f"scale arrays hold {dT.numel()} and {dS.numel()} values, need {want}")
     _cuda(dT, torch.float32), _cuda(dS, torch.float32)
-    if scale_mode == SCALE_GROUP:
-        # the kernel reads scales in aligned 16-byte chunks: give it a fresh,
-        # padded copy whenever the caller's arrays are not such
+    if scale_mode in (SCALE_ROWCOL, SCALE_GROUP):
+        # the kernels read scales in aligned 16-byte chunks: give them a
+        # fresh, padded copy whenever the caller's arrays are not such
         def padded(t):
             if t.data_ptr() % 16 == 0 and t.numel() % 4 == 0:
                 return t

@@ -274,3 +274,19 @@ def test_joint_rounding_beyond_64_products_is_refused_up_front():
                                         fm.SCALE_GROUP | fm.REPAIR_ROWS, fake, fake, fake, fake,
                                         fake, 0, None)
     assert rc == ERR["FM_E_WORKSPACE"]  # rows alone pass the check, then the workspace is short
+
+
+def test_misaligned_scale_arrays_are_refused_before_any_device_work():
+    """The block-product kernels read scale arrays in aligned 16-byte chunks:
+    fm_block_products_scaled refuses misaligned per-column and group scales
+    on the host (no pointer is dereferenced)."""
+    L = fm.lib
+    p = ct.c_void_p
+    good, bad = 0x10000, 0x10004  # never dereferenced: the checks come first
+    rc = L.fm_block_products_scaled(p(good), p(good), p(good), p(bad), 2, 512, 128, 128,
+                                    fm.E4M3, fm.SCALE_ROWCOL, p(good), None)
+    assert fm.ERRORS[rc] == "FM_E_ARG" and "aligned" in L.fm_last_error().decode()
+    for dT, dS in ((bad, good), (good, bad)):
+        rc = L.fm_block_products_scaled(p(good), p(good), p(dT), p(dS), 2, 512, 128, 128,
+                                        fm.E4M3, fm.SCALE_GROUP, p(good), None)
+        assert fm.ERRORS[rc] == "FM_E_ARG" and "aligned" in L.fm_last_error().decode()

@@ -295,10 +295,16 @@ def test_block_products_over_every_code():
     (9, 512, 256, 1024),   # interior tiles only, eight K steps
     (12, 200, 130, 256),   # a row length not a multiple of 4 (element stores)
     (5, 72, 80, 96),       # inner length not a multiple of 128
+    # the wide-wave kernel (512 x 128 tiles, K steps of 64):
+    (5, 512, 128, 64),     # one tile and one K step per product
+    (40, 512, 128, 192),   # three K steps: a ring turn per tile; 40 tiles
+    (7, 1536, 384, 128),   # 63 tiles (not a multiple of 8)
+    (30, 1024, 640, 128),  # 300 tiles: several per workgroup
+    (3, 1024, 640, 3456),  # the three-level projection shape's products
 ])
 def test_block_products_tilings(batch, Mb, Nb, Kb):
     """Batched block products over tilings that exercise the persistent
-    pipelined kernel (ring wrap-around, tile changes inside the ring, ragged
+    pipelined kernels (ring wrap-around, tile changes inside the ring, ragged
     edges) against the exact sums rounded once."""
     say(f"[parity] block products batch {batch} {Mb}x{Nb}x{Kb}")
     rng = np.random.default_rng(batch * 7 + Kb)
@@ -311,6 +317,24 @@ def test_block_products_tilings(batch, Mb, Nb, Kb):
     got = fm.block_products(gpu(Tq), gpu(Sq), gpu(dT), gpu(dS), fm.E4M3).cpu().numpy()
     for b in sorted({0, 1, batch // 2, batch - 1}):
         want = oracle.block_product(Tq[b], Sq[b].T, dT[b], dS[b], oracle.E4M3)
+        assert rel(got[b], want) <= 1e-6, f"product {b}: rel {rel(got[b], want):.2e}"
+
+
+def test_block_products_rowcol_scales_wide_tiles():
+    """Per-row and per-column scales through the wide-wave kernel's epilogue
+    (512 x 128 tiles) against the oracle's scaled exact sums."""
+    rng = np.random.default_rng(17)
+    vals = oracle.fp8_decode(np.arange(256, dtype=np.uint8), oracle.E4M3)
+    finite = np.nonzero(np.isfinite(vals))[0].astype(np.uint8)
+    batch, Mb, Nb, Kb = 4, 512, 256, 256
+    Tq = rng.choice(finite, size=(batch, Mb, Kb)).astype(np.uint8)
+    Sq = rng.choice(finite, size=(batch, Nb, Kb)).astype(np.uint8)
+    dT = (rng.random((batch, Mb)) + 0.5).astype(np.float32)
+    dS = (rng.random((batch, Nb)) + 0.5).astype(np.float32)
+    got = fm.block_products(gpu(Tq), gpu(Sq), gpu(dT), gpu(dS), fm.E4M3,
+                            scale_mode=fm.SCALE_ROWCOL).cpu().numpy()
+    for b in range(batch):
+        want = oracle.block_product_rc(Tq[b], Sq[b].T, dT[b], dS[b], oracle.E4M3)
         assert rel(got[b], want) <= 1e-6, f"product {b}: rel {rel(got[b], want):.2e}"
 
 
@@ -385,18 +409,24 @@ def test_chunked_orbit_equals_single_launch_and_is_deterministic():
     # blocks of whole 256 x 128 tiles: the orbit passes its products to the
     # reconstruction in the tiled layout; its errors equal those of the
     # stand-alone row-major path (the same output bits, sums in another order)
-    wt = sy.scaled(sy.WORKLOADS["strassen1_256_gl64"], 512, 512, 256, G=6)
-    A, B = sy.operands(wt)
-    At, Bt = gpu(A), gpu(B)
-    hips, _, levels = schemes_for(wt, sy.gauges(wt))
-    Cref = fm.reference_f64(At, Bt)
-    for ch in (0, 2):
-        ws = None if ch == 0 else fm.workspace(
-            fm.workspace_size(hips[0], wt.M, wt.N, wt.K, levels, len(hips), ch))
-        errs = fm.orbit_eval(hips, At, Bt, Cref, levels, ws=ws)
-        for gi, h in enumerate(hips):
-            st = fm.error_stats(fm.matmul_lowp(h, At, Bt, levels), Cref)
-            assert abs(errs[gi] / st["rel_fro"] - 1) <= 1e-9, (ch, gi, errs[gi], st["rel_fro"])
+    # (blocks of 256 rows: 256 x 128 tiles; of 512 rows: the wide-wave
+    # kernel's 512 x 128 tiles; three-level Strassen: one position per
+    # thread of the reconstruction)
+    for (name, M, K, N) in (("strassen1_256_gl64", 512, 512, 256),
+                            ("strassen1_256_gl64", 1024, 256, 512),
+                            ("strassen3_8192x27648x5120_sign512", 4096, 512, 1024)):
+        wt = sy.scaled(sy.WORKLOADS[name], M, K, N, G=6 if name.startswith("strassen1") else 3)
+        A, B = sy.operands(wt)
+        At, Bt = gpu(A), gpu(B)
+        hips, _, levels = schemes_for(wt, sy.gauges(wt))
+        Cref = fm.reference_f64(At, Bt)
+        for ch in (0, 2):
+            ws = None if ch == 0 else fm.workspace(
+                fm.workspace_size(hips[0], wt.M, wt.N, wt.K, levels, len(hips), ch))
+            errs = fm.orbit_eval(hips, At, Bt, Cref, levels, ws=ws)
+            for gi, h in enumerate(hips):
+                st = fm.error_stats(fm.matmul_lowp(h, At, Bt, levels), Cref)
+                assert abs(errs[gi] / st["rel_fro"] - 1) <= 1e-9, (name, M, ch, gi, errs[gi], st["rel_fro"])
 
 
 def test_full_size_strassen2_workload_sampled():
