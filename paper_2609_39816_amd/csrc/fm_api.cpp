@@ -82,6 +82,7 @@ struct Tables {
   int G = 0, R = 0;
   Side s[3];
   std::vector<int> pat[3];
+  std::vector<char> trie[2];  // per gauge: coefficients fit the family's shared chains
   std::vector<int> hpat;  // family of each gauge's H support (joint rounding only)
 };
 
@@ -94,8 +95,17 @@ void append(Tables& T, const Lists& L, int R, const int nb[3]) {
     d.idx.insert(d.idx.end(), src[k]->idx.begin(), src[k]->idx.end());
     d.coef.insert(d.coef.end(), src[k]->coef.begin(), src[k]->coef.end());
     T.pat[k].push_back(match_pattern(k, *src[k], R, nb[k]));
+    if (k < 2) T.trie[k].push_back(trie_valid(T.pat[k].back(), k, *src[k]) ? 1 : 0);
   }
   T.G += 1;
+}
+
+// 1 if every gauge of [g0, g0 + n) may use its family's prefix-shared chains
+// on one side (A: 0, B: 1).
+int chunk_trie(const Tables& T, int side, int g0, int n) {
+  for (int g = g0; g < g0 + n; ++g)
+    if (!T.trie[side][g]) return 0;
+  return 1;
 }
 
 // Pattern shared by gauges [g0, g0 + n) on one side, or -1.
@@ -476,9 +486,13 @@ int form_codes_and_next_maxima(const Geometry& geo, const float* A, const float*
                                int fmt, uint8_t* Tq, uint8_t* Sq, hipStream_t st) {
   FormArgs qa, qb, ma, mb;
   tensor_form_args(geo, A, Bt, ws, L.set(c & 1), g0, n, fmt, Tq, Sq, qa, qb);
+  qa.trie = chunk_trie(T, 0, g0, n);
+  qb.trie = chunk_trie(T, 1, g0, n);
   const Layout Ln = L.set((c + 1) & 1);
   if (n1 > 0) {
     tensor_form_args(geo, A, Bt, ws, Ln, g0 + n, n1, fmt, Tq, Sq, ma, mb);
+    ma.trie = chunk_trie(T, 0, g0 + n, n1);
+    mb.trie = chunk_trie(T, 1, g0 + n, n1);
     if (int rc = launch_fill_u32(ma.amax, (size_t)2 * n1 * geo.R, 0u, st)) return rc;
   }
   for (int side = 0; side < 2; ++side) {
@@ -528,6 +542,8 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
               amax, q,     Tq,    fmt,    per_row, mode == FM_SCALE_GROUP ? 2 : 1};
   FormArgs fb{Bt, geo.N, geo.K, geo.gn, geo.gk, geo.Nb, geo.Kb, off(1), idx(1), coef(1), R, n,
               amax + na, q + na, Sq, fmt, per_row, mode == FM_SCALE_GROUP ? 3 : 1};
+  fa.trie = chunk_trie(T, 0, g0, n);
+  fb.trie = chunk_trie(T, 1, g0, n);
   if (int rc = launch_fill_u32(amax, na + nb, 0u, st)) return rc;
   for (int side = 0; side < 2; ++side) {
     timing_begin(T_FORM_AMAX, st);
@@ -1266,6 +1282,8 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
     const int n0 = std::min(chunk, G);
     FormArgs fa, fb;
     tensor_form_args(geo, Aform, Bt, ws, L, 0, n0, fmt, Tq, Sq, fa, fb);
+    fa.trie = chunk_trie(T, 0, 0, n0);
+    fb.trie = chunk_trie(T, 1, 0, n0);
     if ((rc = launch_fill_u32(fa.amax, (size_t)2 * n0 * geo.R, 0u, st))) return rc;
     for (int side = 0; side < 2; ++side) {
       timing_begin(T_FORM_AMAX, st);

@@ -358,7 +358,8 @@ __device__ __forceinline__ void form_static_gauges(const FormArgs& a, int g0, in
               float mf = 0.0f;
 #pragma unroll
               for (int v = 0; v < VW; ++v) mf = __builtin_elementwise_maximum(mf, __builtin_fabsf(acc[v]));
-              lm[j] = active ? __float_as_uint(mf) : 0u;
+              // inactive lanes hold zero operands: their sums and maxima are +0
+              lm[j] = __float_as_uint(mf);
             } else {
               const float q = ROWS ? qv[j] : ro(a.q)[(size_t)g * P::R + r + so];
               form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, acc, q);
@@ -438,6 +439,87 @@ __device__ __forceinline__ void form_static_gauges(const FormArgs& a, int g0, in
 }
 
 
+// Gauges g0 <= g < g1 through the family's prefix-shared chains (P::TRIE,
+// one scale per tensor): chains that begin with the same (block,
+// coefficient) entries share their partial sums, so the block sums are the
+// nodes of a trie walked depth first: node t = fmaf(coef[tent[t]],
+// x[tblk[t]], value of the latest node one level up, or +0 at the root).
+// The value of the node where a product's chain ends is that product's
+// block sum, with the fused multiply-adds of its chain in its order, so the
+// bits are those of form_static_gauges.  (The host uses this form only for
+// gauges whose coefficients agree on every shared entry, P::tchk.)  Mode 0
+// reduces products' maxima in groups of 8 in completion order; mode 1
+// encodes and stores each product's codes as it completes.
+template <class P, int VW, int MODE, int FMT>
+__device__ __forceinline__ void form_trie_gauges(const FormArgs& a, int g0, int g1,
+                                                 const float (&xv)[P::NB][VW],
+                                                 [[maybe_unused]] bool active, uint32_t voff,
+                                                 uint32_t* smax) {
+  constexpr int GR = 8;
+  const int lane = threadIdx.x & 63;
+  const uint32_t bsz = (uint32_t)a.br * (uint32_t)a.bc;
+  for (int g = g0; g < g1; ++g) {
+    const auto coef = ro(a.coef) + ro(a.off)[(size_t)g * (P::R + 1)];
+    __amdgpu_buffer_rsrc_t rsrc;
+    if constexpr (MODE == 1)
+      rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + (size_t)g * P::R * bsz, (short)0,
+                                               (int)(P::R * bsz), 0x00020000);
+    float nv[P::MAXD][VW];
+    [[maybe_unused]] uint32_t lm[GR];
+    // coefficient loads through an offset the compiler cannot see through,
+    // renewed every 16 nodes, so the scalar loads stay near their nodes
+    int so = 0;
+    sfor<0, P::NN>([&](auto tc) {
+      constexpr int t = decltype(tc)::value;
+      if constexpr (t % 16 == 0) {
+        so = 0;
+        asm volatile("" : "+s"(so));
+      }
+      constexpr int d = P::tdepth[t], b = P::tblk[t], e = P::tent[t];
+      const float c = coef[e + so];
+#pragma unroll
+      for (int v = 0; v < VW; ++v) {
+        if constexpr (d == 0) nv[0][v] = __builtin_fmaf(c, xv[b][v], 0.0f);
+        else nv[d][v] = __builtin_fmaf(c, xv[b][v], nv[d - 1][v]);
+      }
+      sfor<P::tendptr[t], P::tendptr[t + 1]>([&](auto kc) {
+        constexpr int kk = decltype(kc)::value, r = P::tendprod[kk];
+        if constexpr (MODE == 0) {
+          float mf = 0.0f;
+#pragma unroll
+          for (int v = 0; v < VW; ++v) mf = __builtin_elementwise_maximum(mf, __builtin_fabsf(nv[d][v]));
+          lm[kk % GR] = __float_as_uint(mf);  // +0 on inactive lanes (zero operands)
+          if constexpr (kk % GR == GR - 1 || kk == P::R - 1) {
+            // row maxima of the group's products (DPP shifts 1, 2, 4, 8;
+            // lane 15 of each row then holds its row's maximum), kept in
+            // the (wave, row) slots of each product
+            constexpr int NJ = kk % GR + 1, k0 = kk - kk % GR;
+            sfor<0, 4>([&](auto sc) {
+              constexpr int ctl = 0x111 + (1 << decltype(sc)::value) - 1;  // row_shr:1,2,4,8
+              uint32_t sh[NJ];
+#pragma unroll
+              for (int j = 0; j < NJ; ++j)
+                sh[j] = (uint32_t)__builtin_amdgcn_mov_dpp((int)lm[j], ctl, 0xf, 0xf, true);
+#pragma unroll
+              for (int j = 0; j < NJ; ++j) lm[j] = max(lm[j], sh[j]);
+            });
+            if ((lane & 15) == 15) {
+              uint32_t* base = smax + (size_t)(g - g0) * P::R * 16 + (threadIdx.x >> 4);
+              sfor<0, NJ>([&](auto jc) {
+                constexpr int j = decltype(jc)::value, rj = P::tendprod[k0 + j];
+                base[rj * 16] = max(base[rj * 16], lm[j]);
+              });
+            }
+          }
+        } else {
+          const float q = ro(a.q)[(size_t)g * P::R + r + so];
+          form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, nv[d], q);
+        }
+      });
+    });
+  }
+}
+
 template <class P, int VW, int MODE, int FMT, bool ROWS>
 __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uint32_t* smax) {
   const int bcv = a.bc / VW;
@@ -452,7 +534,10 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
     const uint32_t voff = active ? (uint32_t)(x * a.bc + y0) : 0x80000000u;
     float xv[P::NB][VW];
     form_load<P::NB, VW>(a, xv, active, x, y0);
-    form_static_gauges<P, VW, MODE, FMT, ROWS>(a, g0, g1, xv, active, x, y0, voff, smax);
+    if constexpr (P::TRIE && !ROWS)
+      form_trie_gauges<P, VW, MODE, FMT>(a, g0, g1, xv, active, voff, smax);
+    else
+      form_static_gauges<P, VW, MODE, FMT, ROWS>(a, g0, g1, xv, active, x, y0, voff, smax);
   }
 }
 
@@ -522,8 +607,13 @@ __global__ __launch_bounds__(kThreads) void form_merged_kernel(FormArgs aq, Form
     const uint32_t voff = active ? (uint32_t)(x * aq.bc + y0) : 0x80000000u;
     float xv[P::NB][VW];
     form_load<P::NB, VW>(aq, xv, active, x, y0);
-    form_static_gauges<P, VW, 1, FMT, false>(aq, g0q, g1q, xv, active, x, y0, voff, smax);
-    form_static_gauges<P, VW, 0, FM_E4M3, false>(am, g0m, g1m, xv, active, x, y0, voff, smax);
+    if constexpr (P::TRIE) {
+      form_trie_gauges<P, VW, 1, FMT>(aq, g0q, g1q, xv, active, voff, smax);
+      form_trie_gauges<P, VW, 0, FM_E4M3>(am, g0m, g1m, xv, active, voff, smax);
+    } else {
+      form_static_gauges<P, VW, 1, FMT, false>(aq, g0q, g1q, xv, active, x, y0, voff, smax);
+      form_static_gauges<P, VW, 0, FM_E4M3, false>(am, g0m, g1m, xv, active, x, y0, voff, smax);
+    }
   }
   __syncthreads();
   const int n = max(0, g1m - g0m) * P::R;
@@ -923,6 +1013,9 @@ int launch_form_merged(const FormArgs& aq, const FormArgs& am, hipStream_t st) {
 template <class P>
 bool static_ok(const FormArgs& a) {
   constexpr int VW = static_vw<P>();
+  // prefix-shared families: tensor scales only for gauges whose
+  // coefficients agree on the shared entries (a.trie); others go generic
+  if (P::TRIE && !a.per_row && !a.trie) return false;
   return a.gr * a.gc == P::NB && a.R == P::R && a.bc % VW == 0 && (VW < 4 || a.cols % 4 == 0) &&
          (size_t)P::R * a.br * a.bc < ((size_t)1 << 31);
 }

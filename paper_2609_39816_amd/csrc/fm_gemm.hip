@@ -231,10 +231,12 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
   const bool vec_store = (Nb & 3) == 0;
 
   const int G = gridDim.x;
-  const bool xcd_split = (G & 7) == 0 && (total & 7) == 0;
-  const int t = xcd_split ? (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+  // (XCD x takes tiles [x per, (x + 1) per), per = ceil(total / 8))
+  const bool xcd_split = (G & 7) == 0;
+  const int per = (total + 7) >> 3;
+  const int t = xcd_split ? (blockIdx.x & 7) * per + (blockIdx.x >> 3) : blockIdx.x;
   const int tstep = xcd_split ? (G >> 3) : G;
-  const int t_end = xcd_split ? ((blockIdx.x & 7) + 1) * (total >> 3) : total;
+  const int t_end = xcd_split ? min(total, ((blockIdx.x & 7) + 1) * per) : total;
   if (t >= t_end) return;
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)lds;
 
@@ -558,7 +560,7 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
 // waves (one per SIMD), each wave 128 rows x 128 columns = 4 x 4 tiles of
 // 32 x 32 (v_mfma_f32_32x32x16_bf16), K step 64 bytes, a ring of 4 LDS
 // stages of 40 KB (512 + 128 rows of 64 bytes; all 160 KB of the CU's LDS)
-// filled by direct global-to-LDS loads, three K steps ahead.  A wave's tile shares every widened A fragment among
+// filled by direct global-to-LDS loads, two to three K steps ahead.  A wave's tile shares every widened A fragment among
 // 4 column tiles and every B fragment among 4 row tiles: per flop half the
 // widening conversions of the 64 x 64 waves of gemm_dma_kernel.  With one
 // wave per SIMD the accumulators (256 per lane) live in the accumulation
@@ -632,10 +634,12 @@ void gemm_wide_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict_
   // range of tiles (whole products), so a product's operand panels stay in
   // one L2
   const int G = gridDim.x;
-  const bool xcd_split = (G & 7) == 0 && (total & 7) == 0;
-  const int t = xcd_split ? (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+  // (XCD x takes tiles [x per, (x + 1) per), per = ceil(total / 8))
+  const bool xcd_split = (G & 7) == 0;
+  const int per = (total + 7) >> 3;
+  const int t = xcd_split ? (blockIdx.x & 7) * per + (blockIdx.x >> 3) : blockIdx.x;
   const int tstep = xcd_split ? (G >> 3) : G;
-  const int t_end = xcd_split ? ((blockIdx.x & 7) + 1) * (total >> 3) : total;
+  const int t_end = xcd_split ? min(total, ((blockIdx.x & 7) + 1) * per) : total;
   if (t >= t_end) return;
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)lds;
 
@@ -762,31 +766,55 @@ void gemm_wide_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict_
   // Sequence of (tile, K-step) pairs p_0, p_1, ...; p_s lives in LDS buffer
   // s mod 4, and its 4 sub-steps run in order.  Iteration s, in four phases
   // whose instructions are interleaved with the matrix instructions (each
-  // region's order fixed by scheduling-group barriers or program order):
+  // region's order fixed by scheduling-group barriers and program order):
   //   A: sub-step 0 of p_s, widening sub-step 1;
   //   B: sub-step 1, widening sub-steps 2 and 3 (the raw codes of p_s are
   //      then dead);
   //   wait until p_{s+1} has landed and every wave is done reading p_s;
-  //   C: sub-step 2, reading p_{s+1} from LDS and starting the loads of
-  //      p_{s+4} into the buffer of p_s;
+  //   C: sub-step 2, reading p_{s+1} from LDS;
   //   D: sub-step 3, widening sub-step 0 of p_{s+1}.
-  // The loads run ahead across tile boundaries; the accumulators are
-  // cleared at the start of a tile and stored after its last K step.
+  // The 10 wave-loads of p_{s+3} go out spread over the four phases (one
+  // after every fourth matrix instruction; the TA then never has a burst to
+  // absorb), into the buffer of p_{s-1}, free since the previous iteration's
+  // barrier.  The loads run ahead across tile boundaries; the accumulators
+  // are cleared at the start of a tile and stored after its last K step.
   auto advance = [&](int& tt, int& kk) {
     if (++kk == nk) {
       kk = 0;
       tt += tstep;
     }
   };
+  // one wave-load j of a stage: j < 8 rows of A, 8 and 9 rows of B
+  auto dma_one = [&](const uint8_t* Ab, const uint8_t* Bb, int kt, int buf, int j) {
+    const uint32_t l0 = lds_base + (uint32_t)(buf * STAGE);
+    if (j < 8)
+      dma16s(Ab + j * kb16 + kt * KS, dma_off, l0 + (uint32_t)((wave * 128 + 16 * j) * KS));
+    else
+      dma16s(Bb + (j - 8) * kb16 + kt * KS, dma_off, l0 + (uint32_t)((BM + wave * 32 + 16 * (j - 8)) * KS));
+  };
+  // mma of one sub-step slot with wave-loads j0..j1-1 of p_{s+3} placed
+  // after matrix instructions 2, 6, 10, 14 (program order)
+  auto mma_dma = [&](int slot, const uint8_t* Ab, const uint8_t* Bb, int kt, int buf, auto j0c,
+                     auto j1c) {
+    constexpr int j0 = decltype(j0c)::value, j1 = decltype(j1c)::value;
+    sfor<0, 16>([&](auto qc) {
+      constexpr int q = decltype(qc)::value;
+      acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb[slot][q & 3], wa[slot][q >> 2], acc[q >> 2][q & 3], 0, 0, 0);
+      if constexpr (q % 4 == 2 && j0 + q / 4 < j1) dma_one(Ab, Bb, kt, buf, j0 + q / 4);
+    });
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I3 = std::integral_constant<int, 3>;
+  using I6 = std::integral_constant<int, 6>;
+  using I8 = std::integral_constant<int, 8>;
+  using I10 = std::integral_constant<int, 10>;
   int t1 = t, k1 = 0;  // p_{s+1}
   advance(t1, k1);
   int t2 = t1, k2 = k1;  // p_{s+2}
   advance(t2, k2);
   int t3 = t2, k3 = k2;  // p_{s+3}
   advance(t3, k3);
-  int t4 = t3, k4 = k3;  // p_{s+4}
-  advance(t4, k4);
-  const uint8_t *A0, *B0;  // panels of the tile being issued
+  const uint8_t *A0, *B0;
   tile_base(t, A0, B0);
   issue(A0, B0, 0, 0);
   int after1 = 0;  // vector-memory operations issued after the group of p_{s+1}
@@ -799,14 +827,8 @@ void gemm_wide_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict_
     issue(A0, B0, k2, 2);
     after1 += LOADS;
   }
-  if (t3 < t_end) {
-    if (t3 != t2) tile_base(t3, A0, B0);
-    issue(A0, B0, k3, 3);
-    after1 += LOADS;
-  }
-  int after2 = t3 < t_end ? LOADS : 0;  // operations issued after the group of p_{s+2}
-  const uint8_t *A4 = A0, *B4 = B0;  // panels of the tile of p_{s+4}
-  if (t4 < t_end && t4 != t3) tile_base(t4, A4, B4);
+  const uint8_t *A3 = A0, *B3 = B0;  // panels of the tile of p_{s+3}
+  if (t3 < t_end && t3 != t2) tile_base(t3, A3, B3);
   wait_vm(t1 < t_end ? after1 + LOADS : 0);  // p_0 has landed
   FM_COMPILER_FENCE();
   __builtin_amdgcn_s_barrier();
@@ -823,51 +845,39 @@ void gemm_wide_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict_
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
     for (int kk = 0; kk < nk; ++kk) {
-      // A
-      mma(0);
+      // the loads of p_{s+3} go out even past the last pair (stale but
+      // in-bounds panels into a free buffer, never read), so every
+      // iteration issues the same operations
+      const int b3 = cb == 0 ? NSTG - 1 : cb - 1;  // buffer of p_{s+3} (that of p_{s-1})
+      // A: 3 wave-loads of p_{s+3}
+      mma_dma(0, A3, B3, k3, b3, I0{}, I3{});
       widen_sub(1, 1);
       interleave<0x002, 2>();
       pin(1);
       __builtin_amdgcn_sched_barrier(0);
-      // B
-      mma(1);
+      // B: 3 more
+      mma_dma(1, A3, B3, k3, b3, I3{}, I6{});
       widen_sub(2, 2);
       widen_sub(3, 0);
       interleave<0x002, 4>();
       pin(2);
       pin(0);
       __builtin_amdgcn_sched_barrier(0);
-      wait_vm(after1);                     // p_{s+1} has landed (this wave's share)
+      // p_{s+1} issued before p_{s+2} (all 10) and 6 of p_{s+3}
+      wait_vm(after1 + 6);
       __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of p_s are done
       FM_COMPILER_FENCE();
       __builtin_amdgcn_s_barrier();
       FM_COMPILER_FENCE();
       const int nb = cb == NSTG - 1 ? 0 : cb + 1;
-      const bool iss = t4 < t_end;
-      const int after3 = iss ? LOADS : 0;  // operations issued after the group of p_{s+3}
-      FM_COMPILER_FENCE();
       more = t1 < t_end;
-      // C: the reads of p_{s+1} (after the last pair a stale stage, never
-      // used), then the loads of p_{s+4} into the buffer of p_s, one after
-      // each of the first ten matrix instructions
+      // C: reads of p_{s+1}, 2 wave-loads
+      mma_dma(2, A3, B3, k3, b3, I6{}, I8{});
       read_stage(nb);
-      {
-        const uint32_t l0 = lds_base + (uint32_t)(cb * STAGE);
-        const uint8_t* pa = A4 + k4 * KS;
-        const uint8_t* pb = B4 + k4 * KS;
-        sfor<0, 16>([&](auto qc) {
-          constexpr int q = decltype(qc)::value;
-          acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb[2][q & 3], wa[2][q >> 2], acc[q >> 2][q & 3], 0, 0, 0);
-          if constexpr (q < 8) {
-            if (iss) dma16s(pa + q * kb16, dma_off, l0 + (uint32_t)((wave * 128 + 16 * q) * KS));
-          } else if constexpr (q < 10) {
-            if (iss) dma16s(pb + (q - 8) * kb16, dma_off, l0 + (uint32_t)((BM + wave * 32 + 16 * (q - 8)) * KS));
-          }
-        });
-      }
+      interleave<0x100, 1>();
       __builtin_amdgcn_sched_barrier(0);
-      // D
-      mma(0);
+      // D: the last 2
+      mma_dma(0, A3, B3, k3, b3, I8{}, I10{});
       widen_sub(0, 1);
       interleave<0x002, 2>();
       pin(1);
@@ -877,22 +887,20 @@ void gemm_wide_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict_
         wa[0][i] = wa[1][i];
         wb[0][i] = wb[1][i];
       }
+      const int after2 = LOADS;  // p_{s+3}'s group, after p_{s+2}'s
       t1 = t2;
       k1 = k2;
       t2 = t3;
       k2 = k3;
-      t3 = t4;
-      k3 = k4;
-      advance(t4, k4);
-      if (k4 == 0 && t4 < t_end) tile_base(t4, A4, B4);
-      after1 = after2 + after3;
-      after2 = after3;
+      advance(t3, k3);
+      if (k3 == 0 && t3 < t_end) tile_base(t3, A3, B3);
+      after1 = after2;
       cb = nb;
     }
     epilogue(tile);
     after1 += STORES;
-    after2 += STORES;
   }
+  ring::wait_vm_n<0>();  // the loads past the last pair land before the workgroup ends
 }
 
 }  // namespace

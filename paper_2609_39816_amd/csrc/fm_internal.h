@@ -63,6 +63,9 @@ void build_lists(const fm_scheme& flat, Lists& out);
 
 // Pattern family of one side of a list (compiled specializations), or -1.
 int match_pattern(int side, const Side& s, int R, int NB);
+// True if one scheme's side list (A: 0, B: 1) of family `pattern` has equal
+// coefficients on every entry the family's prefix-shared chains share.
+bool trie_valid(int pattern, int side, const Side& s);
 // Number of pattern families; side: 0 = A, 1 = B, 2 = W.
 // Family whose H pattern (pairs of products sharing a block of A and a
 // block of C) equals one gauge's H support in compressed rows, or -1.
@@ -119,6 +122,8 @@ struct FormArgs {
                     // consecutive entries, at [((g R + r) (bc/128) + y/128) br + x];
                     // 3 the same values rounded to bf16 first, one per 128 x 128
                     // block, at [((g R + r) (bc/128) + y/128) (br/128) + x/128]
+  int trie = 0;     // every gauge's coefficients agree on the entries that the
+                    // family's prefix-shared chains share (set by the host)
 };
 // pattern: family id from match_pattern (side A or B), or -1 for the
 // generic kernel.

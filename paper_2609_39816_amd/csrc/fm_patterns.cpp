@@ -19,6 +19,9 @@ struct PatternRef {
   int hnnz;
   const int16_t* hrowptr;
   const int16_t* hidx;
+  bool trie[2];             // prefix-shared chains generated (A, B)
+  int nchk[2];              // entries whose coefficient must equal a representative's
+  const int16_t* tchk[2];   // pairs (entry, representative entry)
 };
 
 #define FM_PATTERN_REF(P)                                                    \
@@ -31,7 +34,10 @@ struct PatternRef {
              pat::P::H::JOINT,                                               \
              pat::P::H::NNZ,                                                 \
              pat::P::H::rowptr,                                              \
-             pat::P::H::idx},
+             pat::P::H::idx,                                                 \
+             {pat::P::A::TRIE, pat::P::B::TRIE},                             \
+             {pat::P::A::NCHK, pat::P::B::NCHK},                             \
+             {pat::P::A::tchk, pat::P::B::tchk}},
 
 const PatternRef kPatterns[] = {FM_PATTERN_FAMILIES(FM_PATTERN_REF)};
 constexpr int kNumPatterns = sizeof(kPatterns) / sizeof(kPatterns[0]);
@@ -54,6 +60,22 @@ int match_pattern(int side, const Side& s, int R, int NB) {
     if (ok) return p;
   }
   return -1;
+}
+
+bool trie_valid(int pattern, int side, const Side& s) {
+  if (pattern < 0 || pattern >= kNumPatterns || side < 0 || side > 1) return false;
+  const PatternRef& P = kPatterns[pattern];
+  if (!P.trie[side]) return false;
+  // entries are indices into one scheme's list (s.off[0] == 0)
+  for (int c = 0; c < P.nchk[side]; ++c) {
+    const size_t e = (size_t)P.tchk[side][2 * c], rep = (size_t)P.tchk[side][2 * c + 1];
+    if (e >= s.coef.size() || rep >= s.coef.size()) return false;
+    uint32_t a, b;
+    std::memcpy(&a, &s.coef[e], 4);
+    std::memcpy(&b, &s.coef[rep], 4);
+    if (a != b) return false;
+  }
+  return true;
 }
 
 int match_h_pattern(const int32_t* rowptr, const uint16_t* cols, int R) {

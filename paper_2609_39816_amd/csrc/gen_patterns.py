@@ -56,6 +56,37 @@ def kron_nz(a, b):
     return U, V, W, m, k, n
 
 
+def kron_vals(a, b):
+    """Coefficient values of scheme b applied inside the blocks of scheme a
+    (same index maps as kron_nz), float64."""
+    (Ua, Va, Wa, ma, ka, na), (Ub, Vb, Wb, mb, kb, nb) = a, b
+    Ra, Rb = Ua.shape[0], Ub.shape[0]
+    m, k, n = ma * mb, ka * kb, na * nb
+    U = np.zeros((Ra * Rb, m * k))
+    V = np.zeros((Ra * Rb, k * n))
+    for ra in range(Ra):
+        for rb in range(Rb):
+            r = ra * Rb + rb
+            for ia in range(ma):
+                for ib in range(mb):
+                    for la in range(ka):
+                        for lb in range(kb):
+                            U[r, (ia * mb + ib) * k + la * kb + lb] = Ua[ra, ia * ka + la] * Ub[rb, ib * kb + lb]
+            for la in range(ka):
+                for lb in range(kb):
+                    for ja in range(na):
+                        for jb in range(nb):
+                            V[r, (la * kb + lb) * n + ja * nb + jb] = Va[ra, la * na + ja] * Vb[rb, lb * nb + jb]
+    return U, V, None, m, k, n
+
+
+def power_vals(base, L):
+    out = base
+    for _ in range(L - 1):
+        out = kron_vals(out, base)
+    return out
+
+
 def nz(base):
     U, V, W, m, k, n = base
     return U != 0, V != 0, W != 0, m, k, n
@@ -71,6 +102,17 @@ def power_nz(base, L):
 def dense(R, m, k, n):
     return (np.ones((R, m * k), bool), np.ones((R, k * n), bool), np.ones((R, m * n), bool), m, k, n)
 
+
+# Coefficient values of the families whose block sums share prefixes: the
+# base scheme flattened (sign variants multiply every coefficient of a block
+# by that block's sign, so they share the same prefixes; the library checks
+# each gauge's coefficients before using the shared form).
+VALUES = {
+    "Strassen1": power_vals(schemes.strassen(), 1),
+    "Strassen2": power_vals(schemes.strassen(), 2),
+    "Strassen3": power_vals(schemes.strassen(), 3),
+    "Laderman1": power_vals(schemes.laderman(), 1),
+}
 
 FAMILIES = [
     ("Classical1", nz(schemes.classical(1, 1, 1))),
@@ -103,6 +145,55 @@ def lists(U, V, W, m, k, n):
     return out
 
 
+def trie(rowptr, idx, vals):
+    """Prefix sharing of the block-sum chains of one side.
+
+    Chain r is the list of (block idx[e], coefficient vals[e]) for e in
+    [rowptr[r], rowptr[r + 1]), summed by fused multiply-adds in that order
+    from +0.  Chains that start with the same (block, coefficient) entries
+    compute the same partial sums, so the distinct prefixes form a trie:
+    node = one entry appended to its parent's partial sum.  Returns the
+    nodes in depth-first order (parent before children; a node's parent is
+    the latest node one level up) as (depth, block, representative entry),
+    the products completed at each node (CSR over the completion order),
+    and the (entry, representative entry) pairs whose coefficients a gauge
+    must have equal for the shared form to give its chains' values."""
+    R = len(rowptr) - 1
+    children, key = {}, {}
+    nodes = []  # (parent, block, entry, depth)
+    ends = {}
+    rep_of = []
+    for r in range(R):
+        parent, prefix = -1, ()
+        for pos, e in enumerate(range(rowptr[r], rowptr[r + 1])):
+            prefix = prefix + ((idx[e], float(vals[e])),)
+            if prefix not in key:
+                key[prefix] = len(nodes)
+                nodes.append((parent, idx[e], e, pos))
+                children.setdefault(parent, []).append(key[prefix])
+            node = key[prefix]
+            rep_of.append((e, nodes[node][2]))
+            parent = node
+        ends.setdefault(parent, []).append(r)
+    order = []
+
+    def dfs(n):
+        order.append(n)
+        for c in children.get(n, []):
+            dfs(c)
+    for c in children.get(-1, []):
+        dfs(c)
+    depth = [nodes[n][3] for n in order]
+    blk = [nodes[n][1] for n in order]
+    ent = [nodes[n][2] for n in order]
+    endptr, endprod = [0], []
+    for n in order:
+        endprod += ends.get(n, [])
+        endptr.append(len(endprod))
+    chk = [(e, rep) for e, rep in rep_of if e != rep]
+    return depth, blk, ent, endptr, endprod, chk
+
+
 def arr(vals, per_line=24):
     s = [str(v) for v in vals]
     lines = [", ".join(s[i:i + per_line]) for i in range(0, len(s), per_line)]
@@ -126,6 +217,32 @@ def main():
             out.append(f"    static constexpr int R = {R}, NB = {nbk}, NNZ = {len(idx)};")
             out.append(f"    static constexpr int16_t rowptr[{R + 1}] = {arr(rowptr)};")
             out.append(f"    static constexpr int16_t idx[{max(1, len(idx))}] = {arr(idx or [0])};")
+            if side != "W" and name in VALUES:
+                Uv, Vv = VALUES[name][0], VALUES[name][1]
+                vals = []
+                for r in range(R):
+                    if side == "A":
+                        vals += [Uv[r, i * k + l] for i in range(m) for l in range(k) if Uv[r, i * k + l]]
+                    else:
+                        vals += [Vv[r, l * n + j] for l in range(k) for j in range(n) if Vv[r, l * n + j]]
+                assert len(vals) == len(idx)
+                depth, blk, ent, endptr, endprod, chk = trie(rowptr, idx, vals)
+                out.append("    // prefix-shared chains (depth-first trie; see gen_patterns.trie)")
+                out.append(f"    static constexpr bool TRIE = true;")
+                out.append(f"    static constexpr int NN = {len(depth)}, MAXD = {max(depth) + 1}, "
+                           f"NCHK = {len(chk)};")
+                out.append(f"    static constexpr int16_t tdepth[{len(depth)}] = {arr(depth)};")
+                out.append(f"    static constexpr int16_t tblk[{len(depth)}] = {arr(blk)};")
+                out.append(f"    static constexpr int16_t tent[{len(depth)}] = {arr(ent)};")
+                out.append(f"    static constexpr int16_t tendptr[{len(endptr)}] = {arr(endptr)};")
+                out.append(f"    static constexpr int16_t tendprod[{len(endprod)}] = {arr(endprod)};")
+                out.append(f"    static constexpr int16_t tchk[{max(1, 2 * len(chk))}] = "
+                           f"{arr([x for pair in chk for x in pair] or [0])};")
+            else:
+                out.append("    static constexpr bool TRIE = false;")
+                out.append("    static constexpr int NN = 0, MAXD = 1, NCHK = 0;")
+                out.append("    static constexpr int16_t tdepth[1] = {0}, tblk[1] = {0}, tent[1] = {0};")
+                out.append("    static constexpr int16_t tendptr[2] = {0, 0}, tendprod[1] = {0}, tchk[1] = {0};")
             out.append("  };")
         # where H_rs = <w_r, w_s> <u_r, u_s> of the joint rounding can be
         # nonzero: both products share a block of A and one of C (families of

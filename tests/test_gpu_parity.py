@@ -261,6 +261,29 @@ def test_generic_kernels():
     assert np.all(np.abs(e / np.array(want) - 1) <= 1e-2)
 
 
+def test_family_structure_with_unshared_coefficients():
+    """Two-level Strassen with each product's A coefficients scaled by its
+    own power of two (W scaled back): the family's nonzero structure, so the
+    family kernels take it, but chains that share blocks no longer share
+    coefficients, so the prefix-shared formation must not be used; codes and
+    scales stay bit-exact and the output within 1e-5 of the oracle's."""
+    say("[parity] family structure, unshared coefficients")
+    w = sy.scaled(sy.WORKLOADS["strassen2_2048x4096x4096_sign512"], 256, 256, 256, G=1)
+    A, B = sy.operands(w)
+    At, Bt = gpu(A), gpu(B)
+    U, V, W, m, k, n = fm._schemes.strassen()
+    alpha = np.array([2.0, 0.5, 4.0, 1.0, 0.25, 8.0, 2.0])
+    h = fm.Scheme.load(U * alpha[:, None], V, W / alpha[:, None], m, k, n).kron(2)
+    assert h.kernel_family(1) == "Strassen2"
+    base = osch.strassen()
+    scaled = osch.Scheme(base.U * alpha[:, None], base.V, base.W / alpha[:, None], base.m, base.k,
+                         base.n, base.R)
+    o = so.power(scaled, 2)
+    check_operands(h, o, 1, A, B, At, Bt, "e4m3")
+    Co = oracle.lowp_matmul(A, B, *oracle.flatten_f32(o))
+    assert rel(fm.matmul_lowp(h, At, Bt).cpu().numpy(), Co) <= 1e-5
+
+
 def test_block_products_over_every_code():
     """Codes drawn uniformly from every finite FP8 value (subnormals, both
     signs, the largest values): the default arithmetic stays within 1e-6 of
