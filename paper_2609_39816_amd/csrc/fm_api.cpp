@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <memory>
 #include <string>
@@ -1228,7 +1229,11 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   if (int rc = check_ws(workspace, ws_bytes, L.total)) return rc;
   hipStream_t st = (hipStream_t)hip_stream;
   Pipeline pipe;
-  if (L.two_sets()) {
+  static const bool one_stream = [] {
+    const char* e = std::getenv("FM_ORBIT_STREAMS");
+    return e && std::strcmp(e, "1") == 0;
+  }();
+  if (L.two_sets() && !one_stream) {
     if (int rc = pipe.open(st)) return rc;
   }
   char* ws = (char*)workspace;

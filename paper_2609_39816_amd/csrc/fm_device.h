@@ -448,14 +448,14 @@ __device__ __forceinline__ void form_static_gauges(const FormArgs& a, int g0, in
 // block sum, with the fused multiply-adds of its chain in its order, so the
 // bits are those of form_static_gauges.  (The host uses this form only for
 // gauges whose coefficients agree on every shared entry, P::tchk.)  Mode 0
-// reduces products' maxima in groups of 8 in completion order; mode 1
-// encodes and stores each product's codes as it completes.
+// folds each lane's maximum into the product's slot lane % 16 (of the 16
+// per product that the kernels combine at the end) with an LDS atomic
+// maximum; mode 1 encodes and stores each product's codes as it completes.
 template <class P, int VW, int MODE, int FMT>
 __device__ __forceinline__ void form_trie_gauges(const FormArgs& a, int g0, int g1,
                                                  const float (&xv)[P::NB][VW],
                                                  [[maybe_unused]] bool active, uint32_t voff,
                                                  uint32_t* smax) {
-  constexpr int GR = 8;
   const int lane = threadIdx.x & 63;
   const uint32_t bsz = (uint32_t)a.br * (uint32_t)a.bc;
   for (int g = g0; g < g1; ++g) {
@@ -465,7 +465,6 @@ __device__ __forceinline__ void form_trie_gauges(const FormArgs& a, int g0, int 
       rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + (size_t)g * P::R * bsz, (short)0,
                                                (int)(P::R * bsz), 0x00020000);
     float nv[P::MAXD][VW];
-    [[maybe_unused]] uint32_t lm[GR];
     // coefficient loads through an offset the compiler cannot see through,
     // renewed every 16 nodes, so the scalar loads stay near their nodes
     int so = 0;
@@ -485,32 +484,13 @@ __device__ __forceinline__ void form_trie_gauges(const FormArgs& a, int g0, int 
       sfor<P::tendptr[t], P::tendptr[t + 1]>([&](auto kc) {
         constexpr int kk = decltype(kc)::value, r = P::tendprod[kk];
         if constexpr (MODE == 0) {
+          // the lane's maximum folded into the product's 16 LDS slots (slot
+          // = lane % 16) by an LDS atomic maximum: no cross-lane steps on
+          // the vector unit; +0 on inactive lanes (zero operands)
           float mf = 0.0f;
 #pragma unroll
           for (int v = 0; v < VW; ++v) mf = __builtin_elementwise_maximum(mf, __builtin_fabsf(nv[d][v]));
-          lm[kk % GR] = __float_as_uint(mf);  // +0 on inactive lanes (zero operands)
-          if constexpr (kk % GR == GR - 1 || kk == P::R - 1) {
-            // row maxima of the group's products (DPP shifts 1, 2, 4, 8;
-            // lane 15 of each row then holds its row's maximum), kept in
-            // the (wave, row) slots of each product
-            constexpr int NJ = kk % GR + 1, k0 = kk - kk % GR;
-            sfor<0, 4>([&](auto sc) {
-              constexpr int ctl = 0x111 + (1 << decltype(sc)::value) - 1;  // row_shr:1,2,4,8
-              uint32_t sh[NJ];
-#pragma unroll
-              for (int j = 0; j < NJ; ++j)
-                sh[j] = (uint32_t)__builtin_amdgcn_mov_dpp((int)lm[j], ctl, 0xf, 0xf, true);
-#pragma unroll
-              for (int j = 0; j < NJ; ++j) lm[j] = max(lm[j], sh[j]);
-            });
-            if ((lane & 15) == 15) {
-              uint32_t* base = smax + (size_t)(g - g0) * P::R * 16 + (threadIdx.x >> 4);
-              sfor<0, NJ>([&](auto jc) {
-                constexpr int j = decltype(jc)::value, rj = P::tendprod[k0 + j];
-                base[rj * 16] = max(base[rj * 16], lm[j]);
-              });
-            }
-          }
+          atomicMax(smax + ((size_t)(g - g0) * P::R + r) * 16 + (lane & 15), __float_as_uint(mf));
         } else {
           const float q = ro(a.q)[(size_t)g * P::R + r + so];
           form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, nv[d], q);
