@@ -46,9 +46,10 @@ def kernel_work(cls, w, geo, chunk, G):
     class's roofline bound.  Units of work:
       block_gemm: 2*Mb*Nb*Kb flops per block product; G*R products for the
                   orbit plus the classical product 2*M*N*K;
-      recon:      per gauge, R*Mb*Nb fp32 products read and M*N float64
-                  reference values read (C is not written); the classical
-                  baseline reads M*N products and writes C;
+      recon:      per gauge, R*Mb*Nb fp32 products read; per launch, the
+                  M*N float64 reference read once (the gauges of a launch
+                  share it; C is not written); the classical baseline reads
+                  M*N products and writes C;
       form_amax:  each launch reads one operand once in fp32 (A, or B^T);
       form_quant: each launch reads one operand and writes its FP8 codes;
       reference:  reads A and B in fp32, writes C_ref in float64.
@@ -61,7 +62,7 @@ def kernel_work(cls, w, geo, chunk, G):
     if cls == "block_gemm":
         return "mfma", G * R * 2.0 * Mb * Nb * Kb + 2.0 * M * N * K, "TFLOP/s"
     if cls == "recon":
-        return "hbm", G * (R * Mb * Nb * 4.0 + M * N * 8.0) + M * N * 8.0, "GB/s"
+        return "hbm", G * R * Mb * Nb * 4.0 + chunks * M * N * 8.0 + M * N * 8.0, "GB/s"
     if cls == "form_amax":
         return "hbm", (chunks + 1) * ops, "GB/s"
     if cls == "form_quant":
@@ -174,16 +175,18 @@ def cpu_baseline(w, A, B, gauges, scale_mode=0, budget_s=10.0):
                        f"reference is not included")
 
 
-def pipeline_work(w, geo, G):
+def pipeline_work(w, geo, G, chunk):
     """Algorithmic work of one step's orbit (all G gauges): the block
     products' matrix flops, and the least HBM traffic of the schedule with
-    materialized products: per gauge the FP8 operands written and read once,
-    the fp32 products written and read once, the float64 reference read once
-    (operand inputs, read once per chunk, are left out)."""
+    materialized products: per gauge the FP8 operands written and read once
+    and the fp32 products written and read once; per launch of `chunk`
+    gauges the float64 reference read once (operand inputs, read once per
+    chunk, are left out)."""
     gm, gk, gn, R = geo
     Mb, Kb, Nb = w.M // gm, w.K // gk, w.N // gn
     flops = G * R * 2.0 * Mb * Nb * Kb
-    hbm = G * (2.0 * R * (Mb * Kb + Nb * Kb) + 2.0 * 4.0 * R * Mb * Nb + 8.0 * w.M * w.N)
+    hbm = (G * (2.0 * R * (Mb * Kb + Nb * Kb) + 2.0 * 4.0 * R * Mb * Nb)
+           + -(-G // chunk) * 8.0 * w.M * w.N)
     return flops, hbm
 
 
@@ -387,7 +390,7 @@ def main():
             achieved = work / tot_s / 1e12
             peak = PEAK_FP8_TFLOPS if fp8_mfma else PEAK_BF16_TFLOPS
             peak_note = dict(instruction="FP8 matrix instructions" if fp8_mfma
-                             else "v_mfma_f32_16x16x32_bf16 on exactly widened FP8 codes",
+                             else "bf16 matrix instructions on exactly widened FP8 codes",
                              fp8_peak=PEAK_FP8_TFLOPS,
                              frac_of_fp8_peak=round(achieved / PEAK_FP8_TFLOPS, 4))
         else:
@@ -407,7 +410,7 @@ def main():
 
     flops = G * 2.0 * w.M * w.N * w.K
     value = flops / t / 1e12
-    mfma_flops, hbm_bytes = pipeline_work(w, geo, G)
+    mfma_flops, hbm_bytes = pipeline_work(w, geo, G, args.chunk)
     # the whole orbit against both ceilings: its block products' matrix
     # flops over the step time against the matrix peak of the instruction
     # issued (and the FP8 peak), and its least HBM traffic over the step time
