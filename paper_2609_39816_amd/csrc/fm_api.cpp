@@ -83,7 +83,8 @@ struct Tables {
   int G = 0, R = 0;
   Side s[3];
   std::vector<int> pat[3];
-  std::vector<char> trie[2];  // per gauge: coefficients fit the family's shared chains
+  std::vector<char> trie[2];  // per gauge: a sign variant of its family's base scheme
+  std::vector<uint64_t> sgn[2];  // per gauge: its block signs (bit b: block b negated)
   std::vector<int> hpat;  // family of each gauge's H support (joint rounding only)
 };
 
@@ -96,13 +97,18 @@ void append(Tables& T, const Lists& L, int R, const int nb[3]) {
     d.idx.insert(d.idx.end(), src[k]->idx.begin(), src[k]->idx.end());
     d.coef.insert(d.coef.end(), src[k]->coef.begin(), src[k]->coef.end());
     T.pat[k].push_back(match_pattern(k, *src[k], R, nb[k]));
-    if (k < 2) T.trie[k].push_back(trie_valid(T.pat[k].back(), k, *src[k]) ? 1 : 0);
+    if (k < 2) {
+      uint64_t m = 0;
+      const bool ok = block_signs(T.pat[k].back(), k, *src[k], nb[k], &m);
+      T.trie[k].push_back(ok ? 1 : 0);
+      T.sgn[k].push_back(ok ? m : 0);
+    }
   }
   T.G += 1;
 }
 
 // 1 if every gauge of [g0, g0 + n) may use its family's prefix-shared chains
-// on one side (A: 0, B: 1).
+// on one side (A: 0, B: 1): every one is a sign variant of the base scheme.
 int chunk_trie(const Tables& T, int side, int g0, int n) {
   for (int g = g0; g < g0 + n; ++g)
     if (!T.trie[side][g]) return 0;
@@ -121,7 +127,7 @@ int chunk_pattern(const Tables& T, int side, int g0, int n) {
 struct Layout {
   // *2: a second set of a chunk's maxima, scales and block products when the
   // orbit runs in several chunks (equal to the first set otherwise)
-  size_t flags, bt, off[3], idx[3], coef[3], amax, q, d, tq, sq, mprod, amax2, q2, d2, mprod2,
+  size_t flags, bt, off[3], idx[3], coef[3], sg[2], amax, q, d, tq, sq, mprod, amax2, q2, d2, mprod2,
       partial, errsq, out3, arow, rowup, hg, hgc, hgp, total;
   int recon_nblk;
   bool two_sets() const { return mprod2 != mprod; }
@@ -184,6 +190,7 @@ Layout make_layout(const Geometry& g, int G, int chunk, bool need_bt = true,
     L.idx[k] = take((size_t)G * R * nbk[k] * 4);
     L.coef[k] = take((size_t)G * R * nbk[k] * 4);
   }
+  for (int k = 0; k < 2; ++k) L.sg[k] = take((size_t)G * 8);
   const size_t nsc = (size_t)chunk * R * (scales_a(g, scale_mode) + scales_b(g, scale_mode));
   L.amax = take(nsc * 4);
   L.q = take(nsc * 4);
@@ -396,6 +403,10 @@ int upload_table_range(const Tables& T, char* ws, const Layout& L, int g_from, i
     pieces.push_back({sd.coef.data() + e0, (e1 - e0) * 4});
     dst.push_back(L.coef[k] + e0 * 4);
   }
+  for (int k = 0; k < 2; ++k) {
+    pieces.push_back({T.sgn[k].data() + g_from, (size_t)(g_to - g_from) * 8});
+    dst.push_back(L.sg[k] + (size_t)g_from * 8);
+  }
   size_t total = 0;
   for (auto& p : pieces) total += p.second;
   if (int rc = stage_reserve(total)) return rc;
@@ -445,7 +456,7 @@ Tables make_tables(const fm_scheme* const* schemes, int G, int levels, const Geo
 int upload_tables(const Tables& T, char* ws, const Layout& L, hipStream_t st) {
   // one contiguous region from the first table to the end of the last
   const size_t base = L.off[0];
-  const size_t total = L.coef[2] + T.s[2].coef.size() * 4 - base;
+  const size_t total = L.sg[1] + T.sgn[1].size() * 8 - base;
   std::vector<std::pair<const void*, size_t>> pieces;
   std::vector<size_t> offs;
   for (int k = 0; k < 3; ++k) {
@@ -456,7 +467,18 @@ int upload_tables(const Tables& T, char* ws, const Layout& L, hipStream_t st) {
     pieces.push_back({T.s[k].coef.data(), T.s[k].coef.size() * 4});
     offs.push_back(L.coef[k] - base);
   }
+  for (int k = 0; k < 2; ++k) {
+    pieces.push_back({T.sgn[k].data(), T.sgn[k].size() * 8});
+    offs.push_back(L.sg[k] - base);
+  }
   return upload(ws + base, pieces, offs, total, st);
+}
+
+// The prefix-shared chains for gauges [g0, g0 + n) of one side: the flag,
+// and the gauges' block-sign masks when it is set.
+void set_trie(FormArgs& f, const Tables& T, char* ws, const Layout& L, int side, int g0, int n) {
+  f.trie = chunk_trie(T, side, g0, n);
+  f.sgn = f.trie ? (const uint64_t*)(ws + L.sg[side]) + g0 : nullptr;
 }
 
 // Formation arguments of both sides of the gauges [g0, g0 + n) with one
@@ -487,13 +509,13 @@ int form_codes_and_next_maxima(const Geometry& geo, const float* A, const float*
                                int fmt, uint8_t* Tq, uint8_t* Sq, hipStream_t st) {
   FormArgs qa, qb, ma, mb;
   tensor_form_args(geo, A, Bt, ws, L.set(c & 1), g0, n, fmt, Tq, Sq, qa, qb);
-  qa.trie = chunk_trie(T, 0, g0, n);
-  qb.trie = chunk_trie(T, 1, g0, n);
+  set_trie(qa, T, ws, L, 0, g0, n);
+  set_trie(qb, T, ws, L, 1, g0, n);
   const Layout Ln = L.set((c + 1) & 1);
   if (n1 > 0) {
     tensor_form_args(geo, A, Bt, ws, Ln, g0 + n, n1, fmt, Tq, Sq, ma, mb);
-    ma.trie = chunk_trie(T, 0, g0 + n, n1);
-    mb.trie = chunk_trie(T, 1, g0 + n, n1);
+    set_trie(ma, T, ws, L, 0, g0 + n, n1);
+    set_trie(mb, T, ws, L, 1, g0 + n, n1);
     if (int rc = launch_fill_u32(ma.amax, (size_t)2 * n1 * geo.R, 0u, st)) return rc;
   }
   for (int side = 0; side < 2; ++side) {
@@ -543,8 +565,8 @@ int form_chunk(const Geometry& geo, const float* A, const float* Bt, char* ws, c
               amax, q,     Tq,    fmt,    per_row, mode == FM_SCALE_GROUP ? 2 : 1};
   FormArgs fb{Bt, geo.N, geo.K, geo.gn, geo.gk, geo.Nb, geo.Kb, off(1), idx(1), coef(1), R, n,
               amax + na, q + na, Sq, fmt, per_row, mode == FM_SCALE_GROUP ? 3 : 1};
-  fa.trie = chunk_trie(T, 0, g0, n);
-  fb.trie = chunk_trie(T, 1, g0, n);
+  set_trie(fa, T, ws, L, 0, g0, n);
+  set_trie(fb, T, ws, L, 1, g0, n);
   if (int rc = launch_fill_u32(amax, na + nb, 0u, st)) return rc;
   for (int side = 0; side < 2; ++side) {
     timing_begin(T_FORM_AMAX, st);
@@ -1287,8 +1309,8 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
     const int n0 = std::min(chunk, G);
     FormArgs fa, fb;
     tensor_form_args(geo, Aform, Bt, ws, L, 0, n0, fmt, Tq, Sq, fa, fb);
-    fa.trie = chunk_trie(T, 0, 0, n0);
-    fb.trie = chunk_trie(T, 1, 0, n0);
+    set_trie(fa, T, ws, L, 0, 0, n0);
+    set_trie(fb, T, ws, L, 1, 0, n0);
     if ((rc = launch_fill_u32(fa.amax, (size_t)2 * n0 * geo.R, 0u, st))) return rc;
     for (int side = 0; side < 2; ++side) {
       timing_begin(T_FORM_AMAX, st);

@@ -274,8 +274,12 @@ __device__ __forceinline__ void form_encode_store(__amdgpu_buffer_rsrc_t rsrc, u
 #pragma unroll
   for (int t = 0; t < (VW + 3) / 4; ++t) {
     const float x0 = acc[4 * t] * q, x1 = acc[4 * t + 1] * q;
-    if constexpr (FMT == FM_E4M3) w[t] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x0, x1, 0, false);
-    else w[t] = (uint32_t)__builtin_amdgcn_cvt_pk_bf8_f32(x0, x1, 0, false);
+    // the conversion keeps the other half of its destination; that half is
+    // written next (VW >= 4) or never stored (VW == 2), so the first
+    // conversion is issued as a plain definition of the register (the
+    // intrinsic would have the compiler clear the register first)
+    if constexpr (FMT == FM_E4M3) asm("v_cvt_pk_fp8_f32 %0, %1, %2" : "=v"(w[t]) : "v"(x0), "v"(x1));
+    else asm("v_cvt_pk_bf8_f32 %0, %1, %2" : "=v"(w[t]) : "v"(x0), "v"(x1));
     if constexpr (VW >= 4) {
       const float x2 = acc[4 * t + 2] * q, x3 = acc[4 * t + 3] * q;
       if constexpr (FMT == FM_E4M3) w[t] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x2, x3, (int)w[t], true);
@@ -440,17 +444,19 @@ __device__ __forceinline__ void form_static_gauges(const FormArgs& a, int g0, in
 
 
 // Gauges g0 <= g < g1 through the family's prefix-shared chains (P::TRIE,
-// one scale per tensor): chains that begin with the same (block,
-// coefficient) entries share their partial sums, so the block sums are the
-// nodes of a trie walked depth first: node t = fmaf(coef[tent[t]],
-// x[tblk[t]], value of the latest node one level up, or +0 at the root).
-// The value of the node where a product's chain ends is that product's
-// block sum, with the fused multiply-adds of its chain in its order, so the
-// bits are those of form_static_gauges.  (The host uses this form only for
-// gauges whose coefficients agree on every shared entry, P::tchk.)  Mode 0
-// folds each lane's maximum into the product's slot lane % 16 (of the 16
-// per product that the kernels combine at the end) with an LDS atomic
-// maximum; mode 1 encodes and stores each product's codes as it completes.
+// one scale per tensor), for sign variants of the family's base scheme: a
+// coefficient is the base value of its list entry (compile time) with the
+// sign of its block, from the gauge's 64-bit block-sign mask (bit b set:
+// block b negated), so no coefficient is read from memory.  Chains that
+// begin with the same (block, base coefficient) entries share their partial
+// sums, so the block sums are the nodes of a trie walked depth first: node
+// t = fmaf(c_t, x[tblk[t]], value of the latest node one level up, or +0 at
+// the root).  The value of the node where a product's chain ends is that
+// product's block sum, with the fused multiply-adds of its chain in its
+// order: the bits of the plain chain.  Mode 0 folds each lane's maximum
+// into the product's slot lane % 16 (of the 16 per product that the
+// kernels combine at the end) with an LDS atomic maximum; mode 1 encodes
+// and stores each product's codes as it completes.
 template <class P, int VW, int MODE, int FMT>
 __device__ __forceinline__ void form_trie_gauges(const FormArgs& a, int g0, int g1,
                                                  const float (&xv)[P::NB][VW],
@@ -459,14 +465,14 @@ __device__ __forceinline__ void form_trie_gauges(const FormArgs& a, int g0, int 
   const int lane = threadIdx.x & 63;
   const uint32_t bsz = (uint32_t)a.br * (uint32_t)a.bc;
   for (int g = g0; g < g1; ++g) {
-    const auto coef = ro(a.coef) + ro(a.off)[(size_t)g * (P::R + 1)];
+    const uint64_t neg = ro(a.sgn)[g];
     __amdgpu_buffer_rsrc_t rsrc;
     if constexpr (MODE == 1)
       rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + (size_t)g * P::R * bsz, (short)0,
                                                (int)(P::R * bsz), 0x00020000);
     float nv[P::MAXD][VW];
-    // coefficient loads through an offset the compiler cannot see through,
-    // renewed every 16 nodes, so the scalar loads stay near their nodes
+    // scale loads through an offset the compiler cannot see through,
+    // renewed every 16 nodes, so the scalar loads stay near their products
     int so = 0;
     sfor<0, P::NN>([&](auto tc) {
       constexpr int t = decltype(tc)::value;
@@ -474,8 +480,22 @@ __device__ __forceinline__ void form_trie_gauges(const FormArgs& a, int g0, int 
         so = 0;
         asm volatile("" : "+s"(so));
       }
-      constexpr int d = P::tdepth[t], b = P::tblk[t], e = P::tent[t];
-      const float c = coef[e + so];
+      constexpr int d = P::tdepth[t], b = P::tblk[t];
+      constexpr uint32_t cb = P::tval[t];
+      // the coefficient: base values of +-1 selected on the scalar unit (bit
+      // test, then a select between inline constants) into a scalar
+      // register; the node index in the assembly keeps each node's select
+      // its own, so the compiler neither holds one register per block over
+      // the whole sequence nor moves the selects to the vector unit
+      float c;
+      if constexpr (cb == 0x3f800000u)
+        asm("; node %3\n\ts_bitcmp1_b64 %1, %2\n\ts_cselect_b32 %0, -1.0, 1.0"
+            : "=s"(c) : "s"(neg), "i"(b), "i"(t) : "scc");
+      else if constexpr (cb == 0xbf800000u)
+        asm("; node %3\n\ts_bitcmp1_b64 %1, %2\n\ts_cselect_b32 %0, 1.0, -1.0"
+            : "=s"(c) : "s"(neg), "i"(b), "i"(t) : "scc");
+      else
+        c = ((neg >> b) & 1u) ? -__builtin_bit_cast(float, cb) : __builtin_bit_cast(float, cb);
 #pragma unroll
       for (int v = 0; v < VW; ++v) {
         if constexpr (d == 0) nv[0][v] = __builtin_fmaf(c, xv[b][v], 0.0f);
@@ -993,9 +1013,9 @@ int launch_form_merged(const FormArgs& aq, const FormArgs& am, hipStream_t st) {
 template <class P>
 bool static_ok(const FormArgs& a) {
   constexpr int VW = static_vw<P>();
-  // prefix-shared families: tensor scales only for gauges whose
-  // coefficients agree on the shared entries (a.trie); others go generic
-  if (P::TRIE && !a.per_row && !a.trie) return false;
+  // prefix-shared families: tensor scales only for sign variants of the
+  // base scheme (a.trie, with their block signs in a.sgn); others go generic
+  if (P::TRIE && !a.per_row && (!a.trie || !a.sgn)) return false;
   return a.gr * a.gc == P::NB && a.R == P::R && a.bc % VW == 0 && (VW < 4 || a.cols % 4 == 0) &&
          (size_t)P::R * a.br * a.bc < ((size_t)1 << 31);
 }

@@ -63,9 +63,13 @@ void build_lists(const fm_scheme& flat, Lists& out);
 
 // Pattern family of one side of a list (compiled specializations), or -1.
 int match_pattern(int side, const Side& s, int R, int NB);
-// True if one scheme's side list (A: 0, B: 1) of family `pattern` has equal
-// coefficients on every entry the family's prefix-shared chains share.
-bool trie_valid(int pattern, int side, const Side& s);
+// Sign variants of a family with prefix-shared chains: true if every
+// coefficient of one scheme's side list (A: 0, B: 1) of family `pattern` is
+// the family's base coefficient times a sign that depends on its block
+// alone (NB <= 64 blocks); *mask gets bit b set where block b's sign is -1.
+// The shared chains then give every product's own chain (a shared entry has
+// one block and one base value, hence one coefficient).
+bool block_signs(int pattern, int side, const Side& s, int NB, uint64_t* mask);
 // Number of pattern families; side: 0 = A, 1 = B, 2 = W.
 // Family whose H pattern (pairs of products sharing a block of A and a
 // block of C) equals one gauge's H support in compressed rows, or -1.
@@ -122,8 +126,10 @@ struct FormArgs {
                     // consecutive entries, at [((g R + r) (bc/128) + y/128) br + x];
                     // 3 the same values rounded to bf16 first, one per 128 x 128
                     // block, at [((g R + r) (bc/128) + y/128) (br/128) + x/128]
-  int trie = 0;     // every gauge's coefficients agree on the entries that the
-                    // family's prefix-shared chains share (set by the host)
+  int trie = 0;     // every gauge is a sign variant of the family's base
+                    // scheme (block_signs), so the prefix-shared chains apply
+  const uint64_t* sgn = nullptr;  // with trie: per gauge, bit b set where the
+                                  // coefficients of block b are the base's negated
 };
 // pattern: family id from match_pattern (side A or B), or -1 for the
 // generic kernel.

@@ -20,8 +20,7 @@ struct PatternRef {
   const int16_t* hrowptr;
   const int16_t* hidx;
   bool trie[2];             // prefix-shared chains generated (A, B)
-  int nchk[2];              // entries whose coefficient must equal a representative's
-  const int16_t* tchk[2];   // pairs (entry, representative entry)
+  const uint32_t* val[2];   // the base scheme's coefficient bits per list entry
 };
 
 #define FM_PATTERN_REF(P)                                                    \
@@ -36,8 +35,7 @@ struct PatternRef {
              pat::P::H::rowptr,                                              \
              pat::P::H::idx,                                                 \
              {pat::P::A::TRIE, pat::P::B::TRIE},                             \
-             {pat::P::A::NCHK, pat::P::B::NCHK},                             \
-             {pat::P::A::tchk, pat::P::B::tchk}},
+             {pat::P::A::val, pat::P::B::val}},
 
 const PatternRef kPatterns[] = {FM_PATTERN_FAMILIES(FM_PATTERN_REF)};
 constexpr int kNumPatterns = sizeof(kPatterns) / sizeof(kPatterns[0]);
@@ -62,19 +60,28 @@ int match_pattern(int side, const Side& s, int R, int NB) {
   return -1;
 }
 
-bool trie_valid(int pattern, int side, const Side& s) {
-  if (pattern < 0 || pattern >= kNumPatterns || side < 0 || side > 1) return false;
+bool block_signs(int pattern, int side, const Side& s, int NB, uint64_t* mask) {
+  if (pattern < 0 || pattern >= kNumPatterns || side < 0 || side > 1 || NB > 64) return false;
   const PatternRef& P = kPatterns[pattern];
-  if (!P.trie[side]) return false;
-  // entries are indices into one scheme's list (s.off[0] == 0)
-  for (int c = 0; c < P.nchk[side]; ++c) {
-    const size_t e = (size_t)P.tchk[side][2 * c], rep = (size_t)P.tchk[side][2 * c + 1];
-    if (e >= s.coef.size() || rep >= s.coef.size()) return false;
-    uint32_t a, b;
-    std::memcpy(&a, &s.coef[e], 4);
-    std::memcpy(&b, &s.coef[rep], 4);
-    if (a != b) return false;
+  if (!P.trie[side] || (int)s.coef.size() != P.nnz[side]) return false;
+  // every coefficient must be its base value with the sign of its block:
+  // equal bits, or bits differing in the sign alone, the same way for
+  // every entry of a block (entries index one scheme's list, s.off[0] == 0)
+  uint64_t neg = 0, seen = 0;
+  for (size_t e = 0; e < s.coef.size(); ++e) {
+    const int b = s.idx[e];
+    if (b < 0 || b >= NB) return false;
+    uint32_t c;
+    std::memcpy(&c, &s.coef[e], 4);
+    const uint32_t diff = c ^ P.val[side][e];
+    if (diff != 0u && diff != 0x80000000u) return false;
+    const uint64_t bit = (uint64_t)1 << b;
+    const uint64_t flip = diff ? bit : 0;
+    if ((seen & bit) && (neg & bit) != flip) return false;
+    seen |= bit;
+    neg |= flip;
   }
+  *mask = neg;
   return true;
 }
 

@@ -104,9 +104,10 @@ def dense(R, m, k, n):
 
 
 # Coefficient values of the families whose block sums share prefixes: the
-# base scheme flattened (sign variants multiply every coefficient of a block
-# by that block's sign, so they share the same prefixes; the library checks
-# each gauge's coefficients before using the shared form).
+# base scheme flattened.  A sign variant multiplies every coefficient of a
+# block by that block's sign, so its chains share the same prefixes; the
+# library finds each gauge's block signs on the host and the kernels build
+# the coefficients from them and these values.
 VALUES = {
     "Strassen1": power_vals(schemes.strassen(), 1),
     "Strassen2": power_vals(schemes.strassen(), 2),
@@ -156,13 +157,12 @@ def trie(rowptr, idx, vals):
     nodes in depth-first order (parent before children; a node's parent is
     the latest node one level up) as (depth, block, representative entry),
     the products completed at each node (CSR over the completion order),
-    and the (entry, representative entry) pairs whose coefficients a gauge
-    must have equal for the shared form to give its chains' values."""
+    and the representative entry of every node (its coefficient is the
+    node's)."""
     R = len(rowptr) - 1
     children, key = {}, {}
     nodes = []  # (parent, block, entry, depth)
     ends = {}
-    rep_of = []
     for r in range(R):
         parent, prefix = -1, ()
         for pos, e in enumerate(range(rowptr[r], rowptr[r + 1])):
@@ -171,9 +171,7 @@ def trie(rowptr, idx, vals):
                 key[prefix] = len(nodes)
                 nodes.append((parent, idx[e], e, pos))
                 children.setdefault(parent, []).append(key[prefix])
-            node = key[prefix]
-            rep_of.append((e, nodes[node][2]))
-            parent = node
+            parent = key[prefix]
         ends.setdefault(parent, []).append(r)
     order = []
 
@@ -190,8 +188,14 @@ def trie(rowptr, idx, vals):
     for n in order:
         endprod += ends.get(n, [])
         endptr.append(len(endprod))
-    chk = [(e, rep) for e, rep in rep_of if e != rep]
-    return depth, blk, ent, endptr, endprod, chk
+    return depth, blk, ent, endptr, endprod
+
+
+def f32bits(v):
+    """fp32 bit pattern of v (exactly representable) as a C literal."""
+    b = np.float32(v)
+    assert float(b) == float(v)
+    return f"0x{int(b.view(np.uint32)):08x}u"
 
 
 def arr(vals, per_line=24):
@@ -226,23 +230,25 @@ def main():
                     else:
                         vals += [Vv[r, l * n + j] for l in range(k) for j in range(n) if Vv[r, l * n + j]]
                 assert len(vals) == len(idx)
-                depth, blk, ent, endptr, endprod, chk = trie(rowptr, idx, vals)
-                out.append("    // prefix-shared chains (depth-first trie; see gen_patterns.trie)")
+                depth, blk, ent, endptr, endprod = trie(rowptr, idx, vals)
+                out.append("    // prefix-shared chains (depth-first trie; see gen_patterns.trie) and the")
+                out.append("    // base scheme's coefficients (fp32 bits) per node and per list entry")
                 out.append(f"    static constexpr bool TRIE = true;")
-                out.append(f"    static constexpr int NN = {len(depth)}, MAXD = {max(depth) + 1}, "
-                           f"NCHK = {len(chk)};")
+                out.append(f"    static constexpr int NN = {len(depth)}, MAXD = {max(depth) + 1};")
                 out.append(f"    static constexpr int16_t tdepth[{len(depth)}] = {arr(depth)};")
                 out.append(f"    static constexpr int16_t tblk[{len(depth)}] = {arr(blk)};")
                 out.append(f"    static constexpr int16_t tent[{len(depth)}] = {arr(ent)};")
                 out.append(f"    static constexpr int16_t tendptr[{len(endptr)}] = {arr(endptr)};")
                 out.append(f"    static constexpr int16_t tendprod[{len(endprod)}] = {arr(endprod)};")
-                out.append(f"    static constexpr int16_t tchk[{max(1, 2 * len(chk))}] = "
-                           f"{arr([x for pair in chk for x in pair] or [0])};")
+                out.append(f"    static constexpr uint32_t tval[{len(depth)}] = "
+                           f"{arr([f32bits(vals[e]) for e in ent], 8)};")
+                out.append(f"    static constexpr uint32_t val[{len(vals)}] = {arr([f32bits(v) for v in vals], 8)};")
             else:
                 out.append("    static constexpr bool TRIE = false;")
-                out.append("    static constexpr int NN = 0, MAXD = 1, NCHK = 0;")
+                out.append("    static constexpr int NN = 0, MAXD = 1;")
                 out.append("    static constexpr int16_t tdepth[1] = {0}, tblk[1] = {0}, tent[1] = {0};")
-                out.append("    static constexpr int16_t tendptr[2] = {0, 0}, tendprod[1] = {0}, tchk[1] = {0};")
+                out.append("    static constexpr int16_t tendptr[2] = {0, 0}, tendprod[1] = {0};")
+                out.append("    static constexpr uint32_t tval[1] = {0}, val[1] = {0};")
             out.append("  };")
         # where H_rs = <w_r, w_s> <u_r, u_s> of the joint rounding can be
         # nonzero: both products share a block of A and one of C (families of
