@@ -471,14 +471,33 @@ __device__ __forceinline__ void form_trie_gauges(const FormArgs& a, int g0, int 
       rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + (size_t)g * P::R * bsz, (short)0,
                                                (int)(P::R * bsz), 0x00020000);
     float nv[P::MAXD][VW];
-    // scale loads through an offset the compiler cannot see through,
-    // renewed every 16 nodes, so the scalar loads stay near their products
+    // Mode 1 scales, one group of 16 nodes ahead: the scales of the
+    // products that complete in group G + 1 are loaded at the start of group
+    // G (through an offset the compiler cannot see through, renewed every
+    // group, so the loads neither move to the top of the gauge, which needs
+    // more scalar registers than there are, nor down to their use)
+    constexpr int QG = 16, NGR = (P::NN + QG - 1) / QG;
+    [[maybe_unused]] float qb[2][QG];
     int so = 0;
+    auto load_scales = [&](auto gc) {
+      constexpr int G = decltype(gc)::value;
+      if constexpr (MODE == 1 && G < NGR) {
+        constexpr int k0 = P::tendptr[QG * G];
+        constexpr int k1 = P::tendptr[QG * (G + 1) < P::NN ? QG * (G + 1) : P::NN];
+        static_assert(k1 - k0 <= QG, "products completing in one group of nodes");
+        sfor<k0, k1>([&](auto kc) {
+          constexpr int kk = decltype(kc)::value;
+          qb[G & 1][kk - k0] = ro(a.q)[(size_t)g * P::R + P::tendprod[kk] + so];
+        });
+      }
+    };
+    load_scales(std::integral_constant<int, 0>{});
     sfor<0, P::NN>([&](auto tc) {
       constexpr int t = decltype(tc)::value;
-      if constexpr (t % 16 == 0) {
+      if constexpr (t % QG == 0) {
         so = 0;
         asm volatile("" : "+s"(so));
+        load_scales(std::integral_constant<int, t / QG + 1>{});
       }
       constexpr int d = P::tdepth[t], b = P::tblk[t];
       constexpr uint32_t cb = P::tval[t];
@@ -512,8 +531,8 @@ __device__ __forceinline__ void form_trie_gauges(const FormArgs& a, int g0, int 
           for (int v = 0; v < VW; ++v) mf = __builtin_elementwise_maximum(mf, __builtin_fabsf(nv[d][v]));
           atomicMax(smax + ((size_t)(g - g0) * P::R + r) * 16 + (lane & 15), __float_as_uint(mf));
         } else {
-          const float q = ro(a.q)[(size_t)g * P::R + r + so];
-          form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, nv[d], q);
+          constexpr int G = t / QG, k0 = P::tendptr[QG * G];
+          form_encode_store<FMT, VW>(rsrc, voff, (uint32_t)r * bsz, nv[d], qb[G & 1][kk - k0]);
         }
       });
     });
