@@ -903,20 +903,314 @@ void gemm_wide_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict_
   ring::wait_vm_n<0>();  // the loads past the last pair land before the workgroup ends
 }
 
+// Wide workgroup of 8 waves, two per SIMD (tensor or row/column scales,
+// bf16 products, Mb a multiple of 512, Nb of 128, Kb of 64): the workgroup
+// tile, K step, LDS ring, swizzle and loads of gemm_wide_kernel, but each
+// wave computes 128 rows x 64 columns (4 x 2 tiles of 32 x 32, 128
+// accumulators), so the two waves of a SIMD share its matrix unit: while
+// one issues its loads, LDS reads or conversions (which stall a single
+// wave, and with it the matrix unit), the other's matrix instructions run.
+// Waves w and w + 4 (one SIMD) take the same 128 A rows (w % 4) and the two
+// 64-column halves of B.  Per stage a wave loads 4 x 16 A rows and 16 B rows
+// (5 wave-loads).  The raw codes of a stage are read from LDS in two halves
+// (the first 16 bytes of each lane's 32, sub-steps 0 and 1; then the
+// second), each as soon as the previous stage's half is widened, so only
+// one stage of raw codes and two sub-steps of widened fragments are held.
+namespace wide8 {
+constexpr int BM = 512, BN = 128, KS = 64, NT = 512, NSTG = 4;
+constexpr int ROWS = BM + BN;         // rows of KS bytes per stage
+constexpr int STAGE = ROWS * KS;      // 40 KB
+constexpr int LOADS = ROWS / 16 / 8;  // 1 KB wave-loads per wave per stage (5)
+constexpr int STORES = 32;            // 16-byte stores per lane per tile
+
+// the counts used: after a tile's stores, or not; anything less waits for
+// everything (a count above the one needed waits for more than needed)
+__device__ __forceinline__ void wait_vm(int n) {
+  if (n >= LOADS + 2 + STORES) ring::wait_vm_n<LOADS + 2 + STORES>();
+  else if (n >= LOADS + 2) ring::wait_vm_n<LOADS + 2>();
+  else ring::wait_vm_n<0>();
+}
+}  // namespace wide8
+
+template <int FMT, int SC>
+__global__ __launch_bounds__(wide8::NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void gemm_wide8_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict__ Sq,
+                       const float* __restrict__ dT, const float* __restrict__ dS,
+                       float* __restrict__ Mout, int Mb, int Nb, int Kb, int tiles_m, int tiles_n,
+                       int total, int tiled) {
+  using namespace wide8;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[NSTG * STAGE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 3, wn = wave >> 2;
+  const int r32 = lane & 31, h = lane >> 5;
+  const int tiles = tiles_m * tiles_n;
+  const int nk = Kb / KS;
+
+  // XCD x takes tiles [x per, (x + 1) per), per = ceil(total / 8), as in
+  // gemm_wide_kernel
+  const int G = gridDim.x;
+  const bool xcd_split = (G & 7) == 0;
+  const int per = (total + 7) >> 3;
+  const int t = xcd_split ? (blockIdx.x & 7) * per + (blockIdx.x >> 3) : blockIdx.x;
+  const int tstep = xcd_split ? (G >> 3) : G;
+  const int t_end = xcd_split ? min(total, ((blockIdx.x & 7) + 1) * per) : total;
+  if (t >= t_end) return;
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)lds;
+
+  // wave-loads as in gemm_wide_kernel: lane L writes row L / 4 of 16, slot
+  // L % 4, fetching chunk (L % 4) ^ ((row / 4) % 4)
+  const uint32_t dma_off =
+      (uint32_t)(lane >> 2) * (uint32_t)Kb + (uint32_t)(((lane & 3) ^ ((lane >> 4) & 3)) << 4);
+  const size_t kb16 = (size_t)16 * Kb;
+  // this wave's first A row (64 wave) and B row (16 wave) of a tile's panels
+  auto tile_base = [&](int tile, const uint8_t*& Ab, const uint8_t*& Bb) {
+    const int b = tile / tiles, tt = tile - b * tiles;
+    const int tmi = tt / tiles_n;
+    Ab = Tq + ((size_t)b * Mb + (size_t)tmi * BM + (size_t)wave * 64) * Kb;
+    Bb = Sq + ((size_t)b * Nb + (size_t)(tt - tmi * tiles_n) * BN + (size_t)wave * 16) * Kb;
+  };
+  // wave-load j of a stage: j < 4 A rows 64 wave + 16 j, j = 4 B rows 16 wave
+  auto dma_one = [&](const uint8_t* Ab, const uint8_t* Bb, int kt, int buf, int j) {
+    const uint32_t l0 = lds_base + (uint32_t)(buf * STAGE);
+    if (j < 4)
+      wide::dma16s(Ab + j * kb16 + kt * KS, dma_off, l0 + (uint32_t)((wave * 64 + 16 * j) * KS));
+    else
+      wide::dma16s(Bb + kt * KS, dma_off, l0 + (uint32_t)((BM + wave * 16) * KS));
+  };
+  auto issue = [&](const uint8_t* Ab, const uint8_t* Bb, int kt, int buf) {
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) dma_one(Ab, Bb, kt, buf, j);
+  };
+
+  // one stage's raw codes: A rows 128 wm + 32 i + r32, B rows 64 wn + 32 j +
+  // r32, 32 bytes each (two 16-byte chunks: sub-steps 0-1 and 2-3)
+  uint4 ra[4][2], rb[2][2];
+  const uint32_t rd0 = (uint32_t)r32 * KS + (uint32_t)(((2 * h) ^ ((r32 >> 2) & 3)) << 4);
+  const uint32_t rd1 = (uint32_t)r32 * KS + (uint32_t)(((2 * h + 1) ^ ((r32 >> 2) & 3)) << 4);
+  auto read_half = [&](int buf, auto cc) {
+    constexpr int c = decltype(cc)::value;
+    const uint32_t rd = c ? rd1 : rd0;
+    const uint8_t* sa = lds + buf * STAGE + wm * 128 * KS;
+    const uint8_t* sb = lds + buf * STAGE + (BM + wn * 64) * KS;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ra[i][c] = *reinterpret_cast<const uint4*>(sa + i * 32 * KS + rd);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) rb[j][c] = *reinterpret_cast<const uint4*>(sb + j * 32 * KS + rd);
+  };
+  using C0 = std::integral_constant<int, 0>;
+  using C1 = std::integral_constant<int, 1>;
+  auto sel = [](const uint4 (&r)[2], int tsub, int d) -> int {
+    const uint4& c = r[tsub >> 1];
+    return (tsub & 1) ? (d ? (int)c.w : (int)c.z) : (d ? (int)c.y : (int)c.x);
+  };
+  v8bf wa[2][4], wb[2][2];  // widened fragments of two sub-steps
+  auto widen_sub = [&](int tsub, int slot) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) wa[slot][i] = widen8<FMT>(sel(ra[i], tsub, 0), sel(ra[i], tsub, 1));
+#pragma unroll
+    for (int j = 0; j < 2; ++j) wb[slot][j] = widen8<FMT>(sel(rb[j], tsub, 0), sel(rb[j], tsub, 1));
+  };
+  auto pin = [&](int slot) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(wa[slot][i]));
+#pragma unroll
+    for (int j = 0; j < 2; ++j) asm volatile("" : "+v"(wb[slot][j]));
+  };
+
+  // acc[i][j]: the transposed 32 x 32 product, element v of lane (r32, h)
+  // at row i*32 + r32, column j*32 + 8 (v / 4) + 4 h + v % 4 of the wave's
+  // 128 x 64 block
+  v16f acc[4][2];
+  auto epilogue = [&](int tile) {
+    const int b = tile / tiles, tt = tile - b * tiles;
+    const int tmi = tt / tiles_n;
+    const int m0 = tmi * BM, n0 = (tt - tmi * tiles_n) * BN;
+    float* Mo = Mout + (size_t)b * Mb * Nb;
+    const int r_base = m0 + wm * 128 + r32, c_base = n0 + wn * 64 + 4 * h;
+    // tiled layout: pieces in the order (row block wm, i, column tile 2 wn +
+    // j, column group g, lane), one contiguous kilobyte per wave store
+    float* tbase = Mo + (size_t)tt * (BM * BN) + (size_t)wm * (128 * 128) + lane * 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = r_base + i * 32;
+      const float sT = SC == 1 ? dT[(size_t)b * Mb + row] : dT[b];
+      float* prow = Mo + (size_t)row * Nb + c_base;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          float4 sS;
+          if constexpr (SC == 1) {
+            sS = *reinterpret_cast<const float4*>(dS + (size_t)b * Nb + c_base + j * 32 + 8 * g);
+          } else {
+            const float u = dS[b];
+            sS = make_float4(u, u, u, u);
+          }
+          v4f o;
+          o[0] = (acc[i][j][4 * g + 0] * sT) * sS.x;
+          o[1] = (acc[i][j][4 * g + 1] * sT) * sS.y;
+          o[2] = (acc[i][j][4 * g + 2] * sT) * sS.z;
+          o[3] = (acc[i][j][4 * g + 3] * sT) * sS.w;
+          if (tiled)
+            __builtin_nontemporal_store(
+                o, reinterpret_cast<v4f*>(tbase + ((i * 4 + 2 * wn + j) * 4 + g) * 256));
+          else
+            *reinterpret_cast<v4f*>(prow + j * 32 + 8 * g) = o;
+        }
+      }
+    }
+  };
+
+  // Iteration s over the (tile, K step) pairs p_s, in four phases of 8
+  // matrix instructions (one sub-step each), with the 5 wave-loads of
+  // p_{s+3} (into the buffer of p_{s-1}) after matrix instructions 1 and 5:
+  //   A: sub-step 0 (slot 0), widening sub-step 1 into slot 1; 2 loads;
+  //   wait until p_{s+1} has landed and every wave's reads of p_s are done;
+  //   B: sub-step 1 (slot 1), widening sub-step 2 into slot 0, reading the
+  //      first half of p_{s+1}; 1 load;
+  //   C: sub-step 2 (slot 0), widening sub-step 3 into slot 1; 1 load;
+  //   D: sub-step 3 (slot 1), reading the second half of p_{s+1}, widening
+  //      its sub-step 0 into slot 0; 1 load.
+  auto advance = [&](int& tt, int& kk) {
+    if (++kk == nk) {
+      kk = 0;
+      tt += tstep;
+    }
+  };
+  auto mma_dma = [&](int slot, const uint8_t* Ab, const uint8_t* Bb, int kt, int buf, auto j0c,
+                     auto j1c) {
+    constexpr int j0 = decltype(j0c)::value, j1 = decltype(j1c)::value;
+    sfor<0, 8>([&](auto qc) {
+      constexpr int q = decltype(qc)::value;
+      acc[q >> 1][q & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb[slot][q & 1], wa[slot][q >> 1], acc[q >> 1][q & 1], 0, 0, 0);
+      if constexpr (q % 4 == 1 && j0 + q / 4 < j1) dma_one(Ab, Bb, kt, buf, j0 + q / 4);
+    });
+  };
+  // 8 matrix instructions, each followed by N vector-ALU and R LDS-read
+  // instructions (R for the first 6 only)
+  auto groups = [](auto nc, auto rc) {
+    constexpr int N = decltype(nc)::value, R = decltype(rc)::value;
+    sfor<0, 8>([&](auto qc) {
+      constexpr int q = decltype(qc)::value;
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if constexpr (R > 0 && q < 6) __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, N, 0);
+    });
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using I4 = std::integral_constant<int, 4>;
+  using I5 = std::integral_constant<int, 5>;
+  int t1 = t, k1 = 0;  // p_{s+1}
+  advance(t1, k1);
+  int t2 = t1, k2 = k1;  // p_{s+2}
+  advance(t2, k2);
+  int t3 = t2, k3 = k2;  // p_{s+3}
+  advance(t3, k3);
+  const uint8_t *A0, *B0;
+  tile_base(t, A0, B0);
+  issue(A0, B0, 0, 0);
+  int after1 = 0;  // vector-memory operations issued after the group of p_{s+1}
+  if (t1 < t_end) {
+    if (t1 != t) tile_base(t1, A0, B0);
+    issue(A0, B0, k1, 1);
+  }
+  if (t2 < t_end) {
+    if (t2 != t1) tile_base(t2, A0, B0);
+    issue(A0, B0, k2, 2);
+    after1 += LOADS;
+  }
+  const uint8_t *A3 = A0, *B3 = B0;  // panels of the tile of p_{s+3}
+  if (t3 < t_end && t3 != t2) tile_base(t3, A3, B3);
+  wait_vm(t1 < t_end ? after1 + LOADS : 0);  // p_0 has landed
+  FM_COMPILER_FENCE();
+  __builtin_amdgcn_s_barrier();
+  FM_COMPILER_FENCE();
+  read_half(0, C0{});
+  read_half(0, C1{});
+  widen_sub(0, 0);
+  int cb = 0;  // buffer of p_s
+  bool more = true;
+  for (int tile = t; more; tile += tstep) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+    for (int kk = 0; kk < nk; ++kk) {
+      const int b3 = cb == 0 ? NSTG - 1 : cb - 1;  // buffer of p_{s+3} (that of p_{s-1})
+      // A
+      mma_dma(0, A3, B3, k3, b3, I0{}, I2{});
+      widen_sub(1, 1);
+      groups(std::integral_constant<int, 3>{}, I0{});
+      pin(1);
+      __builtin_amdgcn_sched_barrier(0);
+      // p_{s+1} was issued before p_{s+2}'s 5 loads and 2 of p_{s+3}
+      wait_vm(after1 + 2);
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of p_s are done
+      FM_COMPILER_FENCE();
+      __builtin_amdgcn_s_barrier();
+      FM_COMPILER_FENCE();
+      const int nb = cb == NSTG - 1 ? 0 : cb + 1;
+      more = t1 < t_end;
+      // B
+      mma_dma(1, A3, B3, k3, b3, I2{}, I3{});
+      widen_sub(2, 0);
+      read_half(nb, C0{});
+      groups(std::integral_constant<int, 3>{}, I1{});
+      pin(0);
+      __builtin_amdgcn_sched_barrier(0);
+      // C
+      mma_dma(0, A3, B3, k3, b3, I3{}, I4{});
+      widen_sub(3, 1);
+      groups(std::integral_constant<int, 3>{}, I0{});
+      pin(1);
+      __builtin_amdgcn_sched_barrier(0);
+      // D
+      mma_dma(1, A3, B3, k3, b3, I4{}, I5{});
+      read_half(nb, C1{});
+      widen_sub(0, 0);
+      groups(std::integral_constant<int, 3>{}, I1{});
+      pin(0);
+      __builtin_amdgcn_sched_barrier(0);
+      t1 = t2;
+      k1 = k2;
+      t2 = t3;
+      k2 = k3;
+      advance(t3, k3);
+      if (k3 == 0 && t3 < t_end) tile_base(t3, A3, B3);
+      after1 = LOADS;
+      cb = nb;
+    }
+    epilogue(tile);
+    after1 += STORES;
+  }
+  ring::wait_vm_n<0>();  // the loads past the last pair land before the workgroup ends
+}
+
 }  // namespace
 
 namespace {
 int g_block_product_arith = FM_ACC_BF16;
 
-// The wide-wave kernel is the default where it applies; FM_BLOCK_GEMM=dma
-// in the environment selects gemm_dma_kernel instead (for comparisons).
-bool wide_enabled() {
-  static const bool on = [] {
+// The 8-wave wide kernel is the default where it applies; FM_BLOCK_GEMM in
+// the environment selects another for comparisons: "dma" gemm_dma_kernel,
+// "wide4" the 4-wave gemm_wide_kernel.
+int wide_choice() {
+  static const int c = [] {
     const char* e = std::getenv("FM_BLOCK_GEMM");
-    return !(e && std::strcmp(e, "dma") == 0);
+    if (e && std::strcmp(e, "dma") == 0) return 0;
+    if (e && std::strcmp(e, "wide4") == 0) return 1;
+    return 2;
   }();
-  return on;
+  return c;
 }
+bool wide_enabled() { return wide_choice() != 0; }
 
 bool use_wide(int Mb, int Nb, int Kb, int sc, bool out_bf16) {
   return wide_enabled() && g_block_product_arith == FM_ACC_BF16 && (sc == 0 || sc == 1) &&
@@ -953,6 +1247,13 @@ int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, 
       const int grid = (int)std::min<long long>(total, 256);
       if (tiled && SC != 0)
         return fail(FM_E_UNSUPPORTED, "the tiled product layout needs tensor scales");
+      if (wide_choice() == 2) {
+        if (fmt == FM_E4M3)
+          gemm_wide8_kernel<FM_E4M3, SC><<<grid, wide8::NT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
+        else
+          gemm_wide8_kernel<FM_E5M2, SC><<<grid, wide8::NT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
+        return launched("gemm_wide8_kernel");
+      }
       if (fmt == FM_E4M3)
         gemm_wide_kernel<FM_E4M3, SC><<<grid, wide::NT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
       else
