@@ -445,13 +445,16 @@ __device__ __forceinline__ void form_static_gauges(const FormArgs& a, int g0, in
 
 // Gauges g0 <= g < g1 through the family's prefix-shared chains (P::TRIE,
 // one scale per tensor), for sign variants of the family's base scheme: a
-// coefficient is the base value of its list entry (compile time) with the
-// sign of its block, from the gauge's 64-bit block-sign mask (bit b set:
-// block b negated), so no coefficient is read from memory.  Chains that
-// begin with the same (block, base coefficient) entries share their partial
-// sums, so the block sums are the nodes of a trie walked depth first: node
-// t = fmaf(c_t, x[tblk[t]], value of the latest node one level up, or +0 at
-// the root).  The value of the node where a product's chain ends is that
+// coefficient is the base value of its list entry with the sign of its
+// block, from the gauge's 64-bit block-sign mask (bit b set: block b
+// negated).  fmaf(s c, x, acc) = fmaf(c, s x, acc) exactly for s = +-1, so
+// the operand values of a negated block are negated in place (xv holds them
+// under the signs in `applied`; a gauge flips the blocks whose sign changes)
+// and the chains take the base values as compile-time constants: no
+// coefficient is read or built per term.  Chains that begin with the same
+// (block, base coefficient) entries share their partial sums, so the block
+// sums are the nodes of a trie walked depth first: node t = fmaf(c_t,
+// x[tblk[t]], value of the latest node one level up, or +0 at the root).  The value of the node where a product's chain ends is that
 // product's block sum, with the fused multiply-adds of its chain in its
 // order: the bits of the plain chain.  Mode 0 folds each lane's maximum
 // into the product's slot lane % 16 (of the 16 per product that the
@@ -459,13 +462,22 @@ __device__ __forceinline__ void form_static_gauges(const FormArgs& a, int g0, in
 // and stores each product's codes as it completes.
 template <class P, int VW, int MODE, int FMT>
 __device__ __forceinline__ void form_trie_gauges(const FormArgs& a, int g0, int g1,
-                                                 const float (&xv)[P::NB][VW],
+                                                 float (&xv)[P::NB][VW], uint64_t& applied,
                                                  [[maybe_unused]] bool active, uint32_t voff,
                                                  uint32_t* smax) {
   const int lane = threadIdx.x & 63;
   const uint32_t bsz = (uint32_t)a.br * (uint32_t)a.bc;
   for (int g = g0; g < g1; ++g) {
     const uint64_t neg = ro(a.sgn)[g];
+    const uint64_t flip = neg ^ applied;
+    applied = neg;
+    sfor<0, P::NB>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      // the sign bit of block b's change, on the scalar unit
+      const uint32_t m = (uint32_t)((flip >> b) & 1u) << 31;
+#pragma unroll
+      for (int v = 0; v < VW; ++v) xv[b][v] = __uint_as_float(__float_as_uint(xv[b][v]) ^ m);
+    });
     __amdgpu_buffer_rsrc_t rsrc;
     if constexpr (MODE == 1)
       rsrc = __builtin_amdgcn_make_buffer_rsrc(a.codes + (size_t)g * P::R * bsz, (short)0,
@@ -500,21 +512,7 @@ __device__ __forceinline__ void form_trie_gauges(const FormArgs& a, int g0, int 
         load_scales(std::integral_constant<int, t / QG + 1>{});
       }
       constexpr int d = P::tdepth[t], b = P::tblk[t];
-      constexpr uint32_t cb = P::tval[t];
-      // the coefficient: base values of +-1 selected on the scalar unit (bit
-      // test, then a select between inline constants) into a scalar
-      // register; the node index in the assembly keeps each node's select
-      // its own, so the compiler neither holds one register per block over
-      // the whole sequence nor moves the selects to the vector unit
-      float c;
-      if constexpr (cb == 0x3f800000u)
-        asm("; node %3\n\ts_bitcmp1_b64 %1, %2\n\ts_cselect_b32 %0, -1.0, 1.0"
-            : "=s"(c) : "s"(neg), "i"(b), "i"(t) : "scc");
-      else if constexpr (cb == 0xbf800000u)
-        asm("; node %3\n\ts_bitcmp1_b64 %1, %2\n\ts_cselect_b32 %0, 1.0, -1.0"
-            : "=s"(c) : "s"(neg), "i"(b), "i"(t) : "scc");
-      else
-        c = ((neg >> b) & 1u) ? -__builtin_bit_cast(float, cb) : __builtin_bit_cast(float, cb);
+      constexpr float c = __builtin_bit_cast(float, P::tval[t]);
 #pragma unroll
       for (int v = 0; v < VW; ++v) {
         if constexpr (d == 0) nv[0][v] = __builtin_fmaf(c, xv[b][v], 0.0f);
@@ -553,8 +551,9 @@ __device__ __forceinline__ void form_static_body(const FormArgs& a, int gpb, uin
     const uint32_t voff = active ? (uint32_t)(x * a.bc + y0) : 0x80000000u;
     float xv[P::NB][VW];
     form_load<P::NB, VW>(a, xv, active, x, y0);
+    [[maybe_unused]] uint64_t applied = 0;
     if constexpr (P::TRIE && !ROWS)
-      form_trie_gauges<P, VW, MODE, FMT>(a, g0, g1, xv, active, voff, smax);
+      form_trie_gauges<P, VW, MODE, FMT>(a, g0, g1, xv, applied, active, voff, smax);
     else
       form_static_gauges<P, VW, MODE, FMT, ROWS>(a, g0, g1, xv, active, x, y0, voff, smax);
   }
@@ -627,8 +626,9 @@ __global__ __launch_bounds__(kThreads) void form_merged_kernel(FormArgs aq, Form
     float xv[P::NB][VW];
     form_load<P::NB, VW>(aq, xv, active, x, y0);
     if constexpr (P::TRIE) {
-      form_trie_gauges<P, VW, 1, FMT>(aq, g0q, g1q, xv, active, voff, smax);
-      form_trie_gauges<P, VW, 0, FM_E4M3>(am, g0m, g1m, xv, active, voff, smax);
+      uint64_t applied = 0;
+      form_trie_gauges<P, VW, 1, FMT>(aq, g0q, g1q, xv, applied, active, voff, smax);
+      form_trie_gauges<P, VW, 0, FM_E4M3>(am, g0m, g1m, xv, applied, active, voff, smax);
     } else {
       form_static_gauges<P, VW, 1, FMT, false>(aq, g0q, g1q, xv, active, x, y0, voff, smax);
       form_static_gauges<P, VW, 0, FM_E4M3, false>(am, g0m, g1m, xv, active, x, y0, voff, smax);
