@@ -555,17 +555,23 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
 }
 
 
-// Wide-wave persistent kernel (tensor or row/column scales, bf16 products,
-// Mb a multiple of 512, Nb of 128, Kb of 64): workgroup tile 512 x 128, 4
-// waves (one per SIMD), each wave 128 rows x 128 columns = 4 x 4 tiles of
-// 32 x 32 (v_mfma_f32_32x32x16_bf16), K step 64 bytes, a ring of 4 LDS
-// stages of 40 KB (512 + 128 rows of 64 bytes; all 160 KB of the CU's LDS)
-// filled by direct global-to-LDS loads, two to three K steps ahead.  A wave's tile shares every widened A fragment among
-// 4 column tiles and every B fragment among 4 row tiles: per flop half the
-// widening conversions of the 64 x 64 waves of gemm_dma_kernel.  With one
-// wave per SIMD the accumulators (256 per lane) live in the accumulation
-// registers, and the conversions of the next sub-step and the fragment reads
-// of the next stage sit between the matrix instructions of this one.
+// Wide persistent kernel (tensor or row/column scales, bf16 products, Mb a
+// multiple of 512, Nb of 128, Kb of 64): workgroup tile 512 x 128, K step 64
+// bytes, a ring of 4 LDS stages of 40 KB (512 + 128 rows of 64 bytes; all
+// 160 KB of the CU's LDS) filled by direct global-to-LDS loads two to three
+// K steps ahead, 8 waves, two per SIMD.  Each wave computes 128 rows x 64
+// columns = 4 x 2 tiles of 32 x 32 (v_mfma_f32_32x32x16_bf16, 128
+// accumulators), so a widened A fragment feeds 2 matrix instructions and a
+// B fragment 4, and the two waves of a SIMD share its matrix unit: while one
+// issues its loads, LDS reads or conversions (which stall a wave, and with
+// one wave per SIMD the matrix unit with it), the other's matrix
+// instructions run.  Waves w and w + 4 (one SIMD) take the same 128 A rows
+// (w % 4) and the two 64-column halves of B.  Per stage a wave loads 4 x 16
+// A rows and 16 B rows (5 of the 40 wave-loads).  The raw codes of a stage
+// are read from LDS in two halves (the first 16 bytes of each lane's 32,
+// sub-steps 0 and 1; then the second), each as soon as the previous stage's
+// half is widened, so one stage of raw codes and two sub-steps of widened
+// fragments are held.
 //
 // Within a K step, lane (r, h) = (lane % 32, lane / 32) of a 32-row fragment
 // holds the 32 bytes [32h, 32h + 32) of row r; sub-step t (16 k values)
@@ -576,11 +582,7 @@ __global__ __launch_bounds__(DNT) void gemm_dma_kernel(const uint8_t* __restrict
 // served per LDS cycle of a 16-byte fragment read (16 consecutive rows, 4
 // rows per 256-byte bank window) then hit 16 distinct 16-byte bank groups.
 namespace wide {
-constexpr int BM = 512, BN = 128, KS = 64, NT = 256, NSTG = 4;
-constexpr int ROWS = BM + BN;         // rows of KS bytes per stage
-constexpr int STAGE = ROWS * KS;      // 40 KB
-constexpr int LOADS = ROWS / 16 / 4;  // 1 KB wave-loads per wave per stage (10)
-constexpr int STORES = 64;            // 16-byte stores per lane per tile
+constexpr int BM = 512, BN = 128, KS = 64;
 
 // global_load_lds_dwordx4 with a scalar base and a 32-bit per-lane offset:
 // lane L writes the 16 bytes it fetched at M0 + 16 L (M0 written by SALU
@@ -593,331 +595,10 @@ __device__ __forceinline__ void dma16s(const void* sbase, uint32_t voff, uint32_
                : "v"(voff), "s"(sbase), "s"(lds_addr)
                : "memory", "m0");
 }
-
-// s_waitcnt on the vector-memory counter only, for the few counts used (a
-// count above the largest encodable, 63, waits for more than needed)
-__device__ __forceinline__ void wait_vm(int n) {
-  if (n >= 63) ring::wait_vm_n<63>();
-  else if (n >= 2 * LOADS) ring::wait_vm_n<2 * LOADS>();
-  else if (n >= LOADS) ring::wait_vm_n<LOADS>();
-  else ring::wait_vm_n<0>();
-}
 }  // namespace wide
 
 typedef float v16f __attribute__((ext_vector_type(16)));
 
-// Scheduling-group barriers for one region: 16 times one matrix
-// instruction followed by N instructions of class MASK (0x002 vector ALU,
-// 0x100 LDS reads).
-template <int MASK, int N>
-__device__ __forceinline__ void interleave() {
-  sfor<0, 16>([&](auto) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(MASK, N, 0);
-  });
-}
-
-template <int FMT, int SC>
-__global__ __launch_bounds__(wide::NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void gemm_wide_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict__ Sq,
-                      const float* __restrict__ dT, const float* __restrict__ dS,
-                      float* __restrict__ Mout, int Mb, int Nb, int Kb, int tiles_m, int tiles_n,
-                      int total, int tiled) {
-  using namespace wide;
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[NSTG * STAGE];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int r32 = lane & 31, h = lane >> 5;
-  const int tiles = tiles_m * tiles_n;
-  const int nk = Kb / KS;
-
-  // workgroups go round-robin over the 8 XCDs: give each XCD a contiguous
-  // range of tiles (whole products), so a product's operand panels stay in
-  // one L2
-  const int G = gridDim.x;
-  // (XCD x takes tiles [x per, (x + 1) per), per = ceil(total / 8))
-  const bool xcd_split = (G & 7) == 0;
-  const int per = (total + 7) >> 3;
-  const int t = xcd_split ? (blockIdx.x & 7) * per + (blockIdx.x >> 3) : blockIdx.x;
-  const int tstep = xcd_split ? (G >> 3) : G;
-  const int t_end = xcd_split ? min(total, ((blockIdx.x & 7) + 1) * per) : total;
-  if (t >= t_end) return;
-  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)lds;
-
-  // A wave-load fills 16 rows of 64 bytes: lane L writes row L / 4, slot L %
-  // 4, and fetches the chunk (L % 4) ^ ((row / 4) % 4); rows start at
-  // multiples of 16, so the chunk and the row's offset in the operand depend
-  // on the lane alone (one 32-bit offset), and the row block's address is
-  // uniform (a scalar base).  Wave w loads its own 128 A rows (8 wave-loads)
-  // and B rows [32 w, 32 w + 32) (2 wave-loads).
-  const uint32_t dma_off =
-      (uint32_t)(lane >> 2) * (uint32_t)Kb + (uint32_t)(((lane & 3) ^ ((lane >> 4) & 3)) << 4);
-  const size_t kb16 = (size_t)16 * Kb;
-  // first rows of a tile's A and B panels
-  auto tile_base = [&](int tile, const uint8_t*& Ab, const uint8_t*& Bb) {
-    const int b = tile / tiles, tt = tile - b * tiles;
-    const int tmi = tt / tiles_n;
-    Ab = Tq + ((size_t)b * Mb + (size_t)tmi * BM + (size_t)wave * 128) * Kb;
-    Bb = Sq + ((size_t)b * Nb + (size_t)(tt - tmi * tiles_n) * BN + (size_t)wave * 32) * Kb;
-  };
-  auto issue = [&](const uint8_t* Ab, const uint8_t* Bb, int kt, int buf) {
-    const uint32_t l0 = lds_base + (uint32_t)(buf * STAGE);
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      dma16s(Ab + j * kb16 + kt * KS, dma_off, l0 + (uint32_t)((wave * 128 + 16 * j) * KS));
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      dma16s(Bb + j * kb16 + kt * KS, dma_off, l0 + (uint32_t)((BM + wave * 32 + 16 * j) * KS));
-  };
-
-  // one stage's raw codes: A rows 128 wave + 32 i + r32, B rows 32 j + r32,
-  // 32 bytes each (two 16-byte chunks)
-  uint4 ra[4][2], rb[4][2];
-  // the swizzle of rows 32 i + r32 is (r32 / 4) % 4 for every i: per-lane
-  // offsets of the two chunks, plus compile-time row-block offsets
-  const uint32_t rd0 = (uint32_t)r32 * KS + (uint32_t)(((2 * h) ^ ((r32 >> 2) & 3)) << 4);
-  const uint32_t rd1 = (uint32_t)r32 * KS + (uint32_t)(((2 * h + 1) ^ ((r32 >> 2) & 3)) << 4);
-  auto read_stage = [&](int buf) {
-    const uint8_t* sa = lds + buf * STAGE + wave * 128 * KS;
-    const uint8_t* sb = lds + buf * STAGE + BM * KS;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i][0] = *reinterpret_cast<const uint4*>(sa + i * 32 * KS + rd0);
-      ra[i][1] = *reinterpret_cast<const uint4*>(sa + i * 32 * KS + rd1);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      rb[j][0] = *reinterpret_cast<const uint4*>(sb + j * 32 * KS + rd0);
-      rb[j][1] = *reinterpret_cast<const uint4*>(sb + j * 32 * KS + rd1);
-    }
-  };
-  auto sel = [](const uint4 (&r)[2], int t, int d) -> int {
-    const uint4& c = r[t >> 1];
-    return (t & 1) ? (d ? (int)c.w : (int)c.z) : (d ? (int)c.y : (int)c.x);
-  };
-  v8bf wa[3][4], wb[3][4];  // widened fragments of three sub-steps
-  auto widen_sub = [&](int t, int slot) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) wa[slot][i] = widen8<FMT>(sel(ra[i], t, 0), sel(ra[i], t, 1));
-#pragma unroll
-    for (int j = 0; j < 4; ++j) wb[slot][j] = widen8<FMT>(sel(rb[j], t, 0), sel(rb[j], t, 1));
-  };
-  // makes a slot's values appear used here, so their conversions stay in
-  // the phase that computes them (instead of sinking towards their use)
-  auto pin = [&](int slot) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      asm volatile("" : "+v"(wa[slot][i]));
-      asm volatile("" : "+v"(wb[slot][i]));
-    }
-  };
-
-  // acc[i][j] holds the transposed 32 x 32 product: element v of lane
-  // (r32, h) is output row i*32 + r32, column j*32 + 8 (v / 4) + 4 h + v % 4
-  // of the wave's 128 x 128 block
-  v16f acc[4][4];
-  auto mma = [&](int slot) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb[slot][j], wa[slot][i], acc[i][j], 0, 0, 0);
-  };
-
-  auto epilogue = [&](int tile) {
-    const int b = tile / tiles, tt = tile - b * tiles;
-    const int tmi = tt / tiles_n;
-    const int m0 = tmi * BM, n0 = (tt - tmi * tiles_n) * BN;
-    float* Mo = Mout + (size_t)b * Mb * Nb;
-    const int r_base = m0 + wave * 128 + r32, c_base = n0 + 4 * h;
-    // tiled layout: the 16-byte pieces of a tile in the order (wave, i, j,
-    // column group g, lane), so each store of a wave is one contiguous
-    // kilobyte
-    float* tbase = Mo + (size_t)tt * (BM * BN) + (size_t)wave * (128 * 128) + lane * 4;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = r_base + i * 32;
-      const float sT = SC == 1 ? dT[(size_t)b * Mb + row] : dT[b];
-      float* prow = Mo + (size_t)row * Nb + c_base;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          float4 sS;
-          if constexpr (SC == 1) {
-            sS = *reinterpret_cast<const float4*>(dS + (size_t)b * Nb + c_base + j * 32 + 8 * g);
-          } else {
-            const float u = dS[b];
-            sS = make_float4(u, u, u, u);
-          }
-          v4f o;
-          o[0] = (acc[i][j][4 * g + 0] * sT) * sS.x;
-          o[1] = (acc[i][j][4 * g + 1] * sT) * sS.y;
-          o[2] = (acc[i][j][4 * g + 2] * sT) * sS.z;
-          o[3] = (acc[i][j][4 * g + 3] * sT) * sS.w;
-          if (tiled)
-            __builtin_nontemporal_store(o, reinterpret_cast<v4f*>(tbase + ((i * 4 + j) * 4 + g) * 256));
-          else
-            *reinterpret_cast<v4f*>(prow + j * 32 + 8 * g) = o;
-        }
-      }
-    }
-  };
-
-  // Sequence of (tile, K-step) pairs p_0, p_1, ...; p_s lives in LDS buffer
-  // s mod 4, and its 4 sub-steps run in order.  Iteration s, in four phases
-  // whose instructions are interleaved with the matrix instructions (each
-  // region's order fixed by scheduling-group barriers and program order):
-  //   A: sub-step 0 of p_s, widening sub-step 1;
-  //   B: sub-step 1, widening sub-steps 2 and 3 (the raw codes of p_s are
-  //      then dead);
-  //   wait until p_{s+1} has landed and every wave is done reading p_s;
-  //   C: sub-step 2, reading p_{s+1} from LDS;
-  //   D: sub-step 3, widening sub-step 0 of p_{s+1}.
-  // The 10 wave-loads of p_{s+3} go out spread over the four phases (one
-  // after every fourth matrix instruction; the TA then never has a burst to
-  // absorb), into the buffer of p_{s-1}, free since the previous iteration's
-  // barrier.  The loads run ahead across tile boundaries; the accumulators
-  // are cleared at the start of a tile and stored after its last K step.
-  auto advance = [&](int& tt, int& kk) {
-    if (++kk == nk) {
-      kk = 0;
-      tt += tstep;
-    }
-  };
-  // one wave-load j of a stage: j < 8 rows of A, 8 and 9 rows of B
-  auto dma_one = [&](const uint8_t* Ab, const uint8_t* Bb, int kt, int buf, int j) {
-    const uint32_t l0 = lds_base + (uint32_t)(buf * STAGE);
-    if (j < 8)
-      dma16s(Ab + j * kb16 + kt * KS, dma_off, l0 + (uint32_t)((wave * 128 + 16 * j) * KS));
-    else
-      dma16s(Bb + (j - 8) * kb16 + kt * KS, dma_off, l0 + (uint32_t)((BM + wave * 32 + 16 * (j - 8)) * KS));
-  };
-  // mma of one sub-step slot with wave-loads j0..j1-1 of p_{s+3} placed
-  // after matrix instructions 2, 6, 10, 14 (program order)
-  auto mma_dma = [&](int slot, const uint8_t* Ab, const uint8_t* Bb, int kt, int buf, auto j0c,
-                     auto j1c) {
-    constexpr int j0 = decltype(j0c)::value, j1 = decltype(j1c)::value;
-    sfor<0, 16>([&](auto qc) {
-      constexpr int q = decltype(qc)::value;
-      acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wb[slot][q & 3], wa[slot][q >> 2], acc[q >> 2][q & 3], 0, 0, 0);
-      if constexpr (q % 4 == 2 && j0 + q / 4 < j1) dma_one(Ab, Bb, kt, buf, j0 + q / 4);
-    });
-  };
-  using I0 = std::integral_constant<int, 0>;
-  using I3 = std::integral_constant<int, 3>;
-  using I6 = std::integral_constant<int, 6>;
-  using I8 = std::integral_constant<int, 8>;
-  using I10 = std::integral_constant<int, 10>;
-  int t1 = t, k1 = 0;  // p_{s+1}
-  advance(t1, k1);
-  int t2 = t1, k2 = k1;  // p_{s+2}
-  advance(t2, k2);
-  int t3 = t2, k3 = k2;  // p_{s+3}
-  advance(t3, k3);
-  const uint8_t *A0, *B0;
-  tile_base(t, A0, B0);
-  issue(A0, B0, 0, 0);
-  int after1 = 0;  // vector-memory operations issued after the group of p_{s+1}
-  if (t1 < t_end) {
-    if (t1 != t) tile_base(t1, A0, B0);
-    issue(A0, B0, k1, 1);
-  }
-  if (t2 < t_end) {
-    if (t2 != t1) tile_base(t2, A0, B0);
-    issue(A0, B0, k2, 2);
-    after1 += LOADS;
-  }
-  const uint8_t *A3 = A0, *B3 = B0;  // panels of the tile of p_{s+3}
-  if (t3 < t_end && t3 != t2) tile_base(t3, A3, B3);
-  wait_vm(t1 < t_end ? after1 + LOADS : 0);  // p_0 has landed
-  FM_COMPILER_FENCE();
-  __builtin_amdgcn_s_barrier();
-  FM_COMPILER_FENCE();
-  read_stage(0);
-  widen_sub(0, 0);
-  int cb = 0;  // buffer of p_s
-  bool more = true;
-  for (int tile = t; more; tile += tstep) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
-    for (int kk = 0; kk < nk; ++kk) {
-      // the loads of p_{s+3} go out even past the last pair (stale but
-      // in-bounds panels into a free buffer, never read), so every
-      // iteration issues the same operations
-      const int b3 = cb == 0 ? NSTG - 1 : cb - 1;  // buffer of p_{s+3} (that of p_{s-1})
-      // A: 3 wave-loads of p_{s+3}
-      mma_dma(0, A3, B3, k3, b3, I0{}, I3{});
-      widen_sub(1, 1);
-      interleave<0x002, 2>();
-      pin(1);
-      __builtin_amdgcn_sched_barrier(0);
-      // B: 3 more
-      mma_dma(1, A3, B3, k3, b3, I3{}, I6{});
-      widen_sub(2, 2);
-      widen_sub(3, 0);
-      interleave<0x002, 4>();
-      pin(2);
-      pin(0);
-      __builtin_amdgcn_sched_barrier(0);
-      // p_{s+1} issued before p_{s+2} (all 10) and 6 of p_{s+3}
-      wait_vm(after1 + 6);
-      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of p_s are done
-      FM_COMPILER_FENCE();
-      __builtin_amdgcn_s_barrier();
-      FM_COMPILER_FENCE();
-      const int nb = cb == NSTG - 1 ? 0 : cb + 1;
-      more = t1 < t_end;
-      // C: reads of p_{s+1}, 2 wave-loads
-      mma_dma(2, A3, B3, k3, b3, I6{}, I8{});
-      read_stage(nb);
-      interleave<0x100, 1>();
-      __builtin_amdgcn_sched_barrier(0);
-      // D: the last 2
-      mma_dma(0, A3, B3, k3, b3, I8{}, I10{});
-      widen_sub(0, 1);
-      interleave<0x002, 2>();
-      pin(1);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        wa[0][i] = wa[1][i];
-        wb[0][i] = wb[1][i];
-      }
-      const int after2 = LOADS;  // p_{s+3}'s group, after p_{s+2}'s
-      t1 = t2;
-      k1 = k2;
-      t2 = t3;
-      k2 = k3;
-      advance(t3, k3);
-      if (k3 == 0 && t3 < t_end) tile_base(t3, A3, B3);
-      after1 = after2;
-      cb = nb;
-    }
-    epilogue(tile);
-    after1 += STORES;
-  }
-  ring::wait_vm_n<0>();  // the loads past the last pair land before the workgroup ends
-}
-
-// Wide workgroup of 8 waves, two per SIMD (tensor or row/column scales,
-// bf16 products, Mb a multiple of 512, Nb of 128, Kb of 64): the workgroup
-// tile, K step, LDS ring, swizzle and loads of gemm_wide_kernel, but each
-// wave computes 128 rows x 64 columns (4 x 2 tiles of 32 x 32, 128
-// accumulators), so the two waves of a SIMD share its matrix unit: while
-// one issues its loads, LDS reads or conversions (which stall a single
-// wave, and with it the matrix unit), the other's matrix instructions run.
-// Waves w and w + 4 (one SIMD) take the same 128 A rows (w % 4) and the two
-// 64-column halves of B.  Per stage a wave loads 4 x 16 A rows and 16 B rows
-// (5 wave-loads).  The raw codes of a stage are read from LDS in two halves
-// (the first 16 bytes of each lane's 32, sub-steps 0 and 1; then the
-// second), each as soon as the previous stage's half is widened, so only
-// one stage of raw codes and two sub-steps of widened fragments are held.
 namespace wide8 {
 constexpr int BM = 512, BN = 128, KS = 64, NT = 512, NSTG = 4;
 constexpr int ROWS = BM + BN;         // rows of KS bytes per stage
@@ -950,8 +631,9 @@ void gemm_wide8_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict
   const int tiles = tiles_m * tiles_n;
   const int nk = Kb / KS;
 
-  // XCD x takes tiles [x per, (x + 1) per), per = ceil(total / 8), as in
-  // gemm_wide_kernel
+  // workgroups go round-robin over the 8 XCDs: give each XCD a contiguous
+  // range of tiles (whole products), so a product's operand panels stay in
+  // one L2: XCD x takes tiles [x per, (x + 1) per), per = ceil(total / 8)
   const int G = gridDim.x;
   const bool xcd_split = (G & 7) == 0;
   const int per = (total + 7) >> 3;
@@ -961,8 +643,11 @@ void gemm_wide8_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict
   if (t >= t_end) return;
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)lds;
 
-  // wave-loads as in gemm_wide_kernel: lane L writes row L / 4 of 16, slot
-  // L % 4, fetching chunk (L % 4) ^ ((row / 4) % 4)
+  // A wave-load fills 16 rows of 64 bytes: lane L writes row L / 4, slot L %
+  // 4, and fetches the chunk (L % 4) ^ ((row / 4) % 4); rows start at
+  // multiples of 16, so the chunk and the row's offset in the operand depend
+  // on the lane alone (one 32-bit offset), and the row block's address is
+  // uniform (a scalar base)
   const uint32_t dma_off =
       (uint32_t)(lane >> 2) * (uint32_t)Kb + (uint32_t)(((lane & 3) ^ ((lane >> 4) & 3)) << 4);
   const size_t kb16 = (size_t)16 * Kb;
@@ -1200,19 +885,15 @@ void gemm_wide8_kernel(const uint8_t* __restrict__ Tq, const uint8_t* __restrict
 namespace {
 int g_block_product_arith = FM_ACC_BF16;
 
-// The 8-wave wide kernel is the default where it applies; FM_BLOCK_GEMM in
-// the environment selects another for comparisons: "dma" gemm_dma_kernel,
-// "wide4" the 4-wave gemm_wide_kernel.
-int wide_choice() {
-  static const int c = [] {
+// The wide kernel is the default where it applies; FM_BLOCK_GEMM=dma in the
+// environment selects gemm_dma_kernel instead (for comparisons).
+bool wide_enabled() {
+  static const bool on = [] {
     const char* e = std::getenv("FM_BLOCK_GEMM");
-    if (e && std::strcmp(e, "dma") == 0) return 0;
-    if (e && std::strcmp(e, "wide4") == 0) return 1;
-    return 2;
+    return !(e && std::strcmp(e, "dma") == 0);
   }();
-  return c;
+  return on;
 }
-bool wide_enabled() { return wide_choice() != 0; }
 
 bool use_wide(int Mb, int Nb, int Kb, int sc, bool out_bf16) {
   return wide_enabled() && g_block_product_arith == FM_ACC_BF16 && (sc == 0 || sc == 1) &&
@@ -1249,18 +930,11 @@ int launch_block_gemm_sc(const uint8_t* Tq, const uint8_t* Sq, const float* dT, 
       const int grid = (int)std::min<long long>(total, 256);
       if (tiled && SC != 0)
         return fail(FM_E_UNSUPPORTED, "the tiled product layout needs tensor scales");
-      if (wide_choice() == 2) {
-        if (fmt == FM_E4M3)
-          gemm_wide8_kernel<FM_E4M3, SC><<<grid, wide8::NT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
-        else
-          gemm_wide8_kernel<FM_E5M2, SC><<<grid, wide8::NT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
-        return launched("gemm_wide8_kernel");
-      }
       if (fmt == FM_E4M3)
-        gemm_wide_kernel<FM_E4M3, SC><<<grid, wide::NT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
+        gemm_wide8_kernel<FM_E4M3, SC><<<grid, wide8::NT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
       else
-        gemm_wide_kernel<FM_E5M2, SC><<<grid, wide::NT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
-      return launched("gemm_wide_kernel");
+        gemm_wide8_kernel<FM_E5M2, SC><<<grid, wide8::NT, 0, st>>>(Tq, Sq, dT, dS, Mout, Mb, Nb, Kb, tm, tn, T, tiled);
+      return launched("gemm_wide8_kernel");
     }
   }
   if (Kb % GK == 0) {
