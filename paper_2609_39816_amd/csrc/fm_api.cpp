@@ -8,7 +8,9 @@
 #include <cstring>
 #include <memory>
 #include <string>
+#include <atomic>
 #include <mutex>
+#include <thread>
 #include <vector>
 
 #include "fm_internal.h"
@@ -373,7 +375,10 @@ int extend_tables(Tables& T, const fm_scheme* const* schemes, int g_from, int g_
   for (int g = g_from; g < g_to; ++g) {
     const fm_scheme* s = schemes[g];
     if (!s) return fail(FM_E_ARG, "null scheme in orbit");
-    fm_scheme flat = power(*s, levels);
+    // one level: the scheme itself (no copy)
+    fm_scheme powered;
+    if (levels > 1) powered = power(*s, levels);
+    const fm_scheme& flat = levels > 1 ? powered : *s;
     if (flat.m != geo.gm || flat.k != geo.gk || flat.n != geo.gn || flat.R != geo.R)
       return fail(FM_E_MISMATCH, "schemes of one orbit must share grid and rank");
     Lists L;
@@ -707,6 +712,13 @@ fm_scheme* clone(const fm_scheme& s) {
     return nullptr;
   }
 }
+fm_scheme* clone(fm_scheme&& s) {
+  try {
+    return new fm_scheme(std::move(s));
+  } catch (...) {
+    return nullptr;
+  }
+}
 
 }  // namespace
 
@@ -873,7 +885,7 @@ static int gauge_one(const fm_scheme* s, const double* P, const double* Q, const
           g.W[o] = (Pi[(size_t)a * m + a] * s->W[o]) * Si[(size_t)b * n + b];
         }
     }
-    *out = clone(g);
+    *out = clone(std::move(g));
     return *out ? FM_OK : fail(FM_E_NOMEM, "out of host memory");
   }
   // Terms with an exactly zero factor are skipped: the accumulator starts at
@@ -947,7 +959,7 @@ static int gauge_one(const fm_scheme* s, const double* P, const double* Q, const
   };
   if (!inverse_ok(Pm, Pi, m) || !inverse_ok(Qm, Qi, k) || !inverse_ok(Sm, Si, n))
     return fail(FM_E_SINGULAR, "gauge matrix is too ill-conditioned to invert accurately");
-  *out = clone(g);
+  *out = clone(std::move(g));
   return *out ? FM_OK : fail(FM_E_NOMEM, "out of host memory");
 }
 
@@ -965,13 +977,40 @@ int fm_gauge_apply_batch(const fm_scheme* s, int G, const double* P, const doubl
   if (G < 0) return fail(FM_E_ARG, "G must be non-negative");
   const size_t mm = (size_t)s->m * s->m, kk = (size_t)s->k * s->k, nn = (size_t)s->n * s->n;
   for (int g = 0; g < G; ++g) out[g] = nullptr;
+  // gauges are independent: up to 16 host threads take them in turn (each
+  // gauge of a three-level orbit is about half a millisecond of arithmetic
+  // and copying); a failure is reported for the first failing gauge, by
+  // applying it again on the calling thread (errors are per thread)
+  std::vector<int> rcs((size_t)G, 0);
+  std::atomic<int> next{0};
+  auto work = [&] {
+    for (;;) {
+      const int g = next.fetch_add(1);
+      if (g >= G) break;
+      rcs[g] = gauge_one(s, P + g * mm, Q + g * kk, S + g * nn, &out[g]);
+    }
+  };
+  const long long per_gauge = (long long)s->R * (s->m * s->k + s->k * s->n + s->m * s->n);
+  const int hw = std::max(1, (int)std::thread::hardware_concurrency());
+  const int nt = per_gauge * G < (1 << 16) ? 1 : std::min(std::min(16, hw), G);
+  std::vector<std::thread> pool;
+  try {
+    for (int i = 1; i < nt; ++i) pool.emplace_back(work);
+  } catch (...) {
+    // fewer threads: the calling thread takes the rest
+  }
+  work();
+  for (auto& th : pool) th.join();
   for (int g = 0; g < G; ++g) {
-    if (int rc = gauge_one(s, P + g * mm, Q + g * kk, S + g * nn, &out[g])) {
-      for (int h = 0; h < g; ++h) {
+    if (rcs[g]) {
+      for (int h = 0; h < G; ++h) {
         fm_scheme_free(out[h]);
         out[h] = nullptr;
       }
-      return rc;
+      fm_scheme* again = nullptr;
+      const int rc = gauge_one(s, P + g * mm, Q + g * kk, S + g * nn, &again);
+      fm_scheme_free(again);
+      return rc ? rc : rcs[g];
     }
   }
   return FM_OK;

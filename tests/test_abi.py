@@ -199,6 +199,26 @@ def test_batched_gauge_equals_single_calls():
     assert e.value.name == "FM_E_SINGULAR"
 
 
+def test_batched_gauge_on_host_threads():
+    """A three-level orbit is gauged on several host threads: every result
+    equals the single call bit for bit, and a singular gauge deep in the
+    batch fails the whole call with its own error."""
+    s3 = fm.Scheme.base("strassen").kron(3)
+    w = sy.WORKLOADS["strassen3_8192x27648x5120_sign512"]
+    gs = sy.gauges(w, count=96)
+    batch = s3.gauge_orbit(gs)
+    assert len(batch) == 96
+    for i in (0, 1, 37, 95):
+        P, Q, S = gs[i]
+        for a, b in zip(s3.gauge(P, Q, S).coeffs(), batch[i].coeffs()):
+            assert np.array_equal(a.view(np.uint64), b.view(np.uint64))
+    bad = list(gs)
+    bad[61] = (np.zeros((8, 8)), np.eye(8), np.eye(8))
+    with pytest.raises(fm.FmError) as e:
+        s3.gauge_orbit(bad)
+    assert e.value.name == "FM_E_SINGULAR"
+
+
 def test_int8_certificate_from_the_library():
     """Prop. 1's quantities as the library computes them (host side): the
     printed L_A = L_B = 4, L_W = 16 for two-level Strassen, certified at code
