@@ -599,7 +599,7 @@ __global__ __launch_bounds__(kThreads) void form_static_kernel(FormArgs a, int g
 // so the block's operand values are read from memory once and from that
 // XCD's L2 by the other slices.
 template <class P, int VW, int FMT>
-__global__ __launch_bounds__(kThreads) void form_merged_kernel(FormArgs aq, FormArgs am, int gpbq,
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void form_merged_kernel(FormArgs aq, FormArgs am, int gpbq,
                                                                int gpbm, int gx, int gy) {
   extern __shared__ uint32_t smax[];  // am's [gauge][product][wave * 4 + row]
   const int w = blockIdx.x;
