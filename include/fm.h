@@ -506,6 +506,18 @@ int fm_bf16_round(const float* x, int64_t n, int impl, float* out, void* hip_str
  * string; "" on error. */
 const char* fm_scheme_kernel_family(const fm_scheme* s, int levels);
 
+/* Whether `s` flattened to `levels` is a sign variant of its kernel family's
+ * base scheme on operand side `side` (0: A's block sums, 1: B's): every
+ * coefficient equal to the family's base coefficient times a sign that
+ * depends only on its operand block (the case the family's formation
+ * kernels take with compile-time coefficients, Sec. 2.1's sign orbit
+ * flattened).  *is_sign (host) gets 1 or 0; when 1, *neg_mask (host) gets
+ * bit b set for each block b (row-major over the side's grid of blocks, B's
+ * transposed) whose sign is -1.  Returns FM_E_ARG for null pointers, a side
+ * other than 0 or 1, or levels outside [1, 8]. */
+int fm_scheme_sign_variant(const fm_scheme* s, int levels, int side, int* is_sign,
+                           uint64_t* neg_mask);
+
 /* Kernel timing for measurement.  While enabled (on != 0), every launch of
  * the kernel classes below made by this library is bracketed by two HIP
  * events recorded on the launch's own stream:

@@ -1483,6 +1483,24 @@ const char* fm_scheme_kernel_family(const fm_scheme* s, int levels) {
   return "generic";
 }
 
+int fm_scheme_sign_variant(const fm_scheme* s, int levels, int side, int* is_sign,
+                           uint64_t* neg_mask) {
+  clear_error();
+  if (!s || !is_sign || !neg_mask) return fail(FM_E_ARG, "null pointer");
+  if (side < 0 || side > 1) return fail(FM_E_ARG, "side must be 0 (A) or 1 (B)");
+  if (levels < 1 || levels > 8) return fail(FM_E_ARG, "levels must be in [1, 8]");
+  const fm_scheme f = power(*s, levels);
+  Lists L;
+  build_lists(f, L);
+  const Side& sd = side ? L.b : L.a;
+  const int nb = side ? f.n * f.k : f.m * f.k;
+  const int p = match_pattern(side, sd, f.R, nb);
+  uint64_t m = 0;
+  *is_sign = block_signs(p, side, sd, nb, &m) ? 1 : 0;
+  *neg_mask = *is_sign ? m : 0;
+  return FM_OK;
+}
+
 int fm_timing_enable(int on) {
   clear_error();
   g_timing.on = on != 0;

@@ -93,6 +93,7 @@ def _load():
         "fm_fp8_encode": (i, [p, i64, i, i, p, p]),
         "fm_bf16_round": (i, [p, i64, i, p, p]),
         "fm_scheme_kernel_family": (ct.c_char_p, [p, i]),
+        "fm_scheme_sign_variant": (i, [p, i, i, ct.POINTER(ct.c_int), ct.POINTER(ct.c_uint64)]),
         "fm_status": (i, [p, sz, p]),
         "fm_set_block_product_arithmetic": (i, [i]),
         "fm_timing_enable": (i, [i]),
@@ -220,6 +221,14 @@ class Scheme:
 
     def kernel_family(self, levels: int = 1) -> str:
         return lib.fm_scheme_kernel_family(self._h, levels).decode()
+
+    def sign_variant(self, levels: int = 1, side: int = 0):
+        """(is_sign, neg_mask): whether the flattened scheme's side (0: A,
+        1: B) is a sign variant of its family's base scheme, and the mask of
+        negated blocks."""
+        flag, mask = ct.c_int(), ct.c_uint64()
+        _check(lib.fm_scheme_sign_variant(self._h, levels, side, ct.byref(flag), ct.byref(mask)))
+        return bool(flag.value), int(mask.value)
 
     def flat_dims(self, levels: int = 1):
         m, k, n, R = self.dims

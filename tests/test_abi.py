@@ -310,3 +310,35 @@ def test_misaligned_scale_arrays_are_refused_before_any_device_work():
         rc = L.fm_block_products_scaled(p(good), p(good), p(dT), p(dS), 2, 512, 128, 128,
                                         fm.E4M3, fm.SCALE_GROUP, p(good), None)
         assert fm.ERRORS[rc] == "FM_E_ARG" and "aligned" in L.fm_last_error().decode()
+
+
+def test_sign_variant_masks():
+    """The host's sign-variant check (which selects the compile-time
+    coefficient formation) against Sec. 2.1's sign action written out: block
+    (i, l) of A carries d_i e_l, block (l, j) of B carries e_l f_j; scaled,
+    GL-gauged or rescaled-product schemes are not sign variants."""
+    s3 = fm.Scheme.base("strassen").kron(3)
+    assert s3.sign_variant(1, 0) == (True, 0) and s3.sign_variant(1, 1) == (True, 0)
+    w = sy.WORKLOADS["strassen3_8192x27648x5120_sign512"]
+    for P, Q, S in sy.gauges(w, count=6)[1:]:
+        d, e, f = np.diag(P), np.diag(Q), np.diag(S)
+        want_a = sum(1 << (i * 8 + l) for i in range(8) for l in range(8) if d[i] * e[l] < 0)
+        want_b = sum(1 << (j * 8 + l) for j in range(8) for l in range(8) if e[l] * f[j] < 0)
+        h = s3.gauge(P, Q, S)
+        assert h.sign_variant(1, 0) == (True, want_a)
+        assert h.sign_variant(1, 1) == (True, want_b)
+    s2 = fm.Scheme.base("strassen")
+    # a diagonal gauge with a non-unit entry: same structure, not a sign variant
+    P = np.diag([2.0, 1.0])
+    assert s2.gauge(P, np.eye(2), np.eye(2)).sign_variant(2, 0)[0] is False
+    assert s2.gauge(P, np.eye(2), np.eye(2)).sign_variant(2, 1)[0] is True
+    # a dense GL gauge: no family with compiled coefficients
+    P, Q, S = sy.gl_gauges(2, 2, 2, 1, seed=3)[0]
+    assert s2.gauge(P, Q, S).sign_variant(1, 0)[0] is False
+    # products rescaled one by one: the structure of the family, other values
+    U, V, W, m, k, n = fm._schemes.strassen()
+    alpha = np.array([2.0, 0.5, 4.0, 1.0, 0.25, 8.0, 2.0])
+    h = fm.Scheme.load(U * alpha[:, None], V, W / alpha[:, None], m, k, n)
+    assert h.sign_variant(2, 0)[0] is False and h.sign_variant(2, 1)[0] is True
+    with pytest.raises(fm.FmError):
+        s2.sign_variant(1, 2)
