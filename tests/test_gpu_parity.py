@@ -398,6 +398,34 @@ def test_nonfinite_input_is_reported():
     fm.status(ws)  # cleared
 
 
+def test_orbit_mixing_sign_variants_and_other_family_members():
+    """Sign variants of two-level Strassen take the compile-time coefficient
+    formation; a diagonal gauge with a non-unit entry has the same nonzero
+    structure but is no sign variant, so a chunk holding it is formed by the
+    generic kernels.  Every chunking gives the one-chunk bits, and both kinds
+    of gauge match the oracle's errors."""
+    say("[parity] sign variants beside other family members")
+    w = sy.scaled(sy.WORKLOADS["strassen2_2048x4096x4096_sign512"], 256, 512, 256, G=5)
+    A, B = sy.operands(w)
+    At, Bt = gpu(A), gpu(B)
+    gauges = sy.gauges(w)
+    odd = (np.diag([2.0, 1.0, 1.0, -1.0]), np.diag([1.0, -1.0, 0.5, 1.0]), np.eye(4))
+    gauges = gauges[:3] + [odd] + gauges[3:]
+    hips, orcs, levels = schemes_for(w, gauges)
+    assert hips[0].sign_variant(levels, 0)[0] and not hips[3].sign_variant(levels, 0)[0]
+    Cref = fm.reference_f64(At, Bt)
+    e1 = fm.orbit_eval(hips, At, Bt, Cref, levels)
+    for ch in (1, 2, 4):
+        ws = fm.workspace(fm.workspace_size(hips[0], w.M, w.N, w.K, levels, len(hips), ch))
+        e2 = fm.orbit_eval(hips, At, Bt, Cref, levels, ws=ws)
+        assert np.array_equal(e1.view(np.uint64), e2.view(np.uint64)), ch
+    Cref_o = oracle.reference_f64(A, B)
+    for gi in (2, 3, 4):
+        check_operands(hips[gi], orcs[gi], levels, A, B, At, Bt, "e4m3")
+        Co = oracle.lowp_matmul(A, B, *oracle.flatten_f32(orcs[gi]))
+        assert abs(e1[gi] / oracle.rel_fro(Co, Cref_o) - 1) <= 1e-2, gi
+
+
 def test_chunked_orbit_equals_single_launch_and_is_deterministic():
     say("[parity] chunking and determinism")
     w = sy.scaled(sy.WORKLOADS["strassen2_2048x4096x4096_sign512"], 256, 256, 256, G=24)
