@@ -119,6 +119,55 @@ def cpu_model():
     return None
 
 
+def library_gemm(w, geo, dev, iters=5):
+    """The vendor library's GEMMs (torch, which calls hipBLASLt) on the shapes
+    of the block products, after the timed region: one gauge's R products as
+    one bf16 batched product (bf16 out), and the flat M x K x N product in
+    bf16 and with the FP8 instructions (E4M3, unit scales, fp32 out; their
+    sums are not exact, unlike the library's own block products).  Operands
+    are random, contiguous and resident; times are HIP-event averages."""
+    import torch
+    gm, gk, gn, R = geo
+    Mb, Kb, Nb = w.M // gm, w.K // gk, w.N // gn
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters
+
+    res = {}
+    a = torch.randn((R, Mb, Kb), generator=g, device=dev, dtype=torch.bfloat16)
+    b = torch.randn((R, Kb, Nb), generator=g, device=dev, dtype=torch.bfloat16)
+    ms = timed(lambda: torch.bmm(a, b))
+    res["bmm_bf16_one_gauge"] = dict(shape=[R, Mb, Kb, Nb], ms=round(ms, 4),
+                                     tflops=round(2.0 * R * Mb * Kb * Nb / ms / 1e9, 1))
+    del a, b
+    a = torch.randn((w.M, w.K), generator=g, device=dev, dtype=torch.bfloat16)
+    b = torch.randn((w.K, w.N), generator=g, device=dev, dtype=torch.bfloat16)
+    flat = 2.0 * w.M * w.K * w.N
+    ms = timed(lambda: a @ b)
+    res["mm_bf16_flat"] = dict(shape=[w.M, w.K, w.N], ms=round(ms, 4),
+                               tflops=round(flat / ms / 1e9, 1))
+    a8 = a.to(torch.float8_e4m3fn)
+    b8 = b.t().contiguous().to(torch.float8_e4m3fn).t()
+    one = torch.ones((), device=dev)
+    ms = timed(lambda: torch._scaled_mm(a8, b8, one, one, out_dtype=torch.float32))
+    res["scaled_mm_fp8_flat"] = dict(shape=[w.M, w.K, w.N], ms=round(ms, 4),
+                                     tflops=round(flat / ms / 1e9, 1))
+    del a, b, a8, b8
+    torch.cuda.empty_cache()
+    return res
+
+
 # Classical-equivalent flops the oracle is given per gauge in the CPU sample:
 # at about 0.04 TFLOP/s on 16 host cores this is about 8 s per gauge.
 CPU_SAMPLE_FLOPS = 4e11
@@ -283,6 +332,9 @@ def main():
     ap.add_argument("--int8-size", type=int, default=4096)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--library-gemm", action="store_true",
+                    help="also time the vendor library's GEMMs (torch on hipBLASLt) on the "
+                         "block-product shapes, as context for the block-product kernel")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; the gauge orbit would "
@@ -465,6 +517,9 @@ def main():
         "pipeline": pipe,
         "kernel_classes": per_class_rate,
     }
+    if args.library_gemm:
+        log("[bench] library GEMMs on the block-product shapes")
+        out["library_gemm"] = library_gemm(w, geo, dev)
     if not args.no_cpu_baseline:
         log("[bench] oracle baseline on the host cores")
         out["cpu_baseline"] = cpu_baseline(w, A, B, gauges, smode)
