@@ -30,8 +30,20 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
+
+/* Host allocation that ends the process with a message when it fails (the  */
+/* oracle's buffers are test-sized; a failure is a broken test set-up).      */
+static void* orc_alloc(size_t n) {
+  void* p = malloc(n ? n : 1);
+  if (!p) {
+    fprintf(stderr, "oracle: out of host memory (%zu bytes)\n", n);
+    abort();
+  }
+  return p;
+}
 
 /* ------------------------------------------------------------------------ */
 /* FP8 formats (OCP 8-bit floating point: E4M3FN and E5M2).                  */
@@ -260,7 +272,7 @@ void orc_quantize_row_groups(const float* T, int rows, int cols, int fmt, uint8_
 void orc_quantize_bf16_blocks(const float* T, int rows, int cols, int fmt, uint8_t* codes,
                               float* d) {
   int nkg = rows / ORC_GROUP, nzb = cols / ORC_GROUP;
-  float* t = (float*)malloc(sizeof(float) * (size_t)rows * cols);
+  float* t = (float*)orc_alloc(sizeof(float) * (size_t)rows * cols);
   for (int64_t i = 0; i < (int64_t)rows * cols; ++i) t[i] = orc_bf16_round(T[i]);
   for (int kg = 0; kg < nkg; ++kg)
     for (int zb = 0; zb < nzb; ++zb) {
@@ -304,8 +316,8 @@ static float exact_sum_to_float(__int128 s, int fmt) {
 
 void orc_block_product(const uint8_t* Tq, const uint8_t* Sq, float dT, float dS,
                        int br, int bc, int bk, int fmt, float* Mout) {
-  int64_t* ti = (int64_t*)malloc(sizeof(int64_t) * (size_t)br * bk);
-  int64_t* sti = (int64_t*)malloc(sizeof(int64_t) * (size_t)bc * bk); /* Sq^T */
+  int64_t* ti = (int64_t*)orc_alloc(sizeof(int64_t) * (size_t)br * bk);
+  int64_t* sti = (int64_t*)orc_alloc(sizeof(int64_t) * (size_t)bc * bk); /* Sq^T */
   for (int64_t i = 0; i < (int64_t)br * bk; ++i) ti[i] = code_to_int(Tq[i], fmt);
   for (int y = 0; y < bk; ++y)
     for (int z = 0; z < bc; ++z)
@@ -358,8 +370,8 @@ void orc_block_product_groups_acc(const uint8_t* Tq, const uint8_t* Sq, const fl
                                   const float* dS, int br, int bc, int bk, int fmt, int bf16_out,
                                   float* Mout) {
   int ng = bk / ORC_GROUP, nzb = bc / ORC_GROUP;
-  int64_t* ti = (int64_t*)malloc(sizeof(int64_t) * (size_t)br * bk);
-  int64_t* sti = (int64_t*)malloc(sizeof(int64_t) * (size_t)bc * bk); /* Sq^T */
+  int64_t* ti = (int64_t*)orc_alloc(sizeof(int64_t) * (size_t)br * bk);
+  int64_t* sti = (int64_t*)orc_alloc(sizeof(int64_t) * (size_t)bc * bk); /* Sq^T */
   for (int64_t i = 0; i < (int64_t)br * bk; ++i) ti[i] = code_to_int(Tq[i], fmt);
   for (int y = 0; y < bk; ++y)
     for (int z = 0; z < bc; ++z)
@@ -485,10 +497,10 @@ int orc_lowp_matmul(const float* A, const float* B, int M, int N, int K,
   if (M % gm || K % gk || N % gn) return -1;
   int br = M / gm, bk = K / gk, bc = N / gn;
   int64_t tsz = (int64_t)br * bk, ssz = (int64_t)bk * bc, msz = (int64_t)br * bc;
-  float* T = (float*)malloc(sizeof(float) * (size_t)(tsz > ssz ? tsz : ssz));
-  uint8_t* tq = (uint8_t*)malloc((size_t)tsz);
-  uint8_t* sq = (uint8_t*)malloc((size_t)ssz);
-  float* Mr = Mr_out ? Mr_out : (float*)malloc(sizeof(float) * (size_t)(msz * R));
+  float* T = (float*)orc_alloc(sizeof(float) * (size_t)(tsz > ssz ? tsz : ssz));
+  uint8_t* tq = (uint8_t*)orc_alloc((size_t)tsz);
+  uint8_t* sq = (uint8_t*)orc_alloc((size_t)ssz);
+  float* Mr = Mr_out ? Mr_out : (float*)orc_alloc(sizeof(float) * (size_t)(msz * R));
   for (int r = 0; r < R; ++r) {
     orc_block_sum(A, M, K, gm, gk, U + (int64_t)r * gm * gk, T);
     float dT = orc_quantize_tensor(T, tsz, fmt, tq);
@@ -524,19 +536,19 @@ int orc_lowp_matmul_sm(const float* A, const float* B, int M, int N, int K,
     return orc_lowp_matmul(A, B, M, N, K, gm, gk, gn, R, U, V, W, fmt, C, Tq_out, dT_out,
                            Sq_out, dS_out, Mr_out);
   if (scale_mode != 1 && scale_mode != 2) return -2;
-  if (M % gm || K % gk || N % gn) return -1;
+  if (R < 1 || M % gm || K % gk || N % gn) return -1;
   int br = M / gm, bk = K / gk, bc = N / gn;
   if (scale_mode == 2 && (bk % ORC_GROUP || bc % ORC_GROUP)) return -1;
   /* scales per product: mode 1 br and bc; mode 2 (bk/128) br and (bk/128) (bc/128) */
   int64_t nta = scale_mode == 1 ? br : (int64_t)(bk / ORC_GROUP) * br;
   int64_t nsb = scale_mode == 1 ? bc : (int64_t)(bk / ORC_GROUP) * (bc / ORC_GROUP);
   int64_t tsz = (int64_t)br * bk, ssz = (int64_t)bk * bc, msz = (int64_t)br * bc;
-  float* T = (float*)malloc(sizeof(float) * (size_t)(tsz > ssz ? tsz : ssz));
-  uint8_t* tq = (uint8_t*)malloc((size_t)tsz);
-  uint8_t* sq = (uint8_t*)malloc((size_t)ssz);
-  float* dT = (float*)malloc(sizeof(float) * (size_t)nta);
-  float* dS = (float*)malloc(sizeof(float) * (size_t)nsb);
-  float* Mr = Mr_out ? Mr_out : (float*)malloc(sizeof(float) * (size_t)(msz * R));
+  float* T = (float*)orc_alloc(sizeof(float) * (size_t)(tsz > ssz ? tsz : ssz));
+  uint8_t* tq = (uint8_t*)orc_alloc((size_t)tsz);
+  uint8_t* sq = (uint8_t*)orc_alloc((size_t)ssz);
+  float* dT = (float*)orc_alloc(sizeof(float) * (size_t)nta);
+  float* dS = (float*)orc_alloc(sizeof(float) * (size_t)nsb);
+  float* Mr = Mr_out ? Mr_out : (float*)orc_alloc(sizeof(float) * (size_t)(msz * R));
   for (int r = 0; r < R; ++r) {
     orc_block_sum(A, M, K, gm, gk, U + (int64_t)r * gm * gk, T);
     if (scale_mode == 1) orc_quantize_rows(T, br, bk, fmt, tq, dT);
@@ -567,7 +579,7 @@ int orc_lowp_matmul_sm(const float* A, const float* B, int M, int N, int K,
 void orc_form_operands(const float* X, int rows, int cols, int gr, int gc, int R,
                        const float* coef, int fmt, uint8_t* codes, float* d) {
   int64_t sz = (int64_t)(rows / gr) * (cols / gc);
-  float* T = (float*)malloc(sizeof(float) * (size_t)sz);
+  float* T = (float*)orc_alloc(sizeof(float) * (size_t)sz);
   for (int r = 0; r < R; ++r) {
     orc_block_sum(X, rows, cols, gr, gc, coef + (int64_t)r * gr * gc, T);
     d[r] = orc_quantize_tensor(T, sz, fmt, codes + r * sz);
@@ -589,7 +601,7 @@ void orc_form_operands_sm(const float* X, int rows, int cols, int gr, int gc, in
   }
   int br = rows / gr, bc = cols / gc;
   int64_t sz = (int64_t)br * bc;
-  float* T = (float*)malloc(sizeof(float) * (size_t)sz);
+  float* T = (float*)orc_alloc(sizeof(float) * (size_t)sz);
   /* mode 2 scales per product: A (bc/128) br, B (br/128) (bc/128) */
   int64_t nd = scale_mode == 1 ? (side == 0 ? br : bc)
                                : (side == 0 ? (int64_t)(bc / ORC_GROUP) * br
@@ -686,8 +698,8 @@ static void rescale_accumulate(const double* P, const float* dA, const float* dB
 void orc_int8_classical(const int8_t* Ac, const float* dA, const int8_t* Bc, const float* dB,
                         int M, int N, int K, int g, float* out) {
   int ng = K / g;
-  int64_t* P = (int64_t*)malloc(sizeof(int64_t) * (size_t)M * N);
-  double* Pd = (double*)malloc(sizeof(double) * (size_t)M * N);
+  int64_t* P = (int64_t*)orc_alloc(sizeof(int64_t) * (size_t)M * N);
+  double* Pd = (double*)orc_alloc(sizeof(double) * (size_t)M * N);
   for (int64_t i = 0; i < (int64_t)M * N; ++i) out[i] = 0.0f;
   for (int gi = 0; gi < ng; ++gi) {
     orc_int8_group_product(Ac, Bc, M, N, K, g, gi, P);
@@ -718,9 +730,9 @@ void orc_int8_group_product_fast(const int8_t* Ac, const int8_t* Bc, int M, int 
                                  int64_t* viol) {
   const int br = M / gm, bc = N / gn;
   const int64_t lim = (int64_t)1 << 31;
-  double* T = (double*)malloc(sizeof(double) * (size_t)br * h);
-  double* S = (double*)malloc(sizeof(double) * (size_t)h * bc);
-  double* Mr = (double*)malloc(sizeof(double) * (size_t)R * br * bc);
+  double* T = (double*)orc_alloc(sizeof(double) * (size_t)br * h);
+  double* S = (double*)orc_alloc(sizeof(double) * (size_t)h * bc);
+  double* Mr = (double*)orc_alloc(sizeof(double) * (size_t)R * br * bc);
   for (int64_t i = 0; i < (int64_t)M * N; ++i) P[i] = 0.0;
   for (int k0 = gi * g; k0 < (gi + 1) * g; k0 += gk * h) { /* one call */
     for (int r = 0; r < R; ++r) {
@@ -790,7 +802,7 @@ int orc_int8_fast(const int8_t* Ac, const float* dA, const int8_t* Bc, const flo
                   const float* V, const float* W, float* out, int64_t* viol) {
   if (M % gm || N % gn || K % g || g % (gk * h)) return -1;
   int ng = K / g;
-  double* P = (double*)malloc(sizeof(double) * (size_t)M * N);
+  double* P = (double*)orc_alloc(sizeof(double) * (size_t)M * N);
   for (int64_t i = 0; i < (int64_t)M * N; ++i) out[i] = 0.0f;
   for (int gi = 0; gi < ng; ++gi) {
     orc_int8_group_product_fast(Ac, Bc, M, N, K, g, gi, h, gm, gk, gn, R, U, V, W, 0, P, viol);
@@ -834,12 +846,12 @@ void orc_int8_group_product_corrected(const int8_t* Ac, const int8_t* Bc, int M,
                                       const float* U, const float* V, const float* W, double* P,
                                       double* stats, double* counts) {
   const int br = M / gm, bc = N / gn;
-  int64_t* A0 = (int64_t*)malloc(sizeof(int64_t) * (size_t)br * h);
-  int64_t* RA = (int64_t*)malloc(sizeof(int64_t) * (size_t)br * h);
-  int64_t* B0 = (int64_t*)malloc(sizeof(int64_t) * (size_t)h * bc);
-  int64_t* RB = (int64_t*)malloc(sizeof(int64_t) * (size_t)h * bc);
-  int64_t* Mr = (int64_t*)malloc(sizeof(int64_t) * (size_t)R * br * bc);
-  double* Mabs = (double*)malloc(sizeof(double) * (size_t)R * br * bc);
+  int64_t* A0 = (int64_t*)orc_alloc(sizeof(int64_t) * (size_t)br * h);
+  int64_t* RA = (int64_t*)orc_alloc(sizeof(int64_t) * (size_t)br * h);
+  int64_t* B0 = (int64_t*)orc_alloc(sizeof(int64_t) * (size_t)h * bc);
+  int64_t* RB = (int64_t*)orc_alloc(sizeof(int64_t) * (size_t)h * bc);
+  int64_t* Mr = (int64_t*)orc_alloc(sizeof(int64_t) * (size_t)R * br * bc);
+  double* Mabs = (double*)orc_alloc(sizeof(double) * (size_t)R * br * bc);
   for (int64_t i = 0; i < (int64_t)M * N; ++i) P[i] = 0.0;
   for (int k0 = gi * g; k0 < (gi + 1) * g; k0 += gk * h) { /* one call */
     for (int r = 0; r < R; ++r) {
@@ -952,7 +964,7 @@ int orc_int8_fast_corrected(const int8_t* Ac, const float* dA, const int8_t* Bc,
                             double* stats, double* counts) {
   if (M % gm || N % gn || K % g || g % (gk * h)) return -1;
   int ng = K / g;
-  double* P = (double*)malloc(sizeof(double) * (size_t)M * N);
+  double* P = (double*)orc_alloc(sizeof(double) * (size_t)M * N);
   for (int64_t i = 0; i < (int64_t)M * N; ++i) out[i] = 0.0f;
   for (int gi = 0; gi < ng; ++gi) {
     orc_int8_group_product_corrected(Ac, Bc, M, N, K, g, gi, h, gm, gk, gn, R, U, V, W, P, stats,
@@ -1137,12 +1149,12 @@ int orc_lowp_matmul_repaired(const float* A, const float* B, int M, int N, int K
   int64_t nta = (int64_t)nkg * br, nsb = (int64_t)nkg * nzb;
   int64_t tsz = (int64_t)br * bk, ssz = (int64_t)bk * bc, msz = (int64_t)br * bc;
   /* row scaling */
-  int* kx = (int*)malloc(sizeof(int) * (size_t)M);
+  int* kx = (int*)orc_alloc(sizeof(int) * (size_t)M);
   const float* Ause = A;
   float* As = NULL;
   for (int t = 0; t < M; ++t) kx[t] = (flags & 1) ? orc_row_exponent(A + (int64_t)t * K, K) : 0;
   if (flags & 1) {
-    As = (float*)malloc(sizeof(float) * (size_t)M * K);
+    As = (float*)orc_alloc(sizeof(float) * (size_t)M * K);
     for (int t = 0; t < M; ++t) {
       float f = ldexpf(1.0f, -kx[t]);
       for (int i = 0; i < K; ++i) As[(int64_t)t * K + i] = A[(int64_t)t * K + i] * f;
@@ -1151,11 +1163,11 @@ int orc_lowp_matmul_repaired(const float* A, const float* B, int M, int N, int K
   }
   if (rowexp_out) memcpy(rowexp_out, kx, sizeof(int) * (size_t)M);
   /* B side for every product first: joint rounding looks across r */
-  float* S = (float*)malloc(sizeof(float) * (size_t)ssz);
-  float* Sb = (float*)malloc(sizeof(float) * (size_t)(ssz * R));
-  float* qS = (float*)malloc(sizeof(float) * (size_t)(nsb * R));
-  float* dS = (float*)malloc(sizeof(float) * (size_t)(nsb * R));
-  uint8_t* sq = (uint8_t*)malloc((size_t)(ssz * R));
+  float* S = (float*)orc_alloc(sizeof(float) * (size_t)ssz);
+  float* Sb = (float*)orc_alloc(sizeof(float) * (size_t)(ssz * R));
+  float* qS = (float*)orc_alloc(sizeof(float) * (size_t)(nsb * R));
+  float* dS = (float*)orc_alloc(sizeof(float) * (size_t)(nsb * R));
+  uint8_t* sq = (uint8_t*)orc_alloc((size_t)(ssz * R));
   for (int r = 0; r < R; ++r) {
     orc_block_sum(B, K, N, gk, gn, V + (int64_t)r * gk * gn, S);
     for (int64_t i = 0; i < ssz; ++i) Sb[r * ssz + i] = orc_bf16_round(S[i]);
@@ -1168,11 +1180,11 @@ int orc_lowp_matmul_repaired(const float* A, const float* B, int M, int N, int K
       }
   }
   if (flags & 2) {
-    float* H = (float*)malloc(sizeof(float) * (size_t)R * R);
+    float* H = (float*)orc_alloc(sizeof(float) * (size_t)R * R);
     orc_repair_gram(U, W, R, gm * gk, gm * gn, H);
-    float* sv = (float*)malloc(sizeof(float) * (size_t)R * 3);
+    float* sv = (float*)orc_alloc(sizeof(float) * (size_t)R * 3);
     float *qv = sv + R, *dv = sv + 2 * R;
-    uint8_t* cv = (uint8_t*)malloc((size_t)R);
+    uint8_t* cv = (uint8_t*)orc_alloc((size_t)R);
     for (int y = 0; y < bk; ++y)
       for (int z = 0; z < bc; ++z) {
         int64_t pos = (int64_t)y * bc + z;
@@ -1190,10 +1202,10 @@ int orc_lowp_matmul_repaired(const float* A, const float* B, int M, int N, int K
     free(cv);
   }
   /* A side, products, reconstruction */
-  float* T = (float*)malloc(sizeof(float) * (size_t)tsz);
-  uint8_t* tq = (uint8_t*)malloc((size_t)tsz);
-  float* dT = (float*)malloc(sizeof(float) * (size_t)nta);
-  float* Mr = Mr_out ? Mr_out : (float*)malloc(sizeof(float) * (size_t)(msz * R));
+  float* T = (float*)orc_alloc(sizeof(float) * (size_t)tsz);
+  uint8_t* tq = (uint8_t*)orc_alloc((size_t)tsz);
+  float* dT = (float*)orc_alloc(sizeof(float) * (size_t)nta);
+  float* Mr = Mr_out ? Mr_out : (float*)orc_alloc(sizeof(float) * (size_t)(msz * R));
   for (int r = 0; r < R; ++r) {
     orc_block_sum(Ause, M, K, gm, gk, U + (int64_t)r * gm * gk, T);
     orc_quantize_row_groups(T, br, bk, fmt, tq, dT);

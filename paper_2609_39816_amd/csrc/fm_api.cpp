@@ -987,7 +987,12 @@ int fm_gauge_apply_batch(const fm_scheme* s, int G, const double* P, const doubl
     for (;;) {
       const int g = next.fetch_add(1);
       if (g >= G) break;
-      rcs[g] = gauge_one(s, P + g * mm, Q + g * kk, S + g * nn, &out[g]);
+      // no exception may leave a worker thread (that would end the process)
+      try {
+        rcs[g] = gauge_one(s, P + g * mm, Q + g * kk, S + g * nn, &out[g]);
+      } catch (...) {
+        rcs[g] = FM_E_NOMEM;
+      }
     }
   };
   const long long per_gauge = (long long)s->R * (s->m * s->k + s->k * s->n + s->m * s->n);
@@ -1007,8 +1012,14 @@ int fm_gauge_apply_batch(const fm_scheme* s, int G, const double* P, const doubl
         fm_scheme_free(out[h]);
         out[h] = nullptr;
       }
+      if (rcs[g] == FM_E_NOMEM) return fail(FM_E_NOMEM, "out of host memory");
       fm_scheme* again = nullptr;
-      const int rc = gauge_one(s, P + g * mm, Q + g * kk, S + g * nn, &again);
+      int rc;
+      try {
+        rc = gauge_one(s, P + g * mm, Q + g * kk, S + g * nn, &again);
+      } catch (...) {
+        rc = fail(FM_E_NOMEM, "out of host memory");
+      }
       fm_scheme_free(again);
       return rc ? rc : rcs[g];
     }
