@@ -18,8 +18,10 @@
  *
  * Conventions for every call:
  *   - Return value: FM_OK (0) or a negative FM_E_* code; no call throws or
- *     aborts across the ABI.  fm_last_error() gives a thread-local message
- *     describing the most recent failure on the calling thread.
+ *     aborts across the ABI (a host allocation that fails inside a call
+ *     returns FM_E_NOMEM; the size queries then return 0).  fm_last_error()
+ *     gives a thread-local message describing the most recent failure on
+ *     the calling thread.
  *   - Host arrays are row-major doubles and are copied; the library never
  *     keeps a caller's host pointer.
  *   - Device arrays are caller-owned, row-major, and must be device memory

@@ -727,6 +727,20 @@ int fail(int code, const std::string& msg) {
   return code;
 }
 
+// An exception inside an exported call (a host allocation that failed, or a
+// container asked for more than it can hold) ends the call with FM_E_NOMEM:
+// every exported function is a function-try-block that returns this value
+// (0 or "" for the size and name queries).  Setting the message may itself
+// fail; the message is then left empty.
+int host_failure() noexcept {
+  try {
+    g_err = "host allocation failed";
+  } catch (...) {
+    g_err.clear();
+  }
+  return FM_E_NOMEM;
+}
+
 // ----------------------------------------------------------- kernel timing
 namespace {
 const char* const kTimedNames[T_COUNT] = {"form_amax", "form_quant", "block_gemm", "recon",
@@ -809,7 +823,7 @@ const char* fm_last_error(void) { return g_err.c_str(); }
 const char* fm_version(void) { return "libfm 0.1 (gfx950)"; }
 
 int fm_scheme_load(const double* U, const double* V, const double* W, int m, int n, int k, int R,
-                   fm_scheme** out) {
+                   fm_scheme** out) try {
   clear_error();
   if (!U || !V || !W || !out) return fail(FM_E_ARG, "null pointer");
   *out = nullptr;
@@ -834,6 +848,8 @@ int fm_scheme_load(const double* U, const double* V, const double* W, int m, int
     return fail(FM_E_BRENT, "Brent residual " + std::to_string(res) + " exceeds 1e-9");
   *out = clone(s);
   return *out ? FM_OK : fail(FM_E_NOMEM, "out of host memory");
+} catch (...) {
+  return host_failure();
 }
 
 static int gauge_one(const fm_scheme* s, const double* P, const double* Q, const double* S,
@@ -964,14 +980,16 @@ static int gauge_one(const fm_scheme* s, const double* P, const double* Q, const
 }
 
 int fm_gauge_apply(const fm_scheme* s, const double* P, const double* Q, const double* S,
-                   fm_scheme** out) {
+                   fm_scheme** out) try {
   clear_error();
   if (!s || !P || !Q || !S || !out) return fail(FM_E_ARG, "null pointer");
   return gauge_one(s, P, Q, S, out);
+} catch (...) {
+  return host_failure();
 }
 
 int fm_gauge_apply_batch(const fm_scheme* s, int G, const double* P, const double* Q,
-                         const double* S, fm_scheme** out) {
+                         const double* S, fm_scheme** out) try {
   clear_error();
   if (!s || !P || !Q || !S || !out) return fail(FM_E_ARG, "null pointer");
   if (G < 0) return fail(FM_E_ARG, "G must be non-negative");
@@ -1025,9 +1043,11 @@ int fm_gauge_apply_batch(const fm_scheme* s, int G, const double* P, const doubl
     }
   }
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
-int fm_scheme_kron(const fm_scheme* s, int levels, fm_scheme** out) {
+int fm_scheme_kron(const fm_scheme* s, int levels, fm_scheme** out) try {
   clear_error();
   if (!s || !out) return fail(FM_E_ARG, "null pointer");
   *out = nullptr;
@@ -1043,9 +1063,11 @@ int fm_scheme_kron(const fm_scheme* s, int levels, fm_scheme** out) {
     return fail(FM_E_UNSUPPORTED, "Kronecker power too large");
   *out = clone(power(*s, levels));
   return *out ? FM_OK : fail(FM_E_NOMEM, "out of host memory");
+} catch (...) {
+  return host_failure();
 }
 
-int fm_scheme_dims(const fm_scheme* s, int* m, int* n, int* k, int* R) {
+int fm_scheme_dims(const fm_scheme* s, int* m, int* n, int* k, int* R) try {
   clear_error();
   if (!s) return fail(FM_E_ARG, "null scheme");
   if (m) *m = s->m;
@@ -1053,18 +1075,22 @@ int fm_scheme_dims(const fm_scheme* s, int* m, int* n, int* k, int* R) {
   if (k) *k = s->k;
   if (R) *R = s->R;
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
-int fm_scheme_coeffs(const fm_scheme* s, double* U, double* V, double* W) {
+int fm_scheme_coeffs(const fm_scheme* s, double* U, double* V, double* W) try {
   clear_error();
   if (!s || !U || !V || !W) return fail(FM_E_ARG, "null pointer");
   std::copy(s->U.begin(), s->U.end(), U);
   std::copy(s->V.begin(), s->V.end(), V);
   std::copy(s->W.begin(), s->W.end(), W);
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
-int fm_scheme_coeffs_f32(const fm_scheme* s, int levels, float* U, float* V, float* W) {
+int fm_scheme_coeffs_f32(const fm_scheme* s, int levels, float* U, float* V, float* W) try {
   clear_error();
   if (!s || !U || !V || !W) return fail(FM_E_ARG, "null pointer");
   if (levels < 1 || levels > 8) return fail(FM_E_ARG, "levels must be in [1, 8]");
@@ -1073,6 +1099,8 @@ int fm_scheme_coeffs_f32(const fm_scheme* s, int levels, float* U, float* V, flo
   for (size_t i = 0; i < f.V.size(); ++i) V[i] = (float)f.V[i];
   for (size_t i = 0; i < f.W.size(); ++i) W[i] = (float)f.W[i];
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
 void fm_scheme_free(fm_scheme* s) { delete s; }
@@ -1085,29 +1113,35 @@ static int scale_mode_ok(int m) {
 }
 
 size_t fm_workspace_size_scaled(const fm_scheme* s, int M, int N, int K, int levels, int G,
-                                int chunk, fm_scale_mode scale_mode) {
+                                int chunk, fm_scale_mode scale_mode) try {
   Geometry g;
   if (G < 1 || !scale_mode_ok(scale_mode) || check_geometry(s, levels, M, N, K, g) != FM_OK ||
       scale_shape_ok(g.Mb, g.Nb, g.Kb, g.R, scale_mode) != FM_OK)
     return 0;
   if (chunk <= 0 || chunk > G) chunk = G;
   return make_layout(g, G, chunk, true, scale_mode, chunk < G).total;
+} catch (...) {
+  return host_failure(), (size_t)0;
 }
 
-size_t fm_workspace_size(const fm_scheme* s, int M, int N, int K, int levels, int G, int chunk) {
+size_t fm_workspace_size(const fm_scheme* s, int M, int N, int K, int levels, int G, int chunk) try {
   return fm_workspace_size_scaled(s, M, N, K, levels, G, chunk, FM_SCALE_TENSOR);
+} catch (...) {
+  return host_failure(), (size_t)0;
 }
 
-size_t fm_error_workspace_size(int M, int N) {
+size_t fm_error_workspace_size(int M, int N) try {
   if (M < 1 || N < 1) return 0;
   const size_t n = (size_t)M * N;
   return up((size_t)error_stats_blocks(n) * 3 * 8) + up(3 * 8);
+} catch (...) {
+  return host_failure(), (size_t)0;
 }
 
 int fm_form_operands_scaled(const fm_scheme* s, int levels, const float* A, const float* B,
                             int M, int N, int K, fm_fmt fmt, fm_scale_mode scale_mode, uint8_t* Tq,
                             uint8_t* Sq, float* dT, float* dS, void* workspace, size_t ws_bytes,
-                            void* hip_stream) {
+                            void* hip_stream) try {
   clear_error();
   if (!A || !B || !Tq || !Sq || !dT || !dS) return fail(FM_E_ARG, "null pointer");
   if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
@@ -1129,18 +1163,22 @@ int fm_form_operands_scaled(const fm_scheme* s, int levels, const float* A, cons
   const float *Aform, *rowup;
   if ((rc = prepare_repairs(geo, T, ws, L, scale_mode, A, Aform, rowup, st))) return rc;
   return form_chunk(geo, Aform, Bt, ws, L, T, 0, 1, fmt, scale_mode, Tq, Sq, dT, dS, st);
+} catch (...) {
+  return host_failure();
 }
 
 int fm_form_operands(const fm_scheme* s, int levels, const float* A, const float* B, int M, int N,
                      int K, fm_fmt fmt, uint8_t* Tq, uint8_t* Sq, float* dT, float* dS,
-                     void* workspace, size_t ws_bytes, void* hip_stream) {
+                     void* workspace, size_t ws_bytes, void* hip_stream) try {
   return fm_form_operands_scaled(s, levels, A, B, M, N, K, fmt, FM_SCALE_TENSOR, Tq, Sq, dT, dS,
                                  workspace, ws_bytes, hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
 int fm_block_products_scaled(const uint8_t* Tq, const uint8_t* Sq, const float* dT,
                              const float* dS, int batch, int Mb, int Nb, int Kb, fm_fmt fmt,
-                             fm_scale_mode scale_mode, float* Mout, void* hip_stream) {
+                             fm_scale_mode scale_mode, float* Mout, void* hip_stream) try {
   clear_error();
   if (!Tq || !Sq || !dT || !dS || !Mout) return fail(FM_E_ARG, "null pointer");
   if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
@@ -1157,17 +1195,21 @@ int fm_block_products_scaled(const uint8_t* Tq, const uint8_t* Sq, const float* 
     return fail(FM_E_ARG, "group scales must be 16-byte aligned (and padded to 4 floats)");
   return launch_block_gemm(Tq, Sq, dT, dS, Mout, batch, Mb, Nb, Kb, fmt, scale_mode,
                            (hipStream_t)hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
 int fm_block_products(const uint8_t* Tq, const uint8_t* Sq, const float* dT, const float* dS,
                       int batch, int Mb, int Nb, int Kb, fm_fmt fmt, float* Mout,
-                      void* hip_stream) {
+                      void* hip_stream) try {
   return fm_block_products_scaled(Tq, Sq, dT, dS, batch, Mb, Nb, Kb, fmt, FM_SCALE_TENSOR, Mout,
                                   hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
 int fm_reconstruct(const fm_scheme* s, int levels, const float* Mprod, int M, int N, float* C,
-                   void* workspace, size_t ws_bytes, void* hip_stream) {
+                   void* workspace, size_t ws_bytes, void* hip_stream) try {
   clear_error();
   if (!Mprod || !C) return fail(FM_E_ARG, "null pointer");
   Geometry geo;
@@ -1187,11 +1229,13 @@ int fm_reconstruct(const fm_scheme* s, int levels, const float* Mprod, int M, in
   if ((rc = upload_tables(T, ws, L, st))) return rc;
   const ReconArgs ra = recon_args(geo, ws, L, 0, 1, Mprod, C, nullptr);
   return launch_recon(ra, chunk_pattern(T, 2, 0, 1), st);
+} catch (...) {
+  return host_failure();
 }
 
 int fm_matmul_lowp_scaled(const fm_scheme* s, const float* A, const float* B, float* C, int M,
                           int N, int K, int levels, fm_fmt fmt, fm_scale_mode scale_mode,
-                          void* workspace, size_t ws_bytes, void* hip_stream) {
+                          void* workspace, size_t ws_bytes, void* hip_stream) try {
   clear_error();
   if (!A || !B || !C) return fail(FM_E_ARG, "null pointer");
   if (!fmt_ok(fmt)) return fail(FM_E_ARG, "bad format");
@@ -1231,17 +1275,21 @@ int fm_matmul_lowp_scaled(const fm_scheme* s, const float* A, const float* B, fl
   ra.rowscale = rowup;
   ra.prod_bf16 = bf;
   return launch_recon(ra, chunk_pattern(T, 2, 0, 1), st);
+} catch (...) {
+  return host_failure();
 }
 
 int fm_matmul_lowp(const fm_scheme* s, const float* A, const float* B, float* C, int M, int N,
                    int K, int levels, fm_fmt fmt, void* workspace, size_t ws_bytes,
-                   void* hip_stream) {
+                   void* hip_stream) try {
   return fm_matmul_lowp_scaled(s, A, B, C, M, N, K, levels, fmt, FM_SCALE_TENSOR, workspace,
                                ws_bytes, hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
 int fm_reference_f64(const float* A, const float* B, double* C_ref, int M, int N, int K,
-                     void* hip_stream) {
+                     void* hip_stream) try {
   clear_error();
   if (!A || !B || !C_ref) return fail(FM_E_ARG, "null pointer");
   if (M < 1 || N < 1 || K < 1) return fail(FM_E_ARG, "sizes must be positive");
@@ -1249,10 +1297,12 @@ int fm_reference_f64(const float* A, const float* B, double* C_ref, int M, int N
   const int rc = launch_reference_f64(A, B, C_ref, M, N, K, (hipStream_t)hip_stream);
   timing_end(T_REFERENCE, (hipStream_t)hip_stream);
   return rc;
+} catch (...) {
+  return host_failure();
 }
 
 int fm_error_stats(const float* C, const double* C_ref, int M, int N, fm_stats* out,
-                   void* workspace, size_t ws_bytes, void* hip_stream) {
+                   void* workspace, size_t ws_bytes, void* hip_stream) try {
   clear_error();
   if (!C || !C_ref || !out) return fail(FM_E_ARG, "null pointer");
   if (M < 1 || N < 1) return fail(FM_E_ARG, "sizes must be positive");
@@ -1273,12 +1323,14 @@ int fm_error_stats(const float* C, const double* C_ref, int M, int N, fm_stats* 
   out->rel_fro = h[1] > 0 ? std::sqrt(h[0]) / std::sqrt(h[1]) : 0.0;
   if (!std::isfinite(h[0])) return fail(FM_E_NONFINITE, "non-finite error sum");
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, const float* B,
                          const double* C_ref, int M, int N, int K, int levels, fm_fmt fmt,
                          fm_scale_mode scale_mode, double* rel_fro_out, void* workspace,
-                         size_t ws_bytes, void* hip_stream) {
+                         size_t ws_bytes, void* hip_stream) try {
   clear_error();
   if (!gauged || !A || !B || !C_ref || !rel_fro_out) return fail(FM_E_ARG, "null pointer");
   if (G < 1) return fail(FM_E_ARG, "G must be positive");
@@ -1448,37 +1500,47 @@ int fm_orbit_eval_scaled(const fm_scheme* const* gauged, int G, const float* A, 
   const double ref = std::sqrt(o3[1]);
   for (int g = 0; g < G; ++g) rel_fro_out[g] = ref > 0 ? std::sqrt(h[g]) / ref : 0.0;
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A, const float* B,
                   const double* C_ref, int M, int N, int K, int levels, fm_fmt fmt,
-                  double* rel_fro_out, void* workspace, size_t ws_bytes, void* hip_stream) {
+                  double* rel_fro_out, void* workspace, size_t ws_bytes, void* hip_stream) try {
   return fm_orbit_eval_scaled(gauged, G, A, B, C_ref, M, N, K, levels, fmt, FM_SCALE_TENSOR,
                               rel_fro_out, workspace, ws_bytes, hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
-int fm_set_block_product_arithmetic(fm_accum a) {
+int fm_set_block_product_arithmetic(fm_accum a) try {
   clear_error();
   return set_block_product_arith((int)a);
+} catch (...) {
+  return host_failure();
 }
 
 int fm_fp8_encode(const float* x, int64_t n, fm_fmt fmt, int impl, uint8_t* out,
-                  void* hip_stream) {
+                  void* hip_stream) try {
   clear_error();
   if (!x || !out) return fail(FM_E_ARG, "null pointer");
   if (n < 0 || impl < 0 || impl > 2 || !fmt_ok(fmt)) return fail(FM_E_ARG, "bad argument");
   return launch_fp8_encode(x, out, (size_t)n, fmt, impl, (hipStream_t)hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
-int fm_bf16_round(const float* x, int64_t n, int impl, float* out, void* hip_stream) {
+int fm_bf16_round(const float* x, int64_t n, int impl, float* out, void* hip_stream) try {
   clear_error();
   if (!x || !out) return fail(FM_E_ARG, "null pointer");
   if (n < 0 || impl < 0 || impl > 2) return fail(FM_E_ARG, "bad argument");
   if ((uint64_t)n > ((uint64_t)0xffffffffu) * 256u) return fail(FM_E_SHAPE, "too many values");
   return launch_bf16_round(x, out, (size_t)n, impl, (hipStream_t)hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
-const char* fm_scheme_kernel_family(const fm_scheme* s, int levels) {
+const char* fm_scheme_kernel_family(const fm_scheme* s, int levels) try {
   clear_error();
   if (!s || levels < 1 || levels > 8) {
     fail(FM_E_ARG, "bad argument");
@@ -1492,10 +1554,12 @@ const char* fm_scheme_kernel_family(const fm_scheme* s, int levels) {
   const int pw = match_pattern(2, L.w, f.R, f.m * f.n);
   if (pa >= 0 && pa == pb && pb == pw) return pattern_name(pa);
   return "generic";
+} catch (...) {
+  return host_failure(), "";
 }
 
 int fm_scheme_sign_variant(const fm_scheme* s, int levels, int side, int* is_sign,
-                           uint64_t* neg_mask) {
+                           uint64_t* neg_mask) try {
   clear_error();
   if (!s || !is_sign || !neg_mask) return fail(FM_E_ARG, "null pointer");
   if (side < 0 || side > 1) return fail(FM_E_ARG, "side must be 0 (A) or 1 (B)");
@@ -1510,15 +1574,19 @@ int fm_scheme_sign_variant(const fm_scheme* s, int levels, int side, int* is_sig
   *is_sign = block_signs(p, side, sd, nb, &m) ? 1 : 0;
   *neg_mask = *is_sign ? m : 0;
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
-int fm_timing_enable(int on) {
+int fm_timing_enable(int on) try {
   clear_error();
   g_timing.on = on != 0;
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
-int fm_timing_reset(void) {
+int fm_timing_reset(void) try {
   clear_error();
   for (auto& r : g_timing.recs) {
     (void)hipEventSynchronize(r.stop);
@@ -1527,9 +1595,11 @@ int fm_timing_reset(void) {
   }
   g_timing.recs.clear();
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
-int fm_timing_read(const char* kernel_class, int* launches, double* total_ms) {
+int fm_timing_read(const char* kernel_class, int* launches, double* total_ms) try {
   clear_error();
   if (!kernel_class || !launches || !total_ms) return fail(FM_E_ARG, "null pointer");
   int cls = -1;
@@ -1550,9 +1620,11 @@ int fm_timing_read(const char* kernel_class, int* launches, double* total_ms) {
   *launches = n;
   *total_ms = ms;
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
-int fm_status(void* workspace, size_t ws_bytes, void* hip_stream) {
+int fm_status(void* workspace, size_t ws_bytes, void* hip_stream) try {
   clear_error();
   if (!workspace || ws_bytes < kAlign) return fail(FM_E_WORKSPACE, "workspace too small");
   hipStream_t st = (hipStream_t)hip_stream;
@@ -1562,11 +1634,13 @@ int fm_status(void* workspace, size_t ws_bytes, void* hip_stream) {
   if (flag & 2u) return fail(FM_E_RANGE, "a block sum of integer codes left int8");
   if (flag) return fail(FM_E_NONFINITE, "a block sum was not finite");
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
 // ------------------------------------------------------------ integer path
 int fm_int8_quantize(const float* X, int rows, int K, int g, int b, int8_t* codes, float* d,
-                     uint32_t* flag, void* hip_stream) {
+                     uint32_t* flag, void* hip_stream) try {
   clear_error();
   if (!X || !codes || !d) return fail(FM_E_ARG, "null pointer");
   if (rows < 1 || K < 1) return fail(FM_E_ARG, "sizes must be positive");
@@ -1574,10 +1648,12 @@ int fm_int8_quantize(const float* X, int rows, int K, int g, int b, int8_t* code
   if (g < 64 || g > 512 || g % 64) return fail(FM_E_ARG, "group length must be 64..512, a multiple of 64");
   if (K % g) return fail(FM_E_SHAPE, "K must be a multiple of the group length");
   return launch_i8_quantize(X, rows, K, g, b, codes, d, flag, (hipStream_t)hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
 int fm_int8_matmul_classical(const int8_t* Ac, const float* dA, const int8_t* BTc, const float* dB,
-                             int M, int N, int K, int g, float* out, void* hip_stream) {
+                             int M, int N, int K, int g, float* out, void* hip_stream) try {
   clear_error();
   if (!Ac || !dA || !BTc || !dB || !out) return fail(FM_E_ARG, "null pointer");
   if (M < 1 || N < 1 || K < 1) return fail(FM_E_ARG, "sizes must be positive");
@@ -1586,6 +1662,8 @@ int fm_int8_matmul_classical(const int8_t* Ac, const float* dA, const int8_t* BT
   return launch_i8_gemm(false, Ac, BTc, nullptr, nullptr, dA, dB, out, nullptr, nullptr, 0,
                         nullptr, nullptr, 0, M, N, K, g, 1, 1, 1, 0, 1, nullptr, nullptr, nullptr,
                         nullptr, (hipStream_t)hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
 namespace {
@@ -1894,7 +1972,7 @@ int i8_plan_run(const fm_int8_plan& p, const int8_t* Ac, const float* dA, const 
 }  // namespace
 
 int fm_int8_certify(const fm_scheme* s, int levels, int b_A, int b_B, int h, int g,
-                    int* conditions, double* L) {
+                    int* conditions, double* L) try {
   clear_error();
   if (!conditions || !L) return fail(FM_E_ARG, "null pointer");
   IntScheme is;
@@ -1904,36 +1982,44 @@ int fm_int8_certify(const fm_scheme* s, int levels, int b_A, int b_B, int h, int
   L[1] = is.LB;
   L[2] = is.LW;
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int fm_int8_certify_corrected(const fm_scheme* s, int levels, int b_A, int b_B, int h, int g,
-                              int* conditions, double* bounds) {
+                              int* conditions, double* bounds) try {
   clear_error();
   if (!conditions || !bounds) return fail(FM_E_ARG, "null pointer");
   IntScheme is;
   if (int rc = int_scheme(s, levels, is)) return rc;
   certify_corrected(is, b_A, b_B, h, g, conditions, bounds);
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
-size_t fm_int8_workspace_size(const fm_scheme* s, int levels, int M, int N, int K, int g, int h) {
+size_t fm_int8_workspace_size(const fm_scheme* s, int levels, int M, int N, int K, int g, int h) try {
   IntScheme is;
   if (int_scheme(s, levels, is) != FM_OK) return 0;
   if (i8_fast_shape_ok(is, M, N, K, g, h) != FM_OK) return 0;
   return i8_layout(is, M, N, K, h, false).total;
+} catch (...) {
+  return host_failure(), (size_t)0;
 }
 
 size_t fm_int8_workspace_size_corrected(const fm_scheme* s, int levels, int M, int N, int K, int g,
-                                        int h) {
+                                        int h) try {
   IntScheme is;
   if (int_scheme(s, levels, is) != FM_OK) return 0;
   if (i8_fast_shape_ok(is, M, N, K, g, h) != FM_OK) return 0;
   return i8_layout(is, M, N, K, h, true).total;
+} catch (...) {
+  return host_failure(), (size_t)0;
 }
 
 int fm_int8_plan_create(const fm_scheme* s, int levels, int M, int N, int K, int g, int h,
                         int b_A, int b_B, int correct, void* workspace, size_t ws_bytes,
-                        void* hip_stream, fm_int8_plan** out) {
+                        void* hip_stream, fm_int8_plan** out) try {
   clear_error();
   if (!out) return fail(FM_E_ARG, "null pointer");
   *out = nullptr;
@@ -1945,13 +2031,17 @@ int fm_int8_plan_create(const fm_scheme* s, int levels, int M, int N, int K, int
     return rc;
   *out = p.release();
   return FM_OK;
+} catch (...) {
+  return host_failure();
 }
 
 int fm_int8_plan_run(const fm_int8_plan* p, const int8_t* Ac, const float* dA, const int8_t* BTc,
-                     const float* dB, float* out, void* hip_stream) {
+                     const float* dB, float* out, void* hip_stream) try {
   clear_error();
   if (!p) return fail(FM_E_ARG, "null plan");
   return i8_plan_run(*p, Ac, dA, BTc, dB, out, (hipStream_t)hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
 void fm_int8_plan_free(fm_int8_plan* p) { delete p; }
@@ -1975,17 +2065,21 @@ int int8_fast_once(const fm_scheme* s, int levels, const int8_t* Ac, const float
 int fm_int8_matmul_fast(const fm_scheme* s, int levels, const int8_t* Ac, const float* dA,
                         const int8_t* BTc, const float* dB, int M, int N, int K, int g, int h,
                         int b_A, int b_B, float* out, void* workspace, size_t ws_bytes,
-                        void* hip_stream) {
+                        void* hip_stream) try {
   return int8_fast_once(s, levels, Ac, dA, BTc, dB, M, N, K, g, h, b_A, b_B, false, out,
                         workspace, ws_bytes, hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
 int fm_int8_matmul_corrected(const fm_scheme* s, int levels, const int8_t* Ac, const float* dA,
                              const int8_t* BTc, const float* dB, int M, int N, int K, int g, int h,
                              int b_A, int b_B, float* out, void* workspace, size_t ws_bytes,
-                             void* hip_stream) {
+                             void* hip_stream) try {
   return int8_fast_once(s, levels, Ac, dA, BTc, dB, M, N, K, g, h, b_A, b_B, true, out,
                         workspace, ws_bytes, hip_stream);
+} catch (...) {
+  return host_failure();
 }
 
 }  // extern "C"
