@@ -33,6 +33,7 @@ namespace fm {
 
 // ---------------------------------------------------------------- errors
 int fail(int code, const std::string& msg);  // records msg, returns code
+int host_failure() noexcept;                  // records a host failure, returns FM_E_NOMEM
 void clear_error();
 int hip_check(hipError_t e, const char* what);
 
@@ -70,10 +71,10 @@ int match_pattern(int side, const Side& s, int R, int NB);
 // The shared chains then give every product's own chain (a shared entry has
 // one block and one base value, hence one coefficient).
 bool block_signs(int pattern, int side, const Side& s, int NB, uint64_t* mask);
-// Number of pattern families; side: 0 = A, 1 = B, 2 = W.
 // Family whose H pattern (pairs of products sharing a block of A and a
 // block of C) equals one gauge's H support in compressed rows, or -1.
 int match_h_pattern(const int32_t* rowptr, const uint16_t* cols, int R);
+// Number of pattern families, and the name of family `id`.
 int pattern_count();
 const char* pattern_name(int id);
 

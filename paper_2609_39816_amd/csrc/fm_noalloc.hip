@@ -49,7 +49,7 @@ size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 }  // namespace fm
 
 extern "C" int fm_error_stats_noalloc(const float* C, const double* C_ref, int M, int N,
-                                      fm_stats* out, void* hip_stream) {
+                                      fm_stats* out, void* hip_stream) try {
   using namespace fm;
   clear_error();
   if (!C || !C_ref || !out) return fail(FM_E_ARG, "null pointer");
@@ -78,4 +78,6 @@ extern "C" int fm_error_stats_noalloc(const float* C, const double* C_ref, int M
   out->rel_fro = h[1] > 0 ? std::sqrt(h[0]) / std::sqrt(h[1]) : 0.0;
   if (!std::isfinite(h[0])) return fail(FM_E_NONFINITE, "non-finite error sum");
   return FM_OK;
+} catch (...) {
+  return fm::host_failure();
 }
