@@ -168,6 +168,36 @@ def library_gemm(w, geo, dev, iters=5):
     return res
 
 
+def library_hbm(dev, iters=10):
+    """What plain passes over 4 GiB of fp32 reach in torch's own kernels:
+    a maximum per row of 4096 (reads), a fill (writes) and a copy (reads
+    and writes), in GB/s of bytes moved; HIP-event averages."""
+    import torch
+    n = 1 << 30
+    x = torch.ones(n, dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+
+    def rate(fn, nbytes):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / iters
+        return dict(ms=round(ms, 4), gbs=round(nbytes / ms / 1e6, 1))
+
+    res = dict(row_max_read=rate(lambda: x.view(-1, 4096).amax(dim=1), 4 * n),
+               fill_write=rate(lambda: y.fill_(1.0), 4 * n),
+               copy_read_write=rate(lambda: y.copy_(x), 8 * n))
+    del x, y
+    torch.cuda.empty_cache()
+    return res
+
+
 # Classical-equivalent flops the oracle is given per gauge in the CPU sample:
 # at about 0.04 TFLOP/s on 16 host cores this is about 8 s per gauge.
 CPU_SAMPLE_FLOPS = 4e11
@@ -334,7 +364,8 @@ def main():
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--library-gemm", action="store_true",
                     help="also time the vendor library's GEMMs (torch on hipBLASLt) on the "
-                         "block-product shapes, as context for the block-product kernel")
+                         "block-product shapes, and torch's plain HBM passes (a row maximum, "
+                         "a fill, a copy of 4 GiB), as context for the kernels' rooflines")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; the gauge orbit would "
@@ -520,6 +551,7 @@ def main():
     if args.library_gemm:
         log("[bench] library GEMMs on the block-product shapes")
         out["library_gemm"] = library_gemm(w, geo, dev)
+        out["library_hbm"] = library_hbm(dev)
     if not args.no_cpu_baseline:
         log("[bench] oracle baseline on the host cores")
         out["cpu_baseline"] = cpu_baseline(w, A, B, gauges, smode)
