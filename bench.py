@@ -40,17 +40,31 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_work(cls, w, geo, chunk, G):
+def default_chunk(w):
+    """Gauges per orbit launch: 16 for three-level schemes, 32 otherwise.
+    Measured on one machine at a time, the three-level workload's step took
+    1.0-2.3% less at 16 than at 32 (mostly in the block products; 24 was
+    as fast as 16, 8 slower than 32), and the two-level 2048 x 4096 x 4096
+    step 6% more at 16 than at 32."""
+    return 16 if w.levels >= 3 else 32
+
+
+def kernel_work(cls, w, geo, chunk, G, fused=False):
     """Algorithmic work per step of one kernel class, summed over its launches
     (the orbit's chunks and the classical baseline's single launch), and the
-    class's roofline bound.  Units of work:
+    class's roofline bound.  `fused`: the per-tensor schedule over several
+    chunks, where each chunk's codes are formed in one pass with the next
+    chunk's maxima (the maxima class then runs for the first chunk only).
+    Units of work:
       block_gemm: 2*Mb*Nb*Kb flops per block product; G*R products for the
                   orbit plus the classical product 2*M*N*K;
       recon:      per gauge, R*Mb*Nb fp32 products read; per launch, the
                   M*N float64 reference read once (the gauges of a launch
                   share it; C is not written); the classical baseline reads
                   M*N products and writes C;
-      form_amax:  each launch reads one operand once in fp32 (A, or B^T);
+      form_amax:  each launch reads one operand once in fp32 (A, or B^T):
+                  the classical baseline's and, per chunk, the orbit's (the
+                  first chunk's only when fused);
       form_quant: each launch reads one operand and writes its FP8 codes;
       reference:  reads A and B in fp32, writes C_ref in float64.
     """
@@ -64,7 +78,7 @@ def kernel_work(cls, w, geo, chunk, G):
     if cls == "recon":
         return "hbm", G * R * Mb * Nb * 4.0 + chunks * M * N * 8.0 + M * N * 8.0, "GB/s"
     if cls == "form_amax":
-        return "hbm", (chunks + 1) * ops, "GB/s"
+        return "hbm", (2 if fused else chunks + 1) * ops, "GB/s"
     if cls == "form_quant":
         return "hbm", (chunks + 1) * ops + G * R * (Mb * Kb + Nb * Kb) + (M * K + N * K), "GB/s"
     if cls == "reference":
@@ -349,7 +363,9 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default=HEADLINE)
-    ap.add_argument("--chunk", type=int, default=32, help="gauges per launch batch")
+    ap.add_argument("--chunk", type=int, default=None,
+                    help="gauges per launch (default: default_chunk of the workload; 0: the whole "
+                         "orbit in one launch)")
     ap.add_argument("--fmt", default=None)
     ap.add_argument("--scale-mode", default="tensor", choices=["tensor", "rowcol", "group"],
                     help="scale granularity of the FP8 rounding of block sums")
@@ -411,7 +427,10 @@ def main():
         levels = w.levels
     classical = fm.Scheme.base("classical")
     geo = flat.flat_dims(levels)
-    chunk = min(args.chunk, G) if args.chunk > 0 else G
+    req = default_chunk(w) if args.chunk is None else args.chunk
+    chunk = min(req, G) if req > 0 else G
+    # per-tensor scales over several chunks: codes and the next chunk's maxima in one pass
+    fused = smode == fm.SCALE_TENSOR and chunk < G
     ws = fm.workspace(fm.workspace_size(flat, w.M, w.N, w.K, levels, G, chunk, smode))
     ws_cl = fm.workspace(fm.workspace_size(classical, w.M, w.N, w.K, 1, 1, 1, smode))
     ws_err = fm.workspace(fm.lib.fm_error_workspace_size(w.M, w.N))
@@ -460,7 +479,7 @@ def main():
         fm.timing_reset()
         dom = max(per_class, key=lambda c: per_class[c]["total_ms"])
         n, ms = per_class[dom]["launches"], per_class[dom]["total_ms"]
-        bound, work, unit = kernel_work(dom, w, geo, chunk, G)
+        bound, work, unit = kernel_work(dom, w, geo, chunk, G, fused)
         # achieved = work per launch / average launch duration = work / time
         avg_s = ms / 1e3 / max(1, n)
         tot_s = ms / 1e3 / args.steps
@@ -493,7 +512,7 @@ def main():
 
     flops = G * 2.0 * w.M * w.N * w.K
     value = flops / t / 1e12
-    mfma_flops, hbm_bytes = pipeline_work(w, geo, G, args.chunk)
+    mfma_flops, hbm_bytes = pipeline_work(w, geo, G, chunk)
     # the whole orbit against both ceilings: its block products' matrix
     # flops over the step time against the matrix peak of the instruction
     # issued (and the FP8 peak), and its least HBM traffic over the step time
@@ -511,7 +530,7 @@ def main():
     for cls, v in per_class.items():
         if v["total_ms"] <= 0:
             continue
-        bound, work, unit = kernel_work(cls, w, geo, chunk, G)
+        bound, work, unit = kernel_work(cls, w, geo, chunk, G, fused)
         secs = v["total_ms"] / 1e3 / args.steps
         if unit == "TFLOP/s":
             per_class_rate[cls] = dict(ms_per_step=round(secs * 1e3, 3),

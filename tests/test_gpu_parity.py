@@ -20,6 +20,7 @@ import oracle
 from oracle import scheme_ops as so
 from oracle import schemes as osch
 import synthetic as sy
+from bench import default_chunk
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -486,9 +487,9 @@ def test_chunked_orbit_equals_single_launch_and_is_deterministic():
 
 def test_full_size_strassen2_workload_sampled():
     """Two-level Strassen at 2048 x 4096 x 4096, all 512 sign variants in the
-    schedule the benchmark uses (32 gauges per chunk, so gauges after the
-    first chunk go through the second set of maxima, scales and product
-    buffers and the two-stream overlap); the oracle checks the identity
+    schedule the benchmark uses (32 gauges per launch at two levels, so
+    gauges after the first chunk go through the second set of maxima, scales
+    and product buffers and the two-stream overlap); the oracle checks the identity
     variant's operands bit for bit and the errors of three variants (first,
     a middle and the last chunk) from its whole output."""
     w = sy.WORKLOADS["strassen2_2048x4096x4096_sign512"]
@@ -498,7 +499,7 @@ def test_full_size_strassen2_workload_sampled():
     gauges = sy.gauges(w)
     hips, orcs, levels = schemes_for(w, gauges)
     Cref = fm.reference_f64(At, Bt)
-    errs = fm.orbit_eval(hips, At, Bt, Cref, levels, chunk=32)
+    errs = fm.orbit_eval(hips, At, Bt, Cref, levels, chunk=default_chunk(w))
     check_operands(hips[0], orcs[0], levels, A, B, At, Bt, "e4m3")
     Cref_o = oracle.reference_f64(A, B)
     for gi in (0, 137, 511):
@@ -518,7 +519,8 @@ FULL_SIZE = [("laderman1_3072x4608x12288_gl512", "e4m3"), ("laderman1_3072x4608x
 def test_full_size_workloads_sampled(name, fmt):
     """The other full-size workloads (the last is the benchmark's headline),
     every gauge of the orbit in the launch configuration the benchmark times
-    (32 gauges per chunk, two sets of buffers, two streams).  For gauge 1
+    (`bench.default_chunk`: 16 gauges per launch at three levels, 32
+    otherwise; two sets of buffers, two streams).  For gauge 1
     (first chunk) and the last gauge (last chunk) the oracle checks the
     operands bit for bit over the whole tensors and the output at sampled
     positions of every output block (the block products at those positions,
@@ -534,7 +536,7 @@ def test_full_size_workloads_sampled(name, fmt):
     gauges = sy.gauges(w)
     hips, orcs, levels = schemes_for(w, gauges)
     Cref = fm.reference_f64(At, Bt)
-    errs = fm.orbit_eval(hips, At, Bt, Cref, levels, FMT[fmt], chunk=32)
+    errs = fm.orbit_eval(hips, At, Bt, Cref, levels, FMT[fmt], chunk=default_chunk(w))
     assert errs.shape == (w.G,) and np.all(np.isfinite(errs)) and np.all(errs > 0)
     say(f"[parity] orbit done: errors {errs.min():.4e} .. {errs.max():.4e}")
 
