@@ -145,6 +145,34 @@ def _cuda(t, dtype):
     return t
 
 
+# The library sees only pointers and sizes: the shapes of the tensors behind
+# them are checked here, before any call.
+def _matmul_shapes(A, B):
+    """(M, K, N) of A (M, K) times B (K, N), both contiguous fp32 on one GPU."""
+    _cuda(A, torch.float32), _cuda(B, torch.float32)
+    if A.dim() != 2 or B.dim() != 2 or A.shape[1] != B.shape[0] or A.device != B.device:
+        raise ValueError(f"A {tuple(A.shape)} and B {tuple(B.shape)} are not M x K and K x N "
+                         "on one device")
+    return A.shape[0], A.shape[1], B.shape[1]
+
+
+def _out(out, shape, dtype, device):
+    """A new output tensor, or the caller's after checking it."""
+    if out is None:
+        return torch.empty(shape, dtype=dtype, device=device)
+    _cuda(out, dtype)
+    if tuple(out.shape) != tuple(shape) or out.device != torch.device(device):
+        raise ValueError(f"out must be {tuple(shape)} on {device}, got {tuple(out.shape)}")
+    return out
+
+
+def _ws(ws, device):
+    """Pointer and byte size of a caller's workspace (a contiguous GPU tensor)."""
+    if not (ws.is_cuda and ws.is_contiguous()) or ws.device != torch.device(device):
+        raise ValueError(f"the workspace must be a contiguous tensor on {device}")
+    return _dptr(ws), ws.numel() * ws.element_size()
+
+
 class Scheme:
     """A bilinear scheme held by the library (fm_scheme*)."""
 
@@ -250,9 +278,7 @@ def form_operands(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, st
     """Quantized block sums: Tq (R, Mb, Kb) u8, Sq (R, Nb, Kb) u8 (transposed),
     dT (R,) and dS (R,) fp32, or (R, Mb) and (R, Nb) with SCALE_ROWCOL, or
     (R, Kb/128, Mb) and (R, Kb/128, Nb/128) with SCALE_GROUP."""
-    _cuda(A, torch.float32), _cuda(B, torch.float32)
-    M, K = A.shape
-    N = B.shape[1]
+    M, K, N = _matmul_shapes(A, B)
     gm, gk, gn, R = s.flat_dims(levels)
     Mb, Nb = M // gm, N // gn
     Tq = torch.empty((R, Mb, K // gk), dtype=torch.uint8, device=A.device)
@@ -267,7 +293,7 @@ def form_operands(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, st
         ws = workspace(workspace_size(s, M, N, K, levels, 1, 1, scale_mode), A.device)
     _check(lib.fm_form_operands_scaled(s.handle, levels, _dptr(A), _dptr(B), M, N, K, fmt,
                                        scale_mode, _dptr(Tq), _dptr(Sq), _dptr(dT), _dptr(dS),
-                                       _dptr(ws), ws.numel(), _stream(stream)))
+                                       *_ws(ws, A.device), _stream(stream)))
     return Tq, Sq, dT, dS
 
 
@@ -278,6 +304,10 @@ def block_products(Tq, Sq, dT, dS, fmt: int = E4M3, out=None, stream=None,
     SCALE_GROUP per group (batch, Kb/128, Mb) and (batch, Kb/128, Nb/128),
     products returned in bf16 (as fp32 values)."""
     _cuda(Tq, torch.uint8), _cuda(Sq, torch.uint8)
+    if Tq.dim() != 3 or Sq.dim() != 3 or Sq.shape[0] != Tq.shape[0] or Sq.shape[2] != Tq.shape[2] \
+            or Sq.device != Tq.device:
+        raise ValueError(f"Tq {tuple(Tq.shape)} and Sq {tuple(Sq.shape)} are not "
+                         "(batch, Mb, Kb) and (batch, Nb, Kb) on one device")
     batch, Mb, Kb = Tq.shape
     Nb = Sq.shape[1]
     want = {SCALE_ROWCOL: (batch * Mb, batch * Nb),
@@ -296,8 +326,7 @@ def block_products(Tq, Sq, dT, dS, fmt: int = E4M3, out=None, stream=None,
             p[:t.numel()] = t.reshape(-1)
             return p
         dT, dS = padded(dT), padded(dS)
-    if out is None:
-        out = torch.empty((batch, Mb, Nb), dtype=torch.float32, device=Tq.device)
+    out = _out(out, (batch, Mb, Nb), torch.float32, Tq.device)
     _check(lib.fm_block_products_scaled(_dptr(Tq), _dptr(Sq), _dptr(dT), _dptr(dS), batch, Mb, Nb,
                                         Kb, fmt, scale_mode, _dptr(out), _stream(stream)))
     return out
@@ -305,46 +334,48 @@ def block_products(Tq, Sq, dT, dS, fmt: int = E4M3, out=None, stream=None,
 
 def reconstruct(s: Scheme, Mprod, M: int, N: int, levels: int = 1, ws=None, stream=None):
     _cuda(Mprod, torch.float32)
-    C = torch.empty((M, N), dtype=torch.float32, device=Mprod.device)
     gm, gk, gn, R = s.flat_dims(levels)
+    if M % gm or N % gn or Mprod.numel() != R * (M // gm) * (N // gn):
+        raise ValueError(f"Mprod holds {Mprod.numel()} values, not R x (M/{gm}) x (N/{gn})")
+    C = torch.empty((M, N), dtype=torch.float32, device=Mprod.device)
     if ws is None:
         ws = workspace(workspace_size(s, M, N, gk * 16, levels, 1, 1), Mprod.device)
-    _check(lib.fm_reconstruct(s.handle, levels, _dptr(Mprod), M, N, _dptr(C), _dptr(ws),
-                              ws.numel(), _stream(stream)))
+    _check(lib.fm_reconstruct(s.handle, levels, _dptr(Mprod), M, N, _dptr(C),
+                              *_ws(ws, Mprod.device), _stream(stream)))
     return C
 
 
 def matmul_lowp(s: Scheme, A, B, levels: int = 1, fmt: int = E4M3, ws=None, out=None,
                 stream=None, scale_mode: int = SCALE_TENSOR):
-    _cuda(A, torch.float32), _cuda(B, torch.float32)
-    M, K = A.shape
-    N = B.shape[1]
-    if out is None:
-        out = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    M, K, N = _matmul_shapes(A, B)
+    out = _out(out, (M, N), torch.float32, A.device)
     if ws is None:
         ws = workspace(workspace_size(s, M, N, K, levels, 1, 1, scale_mode), A.device)
     _check(lib.fm_matmul_lowp_scaled(s.handle, _dptr(A), _dptr(B), _dptr(out), M, N, K, levels,
-                                     fmt, scale_mode, _dptr(ws), ws.numel(), _stream(stream)))
+                                     fmt, scale_mode, *_ws(ws, A.device), _stream(stream)))
     return out
 
 
 def reference_f64(A, B, out=None, stream=None):
-    _cuda(A, torch.float32), _cuda(B, torch.float32)
-    M, K = A.shape
-    N = B.shape[1]
-    if out is None:
-        out = torch.empty((M, N), dtype=torch.float64, device=A.device)
+    M, K, N = _matmul_shapes(A, B)
+    out = _out(out, (M, N), torch.float64, A.device)
     _check(lib.fm_reference_f64(_dptr(A), _dptr(B), _dptr(out), M, N, K, _stream(stream)))
     return out
 
 
-def error_stats(C, Cref, ws=None, stream=None) -> dict:
+def _error_shapes(C, Cref):
     _cuda(C, torch.float32), _cuda(Cref, torch.float64)
-    M, N = C.shape
+    if C.dim() != 2 or tuple(C.shape) != tuple(Cref.shape) or C.device != Cref.device:
+        raise ValueError(f"C {tuple(C.shape)} and C_ref {tuple(Cref.shape)} differ")
+    return C.shape
+
+
+def error_stats(C, Cref, ws=None, stream=None) -> dict:
+    M, N = _error_shapes(C, Cref)
     if ws is None:
         ws = workspace(lib.fm_error_workspace_size(M, N), C.device)
     st = _Stats()
-    _check(lib.fm_error_stats(_dptr(C), _dptr(Cref), M, N, ct.byref(st), _dptr(ws), ws.numel(),
+    _check(lib.fm_error_stats(_dptr(C), _dptr(Cref), M, N, ct.byref(st), *_ws(ws, C.device),
                               _stream(stream)))
     return dict(rel_fro=st.rel_fro, err_sq=st.err_sq, ref_sq=st.ref_sq, max_abs=st.max_abs)
 
@@ -352,8 +383,7 @@ def error_stats(C, Cref, ws=None, stream=None) -> dict:
 def error_stats_noalloc(C, Cref, stream=None) -> dict:
     """error_stats without a workspace: the library's static device scratch
     holds the partial sums (calls overlapping on one device race)."""
-    _cuda(C, torch.float32), _cuda(Cref, torch.float64)
-    M, N = C.shape
+    M, N = _error_shapes(C, Cref)
     st = _Stats()
     _check(lib.fm_error_stats_noalloc(_dptr(C), _dptr(Cref), M, N, ct.byref(st), _stream(stream)))
     return dict(rel_fro=st.rel_fro, err_sq=st.err_sq, ref_sq=st.ref_sq, max_abs=st.max_abs)
@@ -362,17 +392,20 @@ def error_stats_noalloc(C, Cref, stream=None) -> dict:
 def orbit_eval(gauged, A, B, Cref, levels: int = 1, fmt: int = E4M3, ws=None, chunk: int = 0,
                stream=None, scale_mode: int = SCALE_TENSOR) -> np.ndarray:
     """Relative Frobenius errors of the FP8 schedule for every gauged scheme."""
-    _cuda(A, torch.float32), _cuda(B, torch.float32), _cuda(Cref, torch.float64)
-    M, K = A.shape
-    N = B.shape[1]
+    M, K, N = _matmul_shapes(A, B)
+    _cuda(Cref, torch.float64)
+    if tuple(Cref.shape) != (M, N) or Cref.device != A.device:
+        raise ValueError(f"C_ref must be ({M}, {N}) on {A.device}, got {tuple(Cref.shape)}")
     G = len(gauged)
+    if G < 1:
+        raise ValueError("the orbit needs at least one scheme")
     handles = (ct.c_void_p * G)(*[g.handle.value for g in gauged])
     if ws is None:
         ws = workspace(workspace_size(gauged[0], M, N, K, levels, G, chunk, scale_mode), A.device)
     out = np.empty(G, np.float64)
     _check(lib.fm_orbit_eval_scaled(ct.cast(handles, ct.c_void_p), G, _dptr(A), _dptr(B),
                                     _dptr(Cref), M, N, K, levels, fmt, scale_mode, _np_ptr(out),
-                                    _dptr(ws), ws.numel(), _stream(stream)))
+                                    *_ws(ws, A.device), _stream(stream)))
     return out
 
 
@@ -391,7 +424,7 @@ def bf16_round(x, impl: int = 0, stream=None):
 
 
 def status(ws, stream=None):
-    _check(lib.fm_status(_dptr(ws), ws.numel(), _stream(stream)))
+    _check(lib.fm_status(*_ws(ws, ws.device), _stream(stream)))
 
 
 _arith = ACC_BF16
@@ -512,7 +545,7 @@ def int8_matmul_fast(s: Scheme, Ac, dA, BTc, dB, levels: int = 1, g: int = 128, 
             raise FmError(-1, "fm_int8_workspace_size: arguments not supported")
         ws = workspace(need, Ac.device)
     _check(lib.fm_int8_matmul_fast(s.handle, levels, _dptr(Ac), _dptr(dA), _dptr(BTc), _dptr(dB),
-                                   M, N, K, g, h, b_A, b_B, _dptr(out), _dptr(ws), ws.numel(),
+                                   M, N, K, g, h, b_A, b_B, _dptr(out), *_ws(ws, Ac.device),
                                    _stream(stream)))
     return out
 
@@ -530,7 +563,7 @@ def int8_matmul_corrected(s: Scheme, Ac, dA, BTc, dB, levels: int = 1, g: int = 
         ws = workspace(need, Ac.device)
     _check(lib.fm_int8_matmul_corrected(s.handle, levels, _dptr(Ac), _dptr(dA), _dptr(BTc),
                                         _dptr(dB), M, N, K, g, h, b_A, b_B, _dptr(out),
-                                        _dptr(ws), ws.numel(), _stream(stream)))
+                                        *_ws(ws, Ac.device), _stream(stream)))
     return out
 
 
@@ -550,7 +583,7 @@ class Int8Plan:
         self.M, self.N, self.K, self.g = M, N, K, g
         out = ct.c_void_p()
         _check(lib.fm_int8_plan_create(s.handle, levels, M, N, K, g, h, b_A, b_B, int(correct),
-                                       _dptr(self.ws), self.ws.numel(), _stream(stream),
+                                       *_ws(self.ws, self.ws.device), _stream(stream),
                                        ct.byref(out)))
         self._h = out.value
 
