@@ -293,8 +293,9 @@ int fm_error_stats_noalloc(const float* C, const double* C_ref, int M, int N,
  * beside the next chunk's formation; concurrent calls on one device share
  * that stream (their reconstructions then run one after another).  The
  * results are the bits of the one-buffer schedule; within a chunk the
- * products may be stored in a tiled order internally (whole 256 x 128
- * tiles, tensor scales).  Synchronizes. */
+ * products may be stored in a tiled order internally (when they are whole
+ * tiles of the block-product kernel, 512 x 128 or 256 x 128, with tensor
+ * scales).  Synchronizes. */
 int fm_orbit_eval(const fm_scheme* const* gauged, int G, const float* A,
                   const float* B, const double* C_ref, int M, int N, int K,
                   int levels, fm_fmt fmt, double* rel_fro_out,
