@@ -43,8 +43,8 @@ def log(*a):
 def default_chunk(w):
     """Gauges per orbit launch: 16 for three-level schemes, 32 otherwise.
     Measured on one machine at a time, the three-level workload's step took
-    1.0-2.3% less at 16 than at 32 (mostly in the block products; 24 was
-    as fast as 16, 8 slower than 32), and the two-level 2048 x 4096 x 4096
+    1.0-2.3% less at 16 than at 32 (mostly in the block products; 8 was
+    slower than 32, 64 as fast as 32), and the two-level 2048 x 4096 x 4096
     step 6% more at 16 than at 32."""
     return 16 if w.levels >= 3 else 32
 
@@ -364,8 +364,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--chunk", type=int, default=None,
-                    help="gauges per launch (default: default_chunk of the workload; 0: the whole "
-                         "orbit in one launch)")
+                    help="gauges per launch, rounded down to G / 2^k (default: default_chunk of "
+                         "the workload; 0: the whole orbit in one launch)")
     ap.add_argument("--fmt", default=None)
     ap.add_argument("--scale-mode", default="tensor", choices=["tensor", "rowcol", "group"],
                     help="scale granularity of the FP8 rounding of block sums")
@@ -428,7 +428,13 @@ def main():
     classical = fm.Scheme.base("classical")
     geo = flat.flat_dims(levels)
     req = default_chunk(w) if args.chunk is None else args.chunk
-    chunk = min(req, G) if req > 0 else G
+    # the orbit runs in chunks of G / 2^k gauges: the largest such that its
+    # workspace fits, here the largest not above the request
+    chunk = G
+    while req > 0 and chunk > max(1, req):
+        chunk = max(1, chunk // 2)
+    if req > 0 and chunk != req:
+        log(f"[bench] {req} gauges per launch requested: the orbit runs {chunk} (G / 2^k)")
     # per-tensor scales over several chunks: codes and the next chunk's maxima in one pass
     fused = smode == fm.SCALE_TENSOR and chunk < G
     ws = fm.workspace(fm.workspace_size(flat, w.M, w.N, w.K, levels, G, chunk, smode))
