@@ -278,38 +278,42 @@ __global__ __launch_bounds__(64) void reduce_rows_kernel(const double* partial, 
 }
 
 // ----------------------------------------------------- float64 reference
-// On the float64 matrix cores: 128 x 128 output tile per workgroup of 4
-// waves (64 x 64 each: 4 x 4 blocks of v_mfma_f64_16x16x4_f64), K step 32;
-// operands staged in LDS as fp32 and widened to float64 when read (products
-// of two fp32 values are exact in float64; the sums are float64).
+// On the float64 matrix cores: 128 x 128 output tile per workgroup of 8
+// waves (64 x 32 each: 4 x 2 blocks of v_mfma_f64_16x16x4_f64; two waves
+// per SIMD hide each other's LDS reads and conversions), K step 64;
+// operands staged in LDS as fp32 (67 KB) and widened to float64 when read
+// (products of two fp32 values are exact in float64; the sums are float64,
+// in ascending K steps of 4 for every output, whatever the tiling).
 // Lane l of a 16 x 16 x 4 step holds A[l % 16][l / 16] and B[l / 16][l % 16];
 // its four results v = 0..3 are rows l / 16 + 4 v, column l % 16 of the block
 // (checked on the device with small integer operands).
 typedef double v4d __attribute__((ext_vector_type(4)));
-__global__ __launch_bounds__(kThreads) void ref_f64_mfma_kernel(const float* __restrict__ A,
-                                                                const float* __restrict__ B,
-                                                                double* __restrict__ C, int M,
-                                                                int N, int K) {
-  constexpr int KS = 32;  // K step
+constexpr int kRefThreads = 512;
+__global__ __launch_bounds__(kRefThreads) void ref_f64_mfma_kernel(const float* __restrict__ A,
+                                                                   const float* __restrict__ B,
+                                                                   double* __restrict__ C, int M,
+                                                                   int N, int K) {
+  constexpr int KS = 64;  // K step
+  constexpr int NL = 128 * KS / kRefThreads;  // loads per thread and operand (16)
   __shared__ float As[128][KS + 1];
   __shared__ float Bs[KS][128 + 4];
   const int m0 = blockIdx.y * 128, n0 = blockIdx.x * 128;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;  // 64-row half, 32-column quarter
   const int l16 = lane & 15, lq = lane >> 4;
-  v4d acc[4][4];
+  v4d acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = (v4d){0.0, 0.0, 0.0, 0.0};
+    for (int j = 0; j < 2; ++j) acc[i][j] = (v4d){0.0, 0.0, 0.0, 0.0};
   // the next step's operands are loaded into registers while this step's
   // products run
-  float ra[16], rb[16];
+  float ra[NL], rb[NL];
   auto load = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int idx = tid + kThreads * i;  // 0 .. 4095
-      const int r = idx >> 5, kk = idx & 31;
+    for (int i = 0; i < NL; ++i) {
+      const int idx = tid + kRefThreads * i;  // 0 .. 8191
+      const int r = idx >> 6, kk = idx & 63;
       const int gr = m0 + r, gk = k0 + kk;
       ra[i] = (gr < M && gk < K) ? A[(size_t)gr * K + gk] : 0.0f;
       const int kb = idx >> 7, c = idx & 127;
@@ -319,9 +323,9 @@ __global__ __launch_bounds__(kThreads) void ref_f64_mfma_kernel(const float* __r
   };
   auto store = [&]() {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int idx = tid + kThreads * i;
-      As[idx >> 5][idx & 31] = ra[i];
+    for (int i = 0; i < NL; ++i) {
+      const int idx = tid + kRefThreads * i;
+      As[idx >> 6][idx & 63] = ra[i];
       Bs[idx >> 7][idx & 127] = rb[i];
     }
   };
@@ -332,15 +336,15 @@ __global__ __launch_bounds__(kThreads) void ref_f64_mfma_kernel(const float* __r
     if (k0 + KS < K) load(k0 + KS);
 #pragma unroll
     for (int kk = 0; kk < KS; kk += 4) {
-      double a[4], b[4];
+      double a[4], b[2];
 #pragma unroll
       for (int i = 0; i < 4; ++i) a[i] = (double)As[wm * 64 + i * 16 + l16][kk + lq];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = (double)Bs[kk + lq][wn * 64 + j * 16 + l16];
+      for (int j = 0; j < 2; ++j) b[j] = (double)Bs[kk + lq][wn * 32 + j * 16 + l16];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
@@ -352,8 +356,8 @@ __global__ __launch_bounds__(kThreads) void ref_f64_mfma_kernel(const float* __r
       const int row = m0 + wm * 64 + i * 16 + lq + 4 * v;
       if (row >= M) continue;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int col = n0 + wn * 64 + j * 16 + l16;
+      for (int j = 0; j < 2; ++j) {
+        const int col = n0 + wn * 32 + j * 16 + l16;
         if (col < N) C[(size_t)row * N + col] = acc[i][j][v];
       }
     }
@@ -495,7 +499,7 @@ int launch_reduce_rows(const double* partial, int nblk, int G, double* out, hipS
 int launch_reference_f64(const float* A, const float* B, double* C, int M, int N, int K,
                          hipStream_t st) {
   dim3 grid((N + 127) / 128, (M + 127) / 128);
-  ref_f64_mfma_kernel<<<grid, kThreads, 0, st>>>(A, B, C, M, N, K);
+  ref_f64_mfma_kernel<<<grid, kRefThreads, 0, st>>>(A, B, C, M, N, K);
   return launched("ref_f64_mfma_kernel");
 }
 
